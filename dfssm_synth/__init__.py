@@ -1,0 +1,120 @@
+"""Seeded synthetic inputs for the DF-SSM scaffold + int8 LoRA linear.
+
+This module only draws random numbers in the layouts the library takes; it
+holds none of the method's arithmetic and imports neither the oracle nor the
+GPU package, so both sides can be fed the same bytes.
+
+Shapes follow Mamba-2 (the paper's model, Sec. 3 / Table 1): the 1.3B model
+has d_model 2048 and 48 layers, in_proj 2048 -> 8512 (2*4096 + 2*128 + 64)
+and out_proj 4096 -> 2048; the 130M model has d_model 768 and in_proj
+768 -> 3352.  No trained weights are available, so every tensor is drawn:
+
+  sign bits   i.i.d. Bernoulli(1/2), packed 32 per uint32, [N][K/32]
+  alpha       U(0.01, 0.05) fp32 per output row
+  A, B        int8 uniform on [-127, 127]   (A: [r,K], B: [N,r])
+  beta        U(1e-4, 1e-3) fp32 per output row (times beta_scale)
+  x           fp16 N(0,1), with a fixed seeded set of round(0.01*K) input
+              channels multiplied by 20 (activation outliers)
+
+Each tensor set has its own numpy PCG64 stream keyed by
+(config, layer, projection, variant), so sets never share a stream.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Dict, List, Tuple
+
+import numpy as np
+
+# 1.3B Mamba-2 projection shapes (K = input features, N = output features)
+IN_PROJ_1P3B = (2048, 8512)
+OUT_PROJ_1P3B = (4096, 2048)
+N_LAYERS_1P3B = 48
+
+
+@dataclass(frozen=True)
+class Config:
+    name: str
+    M: Tuple[int, ...]
+    K: int
+    N: int
+    r: int
+    doc: str
+
+
+CONFIGS: Dict[int, Config] = {
+    0: Config("130m_in_proj_m1", (1,), 768, 3352, 16, "Mamba-2-130M in_proj, one token"),
+    1: Config("1p3b_in_proj_m1", (1,), 2048, 8512, 64, "Mamba-2-1.3B in_proj decode, one token"),
+    2: Config("1p3b_out_proj_small_m", (1, 4, 8, 16, 32), 4096, 2048, 64,
+              "Mamba-2-1.3B out_proj, small-batch decode"),
+    3: Config("1p3b_decode_sweep", (1,), 0, 0, 64,
+              "48 x (in_proj 2048->8512, out_proj 4096->2048), each output re-quantised"),
+    4: Config("1p3b_in_proj_prefill", (2048,), 2048, 8512, 64, "Mamba-2-1.3B in_proj, 2048-token prefill"),
+}
+
+
+def _rng(*key: int) -> np.random.Generator:
+    return np.random.default_rng([int(k) for k in key])
+
+
+def weights(K: int, N: int, r: int, key=(0, 0, 0, 0), beta_scale: float = 1.0) -> dict:
+    """One weight set: packed sign bits, alpha, A, B, beta (numpy, host)."""
+    if K % 32:
+        raise ValueError("K must be a multiple of 32")
+    g = _rng(1, *key)
+    bits = g.integers(0, 2 ** 32, size=(N, K // 32), dtype=np.uint32)
+    alpha = g.uniform(0.01, 0.05, size=N).astype(np.float32)
+    A = g.integers(-127, 128, size=(r, K), dtype=np.int8)
+    B = g.integers(-127, 128, size=(N, r), dtype=np.int8)
+    beta = (g.uniform(1e-4, 1e-3, size=N) * beta_scale).astype(np.float32)
+    return dict(w_bits=bits, alpha=alpha, A=A, B=B, beta=beta)
+
+
+def activations(M: int, K: int, key=(0, 0), dtype=np.float16, outlier_frac: float = 0.01,
+                outlier_gain: float = 20.0) -> np.ndarray:
+    """x [M,K]: N(0,1) with a fixed set of outlier channels scaled by outlier_gain."""
+    g = _rng(2, *key)
+    z = g.standard_normal((M, K), dtype=np.float32)
+    n_out = int(round(outlier_frac * K))
+    if n_out:
+        ch = g.choice(K, n_out, replace=False)
+        z[:, ch] *= np.float32(outlier_gain)
+    return z.astype(dtype)
+
+
+def config_weights(cfg: int, variant: int = 0, beta_scale: float = 1.0) -> dict:
+    c = CONFIGS[cfg]
+    return weights(c.K, c.N, c.r, key=(cfg, 0, 0, variant), beta_scale=beta_scale)
+
+
+def config_activations(cfg: int, M: int, variant: int = 0) -> np.ndarray:
+    c = CONFIGS[cfg]
+    return activations(M, c.K, key=(cfg, 999_999 + variant))
+
+
+def sweep_shapes(n_layers: int = N_LAYERS_1P3B) -> List[Tuple[int, int]]:
+    """(K, N) of every linear of the decode sweep: in_proj, out_proj, ... ."""
+    out = []
+    for _ in range(n_layers):
+        out.append(IN_PROJ_1P3B)
+        out.append(OUT_PROJ_1P3B)
+    return out
+
+
+def sweep_weights(n_layers: int = N_LAYERS_1P3B, r: int = 64, variant: int = 0,
+                  beta_scale: float = 1.0, shapes=None) -> List[dict]:
+    """The decode sweep's weight sets, one per linear (2 per layer)."""
+    shapes = sweep_shapes(n_layers) if shapes is None else shapes
+    out = []
+    for i, (K, N) in enumerate(shapes):
+        out.append(weights(K, N, r, key=(3, i // 2, i % 2, variant), beta_scale=beta_scale))
+    return out
+
+
+def sweep_input(M: int = 1, K: int = IN_PROJ_1P3B[0], variant: int = 0) -> np.ndarray:
+    return activations(M, K, key=(3, 999_999 + variant))
+
+
+def weight_bytes(ws: dict) -> int:
+    """Bytes of one weight set as stored: signs + A + B + alpha + beta."""
+    return int(sum(ws[k].nbytes for k in ("w_bits", "A", "B", "alpha", "beta")))

@@ -1,0 +1,171 @@
+"""CPU oracle for the DF-SSM scaffold + int8 LoRA linear (test infrastructure).
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may
+import this package.  It wraps the plain C implementation in dfssm_ref.c
+(built with gcc, no GPU code, no code shared with the HIP library) in numpy
+helpers.  See dfssm_ref.h for the definitions it follows (Sec. 3.2 Eq. 3,
+Sec. 3.3 / Table 1, Sec. 4.1 of the paper).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "dfssm_ref.c")
+LIB = os.path.join(HERE, "libdfssm_ref.so")
+
+OK, ERR_NULL, ERR_SHAPE, ERR_NONFINITE = 0, 1, 2, 7
+F16, F32 = 0, 1
+
+
+def build(src: str = SRC, out: str = LIB, extra: Sequence[str] = (), openmp: bool = True) -> str:
+    """Compile the oracle with gcc: -O2, no contraction, no fast-math."""
+    cmd = ["gcc", "-std=c11", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared",
+           "-Wall", "-Wextra", "-Werror", "-I", HERE]
+    if openmp:
+        cmd.append("-fopenmp")
+    cmd += list(extra) + [src, "-o", out, "-lm"]
+    subprocess.run(cmd, check=True)
+    return out
+
+
+def _p(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+class Oracle:
+    """numpy front end over one build of the C oracle (a path to a .so)."""
+
+    def __init__(self, path: str = LIB):
+        if not os.path.exists(path):
+            build(out=path)
+        self.path = path
+        lib = ctypes.CDLL(path)
+        vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+        lib.dfssm_ref_f16_to_f32.argtypes = [ctypes.c_uint16]
+        lib.dfssm_ref_f16_to_f32.restype = ctypes.c_float
+        lib.dfssm_ref_quantize_act.argtypes = [vp, i32, i64, i64, i64, vp, vp]
+        lib.dfssm_ref_quantize_act.restype = i32
+        lib.dfssm_ref_scaffold_lora_linear.argtypes = [vp, vp, i64, i64, i64, i64, vp, vp, vp, vp,
+                                                       vp, vp, vp, vp, vp, vp]
+        lib.dfssm_ref_scaffold_lora_linear.restype = i32
+        lib.dfssm_ref_chain.argtypes = [i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        lib.dfssm_ref_chain.restype = i32
+        lib.dfssm_ref_threads.restype = i32
+        self.lib = lib
+
+    # -- activation quantisation ------------------------------------------------
+    def f16_to_f32(self, h: int) -> float:
+        return self.lib.dfssm_ref_f16_to_f32(int(h))
+
+    def quantize_act(self, x: np.ndarray, K: Optional[int] = None):
+        """x: [M, ldx] float16 or float32; quantises the first K columns.
+        Returns (Q int8 [M,K], s float32 [M]); raises on a status error."""
+        x = np.ascontiguousarray(x)
+        if x.ndim != 2:
+            raise ValueError("x must be 2-D")
+        M, ldx = x.shape
+        K = ldx if K is None else K
+        dt = {np.dtype(np.float16): F16, np.dtype(np.float32): F32}[x.dtype]
+        q = np.zeros((M, K), np.int8)
+        s = np.zeros((M,), np.float32)
+        st = self.lib.dfssm_ref_quantize_act(_p(x), dt, M, K, ldx, _p(q), _p(s))
+        if st != OK:
+            raise OracleError(st)
+        return q, s
+
+    # -- the linear -----------------------------------------------------------------
+    def linear(self, q, s, w_bits, alpha, A, B, beta):
+        """Returns dict with acc_s (int32 [M,N]), acc_a (int32 [M,r]),
+        acc_b (int64 [M,N]), y32 (float32 [M,N]), y64 (float64 [M,N])."""
+        q = np.ascontiguousarray(q, np.int8)
+        s = np.ascontiguousarray(s, np.float32)
+        w_bits = np.ascontiguousarray(w_bits, np.uint32)
+        alpha = np.ascontiguousarray(alpha, np.float32)
+        M, K = q.shape
+        N = w_bits.shape[0]
+        if w_bits.shape[1] * 32 != K:
+            raise ValueError("w_bits must be [N, K/32]")
+        r = 0 if A is None else A.shape[0]
+        if r > 0:
+            A = np.ascontiguousarray(A, np.int8)
+            B = np.ascontiguousarray(B, np.int8)
+            beta = np.ascontiguousarray(beta, np.float32)
+        else:
+            A = B = beta = None
+        out = dict(acc_s=np.zeros((M, N), np.int32), acc_a=np.zeros((M, max(r, 0)), np.int32),
+                   acc_b=np.zeros((M, N), np.int64), y32=np.zeros((M, N), np.float32),
+                   y64=np.zeros((M, N), np.float64))
+        st = self.lib.dfssm_ref_scaffold_lora_linear(
+            _p(q), _p(s), M, K, N, r, _p(w_bits), _p(alpha), _p(A), _p(B), _p(beta),
+            _p(out["acc_s"]), _p(out["acc_a"]) if r > 0 else None, _p(out["acc_b"]),
+            _p(out["y32"]), _p(out["y64"]))
+        if st != OK:
+            raise OracleError(st)
+        return out
+
+    # -- the chain ------------------------------------------------------------------
+    def chain(self, layers, q0, s0):
+        """layers: sequence of dicts with w_bits, alpha, A, B, beta.
+        Returns (list of y32 [M,N_l], list of Q [M,K_l])."""
+        q0 = np.ascontiguousarray(q0, np.int8)
+        s0 = np.ascontiguousarray(s0, np.float32)
+        M = q0.shape[0]
+        L = len(layers)
+        Ks = np.array([ly["w_bits"].shape[1] * 32 for ly in layers], np.int64)
+        Ns = np.array([ly["w_bits"].shape[0] for ly in layers], np.int64)
+        rs = np.array([0 if ly.get("A") is None else ly["A"].shape[0] for ly in layers], np.int64)
+        keep = []
+
+        def arr(name, dtype):
+            ptrs = (ctypes.c_void_p * L)()
+            for i, ly in enumerate(layers):
+                a = ly.get(name)
+                if a is None or (name in ("A", "B", "beta") and rs[i] == 0):
+                    ptrs[i] = None
+                    continue
+                a = np.ascontiguousarray(a, dtype)
+                keep.append(a)
+                ptrs[i] = a.ctypes.data
+            return ptrs
+
+        pw, pa, pA, pB, pb = (arr("w_bits", np.uint32), arr("alpha", np.float32),
+                              arr("A", np.int8), arr("B", np.int8), arr("beta", np.float32))
+        y_all = np.zeros(int((M * Ns).sum()), np.float32)
+        q_all = np.zeros(int((M * Ks).sum()), np.int8)
+        st = self.lib.dfssm_ref_chain(L, M, _p(Ks), _p(Ns), _p(rs), pw, pa, pA, pB, pb,
+                                      _p(q0), _p(s0), _p(y_all), _p(q_all))
+        if st != OK:
+            raise OracleError(st)
+        ys, qs, yo, qo = [], [], 0, 0
+        for l in range(L):
+            ys.append(y_all[yo:yo + M * Ns[l]].reshape(M, Ns[l]))
+            qs.append(q_all[qo:qo + M * Ks[l]].reshape(M, Ks[l]))
+            yo += M * Ns[l]
+            qo += M * Ks[l]
+        return ys, qs
+
+    def threads(self) -> int:
+        return self.lib.dfssm_ref_threads()
+
+
+class OracleError(RuntimeError):
+    def __init__(self, status: int):
+        super().__init__(f"oracle status {status}")
+        self.status = status
+
+
+_default: Optional[Oracle] = None
+
+
+def get() -> Oracle:
+    """The oracle built from dfssm_ref.c (built on first use)."""
+    global _default
+    if _default is None:
+        _default = Oracle(LIB)
+    return _default

@@ -1,0 +1,105 @@
+/*
+ * dfssm_ref.h -- CPU oracle for the DF-SSM scaffold + int8 LoRA linear.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This is a plain, slow, obviously-correct host
+ * implementation used to check the GPU library.  Only the test suite, the
+ * smoke check and the CPU-baseline leg of the benchmark may load it.  The
+ * product path (include/dfssm.h and its HIP kernels) never calls, links or
+ * includes anything from this directory, and this directory includes nothing
+ * from the product.
+ *
+ * What is computed (paper: Sec. 3.2, Eq. 3, frozen scaffold plus low-rank
+ * correction; Sec. 3.3 and Table 1, 1-bit packed scaffold and int8 LoRA with
+ * per-channel scales; Sec. 4.1, int8 activations fed to an int8 x int8
+ * product), with the scaffold binarised to sign(W) and a per-row scale:
+ *
+ *     y = diag(alpha) * S * q(x)  +  diag(beta) * B * (A * q(x))
+ *
+ *   S      [N,K]  +-1 signs, stored 1 bit each, uint32 words [N][K/32],
+ *                 bit j of word w is column 32*w + j, bit 1 means +1.
+ *   A      [r,K]  int8 LoRA down-projection (the paper's W_B).
+ *   B      [N,r]  int8 LoRA up-projection   (the paper's W_A).
+ *   alpha  [N]    fp32 per-row scaffold scale.
+ *   beta   [N]    fp32 per-row LoRA scale (per-channel int8 scales and the
+ *                 scalar LoRA gain folded together).
+ *   q(x)   = s * Q, per-token absmax int8 quantisation of x.
+ *
+ * Integer accumulators (exact):
+ *   acc_s[m,n] = sum_k S[n,k] * Q[m,k]          int32
+ *   acc_a[m,j] = sum_k A[j,k] * Q[m,k]          int32
+ *   acc_b[m,n] = sum_j B[n,j] * acc_a[m,j]      int64
+ *
+ * Output:
+ *   y64[m,n] = s[m] * (alpha[n]*acc_s + beta[n]*acc_b)   evaluated in fp64
+ *   y32[m,n] = the same in fp32, one rounding per operation, in the order
+ *              fs=(float)acc_s; u=alpha*fs; fb=(float)acc_b; v=beta*fb;
+ *              w=u+v; y=s*w   (r==0: y=s*u).  This is the order in which
+ *              the GPU library evaluates it; the chain needs it bit-exact
+ *              because each output is re-quantised into the next input.
+ *
+ * Parity status: every function here is pinned by the CPU tests (brute
+ * force, closed forms, invariants, hand-derived fixtures).
+ */
+#ifndef DFSSM_REF_H
+#define DFSSM_REF_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  DFSSM_REF_OK = 0,
+  DFSSM_REF_ERR_NULL = 1,
+  DFSSM_REF_ERR_SHAPE = 2,
+  DFSSM_REF_ERR_NONFINITE = 7
+};
+
+enum { DFSSM_REF_F16 = 0, DFSSM_REF_F32 = 1 };
+
+/* IEEE 754 binary16 bit pattern -> the binary32 value it denotes (exact). */
+float dfssm_ref_f16_to_f32(uint16_t h);
+
+/* Per-token absmax quantisation of x [M rows, row stride ldx elements] to
+ * Q int8 [M,K] and s fp32 [M]:
+ *   a = max_k |x[m,k]|
+ *   a < FLT_MIN  ->  Q[m,:] = 0, s[m] = 0
+ *   otherwise       s[m] = a/127, inv = 127/a, Q = clamp(rint(x*inv), -127, 127)
+ * every step one fp32 operation rounded to nearest-even.
+ * Returns DFSSM_REF_ERR_NONFINITE if any x is Inf/NaN. */
+int dfssm_ref_quantize_act(const void* x, int x_dtype, int64_t M, int64_t K,
+                           int64_t ldx, int8_t* q, float* s);
+
+/* The linear.  All outputs are written (acc_* and y32/y64 may be NULL to
+ * skip them).  K > 0, K % 32 == 0, M >= 0, N >= 0, 0 <= r <= 256. */
+int dfssm_ref_scaffold_lora_linear(const int8_t* q, const float* s,
+                                   int64_t M, int64_t K, int64_t N, int64_t r,
+                                   const uint32_t* w_bits, const float* alpha,
+                                   const int8_t* A, const int8_t* B,
+                                   const float* beta,
+                                   int32_t* acc_s, int32_t* acc_a,
+                                   int64_t* acc_b, float* y32, double* y64);
+
+/* A chain of linears in which each output is re-quantised as the next
+ * input: linear 0 consumes (q0, s0); linear l >= 1 consumes
+ * Q_l = quantise(y32_{l-1}[:, 0:K_l]) (fp32 input, row stride N_{l-1}) with
+ * its scale fixed to s_l = 1/127, standing in for the normalisation that
+ * sits between projections in the model.  Requires K_l <= N_{l-1}.
+ * y_all receives every linear's y32 back to back (sum_l M*N_l floats);
+ * q_all (optional) every linear's Q (sum_l M*K_l bytes). */
+int dfssm_ref_chain(int n_layers, int64_t M, const int64_t* K,
+                    const int64_t* N, const int64_t* r,
+                    const uint32_t* const* w_bits, const float* const* alpha,
+                    const int8_t* const* A, const int8_t* const* B,
+                    const float* const* beta, const int8_t* q0,
+                    const float* s0, float* y_all, int8_t* q_all);
+
+/* Number of OpenMP threads the row loops use (1 without OpenMP). */
+int dfssm_ref_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DFSSM_REF_H */

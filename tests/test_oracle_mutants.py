@@ -1,0 +1,59 @@
+"""Planted mistakes in the oracle (on the CPU): each broken copy of
+dfssm_ref.c must fail at least one pin.  This is what shows the pins can
+catch a dropped term, a wrong sign, a wrong index or a transposed operand."""
+import os
+
+import pytest
+
+import oracle
+from oracle import Oracle
+from oracle_pins import ALL_PINS
+
+# (name, [(original text, replacement), ...]) -- every original must occur
+# exactly once in dfssm_ref.c
+MUTANTS = [
+    ("bit_order_msb_first", [("(word >> (k % 32))", "(word >> (31 - k % 32))")]),
+    ("sign_polarity", [("? +1 : -1", "? -1 : +1")]),
+    ("drop_lora_term", [("if (r > 0) d = d + (double)beta[n] * (double)sb;", "(void)sb;"),
+                        ("w = u + v;", "w = u; (void)v;")]),
+    ("A_transposed", [("(int64_t)A[j * K + k]", "(int64_t)A[(k % r) * K + (k / r) % K]")]),
+    ("B_transposed", [("(int64_t)B[n * r + j]", "(int64_t)B[j * N + n]")]),
+    ("lora_down_row0", [("(int64_t)A[j * K + k] * (int64_t)q[m * K + k]", "(int64_t)A[j * K + k] * (int64_t)q[k]")]),
+    ("round_half_away", [("float rq = rintf(t);", "float rq = roundf(t);")]),
+    ("scale_over_128", [("s[m] = a / 127.0f;", "s[m] = a / 128.0f;")]),
+    ("inv_from_s", [("float inv = 127.0f / a;", "float inv = 1.0f / (a / 127.0f);")]),
+    ("acc_b_int32", [("int64_t sb = 0;", "int32_t sb = 0;")]),
+    ("acc_a_int16", [("a_buf[m * r + j] = (int32_t)sum;", "a_buf[m * r + j] = (int16_t)sum;")]),
+    ("f16_bias", [("(1024 + f), e - 25)", "(1024 + f), e - 24)")]),
+    ("f16_subnormal", [("ldexpf((float)f, -24)", "ldexpf((float)f, -25)")]),
+    ("y_missing_s", [("y32[m * N + n] = s[m] * w;", "y32[m * N + n] = w;"),
+                     ("y64[m * N + n] = (double)s[m] * d;", "y64[m * N + n] = d;")]),
+    ("alpha_row0", [("float u = alpha[n] * fs;", "float u = alpha[0] * fs;"),
+                    ("double d = (double)alpha[n] * (double)ss;", "double d = (double)alpha[0] * (double)ss;")]),
+    ("fma_in_epilogue", [("w = u + v;", "w = fmaf(beta[n], fb, u); (void)v;")]),
+    ("absmax_over_stride", [("for (int64_t k = 0; k < K; ++k) {\n      float v = load_x(x, x_dtype, m * ldx + k);\n      if (!isfinite(v))",
+                             "for (int64_t k = 0; k < ldx; ++k) {\n      float v = load_x(x, x_dtype, m * ldx + k);\n      if (!isfinite(v))")]),
+    ("zero_row_unit_scale", [("if (a < FLT_MIN) {\n      s[m] = 0.0f;", "if (a < FLT_MIN) {\n      s[m] = 1.0f;")]),
+    ("chain_keeps_scale", [("for (int64_t m = 0; m < M; ++m) sbuf[m] = 1.0f / 127.0f;", "(void)0;")]),
+    ("chain_wrong_prefix_stride", [("N[l - 1], qbuf, sbuf);", "K[l], qbuf, sbuf);")]),
+]
+
+
+@pytest.mark.parametrize("name,edits", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, name, edits):
+    src = open(oracle.SRC).read()
+    for old, new in edits:
+        assert src.count(old) == 1, (name, old)
+        src = src.replace(old, new)
+    c = tmp_path / "dfssm_ref.c"
+    c.write_text(src)
+    so = str(tmp_path / f"libref_{name}.so")
+    oracle.build(src=str(c), out=so, extra=["-Wno-unused-variable", "-Wno-unused-but-set-variable"])
+    o = Oracle(so)
+    failed = []
+    for pin in ALL_PINS:
+        try:
+            pin(o)
+        except (AssertionError, oracle.OracleError):
+            failed.append(pin.__name__)
+    assert failed, f"planted mistake {name} passed every pin"
