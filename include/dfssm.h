@@ -1,0 +1,166 @@
+/*
+ * dfssm.h -- C ABI of the DF-SSM scaffold + int8 LoRA linear for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The operation (paper: Sec. 3.2, Eq. 3 -- a frozen scaffold plus a low-rank
+ * correction; Sec. 3.3 and Table 1 -- the scaffold stored at 1 bit per
+ * weight, the LoRA factors in int8 with per-channel scales; Sec. 4.1 -- int8
+ * activations feeding an int8 x int8 scaffold product), with the scaffold
+ * binarised to sign(W) and a per-output-row scale:
+ *
+ *     y = diag(alpha) * S * q(x)  +  diag(beta) * B * (A * q(x))
+ *
+ * where q(x) = s * Q is per-token absmax int8 quantisation of x.
+ *
+ * Conventions for every entry point:
+ *  - All array pointers are DEVICE pointers (hipMalloc'd or torch tensors)
+ *    unless a comment says host.  The caller owns every buffer; the library
+ *    never allocates or frees device memory in these calls.
+ *  - Arrays are dense row-major with the shapes given; base pointers must be
+ *    16-byte aligned (DFSSM_ERR_ALIGN otherwise).
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Calls are
+ *    stream-ordered and asynchronous: they validate on the host, enqueue
+ *    kernels and return.  A validation failure returns before anything is
+ *    enqueued.  A launch failure returns DFSSM_ERR_DEVICE.  Faults inside a
+ *    kernel surface at the caller's next synchronisation.
+ *  - Outputs must not alias inputs.  Inputs must be finite; the kernels do
+ *    not check this and the output for non-finite input is unspecified.
+ *  - Results are bitwise deterministic run to run (integer arithmetic, no
+ *    floating-point atomics).
+ *  - No C++ exception crosses this interface.  dfssm_last_error() returns a
+ *    thread-local message describing the last failure on the calling thread.
+ *
+ * Layouts:
+ *   x      [M, ldx]  fp16 or fp32 activations, row stride ldx >= K elements
+ *   q      [M, K]    int8 codes Q, |Q| <= 127
+ *   s      [M]       fp32 per-token scale
+ *   w_bits [N, K/32] uint32; bit j of word w of row n is S[n, 32*w + j],
+ *                    1 -> +1, 0 -> -1 (little-endian, least significant bit
+ *                    first)
+ *   alpha  [N]       fp32 scaffold row scale
+ *   A      [r, K]    int8 LoRA down-projection (the paper's W_B)
+ *   B      [N, r]    int8 LoRA up-projection   (the paper's W_A)
+ *   beta   [N]       fp32 LoRA row scale (per-channel int8 scales and the
+ *                    scalar LoRA gain folded together)
+ *   y      [M, N]    fp32 output
+ * Limits: 0 < K <= 65536, K % 32 == 0; M, N >= 0 (0 is a no-op);
+ *         0 <= r <= 256.  When r == 0, A, B and beta may be NULL.
+ *
+ * Arithmetic (exact where it is integer):
+ *   acc_s = Q * S^T  (int32), acc_a = Q * A^T (int32),
+ *   acc_b = acc_a * B^T (int64, exact), then per element in fp32 with one
+ *   rounding per operation: fs=(float)acc_s; u=alpha*fs; fb=(float)acc_b;
+ *   v=beta*fb; w=u+v; y=s*w   (r == 0: y = s*u).
+ */
+#ifndef DFSSM_H
+#define DFSSM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DFSSM_OK = 0,
+  DFSSM_ERR_NULL = 1,        /* a required pointer is NULL */
+  DFSSM_ERR_SHAPE = 2,       /* a size or stride is outside the limits */
+  DFSSM_ERR_ALIGN = 3,       /* a pointer is not 16-byte aligned */
+  DFSSM_ERR_WORKSPACE = 4,   /* workspace missing or smaller than required */
+  DFSSM_ERR_DEVICE = 5,      /* a HIP call failed (see dfssm_last_error) */
+  DFSSM_ERR_UNSUPPORTED = 6  /* valid request this build does not handle */
+} dfssm_status;
+
+typedef enum { DFSSM_F16 = 0, DFSSM_F32 = 1 } dfssm_dtype;
+
+/* Kernel family selection for dfssm_scaffold_lora_linear_ex. */
+typedef enum {
+  DFSSM_PATH_AUTO = 0,    /* decode kernels for small M, MFMA kernels above */
+  DFSSM_PATH_DECODE = 1,  /* bit-plane popcount GEMV (any M, best for M <= 4) */
+  DFSSM_PATH_MFMA = 2     /* sign bits expanded on chip + int8 MFMA */
+} dfssm_path;
+
+/* Per-token absmax int8 quantisation of the activations (the int8 operand
+ * of the scaffold product, Sec. 4.1).  For each row m:
+ *   a = max_k |x[m,k]|;  a < FLT_MIN -> Q[m,:] = 0, s[m] = 0;
+ *   else s[m] = a/127, inv = 127/a, Q[m,k] = clamp(rint(x[m,k]*inv), +-127)
+ * with fp32 operations rounded to nearest-even (fp16 input is widened to
+ * fp32 exactly first).
+ *   x       device [M, ldx], element type x_dtype (DFSSM_F16 or DFSSM_F32)
+ *   q       device [M, K] int8 output;  s  device [M] fp32 output
+ * Errors: NULL/SHAPE/ALIGN (x needs only element alignment: 2 B for fp16,
+ * 4 B for fp32), DEVICE. */
+dfssm_status dfssm_quantize_act(const void* x, int x_dtype, int64_t M, int64_t K,
+                                int64_t ldx, int8_t* q, float* s, void* stream);
+
+/* Bytes of device workspace dfssm_scaffold_lora_linear needs for (M,K,N,r). */
+size_t dfssm_linear_workspace_bytes(int64_t M, int64_t K, int64_t N, int64_t r);
+
+/* The scaffold + LoRA linear (Eq. 3 with a binary scaffold), on already
+ * quantised activations (q, s).  Writes y [M,N].  `workspace` is device
+ * memory of at least dfssm_linear_workspace_bytes(M,K,N,r) bytes, used for
+ * acc_a and per-token staging; its contents on entry do not matter.
+ * Errors: NULL, SHAPE, ALIGN, WORKSPACE, DEVICE. */
+dfssm_status dfssm_scaffold_lora_linear(const int8_t* q, const float* s, int64_t M,
+                                        int64_t K, int64_t N, int64_t r,
+                                        const uint32_t* w_bits, const float* alpha,
+                                        const int8_t* A, const int8_t* B,
+                                        const float* beta, float* y, void* workspace,
+                                        size_t workspace_bytes, void* stream);
+
+/* Same operation with an explicit kernel family and optional integer
+ * accumulator outputs (each may be NULL): acc_s int32 [M,N], acc_a int32
+ * [M,r], acc_b int64 [M,N].  y may be NULL too.  The accumulators are the
+ * exact integers defined above, identical on every path. */
+dfssm_status dfssm_scaffold_lora_linear_ex(const int8_t* q, const float* s, int64_t M,
+                                           int64_t K, int64_t N, int64_t r,
+                                           const uint32_t* w_bits, const float* alpha,
+                                           const int8_t* A, const int8_t* B,
+                                           const float* beta, float* y, int path,
+                                           int32_t* acc_s, int32_t* acc_a,
+                                           int64_t* acc_b, void* workspace,
+                                           size_t workspace_bytes, void* stream);
+
+/* One projection of a chain (host struct; the pointers in it are device
+ * pointers with the layouts above). */
+typedef struct {
+  const uint32_t* w_bits;
+  const float* alpha;
+  const int8_t* A;
+  const int8_t* B;
+  const float* beta;
+  int64_t K, N, r;
+} dfssm_layer;
+
+/* Bytes of device workspace dfssm_scaffold_lora_chain needs. */
+size_t dfssm_chain_workspace_bytes(const dfssm_layer* layers, int n_layers, int64_t M);
+
+/* A chain of linears run back to back on one stream, each output
+ * re-quantised as the next input (the decode sweep over a model's
+ * projections, Sec. 4.1):
+ *   linear 0 consumes (q0 [M,K_0], s0 [M]);
+ *   linear l >= 1 consumes Q_l = quantise(y_{l-1}[:, 0:K_l]) (fp32, row
+ *   stride N_{l-1}, same rule as dfssm_quantize_act) with s_l = 1/127 for
+ *   every token, standing in for the normalisation between projections.
+ * Requires K_l <= N_{l-1}.  y_all (device) receives every linear's y back
+ * to back: sum_l M*N_l floats, linear l at offset sum_{i<l} M*N_i.
+ * `layers` is a HOST array of n_layers entries.  M must be 1..4.
+ * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */
+dfssm_status dfssm_scaffold_lora_chain(const dfssm_layer* layers, int n_layers, int64_t M,
+                                       const int8_t* q0, const float* s0, float* y_all,
+                                       void* workspace, size_t workspace_bytes,
+                                       void* stream);
+
+/* Static text for a status code. */
+const char* dfssm_status_string(int status);
+/* Thread-local description of the last failure on this thread ("" if none). */
+const char* dfssm_last_error(void);
+/* Library version string. */
+const char* dfssm_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DFSSM_H */

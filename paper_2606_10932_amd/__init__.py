@@ -1,0 +1,208 @@
+"""Python binding of libdfssm.so, the MI355X (gfx950) DF-SSM scaffold + int8
+LoRA linear (include/dfssm.h).
+
+Argument marshalling only: every step runs in the library's HIP kernels.
+PyTorch provides device memory and the current HIP stream.  Importing this
+package loads the in-tree library and fails loudly if it has not been built
+(``python -m paper_2606_10932_amd.build``); there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdfssm.so")
+
+OK, ERR_NULL, ERR_SHAPE, ERR_ALIGN, ERR_WORKSPACE, ERR_DEVICE, ERR_UNSUPPORTED = range(7)
+F16, F32 = 0, 1
+PATH_AUTO, PATH_DECODE, PATH_MFMA = 0, 1, 2
+
+EXPORTS = ["dfssm_quantize_act", "dfssm_linear_workspace_bytes", "dfssm_scaffold_lora_linear",
+           "dfssm_scaffold_lora_linear_ex", "dfssm_chain_workspace_bytes",
+           "dfssm_scaffold_lora_chain", "dfssm_status_string", "dfssm_last_error", "dfssm_version"]
+
+
+class DfssmError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"dfssm status {status} ({msg})")
+        self.status = status
+
+
+class Layer(ctypes.Structure):
+    """dfssm_layer: one projection of a chain (device pointers + sizes)."""
+    _fields_ = [("w_bits", ctypes.c_void_p), ("alpha", ctypes.c_void_p), ("A", ctypes.c_void_p),
+                ("B", ctypes.c_void_p), ("beta", ctypes.c_void_p), ("K", ctypes.c_int64),
+                ("N", ctypes.c_int64), ("r", ctypes.c_int64)]
+
+
+def _load(path: str = LIB_PATH) -> ctypes.CDLL:
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with `python -m paper_2606_10932_amd.build`")
+    lib = ctypes.CDLL(path)
+    vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
+    lib.dfssm_quantize_act.argtypes = [vp, i32, i64, i64, i64, vp, vp, vp]
+    lib.dfssm_quantize_act.restype = i32
+    lib.dfssm_linear_workspace_bytes.argtypes = [i64, i64, i64, i64]
+    lib.dfssm_linear_workspace_bytes.restype = sz
+    lib.dfssm_scaffold_lora_linear.argtypes = [vp, vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.dfssm_scaffold_lora_linear.restype = i32
+    lib.dfssm_scaffold_lora_linear_ex.argtypes = [vp, vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, i32,
+                                                  vp, vp, vp, vp, sz, vp]
+    lib.dfssm_scaffold_lora_linear_ex.restype = i32
+    lib.dfssm_chain_workspace_bytes.argtypes = [ctypes.POINTER(Layer), i32, i64]
+    lib.dfssm_chain_workspace_bytes.restype = sz
+    lib.dfssm_scaffold_lora_chain.argtypes = [ctypes.POINTER(Layer), i32, i64, vp, vp, vp, vp, sz, vp]
+    lib.dfssm_scaffold_lora_chain.restype = i32
+    lib.dfssm_status_string.argtypes = [i32]
+    lib.dfssm_status_string.restype = ctypes.c_char_p
+    lib.dfssm_last_error.restype = ctypes.c_char_p
+    lib.dfssm_version.restype = ctypes.c_char_p
+    return lib
+
+
+lib = _load()
+
+
+def last_error() -> str:
+    return lib.dfssm_last_error().decode()
+
+
+def _check(status: int):
+    if status != OK:
+        raise DfssmError(status, f"{lib.dfssm_status_string(status).decode()}: {last_error()}")
+
+
+# ------------------------------------------------------------------ torch glue
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream=None) -> int:
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _need(t, dtype, name, ndim=None):
+    torch = _torch()
+    if t is None:
+        return
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must be {ndim}-D")
+    del torch
+
+
+def linear_workspace_bytes(M: int, K: int, N: int, r: int) -> int:
+    return int(lib.dfssm_linear_workspace_bytes(M, K, N, r))
+
+
+def quantize_act(x, K: Optional[int] = None, q=None, s=None, stream=None):
+    """Per-token absmax int8 quantisation of x ([M, ldx] fp16/fp32 device
+    tensor, unit stride along K).  Returns (q int8 [M,K], s fp32 [M])."""
+    torch = _torch()
+    if x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be 2-D with unit column stride")
+    M, ldx = x.shape[0], x.stride(0) if x.shape[0] > 1 else x.shape[1]
+    K = x.shape[1] if K is None else K
+    dt = {torch.float16: F16, torch.float32: F32}[x.dtype]
+    q = torch.empty((M, K), dtype=torch.int8, device=x.device) if q is None else q
+    s = torch.empty((M,), dtype=torch.float32, device=x.device) if s is None else s
+    _need(q, torch.int8, "q", 2)
+    _need(s, torch.float32, "s", 1)
+    _check(lib.dfssm_quantize_act(x.data_ptr(), dt, M, K, ldx, q.data_ptr(), s.data_ptr(), _stream(stream)))
+    return q, s
+
+
+def scaffold_lora_linear(q, s, w_bits, alpha, A=None, B=None, beta=None, y=None, workspace=None,
+                         path: int = PATH_AUTO, acc: bool = False, stream=None):
+    """y = s*(alpha*acc_s + beta*acc_b) for int8 codes q [M,K], scales s [M],
+    packed signs w_bits [N,K/32] (int32 or uint32 storage), alpha/beta [N],
+    A [r,K], B [N,r].  With acc=True also returns (acc_s, acc_a, acc_b)."""
+    torch = _torch()
+    M, K = q.shape
+    N = w_bits.shape[0]
+    r = 0 if A is None else A.shape[0]
+    _need(q, torch.int8, "q", 2)
+    _need(s, torch.float32, "s", 1)
+    if w_bits.dtype not in (torch.int32, torch.uint32):
+        raise ValueError("w_bits must be int32/uint32 storage")
+    _need(w_bits, w_bits.dtype, "w_bits", 2)
+    if w_bits.shape[1] * 32 != K:
+        raise ValueError("w_bits must be [N, K/32]")
+    _need(alpha, torch.float32, "alpha", 1)
+    if r:
+        _need(A, torch.int8, "A", 2)
+        _need(B, torch.int8, "B", 2)
+        _need(beta, torch.float32, "beta", 1)
+        if tuple(A.shape) != (r, K) or tuple(B.shape) != (N, r):
+            raise ValueError("A must be [r,K] and B [N,r]")
+    dev = q.device
+    y = torch.empty((M, N), dtype=torch.float32, device=dev) if y is None else y
+    _need(y, torch.float32, "y", 2)
+    nbytes = linear_workspace_bytes(M, K, N, r)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    acc_s = acc_a = acc_b = None
+    if acc:
+        acc_s = torch.empty((M, N), dtype=torch.int32, device=dev)
+        acc_a = torch.empty((M, max(r, 1)), dtype=torch.int32, device=dev)
+        acc_b = torch.empty((M, N), dtype=torch.int64, device=dev)
+    st = lib.dfssm_scaffold_lora_linear_ex(
+        q.data_ptr(), s.data_ptr(), M, K, N, r, w_bits.data_ptr(), alpha.data_ptr(),
+        _ptr(A) if r else None, _ptr(B) if r else None, _ptr(beta) if r else None, y.data_ptr(),
+        path, _ptr(acc_s), _ptr(acc_a) if r else None, _ptr(acc_b), workspace.data_ptr(),
+        workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st)
+    if acc:
+        return y, acc_s, acc_a[:, :r], acc_b
+    return y
+
+
+def make_layers(layers: Sequence[dict]):
+    """ctypes array of dfssm_layer from dicts of device tensors."""
+    arr = (Layer * len(layers))()
+    for i, ly in enumerate(layers):
+        r = 0 if ly.get("A") is None else ly["A"].shape[0]
+        arr[i] = Layer(ly["w_bits"].data_ptr(), ly["alpha"].data_ptr(),
+                       ly["A"].data_ptr() if r else None, ly["B"].data_ptr() if r else None,
+                       ly["beta"].data_ptr() if r else None, ly["w_bits"].shape[1] * 32,
+                       ly["w_bits"].shape[0], r)
+    return arr
+
+
+def chain_workspace_bytes(layer_arr, M: int) -> int:
+    return int(lib.dfssm_chain_workspace_bytes(layer_arr, len(layer_arr), M))
+
+
+def scaffold_lora_chain(layers, q0, s0, y_all=None, workspace=None, layer_arr=None, stream=None) -> List:
+    """Run the re-quantising chain.  Returns the list of per-linear outputs
+    (views into y_all)."""
+    torch = _torch()
+    arr = make_layers(layers) if layer_arr is None else layer_arr
+    M = q0.shape[0]
+    Ns = [ly["w_bits"].shape[0] for ly in layers]
+    total = M * sum(Ns)
+    if y_all is None:
+        y_all = torch.empty(total, dtype=torch.float32, device=q0.device)
+    if workspace is None:
+        workspace = torch.empty(max(chain_workspace_bytes(arr, M), 1), dtype=torch.uint8, device=q0.device)
+    _check(lib.dfssm_scaffold_lora_chain(arr, len(arr), M, q0.data_ptr(), s0.data_ptr(), y_all.data_ptr(),
+                                         workspace.data_ptr(), workspace.numel(), _stream(stream)))
+    outs, off = [], 0
+    for N in Ns:
+        outs.append(y_all[off:off + M * N].view(M, N))
+        off += M * N
+    return outs

@@ -1,0 +1,242 @@
+// dfssm_api.hip -- host side of include/dfssm.h: argument validation,
+// workspace sizing, kernel-family dispatch, the chain driver and error
+// reporting.  Validation is pure host code that runs before any HIP call,
+// so a rejected call enqueues nothing.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "dfssm_internal.hpp"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+void clear_error() { g_last_error[0] = 0; }
+
+dfssm_status fail(dfssm_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+dfssm_status device_fail(hipError_t e, const char* what) {
+  return fail(DFSSM_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+dfssm_status check_linear(int64_t M, int64_t K, int64_t N, int64_t r) {
+  if (K <= 0 || K % 32 != 0 || K > dfssm::kMaxK)
+    return fail(DFSSM_ERR_SHAPE, "K=%lld must be a positive multiple of 32 and <= %lld",
+                (long long)K, (long long)dfssm::kMaxK);
+  if (M < 0 || N < 0) return fail(DFSSM_ERR_SHAPE, "M=%lld and N=%lld must be >= 0", (long long)M, (long long)N);
+  if (M > INT32_MAX / 2 || N > INT32_MAX / 2)
+    return fail(DFSSM_ERR_SHAPE, "M=%lld or N=%lld too large", (long long)M, (long long)N);
+  if (r < 0 || r > dfssm::kMaxRank)
+    return fail(DFSSM_ERR_SHAPE, "r=%lld must be in [0, %lld]", (long long)r, (long long)dfssm::kMaxRank);
+  return DFSSM_OK;
+}
+
+struct Ptr {
+  const void* p;
+  const char* name;
+};
+
+dfssm_status check_ptrs(std::initializer_list<Ptr> required, std::initializer_list<Ptr> optional) {
+  for (const Ptr& x : required) {
+    if (!x.p) return fail(DFSSM_ERR_NULL, "%s is NULL", x.name);
+    if (!aligned16(x.p)) return fail(DFSSM_ERR_ALIGN, "%s is not 16-byte aligned", x.name);
+  }
+  for (const Ptr& x : optional)
+    if (x.p && !aligned16(x.p)) return fail(DFSSM_ERR_ALIGN, "%s is not 16-byte aligned", x.name);
+  return DFSSM_OK;
+}
+
+size_t linear_ws_bytes(int64_t M, int64_t K, int64_t r) {
+  return dfssm::carve_linear_workspace(nullptr, M, K, r).bytes;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dfssm_version(void) { return "dfssm-gfx950 0.1"; }
+
+const char* dfssm_status_string(int status) {
+  switch (status) {
+    case DFSSM_OK: return "ok";
+    case DFSSM_ERR_NULL: return "null pointer";
+    case DFSSM_ERR_SHAPE: return "invalid shape";
+    case DFSSM_ERR_ALIGN: return "misaligned pointer";
+    case DFSSM_ERR_WORKSPACE: return "workspace too small";
+    case DFSSM_ERR_DEVICE: return "device error";
+    case DFSSM_ERR_UNSUPPORTED: return "unsupported";
+    default: return "unknown status";
+  }
+}
+
+const char* dfssm_last_error(void) { return g_last_error; }
+
+dfssm_status dfssm_quantize_act(const void* x, int x_dtype, int64_t M, int64_t K, int64_t ldx,
+                                int8_t* q, float* s, void* stream) {
+  clear_error();
+  if (x_dtype != DFSSM_F16 && x_dtype != DFSSM_F32) return fail(DFSSM_ERR_SHAPE, "x_dtype=%d", x_dtype);
+  if (K <= 0 || K % 32 != 0 || K > dfssm::kMaxK)
+    return fail(DFSSM_ERR_SHAPE, "K=%lld must be a positive multiple of 32 and <= %lld", (long long)K,
+                (long long)dfssm::kMaxK);
+  if (M < 0 || M > INT32_MAX / 2) return fail(DFSSM_ERR_SHAPE, "M=%lld", (long long)M);
+  if (ldx < K) return fail(DFSSM_ERR_SHAPE, "ldx=%lld < K=%lld", (long long)ldx, (long long)K);
+  if (M == 0) return DFSSM_OK;
+  if (!x) return fail(DFSSM_ERR_NULL, "x is NULL");
+  const size_t esz = x_dtype == DFSSM_F16 ? 2 : 4;
+  if (reinterpret_cast<uintptr_t>(x) % esz) return fail(DFSSM_ERR_ALIGN, "x is not element aligned");
+  dfssm_status st = check_ptrs({{q, "q"}, {s, "s"}}, {});
+  if (st != DFSSM_OK) return st;
+  hipError_t e = dfssm::launch_quantize(x, x_dtype, M, K, ldx, q, s, 0, (hipStream_t)stream);
+  return e == hipSuccess ? DFSSM_OK : device_fail(e, "quantize launch");
+}
+
+size_t dfssm_linear_workspace_bytes(int64_t M, int64_t K, int64_t N, int64_t r) {
+  (void)N;
+  if (M < 0 || K <= 0 || r < 0) return 0;
+  return linear_ws_bytes(M, K, r);
+}
+
+dfssm_status dfssm_scaffold_lora_linear_ex(const int8_t* q, const float* s, int64_t M, int64_t K,
+                                           int64_t N, int64_t r, const uint32_t* w_bits,
+                                           const float* alpha, const int8_t* A, const int8_t* B,
+                                           const float* beta, float* y, int path, int32_t* acc_s,
+                                           int32_t* acc_a, int64_t* acc_b, void* workspace,
+                                           size_t workspace_bytes, void* stream) {
+  clear_error();
+  dfssm_status st = check_linear(M, K, N, r);
+  if (st != DFSSM_OK) return st;
+  if (path != DFSSM_PATH_AUTO && path != DFSSM_PATH_DECODE && path != DFSSM_PATH_MFMA)
+    return fail(DFSSM_ERR_SHAPE, "path=%d", path);
+  if (M == 0 || N == 0) return DFSSM_OK;
+  st = check_ptrs({{q, "q"}, {s, "s"}, {w_bits, "w_bits"}, {alpha, "alpha"}, {workspace, "workspace"}},
+                  {{y, "y"}, {acc_s, "acc_s"}, {acc_a, "acc_a"}, {acc_b, "acc_b"}});
+  if (st != DFSSM_OK) return st;
+  if (r > 0) {
+    st = check_ptrs({{A, "A"}, {B, "B"}, {beta, "beta"}}, {});
+    if (st != DFSSM_OK) return st;
+  }
+  const size_t need = linear_ws_bytes(M, K, r);
+  if (workspace_bytes < need)
+    return fail(DFSSM_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, need);
+  dfssm::LinearWorkspace ws = dfssm::carve_linear_workspace(workspace, M, K, r);
+  if (path == DFSSM_PATH_AUTO) path = M <= dfssm::kDecodeM0 ? DFSSM_PATH_DECODE : DFSSM_PATH_MFMA;
+  hipStream_t hs = (hipStream_t)stream;
+  hipError_t e = path == DFSSM_PATH_DECODE
+                     ? dfssm::launch_decode_linear(q, s, M, K, N, r, w_bits, alpha, A, B, beta, y,
+                                                   acc_s, acc_a, acc_b, ws, hs)
+                     : dfssm::launch_mfma_linear(q, s, M, K, N, r, w_bits, alpha, A, B, beta, y,
+                                                 acc_s, acc_a, acc_b, ws, hs);
+  return e == hipSuccess ? DFSSM_OK : device_fail(e, "linear launch");
+}
+
+dfssm_status dfssm_scaffold_lora_linear(const int8_t* q, const float* s, int64_t M, int64_t K,
+                                        int64_t N, int64_t r, const uint32_t* w_bits,
+                                        const float* alpha, const int8_t* A, const int8_t* B,
+                                        const float* beta, float* y, void* workspace,
+                                        size_t workspace_bytes, void* stream) {
+  if (!y && M > 0 && N > 0) {
+    clear_error();
+    return fail(DFSSM_ERR_NULL, "y is NULL");
+  }
+  return dfssm_scaffold_lora_linear_ex(q, s, M, K, N, r, w_bits, alpha, A, B, beta, y,
+                                       DFSSM_PATH_AUTO, nullptr, nullptr, nullptr, workspace,
+                                       workspace_bytes, stream);
+}
+
+// ---------------------------------------------------------------- chain
+// Workspace: Q [M, Kmax] int8, s [M] fp32, then one linear workspace sized
+// for the largest layer.
+static size_t chain_ws_parts(const dfssm_layer* layers, int n_layers, int64_t M, size_t* off_s,
+                             size_t* off_lin) {
+  int64_t kmax = 0, rmax = 0;
+  for (int l = 0; l < n_layers; ++l) {
+    kmax = std::max(kmax, layers[l].K);
+    rmax = std::max(rmax, layers[l].r);
+  }
+  size_t o = (size_t)dfssm::round_up(M * kmax, 256);
+  *off_s = o;
+  o += (size_t)dfssm::round_up(M * 4, 256);
+  *off_lin = o;
+  size_t lin = 0;
+  for (int l = 0; l < n_layers; ++l) lin = std::max(lin, linear_ws_bytes(M, layers[l].K, layers[l].r));
+  return o + lin;
+}
+
+size_t dfssm_chain_workspace_bytes(const dfssm_layer* layers, int n_layers, int64_t M) {
+  if (!layers || n_layers <= 0 || M <= 0) return 0;
+  size_t a, b;
+  return chain_ws_parts(layers, n_layers, M, &a, &b);
+}
+
+dfssm_status dfssm_scaffold_lora_chain(const dfssm_layer* layers, int n_layers, int64_t M,
+                                       const int8_t* q0, const float* s0, float* y_all,
+                                       void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  if (n_layers < 0) return fail(DFSSM_ERR_SHAPE, "n_layers=%d", n_layers);
+  if (n_layers == 0 || M == 0) return DFSSM_OK;
+  if (!layers) return fail(DFSSM_ERR_NULL, "layers is NULL");
+  if (M < 0 || M > 4) return fail(M < 0 ? DFSSM_ERR_SHAPE : DFSSM_ERR_UNSUPPORTED, "chain M=%lld (1..4)", (long long)M);
+  for (int l = 0; l < n_layers; ++l) {
+    const dfssm_layer& L = layers[l];
+    char why[256];
+    dfssm_status st = check_linear(M, L.K, L.N, L.r);
+    if (st != DFSSM_OK) {
+      snprintf(why, sizeof(why), "%s", g_last_error);
+      return fail(st, "layer %d: %s", l, why);
+    }
+    if (L.N <= 0) return fail(DFSSM_ERR_SHAPE, "layer %d: N must be > 0", l);
+    if (l > 0 && L.K > layers[l - 1].N)
+      return fail(DFSSM_ERR_SHAPE, "layer %d: K=%lld > previous N=%lld", l, (long long)L.K,
+                  (long long)layers[l - 1].N);
+    st = check_ptrs({{L.w_bits, "w_bits"}, {L.alpha, "alpha"}}, {});
+    if (st == DFSSM_OK && L.r > 0) st = check_ptrs({{L.A, "A"}, {L.B, "B"}, {L.beta, "beta"}}, {});
+    if (st != DFSSM_OK) {
+      snprintf(why, sizeof(why), "%s", g_last_error);
+      return fail(st, "layer %d: %s", l, why);
+    }
+  }
+  dfssm_status st = check_ptrs({{q0, "q0"}, {s0, "s0"}, {y_all, "y_all"}, {workspace, "workspace"}}, {});
+  if (st != DFSSM_OK) return st;
+  size_t off_s, off_lin;
+  const size_t need = chain_ws_parts(layers, n_layers, M, &off_s, &off_lin);
+  if (workspace_bytes < need)
+    return fail(DFSSM_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, need);
+
+  hipStream_t hs = (hipStream_t)stream;
+  char* base = static_cast<char*>(workspace);
+  int8_t* qbuf = reinterpret_cast<int8_t*>(base);
+  float* sbuf = reinterpret_cast<float*>(base + off_s);
+  float* y_prev = nullptr;
+  float* y_cur = y_all;
+  for (int l = 0; l < n_layers; ++l) {
+    const dfssm_layer& L = layers[l];
+    const int8_t* ql = q0;
+    const float* sl = s0;
+    if (l > 0) {
+      hipError_t e = dfssm::launch_quantize(y_prev, DFSSM_F32, M, L.K, layers[l - 1].N, qbuf, sbuf, 1, hs);
+      if (e != hipSuccess) return device_fail(e, "chain quantize launch");
+      ql = qbuf;
+      sl = sbuf;
+    }
+    dfssm::LinearWorkspace ws = dfssm::carve_linear_workspace(base + off_lin, M, L.K, L.r);
+    hipError_t e = dfssm::launch_decode_linear(ql, sl, M, L.K, L.N, L.r, L.w_bits, L.alpha, L.A, L.B,
+                                               L.beta, y_cur, nullptr, nullptr, nullptr, ws, hs);
+    if (e != hipSuccess) return device_fail(e, "chain linear launch");
+    y_prev = y_cur;
+    y_cur += M * L.N;
+  }
+  return DFSSM_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,122 @@
+// dfssm_internal.hpp -- shared declarations of the HIP implementation of
+// include/dfssm.h: workspace layout, kernel launchers and small device
+// helpers.  gfx950 (CDNA4) only: wave64, v_mfma_i32_16x16x64_i8,
+// v_dot4_i32_i8, v_bcnt_u32_b32.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "dfssm.h"
+
+namespace dfssm {
+
+constexpr int kWave = 64;
+constexpr int64_t kMaxK = 65536;
+constexpr int64_t kMaxRank = 256;
+// Largest M the bit-plane decode kernels take in one pass; larger M on the
+// decode path is processed in blocks of this many tokens.
+constexpr int kDecodeMaxTokens = 4;
+// Automatic dispatch: M <= kDecodeM0 uses the decode kernels.
+constexpr int64_t kDecodeM0 = 4;
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+
+// Per-call workspace (device), every region 256-byte aligned:
+//   acc_a  int32 [M][r]           LoRA down-projection
+//   limbs  int8  [4][M][rp]       acc_a split into 4 signed base-256 digits,
+//                                 rp = r rounded up to 64 (zero padded)
+//   sumq   int32 [M]              sum_k Q[m,k]
+//   planes uint32 [M][C][8][4]    two's-complement bit-planes of Q, C =
+//                                 ceil(K/128) chunks of 4 words (zero padded)
+struct LinearWorkspace {
+  int32_t* acc_a;
+  int8_t* limbs;
+  int32_t* sumq;
+  uint32_t* planes;
+  size_t bytes;
+};
+
+inline int64_t rank_padded(int64_t r) { return round_up(r > 0 ? r : 1, 64); }
+inline int64_t plane_chunks(int64_t K) { return ceil_div(K, 128); }
+
+inline LinearWorkspace carve_linear_workspace(void* base, int64_t M, int64_t K, int64_t r) {
+  LinearWorkspace ws{};
+  size_t off = 0;
+  auto take = [&](size_t n) {
+    size_t o = off;
+    off += (size_t)round_up((int64_t)n, 256);
+    return o;
+  };
+  size_t o_acc = take((size_t)(M * r) * 4);
+  size_t o_limb = take((size_t)(4 * M * rank_padded(r)));
+  size_t o_sum = take((size_t)M * 4);
+  size_t o_pl = take((size_t)(M * plane_chunks(K) * 128));
+  char* b = static_cast<char*>(base);
+  ws.acc_a = reinterpret_cast<int32_t*>(b + o_acc);
+  ws.limbs = reinterpret_cast<int8_t*>(b + o_limb);
+  ws.sumq = reinterpret_cast<int32_t*>(b + o_sum);
+  ws.planes = reinterpret_cast<uint32_t*>(b + o_pl);
+  ws.bytes = off;
+  return ws;
+}
+
+// ---------------------------------------------------------------- launchers
+// All return hipSuccess or the launch error; shapes are validated by the
+// caller.
+
+// scale_mode 0: s = absmax/127 (0 for an all-zero row); 1: s = 1/127.
+hipError_t launch_quantize(const void* x, int x_dtype, int64_t M, int64_t K, int64_t ldx,
+                           int8_t* q, float* s, int scale_mode, hipStream_t st);
+
+// Decode path: prep (acc_a, bit-planes) then the popcount GEMV with the
+// fused LoRA up-projection and epilogue.
+hipError_t launch_decode_linear(const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N,
+                                int64_t r, const uint32_t* w_bits, const float* alpha,
+                                const int8_t* A, const int8_t* B, const float* beta, float* y,
+                                int32_t* acc_s, int32_t* acc_a_out, int64_t* acc_b,
+                                const LinearWorkspace& ws, hipStream_t st);
+
+// MFMA path: LoRA down-projection + limbs + sum Q, then the expanded-sign
+// int8 MFMA GEMM with the LoRA up-projection and epilogue.
+hipError_t launch_mfma_linear(const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N,
+                              int64_t r, const uint32_t* w_bits, const float* alpha,
+                              const int8_t* A, const int8_t* B, const float* beta, float* y,
+                              int32_t* acc_s, int32_t* acc_a_out, int64_t* acc_b,
+                              const LinearWorkspace& ws, hipStream_t st);
+
+}  // namespace dfssm
+
+// ------------------------------------------------------------ device helpers
+namespace dfssm_dev {
+
+// Signed base-256 digits of v with every digit in [-128, 127]:
+// v = d0 + 256*d1 + 65536*d2 + 16777216*d3, valid for |v| < 2^31 - 2^24.
+__device__ __forceinline__ void split_limbs(int32_t v, int8_t d[4]) {
+#pragma unroll
+  for (int t = 0; t < 3; ++t) {
+    int8_t lo = (int8_t)(v & 0xff);
+    d[t] = lo;
+    v = (v - (int32_t)lo) >> 8;  // exact: v - lo is a multiple of 256
+  }
+  d[3] = (int8_t)v;
+}
+
+// The fixed-order fp32 output scaling y = s*(alpha*fs + beta*fb); the
+// library is compiled with -ffp-contract=off so no multiply-add fuses.
+__device__ __forceinline__ float epilogue(float s, float alpha, float beta, int32_t acc_s,
+                                          int64_t acc_b, bool lora) {
+  float fs = (float)acc_s;
+  float u = alpha * fs;
+  float w = u;
+  if (lora) {
+    float fb = (float)acc_b;
+    float v = beta * fb;
+    w = u + v;
+  }
+  return s * w;
+}
+
+}  // namespace dfssm_dev

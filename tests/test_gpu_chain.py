@@ -1,0 +1,54 @@
+"""GPU parity of the re-quantising chain (dfssm_scaffold_lora_chain) against
+the oracle chain.  Every linear's y is compared: bit-exact against the
+fp32-ordered oracle (a one-ulp difference would change a later Q) and within
+the fp32 tolerance of it."""
+import numpy as np
+import pytest
+
+import dfssm_synth as S
+import oracle
+from gpu_util import Y_TOL, dev, dev_weights, host, say, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def env():
+    torch = torch_cuda()
+    import paper_2606_10932_amd as D
+    oracle.build()
+    return torch, D, oracle.get()
+
+
+def _check_chain(env, shapes, r, M, key):
+    torch, D, o = env
+    layers = [S.weights(K, N, r, key=(20, key, i)) for i, (K, N) in enumerate(shapes)]
+    x = S.activations(M, shapes[0][0], key=(20, key))
+    q0, s0 = o.quantize_act(x)
+    ys_ref, _ = o.chain(layers, q0, s0)
+    dl = [dev_weights(ly) for ly in layers]
+    ys = D.scaffold_lora_chain(dl, dev(q0), dev(s0))
+    torch.cuda.synchronize()
+    for l, (yg, yr) in enumerate(zip(ys, ys_ref)):
+        yg = host(yg)
+        scale = float(np.abs(yr).max())
+        assert float(np.abs(yg - yr).max()) <= Y_TOL * scale, f"linear {l}"
+        bad = np.flatnonzero(yg.view(np.uint32) != yr.view(np.uint32))
+        assert bad.size == 0, f"linear {l}: {bad.size} values differ"
+
+
+def test_chain_small(env):
+    say("chain small")
+    _check_chain(env, [(64, 96), (96, 64), (64, 160), (128, 64), (64, 32)], r=5, M=1, key=0)
+
+
+@pytest.mark.parametrize("M", [2, 4])
+def test_chain_multi_token(env, M):
+    say(f"chain M={M}")
+    _check_chain(env, [(256, 512), (512, 256), (256, 300)], r=16, M=M, key=M)
+
+
+def test_chain_decode_sweep_full(env):
+    """The full Mamba-2-1.3B decode sweep: 48 x (in_proj, out_proj), r = 64."""
+    say("chain full 1.3B sweep")
+    _check_chain(env, S.sweep_shapes(48), r=64, M=1, key=99)

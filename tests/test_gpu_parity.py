@@ -1,0 +1,197 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle on
+the same seeded inputs.  Integers (Q, acc_s, acc_a, acc_b) must match
+bit-exactly; y must be within 1e-3 * max|y| of the fp64 oracle and is also
+checked bit-exact against the oracle's fp32 evaluation in the same order."""
+import numpy as np
+import pytest
+
+import dfssm_synth as S
+import oracle
+from gpu_util import assert_y, dev, dev_weights, host, say, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def env():
+    torch = torch_cuda()
+    import paper_2606_10932_amd as D
+    oracle.build()
+    return torch, D, oracle.get()
+
+
+# ---------------------------------------------------------------- quantiser
+QSHAPES = [(1, 768, 768), (1, 2048, 2048), (3, 4096, 4096), (5, 32, 32), (2, 96, 96),
+           (4, 64, 72), (2, 128, 131), (64, 2048, 2048)]
+
+
+@pytest.mark.parametrize("dtype", ["f16", "f32"])
+@pytest.mark.parametrize("M,K,ldx", QSHAPES)
+def test_quantize(env, dtype, M, K, ldx):
+    torch, D, o = env
+    say(f"quantize {dtype} M={M} K={K} ldx={ldx}")
+    x = S.activations(M, ldx, key=(10, M, K, ldx))
+    x = x if dtype == "f16" else (x.astype(np.float32) * np.float32(3.7))
+    if M > 2:
+        x[1, :] = 0  # an all-zero row
+    qr, sr = o.quantize_act(x, K=K)
+    xd = dev(x)
+    q, s = D.quantize_act(xd[:, :K] if ldx != K else xd, K=K)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(q), qr)
+    assert np.array_equal(host(s).view(np.uint32), sr.view(np.uint32))
+
+
+def test_quantize_ties_and_subnormals(env):
+    torch, D, o = env
+    say("quantize ties/subnormals")
+    x = np.zeros((3, 32), np.float32)
+    x[0, :8] = [0.5, 1.5, 2.5, -0.5, -2.5, 126.5, -126.5, 127.0]
+    x[1, :2] = [1.375, 0.6875]
+    x[2, 3] = 1e-40
+    qr, sr = o.quantize_act(x)
+    q, s = D.quantize_act(dev(x))
+    torch.cuda.synchronize()
+    assert np.array_equal(host(q), qr) and np.array_equal(host(s), sr)
+
+
+# ---------------------------------------------------------------- the linear
+LSHAPES = [
+    # (M, K, N, r)  -- several tiles, ragged tails, both families
+    (1, 768, 3352, 16),      # Mamba-2-130M in_proj
+    (1, 2048, 8512, 64),     # Mamba-2-1.3B in_proj
+    (1, 4096, 2048, 64),     # Mamba-2-1.3B out_proj
+    (2, 4096, 2048, 64),
+    (3, 2048, 333, 64),
+    (4, 4096, 2048, 64),
+    (5, 160, 77, 5),         # K % 128 != 0, r % 4 != 0
+    (1, 32, 1, 0),
+    (3, 96, 33, 1),
+    (2, 256, 31, 256),
+    (7, 8192, 130, 64),
+    (1, 12288, 70, 32),      # two chunks per lane
+    (2, 20480, 40, 8),       # planes streamed from memory
+    (33, 128, 130, 64),
+    (130, 2048, 300, 64),
+    (16, 4096, 2048, 64),
+]
+
+
+def _run_linear(env, M, K, N, r, path, beta_scale=1.0, key=0):
+    torch, D, o = env
+    ws = S.weights(K, N, r, key=(11, M, K, N, r, key), beta_scale=beta_scale)
+    x = S.activations(M, K, key=(11, M, K, key))
+    q, s = o.quantize_act(x)
+    ref = o.linear(q, s, **ws)
+    d = dev_weights(ws)
+    y, acc_s, acc_a, acc_b = D.scaffold_lora_linear(dev(q), dev(s), d["w_bits"], d["alpha"], d["A"], d["B"],
+                                                    d["beta"], path=path, acc=True)
+    torch.cuda.synchronize()
+    return ref, host(y), host(acc_s), host(acc_a), host(acc_b)
+
+
+@pytest.mark.parametrize("path", ["decode", "mfma"])
+@pytest.mark.parametrize("M,K,N,r", LSHAPES)
+def test_linear(env, path, M, K, N, r):
+    torch, D, o = env
+    say(f"linear path={path} M={M} K={K} N={N} r={r}")
+    p = D.PATH_DECODE if path == "decode" else D.PATH_MFMA
+    ref, y, acc_s, acc_a, acc_b = _run_linear(env, M, K, N, r, p)
+    assert np.array_equal(acc_s, ref["acc_s"]), "acc_s"
+    if r:
+        assert np.array_equal(acc_a, ref["acc_a"]), "acc_a"
+    assert np.array_equal(acc_b, ref["acc_b"]), "acc_b"
+    assert_y(y, ref, what=f"{path} {M}x{K}x{N} r{r}")
+
+
+@pytest.mark.parametrize("M", [1, 4, 8, 16, 32])
+def test_out_proj_small_batch_auto(env, M):
+    """Mamba-2-1.3B out_proj at the small-batch decode sizes, automatic path."""
+    say(f"out_proj auto M={M}")
+    ref, y, acc_s, acc_a, acc_b = _run_linear(env, M, 4096, 2048, 64, 0, key=M)
+    assert np.array_equal(acc_s, ref["acc_s"]) and np.array_equal(acc_b, ref["acc_b"])
+    assert_y(y, ref, what=f"out_proj M={M}")
+
+
+@pytest.mark.parametrize("path", ["decode", "mfma"])
+def test_realistic_lora_ratio(env, path):
+    """beta scaled so the LoRA term is ~1.5% of the scaffold term (the trained
+    model's ratio) -- y then depends visibly on the scaffold product."""
+    torch, D, o = env
+    say(f"realistic ratio {path}")
+    p = D.PATH_DECODE if path == "decode" else D.PATH_MFMA
+    ref, y, acc_s, _, acc_b = _run_linear(env, 2, 2048, 8512, 64, p, beta_scale=1.8e-5)
+    assert np.array_equal(acc_s, ref["acc_s"]) and np.array_equal(acc_b, ref["acc_b"])
+    assert_y(y, ref, what="realistic ratio")
+
+
+def test_prefill_full_size_sampled(env):
+    """Mamba-2-1.3B in_proj at 2048 tokens (the launch the benchmark times):
+    every acc_s/acc_b/y of a sample of token rows against the oracle run on
+    those rows (rows are independent)."""
+    torch, D, o = env
+    M, K, N, r = 2048, 2048, 8512, 64
+    say(f"prefill {M}x{K}x{N} r{r}")
+    ws = S.config_weights(4)
+    x = S.config_activations(4, M)
+    q, s = o.quantize_act(x)
+    d = dev_weights(ws)
+    qd, sd = D.quantize_act(dev(x))
+    y, acc_s, acc_a, acc_b = D.scaffold_lora_linear(qd, sd, d["w_bits"], d["alpha"], d["A"], d["B"], d["beta"],
+                                                    acc=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(qd), q) and np.array_equal(host(sd), s)
+    rows = np.unique(np.concatenate([[0, 1, 127, 128, M - 1], np.random.default_rng(0).choice(M, 27, replace=False)]))
+    ref = o.linear(q[rows], s[rows], **ws)
+    assert np.array_equal(host(acc_s)[rows], ref["acc_s"])
+    assert np.array_equal(host(acc_a)[rows], ref["acc_a"])
+    assert np.array_equal(host(acc_b)[rows], ref["acc_b"])
+    assert_y(host(y)[rows], ref, what="prefill sample")
+    # every row: acc_s parity with the popcount identity's range bound
+    assert np.abs(host(acc_s)).max() <= 127 * K
+
+
+def test_edge_cases(env):
+    torch, D, o = env
+    say("edge cases")
+    K, N, r = 256, 40, 8
+    ws = S.weights(K, N, r, key=(12,))
+    d = dev_weights(ws)
+    # M = 0 and N = 0 are no-ops
+    q0 = torch.empty((0, K), dtype=torch.int8, device="cuda")
+    s0 = torch.empty((0,), dtype=torch.float32, device="cuda")
+    y = D.scaffold_lora_linear(q0, s0, d["w_bits"], d["alpha"], d["A"], d["B"], d["beta"])
+    assert y.shape == (0, N)
+    # all-zero activations -> y = 0; A = 0 -> scaffold only
+    for path in (D.PATH_DECODE, D.PATH_MFMA):
+        x = np.zeros((3, K), np.float32)
+        x[1] = S.activations(1, K, key=(12, 1))[0]
+        q, s = o.quantize_act(x)
+        Az = np.zeros_like(ws["A"])
+        ref = o.linear(q, s, ws["w_bits"], ws["alpha"], Az, ws["B"], ws["beta"])
+        y, acc_s, acc_a, acc_b = D.scaffold_lora_linear(dev(q), dev(s), d["w_bits"], d["alpha"], dev(Az),
+                                                        d["B"], d["beta"], path=path, acc=True)
+        torch.cuda.synchronize()
+        assert not host(y)[0].any() and not host(y)[2].any()
+        assert np.array_equal(host(acc_s), ref["acc_s"]) and not host(acc_b).any()
+        assert_y(host(y), ref, what="A=0")
+
+
+def test_deterministic_and_streams(env):
+    """Bitwise identical repeats, on the default stream and on a side stream
+    ordered by events."""
+    torch, D, o = env
+    say("determinism")
+    ws = S.config_weights(1)
+    d = dev_weights(ws)
+    q, s = D.quantize_act(dev(S.config_activations(1, 1)))
+    y1 = D.scaffold_lora_linear(q, s, d["w_bits"], d["alpha"], d["A"], d["B"], d["beta"])
+    side = torch.cuda.Stream()
+    ev = torch.cuda.Event()
+    ev.record()
+    with torch.cuda.stream(side):
+        side.wait_event(ev)
+        y2 = D.scaffold_lora_linear(q, s, d["w_bits"], d["alpha"], d["A"], d["B"], d["beta"])
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)

@@ -1,0 +1,129 @@
+"""Host-side checks of the HIP library (no GPU needed): it loads, exports
+every function include/dfssm.h declares, and rejects invalid arguments on the
+host before any HIP call.  Also checks the product/oracle separation."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dfssm.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dfssm_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def dl():
+    import paper_2606_10932_amd as D
+    return D
+
+
+def test_exports_every_declared_function(dl):
+    names = header_functions()
+    assert len(names) >= 9
+    for n in names:
+        assert hasattr(dl.lib, n), n          # dlsym succeeds
+    assert set(names) == set(dl.EXPORTS)
+
+
+def test_version_and_status_strings(dl):
+    assert dl.lib.dfssm_version().decode().startswith("dfssm")
+    for st in range(7):
+        assert dl.lib.dfssm_status_string(st).decode() not in ("", "unknown status")
+    assert dl.lib.dfssm_status_string(99).decode() == "unknown status"
+
+
+def _lin(dl, M=1, K=64, N=8, r=4, q=16, s=16, w=16, al=16, A=16, B=16, be=16, y=16, ws=16,
+         wsb=1 << 20, path=0):
+    return dl.lib.dfssm_scaffold_lora_linear_ex(q, s, M, K, N, r, w, al, A, B, be, y, path, None, None,
+                                                None, ws, wsb, None)
+
+
+def test_linear_validation(dl):
+    # fake, aligned, non-null "device" pointers: every call below must be
+    # rejected on the host before anything touches a device
+    assert _lin(dl, K=48) == dl.ERR_SHAPE
+    assert _lin(dl, K=0) == dl.ERR_SHAPE
+    assert _lin(dl, K=65536 + 32) == dl.ERR_SHAPE
+    assert _lin(dl, M=-1) == dl.ERR_SHAPE
+    assert _lin(dl, N=-1) == dl.ERR_SHAPE
+    assert _lin(dl, r=257) == dl.ERR_SHAPE
+    assert _lin(dl, r=-1) == dl.ERR_SHAPE
+    assert _lin(dl, path=7) == dl.ERR_SHAPE
+    assert _lin(dl, q=None) == dl.ERR_NULL
+    assert _lin(dl, w=None) == dl.ERR_NULL
+    assert _lin(dl, ws=None) == dl.ERR_NULL
+    assert _lin(dl, A=None) == dl.ERR_NULL           # r > 0 needs A, B, beta
+    assert _lin(dl, be=None) == dl.ERR_NULL
+    assert _lin(dl, q=17) == dl.ERR_ALIGN
+    assert _lin(dl, y=20) == dl.ERR_ALIGN
+    assert _lin(dl, wsb=10) == dl.ERR_WORKSPACE
+    assert "workspace" in dl.last_error()
+    # empty problems are accepted as no-ops
+    assert _lin(dl, M=0, q=None, s=None) == dl.OK
+    assert _lin(dl, N=0, w=None) == dl.OK
+    # the plain entry point needs y
+    assert dl.lib.dfssm_scaffold_lora_linear(16, 16, 1, 64, 8, 0, 16, 16, None, None, None, None, 16,
+                                              1 << 20, None) == dl.ERR_NULL
+
+
+def test_quantize_validation(dl):
+    f = dl.lib.dfssm_quantize_act
+    assert f(16, 2, 1, 64, 64, 16, 16, None) == dl.ERR_SHAPE      # dtype
+    assert f(16, dl.F16, 1, 48, 64, 16, 16, None) == dl.ERR_SHAPE
+    assert f(16, dl.F16, 1, 64, 32, 16, 16, None) == dl.ERR_SHAPE  # ldx < K
+    assert f(None, dl.F16, 1, 64, 64, 16, 16, None) == dl.ERR_NULL
+    assert f(17, dl.F16, 1, 64, 64, 16, 16, None) == dl.ERR_ALIGN  # fp16 needs 2-byte alignment
+    assert f(18, dl.F32, 1, 64, 64, 16, 16, None) == dl.ERR_ALIGN
+    assert f(16, dl.F16, 1, 64, 64, 24, 16, None) == dl.ERR_ALIGN
+    assert f(None, dl.F16, 0, 64, 64, None, None, None) == dl.OK   # M = 0
+
+
+def test_chain_validation(dl):
+    L = dl.Layer
+    good = dict(w_bits=16, alpha=16, A=16, B=16, beta=16, K=64, N=96, r=4)
+    arr = (L * 2)(L(**good), L(**dict(good, K=128)))              # K_1 = 128 > N_0 = 96
+    f = dl.lib.dfssm_scaffold_lora_chain
+    assert f(arr, 2, 1, 16, 16, 16, 16, 1 << 30, None) == dl.ERR_SHAPE
+    arr = (L * 2)(L(**good), L(**dict(good, K=64)))
+    assert f(arr, 2, 5, 16, 16, 16, 16, 1 << 30, None) == dl.ERR_UNSUPPORTED   # M > 4
+    assert f(arr, 2, 1, 16, 16, 16, 16, 8, None) == dl.ERR_WORKSPACE
+    assert f(arr, 2, 1, None, 16, 16, 16, 1 << 30, None) == dl.ERR_NULL
+    arr = (L * 1)(L(**dict(good, A=None)))
+    assert f(arr, 1, 1, 16, 16, 16, 16, 1 << 30, None) == dl.ERR_NULL
+    assert "layer 0" in dl.last_error()
+    assert f(arr, 0, 1, None, None, None, None, 0, None) == dl.OK
+    assert dl.lib.dfssm_chain_workspace_bytes(arr, 1, 1) > 0
+
+
+def test_workspace_sizes(dl):
+    a = dl.linear_workspace_bytes(1, 2048, 8512, 64)
+    b = dl.linear_workspace_bytes(2048, 2048, 8512, 64)
+    assert 0 < a < b
+    assert dl.linear_workspace_bytes(1, 2048, 8512, 0) > 0
+
+
+def _imports(path):
+    out = []
+    for dirpath, _, files in os.walk(path):
+        for f in files:
+            if f.endswith((".py", ".hip", ".cpp", ".hpp", ".h", ".c")):
+                out.append((os.path.join(dirpath, f), open(os.path.join(dirpath, f)).read()))
+    return out
+
+
+def test_product_and_oracle_are_separate():
+    for p, text in _imports(os.path.join(ROOT, "paper_2606_10932_amd")):
+        assert not re.search(r"^\s*(from|import)\s+oracle\b", text, re.M), p
+        assert "dfssm_ref" not in text, p
+    for p, text in _imports(os.path.join(ROOT, "oracle")):
+        assert "paper_2606_10932_amd" not in text, p
+        assert not re.search(r'#\s*include\s*[<"](dfssm\.h|dfssm_internal)', text), p
+    for p, text in _imports(os.path.join(ROOT, "dfssm_synth")):
+        assert "oracle" not in text.replace("imports neither the oracle", ""), p
+        assert "paper_2606_10932_amd" not in text, p
