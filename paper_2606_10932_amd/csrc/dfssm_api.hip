@@ -7,6 +7,8 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
+#include <vector>
 
 #include "dfssm_internal.hpp"
 
@@ -55,6 +57,16 @@ dfssm_status check_ptrs(std::initializer_list<Ptr> required, std::initializer_li
   for (const Ptr& x : optional)
     if (x.p && !aligned16(x.p)) return fail(DFSSM_ERR_ALIGN, "%s is not 16-byte aligned", x.name);
   return DFSSM_OK;
+}
+
+// Per-launch tag of the persistent chain's exchange words (24 bits, never 0).
+uint32_t next_chain_seq() {
+  static std::atomic<uint32_t> seq{0};
+  uint32_t s;
+  do {
+    s = (seq.fetch_add(1, std::memory_order_relaxed) + 1) & 0xffffffu;
+  } while (s == 0);
+  return s;
 }
 
 size_t linear_ws_bytes(int64_t M, int64_t K, int64_t r) {
@@ -155,28 +167,51 @@ dfssm_status dfssm_scaffold_lora_linear(const int8_t* q, const float* s, int64_t
 }
 
 // ---------------------------------------------------------------- chain
-// Workspace: Q [M, Kmax] int8, s [M] fp32, then one linear workspace sized
-// for the largest layer.
-static size_t chain_ws_parts(const dfssm_layer* layers, int n_layers, int64_t M, size_t* off_s,
-                             size_t* off_lin) {
-  int64_t kmax = 0, rmax = 0;
+// Workspace of the host-sequenced chain: Q [M, Kmax] int8, s [M] fp32, one
+// linear workspace sized for the largest layer.  Workspace of the persistent
+// chain (M = 1): layer table, then the exchange region y_ll (one 64-bit word
+// per output of every linear), acc_ll (n_layers x acc_stride words), done_ll
+// (n_layers x workgroups words) and one status word.  The larger of the two is required.
+struct ChainLayout {
+  size_t off_s, off_lin, seq_bytes;
+  size_t off_table, off_yll, off_acc, off_done, off_status, pers_bytes;
+  int64_t y_words;
+};
+
+static ChainLayout chain_layout(const dfssm_layer* layers, int n_layers, int64_t M) {
+  ChainLayout c{};
+  int64_t kmax = 0, rmax = 0, ysum = 0;
   for (int l = 0; l < n_layers; ++l) {
     kmax = std::max(kmax, layers[l].K);
     rmax = std::max(rmax, layers[l].r);
+    ysum += layers[l].N;
   }
   size_t o = (size_t)dfssm::round_up(M * kmax, 256);
-  *off_s = o;
+  c.off_s = o;
   o += (size_t)dfssm::round_up(M * 4, 256);
-  *off_lin = o;
+  c.off_lin = o;
   size_t lin = 0;
   for (int l = 0; l < n_layers; ++l) lin = std::max(lin, linear_ws_bytes(M, layers[l].K, layers[l].r));
-  return o + lin;
+  c.seq_bytes = o + lin;
+  c.off_table = 0;
+  o = (size_t)dfssm::round_up((int64_t)(n_layers * sizeof(dfssm::ChainLayerDev)), 256);
+  c.off_yll = o;
+  c.y_words = ysum * M;
+  o += (size_t)c.y_words * 8;
+  c.off_acc = o;
+  o += (size_t)n_layers * dfssm::kMaxRank * dfssm::kChainPad * 8;
+  c.off_done = o;
+  o += (size_t)n_layers * dfssm::chain_grid() * dfssm::kChainPad * 8;
+  c.off_status = o;
+  o += 256;
+  c.pers_bytes = o;
+  return c;
 }
 
 size_t dfssm_chain_workspace_bytes(const dfssm_layer* layers, int n_layers, int64_t M) {
   if (!layers || n_layers <= 0 || M <= 0) return 0;
-  size_t a, b;
-  return chain_ws_parts(layers, n_layers, M, &a, &b);
+  ChainLayout c = chain_layout(layers, n_layers, M);
+  return std::max(c.seq_bytes, c.pers_bytes);
 }
 
 dfssm_status dfssm_scaffold_lora_chain(const dfssm_layer* layers, int n_layers, int64_t M,
@@ -208,15 +243,48 @@ dfssm_status dfssm_scaffold_lora_chain(const dfssm_layer* layers, int n_layers, 
   }
   dfssm_status st = check_ptrs({{q0, "q0"}, {s0, "s0"}, {y_all, "y_all"}, {workspace, "workspace"}}, {});
   if (st != DFSSM_OK) return st;
-  size_t off_s, off_lin;
-  const size_t need = chain_ws_parts(layers, n_layers, M, &off_s, &off_lin);
+  const ChainLayout c = chain_layout(layers, n_layers, M);
+  const size_t need = std::max(c.seq_bytes, c.pers_bytes);
   if (workspace_bytes < need)
     return fail(DFSSM_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, need);
 
   hipStream_t hs = (hipStream_t)stream;
   char* base = static_cast<char*>(workspace);
+
+  if (dfssm::chain_persistent_supported(layers, n_layers, M, dfssm::chain_grid())) {
+    // the layer table travels by value in the setup kernels' arguments
+    static thread_local std::vector<dfssm::ChainLayerDev> table;
+    table.resize(n_layers);
+    int64_t off = 0;
+    for (int l = 0; l < n_layers; ++l) {
+      const dfssm_layer& L = layers[l];
+      // rank 0: the kernel reads through A/B/beta unconditionally (and masks
+      // the values), so give it a valid address
+      const bool lr = L.r > 0;
+      table[l] = dfssm::ChainLayerDev{L.w_bits,
+                                      L.alpha,
+                                      lr ? L.A : reinterpret_cast<const int8_t*>(L.alpha),
+                                      lr ? L.B : reinterpret_cast<const int8_t*>(L.alpha),
+                                      lr ? L.beta : L.alpha,
+                                      (int32_t)L.K,
+                                      (int32_t)L.N,
+                                      (int32_t)L.r,
+                                      dfssm::chain_lanes_per_row(L.K),
+                                      off};
+      off += L.N;
+    }
+    auto* tdev = reinterpret_cast<dfssm::ChainLayerDev*>(base + c.off_table);
+    auto* exch = reinterpret_cast<uint64_t*>(base + c.off_yll);
+    const int64_t exch_words = (int64_t)(c.off_status + 8 - c.off_yll) / 8;
+    hipError_t e = dfssm::launch_chain_persistent(
+        table.data(), tdev, n_layers, q0, s0, exch, exch_words, exch,
+        reinterpret_cast<uint64_t*>(base + c.off_acc), reinterpret_cast<uint64_t*>(base + c.off_done), y_all,
+        reinterpret_cast<unsigned*>(base + c.off_status), next_chain_seq(), hs);
+    return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain persistent launch");
+  }
+
   int8_t* qbuf = reinterpret_cast<int8_t*>(base);
-  float* sbuf = reinterpret_cast<float*>(base + off_s);
+  float* sbuf = reinterpret_cast<float*>(base + c.off_s);
   float* y_prev = nullptr;
   float* y_cur = y_all;
   for (int l = 0; l < n_layers; ++l) {
@@ -229,7 +297,7 @@ dfssm_status dfssm_scaffold_lora_chain(const dfssm_layer* layers, int n_layers, 
       ql = qbuf;
       sl = sbuf;
     }
-    dfssm::LinearWorkspace ws = dfssm::carve_linear_workspace(base + off_lin, M, L.K, L.r);
+    dfssm::LinearWorkspace ws = dfssm::carve_linear_workspace(base + c.off_lin, M, L.K, L.r);
     hipError_t e = dfssm::launch_decode_linear(ql, sl, M, L.K, L.N, L.r, L.w_bits, L.alpha, L.A, L.B,
                                                L.beta, y_cur, nullptr, nullptr, nullptr, ws, hs);
     if (e != hipSuccess) return device_fail(e, "chain linear launch");

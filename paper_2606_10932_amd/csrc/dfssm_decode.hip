@@ -275,20 +275,20 @@ __global__ __launch_bounds__(kThreads) void decode_gemv(
 
     // epilogue: lane g handles token g
     if (row_ok && g < mt) {
-      int32_t as = part[0];
-      int64_t ab = (int64_t)elo[0] + ((int64_t)ehi[0] << 16);
+      int32_t as = part[0], hi = ehi[0], lo = elo[0];
 #pragma unroll
       for (int m = 1; m < MT; ++m)
         if (g == m) {
           as = part[m];
-          ab = (int64_t)elo[m] + ((int64_t)ehi[m] << 16);
+          hi = ehi[m];
+          lo = elo[m];
         }
       const int mm = m0 + g;
       if (y)
         y[(int64_t)mm * N_out + n] =
-            dfssm_dev::epilogue(s[mm], alpha[n], r > 0 ? beta[n] : 0.0f, as, ab, r > 0);
+            dfssm_dev::epilogue(s[mm], alpha[n], r > 0 ? beta[n] : 0.0f, as, hi, lo, r > 0);
       if (acc_s_out) acc_s_out[(int64_t)mm * N_out + n] = as;
-      if (acc_b_out) acc_b_out[(int64_t)mm * N_out + n] = r > 0 ? ab : 0;
+      if (acc_b_out) acc_b_out[(int64_t)mm * N_out + n] = r > 0 ? (int64_t)lo + ((int64_t)hi << 16) : 0;
     }
   }
 }

@@ -87,6 +87,42 @@ hipError_t launch_mfma_linear(const int8_t* q, const float* s, int64_t M, int64_
                               int32_t* acc_s, int32_t* acc_a_out, int64_t* acc_b,
                               const LinearWorkspace& ws, hipStream_t st);
 
+// ---------------------------------------------------------------- chain
+// Largest K the persistent chain kernel takes (its per-thread register
+// staging of the previous output holds K/256 values).
+constexpr int kChainMaxK = 4096;
+// Row steps of one workgroup per linear held in registers, and waves per
+// role group of the persistent kernel.
+constexpr int kChainMaxSteps = 2;
+constexpr int kChainWaves = 8;
+// Layer-table entries passed by value per setup launch.
+constexpr int kChainSetupChunk = 48;
+// 64-bit words per padded exchange slot (one 128-byte line).
+constexpr int kChainPad = 16;
+
+// One linear of the persistent chain, as the kernel reads it (device table).
+struct ChainLayerDev {
+  const uint32_t* w_bits;
+  const float* alpha;
+  const int8_t* A;
+  const int8_t* B;
+  const float* beta;
+  int32_t K, N, r, G;  // G: lanes per output row (power of two, 8..64)
+  int64_t y_off;       // offset of this linear's outputs in y_all
+};
+
+int chain_lanes_per_row(int64_t K);
+int chain_grid();
+bool chain_persistent_supported(const dfssm_layer* layers, int n_layers, int64_t M, int nwg);
+// Copies the layer table to table_dev and zeroes the exchange region
+// [exch, exch + exch_words) (y_ll, acc_ll, done_ll and the status word) with
+// small setup kernels, then launches the cooperative persistent kernel.
+hipError_t launch_chain_persistent(const ChainLayerDev* table_host, ChainLayerDev* table_dev,
+                                   int n_layers, const int8_t* q0, const float* s0,
+                                   uint64_t* exch, int64_t exch_words, uint64_t* y_ll,
+                                   uint64_t* acc_ll, uint64_t* done_ll, float* y_all,
+                                   unsigned* status, uint32_t seq, hipStream_t st);
+
 }  // namespace dfssm
 
 // ------------------------------------------------------------ device helpers
@@ -104,15 +140,19 @@ __device__ __forceinline__ void split_limbs(int32_t v, int8_t d[4]) {
   d[3] = (int8_t)v;
 }
 
-// The fixed-order fp32 output scaling y = s*(alpha*fs + beta*fb); the
-// library is compiled with -ffp-contract=off so no multiply-add fuses.
+// The fixed-order fp32 output scaling y = s*(alpha*fs + beta*fb) with
+// acc_b = hi*2^16 + lo.  fb is the int64 acc_b rounded once to fp32: the
+// fp64 sum hi*65536 + lo is exact (|acc_b| < 2^53), so converting it to fp32
+// is the single round-to-nearest-even of the integer.  The library is
+// compiled with -ffp-contract=off, so no multiply-add fuses.
 __device__ __forceinline__ float epilogue(float s, float alpha, float beta, int32_t acc_s,
-                                          int64_t acc_b, bool lora) {
+                                          int32_t hi, int32_t lo, bool lora) {
   float fs = (float)acc_s;
   float u = alpha * fs;
   float w = u;
   if (lora) {
-    float fb = (float)acc_b;
+    double db = (double)hi * 65536.0 + (double)lo;
+    float fb = (float)db;
     float v = beta * fb;
     w = u + v;
   }

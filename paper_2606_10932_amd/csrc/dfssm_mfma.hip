@@ -251,10 +251,10 @@ __global__ __launch_bounds__(kThreads) void mfma_scaffold(
         const int m = wm0 + 16 * i + 4 * kg + v;
         if (m >= M) continue;
         const int32_t as = acc[i][t][v];
-        const int64_t ab = (int64_t)elo[i][t][v] + ((int64_t)ehi[i][t][v] << 16);
-        if (y) y[(int64_t)m * N + n] = dfssm_dev::epilogue(s[m], al, be, as, ab, r > 0);
+        const int32_t hi = ehi[i][t][v], lo = elo[i][t][v];
+        if (y) y[(int64_t)m * N + n] = dfssm_dev::epilogue(s[m], al, be, as, hi, lo, r > 0);
         if (acc_s_out) acc_s_out[(int64_t)m * N + n] = as;
-        if (acc_b_out) acc_b_out[(int64_t)m * N + n] = r > 0 ? ab : 0;
+        if (acc_b_out) acc_b_out[(int64_t)m * N + n] = r > 0 ? (int64_t)lo + ((int64_t)hi << 16) : 0;
       }
   }
 }

@@ -52,3 +52,33 @@ def test_chain_decode_sweep_full(env):
     """The full Mamba-2-1.3B decode sweep: 48 x (in_proj, out_proj), r = 64."""
     say("chain full 1.3B sweep")
     _check_chain(env, S.sweep_shapes(48), r=64, M=1, key=99)
+
+
+PERSISTENT_SHAPES = {
+    0: [(128, 256), (256, 4000), (3968, 2048), (2048, 16384), (4096, 130)],
+    8: [(128, 256), (256, 4000), (3968, 2048), (2048, 16384), (4096, 130)],
+    64: [(2048, 4000), (3968, 2048), (2048, 16384), (4096, 130), (128, 64)][:4],
+}
+
+
+def _lanes_per_row(K):
+    G = 8
+    while G < K // 128 and G < 64:
+        G *= 2
+    return G
+
+
+@pytest.mark.parametrize("r", [0, 8, 64])
+def test_chain_persistent_shapes(env, r):
+    """Shapes inside the persistent kernel's limits (K % 128 == 0, K <= 4096,
+    r % 4 == 0, r <= 4 lanes-per-row, at most 2 row steps of 8 waves per
+    workgroup): ragged N, rank 0, and a linear that needs both row steps
+    (N = 16384 at K = 2048)."""
+    shapes = PERSISTENT_SHAPES[r]
+    for K, N in shapes:
+        G = _lanes_per_row(K)
+        assert K % 128 == 0 and K <= 4096 and r % 4 == 0 and r // 4 <= G
+        rows_per_wg = -(-N // 256)
+        assert -(-rows_per_wg // (8 * (64 // G))) <= 2
+    say(f"chain persistent r={r}")
+    _check_chain(env, shapes, r=r, M=1, key=100 + r)
