@@ -2,20 +2,24 @@
 
 Headline workload (one "step"): the Mamba-2-1.3B decode sweep at one token --
 48 layers x (in_proj 2048->8512, out_proj 4096->2048), rank-64 int8 LoRA,
-every output re-quantised as the next input (dfssm_scaffold_lora_chain).
+every output re-quantised as the next input.  One step is one
+dfssm_chain_run, i.e. one launch of the persistent chain kernel, on a
+workspace prepared once per weight set (dfssm_chain_prepare, untimed).
 Metric: effective packed-weight GB/s (sign words + LoRA factors + row scales
 read per step / step time) and us per layer; the 2048-token prefill in_proj
 is measured beside it in int8 TOPS.
 
 Weights are synthetic and seeded (no trained weights exist here).  The sweep
 reads 210 MB per step, which fits the 256 MB Infinity Cache, so steps rotate
-over several distinct weight copies to keep the measurement cold.
+over several distinct weight copies (630 MB for 3) to keep the measurement
+cold.
 
 Prints one JSON line.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -28,18 +32,47 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 PEAK_I8_TOPS = 5000.0        # MI355X dense int8 MFMA
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "chain_persistent_1p3b_sweep_traffic.txt")
+CHAIN_SOURCES = ["paper_2606_10932_amd/csrc/dfssm_chain.hip", "paper_2606_10932_amd/csrc/dfssm_internal.hpp"]
 
 
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--copies", type=int, default=3, help="distinct weight copies rotated per step")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--no-prefill", action="store_true")
-    p.add_argument("--cpu-sample-linears", type=int, default=16)
+    p.add_argument("--cpu-seconds", type=float, default=12.0, help="minimum CPU oracle sample time")
+    p.add_argument("--copy-calibration-mib", type=int, default=0,
+                   help="run one plain device copy of this size first (for HBM counter scaling)")
     return p.parse_args()
+
+
+def chain_source_digest() -> str:
+    h = hashlib.sha256()
+    for rel in CHAIN_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per chain launch from the committed counter summary, or None
+    when it is missing or was taken on other kernel sources."""
+    try:
+        kv = {}
+        with open(TRAFFIC_FILE) as f:
+            for line in f:
+                if ":" in line and not line.startswith("#"):
+                    k, v = line.split(":", 1)
+                    kv[k.strip()] = v.strip()
+        if kv.get("chain_source_sha256") != chain_source_digest():
+            return None
+        return int(float(kv["hbm_bytes_per_launch"]))
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def main():
@@ -61,49 +94,74 @@ def main():
         a = a.view(np.int32) if a.dtype == np.uint32 else a
         return torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
 
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib << 20
+        a = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
     # ---- the decode sweep: copies of 96 seeded weight sets -----------------
     shapes = S.sweep_shapes(48)
-    copies, arrays, host0 = [], [], None
+    M = 1
+    copies, arrays, workspaces, host0 = [], [], [], None
     for c in range(args.copies):
         hs = S.sweep_weights(48, r=64, variant=c)
         if c == 0:
             host0 = hs
         dl = [{k: dev(v) for k, v in ly.items()} for ly in hs]
+        arr = D.make_layers(dl)
+        ws = torch.empty(D.chain_workspace_bytes(arr, M), dtype=torch.uint8, device="cuda")
+        D.chain_prepare(arr, M, ws)
         copies.append(dl)
-        arrays.append(D.make_layers(dl))
+        arrays.append(arr)
+        workspaces.append(ws)
         if c:
             del hs
     weight_bytes = sum(S.weight_bytes(ly) for ly in host0)
     x = S.sweep_input(1)
     q0, s0 = D.quantize_act(dev(x))
-    M = 1
-    ws_bytes = D.chain_workspace_bytes(arrays[0], M)
-    workspace = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
     y_all = torch.empty(sum(N for _, N in shapes), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
 
     def step(i):
         c = i % len(copies)
-        D.scaffold_lora_chain(copies[c], q0, s0, y_all=y_all, workspace=workspace, layer_arr=arrays[c])
+        D.chain_run(arrays[c], q0, s0, y_all, workspaces[c], stream=stream)
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for i in range(args.steps):
-        step(i)
-    e1.record()
+    # timed region: K launches back to back; an event pair around each launch
+    # (on the launch stream) gives the kernel's own duration
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
+    t0.record(stream)
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        step(i)
+        ev[i][1].record(stream)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / args.steps
+    launch_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    status = max(D.chain_status(arrays[c], M, workspaces[c]) for c in range(len(copies)))
+    if status:
+        print(f"chain status word {status:#x}: a bounded wait gave up", file=sys.stderr)
+        sys.exit(3)
     gbs = weight_bytes / (ms * 1e-3) / 1e9
+    launch_gbs = weight_bytes / (launch_ms * 1e-3) / 1e9
 
     # warm (one copy, cache resident) for context
-    e0.record()
+    t0.record(stream)
     for i in range(args.steps):
         step(0)
-    e1.record()
+    t1.record(stream)
     torch.cuda.synchronize()
-    ms_warm = e0.elapsed_time(e1) / args.steps
+    ms_warm = t0.elapsed_time(t1) / args.steps
 
     # ---- prefill: 2048-token in_proj -----------------------------------------
     prefill = None
@@ -115,20 +173,21 @@ def main():
 
         def pstep():
             D.scaffold_lora_linear(xq, xs, pw["w_bits"], pw["alpha"], pw["A"], pw["B"], pw["beta"], y=yp,
-                                   workspace=wsp)
+                                   workspace=wsp, stream=stream)
         for _ in range(3):
             pstep()
         torch.cuda.synchronize()
-        e0.record()
+        t0.record(stream)
         n = 20
         for _ in range(n):
             pstep()
-        e1.record()
+        t1.record(stream)
         torch.cuda.synchronize()
-        pms = e0.elapsed_time(e1) / n
+        pms = t0.elapsed_time(t1) / n
         ops = 2.0 * 2048 * 2048 * 8512
         lora_ops = 2.0 * 2048 * 64 * (2048 + 8512)
-        prefill = {"workload": "1.3B in_proj prefill M=2048 K=2048 N=8512 r=64", "us": round(pms * 1e3, 2),
+        prefill = {"workload": "1.3B in_proj prefill M=2048 K=2048 N=8512 r=64 (down-projection + scaffold "
+                               "launches)", "us": round(pms * 1e3, 2),
                    "scaffold_tops": round(ops / (pms * 1e-3) / 1e12, 1),
                    "algorithmic_tops": round((ops + lora_ops) / (pms * 1e-3) / 1e12, 1),
                    "frac_i8_peak": round(ops / (pms * 1e-3) / 1e12 / PEAK_I8_TOPS, 4)}
@@ -140,17 +199,20 @@ def main():
         if not os.path.exists(oracle.LIB):
             oracle.build()
         o = oracle.get()
-        nl = max(2, min(args.cpu_sample_linears, len(host0)))
         q0h, s0h = o.quantize_act(x)
-        t = time.perf_counter()
-        o.chain(host0[:nl], q0h, s0h)
-        dt = time.perf_counter() - t
-        sample_bytes = sum(S.weight_bytes(ly) for ly in host0[:nl])
-        cpu = {"value": round(sample_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": o.threads(),
+        reps, t = 0, time.perf_counter()
+        while True:
+            o.chain(host0, q0h, s0h)
+            reps += 1
+            dt = time.perf_counter() - t
+            if dt >= args.cpu_seconds:
+                break
+        cpu = {"value": round(reps * weight_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": o.threads(),
                "kind": "oracle",
-               "sample": f"first {nl} of the 96 chained linears (M=1), {sample_bytes} weight bytes, {dt:.2f} s"}
+               "sample": f"the full 96-linear sweep (weight copy 0, same input) run {reps} times in {dt:.1f} s",
+               "us_per_layer": round(dt / reps / 48 * 1e6, 1)}
 
-    roof_achieved = gbs
+    traffic = measured_traffic()
     out = {
         "metric": "effective packed-weight GB/s (1.3B decode sweep, M=1)",
         "value": round(gbs, 2),
@@ -169,8 +231,10 @@ def main():
                                "r=64 int8 LoRA, M=1, each output re-quantised",
                    "weight_bytes_per_step": weight_bytes, "weight_copies_rotated": len(copies),
                    "warm_ms_per_step": round(ms_warm, 4)},
-        "roofline": {"bound": "hbm", "achieved": round(roof_achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(roof_achieved / PEAK_HBM_GBS, 4), "traffic": None},
+        "roofline": {"bound": "hbm", "kernel": "chain_persistent", "achieved": round(launch_gbs, 2),
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(launch_gbs / PEAK_HBM_GBS, 4),
+                     "traffic": traffic, "avg_launch_us": round(launch_ms * 1e3, 2),
+                     "algorithmic_bytes_per_launch": weight_bytes},
         "prefill": prefill,
         "cpu_baseline": cpu,
     }

@@ -146,11 +146,45 @@ size_t dfssm_chain_workspace_bytes(const dfssm_layer* layers, int n_layers, int6
  * Requires K_l <= N_{l-1}.  y_all (device) receives every linear's y back
  * to back: sum_l M*N_l floats, linear l at offset sum_{i<l} M*N_i.
  * `layers` is a HOST array of n_layers entries.  M must be 1..4.
+ * Equivalent to dfssm_chain_prepare followed by dfssm_chain_run.
  * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */
 dfssm_status dfssm_scaffold_lora_chain(const dfssm_layer* layers, int n_layers, int64_t M,
                                        const int8_t* q0, const float* s0, float* y_all,
                                        void* workspace, size_t workspace_bytes,
                                        void* stream);
+
+/* Prepares `workspace` for dfssm_chain_run with these layers: writes the
+ * persistent kernel's layer table and its 64-bit fingerprint into the
+ * workspace and clears the exchange region and the status word
+ * (stream-ordered, asynchronous).  Needed once per (layers, workspace): a
+ * prepared workspace can be run any number of times, as long as nothing
+ * but dfssm_chain_run writes to it in between.  Chains the persistent
+ * kernel does not take (M > 1, K % 128 != 0, K > 4096, r % 4 != 0, ...)
+ * need no preparation and return DFSSM_OK.
+ * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */
+dfssm_status dfssm_chain_prepare(const dfssm_layer* layers, int n_layers, int64_t M,
+                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* Runs the chain (same contract as dfssm_scaffold_lora_chain) on a
+ * workspace prepared for exactly these layers: at M = 1 one cooperative
+ * kernel launch.  If the workspace's fingerprint does not match these
+ * layers, the kernel leaves before reading the table, writes nothing and
+ * sets status bit 8 (see dfssm_chain_status).
+ * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */
+dfssm_status dfssm_chain_run(const dfssm_layer* layers, int n_layers, int64_t M, const int8_t* q0,
+                             const float* s0, float* y_all, void* workspace,
+                             size_t workspace_bytes, void* stream);
+
+/* Synchronises `stream` and reads the persistent chain's status word into
+ * *status (host): 0 = fine; bit 1 = a wait for a previous output timed out;
+ * bit 2 = a wait for the LoRA down-projection timed out; bit 4 = an output
+ * word never became valid; bit 8 = the workspace was not prepared for these
+ * layers.  Bits accumulate over runs until the next dfssm_chain_prepare.
+ * Always 0 for chains that do not use the persistent kernel.
+ * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */
+dfssm_status dfssm_chain_status(const dfssm_layer* layers, int n_layers, int64_t M,
+                                const void* workspace, size_t workspace_bytes, unsigned* status,
+                                void* stream);
 
 /* Static text for a status code. */
 const char* dfssm_status_string(int status);

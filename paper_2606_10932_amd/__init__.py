@@ -21,7 +21,8 @@ PATH_AUTO, PATH_DECODE, PATH_MFMA = 0, 1, 2
 
 EXPORTS = ["dfssm_quantize_act", "dfssm_linear_workspace_bytes", "dfssm_scaffold_lora_linear",
            "dfssm_scaffold_lora_linear_ex", "dfssm_chain_workspace_bytes",
-           "dfssm_scaffold_lora_chain", "dfssm_status_string", "dfssm_last_error", "dfssm_version"]
+           "dfssm_scaffold_lora_chain", "dfssm_chain_prepare", "dfssm_chain_run", "dfssm_chain_status",
+           "dfssm_status_string", "dfssm_last_error", "dfssm_version"]
 
 
 class DfssmError(RuntimeError):
@@ -55,6 +56,12 @@ def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dfssm_chain_workspace_bytes.restype = sz
     lib.dfssm_scaffold_lora_chain.argtypes = [ctypes.POINTER(Layer), i32, i64, vp, vp, vp, vp, sz, vp]
     lib.dfssm_scaffold_lora_chain.restype = i32
+    lib.dfssm_chain_prepare.argtypes = [ctypes.POINTER(Layer), i32, i64, vp, sz, vp]
+    lib.dfssm_chain_prepare.restype = i32
+    lib.dfssm_chain_run.argtypes = [ctypes.POINTER(Layer), i32, i64, vp, vp, vp, vp, sz, vp]
+    lib.dfssm_chain_run.restype = i32
+    lib.dfssm_chain_status.argtypes = [ctypes.POINTER(Layer), i32, i64, vp, sz, ctypes.POINTER(ctypes.c_uint), vp]
+    lib.dfssm_chain_status.restype = i32
     lib.dfssm_status_string.argtypes = [i32]
     lib.dfssm_status_string.restype = ctypes.c_char_p
     lib.dfssm_last_error.restype = ctypes.c_char_p
@@ -206,3 +213,23 @@ def scaffold_lora_chain(layers, q0, s0, y_all=None, workspace=None, layer_arr=No
         outs.append(y_all[off:off + M * N].view(M, N))
         off += M * N
     return outs
+
+
+def chain_prepare(layer_arr, M: int, workspace, stream=None):
+    """Prepare `workspace` (device uint8 tensor) for chain_run on these layers."""
+    _check(lib.dfssm_chain_prepare(layer_arr, len(layer_arr), M, workspace.data_ptr(), workspace.numel(),
+                                   _stream(stream)))
+
+
+def chain_run(layer_arr, q0, s0, y_all, workspace, stream=None):
+    """Run a prepared chain: q0 [M,K0] int8, s0 [M] fp32 -> y_all (flat fp32)."""
+    _check(lib.dfssm_chain_run(layer_arr, len(layer_arr), q0.shape[0], q0.data_ptr(), s0.data_ptr(),
+                               y_all.data_ptr(), workspace.data_ptr(), workspace.numel(), _stream(stream)))
+
+
+def chain_status(layer_arr, M: int, workspace, stream=None) -> int:
+    """Synchronise and read the persistent chain's status word (0 = fine)."""
+    out = ctypes.c_uint(0)
+    _check(lib.dfssm_chain_status(layer_arr, len(layer_arr), M, workspace.data_ptr(), workspace.numel(),
+                                  ctypes.byref(out), _stream(stream)))
+    return int(out.value)

@@ -169,21 +169,21 @@ dfssm_status dfssm_scaffold_lora_linear(const int8_t* q, const float* s, int64_t
 // ---------------------------------------------------------------- chain
 // Workspace of the host-sequenced chain: Q [M, Kmax] int8, s [M] fp32, one
 // linear workspace sized for the largest layer.  Workspace of the persistent
-// chain (M = 1): layer table, then the exchange region y_ll (one 64-bit word
-// per output of every linear), acc_ll (n_layers x acc_stride words), done_ll
-// (n_layers x workgroups words) and one status word.  The larger of the two is required.
+// chain (M = 1): layer table, its 64-bit fingerprint, then the exchange
+// region y_ll (one 64-bit word per output of every linear), acc_ll
+// (n_layers x 256 padded words), done_ll (n_layers x workgroups padded
+// words) and the status word.  The larger of the two is required.
 struct ChainLayout {
   size_t off_s, off_lin, seq_bytes;
-  size_t off_table, off_yll, off_acc, off_done, off_status, pers_bytes;
+  size_t off_table, off_hash, off_yll, off_acc, off_done, off_status, pers_bytes;
   int64_t y_words;
 };
 
 static ChainLayout chain_layout(const dfssm_layer* layers, int n_layers, int64_t M) {
   ChainLayout c{};
-  int64_t kmax = 0, rmax = 0, ysum = 0;
+  int64_t kmax = 0, ysum = 0;
   for (int l = 0; l < n_layers; ++l) {
     kmax = std::max(kmax, layers[l].K);
-    rmax = std::max(rmax, layers[l].r);
     ysum += layers[l].N;
   }
   size_t o = (size_t)dfssm::round_up(M * kmax, 256);
@@ -195,6 +195,8 @@ static ChainLayout chain_layout(const dfssm_layer* layers, int n_layers, int64_t
   c.seq_bytes = o + lin;
   c.off_table = 0;
   o = (size_t)dfssm::round_up((int64_t)(n_layers * sizeof(dfssm::ChainLayerDev)), 256);
+  c.off_hash = o;
+  o += 256;
   c.off_yll = o;
   c.y_words = ysum * M;
   o += (size_t)c.y_words * 8;
@@ -208,16 +210,7 @@ static ChainLayout chain_layout(const dfssm_layer* layers, int n_layers, int64_t
   return c;
 }
 
-size_t dfssm_chain_workspace_bytes(const dfssm_layer* layers, int n_layers, int64_t M) {
-  if (!layers || n_layers <= 0 || M <= 0) return 0;
-  ChainLayout c = chain_layout(layers, n_layers, M);
-  return std::max(c.seq_bytes, c.pers_bytes);
-}
-
-dfssm_status dfssm_scaffold_lora_chain(const dfssm_layer* layers, int n_layers, int64_t M,
-                                       const int8_t* q0, const float* s0, float* y_all,
-                                       void* workspace, size_t workspace_bytes, void* stream) {
-  clear_error();
+static dfssm_status validate_chain(const dfssm_layer* layers, int n_layers, int64_t M) {
   if (n_layers < 0) return fail(DFSSM_ERR_SHAPE, "n_layers=%d", n_layers);
   if (n_layers == 0 || M == 0) return DFSSM_OK;
   if (!layers) return fail(DFSSM_ERR_NULL, "layers is NULL");
@@ -241,46 +234,102 @@ dfssm_status dfssm_scaffold_lora_chain(const dfssm_layer* layers, int n_layers, 
       return fail(st, "layer %d: %s", l, why);
     }
   }
-  dfssm_status st = check_ptrs({{q0, "q0"}, {s0, "s0"}, {y_all, "y_all"}, {workspace, "workspace"}}, {});
+  return DFSSM_OK;
+}
+
+// The persistent kernel's device table for these layers and its FNV-1a
+// fingerprint (over the table bytes and the layer count).
+static uint64_t chain_table(const dfssm_layer* layers, int n_layers,
+                            std::vector<dfssm::ChainLayerDev>& table) {
+  table.assign(n_layers, dfssm::ChainLayerDev{});
+  int64_t off = 0;
+  for (int l = 0; l < n_layers; ++l) {
+    const dfssm_layer& L = layers[l];
+    // rank 0: the kernel reads through A/B/beta unconditionally (and masks
+    // the values), so give it a valid address
+    const bool lr = L.r > 0;
+    table[l] = dfssm::ChainLayerDev{L.w_bits,
+                                    L.alpha,
+                                    lr ? L.A : reinterpret_cast<const int8_t*>(L.alpha),
+                                    lr ? L.B : reinterpret_cast<const int8_t*>(L.alpha),
+                                    lr ? L.beta : L.alpha,
+                                    (int32_t)L.K,
+                                    (int32_t)L.N,
+                                    (int32_t)L.r,
+                                    dfssm::chain_lanes_per_row(L.K),
+                                    off};
+    off += L.N;
+  }
+  uint64_t h = 1469598103934665603ull;
+  auto mix = [&](const void* p, size_t n) {
+    const unsigned char* b = static_cast<const unsigned char*>(p);
+    for (size_t i = 0; i < n; ++i) h = (h ^ b[i]) * 1099511628211ull;
+  };
+  mix(&n_layers, sizeof(n_layers));
+  mix(table.data(), table.size() * sizeof(table[0]));
+  return h;
+}
+
+size_t dfssm_chain_workspace_bytes(const dfssm_layer* layers, int n_layers, int64_t M) {
+  if (!layers || n_layers <= 0 || M <= 0) return 0;
+  ChainLayout c = chain_layout(layers, n_layers, M);
+  return std::max(c.seq_bytes, c.pers_bytes);
+}
+
+static dfssm_status chain_common(const dfssm_layer* layers, int n_layers, int64_t M, void* workspace,
+                                 size_t workspace_bytes, ChainLayout* c) {
+  dfssm_status st = check_ptrs({{workspace, "workspace"}}, {});
   if (st != DFSSM_OK) return st;
-  const ChainLayout c = chain_layout(layers, n_layers, M);
-  const size_t need = std::max(c.seq_bytes, c.pers_bytes);
+  *c = chain_layout(layers, n_layers, M);
+  const size_t need = std::max(c->seq_bytes, c->pers_bytes);
   if (workspace_bytes < need)
     return fail(DFSSM_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, need);
+  return DFSSM_OK;
+}
 
+dfssm_status dfssm_chain_prepare(const dfssm_layer* layers, int n_layers, int64_t M, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  clear_error();
+  dfssm_status st = validate_chain(layers, n_layers, M);
+  if (st != DFSSM_OK || n_layers == 0 || M == 0) return st;
+  ChainLayout c;
+  st = chain_common(layers, n_layers, M, workspace, workspace_bytes, &c);
+  if (st != DFSSM_OK) return st;
+  if (!dfssm::chain_persistent_supported(layers, n_layers, M, dfssm::chain_grid())) return DFSSM_OK;
+  static thread_local std::vector<dfssm::ChainLayerDev> table;
+  const uint64_t h = chain_table(layers, n_layers, table);
+  char* base = static_cast<char*>(workspace);
+  auto* exch = reinterpret_cast<uint64_t*>(base + c.off_yll);
+  const int64_t exch_words = (int64_t)(c.off_status + 8 - c.off_yll) / 8;
+  hipError_t e = dfssm::launch_chain_setup(table.data(), reinterpret_cast<dfssm::ChainLayerDev*>(base + c.off_table),
+                                           n_layers, exch, exch_words,
+                                           reinterpret_cast<uint64_t*>(base + c.off_hash), h, (hipStream_t)stream);
+  return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain prepare launch");
+}
+
+dfssm_status dfssm_chain_run(const dfssm_layer* layers, int n_layers, int64_t M, const int8_t* q0,
+                             const float* s0, float* y_all, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+  clear_error();
+  dfssm_status st = validate_chain(layers, n_layers, M);
+  if (st != DFSSM_OK || n_layers == 0 || M == 0) return st;
+  st = check_ptrs({{q0, "q0"}, {s0, "s0"}, {y_all, "y_all"}}, {});
+  if (st != DFSSM_OK) return st;
+  ChainLayout c;
+  st = chain_common(layers, n_layers, M, workspace, workspace_bytes, &c);
+  if (st != DFSSM_OK) return st;
   hipStream_t hs = (hipStream_t)stream;
   char* base = static_cast<char*>(workspace);
 
   if (dfssm::chain_persistent_supported(layers, n_layers, M, dfssm::chain_grid())) {
-    // the layer table travels by value in the setup kernels' arguments
     static thread_local std::vector<dfssm::ChainLayerDev> table;
-    table.resize(n_layers);
-    int64_t off = 0;
-    for (int l = 0; l < n_layers; ++l) {
-      const dfssm_layer& L = layers[l];
-      // rank 0: the kernel reads through A/B/beta unconditionally (and masks
-      // the values), so give it a valid address
-      const bool lr = L.r > 0;
-      table[l] = dfssm::ChainLayerDev{L.w_bits,
-                                      L.alpha,
-                                      lr ? L.A : reinterpret_cast<const int8_t*>(L.alpha),
-                                      lr ? L.B : reinterpret_cast<const int8_t*>(L.alpha),
-                                      lr ? L.beta : L.alpha,
-                                      (int32_t)L.K,
-                                      (int32_t)L.N,
-                                      (int32_t)L.r,
-                                      dfssm::chain_lanes_per_row(L.K),
-                                      off};
-      off += L.N;
-    }
-    auto* tdev = reinterpret_cast<dfssm::ChainLayerDev*>(base + c.off_table);
-    auto* exch = reinterpret_cast<uint64_t*>(base + c.off_yll);
-    const int64_t exch_words = (int64_t)(c.off_status + 8 - c.off_yll) / 8;
-    hipError_t e = dfssm::launch_chain_persistent(
-        table.data(), tdev, n_layers, q0, s0, exch, exch_words, exch,
-        reinterpret_cast<uint64_t*>(base + c.off_acc), reinterpret_cast<uint64_t*>(base + c.off_done), y_all,
-        reinterpret_cast<unsigned*>(base + c.off_status), next_chain_seq(), hs);
-    return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain persistent launch");
+    const uint64_t h = chain_table(layers, n_layers, table);
+    hipError_t e = dfssm::launch_chain_run(
+        reinterpret_cast<const dfssm::ChainLayerDev*>(base + c.off_table), n_layers, q0, s0,
+        reinterpret_cast<uint64_t*>(base + c.off_yll), reinterpret_cast<uint64_t*>(base + c.off_acc),
+        reinterpret_cast<uint64_t*>(base + c.off_done), y_all, reinterpret_cast<unsigned*>(base + c.off_status),
+        next_chain_seq(), reinterpret_cast<const uint64_t*>(base + c.off_hash), h, hs);
+    return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain run launch");
   }
 
   int8_t* qbuf = reinterpret_cast<int8_t*>(base);
@@ -305,6 +354,32 @@ dfssm_status dfssm_scaffold_lora_chain(const dfssm_layer* layers, int n_layers, 
     y_cur += M * L.N;
   }
   return DFSSM_OK;
+}
+
+dfssm_status dfssm_scaffold_lora_chain(const dfssm_layer* layers, int n_layers, int64_t M,
+                                       const int8_t* q0, const float* s0, float* y_all,
+                                       void* workspace, size_t workspace_bytes, void* stream) {
+  dfssm_status st = dfssm_chain_prepare(layers, n_layers, M, workspace, workspace_bytes, stream);
+  if (st != DFSSM_OK) return st;
+  return dfssm_chain_run(layers, n_layers, M, q0, s0, y_all, workspace, workspace_bytes, stream);
+}
+
+dfssm_status dfssm_chain_status(const dfssm_layer* layers, int n_layers, int64_t M, const void* workspace,
+                                size_t workspace_bytes, unsigned* status, void* stream) {
+  clear_error();
+  if (!status) return fail(DFSSM_ERR_NULL, "status is NULL");
+  *status = 0;
+  dfssm_status st = validate_chain(layers, n_layers, M);
+  if (st != DFSSM_OK || n_layers == 0 || M == 0) return st;
+  ChainLayout c;
+  st = chain_common(layers, n_layers, M, const_cast<void*>(workspace), workspace_bytes, &c);
+  if (st != DFSSM_OK) return st;
+  if (!dfssm::chain_persistent_supported(layers, n_layers, M, dfssm::chain_grid())) return DFSSM_OK;
+  hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+  if (e == hipSuccess)
+    e = hipMemcpy(status, static_cast<const char*>(workspace) + c.off_status, sizeof(unsigned),
+                  hipMemcpyDeviceToHost);
+  return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain status read");
 }
 
 }  // extern "C"

@@ -27,6 +27,10 @@
 //    epilogue; publishes its y rows; then prefetches linear l+2.
 //  * Every wait is bounded: on time-out the workgroup records an error in
 //    the status word and leaves, so the grid always drains.
+//  * The layer table lives in the workspace, written by a setup launch
+//    (dfssm_chain_prepare) together with a fingerprint of the table; the
+//    kernel compares that fingerprint with the caller's before it reads the
+//    table, and leaves (status bit 8) if they differ.
 #include <float.h>
 
 #include "dfssm_internal.hpp"
@@ -199,7 +203,13 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
     const dfssm::ChainLayerDev* __restrict__ layers, int L, const int8_t* __restrict__ q0,
     const float* __restrict__ s0, uint64_t* __restrict__ y_ll, uint64_t* __restrict__ acc_ll,
     uint64_t* __restrict__ done_ll, float* __restrict__ y_all, unsigned* __restrict__ status,
-    uint32_t seq) {
+    uint32_t seq, const uint64_t* __restrict__ table_hash, uint64_t expect_hash) {
+  // the table was written by a prepare of the same layers, or nothing here
+  // is trusted: leave before reading it
+  if (*table_hash != expect_hash) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(status, 8u);
+    return;
+  }
   __shared__ uint4 pl_lds[(dfssm::kChainMaxK / 128) * 8];
   __shared__ int4 acc_lds[dfssm::kMaxRank / 4];
   __shared__ int32_t dot_part[kGW];
@@ -444,6 +454,8 @@ struct SetupArgs {
   dfssm::ChainLayerDev* table;
   uint64_t* zero_base;
   int64_t zero_words;
+  uint64_t* hash_dst;
+  uint64_t hash;
   int first, count;
 };
 
@@ -451,6 +463,7 @@ __global__ void chain_setup(SetupArgs a) {
   const int64_t i0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   if (i0 < a.count) a.table[a.first + i0] = a.e[i0];
   for (int64_t i = i0; i < a.zero_words; i += (int64_t)gridDim.x * blockDim.x) a.zero_base[i] = 0;
+  if (a.hash_dst && i0 == 0) *a.hash_dst = a.hash;
 }
 
 }  // namespace
@@ -479,11 +492,9 @@ bool chain_persistent_supported(const dfssm_layer* layers, int n_layers, int64_t
   return true;
 }
 
-hipError_t launch_chain_persistent(const ChainLayerDev* table_host, ChainLayerDev* table_dev,
-                                   int n_layers, const int8_t* q0, const float* s0,
-                                   uint64_t* exch, int64_t exch_words, uint64_t* y_ll,
-                                   uint64_t* acc_ll, uint64_t* done_ll, float* y_all,
-                                   unsigned* status, uint32_t seq, hipStream_t st) {
+hipError_t launch_chain_setup(const ChainLayerDev* table_host, ChainLayerDev* table_dev, int n_layers,
+                              uint64_t* exch, int64_t exch_words, uint64_t* hash_dev, uint64_t hash,
+                              hipStream_t st) {
   for (int first = 0; first < n_layers; first += kChainSetupChunk) {
     SetupArgs a{};
     a.count = n_layers - first < kChainSetupChunk ? n_layers - first : kChainSetupChunk;
@@ -492,13 +503,25 @@ hipError_t launch_chain_persistent(const ChainLayerDev* table_host, ChainLayerDe
     a.first = first;
     a.zero_base = exch;
     a.zero_words = first == 0 ? exch_words : 0;
+    // the last chunk publishes the table's fingerprint (stream order puts it
+    // after every chunk)
+    a.hash_dst = first + kChainSetupChunk >= n_layers ? hash_dev : nullptr;
+    a.hash = hash;
     chain_setup<<<dim3(first == 0 ? 256 : 1), dim3(256), 0, st>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  return hipSuccess;
+}
+
+hipError_t launch_chain_run(const ChainLayerDev* table_dev, int n_layers, const int8_t* q0, const float* s0,
+                            uint64_t* y_ll, uint64_t* acc_ll, uint64_t* done_ll, float* y_all,
+                            unsigned* status, uint32_t seq, const uint64_t* hash_dev, uint64_t hash,
+                            hipStream_t st) {
   int L = n_layers;
-  void* args[] = {(void*)&table_dev, (void*)&L,       (void*)&q0,    (void*)&s0,     (void*)&y_ll,
-                  (void*)&acc_ll,    (void*)&done_ll, (void*)&y_all, (void*)&status, (void*)&seq};
+  void* args[] = {(void*)&table_dev, (void*)&L,      (void*)&q0,       (void*)&s0,
+                  (void*)&y_ll,      (void*)&acc_ll, (void*)&done_ll,  (void*)&y_all,
+                  (void*)&status,    (void*)&seq,    (void*)&hash_dev, (void*)&hash};
   return hipLaunchCooperativeKernel((const void*)chain_persistent, dim3(chain_grid()), dim3(kCT), args, 0, st);
 }
 

@@ -114,14 +114,17 @@ struct ChainLayerDev {
 int chain_lanes_per_row(int64_t K);
 int chain_grid();
 bool chain_persistent_supported(const dfssm_layer* layers, int n_layers, int64_t M, int nwg);
-// Copies the layer table to table_dev and zeroes the exchange region
-// [exch, exch + exch_words) (y_ll, acc_ll, done_ll and the status word) with
-// small setup kernels, then launches the cooperative persistent kernel.
-hipError_t launch_chain_persistent(const ChainLayerDev* table_host, ChainLayerDev* table_dev,
-                                   int n_layers, const int8_t* q0, const float* s0,
-                                   uint64_t* exch, int64_t exch_words, uint64_t* y_ll,
-                                   uint64_t* acc_ll, uint64_t* done_ll, float* y_all,
-                                   unsigned* status, uint32_t seq, hipStream_t st);
+// Writes the layer table (by value, chunked) to table_dev, zeroes the
+// exchange region [exch, exch + exch_words) and stores the table's
+// fingerprint at hash_dev.
+hipError_t launch_chain_setup(const ChainLayerDev* table_host, ChainLayerDev* table_dev, int n_layers,
+                              uint64_t* exch, int64_t exch_words, uint64_t* hash_dev, uint64_t hash,
+                              hipStream_t st);
+// Cooperative launch of the persistent chain kernel on a prepared workspace.
+hipError_t launch_chain_run(const ChainLayerDev* table_dev, int n_layers, const int8_t* q0, const float* s0,
+                            uint64_t* y_ll, uint64_t* acc_ll, uint64_t* done_ll, float* y_all,
+                            unsigned* status, uint32_t seq, const uint64_t* hash_dev, uint64_t hash,
+                            hipStream_t st);
 
 }  // namespace dfssm
 

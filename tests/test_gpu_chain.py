@@ -82,3 +82,38 @@ def test_chain_persistent_shapes(env, r):
         assert -(-rows_per_wg // (8 * (64 // G))) <= 2
     say(f"chain persistent r={r}")
     _check_chain(env, shapes, r=r, M=1, key=100 + r)
+
+
+def test_chain_prepare_once_run_many(env):
+    """One prepare, several runs with different inputs and weight sets
+    prepared in separate workspaces; each run bit-exact; status stays 0; a
+    workspace prepared for other layers is refused by the kernel (status
+    bit 8) without writing the output."""
+    torch, D, o = env
+    say("chain prepare/run")
+    shapes = [(256, 512), (512, 256), (256, 384)]
+    sets = [[S.weights(K, N, 8, key=(21, v, i)) for i, (K, N) in enumerate(shapes)] for v in range(2)]
+    dls = [[dev_weights(ly) for ly in layers] for layers in sets]
+    arrs = [D.make_layers(dl) for dl in dls]
+    nbytes = D.chain_workspace_bytes(arrs[0], 1)
+    wss = [torch.empty(nbytes, dtype=torch.uint8, device="cuda") for _ in range(2)]
+    for arr, ws in zip(arrs, wss):
+        D.chain_prepare(arr, 1, ws)
+    y = torch.empty(sum(N for _, N in shapes), dtype=torch.float32, device="cuda")
+    for it in range(4):
+        v = it % 2
+        x = S.activations(1, 256, key=(21, 100 + it))
+        q0, s0 = o.quantize_act(x)
+        ys_ref, _ = o.chain(sets[v], q0, s0)
+        D.chain_run(arrs[v], dev(q0), dev(s0), y, wss[v])
+        assert D.chain_status(arrs[v], 1, wss[v]) == 0
+        got = host(y)
+        off = 0
+        for l, yr in enumerate(ys_ref):
+            assert np.array_equal(got[off:off + yr.size].reshape(yr.shape).view(np.uint32), yr.view(np.uint32)), (it, l)
+            off += yr.size
+    # layers of set 1 against the workspace prepared for set 0: refused
+    y.fill_(-1.0)
+    D.chain_run(arrs[1], dev(q0), dev(s0), y, wss[0])
+    assert D.chain_status(arrs[1], 1, wss[0]) & 8
+    assert bool((y == -1.0).all())

@@ -99,6 +99,16 @@ def test_chain_validation(dl):
     assert "layer 0" in dl.last_error()
     assert f(arr, 0, 1, None, None, None, None, 0, None) == dl.OK
     assert dl.lib.dfssm_chain_workspace_bytes(arr, 1, 1) > 0
+    # prepare / run / status validate the same way, before any HIP call
+    arr = (L * 2)(L(**good), L(**dict(good, K=128)))
+    assert dl.lib.dfssm_chain_prepare(arr, 2, 1, 16, 1 << 30, None) == dl.ERR_SHAPE
+    assert dl.lib.dfssm_chain_run(arr, 2, 1, 16, 16, 16, 16, 1 << 30, None) == dl.ERR_SHAPE
+    arr = (L * 2)(L(**good), L(**dict(good, K=64)))
+    assert dl.lib.dfssm_chain_prepare(arr, 2, 1, 16, 8, None) == dl.ERR_WORKSPACE
+    assert dl.lib.dfssm_chain_run(arr, 2, 1, None, 16, 16, 16, 1 << 30, None) == dl.ERR_NULL
+    st = ctypes.c_uint(7)
+    assert dl.lib.dfssm_chain_status(arr, 2, 1, 16, 8, ctypes.byref(st), None) == dl.ERR_WORKSPACE
+    assert dl.lib.dfssm_chain_status(arr, 2, 1, 16, 1 << 30, None, None) == dl.ERR_NULL
 
 
 def test_workspace_sizes(dl):
