@@ -18,7 +18,7 @@
 // gets the exact int64 acc_b = sum_j B[n,j] acc_a[m,j] from four int8
 // MFMAs, E_hi = 256*(L3.B) + L2.B and E_lo = 256*(L1.B) + L0.B (each < 2^31
 // for r <= 256), acc_b = E_lo + 65536*E_hi, 16 output rows at a time, so
-// the K-loop holds only the scaffold accumulators (4 blocks per CU).
+// the K-loop holds only the scaffold accumulators (3 blocks per CU).
 #include "dfssm_internal.hpp"
 
 namespace {
