@@ -177,9 +177,12 @@ dfssm_status dfssm_chain_run(const dfssm_layer* layers, int n_layers, int64_t M,
 
 /* Synchronises `stream` and reads the persistent chain's status word into
  * *status (host): 0 = fine; bit 1 = a wait for a previous output timed out;
- * bit 2 = a wait for the LoRA down-projection timed out; bit 4 = an output
- * word never became valid; bit 8 = the workspace was not prepared for these
- * layers.  Bits accumulate over runs until the next dfssm_chain_prepare.
+ * bit 2 = a wait for the LoRA down-projection timed out; bit 8 = the
+ * workspace was not prepared for these layers; bit 16 = the workgroups'
+ * placement on the XCDs could not be read or leaves an XCD too few
+ * workgroups for the rank (r > 2 x workgroups of the smallest XCD).  After a
+ * nonzero status the outputs of that run are incomplete.  Bits accumulate
+ * over runs until the next dfssm_chain_prepare.
  * Always 0 for chains that do not use the persistent kernel.
  * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */
 dfssm_status dfssm_chain_status(const dfssm_layer* layers, int n_layers, int64_t M,

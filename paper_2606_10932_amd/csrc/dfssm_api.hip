@@ -170,12 +170,13 @@ dfssm_status dfssm_scaffold_lora_linear(const int8_t* q, const float* s, int64_t
 // Workspace of the host-sequenced chain: Q [M, Kmax] int8, s [M] fp32, one
 // linear workspace sized for the largest layer.  Workspace of the persistent
 // chain (M = 1): layer table, its 64-bit fingerprint, then the exchange
-// region y_ll (one 64-bit word per output of every linear), acc_ll
-// (n_layers x 256 padded words), done_ll (n_layers x workgroups padded
-// words) and the status word.  The larger of the two is required.
+// region: y_ll (one 64-bit word per output of every linear), y_rel (one copy
+// of y_ll per XCD), acc_rel (per XCD, n_layers x kMaxRank words), xmap (one
+// word per workgroup) and the status word.  The larger of the two is
+// required.
 struct ChainLayout {
   size_t off_s, off_lin, seq_bytes;
-  size_t off_table, off_hash, off_yll, off_acc, off_done, off_status, pers_bytes;
+  size_t off_table, off_hash, off_yll, off_yrel, off_acc, off_xmap, off_status, pers_bytes;
   int64_t y_words;
 };
 
@@ -199,11 +200,13 @@ static ChainLayout chain_layout(const dfssm_layer* layers, int n_layers, int64_t
   o += 256;
   c.off_yll = o;
   c.y_words = ysum * M;
-  o += (size_t)c.y_words * 8;
+  o += (size_t)dfssm::round_up(c.y_words * 8, 256);
+  c.off_yrel = o;
+  o += (size_t)dfssm::kChainXcds * dfssm::round_up(c.y_words * 8, 256);
   c.off_acc = o;
-  o += (size_t)n_layers * dfssm::kMaxRank * dfssm::kChainPad * 8;
-  c.off_done = o;
-  o += (size_t)n_layers * dfssm::chain_grid() * dfssm::kChainPad * 8;
+  o += (size_t)dfssm::kChainXcds * n_layers * dfssm::kMaxRank * 8;
+  c.off_xmap = o;
+  o += (size_t)dfssm::chain_grid() * 8;
   c.off_status = o;
   o += 256;
   c.pers_bytes = o;
@@ -324,11 +327,19 @@ dfssm_status dfssm_chain_run(const dfssm_layer* layers, int n_layers, int64_t M,
   if (dfssm::chain_persistent_supported(layers, n_layers, M, dfssm::chain_grid())) {
     static thread_local std::vector<dfssm::ChainLayerDev> table;
     const uint64_t h = chain_table(layers, n_layers, table);
-    hipError_t e = dfssm::launch_chain_run(
-        reinterpret_cast<const dfssm::ChainLayerDev*>(base + c.off_table), n_layers, q0, s0,
-        reinterpret_cast<uint64_t*>(base + c.off_yll), reinterpret_cast<uint64_t*>(base + c.off_acc),
-        reinterpret_cast<uint64_t*>(base + c.off_done), y_all, reinterpret_cast<unsigned*>(base + c.off_status),
-        next_chain_seq(), reinterpret_cast<const uint64_t*>(base + c.off_hash), h, hs);
+    dfssm::ChainExch ex{};
+    ex.y_ll = reinterpret_cast<uint64_t*>(base + c.off_yll);
+    // per-XCD copies are spaced by the (256-byte rounded) size of y_ll
+    ex.y_rel = reinterpret_cast<uint64_t*>(base + c.off_yrel);
+    ex.ysum = dfssm::round_up(c.y_words * 8, 256) / 8;
+    ex.acc_rel = reinterpret_cast<uint64_t*>(base + c.off_acc);
+    ex.xmap = reinterpret_cast<uint64_t*>(base + c.off_xmap);
+    ex.status = reinterpret_cast<unsigned*>(base + c.off_status);
+    ex.r_max = 0;
+    for (int l = 0; l < n_layers; ++l) ex.r_max = std::max(ex.r_max, (int32_t)layers[l].r);
+    hipError_t e = dfssm::launch_chain_run(reinterpret_cast<const dfssm::ChainLayerDev*>(base + c.off_table),
+                                           n_layers, q0, s0, ex, y_all, next_chain_seq(),
+                                           reinterpret_cast<const uint64_t*>(base + c.off_hash), h, hs);
     return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain run launch");
   }
 

@@ -5,26 +5,40 @@
 //
 // Every linear depends on all of the previous linear's output (its absmax
 // and its LoRA down-projection are reductions over all of it), so the chain
-// is bound by cross-CU communication latency, not by HBM.  The design keeps
-// that to two one-way hops per linear and never uses an agent-scope fence
-// (on MI355X a release/acquire pair costs ~3.5 us: it writes back and
-// invalidates the whole L2):
+// is bound by cross-CU communication latency, not by HBM.  The design:
 //
-//  * Data crosses workgroups as 64-bit words {tag:32, value:32}, each written
-//    with one relaxed agent-scope atomic store and read with relaxed atomic
-//    loads, so a consumer polls the data itself: a word is valid once its
-//    tag equals the linear's tag.  The exchange region is zeroed before the
-//    launch, so tag 0 never matches.
-//  * A workgroup is two groups of 4 waves that alternate roles: while one
+//  * Data crosses workgroups as 64-bit words {tag:32, value:32}, so a
+//    consumer polls the data itself: a word is valid once its tag equals
+//    the linear's tag.  Tags carry a per-launch sequence number, so words
+//    left from an earlier launch never validate.  No fences are used (on
+//    MI355X a release/acquire pair costs ~3.5 us: it writes back and
+//    invalidates the whole L2).
+//  * Two levels of exchange.  MI355X has 8 XCDs, each with its own L2; a
+//    cross-XCD word needs an agent-scope store and load (~0.9 us round
+//    trip), a word inside one XCD only a store into that XCD's L2 and a
+//    load that skips the CU's L1 (~0.6 us).  At start every workgroup reads
+//    its XCD id (hardware register XCC_ID) and publishes it, so each knows
+//    its rank rho among the n_x workgroups of its XCD.  Per linear:
+//      - outputs y_{l-1} are stored once at agent scope (y_ll);
+//      - workgroup rho of XCD x copies slice rho of y_{l-1}[0:K] from y_ll
+//        into x's own region (y_rel[x]) as soon as each word is valid;
+//      - every workgroup polls all of y_{l-1}[0:K] in its XCD's region
+//        (L2 hits): 1/n_x of the cross-XCD polling traffic of reading y_ll
+//        directly;
+//      - the LoRA down-projection is computed inside each XCD: workgroup
+//        rho computes acc_a[j] for j = rho + n_x*t (t < kChainAccRows) and
+//        stores it into x's region, so acc_a never crosses an XCD.
+//  * A workgroup is two groups of 8 waves that alternate roles: while one
 //    group computes linear l, the other holds (in its own registers) the
 //    weights of linear l+1 it loaded during linear l-1.  So the
 //    latency-critical waits (which wait for all of a wave's outstanding
 //    loads) never wait behind a weight prefetch.
-//  * Per linear, the active group: polls y_{l-1}[0:K_l] -> absmax -> Q (the
-//    quantiser's fp32 decisions) -> bit-planes in LDS; workgroup j < r
-//    computes acc_a[j] = A[j,:].Q and publishes it; the popcount GEMV on the
-//    workgroup's rows; waits for the r acc_a words; LoRA up-projection and
-//    epilogue; publishes its y rows; then prefetches linear l+2.
+//  * Per linear, the active group: relays its slice; polls its words of
+//    y_{l-1}[0:K_l], reducing their absmax on the way -> Q (the quantiser's
+//    fp32 decisions) -> bit-planes in LDS and its acc_a rows; the popcount
+//    GEMV on the workgroup's rows; collects the r acc_a words of its XCD;
+//    LoRA up-projection and epilogue; stores its y rows; then prefetches
+//    linear l+2.
 //  * Every wait is bounded: on time-out the workgroup records an error in
 //    the status word and leaves, so the grid always drains.
 //  * The layer table lives in the workspace, written by a setup launch
@@ -42,57 +56,47 @@ constexpr int kCT = 2 * kGT;          // threads per workgroup
 constexpr int kGW = kGT / 64;         // waves per group
 static_assert(kGW == dfssm::kChainWaves, "waves per role group");
 constexpr int kMaxSteps = dfssm::kChainMaxSteps;
-constexpr int kPollVals = dfssm::kChainMaxK / kGT;
+constexpr int kCols = dfssm::kChainMaxK / kCT;  // previous-output columns per thread
+constexpr int kAccRows = dfssm::kChainAccRows;
+constexpr int kXcds = dfssm::kChainXcds;
+constexpr int kMaxGrid = 256;
 constexpr long kSpinLimit = 1L << 20;
-// done and acc_a words are spread one per 128-byte line (16 words), so the
-// workgroups polling them do not all hit one memory channel
-constexpr int kPad = dfssm::kChainPad;
 
+// status bits
+constexpr unsigned kStY = 1u, kStAcc = 2u, kStPlace = 16u;
+
+// agent scope: crosses XCDs (bypasses the non-coherent per-XCD L2s)
 __device__ __forceinline__ uint64_t ll_load(const uint64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// workgroup scope: may hit a copy in this XCD's L2 (shared by the
-// workgroups of the XCD); a stale copy fails the tag check and is re-read
-// at agent scope
-__device__ __forceinline__ uint64_t ll_load_cached(const uint64_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
 __device__ __forceinline__ void ll_store(uint64_t* p, uint32_t tag, uint32_t v) {
   __hip_atomic_store(p, ((uint64_t)tag << 32) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// inside one XCD: the store goes through (write-through L1) to the XCD's L2;
+// the load is a buffer load with sc0|nt, which skips the CU's L1 and is
+// served by that L2 (each poll loop also holds the status atomic, which keeps
+// the compiler from hoisting the loads out of it)
+__device__ __forceinline__ void xcd_store(uint64_t* p, uint64_t w) {
+  __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+typedef unsigned v2u __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint64_t xcd_load(__amdgpu_buffer_rsrc_t rs, uint32_t word) {
+  const v2u v = __builtin_amdgcn_raw_buffer_load_b64(rs, word * 8u, 0, 3);
+  return ((uint64_t)v.y << 32) | v.x;
+}
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t xcd_region(uint64_t* base, int64_t words) {
+  // dword 3 of the resource: 32-bit data format, as the gfx9 family needs
+  return __builtin_amdgcn_make_buffer_rsrc(base, 0, (int)(words * 8), 0x00020000);
 }
 
 __device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
   return __builtin_amdgcn_sdot4((int)a, (int)b, c, false);
 }
 
-__device__ __forceinline__ int8_t code(float v, float inv) {
-  float r = rintf(v * inv);
-  r = fminf(fmaxf(r, -127.0f), 127.0f);
-  return (int8_t)(int)r;
-}
-
-__device__ __forceinline__ int plane_sum(const int (&c)[8]) {
-  int s = c[0] + (c[1] << 1) + (c[2] << 2) + (c[3] << 3) + (c[4] << 4) + (c[5] << 5) + (c[6] << 6);
-  return s - (c[7] << 7);
-}
-
-__device__ __forceinline__ int chunk_masked_sum(const uint4 w, const uint4 (&P)[8]) {
-  int c[8];
-#pragma unroll
-  for (int b = 0; b < 8; ++b)
-    c[b] = __builtin_popcount(w.x & P[b].x) + __builtin_popcount(w.y & P[b].y) +
-           __builtin_popcount(w.z & P[b].z) + __builtin_popcount(w.w & P[b].w);
-  return plane_sum(c);
-}
-
-__device__ __forceinline__ int chunk_qsum(const uint4 (&P)[8]) {
-  int c[8];
-#pragma unroll
-  for (int b = 0; b < 8; ++b)
-    c[b] = __builtin_popcount(P[b].x) + __builtin_popcount(P[b].y) + __builtin_popcount(P[b].z) +
-           __builtin_popcount(P[b].w);
-  return plane_sum(c);
-}
+// The quantiser's code of v for inv = 127/a, where |v| <= a: |v * inv| is
+// at most 127 * (1 + 2^-23)^2 < 127.5, so rint() already lands in [-127, 127]
+// and the clamp of the definition never changes the result.
+__device__ __forceinline__ int code(float v, float inv) { return (int)rintf(v * inv); }
 
 __device__ __forceinline__ int dpp_sum16(int v) {
   v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
@@ -114,31 +118,32 @@ __device__ __forceinline__ int group_sum(int v, int G) {
   return v;
 }
 
-__device__ __forceinline__ int wave_sum(int v) {
+// Whole-wave reductions with the result as a uniform value: DPP inside each
+// 16-lane row, then row_bcast:15 (rows 1, 3 take lane 15 of the row below)
+// and row_bcast:31 (rows 2, 3 take lane 31), which leaves the total in lane
+// 63.  No LDS permute on the way.
+__device__ __forceinline__ int wave_sum_u(int v) {
   v = dpp_sum16(v);
-  v += __shfl_xor(v, 16, 64);
-  v += __shfl_xor(v, 32, 64);
-  return v;
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);
+  return __builtin_amdgcn_readlane(v, 63);
 }
-
-// max over the wave of non-negative floats, compared as their bit patterns
-__device__ __forceinline__ uint32_t wave_max_bits(uint32_t v) {
+// max of non-negative floats, compared as their bit patterns
+__device__ __forceinline__ uint32_t wave_max_bits_u(uint32_t v) {
   v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));
   v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
   v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));
   v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false));
-  v = max(v, (uint32_t)__shfl_xor((int)v, 16, 64));
-  v = max(v, (uint32_t)__shfl_xor((int)v, 32, 64));
-  return v;
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false));
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
-// One linear's operands of this workgroup, per lane of a group.  The A row
-// is held in the column layout of the codes: a[i] is column gt + kGT * i.
+// One linear's operands of this workgroup's rows, per lane of a group.
 struct Pref {
   uint4 w[kMaxSteps];
   uint32_t b[kMaxSteps];
   float al[kMaxSteps], be[kMaxSteps];
-  int32_t a[kPollVals];
 };
 
 // Loads go through the global address space (the table's pointers are
@@ -146,8 +151,9 @@ struct Pref {
 // addresses; nothing is masked here, so no instruction waits on a prefetched
 // value before its use.  Values read for lanes outside the data are harmless
 // by construction: lanes past a row's chunks meet all-zero bit-planes, LoRA
-// lanes past r meet zero limbs, A bytes past K meet zero codes, and rows
-// outside the workgroup's range are never stored.
+// lanes past r meet zero limbs, A bytes past K meet zero codes, A rows past
+// r are never published, and rows outside the workgroup's range are never
+// stored.
 typedef unsigned v4u __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 gload16(const void* p) {
   v4u v = *(const __attribute__((address_space(1))) v4u*)(p);
@@ -160,8 +166,7 @@ __device__ __forceinline__ int32_t gload1s(const void* p) {
   return *(const __attribute__((address_space(1))) int8_t*)(p);
 }
 
-__device__ __forceinline__ void prefetch(const dfssm::ChainLayerDev& L, int wg, int nwg, int gt,
-                                         Pref& p) {
+__device__ __forceinline__ void prefetch(const dfssm::ChainLayerDev& L, int wg, int nwg, int gt, Pref& p) {
   const int lane = gt & 63, wave = gt >> 6;
   const int G = L.G, g = lane & (G - 1), grp = lane / G;
   const int RW = 64 / G;
@@ -178,11 +183,21 @@ __device__ __forceinline__ void prefetch(const dfssm::ChainLayerDev& L, int wg, 
     p.b[s] = gload4(L.B + (int64_t)nc * L.r + 4 * (g < r4 ? g : 0));
     p.be[s] = __uint_as_float(gload4(L.beta + nc));
   }
-  const int8_t* arow = L.A + (int64_t)(wg < L.r ? wg : 0) * L.K;
+}
+
+// This thread's bytes of the LoRA down rows rho + n_x*t (t < kAccRows) of a
+// linear, in the column layout of the codes: a[t][i] is column tid + kCT*i.
+__device__ __forceinline__ void load_a_cols(const dfssm::ChainLayerDev& L, int tid, int rho, int nx,
+                                            int32_t (&a)[kAccRows][kCols]) {
 #pragma unroll
-  for (int i = 0; i < kPollVals; ++i) {
-    const int k = gt + i * kGT;
-    p.a[i] = gload1s(arow + (k < L.K ? k : 0));
+  for (int t = 0; t < kAccRows; ++t) {
+    const int j = rho + nx * t;
+    const int8_t* arow = L.A + (int64_t)(j < L.r ? j : 0) * L.K;
+#pragma unroll
+    for (int i = 0; i < kCols; ++i) {
+      const int k = tid + i * kCT;
+      a[t][i] = gload1s(arow + (k < L.K ? k : 0));
+    }
   }
 }
 
@@ -201,9 +216,9 @@ __device__ __forceinline__ bool poll_ll(const uint64_t* p, uint32_t tag, uint64_
 
 __global__ __launch_bounds__(kCT, 1) void chain_persistent(
     const dfssm::ChainLayerDev* __restrict__ layers, int L, const int8_t* __restrict__ q0,
-    const float* __restrict__ s0, uint64_t* __restrict__ y_ll, uint64_t* __restrict__ acc_ll,
-    uint64_t* __restrict__ done_ll, float* __restrict__ y_all, unsigned* __restrict__ status,
-    uint32_t seq, const uint64_t* __restrict__ table_hash, uint64_t expect_hash) {
+    const float* __restrict__ s0, dfssm::ChainExch ex, float* __restrict__ y_all, uint32_t seq,
+    const uint64_t* __restrict__ table_hash, uint64_t expect_hash) {
+  unsigned* const status = ex.status;
   // the table was written by a prepare of the same layers, or nothing here
   // is trusted: leave before reading it
   if (*table_hash != expect_hash) {
@@ -212,30 +227,82 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
   }
   __shared__ uint4 pl_lds[(dfssm::kChainMaxK / 128) * 8];
   __shared__ int4 acc_lds[dfssm::kMaxRank / 4];
-  __shared__ int32_t dot_part[kGW];
+  __shared__ int32_t dot_part[kAccRows][2 * kGW];
   __shared__ uint32_t ymax_lds;
-  __shared__ int cnt_dot, cnt_epi;
-  __shared__ float inv_lds;
-  __shared__ int zero_lds;
+  __shared__ int sumq_lds;
+  __shared__ int cnt_dot;
   __shared__ int abort_;
+  __shared__ int rho_lds, nx_lds;
   const int wg = blockIdx.x, nwg = gridDim.x;
   const int tid = threadIdx.x;
   const int group = tid / kGT, gt = tid % kGT, lane = gt & 63, wave = gt >> 6;
+  const int wave16 = tid >> 6;  // wave index in the workgroup
+
+  // a word written for linear l carries tag(l); seq differs per launch
+  auto tag_of = [seq](int l) -> uint32_t { return (seq << 8) | (uint32_t)((l + 1) & 0xff); };
+  const uint32_t tag_place = seq << 8;
+
+  // ---- placement: the XCD of every workgroup, this one's rank among the
+  //      workgroups of its XCD, and the smallest XCD's size
+  const uint32_t xcc = __builtin_amdgcn_s_getreg((20) | (0 << 6) | ((4 - 1) << 11));  // HW_REG_XCC_ID[3:0]
   if (tid == 0) {
     abort_ = 0;
     cnt_dot = 0;
-    cnt_epi = 0;
     ymax_lds = 0;
+    sumq_lds = 0;
+    ll_store(ex.xmap + wg, tag_place, xcc);
   }
+  if (tid < 64) {
+    uint32_t x[kMaxGrid / 64];
+    bool ok = true;
+#pragma unroll
+    for (int t = 0; t < kMaxGrid / 64; ++t) {
+      const int w = tid + 64 * t;
+      x[t] = 0xffu;
+      if (w < nwg) {
+        uint64_t wd;
+        if (!poll_ll(ex.xmap + w, tag_place, wd, status, kStPlace)) ok = false;
+        x[t] = (uint32_t)wd;
+      }
+    }
+    int rho = 0, nx = 0, nmin = nwg;
+    for (int c = 0; c < 16; ++c) {
+      int cnt = 0, below = 0;
+#pragma unroll
+      for (int t = 0; t < kMaxGrid / 64; ++t) {
+        const uint64_t m = __ballot(x[t] == (uint32_t)c);
+        cnt += __popcll(m);
+        // lanes holding workgroups 64t .. 64t+63 that come before wg
+        const int w0 = 64 * t;
+        const uint64_t below_mask = wg <= w0 ? 0ull : (wg >= w0 + 64 ? ~0ull : ((1ull << (wg - w0)) - 1));
+        below += __popcll(m & below_mask);
+      }
+      if (cnt > 0) nmin = min(nmin, cnt);
+      if (c == (int)xcc) {
+        rho = below;
+        nx = cnt;
+      }
+    }
+    const bool bad = __ballot(!ok) != 0 || xcc >= (uint32_t)kXcds || (ex.r_max + nmin - 1) / nmin > kAccRows;
+    if (tid == 0) {
+      rho_lds = rho;
+      nx_lds = nx;
+      if (bad) {
+        atomicOr(status, kStPlace);
+        abort_ = 1;
+      }
+    }
+  }
+  __syncthreads();
+  if (abort_) return;
+  const int rho = rho_lds, nx = nx_lds;
+  uint64_t* const y_rel = ex.y_rel + (int64_t)xcc * ex.ysum;
+  uint64_t* const acc_rel = ex.acc_rel + (int64_t)xcc * L * dfssm::kMaxRank;
+  const __amdgpu_buffer_rsrc_t rs_y = xcd_region(y_rel, ex.ysum);
+  const __amdgpu_buffer_rsrc_t rs_acc = xcd_region(acc_rel, (int64_t)L * dfssm::kMaxRank);
 
   Pref pf;
   if (group < L) prefetch(layers[group], wg, nwg, gt, pf);
-  __syncthreads();
-
-  // a word written for linear l carries tag(l); seq differs per launch, so a
-  // word left from an earlier launch (or a stale cached copy of one) never
-  // validates
-  auto tag_of = [seq](int l) -> uint32_t { return (seq << 8) | (uint32_t)((l + 1) & 0xff); };
 
   for (int l = 0; l < L; ++l) {
     const bool active = group == (l & 1);
@@ -243,113 +310,135 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
     const int K = Ld.K, N = Ld.N, r = Ld.r, G = Ld.G;
     const float s = l == 0 ? s0[0] : 1.0f / 127.0f;
 
-    // ---- 0. wait for the producers of y_{l-1}[0:K]; their done words carry
-    //         the absmax of their rows below K, so the scale comes for free
-    if (active && l > 0 && wave == 0) {
-      const int Rp = (layers[l - 1].N + nwg - 1) / nwg;
-      const int P = min(nwg, (K + Rp - 1) / Rp);
-      const uint64_t* dn = done_ll + (int64_t)(l - 1) * nwg * kPad;
-      // up to 4 producers per lane (nwg <= 256), all polled together
-      uint32_t am = 0, need = 0;
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
-        if (lane + 64 * t < P) need |= 1u << t;
-      long spins = 0;
-      while (need) {
-        uint64_t wd[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-          if (need & (1u << t)) wd[t] = ll_load(dn + (lane + 64 * t) * kPad);
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-          if ((need & (1u << t)) && (uint32_t)(wd[t] >> 32) == tag_of(l - 1)) {
-            am = max(am, (uint32_t)wd[t]);
-            need &= ~(1u << t);
+    // ---- 0. the active group relays this workgroup's slice of
+    //         y_{l-1}[0:K] into the XCD's copy; then every thread loads its
+    //         A bytes and polls its words of the copy (columns tid + kCT*i)
+    //         until all carry tag(l-1); their absmax is reduced into LDS
+    int32_t av[kAccRows][kCols];
+    uint32_t yv[kCols];
+    if (l > 0) {
+      const int64_t prev = layers[l - 1].y_off;
+      const uint32_t tag = tag_of(l - 1);
+      if (active) {
+        const int slice = (K + nx - 1) / nx;
+        const int k1 = min(K, (rho + 1) * slice);
+        for (int k = rho * slice + gt; k < k1; k += kGT) {
+          uint64_t wd;
+          if (!poll_ll(ex.y_ll + prev + k, tag, wd, status, kStY)) {
+            abort_ = 1;
+            break;
           }
-        if (need) {
+          xcd_store(y_rel + prev + k, wd);
+        }
+      }
+      if (rho < r) load_a_cols(Ld, tid, rho, nx, av);
+      uint32_t pend = 0;
+#pragma unroll
+      for (int i = 0; i < kCols; ++i)
+        if (tid + i * kCT < K) pend |= 1u << i;
+      long spins = 0;
+      uint32_t m = 0;
+      while (pend) {
+        uint64_t wd[kCols];
+#pragma unroll
+        for (int i = 0; i < kCols; ++i)
+          if (pend & (1u << i)) wd[i] = xcd_load(rs_y, (uint32_t)(prev + tid + i * kCT));
+#pragma unroll
+        for (int i = 0; i < kCols; ++i)
+          if ((pend & (1u << i)) && (uint32_t)(wd[i] >> 32) == tag) {
+            yv[i] = (uint32_t)wd[i];
+            m = max(m, yv[i] & 0x7fffffffu);
+            pend &= ~(1u << i);
+          }
+        if (pend) {
           if (++spins > kSpinLimit) {
-            atomicOr(status, 1u);
+            atomicOr(status, kStY);
             abort_ = 1;
             break;
           }
           __builtin_amdgcn_s_sleep(1);
         }
       }
-      am = wave_max_bits(am);
-      if (lane == 0) {
-        const float a = __uint_as_float(am);
-        zero_lds = a < FLT_MIN;
-        inv_lds = a < FLT_MIN ? 0.0f : 127.0f / a;
-      }
+      m = wave_max_bits_u(m);
+      if (lane == 0) __hip_atomic_fetch_max(&ymax_lds, m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    } else if (rho < r) {
+      load_a_cols(Ld, tid, rho, nx, av);
     }
     __syncthreads();  // B0
     if (abort_) return;
 
-    // ---- 1. codes (column gt + kGT*i), LoRA down row j = wg, bit-planes ---
-    int q[kPollVals];
-    if (active) {
-      if (l == 0) {
+    // ---- 1. codes, LoRA down rows, bit-planes: all 16 waves, columns
+    //         tid + kCT*i ----------------------------------------------------
+    int q[kCols];
+    if (l == 0) {
 #pragma unroll
-        for (int i = 0; i < kPollVals; ++i) {
-          const int k = gt + i * kGT;
-          const int c = gload1s(q0 + (k < K ? k : 0));
-          q[i] = k < K ? c : 0;
-        }
-      } else {
-        const float inv = inv_lds;
-        const bool zero = zero_lds;
-        const uint64_t* src = y_ll + layers[l - 1].y_off;
-        const uint32_t tag = tag_of(l - 1);
-        uint64_t wd[kPollVals];
-#pragma unroll
-        for (int i = 0; i < kPollVals; ++i)
-          wd[i] = gt + i * kGT < K ? ll_load_cached(src + gt + i * kGT) : ((uint64_t)tag << 32);
-#pragma unroll
-        for (int i = 0; i < kPollVals; ++i) {
-          // normally valid on the first read (its producer's done word was
-          // seen); a word whose store is not visible yet is polled again
-          if ((uint32_t)(wd[i] >> 32) != tag && !poll_ll(src + gt + i * kGT, tag, wd[i], status, 4u))
-            abort_ = 1;
-          q[i] = (zero || gt + i * kGT >= K) ? 0 : (int)code(__uint_as_float((uint32_t)wd[i]), inv);
-        }
+      for (int i = 0; i < kCols; ++i) {
+        const int k = tid + i * kCT;
+        const int c = gload1s(q0 + (k < K ? k : 0));
+        q[i] = k < K ? c : 0;
       }
-      if (wg < r) {  // acc_a[wg]: per-wave partials summed in LDS, last wave publishes
-        int acc = 0;
+    } else {
+      const float a = __uint_as_float(ymax_lds);
+      const bool zero = a < FLT_MIN;
+      const float inv = zero ? 0.0f : 127.0f / a;
 #pragma unroll
-        for (int i = 0; i < kPollVals; ++i) acc += pf.a[i] * q[i];
-        acc = wave_sum(acc);
-        if (lane == 0) {
-          dot_part[wave] = acc;
-          const int old = __hip_atomic_fetch_add(&cnt_dot, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
-          if (old == kGW - 1) {
-            int tot = 0;
+      for (int i = 0; i < kCols; ++i) q[i] = (zero || tid + i * kCT >= K) ? 0 : code(__uint_as_float(yv[i]), inv);
+    }
+    if (rho < r) {  // acc_a rows rho + nx*t: per-wave partials in LDS, the last wave publishes
+      int acc[kAccRows];
 #pragma unroll
-            for (int w = 0; w < kGW; ++w) tot += __hip_atomic_load(&dot_part[w], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-            ll_store(acc_ll + ((int64_t)l * dfssm::kMaxRank + wg) * kPad, tag_of(l), (uint32_t)tot);
-            cnt_dot = 0;
-          }
-        }
+      for (int t = 0; t < kAccRows; ++t) {
+        acc[t] = 0;
+#pragma unroll
+        for (int i = 0; i < kCols; ++i) acc[t] += av[t][i] * q[i];
+        acc[t] = wave_sum_u(acc[t]);
       }
-      // wave `wave` holds columns kGT*i + 64*wave + lane: one ballot per plane
+      if (lane == 0) {
 #pragma unroll
-      for (int i = 0; i < kPollVals; ++i) {
-        if (i * kGT < K) {  // uniform
-          uint64_t mk[8];
+        for (int t = 0; t < kAccRows; ++t) dot_part[t][wave16] = acc[t];
+        const int old = __hip_atomic_fetch_add(&cnt_dot, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (old == 2 * kGW - 1) {
 #pragma unroll
-          for (int b = 0; b < 8; ++b) mk[b] = __ballot((q[i] >> b) & 1);
-          if (lane < 16) {
-            const int b = lane >> 1, h = lane & 1;
-            uint64_t m = mk[0];
+          for (int t = 0; t < kAccRows; ++t) {
+            const int j = rho + nx * t;
+            if (j < r) {
+              int tot = 0;
 #pragma unroll
-            for (int t = 1; t < 8; ++t) m = (b == t) ? mk[t] : m;
-            const int word = (i * kGT + wave * 64) / 32 + h;
-            reinterpret_cast<uint32_t*>(pl_lds)[((word >> 2) * 8 + b) * 4 + (word & 3)] = (uint32_t)(m >> (32 * h));
+              for (int w = 0; w < 2 * kGW; ++w)
+                tot += __hip_atomic_load(&dot_part[t][w], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+              xcd_store(acc_rel + (int64_t)l * dfssm::kMaxRank + j, ((uint64_t)tag_of(l) << 32) | (uint32_t)tot);
+            }
           }
+          cnt_dot = 0;
         }
       }
     }
+    // wave16 holds columns kCT*i + 64*wave16 + lane: one ballot per plane
+    // gives two plane words, written by lane 0 as one 8-byte store
+    {
+      int qs = 0;
+#pragma unroll
+      for (int i = 0; i < kCols; ++i) {
+        if (i * kCT < K) {  // uniform
+          qs += q[i];
+          uint64_t mk[8];
+#pragma unroll
+          for (int b = 0; b < 8; ++b) mk[b] = __ballot((q[i] >> b) & 1);
+          if (lane == 0) {
+            const int word = (i * kCT + wave16 * 64) / 32;  // even
+#pragma unroll
+            for (int b = 0; b < 8; ++b)
+              *reinterpret_cast<uint64_t*>(reinterpret_cast<uint32_t*>(pl_lds) + ((word >> 2) * 8 + b) * 4 +
+                                           (word & 3)) = mk[b];
+          }
+        }
+      }
+      qs = wave_sum_u(qs);
+      if (lane == 0) __hip_atomic_fetch_add(&sumq_lds, qs, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
     __syncthreads();  // B2
     if (abort_) return;
+    if (tid == 0) ymax_lds = 0;  // every read of it came before B2
 
     // ---- 2. scaffold GEMV on the prefetched rows; collect acc_a -----------
     const int RW = 64 / G;
@@ -358,18 +447,16 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
     const int g = lane & (G - 1);
     int part[kMaxSteps];
     if (active) {
-      // one bit-plane at a time: weight c_b = 2^b (b < 7), -128 (b = 7)
+      // one bit-plane at a time: weight c_b = 2^b (b < 7), -128 (b = 7);
+      // acc_s = 2 * sum_{bit=1} Q - sum Q
       const int C = K >> 7;
-      int qpart = 0;
+      const int sq = sumq_lds;
       int dsum[kMaxSteps];
 #pragma unroll
       for (int st = 0; st < kMaxSteps; ++st) dsum[st] = 0;
 #pragma unroll
       for (int b = 0; b < 8; ++b) {
         const uint4 Pb = g < C ? pl_lds[g * 8 + b] : make_uint4(0, 0, 0, 0);
-        const int qc = __builtin_popcount(Pb.x) + __builtin_popcount(Pb.y) + __builtin_popcount(Pb.z) +
-                       __builtin_popcount(Pb.w);
-        qpart += b < 7 ? (qc << b) : -(qc << 7);
 #pragma unroll
         for (int st = 0; st < kMaxSteps; ++st) {
           const uint4 w = pf.w[st];
@@ -380,22 +467,32 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
       }
 #pragma unroll
       for (int st = 0; st < kMaxSteps; ++st)
-        part[st] = st < steps ? group_sum(2 * dsum[st] - qpart, G) : 0;
+        part[st] = st < steps ? 2 * group_sum(dsum[st], G) - sq : 0;
       if (gt < r) {
+        const uint32_t tag = tag_of(l);
+        const uint32_t word = (uint32_t)(l * dfssm::kMaxRank + gt);
         uint64_t wd;
-        if (!poll_ll(acc_ll + ((int64_t)l * dfssm::kMaxRank + gt) * kPad, tag_of(l), wd, status, 2u)) abort_ = 1;
+        long spins = 0;
+        while ((uint32_t)((wd = xcd_load(rs_acc, word)) >> 32) != tag) {
+          if (++spins > kSpinLimit) {
+            atomicOr(status, kStAcc);
+            abort_ = 1;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+        }
         reinterpret_cast<int32_t*>(acc_lds)[gt] = (int32_t)(uint32_t)wd;
       }
     }
     __syncthreads();  // B3
     if (abort_) return;
+    if (tid == 0) sumq_lds = 0;  // every read of it came before B3
 
     // ---- 3. LoRA up-projection, epilogue, publish; prefetch linear l+2 ----
     if (active) {
       const int r4 = (r + 3) >> 2;
       const int grp = lane / G;
       const int n0 = wg * R, n1 = min(N, n0 + R);
-      const int Knext = l + 1 < L ? layers[l + 1].K : 0;
       // limbs of acc_a[4g .. 4g+3], packed per limb (j >= r read as 0)
       uint32_t lb0 = 0, lb1 = 0, lb2 = 0, lb3 = 0;
       if (r > 0 && g < r4) {
@@ -411,7 +508,6 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
           lb3 |= (uint32_t)(uint8_t)d[3] << (8 * e);
         }
       }
-      uint32_t ymax = 0;  // |y| of this lane's rows below Knext, as bits
 #pragma unroll
       for (int st = 0; st < kMaxSteps; ++st) {
         if (st >= steps) break;
@@ -424,22 +520,8 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
         const int n = n0 + st * kGW * RW + wave * RW + grp;
         if (g == 0 && n < n1) {
           const float y = dfssm_dev::epilogue(s, pf.al[st], pf.be[st], part[st], ehi, elo, r > 0);
-          ll_store(y_ll + Ld.y_off + n, tag_of(l), __float_as_uint(y));
+          ll_store(ex.y_ll + Ld.y_off + n, tag_of(l), __float_as_uint(y));
           y_all[Ld.y_off + n] = y;
-          if (n < Knext) ymax = max(ymax, __float_as_uint(fabsf(y)));
-        }
-      }
-      if (l + 1 < L) {  // done word: last wave to finish publishes the workgroup's max
-        ymax = wave_max_bits(ymax);
-        if (lane == 0) {
-          __hip_atomic_fetch_max(&ymax_lds, ymax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-          const int old = __hip_atomic_fetch_add(&cnt_epi, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
-          if (old == kGW - 1) {
-            const uint32_t m = __hip_atomic_load(&ymax_lds, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-            ll_store(done_ll + ((int64_t)l * nwg + wg) * kPad, tag_of(l), m);
-            ymax_lds = 0;
-            cnt_epi = 0;
-          }
         }
       }
       if (l + 2 < L) prefetch(layers[l + 2], wg, nwg, gt, pf);
@@ -477,13 +559,14 @@ int chain_lanes_per_row(int64_t K) {
   return G;
 }
 
-int chain_grid() { return 256; }  // one workgroup per CU; the done-word poll assumes <= 256
+int chain_grid() { return kMaxGrid; }  // one workgroup per CU
 
 bool chain_persistent_supported(const dfssm_layer* layers, int n_layers, int64_t M, int nwg) {
-  if (M != 1) return false;
+  if (M != 1 || nwg > kMaxGrid) return false;
   for (int l = 0; l < n_layers; ++l) {
     const dfssm_layer& L = layers[l];
-    if (L.K % 128 != 0 || L.K > kChainMaxK || L.r % 4 != 0 || L.r > nwg) return false;
+    if (L.K % 128 != 0 || L.K > kChainMaxK || L.r % 4 != 0) return false;
+    if (L.r > kChainAccRows * kChainWgPerXcd) return false;
     const int G = chain_lanes_per_row(L.K);
     if (L.r / 4 > G) return false;
     const int64_t R = ceil_div(L.N, nwg);
@@ -515,13 +598,12 @@ hipError_t launch_chain_setup(const ChainLayerDev* table_host, ChainLayerDev* ta
 }
 
 hipError_t launch_chain_run(const ChainLayerDev* table_dev, int n_layers, const int8_t* q0, const float* s0,
-                            uint64_t* y_ll, uint64_t* acc_ll, uint64_t* done_ll, float* y_all,
-                            unsigned* status, uint32_t seq, const uint64_t* hash_dev, uint64_t hash,
-                            hipStream_t st) {
+                            const ChainExch& ex, float* y_all, uint32_t seq, const uint64_t* hash_dev,
+                            uint64_t hash, hipStream_t st) {
   int L = n_layers;
-  void* args[] = {(void*)&table_dev, (void*)&L,      (void*)&q0,       (void*)&s0,
-                  (void*)&y_ll,      (void*)&acc_ll, (void*)&done_ll,  (void*)&y_all,
-                  (void*)&status,    (void*)&seq,    (void*)&hash_dev, (void*)&hash};
+  ChainExch e = ex;
+  void* args[] = {(void*)&table_dev, (void*)&L,   (void*)&q0,       (void*)&s0,   (void*)&e,
+                  (void*)&y_all,     (void*)&seq, (void*)&hash_dev, (void*)&hash};
   return hipLaunchCooperativeKernel((const void*)chain_persistent, dim3(chain_grid()), dim3(kCT), args, 0, st);
 }
 

@@ -89,16 +89,37 @@ hipError_t launch_mfma_linear(const int8_t* q, const float* s, int64_t M, int64_
 
 // ---------------------------------------------------------------- chain
 // Largest K the persistent chain kernel takes (its per-thread register
-// staging of the previous output holds K/256 values).
+// staging of the previous output holds K/512 values).
 constexpr int kChainMaxK = 4096;
 // Row steps of one workgroup per linear held in registers, and waves per
 // role group of the persistent kernel.
 constexpr int kChainMaxSteps = 2;
 constexpr int kChainWaves = 8;
+// LoRA down-projection rows one workgroup computes per linear; the chain
+// needs r <= kChainAccRows * (workgroups on the smallest XCD).
+constexpr int kChainAccRows = 2;
+// Workgroups per XCD the host assumes when it accepts a chain (256
+// workgroups dealt to 8 XCDs); the kernel checks the real placement.
+constexpr int kChainWgPerXcd = 32;
+// XCDs (L2 domains) the exchange regions provide for.
+constexpr int kChainXcds = 8;
 // Layer-table entries passed by value per setup launch.
 constexpr int kChainSetupChunk = 48;
-// 64-bit words per padded exchange slot (one 128-byte line).
-constexpr int kChainPad = 16;
+
+// Exchange regions of the persistent chain (all inside the workspace):
+//   y_ll    [ysum]                 every linear's outputs as {tag, value} words
+//   y_rel   [kChainXcds][ysum]     each XCD's relayed copy of y_ll
+//   acc_rel [kChainXcds][L][kMaxRank]  each XCD's acc_a words
+//   xmap    [grid]                 workgroup -> XCD id words
+struct ChainExch {
+  uint64_t* y_ll;
+  uint64_t* y_rel;
+  uint64_t* acc_rel;
+  uint64_t* xmap;
+  unsigned* status;
+  int64_t ysum;
+  int32_t r_max;
+};
 
 // One linear of the persistent chain, as the kernel reads it (device table).
 struct ChainLayerDev {
@@ -122,9 +143,8 @@ hipError_t launch_chain_setup(const ChainLayerDev* table_host, ChainLayerDev* ta
                               hipStream_t st);
 // Cooperative launch of the persistent chain kernel on a prepared workspace.
 hipError_t launch_chain_run(const ChainLayerDev* table_dev, int n_layers, const int8_t* q0, const float* s0,
-                            uint64_t* y_ll, uint64_t* acc_ll, uint64_t* done_ll, float* y_all,
-                            unsigned* status, uint32_t seq, const uint64_t* hash_dev, uint64_t hash,
-                            hipStream_t st);
+                            const ChainExch& ex, float* y_all, uint32_t seq, const uint64_t* hash_dev,
+                            uint64_t hash, hipStream_t st);
 
 }  // namespace dfssm
 
