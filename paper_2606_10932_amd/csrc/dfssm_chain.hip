@@ -213,6 +213,18 @@ __device__ __forceinline__ bool poll_ll(const uint64_t* p, uint32_t tag, uint64_
   }
   return true;
 }
+__device__ __forceinline__ bool poll_xcd(__amdgpu_buffer_rsrc_t rs, uint32_t word, uint32_t tag, uint64_t& wd,
+                                         unsigned* status, unsigned code_bit) {
+  long spins = 0;
+  while ((uint32_t)((wd = xcd_load(rs, word)) >> 32) != tag) {
+    if (++spins > kSpinLimit) {
+      atomicOr(status, code_bit);
+      return false;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
+  return true;
+}
 
 __global__ __launch_bounds__(kCT, 1) void chain_persistent(
     const dfssm::ChainLayerDev* __restrict__ layers, int L, const int8_t* __restrict__ q0,
@@ -443,7 +455,6 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
     // ---- 2. scaffold GEMV on the prefetched rows; collect acc_a -----------
     const int RW = 64 / G;
     const int R = (N + nwg - 1) / nwg;
-    const int steps = (R + kGW * RW - 1) / (kGW * RW);
     const int g = lane & (G - 1);
     int part[kMaxSteps];
     if (active) {
@@ -451,36 +462,29 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
       // acc_s = 2 * sum_{bit=1} Q - sum Q
       const int C = K >> 7;
       const int sq = sumq_lds;
-      int dsum[kMaxSteps];
+      const int n0 = wg * R, n1 = min(N, n0 + R);
 #pragma unroll
-      for (int st = 0; st < kMaxSteps; ++st) dsum[st] = 0;
-#pragma unroll
-      for (int b = 0; b < 8; ++b) {
-        const uint4 Pb = g < C ? pl_lds[g * 8 + b] : make_uint4(0, 0, 0, 0);
-#pragma unroll
-        for (int st = 0; st < kMaxSteps; ++st) {
+      for (int st = 0; st < kMaxSteps; ++st) {
+        part[st] = 0;
+        // uniform per wave: does this wave own rows in step st?
+        if (n0 + st * kGW * RW + wave * RW < n1) {
           const uint4 w = pf.w[st];
-          const int c = __builtin_popcount(w.x & Pb.x) + __builtin_popcount(w.y & Pb.y) +
-                        __builtin_popcount(w.z & Pb.z) + __builtin_popcount(w.w & Pb.w);
-          dsum[st] += b < 7 ? (c << b) : -(c << 7);
+          int dsum = 0;
+#pragma unroll
+          for (int b = 0; b < 8; ++b) {
+            const uint4 Pb = g < C ? pl_lds[g * 8 + b] : make_uint4(0, 0, 0, 0);
+            const int c = __builtin_popcount(w.x & Pb.x) + __builtin_popcount(w.y & Pb.y) +
+                          __builtin_popcount(w.z & Pb.z) + __builtin_popcount(w.w & Pb.w);
+            dsum += b < 7 ? (c << b) : -(c << 7);
+          }
+          part[st] = 2 * group_sum(dsum, G) - sq;
         }
       }
-#pragma unroll
-      for (int st = 0; st < kMaxSteps; ++st)
-        part[st] = st < steps ? 2 * group_sum(dsum[st], G) - sq : 0;
       if (gt < r) {
         const uint32_t tag = tag_of(l);
         const uint32_t word = (uint32_t)(l * dfssm::kMaxRank + gt);
         uint64_t wd;
-        long spins = 0;
-        while ((uint32_t)((wd = xcd_load(rs_acc, word)) >> 32) != tag) {
-          if (++spins > kSpinLimit) {
-            atomicOr(status, kStAcc);
-            abort_ = 1;
-            break;
-          }
-          __builtin_amdgcn_s_sleep(1);
-        }
+        if (!poll_xcd(rs_acc, word, tag, wd, status, kStAcc)) abort_ = 1;
         reinterpret_cast<int32_t*>(acc_lds)[gt] = (int32_t)(uint32_t)wd;
       }
     }
@@ -510,7 +514,7 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
       }
 #pragma unroll
       for (int st = 0; st < kMaxSteps; ++st) {
-        if (st >= steps) break;
+        if (n0 + st * kGW * RW + wave * RW >= n1) break;  // uniform per wave
         int elo = 0, ehi = 0;
         if (r > 0) {
           const uint32_t bw = pf.b[st];
