@@ -34,6 +34,17 @@ __device__ __forceinline__ v4i mfma(v4i a, v4i b, v4i c) {
 
 __device__ __forceinline__ v4i zero4() { return v4i{0, 0, 0, 0}; }
 
+// bits [sh, sh+16) of w -> 16 bytes of {0,1}, byte b of dword t = bit sh+4t+b
+__device__ __forceinline__ v4i expand16_at(uint32_t w, uint32_t sh) {
+  v4i o;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const uint32_t nib = __builtin_amdgcn_ubfe(w, sh + 4 * t, 4);
+    o[t] = (int)((nib * 0x00204081u) & 0x01010101u);
+  }
+  return o;
+}
+
 // 16 sign bits -> 16 bytes of {0,1}, byte b of dword t = bit 4t+b
 __device__ __forceinline__ v4i expand16(uint32_t bits16) {
   v4i o;
@@ -152,21 +163,58 @@ __global__ __launch_bounds__(kThreads) void mfma_lora_down(const int8_t* __restr
 
 // ------------------------------------------------------------ main GEMM
 // Block tile 128 (tokens) x 128 (output rows), 4 waves as 2 x 2 with wave
-// tiles of 64 x 64 (4 x 4 MFMA tiles); 64 K per stage, two LDS stages.  The
-// Q tile is staged with a padded row pitch (80 B) to spread LDS banks; the
-// sign words of the tile (1 KB per stage) are staged raw and expanded by
-// each wave into its B operands.
+// tiles of 64 x 64 (4 x 4 MFMA tiles); 64 K per stage.  The K-loop runs a
+// 4-stage LDS ring filled by direct-to-LDS loads (global_load_lds: no
+// register staging):
+//   Q stage: 128 rows x 64 bytes, the four 16-byte chunks of row r stored
+//            at chunk slot c ^ ((r >> 2) & 3), so the 16 lanes reading one
+//            MFMA operand column hit 16 distinct 4-bank groups;
+//   sign stage: 128 rows x 2 words (64 sign bits per row), expanded to
+//            {0,1} bytes in registers right before use.
+// Each wave issues exactly three loads per stage (two 1 KB Q pieces and
+// one 256-byte sign piece), so "stage ks has landed" is a vector-memory
+// count; past the last stage the issue repeats the last stage's loads (the
+// same bytes into the same slot), which keeps the count uniform.
 constexpr int kBM = 128, kBN = 128, kBK = 64;
-constexpr int kQPitch = kBK + 16;
-// sign-word stage: 2 x 256 rows, so all 256 threads store (rows >= 128 hold
-// masked zeros and are never read): no divergent branch in the K-loop
-constexpr int kWRows = 2 * kBN;
-constexpr int kLdsLoop = 2 * kBM * kQPitch + 2 * kWRows * 2 * 4;
-constexpr int kLdsLora = 4 * kBM * kQPitch + kBN * kQPitch;
+constexpr int kStages = 4;
+constexpr int kLoadsPerStage = 3;
+constexpr int kQStage = kBM * kBK;               // 8 KB
+constexpr int kWStage = kBN * 2 * 4;             // 1 KB
+constexpr int kStageBytes = kQStage + kWStage;
+// epilogue: limbs [4][kBM][64] and B [kBN][64] with the same chunk swizzle,
+// then one transpose buffer of 16 x kYPitch floats per wave
+constexpr int kYPitch = 20;                      // 16 columns + 4: conflict-free both ways
+constexpr int kLdsLoop = kStages * kStageBytes;
+constexpr int kLdsLora = 4 * kBM * kBK + kBN * kBK + 4 * 16 * kYPitch * 4;
 constexpr int kLdsBytes = kLdsLoop > kLdsLora ? kLdsLoop : kLdsLora;
 #ifndef DFSSM_MFMA_OCC
 #define DFSSM_MFMA_OCC 3
 #endif
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Direct-to-LDS loads (gfx950 global_load_lds): each lane's 16 (or 4) bytes
+// land at m0 + 16*lane (4*lane).  Issued as inline assembly so the compiler
+// does not treat every later LDS read as depending on them (it cannot tell
+// the ring slots apart and would wait for all loads); the K-loop orders them
+// itself with DFSSM_WAIT_VMCNT and the barrier.
+// (the address is wave-uniform; readfirstlane puts it in an SGPR for m0)
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(uintptr_t)(const lds_void*)p);
+}
+__device__ __forceinline__ void lds_dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+__device__ __forceinline__ void lds_dma4(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+
+// s_waitcnt with only the vector-memory counter constrained
+#define DFSSM_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(0x0F70 | ((n) & 0xF) | (((n) >> 4) << 14))
+// workgroup barrier that does not drain outstanding direct-to-LDS loads
+// (the compiler's barrier fence would wait for all of them); LDS visibility
+// of the loads is ordered by the DFSSM_WAIT_VMCNT before it
+#define DFSSM_BARRIER() asm volatile("s_barrier" ::: "memory")
 
 template <bool kLoraLds>
 __global__ __launch_bounds__(kThreads, DFSSM_MFMA_OCC) void mfma_scaffold(
@@ -178,12 +226,10 @@ __global__ __launch_bounds__(kThreads, DFSSM_MFMA_OCC) void mfma_scaffold(
   // one LDS buffer, two uses: the K-loop stages (Q tile + sign words, x2),
   // then the LoRA operands of the epilogue (4 limbs x 128 rows + 128 B rows)
   __shared__ __attribute__((aligned(16))) int8_t lds_raw[kLdsBytes];
-  int8_t(*q_lds)[kBM * kQPitch] = reinterpret_cast<int8_t(*)[kBM * kQPitch]>(lds_raw);
-  uint32_t(*w_lds)[kWRows * 2] = reinterpret_cast<uint32_t(*)[kWRows * 2]>(lds_raw + 2 * kBM * kQPitch);
-  int8_t* limb_lds = lds_raw;                       // [4][kBM][kQPitch]
-  int8_t* b_lds = lds_raw + 4 * kBM * kQPitch;      // [kBN][kQPitch]
-  __shared__ float al_lds[kBN], be_lds[kBN], s_lds[kBM];
-  __shared__ int32_t sq_lds[kBM];
+  int8_t* limb_lds = lds_raw;                       // [4][kBM][64], swizzled
+  int8_t* b_lds = lds_raw + 4 * kBM * kBK;          // [kBN][64], swizzled
+  __shared__ __attribute__((aligned(16))) float al_lds[kBN], be_lds[kBN], s_lds[kBM];
+  __shared__ __attribute__((aligned(16))) int32_t sq_lds[kBM];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int row = lane & 15, kg = lane >> 4;
 
@@ -214,45 +260,31 @@ __global__ __launch_bounds__(kThreads, DFSSM_MFMA_OCC) void mfma_scaffold(
   __syncthreads();
 
   // ---- scaffold K-loop ------------------------------------------------------
-  // staging: thread t loads Q row m0 + t/2, bytes (t&1)*32 .. +31 of the
-  // stage; threads t < 128 load the two sign words of row n0 + t
-  const int qr_row = tid >> 1, qr_off = (tid & 1) * 32;
-  const int8_t* qsrc = q + (int64_t)min(m0 + qr_row, M - 1) * K;
-  const bool q_row_ok = m0 + qr_row < M;
-  const uint32_t* wsrc = w_bits + (int64_t)min(n0 + (tid & 127), N - 1) * W;
-  const bool w_row_ok = tid < 128 && n0 + tid < N;
-  // Loads read clamped in-range addresses unconditionally; the masks are
-  // applied when the data is stored to LDS.  Two register stages: the loads
-  // of K-stage ks+2 are issued while stage ks is multiplied and are stored to
-  // LDS only at the end of stage ks+1, so each load has two stages of MFMA
-  // work to arrive.
-  struct Stage {
-    uint4 q0, q1;
-    uint32_t w0, w1, mq, mw0, mw1;
-  };
-  // stage indexes past the last K-stage load the last stage's addresses and
-  // store zeros (all masks off), so the loop below has no branches and the
-  // compiler can count outstanding loads exactly
-  auto gload = [&](Stage& st, int ks) {
-    const int kk = ks * kBK + qr_off;
-    const bool ok = q_row_ok && kk < K;
-    const int kc = ok ? kk : 0;
-    st.q0 = *reinterpret_cast<const uint4*>(qsrc + kc);
-    st.q1 = *reinterpret_cast<const uint4*>(qsrc + kc + 16);
-    st.mq = ok ? ~0u : 0u;
-    const int w0 = 2 * ks;
-    st.w0 = wsrc[w0 < W ? w0 : 0];
-    st.w1 = wsrc[w0 + 1 < W ? w0 + 1 : 0];
-    st.mw0 = (w_row_ok && w0 < W) ? ~0u : 0u;
-    st.mw1 = (w_row_ok && w0 + 1 < W) ? ~0u : 0u;
-  };
-  auto sstore = [&](int buf, const Stage& st) {
-    *reinterpret_cast<uint4*>(&q_lds[buf][qr_row * kQPitch + qr_off]) =
-        make_uint4(st.q0.x & st.mq, st.q0.y & st.mq, st.q0.z & st.mq, st.q0.w & st.mq);
-    *reinterpret_cast<uint4*>(&q_lds[buf][qr_row * kQPitch + qr_off + 16]) =
-        make_uint4(st.q1.x & st.mq, st.q1.y & st.mq, st.q1.z & st.mq, st.q1.w & st.mq);
-    w_lds[buf][tid * 2] = st.w0 & st.mw0;
-    w_lds[buf][tid * 2 + 1] = st.w1 & st.mw1;
+  // loads of stage ks (clamped to the last stage): this wave's Q rows
+  // 32*wave + 16*j + lane/4, slot lane%4 <- chunk (lane%4) ^ ((row >> 2) & 3),
+  // and sign rows 32*wave + lane/2, word lane%2.  Rows past M or N read the
+  // last row (their outputs are never stored); a chunk past K reads the
+  // chunk two before it (its sign bits are masked to zero below).
+  const int8_t* qrow[2];
+  int qchunk[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int rl = 32 * wave + 16 * j + (lane >> 2);
+    qrow[j] = q + (int64_t)min(m0 + rl, M - 1) * K;
+    qchunk[j] = ((lane & 3) ^ ((rl >> 2) & 3)) * 16;
+  }
+  const int wrl = 32 * wave + (lane >> 1);
+  const uint32_t* wrow = w_bits + (int64_t)min(n0 + wrl, N - 1) * W + (lane & 1);
+  auto issue = [&](int ks) {
+    ks = min(ks, nks - 1);
+    int8_t* base = lds_raw + (ks % kStages) * kStageBytes;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      int kk = ks * kBK + qchunk[j];
+      if (kk >= K) kk -= 32;
+      lds_dma16(qrow[j] + kk, lds_addr(base + (32 * wave + 16 * j) * kBK));
+    }
+    lds_dma4(wrow + 2 * ks - ((2 * ks + (lane & 1)) >= W ? 1 : 0), lds_addr(base + kQStage + 32 * wave * 8));
   };
 
   v4i acc[4][4];
@@ -261,41 +293,73 @@ __global__ __launch_bounds__(kThreads, DFSSM_MFMA_OCC) void mfma_scaffold(
 #pragma unroll
     for (int t = 0; t < 4; ++t) acc[i][t] = zero4();
 
-  const int am_off = ((wave >> 1) * 64 + row) * kQPitch + 16 * kg;
+  // operand addresses inside a stage: A tile i is rows 64*(wave>>1) + 16*i +
+  // row (row & 3 and (row >> 2) & 3 are the same for every i)
+  const int am_off = ((wave >> 1) * 64 + row) * kBK + 16 * (kg ^ ((row >> 2) & 3));
   const int bn_off = ((wave & 1) * 64 + row) * 2 + (kg >> 1);
   const int bshift = (kg & 1) * 16;
-  // one K-stage: refill `ld` with stage ks+2, multiply stage ks (LDS buffer
-  // ks & 1), then move stage ks+1 (held in `st`) into the other buffer
-  auto kstep = [&](int ks, Stage& ld, const Stage& st) {
-    const int cur = ks & 1;
-    gload(ld, ks + 2);
-    v4i a[4], b[4];
+  // operands of one stage: 4 A tiles (Q rows) and 4 B tiles (expanded signs)
+  auto read_stage = [&](int ks, v4i (&a)[4], v4i (&b)[4]) {
+    const int8_t* st = lds_raw + (ks % kStages) * kStageBytes;
+    const uint32_t* ws = reinterpret_cast<const uint32_t*>(st + kQStage);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const v4i*>(&q_lds[cur][am_off + 16 * i * kQPitch]);
+    for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const v4i*>(st + am_off + 16 * i * kBK);
+    const bool whole = 2 * ks + 1 < W;  // uniform: only a K tail has a second word past K
 #pragma unroll
-    for (int t = 0; t < 4; ++t) b[t] = expand16((w_lds[cur][bn_off + 32 * t] >> bshift) & 0xffffu);
+    for (int t = 0; t < 4; ++t) {
+      uint32_t w = ws[bn_off + 32 * t];
+      if (!whole && (kg >> 1)) w = 0;  // sign words past K count as 0
+      b[t] = expand16_at(w, bshift);
+    }
+  };
+  // Software pipeline: the MFMAs of stage ks are issued together with the
+  // LDS reads and sign expansion of stage ks+1 (independent instructions,
+  // so the matrix core and the vector ALU work at the same time).  The LDS
+  // ring runs three stages ahead of the multiply.
+  v4i a0[4], b0[4], a1[4], b1[4];
+  auto step = [&](int ks, const v4i (&ac)[4], const v4i (&bc)[4], v4i (&an)[4], v4i (&bn)[4]) {
+    // stages ks+1 and ks+2 are in flight here: leaving only stage ks+2's
+    // loads outstanding means this wave's loads of stage ks+1 have landed
+    DFSSM_WAIT_VMCNT(kLoadsPerStage);
+    DFSSM_BARRIER();  // so have every wave's; stage ks-1 is no longer read
+    issue(ks + 3);
+    read_stage(ks + 1, an, bn);  // past the end: clamped loads, unused
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int t = 0; t < 4; ++t) acc[i][t] = mfma(a[i], b[t], acc[i][t]);
-    sstore(cur ^ 1, st);
-    __syncthreads();
+      for (int t = 0; t < 4; ++t) acc[i][t] = mfma(ac[i], bc[t], acc[i][t]);
+    // interleave: after the LDS reads, one MFMA then three vector ALU ops
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // DS reads
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // VALU
+    }
   };
-  Stage s0, s1;
-  gload(s0, 0);
-  gload(s1, 1);
-  sstore(0, s0);
-  __syncthreads();
-  for (int ks = 0; ks < nks; ks += 2) {  // an odd count runs one zero stage
-    kstep(ks, s0, s1);      // stage ks+1 lives in s1, ks+2 -> s0
-    kstep(ks + 1, s1, s0);  // stage ks+2 lives in s0, ks+3 -> s1
+  issue(0);
+  issue(1);
+  issue(2);
+  DFSSM_WAIT_VMCNT(2 * kLoadsPerStage);  // stage 0 landed, stages 1 and 2 in flight
+  DFSSM_BARRIER();
+  read_stage(0, a0, b0);
+  int ks = 0;
+  for (; ks + 1 < nks; ks += 2) {
+    step(ks, a0, b0, a1, b1);
+    step(ks + 1, a1, b1, a0, b0);
   }
+  if (ks < nks) step(ks, a0, b0, a1, b1);
+  // the ring is reused below: drain the loads still in flight and wait for
+  // every wave to finish its last stage
+  DFSSM_WAIT_VMCNT(0);
+  __syncthreads();
 
   // ---- epilogue, one n-subtile (16 output rows) at a time: the LoRA term
   //      from four limb MFMAs (exact int64 acc_b = E_lo + 65536*E_hi) on
   //      operands staged in LDS, then acc_s = 2*D - sum Q and
-  //      y = s*(alpha*fs + beta*fb)
+  //      y = s*(alpha*fs + beta*fb); y leaves through a per-wave LDS
+  //      transpose as 16-byte row pieces
   const bool baligned = (r % 16) == 0;
+  auto swz = [](int rr) { return (rr >> 2) & 3; };
   // stage 64 LoRA columns [j0, j0+64): limbs of the tile's rows, B of its
   // columns; 10 x 16 bytes per thread, all loads issued before the stores
   auto stage_lora = [&](int j0) {
@@ -320,7 +384,7 @@ __global__ __launch_bounds__(kThreads, DFSSM_MFMA_OCC) void mfma_scaffold(
       const int idx = tid + u * kThreads;
       const int limb = idx >> 9, ml = (idx >> 2) & 127, c = idx & 3;
       const uint32_t mk = m0 + ml < M ? ~0u : 0u;
-      *reinterpret_cast<uint4*>(limb_lds + (limb * kBM + ml) * kQPitch + 16 * c) =
+      *reinterpret_cast<uint4*>(limb_lds + (limb * kBM + ml) * kBK + 16 * (c ^ swz(ml))) =
           make_uint4(lv[u].x & mk, lv[u].y & mk, lv[u].z & mk, lv[u].w & mk);
     }
 #pragma unroll
@@ -328,14 +392,17 @@ __global__ __launch_bounds__(kThreads, DFSSM_MFMA_OCC) void mfma_scaffold(
       const int idx = tid + u * kThreads;
       const int nl = idx >> 2, c = idx & 3;
       const uint32_t mk = n0 + nl < N ? ~0u : 0u;
-      *reinterpret_cast<uint4*>(b_lds + nl * kQPitch + 16 * c) =
+      *reinterpret_cast<uint4*>(b_lds + nl * kBK + 16 * (c ^ swz(nl))) =
           make_uint4(bv[u].x & mk, bv[u].y & mk, bv[u].z & mk, bv[u].w & mk);
     }
   };
   if (kLoraLds && r > 0) {
-    stage_lora(0);  // the K-loop's last barrier has released the buffer
+    stage_lora(0);
     __syncthreads();
   }
+  float* ybuf = reinterpret_cast<float*>(lds_raw + 4 * kBM * kBK + kBN * kBK) + wave * 16 * kYPitch;
+  const int sw = 16 * (kg ^ swz(row));
+  const bool nvec = (N & 3) == 0;  // rows of y are 16-byte aligned
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     v4i ehi[4], elo[4];
@@ -348,11 +415,11 @@ __global__ __launch_bounds__(kThreads, DFSSM_MFMA_OCC) void mfma_scaffold(
       for (int pass = 0; pass < 4; ++pass) {  // limbs 3, 2, 1, 0
         const int limb = 3 - pass;
         if constexpr (kLoraLds) {  // rank <= 64: one chunk, operands in LDS
-          const v4i bl = *reinterpret_cast<const v4i*>(b_lds + nl * kQPitch + 16 * kg);
+          const v4i bl = *reinterpret_cast<const v4i*>(b_lds + nl * kBK + sw);
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int ml = (wave >> 1) * 64 + 16 * i + row;
-            const v4i al = *reinterpret_cast<const v4i*>(limb_lds + (limb * kBM + ml) * kQPitch + 16 * kg);
+            const v4i al = *reinterpret_cast<const v4i*>(limb_lds + (limb * kBM + ml) * kBK + sw);
             if (limb >= 2)
               ehi[i] = mfma(al, bl, ehi[i]);
             else
@@ -388,21 +455,49 @@ __global__ __launch_bounds__(kThreads, DFSSM_MFMA_OCC) void mfma_scaffold(
         }
       }
     }
-    if (n >= N) continue;
     const float al = al_lds[nl], be = be_lds[nl];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i) {
+      const int mlb = (wave >> 1) * 64 + 16 * i + 4 * kg;  // this lane's rows mlb + v
+      const float4 s4 = *reinterpret_cast<const float4*>(&s_lds[mlb]);
+      const int4 q4 = *reinterpret_cast<const int4*>(&sq_lds[mlb]);
+      const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
+      const int32_t qv[4] = {q4.x, q4.y, q4.z, q4.w};
+      float yv[4];
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int ml = (wave >> 1) * 64 + 16 * i + 4 * kg + v;
-        const int m = m0 + ml;
-        if (m >= M) continue;
-        const int32_t as = 2 * acc[i][t][v] - sq_lds[ml];
+        const int32_t as = 2 * acc[i][t][v] - qv[v];
         const int32_t hi = ehi[i][v], lo = elo[i][v];
-        if (y) y[(int64_t)m * N + n] = dfssm_dev::epilogue(s_lds[ml], al, be, as, hi, lo, r > 0);
-        if (acc_s_out) acc_s_out[(int64_t)m * N + n] = as;
-        if (acc_b_out) acc_b_out[(int64_t)m * N + n] = r > 0 ? (int64_t)lo + ((int64_t)hi << 16) : 0;
+        yv[v] = dfssm_dev::epilogue(sv[v], al, be, as, hi, lo, r > 0);
+        const int m = m0 + mlb + v;
+        if (m < M && n < N) {
+          if (acc_s_out) acc_s_out[(int64_t)m * N + n] = as;
+          if (acc_b_out) acc_b_out[(int64_t)m * N + n] = r > 0 ? (int64_t)lo + ((int64_t)hi << 16) : 0;
+        }
       }
+      if (y) {
+        // [row 4*kg + v][column row] in, [row lane/4][columns 4*(lane%4)..+3]
+        // out; the buffer is this wave's own and LDS instructions of one
+        // wave complete in order, so no barrier is involved
+#pragma unroll
+        for (int v = 0; v < 4; ++v) ybuf[(4 * kg + v) * kYPitch + row] = yv[v];
+        const int mr = lane >> 2, nc = 4 * (lane & 3);
+        const float4 o = *reinterpret_cast<const float4*>(&ybuf[mr * kYPitch + nc]);
+        const int m = m0 + (wave >> 1) * 64 + 16 * i + mr;
+        const int nn = n0 + (wave & 1) * 64 + 16 * t + nc;
+        if (m < M) {
+          float* dst = y + (int64_t)m * N + nn;
+          if (nvec && nn + 3 < N) {
+            *reinterpret_cast<float4*>(dst) = o;
+          } else {
+            const float ov[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (nn + e < N) dst[e] = ov[e];
+          }
+        }
+      }
+    }
   }
 }
 
