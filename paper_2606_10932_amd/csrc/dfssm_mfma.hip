@@ -75,8 +75,9 @@ __device__ __forceinline__ v4i load16_guarded(const int8_t* row, int start, int 
 }
 
 // ------------------------------------------------------------ lora_down
-// A block owns 16 tokens; its 4 waves split the K steps into quarters and
-// reduce their partial sums in LDS.  Loads are issued 4 K-steps at a time.
+// A block owns 16 tokens x 16 ranks (one MFMA tile; blockIdx.y is the rank
+// tile, covering rp); its 4 waves split the K steps into quarters and reduce
+// their partial sums in LDS.  Loads are issued kLdBatch K-steps at a time.
 constexpr int kLdBatch = 4;
 
 __global__ __launch_bounds__(kThreads) void mfma_lora_down(const int8_t* __restrict__ q, int M, int K,
@@ -84,81 +85,72 @@ __global__ __launch_bounds__(kThreads) void mfma_lora_down(const int8_t* __restr
                                                            int32_t* __restrict__ acc_a,
                                                            int8_t* __restrict__ limbs,
                                                            int32_t* __restrict__ sumq) {
-  __shared__ int32_t part[4][16 * 64];
+  __shared__ int32_t part[4][16 * 16];
   __shared__ int32_t qpart[4][16];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int row = lane & 15, kg = lane >> 4;
-  const int m0 = blockIdx.x * 16;
-  const int m = m0 + row;
-  const bool m_ok = m < M;
+  const int m0 = blockIdx.x * 16, j0 = blockIdx.y * 16;
+  const bool first = blockIdx.y == 0;  // the rank tile that also sums Q
+  const int m = m0 + row, j = j0 + row;
+  const bool m_ok = m < M, j_ok = j < r;
   const int8_t* qrow = q + (int64_t)(m_ok ? m : 0) * K;
+  const int8_t* arow = A + (int64_t)(j_ok ? j : 0) * K;
   const int nks = (K + 63) / 64;
   const int per = (nks + 3) / 4;
   const int ks0 = wave * per, ks1 = min(nks, ks0 + per);
 
-  for (int jt = 0; jt < rp / 64; ++jt) {
-    v4i acc[4] = {zero4(), zero4(), zero4(), zero4()};
-    int qs = 0;
-    for (int kb = ks0; kb < ks1; kb += kLdBatch) {
-      // all loads of the batch from clamped addresses first, masks after
-      v4i a[kLdBatch], b[kLdBatch][4];
-      int ma[kLdBatch], mb[kLdBatch][4];
+  v4i acc = zero4();
+  int qs = 0;
+  for (int kb = ks0; kb < ks1; kb += kLdBatch) {
+    // all loads of the batch from clamped addresses first, masks after
+    v4i a[kLdBatch], b[kLdBatch];
+    int ma[kLdBatch], mb[kLdBatch];
 #pragma unroll
-      for (int u = 0; u < kLdBatch; ++u) {
-        const int kk = (kb + u) * 64 + 16 * kg;
-        const bool kok = kb + u < ks1 && kk < K;
-        const int kc = kok ? kk : 0;
-        a[u] = load16(qrow + kc);
-        ma[u] = (m_ok && kok) ? -1 : 0;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const int j = jt * 64 + 16 * t + row;
-          b[u][t] = r > 0 ? load16(A + (int64_t)(j < r ? j : 0) * K + kc) : zero4();
-          mb[u][t] = (j < r && kok) ? -1 : 0;
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < kLdBatch; ++u) {
-        a[u] &= ma[u];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) b[u][t] &= mb[u][t];
-      }
-#pragma unroll
-      for (int u = 0; u < kLdBatch; ++u) {
-        if (jt == 0) {
-#pragma unroll
-          for (int t = 0; t < 4; ++t) qs = __builtin_amdgcn_sdot4(a[u][t], 0x01010101, qs, false);
-        }
-#pragma unroll
-        for (int t = 0; t < 4; ++t) acc[t] = mfma(a[u], b[u][t], acc[t]);
-      }
+    for (int u = 0; u < kLdBatch; ++u) {
+      const int kk = (kb + u) * 64 + 16 * kg;
+      const bool kok = kb + u < ks1 && kk < K;
+      const int kc = kok ? kk : 0;
+      a[u] = load16(qrow + kc);
+      ma[u] = (m_ok && kok) ? -1 : 0;
+      b[u] = r > 0 ? load16(arow + kc) : zero4();
+      mb[u] = (j_ok && kok) ? -1 : 0;
     }
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
+    for (int u = 0; u < kLdBatch; ++u) {
+      a[u] &= ma[u];
+      b[u] &= mb[u];
+      if (first) {
 #pragma unroll
-      for (int v = 0; v < 4; ++v) part[wave][(4 * kg + v) * 64 + 16 * t + row] = acc[t][v];
-    if (jt == 0) {
-      qs += __shfl_xor(qs, 16, 64);
-      qs += __shfl_xor(qs, 32, 64);
-      if (kg == 0) qpart[wave][row] = qs;
+        for (int t = 0; t < 4; ++t) qs = __builtin_amdgcn_sdot4(a[u][t], 0x01010101, qs, false);
+      }
+      acc = mfma(a[u], b[u], acc);
     }
-    __syncthreads();
-    for (int i = threadIdx.x; i < 16 * 64; i += kThreads) {
-      const int mi = i >> 6, ji = i & 63;
-      const int mm = m0 + mi, j = jt * 64 + ji;
-      if (mm >= M) continue;
+  }
+  // D[token 4*kg + v][rank row]
+#pragma unroll
+  for (int v = 0; v < 4; ++v) part[wave][(4 * kg + v) * 16 + row] = acc[v];
+  if (first) {
+    qs += __shfl_xor(qs, 16, 64);
+    qs += __shfl_xor(qs, 32, 64);
+    if (kg == 0) qpart[wave][row] = qs;
+  }
+  __syncthreads();
+  {
+    const int i = threadIdx.x;  // 256 threads = 16 tokens x 16 ranks
+    const int mi = i >> 4, ji = i & 15;
+    const int mm = m0 + mi, jj = j0 + ji;
+    if (mm < M) {
       const int32_t val = part[0][i] + part[1][i] + part[2][i] + part[3][i];
       int8_t d[4];
-      dfssm_dev::split_limbs(j < r ? val : 0, d);
+      dfssm_dev::split_limbs(jj < r ? val : 0, d);
 #pragma unroll
-      for (int l = 0; l < 4; ++l) limbs[((int64_t)l * M + mm) * rp + j] = d[l];
-      if (j < r) acc_a[(int64_t)mm * r + j] = val;
+      for (int l = 0; l < 4; ++l) limbs[((int64_t)l * M + mm) * rp + jj] = d[l];
+      if (jj < r) acc_a[(int64_t)mm * r + jj] = val;
     }
-    if (jt == 0 && threadIdx.x < 16 && m0 + threadIdx.x < M)
-      sumq[m0 + threadIdx.x] = qpart[0][threadIdx.x] + qpart[1][threadIdx.x] + qpart[2][threadIdx.x] +
-                               qpart[3][threadIdx.x];
-    __syncthreads();
   }
+  if (first && threadIdx.x < 16 && m0 + threadIdx.x < M)
+    sumq[m0 + threadIdx.x] = qpart[0][threadIdx.x] + qpart[1][threadIdx.x] + qpart[2][threadIdx.x] +
+                             qpart[3][threadIdx.x];
 }
 
 // ------------------------------------------------------------ main GEMM
@@ -512,7 +504,7 @@ hipError_t launch_mfma_linear(const int8_t* q, const float* s, int64_t M, int64_
                               const LinearWorkspace& ws, hipStream_t st) {
   if (M == 0 || N == 0) return hipSuccess;
   const int rp = (int)rank_padded(r);
-  mfma_lora_down<<<dim3((unsigned)ceil_div(M, 16)), dim3(kThreads), 0, st>>>(
+  mfma_lora_down<<<dim3((unsigned)ceil_div(M, 16), (unsigned)(rp / 16)), dim3(kThreads), 0, st>>>(
       q, (int)M, (int)K, (int)r, rp, A, ws.acc_a, ws.limbs, ws.sumq);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
