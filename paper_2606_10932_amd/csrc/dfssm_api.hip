@@ -259,7 +259,9 @@ static uint64_t chain_table(const dfssm_layer* layers, int n_layers,
                                     (int32_t)L.K,
                                     (int32_t)L.N,
                                     (int32_t)L.r,
-                                    dfssm::chain_lanes_per_row(L.K),
+                                    __builtin_ctz((unsigned)dfssm::chain_lanes_per_row(L.K)),
+                                    (int32_t)dfssm::ceil_div(L.N, dfssm::chain_grid()),
+                                    0,
                                     off};
     off += L.N;
   }

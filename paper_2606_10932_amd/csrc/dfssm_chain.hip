@@ -29,16 +29,20 @@
 //        rho computes acc_a[j] for j = rho + n_x*t (t < kChainAccRows) and
 //        stores it into x's region, so acc_a never crosses an XCD.
 //  * A workgroup is two groups of 8 waves that alternate roles: while one
-//    group computes linear l, the other holds (in its own registers) the
-//    weights of linear l+1 it loaded during linear l-1.  So the
-//    latency-critical waits (which wait for all of a wave's outstanding
-//    loads) never wait behind a weight prefetch.
-//  * Per linear, the active group: relays its slice; polls its words of
-//    y_{l-1}[0:K_l], reducing their absmax on the way -> Q (the quantiser's
-//    fp32 decisions) -> bit-planes in LDS and its acc_a rows; the popcount
-//    GEMV on the workgroup's rows; collects the r acc_a words of its XCD;
-//    LoRA up-projection and epilogue; stores its y rows; then prefetches
-//    linear l+2.
+//    group computes linear l, the other loads the weights of linear l+1
+//    into its own registers, once the bit-planes of linear l are built.  A
+//    wave's loads complete in order, so a latency-critical wait (a poll)
+//    never sits behind a weight load issued shortly before it.
+//  * Per linear: the active group relays its slice; all 16 waves poll their
+//    words of y_{l-1}[0:K_l], reducing their absmax on the way -> Q (the
+//    quantiser's fp32 decisions) -> bit-planes in LDS (ballots, gathered
+//    with v_writelane) and the workgroup's acc_a rows.  Then the active
+//    group runs the popcount GEMV on the workgroup's rows, its first wave
+//    collects the r acc_a words of the XCD and splits them into limbs in
+//    LDS, and the group does the LoRA up-projection and epilogue and stores
+//    its y rows.
+//  * Row-split constants come precomputed in the layer table, and the loop
+//    index is kept uniform, so per-linear set-up runs on the scalar unit.
 //  * Every wait is bounded: on time-out the workgroup records an error in
 //    the status word and leaves, so the grid always drains.
 //  * The layer table lives in the workspace, written by a setup launch
@@ -57,6 +61,7 @@ constexpr int kGW = kGT / 64;         // waves per group
 static_assert(kGW == dfssm::kChainWaves, "waves per role group");
 constexpr int kMaxSteps = dfssm::kChainMaxSteps;
 constexpr int kCols = dfssm::kChainMaxK / kCT;  // previous-output columns per thread
+constexpr int kChunks = dfssm::kChainMaxK / 128;  // 128-column chunks of the bit-planes
 constexpr int kAccRows = dfssm::kChainAccRows;
 constexpr int kXcds = dfssm::kChainXcds;
 constexpr int kMaxGrid = 256;
@@ -107,14 +112,24 @@ __device__ __forceinline__ int dpp_sum16(int v) {
 }
 
 // Sum over aligned groups of G lanes (G = 8..64), result in every lane of
-// the group: DPP butterflies inside a 16-lane row, lane swaps across rows.
+// the group: DPP butterflies inside a 16-lane row; across rows, gfx950's
+// permlane swaps.  v_permlane16_swap of a value with itself leaves rows
+// (0,0,2,2) in one result and (1,1,3,3) in the other, so their sum is the
+// 32-lane half's total in every lane; v_permlane32_swap does the same for
+// the two halves.
 __device__ __forceinline__ int group_sum(int v, int G) {
   v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
   v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
   v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);
   if (G >= 16) v += __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);
-  if (G >= 32) v += __shfl_xor(v, 16, 64);
-  if (G >= 64) v += __shfl_xor(v, 32, 64);
+  if (G >= 32) {
+    const auto p = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v, false, false);
+    v = (int)(p[0] + p[1]);
+  }
+  if (G >= 64) {
+    const auto p = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+    v = (int)(p[0] + p[1]);
+  }
   return v;
 }
 
@@ -138,6 +153,41 @@ __device__ __forceinline__ uint32_t wave_max_bits_u(uint32_t v) {
   v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false));
   return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
+
+// Bit-planes of the codes c of column block I (one code per lane): plane
+// b's ballot gives two 32-column words, written into lanes 16*I + 2*b and
+// 16*I + 2*b + 1 of pw.  v_writelane takes the ballot from a scalar register
+// and ignores EXEC; it does not wait for a scalar register that a VALU
+// instruction (the ballot's compare) has just written, so each block of
+// writes starts with 5 wait states (s_nop 4): without them it can read the
+// previous value.
+#define DFSSM_WL8()                                                                              \
+  "s_nop 4\n\t"                                                                                    \
+  "v_writelane_b32 %0, %1, %9\n\tv_writelane_b32 %0, %2, %10\n\tv_writelane_b32 %0, %3, %11\n\t"      \
+  "v_writelane_b32 %0, %4, %12\n\tv_writelane_b32 %0, %5, %13\n\tv_writelane_b32 %0, %6, %14\n\t"     \
+  "v_writelane_b32 %0, %7, %15\n\tv_writelane_b32 %0, %8, %16"
+template <int I>
+__device__ __forceinline__ void put_planes(int c, int& qs, uint32_t& pw) {
+  qs += c;
+  uint32_t m[16];
+#pragma unroll
+  for (int b = 0; b < 8; ++b) {
+    const uint64_t mk = __ballot((c >> b) & 1);
+    m[2 * b] = (uint32_t)mk;
+    m[2 * b + 1] = (uint32_t)(mk >> 32);
+  }
+  asm(DFSSM_WL8()
+      : "+v"(pw)
+      : "s"(m[0]), "s"(m[1]), "s"(m[2]), "s"(m[3]), "s"(m[4]), "s"(m[5]), "s"(m[6]), "s"(m[7]),
+        "n"(16 * I + 0), "n"(16 * I + 1), "n"(16 * I + 2), "n"(16 * I + 3), "n"(16 * I + 4), "n"(16 * I + 5),
+        "n"(16 * I + 6), "n"(16 * I + 7));
+  asm(DFSSM_WL8()
+      : "+v"(pw)
+      : "s"(m[8]), "s"(m[9]), "s"(m[10]), "s"(m[11]), "s"(m[12]), "s"(m[13]), "s"(m[14]), "s"(m[15]),
+        "n"(16 * I + 8), "n"(16 * I + 9), "n"(16 * I + 10), "n"(16 * I + 11), "n"(16 * I + 12), "n"(16 * I + 13),
+        "n"(16 * I + 14), "n"(16 * I + 15));
+}
+#undef DFSSM_WL8
 
 // One linear's operands of this workgroup's rows, per lane of a group.
 struct Pref {
@@ -166,12 +216,11 @@ __device__ __forceinline__ int32_t gload1s(const void* p) {
   return *(const __attribute__((address_space(1))) int8_t*)(p);
 }
 
-__device__ __forceinline__ void prefetch(const dfssm::ChainLayerDev& L, int wg, int nwg, int gt, Pref& p) {
+__device__ __forceinline__ void prefetch(const dfssm::ChainLayerDev& L, int wg, int gt, Pref& p) {
   const int lane = gt & 63, wave = gt >> 6;
-  const int G = L.G, g = lane & (G - 1), grp = lane / G;
-  const int RW = 64 / G;
-  const int R = (L.N + nwg - 1) / nwg;
-  const int n0 = wg * R, n1 = min(L.N, n0 + R);
+  const int G = 1 << L.lgG, g = lane & (G - 1), grp = lane >> L.lgG;
+  const int RW = 64 >> L.lgG;
+  const int n0 = wg * L.R, n1 = min(L.N, n0 + L.R);
   const int C = L.K >> 7, W = L.K >> 5, r4 = L.r >> 2;
 #pragma unroll
   for (int s = 0; s < kMaxSteps; ++s) {
@@ -237,8 +286,12 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
     if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(status, 8u);
     return;
   }
-  __shared__ uint4 pl_lds[(dfssm::kChainMaxK / 128) * 8];
-  __shared__ int4 acc_lds[dfssm::kMaxRank / 4];
+  // bit-planes, plane-major: the G lanes of a row read consecutive chunks
+  __shared__ uint4 pl_lds[8 * kChunks];
+  // LoRA down-projection of the current linear as 4 signed base-256 limbs:
+  // entry g holds acc_a[4g .. 4g+3], dword t = limb t (r <= 64)
+  static_assert(dfssm::kChainAccRows * dfssm::kChainWgPerXcd <= 64, "limb table size");
+  __shared__ uint4 limb_lds[16];
   __shared__ int32_t dot_part[kAccRows][2 * kGW];
   __shared__ uint32_t ymax_lds;
   __shared__ int sumq_lds;
@@ -307,19 +360,22 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
   }
   __syncthreads();
   if (abort_) return;
-  const int rho = rho_lds, nx = nx_lds;
+  const int rho = __builtin_amdgcn_readfirstlane(rho_lds), nx = __builtin_amdgcn_readfirstlane(nx_lds);
   uint64_t* const y_rel = ex.y_rel + (int64_t)xcc * ex.ysum;
   uint64_t* const acc_rel = ex.acc_rel + (int64_t)xcc * L * dfssm::kMaxRank;
   const __amdgpu_buffer_rsrc_t rs_y = xcd_region(y_rel, ex.ysum);
   const __amdgpu_buffer_rsrc_t rs_acc = xcd_region(acc_rel, (int64_t)L * dfssm::kMaxRank);
 
   Pref pf;
-  if (group < L) prefetch(layers[group], wg, nwg, gt, pf);
+  if (group < L) prefetch(layers[group], wg, gt, pf);
 
   for (int l = 0; l < L; ++l) {
     const bool active = group == (l & 1);
-    const dfssm::ChainLayerDev Ld = layers[l];
-    const int K = Ld.K, N = Ld.N, r = Ld.r, G = Ld.G;
+    // the loop index is uniform: keeps the table reads and the row-split
+    // arithmetic on the scalar unit
+    const int lu = __builtin_amdgcn_readfirstlane(l);
+    const dfssm::ChainLayerDev Ld = layers[lu];
+    const int K = Ld.K, N = Ld.N, r = Ld.r, lgG = Ld.lgG, G = 1 << lgG, R = Ld.R;
     const float s = l == 0 ? s0[0] : 1.0f / 127.0f;
 
     // ---- 0. the active group relays this workgroup's slice of
@@ -329,7 +385,7 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
     int32_t av[kAccRows][kCols];
     uint32_t yv[kCols];
     if (l > 0) {
-      const int64_t prev = layers[l - 1].y_off;
+      const int64_t prev = layers[lu - 1].y_off;
       const uint32_t tag = tag_of(l - 1);
       if (active) {
         const int slice = (K + nx - 1) / nx;
@@ -402,13 +458,20 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
       for (int t = 0; t < kAccRows; ++t) {
         acc[t] = 0;
 #pragma unroll
-        for (int i = 0; i < kCols; ++i) acc[t] += av[t][i] * q[i];
+        for (int i = 0; i < kCols; ++i) acc[t] += __mul24(av[t][i], q[i]);  // |.| < 2^14: full-rate multiply
         acc[t] = wave_sum_u(acc[t]);
       }
       if (lane == 0) {
 #pragma unroll
         for (int t = 0; t < kAccRows; ++t) dot_part[t][wave16] = acc[t];
-        const int old = __hip_atomic_fetch_add(&cnt_dot, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
+        // relaxed: one wave's LDS operations complete in issue order, so this
+        // wave's partials are in LDS before its count is; the signal fences
+        // keep the compiler from moving the plain LDS accesses across it (an
+        // acquire-release atomic would also wait for every outstanding
+        // global load and store of the wave)
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        const int old = __hip_atomic_fetch_add(&cnt_dot, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
         if (old == 2 * kGW - 1) {
 #pragma unroll
           for (int t = 0; t < kAccRows; ++t) {
@@ -426,23 +489,23 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
       }
     }
     // wave16 holds columns kCT*i + 64*wave16 + lane: one ballot per plane
-    // gives two plane words, written by lane 0 as one 8-byte store
+    // gives two plane words; they are gathered into one register, lane
+    // 16*i + 2*b + h holding half h of plane b of column block i, and stored
+    // with one LDS write per lane
     {
+      static_assert(kCols * 16 == 64, "one plane word per lane");
       int qs = 0;
-#pragma unroll
-      for (int i = 0; i < kCols; ++i) {
-        if (i * kCT < K) {  // uniform
-          qs += q[i];
-          uint64_t mk[8];
-#pragma unroll
-          for (int b = 0; b < 8; ++b) mk[b] = __ballot((q[i] >> b) & 1);
-          if (lane == 0) {
-            const int word = (i * kCT + wave16 * 64) / 32;  // even
-#pragma unroll
-            for (int b = 0; b < 8; ++b)
-              *reinterpret_cast<uint64_t*>(reinterpret_cast<uint32_t*>(pl_lds) + ((word >> 2) * 8 + b) * 4 +
-                                           (word & 3)) = mk[b];
-          }
+      uint32_t pw = 0;
+      static_assert(kCols == 4, "column blocks below");
+      if (0 * kCT < K) put_planes<0>(q[0], qs, pw);
+      if (1 * kCT < K) put_planes<1>(q[1], qs, pw);
+      if (2 * kCT < K) put_planes<2>(q[2], qs, pw);
+      if (3 * kCT < K) put_planes<3>(q[3], qs, pw);
+      {
+        const int i = lane >> 4, b = (lane >> 1) & 7;
+        if (i * kCT < K) {
+          const int word = (i * kCT + wave16 * 64) / 32 + (lane & 1);
+          reinterpret_cast<uint32_t*>(pl_lds)[(b * kChunks + (word >> 2)) * 4 + (word & 3)] = pw;
         }
       }
       qs = wave_sum_u(qs);
@@ -451,10 +514,14 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
     __syncthreads();  // B2
     if (abort_) return;
     if (tid == 0) ymax_lds = 0;  // every read of it came before B2
+    // the group idle in this linear loads the weights of the next one now:
+    // none of its waits before its next GEMV are latency-critical, whereas
+    // loads issued earlier would hold up its polls in this linear (a wave's
+    // loads complete in order)
+    if (!active && l >= 1 && l + 1 < L) prefetch(layers[lu + 1], wg, gt, pf);
 
     // ---- 2. scaffold GEMV on the prefetched rows; collect acc_a -----------
-    const int RW = 64 / G;
-    const int R = (N + nwg - 1) / nwg;
+    const int RW = 64 >> lgG;
     const int g = lane & (G - 1);
     int part[kMaxSteps];
     if (active) {
@@ -472,7 +539,7 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
           int dsum = 0;
 #pragma unroll
           for (int b = 0; b < 8; ++b) {
-            const uint4 Pb = g < C ? pl_lds[g * 8 + b] : make_uint4(0, 0, 0, 0);
+            const uint4 Pb = g < C ? pl_lds[b * kChunks + g] : make_uint4(0, 0, 0, 0);
             const int c = __builtin_popcount(w.x & Pb.x) + __builtin_popcount(w.y & Pb.y) +
                           __builtin_popcount(w.z & Pb.z) + __builtin_popcount(w.w & Pb.w);
             dsum += b < 7 ? (c << b) : -(c << 7);
@@ -480,12 +547,23 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
           part[st] = 2 * group_sum(dsum, G) - sq;
         }
       }
-      if (gt < r) {
-        const uint32_t tag = tag_of(l);
-        const uint32_t word = (uint32_t)(l * dfssm::kMaxRank + gt);
-        uint64_t wd;
-        if (!poll_xcd(rs_acc, word, tag, wd, status, kStAcc)) abort_ = 1;
-        reinterpret_cast<int32_t*>(acc_lds)[gt] = (int32_t)(uint32_t)wd;
+      if (gt < 64) {
+        // wave 0 of the group: lane j collects acc_a[j] (0 past r) and
+        // stores its 4 signed base-256 limbs as bytes of limb_lds[j / 4],
+        // dword t = limb t, byte j % 4
+        int32_t v = 0;
+        if (gt < r) {
+          const uint32_t tag = tag_of(l);
+          const uint32_t word = (uint32_t)(l * dfssm::kMaxRank + gt);
+          uint64_t wd;
+          if (!poll_xcd(rs_acc, word, tag, wd, status, kStAcc)) abort_ = 1;
+          v = (int32_t)(uint32_t)wd;
+        }
+        int8_t d[4];
+        dfssm_dev::split_limbs(v, d);
+        uint8_t* lb = reinterpret_cast<uint8_t*>(limb_lds) + (gt >> 2) * 16 + (gt & 3);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) lb[4 * t] = (uint8_t)d[t];
       }
     }
     __syncthreads();  // B3
@@ -495,22 +573,16 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
     // ---- 3. LoRA up-projection, epilogue, publish; prefetch linear l+2 ----
     if (active) {
       const int r4 = (r + 3) >> 2;
-      const int grp = lane / G;
+      const int grp = lane >> lgG;
       const int n0 = wg * R, n1 = min(N, n0 + R);
       // limbs of acc_a[4g .. 4g+3], packed per limb (j >= r read as 0)
       uint32_t lb0 = 0, lb1 = 0, lb2 = 0, lb3 = 0;
       if (r > 0 && g < r4) {
-        const int4 a4 = acc_lds[g];
-        const int av[4] = {a4.x, a4.y, a4.z, a4.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          int8_t d[4];
-          dfssm_dev::split_limbs(4 * g + e < r ? av[e] : 0, d);
-          lb0 |= (uint32_t)(uint8_t)d[0] << (8 * e);
-          lb1 |= (uint32_t)(uint8_t)d[1] << (8 * e);
-          lb2 |= (uint32_t)(uint8_t)d[2] << (8 * e);
-          lb3 |= (uint32_t)(uint8_t)d[3] << (8 * e);
-        }
+        const uint4 t = limb_lds[g];
+        lb0 = t.x;
+        lb1 = t.y;
+        lb2 = t.z;
+        lb3 = t.w;
       }
 #pragma unroll
       for (int st = 0; st < kMaxSteps; ++st) {
@@ -528,7 +600,6 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
           y_all[Ld.y_off + n] = y;
         }
       }
-      if (l + 2 < L) prefetch(layers[l + 2], wg, nwg, gt, pf);
     }
     // the next linear's B0 orders every LDS reuse
   }

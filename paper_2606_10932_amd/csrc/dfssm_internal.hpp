@@ -128,8 +128,11 @@ struct ChainLayerDev {
   const int8_t* A;
   const int8_t* B;
   const float* beta;
-  int32_t K, N, r, G;  // G: lanes per output row (power of two, 8..64)
-  int64_t y_off;       // offset of this linear's outputs in y_all
+  int32_t K, N, r;
+  int32_t lgG;    // log2 of the lanes per output row (G = 8..64)
+  int32_t R;      // output rows per workgroup, ceil(N / grid)
+  int32_t pad;
+  int64_t y_off;  // offset of this linear's outputs in y_all
 };
 
 int chain_lanes_per_row(int64_t K);
