@@ -4,7 +4,7 @@ LoRA linear (include/dfssm.h).
 Argument marshalling only: every step runs in the library's HIP kernels.
 PyTorch provides device memory and the current HIP stream.  Importing this
 package loads the in-tree library and fails loudly if it has not been built
-(``python -m paper_2606_10932_amd.build``); there is no fallback.
+(``python paper_2606_10932_amd/build.py``); there is no fallback.
 """
 from __future__ import annotations
 
@@ -40,7 +40,7 @@ class Layer(ctypes.Structure):
 
 def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     if not os.path.exists(path):
-        raise ImportError(f"{path} is missing: build it with `python -m paper_2606_10932_amd.build`")
+        raise ImportError(f"{path} is missing: build it with `python paper_2606_10932_amd/build.py`")
     lib = ctypes.CDLL(path)
     vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
     lib.dfssm_quantize_act.argtypes = [vp, i32, i64, i64, i64, vp, vp, vp]

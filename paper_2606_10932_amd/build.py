@@ -1,6 +1,7 @@
 """Build libdfssm.so (the HIP library behind include/dfssm.h) for gfx950.
 
-Run as ``python -m paper_2606_10932_amd.build`` or call build().  The
+Run as ``python paper_2606_10932_amd/build.py`` (the package itself refuses to
+import until the library exists) or call build().  The
 library is built in-tree next to this file.
 """
 from __future__ import annotations
