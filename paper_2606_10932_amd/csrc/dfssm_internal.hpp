@@ -135,6 +135,10 @@ struct ChainLayerDev {
   int64_t y_off;  // offset of this linear's outputs in y_all
 };
 
+// Compute units of the current device (cached per device; 256 if the query
+// fails).
+int device_cu_count();
+
 int chain_lanes_per_row(int64_t K);
 int chain_grid();
 bool chain_persistent_supported(const dfssm_layer* layers, int n_layers, int64_t M, int nwg);
@@ -168,8 +172,8 @@ __device__ __forceinline__ void split_limbs(int32_t v, int8_t d[4]) {
 
 // The fixed-order fp32 output scaling y = s*(alpha*fs + beta*fb) with
 // acc_b = hi*2^16 + lo.  fb is the int64 acc_b rounded once to fp32: the
-// fp64 sum hi*65536 + lo is exact (|acc_b| < 2^53), so converting it to fp32
-// is the single round-to-nearest-even of the integer.  The library is
+// fp64 value hi*65536 + lo is exact (|acc_b| < 2^53), so converting it to
+// fp32 is the single round-to-nearest-even of the integer.  The library is
 // compiled with -ffp-contract=off, so no multiply-add fuses.
 __device__ __forceinline__ float epilogue(float s, float alpha, float beta, int32_t acc_s,
                                           int32_t hi, int32_t lo, bool lora) {
@@ -177,7 +181,8 @@ __device__ __forceinline__ float epilogue(float s, float alpha, float beta, int3
   float u = alpha * fs;
   float w = u;
   if (lora) {
-    double db = (double)hi * 65536.0 + (double)lo;
+    // one fused multiply-add: hi*2^16 + lo is exact in fp64 either way
+    double db = __builtin_fma((double)hi, 65536.0, (double)lo);
     float fb = (float)db;
     float v = beta * fb;
     w = u + v;

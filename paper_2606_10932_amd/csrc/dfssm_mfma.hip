@@ -3,30 +3,31 @@
 //
 // The sign bits are expanded on chip, in registers, to {0,1} bytes (a
 // nibble n becomes bytes via (n * 0x00204081) & 0x01010101), so the MFMA
-// computes D[m,n] = sum_{bit=1} Q[m,k] and acc_s = 2*D - sum_k Q[m,k]; the
+// computes D[n,m] = sum_{bit=1} Q[m,k] and acc_s = 2*D - sum_k Q[m,k]; the
 // expanded signs never touch memory or LDS (the paper expands to int8 "on
-// the fly" ahead of a library int8 GEMM, Sec. 4.1).
+// the fly" ahead of a library int8 GEMM, Sec. 4.1).  An expanded operand
+// costs 12 vector instructions and feeds 8 MFMAs (a wave covers 128 tokens),
+// which keeps the vector ALU below the matrix core.
 //
 // Operand layout of v_mfma_i32_16x16x64_i8 (wave64): lane l supplies row
-// (l % 16) of A and column (l % 16) of B, each as 16 consecutive K-bytes of
-// K-group (l / 16); the 16x16 int32 result D has D[4*(l/16)+v][l%16] in
-// lane l, register v.  A = Q rows (tokens), B = sign columns (output rows).
+// (l % 16) of the first operand and column (l % 16) of the second, each as
+// 16 consecutive K-bytes of K-group (l / 16); the 16x16 int32 result D has
+// D[4*(l/16)+v][l%16] in lane l, register v.
 //
-// LoRA: lora_down computes acc_a = Q * A^T with the same MFMA (K split over
-// the 4 waves of a block, reduced in LDS), sum_k Q, and writes acc_a as 4
-// signed base-256 int8 limbs.  After the scaffold K-loop the main kernel
-// gets the exact int64 acc_b = sum_j B[n,j] acc_a[m,j] from four int8
-// MFMAs, E_hi = 256*(L3.B) + L2.B and E_lo = 256*(L1.B) + L0.B (each < 2^31
-// for r <= 256), acc_b = E_lo + 65536*E_hi, 16 output rows at a time, so
-// the K-loop holds only the scaffold accumulators (3 blocks per CU).
+// LoRA: lora_down computes acc_a = Q * A^T with the same MFMA and writes it
+// as 4 signed base-256 int8 limbs.  After the scaffold K-loop the main kernel
+// gets the exact int64 acc_b = sum_j B[n,j] acc_a[m,j] from four int8 MFMAs
+// per 16x16 tile, E_hi = 256*(B.L3) + B.L2 and E_lo = 256*(B.L1) + B.L0
+// (each < 2^31 for r <= 256), acc_b = E_lo + 65536*E_hi, so the K-loop holds
+// only the scaffold accumulators.
+#include <algorithm>
+#include <atomic>
+
 #include "dfssm_internal.hpp"
 
 namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
-typedef float v4f __attribute__((ext_vector_type(4)));
-
-constexpr int kThreads = 256;
 
 __device__ __forceinline__ v4i mfma(v4i a, v4i b, v4i c) {
   return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
@@ -75,60 +76,84 @@ __device__ __forceinline__ v4i load16_guarded(const int8_t* row, int start, int 
 }
 
 // ------------------------------------------------------------ lora_down
-// A block owns 16 tokens x 16 ranks (one MFMA tile; blockIdx.y is the rank
-// tile, covering rp); its 4 waves split the K steps into quarters and reduce
-// their partial sums in LDS.  Loads are issued kLdBatch K-steps at a time.
-constexpr int kLdBatch = 4;
+// acc_a = Q A^T on the same MFMA.  A block owns 16 tokens x 32 ranks (two
+// 16-rank tiles; blockIdx.y walks the padded rank range rp); its 8 waves
+// split the K steps, each issuing the loads of up to kLdBatch steps before
+// its first multiply, and reduce their partial sums in LDS.  The block writes
+// acc_a, its 4 signed base-256 int8 limbs (zero for ranks in [r, rp)) and,
+// for blockIdx.y == 0, sum_k Q[m,k].
+constexpr int kLdThreads = 512;
+constexpr int kLdWaves = kLdThreads / 64;
+constexpr int kLdRanks = 32;
+constexpr int kLdBatch = 8;
+constexpr int kLdPitch = 17;  // padded rank pitch of the partial sums
 
-__global__ __launch_bounds__(kThreads) void mfma_lora_down(const int8_t* __restrict__ q, int M, int K,
-                                                           int r, int rp, const int8_t* __restrict__ A,
-                                                           int32_t* __restrict__ acc_a,
-                                                           int8_t* __restrict__ limbs,
-                                                           int32_t* __restrict__ sumq) {
-  __shared__ int32_t part[4][16 * 16];
-  __shared__ int32_t qpart[4][16];
+__global__ __launch_bounds__(kLdThreads) void mfma_lora_down(const int8_t* __restrict__ q, int M, int K,
+                                                             int r, int rp, const int8_t* __restrict__ A,
+                                                             int32_t* __restrict__ acc_a,
+                                                             int8_t* __restrict__ limbs,
+                                                             int32_t* __restrict__ sumq) {
+  __shared__ int32_t part[kLdWaves][kLdRanks * kLdPitch];
+  __shared__ int32_t qpart[kLdWaves][16];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int row = lane & 15, kg = lane >> 4;
-  const int m0 = blockIdx.x * 16, j0 = blockIdx.y * 16;
-  const bool first = blockIdx.y == 0;  // the rank tile that also sums Q
-  const int m = m0 + row, j = j0 + row;
-  const bool m_ok = m < M, j_ok = j < r;
+  const int m0 = blockIdx.x * 16, j0 = blockIdx.y * kLdRanks;
+  const bool first = blockIdx.y == 0;  // the rank block that also sums Q
+  const int m = m0 + row;
+  const bool m_ok = m < M;
   const int8_t* qrow = q + (int64_t)(m_ok ? m : 0) * K;
-  const int8_t* arow = A + (int64_t)(j_ok ? j : 0) * K;
+  const int8_t* arow[2];
+  bool j_ok[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int j = j0 + 16 * u + row;
+    j_ok[u] = j < r;
+    arow[u] = A + (int64_t)(j_ok[u] ? j : 0) * K;
+  }
   const int nks = (K + 63) / 64;
-  const int per = (nks + 3) / 4;
+  const int per = (nks + kLdWaves - 1) / kLdWaves;
   const int ks0 = wave * per, ks1 = min(nks, ks0 + per);
 
-  v4i acc = zero4();
+  v4i acc[2] = {zero4(), zero4()};
   int qs = 0;
   for (int kb = ks0; kb < ks1; kb += kLdBatch) {
-    // all loads of the batch from clamped addresses first, masks after
-    v4i a[kLdBatch], b[kLdBatch];
-    int ma[kLdBatch], mb[kLdBatch];
+    // every load of the batch first (steps past ks1 are skipped, uniformly)
+    v4i b[kLdBatch], a0[kLdBatch], a1[kLdBatch];
 #pragma unroll
     for (int u = 0; u < kLdBatch; ++u) {
-      const int kk = (kb + u) * 64 + 16 * kg;
-      const bool kok = kb + u < ks1 && kk < K;
-      const int kc = kok ? kk : 0;
-      a[u] = load16(qrow + kc);
-      ma[u] = (m_ok && kok) ? -1 : 0;
-      b[u] = r > 0 ? load16(arow + kc) : zero4();
-      mb[u] = (j_ok && kok) ? -1 : 0;
+      b[u] = a0[u] = a1[u] = zero4();
+      if (kb + u < ks1) {
+        const int kk = (kb + u) * 64 + 16 * kg;
+        const int kc = kk < K ? kk : 0;  // K % 32 == 0: a 16-byte chunk is wholly in or out
+        b[u] = load16(qrow + kc);
+        if (r > 0) {
+          a0[u] = load16(arow[0] + kc);
+          a1[u] = load16(arow[1] + kc);
+        }
+      }
     }
 #pragma unroll
     for (int u = 0; u < kLdBatch; ++u) {
-      a[u] &= ma[u];
-      b[u] &= mb[u];
-      if (first) {
+      if (kb + u < ks1) {
+        const int kk = (kb + u) * 64 + 16 * kg;
+        if (!(m_ok && kk < K)) b[u] = zero4();
+        if (!j_ok[0]) a0[u] = zero4();
+        if (!j_ok[1]) a1[u] = zero4();
+        if (first) {
 #pragma unroll
-        for (int t = 0; t < 4; ++t) qs = __builtin_amdgcn_sdot4(a[u][t], 0x01010101, qs, false);
+          for (int t = 0; t < 4; ++t) qs = __builtin_amdgcn_sdot4(b[u][t], 0x01010101, qs, false);
+        }
+        // D[rank][token]: the A rows are the first operand
+        acc[0] = mfma(a0[u], b[u], acc[0]);
+        acc[1] = mfma(a1[u], b[u], acc[1]);
       }
-      acc = mfma(a[u], b[u], acc);
     }
   }
-  // D[token 4*kg + v][rank row]
+  // lane (row, kg) holds D[rank 16u + 4kg + v][token row]
 #pragma unroll
-  for (int v = 0; v < 4; ++v) part[wave][(4 * kg + v) * 16 + row] = acc[v];
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) part[wave][(16 * u + 4 * kg + v) * kLdPitch + row] = acc[u][v];
   if (first) {
     qs += __shfl_xor(qs, 16, 64);
     qs += __shfl_xor(qs, 32, 64);
@@ -136,11 +161,14 @@ __global__ __launch_bounds__(kThreads) void mfma_lora_down(const int8_t* __restr
   }
   __syncthreads();
   {
-    const int i = threadIdx.x;  // 256 threads = 16 tokens x 16 ranks
-    const int mi = i >> 4, ji = i & 15;
-    const int mm = m0 + mi, jj = j0 + ji;
+    // thread i: token i / 32, rank i % 32 (consecutive threads, consecutive ranks)
+    const int i = threadIdx.x;
+    const int ml = i >> 5, jl = i & 31;
+    const int mm = m0 + ml, jj = j0 + jl;
     if (mm < M) {
-      const int32_t val = part[0][i] + part[1][i] + part[2][i] + part[3][i];
+      int32_t val = 0;
+#pragma unroll
+      for (int w = 0; w < kLdWaves; ++w) val += part[w][jl * kLdPitch + ml];
       int8_t d[4];
       dfssm_dev::split_limbs(jj < r ? val : 0, d);
 #pragma unroll
@@ -148,57 +176,70 @@ __global__ __launch_bounds__(kThreads) void mfma_lora_down(const int8_t* __restr
       if (jj < r) acc_a[(int64_t)mm * r + jj] = val;
     }
   }
-  if (first && threadIdx.x < 16 && m0 + threadIdx.x < M)
-    sumq[m0 + threadIdx.x] = qpart[0][threadIdx.x] + qpart[1][threadIdx.x] + qpart[2][threadIdx.x] +
-                             qpart[3][threadIdx.x];
+  if (first && threadIdx.x < 16 && m0 + (int)threadIdx.x < M) {
+    int32_t t = 0;
+#pragma unroll
+    for (int w = 0; w < kLdWaves; ++w) t += qpart[w][threadIdx.x];
+    sumq[m0 + threadIdx.x] = t;
+  }
 }
 
-// ------------------------------------------------------------ main GEMM
-// Block tile 128 (tokens) x 128 (output rows), 4 waves as 2 x 2 with wave
-// tiles of 64 x 64 (4 x 4 MFMA tiles); 64 K per stage.  The K-loop runs a
-// 4-stage LDS ring filled by direct-to-LDS loads (global_load_lds: no
-// register staging):
-//   Q stage: 128 rows x 64 bytes, the four 16-byte chunks of row r stored
-//            at chunk slot c ^ ((r >> 2) & 3), so the 16 lanes reading one
-//            MFMA operand column hit 16 distinct 4-bank groups;
-//   sign stage: 128 rows x 2 words (64 sign bits per row), expanded to
-//            {0,1} bytes in registers right before use.
-// Each wave issues exactly three loads per stage (two 1 KB Q pieces and
-// one 256-byte sign piece), so "stage ks has landed" is a vector-memory
-// count; past the last stage the issue repeats the last stage's loads (the
-// same bytes into the same slot), which keeps the count uniform.
-constexpr int kBM = 128, kBN = 128, kBK = 64;
+// ------------------------------------------------------------ scaffold GEMM
+// Operand roles: the expanded signs are the MFMA's first operand (rows =
+// output rows n) and the codes Q its second (columns = tokens m), so lane
+// (rho, kg) of a 16x16 result holds D[n = 4kg + v][m = rho] for v = 0..3:
+// four consecutive outputs of one token row, stored as one 16-byte write.
+//
+// Block: 128 tokens x a run of 16-row "row tiles".  The row tiles of each
+// 128-token slice are dealt to blocks in runs whose lengths differ by at most
+// one and are at most 17, with enough blocks per slice to fill the chip's
+// block slots (two per CU) in whole rounds -- so every block finishes at about
+// the same time and no round of leftover tiles follows.  Wave w owns row
+// tiles 4w .. 4w+3 of the run (wave tile 128 x 64: each expanded sign operand
+// feeds 8 MFMAs, and the Q tile in LDS is shared by the 4 waves); a 17th row
+// tile is shared by all 4 waves, wave w taking its token tiles 2w and 2w+1.
+//
+// K-loop: 64 K per stage through a kStages-deep LDS ring filled by
+// direct-to-LDS loads (global_load_lds with a scalar base and a per-lane
+// offset that stays fixed, so the loop does no address arithmetic):
+//   Q stage: 128 rows x 64 bytes, the four 16-byte chunks of row m stored
+//            at chunk slot c ^ ((m >> 1) & 3), so each 8 lanes of a 16-byte
+//            LDS read hit 8 distinct 4-bank groups of the 32 banks;
+//   sign stage: per wave, 64 rows x 2 words ordered [rho][half][t] (a lane
+//            fetches its 4 row tiles' words with one LDS read), then the
+//            17th row tile's 16 rows x 2 words.
+// Each wave issues 5 loads per stage (the 17th tile's words are loaded
+// whether or not the run has one), so "stage ks has landed" is a count of
+// vector-memory operations.
+constexpr int kThreads = 256;
+constexpr int kBM = 128;
+constexpr int kBK = 64;
 constexpr int kStages = 4;
-constexpr int kLoadsPerStage = 3;
-constexpr int kQStage = kBM * kBK;               // 8 KB
-constexpr int kWStage = kBN * 2 * 4;             // 1 KB
-constexpr int kStageBytes = kQStage + kWStage;
-// epilogue: limbs [4][kBM][64] and B [kBN][64] with the same chunk swizzle,
-// then one transpose buffer of 16 x kYPitch floats per wave
-constexpr int kYPitch = 20;                      // 16 columns + 4: conflict-free both ways
-constexpr int kLdsLoop = kStages * kStageBytes;
-constexpr int kLdsLora = 4 * kBM * kBK + kBN * kBK + 4 * 16 * kYPitch * 4;
-constexpr int kLdsBytes = kLdsLoop > kLdsLora ? kLdsLoop : kLdsLora;
-#ifndef DFSSM_MFMA_OCC
-#define DFSSM_MFMA_OCC 3
-#endif
+constexpr int kRunMax = 17;                             // row tiles per block
+constexpr int kQStage = kBM * kBK;                      // 8 KB
+constexpr int kWMain = 4 * 64 * 8;                      // 2 KB: 4 waves x 64 rows x 8 bytes
+constexpr int kStageBytes = kQStage + kWMain + 16 * 8;  // + the 17th tile's words
+constexpr int kLps = 5;                                 // loads per wave per stage
+constexpr int kLdsRing = kStages * kStageBytes;         // 40.5 KB
+constexpr int kLimbBytes = 4 * kBM * 64;                // LoRA limbs of the tile, 64 ranks
+constexpr int kLdsLora = kLimbBytes + kRunMax * 16 * 64;  // + B rows of the run
+constexpr int kLdsBytes = kLdsRing > kLdsLora ? kLdsRing : kLdsLora;
+constexpr int kMaxRows = kRunMax * 16;
+static_assert(4 * kLps <= 63, "vector-memory counter range");
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Direct-to-LDS loads (gfx950 global_load_lds): each lane's 16 (or 4) bytes
-// land at m0 + 16*lane (4*lane).  Issued as inline assembly so the compiler
-// does not treat every later LDS read as depending on them (it cannot tell
-// the ring slots apart and would wait for all loads); the K-loop orders them
-// itself with DFSSM_WAIT_VMCNT and the barrier.
-// (the address is wave-uniform; readfirstlane puts it in an SGPR for m0)
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(uintptr_t)(const lds_void*)p);
+// Direct-to-LDS loads (gfx950 global_load_lds): lane i's 16 (or 4) bytes from
+// sbase + voff land at m0 + 16*i (4*i).  Inline assembly, so the compiler does
+// not make every later LDS read wait for them; the K-loop orders them with
+// DFSSM_WAIT_VMCNT and the barrier.
+__device__ __forceinline__ void lds_dma16(uint32_t voff, const void* sbase, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
 }
-__device__ __forceinline__ void lds_dma16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
-}
-__device__ __forceinline__ void lds_dma4(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+__device__ __forceinline__ void lds_dma4(uint32_t voff, const void* sbase, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1" ::"v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
 }
 
 // s_waitcnt with only the vector-memory counter constrained
@@ -208,294 +249,445 @@ __device__ __forceinline__ void lds_dma4(const void* g, uint32_t lds) {
 // of the loads is ordered by the DFSSM_WAIT_VMCNT before it
 #define DFSSM_BARRIER() asm volatile("s_barrier" ::: "memory")
 
-template <bool kLoraLds>
-__global__ __launch_bounds__(kThreads, DFSSM_MFMA_OCC) void mfma_scaffold(
-    const int8_t* __restrict__ q, const float* __restrict__ s, int M, int K, int N, int r, int rp,
-    const uint32_t* __restrict__ w_bits, const float* __restrict__ alpha,
-    const int8_t* __restrict__ limbs, const int8_t* __restrict__ B,
-    const float* __restrict__ beta, const int32_t* __restrict__ sumq, float* __restrict__ y,
-    int32_t* __restrict__ acc_s_out, int64_t* __restrict__ acc_b_out, int nbm, int nbn) {
-  // one LDS buffer, two uses: the K-loop stages (Q tile + sign words, x2),
-  // then the LoRA operands of the epilogue (4 limbs x 128 rows + 128 B rows)
-  __shared__ __attribute__((aligned(16))) int8_t lds_raw[kLdsBytes];
-  int8_t* limb_lds = lds_raw;                       // [4][kBM][64], swizzled
-  int8_t* b_lds = lds_raw + 4 * kBM * kBK;          // [kBN][64], swizzled
-  __shared__ __attribute__((aligned(16))) float al_lds[kBN], be_lds[kBN], s_lds[kBM];
-  __shared__ __attribute__((aligned(16))) int32_t sq_lds[kBM];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int row = lane & 15, kg = lane >> 4;
+// 16-byte chunk swizzle of 64-byte rows: conflict-free 16-byte reads of one
+// chunk column on gfx950's 32-bank LDS
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 3; }
 
-  // XCD-aware tile order: blocks are dealt to the 8 XCDs round-robin, so
-  // give each XCD a contiguous run of tiles (same n-tile, successive m-tiles:
-  // the tile's sign words and the Q tiles stay in that XCD's L2)
-  const int nblk = nbm * nbn;
-  const int bid = blockIdx.x;
-  const int per_xcd = nblk / 8, rem = nblk % 8;
-  const int xcd = bid % 8, idx = bid / 8;
-  const int tile = xcd < rem ? xcd * (per_xcd + 1) + idx : rem * (per_xcd + 1) + (xcd - rem) * per_xcd + idx;
-  const int bm = tile % nbm, bn = tile / nbm;
-  const int m0 = bm * kBM, n0 = bn * kBN;
-  const int wm0 = m0 + (wave >> 1) * 64, wn0 = n0 + (wave & 1) * 64;
-  const int W = K / 32;
-  const int nks = (K + kBK - 1) / kBK;
+struct GemmArgs {
+  const int8_t* q;
+  const float* s;
+  int M, K, N, r, rp;
+  const uint32_t* w_bits;
+  const float* alpha;
+  const int8_t* limbs;
+  const int8_t* B;
+  const float* beta;
+  const int32_t* sumq;
+  float* y;
+  int32_t* acc_s_out;
+  int64_t* acc_b_out;
+  int nt16;  // row tiles of N: ceil(N / 16)
+  int bpm;   // blocks per 128-token slice
+};
 
-  // per-row and per-column scalars of the tile, staged once in LDS
-  if (tid < kBN) {
-    const int n = min(n0 + tid, N - 1);
-    al_lds[tid] = alpha[n];
-    be_lds[tid] = r > 0 ? beta[n] : 0.0f;
-  } else {
-    const int m = min(m0 + tid - kBN, M - 1);
-    s_lds[tid - kBN] = s[m];
-    sq_lds[tid - kBN] = sumq[m];
+// Tile index of block b among cnt blocks whose XCD is b % 8: each XCD gets a
+// contiguous run of the slice-major block list, so it works on few token rows
+// (its Q rows stay in its L2) across all their output rows.
+__device__ __forceinline__ int xcd_tile(int b, int cnt) {
+  const int per = cnt / 8, rem = cnt % 8;
+  const int x = b % 8, idx = b / 8;
+  return (x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per) + idx;
+}
+
+// LoRA limb products of one 16x16 tile for rank above 64, operands straight
+// from memory, 64 ranks at a time
+__device__ __forceinline__ void lora_from_memory(const GemmArgs& a, int nrow, int mrow, int kg, v4i& ehi,
+                                                 v4i& elo) {
+  const bool baligned = (a.r % 16) == 0;
+  ehi = zero4();
+  elo = zero4();
+#pragma unroll
+  for (int pass = 0; pass < 4; ++pass) {  // limbs 3, 2, 1, 0
+    const int limb = 3 - pass;
+    v4i e = limb >= 2 ? ehi : elo;
+    for (int j0 = 0; j0 < a.rp; j0 += 64) {
+      const v4i bl = load16_guarded(a.B + (int64_t)nrow * a.r, j0 + 16 * kg, a.r, baligned);
+      const v4i al = load16(a.limbs + ((int64_t)limb * a.M + mrow) * a.rp + j0 + 16 * kg);
+      e = mfma(bl, al, e);
+    }
+    if (limb == 3 || limb == 1) e = e << 8;
+    if (limb >= 2)
+      ehi = e;
+    else
+      elo = e;
   }
-  __syncthreads();
+}
 
-  // ---- scaffold K-loop ------------------------------------------------------
-  // loads of stage ks (clamped to the last stage): this wave's Q rows
-  // 32*wave + 16*j + lane/4, slot lane%4 <- chunk (lane%4) ^ ((row >> 2) & 3),
-  // and sign rows 32*wave + lane/2, word lane%2.  Rows past M or N read the
-  // last row (their outputs are never stored); a chunk past K reads the
-  // chunk two before it (its sign bits are masked to zero below).
-  const int8_t* qrow[2];
-  int qchunk[2];
+// LDS-side state of a block, shared by the K-loop and the epilogue
+struct TileLds {
+  int8_t* lds;     // ring, then LoRA staging
+  float* al;       // alpha of the run's rows
+  float* be;       // beta of the run's rows
+  float* sv;       // s of the tile's tokens
+  int32_t* sq;     // sum Q of the tile's tokens
+};
+
+// Outputs of one 16x16 tile (row tile at row offset nl of the run, token
+// tile i): the LoRA term from four limb MFMAs (exact int64 acc_b = E_lo +
+// 65536*E_hi, E_hi = 256*(B.L3) + B.L2, E_lo = 256*(B.L1) + B.L0), then
+// acc_s = 2*D - sum Q and y = s*(alpha*fs + beta*fb).  kLdsLora: the limbs
+// and B rows are in LDS (rank <= 64); otherwise the LoRA operands come from
+// memory (rank above 64) or there is no LoRA (rank 0).  kChecked: rows past
+// M or N, unaligned rows of y and the accumulator outputs are handled.
+template <bool kLdsLora, bool kChecked>
+__device__ __forceinline__ void tile_out(const GemmArgs& a, const TileLds& L, const v4i& acc, const v4i& bop,
+                                         const v4i (&lm)[4], int m0, int n0, int nl, int i, int rho, int kg) {
+  const int M = a.M, N = a.N;
+  const bool lora = a.r > 0;
+  const int ml = 16 * i + rho;
+  const int m = m0 + ml;
+  const int n = n0 + nl + 4 * kg;  // this lane's rows n .. n+3
+  v4i ehi = zero4(), elo = zero4();
+  if (kLdsLora) {
+    ehi = mfma(bop, lm[3], ehi);
+    ehi = ehi << 8;
+    ehi = mfma(bop, lm[2], ehi);
+    elo = mfma(bop, lm[1], elo);
+    elo = elo << 8;
+    elo = mfma(bop, lm[0], elo);
+  } else if (lora) {
+    lora_from_memory(a, min(n0 + nl + rho, N - 1), min(m, M - 1), kg, ehi, elo);
+  }
+  const float4 al4 = *reinterpret_cast<const float4*>(&L.al[nl + 4 * kg]);
+  const float4 be4 = *reinterpret_cast<const float4*>(&L.be[nl + 4 * kg]);
+  const float alv[4] = {al4.x, al4.y, al4.z, al4.w};
+  const float bev[4] = {be4.x, be4.y, be4.z, be4.w};
+  const float sm = L.sv[ml];
+  const int qm = L.sq[ml];
+  float yv[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int32_t as = 2 * acc[v] - qm;
+    yv[v] = dfssm_dev::epilogue(sm, alv[v], bev[v], as, ehi[v], elo[v], kLdsLora || lora);
+    if (kChecked && m < M && n + v < N) {
+      if (a.acc_s_out) a.acc_s_out[(int64_t)m * N + n + v] = as;
+      if (a.acc_b_out) a.acc_b_out[(int64_t)m * N + n + v] = lora ? (int64_t)elo[v] + ((int64_t)ehi[v] << 16) : 0;
+    }
+  }
+  float* dst = a.y + (int64_t)m * N + n;
+  if (!kChecked) {
+    *reinterpret_cast<float4*>(dst) = make_float4(yv[0], yv[1], yv[2], yv[3]);
+  } else if (m < M) {
+    if ((N & 3) == 0 && n + 3 < N) {
+      *reinterpret_cast<float4*>(dst) = make_float4(yv[0], yv[1], yv[2], yv[3]);
+    } else {
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        if (n + v < N) dst[v] = yv[v];
+    }
+  }
+}
+
+// Epilogue of the block, per wave: its (up to) 4 row tiles x 8 token tiles,
+// then its 2 token tiles of the 17th row tile.
+template <bool kLdsLora, bool kChecked>
+__device__ __forceinline__ void block_epilogue(const GemmArgs& a, const TileLds& L, const v4i (&acc)[4][8],
+                                               const v4i (&accx)[2], int m0, int n0, int wave, int ntw,
+                                               bool extra, int rho, int kg, int l_off) {
+  const int8_t* limb_lds = L.lds;
+  const int8_t* b_lds = L.lds + kLimbBytes;
+  v4i bop[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+    bop[t] = kLdsLora ? *reinterpret_cast<const v4i*>(b_lds + (64 * wave + 16 * t) * 64 + l_off) : zero4();
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    v4i lm[4];
+#pragma unroll
+    for (int l = 0; l < 4; ++l)
+      lm[l] = kLdsLora ? *reinterpret_cast<const v4i*>(limb_lds + (l * kBM + 16 * i) * 64 + l_off) : zero4();
+    if (ntw == 4) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        tile_out<kLdsLora, kChecked>(a, L, acc[t][i], bop[t], lm, m0, n0, 64 * wave + 16 * t, i, rho, kg);
+    } else {
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        if (t < ntw) tile_out<kLdsLora, kChecked>(a, L, acc[t][i], bop[t], lm, m0, n0, 64 * wave + 16 * t, i, rho, kg);
+    }
+  }
+  if (extra) {
+    const v4i bx = kLdsLora ? *reinterpret_cast<const v4i*>(b_lds + 256 * 64 + l_off) : zero4();
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int i = 2 * wave + h;
+      v4i lm[4];
+#pragma unroll
+      for (int l = 0; l < 4; ++l)
+        lm[l] = kLdsLora ? *reinterpret_cast<const v4i*>(limb_lds + (l * kBM + 16 * i) * 64 + l_off) : zero4();
+      tile_out<kLdsLora, kChecked>(a, L, accx[h], bx, lm, m0, n0, 256, i, rho, kg);
+    }
+  }
+}
+
+template <bool kLoraLds>
+__device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds& L, int m0, int rt0, int cnt) {
+  const int M = a.M, K = a.K, N = a.N, r = a.r, rp = a.rp;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS addresses of the loads
+  const int rho = lane & 15, kg = lane >> 4;
+  const int W = K >> 5;
+  const int nks = (K + kBK - 1) / kBK;
+  const bool ktail = (K & (kBK - 1)) != 0;  // the last stage holds 32 columns
+  const int n0 = 16 * rt0;
+  const int cmain = min(cnt, 16);
+  const int ntw = min(max(cmain - 4 * wave, 0), 4);  // this wave's row tiles
+  const bool extra = cnt > 16;                        // the 17th row tile
+  const int nrows = 16 * cnt;
+  int8_t* const lds = L.lds;
+
+  // per-row and per-token scalars of the block (read after the K-loop's
+  // final barrier)
+  for (int x = tid; x < nrows; x += kThreads) {
+    const int n = min(n0 + x, N - 1);
+    L.al[x] = a.alpha[n];
+    L.be[x] = r > 0 ? a.beta[n] : 0.0f;
+  }
+  if (tid < kBM) {
+    const int m = min(m0 + tid, M - 1);
+    L.sv[tid] = a.s[m];
+    L.sq[tid] = a.sumq[m];
+  }
+
+  // ---- direct-to-LDS load constants: per-lane offsets fixed for the loop
+  //      (rows past M or N read the last row; their outputs are never stored)
+  uint32_t voff_q[2], lds_q[2];
+  bool hi_chunk[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
-    const int rl = 32 * wave + 16 * j + (lane >> 2);
-    qrow[j] = q + (int64_t)min(m0 + rl, M - 1) * K;
-    qchunk[j] = ((lane & 3) ^ ((rl >> 2) & 3)) * 16;
+    const int slot = 64 * (2 * wave + j) + lane;  // 16-byte slot in the Q stage
+    const int m = slot >> 2;
+    const int c = (lane & 3) ^ swz(m);
+    hi_chunk[j] = c >= 2;
+    voff_q[j] = (uint32_t)((min(m0 + m, M - 1) - m0) * K + 16 * c);
+    lds_q[j] = 1024u * (2 * wave + j);
   }
-  const int wrl = 32 * wave + (lane >> 1);
-  const uint32_t* wrow = w_bits + (int64_t)min(n0 + wrl, N - 1) * W + (lane & 1);
-  auto issue = [&](int ks) {
-    ks = min(ks, nks - 1);
-    int8_t* base = lds_raw + (ks % kStages) * kStageBytes;
+  // sign words: [3 loads] main rows (two), the 17th tile's rows (lanes < 8)
+  uint32_t voff_w[3], lds_w[3];
+  bool hi_word[3];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      int kk = ks * kBK + qchunk[j];
-      if (kk >= K) kk -= 32;
-      lds_dma16(qrow[j] + kk, lds_addr(base + (32 * wave + 16 * j) * kBK));
+  for (int j = 0; j < 2; ++j) {
+    const int D = 64 * j + lane;  // word D of the wave's area: t = D % 4, half = (D / 4) % 2, rho = D / 8
+    const int t = D & 3, h = (D >> 2) & 1, rr = D >> 3;
+    const int n = min(n0 + 64 * wave + 16 * t + rr, N - 1);
+    hi_word[j] = h != 0;
+    voff_w[j] = (uint32_t)(((n - n0) * W + h) * 4);
+    lds_w[j] = kQStage + 512u * wave + 256u * j;
+  }
+  {
+    const int D = 8 * wave + (lane & 7);  // word D of the 17th tile's area: rho = D / 2, half = D % 2
+    const int h = D & 1, rr = D >> 1;
+    const int n = min(n0 + 256 + rr, N - 1);
+    hi_word[2] = h != 0;
+    voff_w[2] = (uint32_t)(((n - n0) * W + h) * 4);
+    lds_w[2] = kQStage + kWMain + 32u * wave;
+  }
+  const int8_t* qbase = a.q + (int64_t)m0 * K;
+  const uint32_t* wbase = a.w_bits + (int64_t)n0 * W;
+  const uint32_t lds0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(uintptr_t)(lds_void*)lds);
+
+  auto issue = [&](int ks, int slot) {
+    const int8_t* qs = qbase + ks * kBK;
+    const uint32_t* ws = wbase + 2 * ks;
+    const uint32_t sb = lds0 + slot * kStageBytes;
+    if (ktail && ks == nks - 1) {
+      // past K: Q chunks 2, 3 re-read chunks 0, 1 and the second sign word
+      // re-reads the first (their bits are zeroed when the stage is used)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) lds_dma16(voff_q[j] - (hi_chunk[j] ? 32u : 0u), qs, sb + lds_q[j]);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) lds_dma4(voff_w[j] - (hi_word[j] ? 4u : 0u), ws, sb + lds_w[j]);
+      if (lane < 8) lds_dma4(voff_w[2] - (hi_word[2] ? 4u : 0u), ws, sb + lds_w[2]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 2; ++j) lds_dma16(voff_q[j], qs, sb + lds_q[j]);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) lds_dma4(voff_w[j], ws, sb + lds_w[j]);
+      if (lane < 8) lds_dma4(voff_w[2], ws, sb + lds_w[2]);
     }
-    lds_dma4(wrow + 2 * ks - ((2 * ks + (lane & 1)) >= W ? 1 : 0), lds_addr(base + kQStage + 32 * wave * 8));
   };
 
-  v4i acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int t = 0; t < 4; ++t) acc[i][t] = zero4();
+  // LDS read offsets: the Q operand of token tile i is row 16i + rho, chunk
+  // kg; a lane's sign words are [rho][kg / 2][0..4) of its wave's area and
+  // [rho][kg / 2] of the 17th tile's
+  const int q_off = rho * kBK + 16 * (kg ^ swz(rho));
+  const int w_off = kQStage + 512 * wave + (2 * rho + (kg >> 1)) * 16;
+  const int x_off = kQStage + kWMain + (2 * rho + (kg >> 1)) * 4;
+  const uint32_t sh = 16u * (kg & 1);
 
-  // operand addresses inside a stage: A tile i is rows 64*(wave>>1) + 16*i +
-  // row (row & 3 and (row >> 2) & 3 are the same for every i)
-  const int am_off = ((wave >> 1) * 64 + row) * kBK + 16 * (kg ^ ((row >> 2) & 3));
-  const int bn_off = ((wave & 1) * 64 + row) * 2 + (kg >> 1);
-  const int bshift = (kg & 1) * 16;
-  // operands of one stage: 4 A tiles (Q rows) and 4 B tiles (expanded signs)
-  auto read_stage = [&](int ks, v4i (&a)[4], v4i (&b)[4]) {
-    const int8_t* st = lds_raw + (ks % kStages) * kStageBytes;
-    const uint32_t* ws = reinterpret_cast<const uint32_t*>(st + kQStage);
+  typedef uint32_t raw_t __attribute__((ext_vector_type(4)));
+  struct Raw {
+    raw_t w;
+    uint32_t x;
+  };
+  // sign words of stage ks: read one stage ahead of their use
+  auto read_signs = [&](int slot) -> Raw {
+    const int8_t* st = lds + slot * kStageBytes;
+    Raw rw;
+    rw.w = *reinterpret_cast<const raw_t*>(st + w_off);
+    rw.x = *reinterpret_cast<const uint32_t*>(st + x_off);
+    return rw;
+  };
+
+  v4i acc[4][8], accx[2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const v4i*>(st + am_off + 16 * i * kBK);
-    const bool whole = 2 * ks + 1 < W;  // uniform: only a K tail has a second word past K
+  for (int t = 0; t < 4; ++t)
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      uint32_t w = ws[bn_off + 32 * t];
-      if (!whole && (kg >> 1)) w = 0;  // sign words past K count as 0
-      b[t] = expand16_at(w, bshift);
+    for (int i = 0; i < 8; ++i) acc[t][i] = zero4();
+  accx[0] = accx[1] = zero4();
+
+  // multiply stage ks: the 8 Q operands are read from LDS first; then row
+  // tile t's 8 MFMAs run while the vector ALU expands tile t+1's signs
+  const bool kg_hi = kg >= 2;
+  auto compute = [&](int ks, int slot, const Raw& rw) {
+    const int8_t* st = lds + slot * kStageBytes + q_off;
+    v4i qv[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) qv[i] = *reinterpret_cast<const v4i*>(st + i * 16 * kBK);
+    raw_t w = rw.w;
+    uint32_t wx = rw.x;
+    if (ktail && ks == nks - 1) {  // uniform: sign words past K count as 0
+#pragma unroll
+      for (int t = 0; t < 4; ++t) w[t] = kg_hi ? 0u : w[t];
+      wx = kg_hi ? 0u : wx;
+    }
+    {
+      // waves owning fewer than 4 row tiles (a short run) multiply all 4
+      // anyway: the rows past their run are valid clamped reads and their
+      // results are never stored
+      v4i sg = expand16_at(w[0], sh);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const v4i sgn = t + 1 < 4 ? expand16_at(w[t + 1], sh) : sg;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[t][i] = mfma(sg, qv[i], acc[t][i]);
+        sg = sgn;
+      }
+      // the LDS reads, the first expansion, then per row tile 8 MFMAs with
+      // the next tile's 12 expansion instructions between them
+      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);   // DS reads
+      __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);  // VALU
+#pragma unroll
+      for (int t = 0; t < 3; ++t) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // VALU
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
+        }
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    }
+    if (extra) {  // uniform: the 17th row tile, token tiles 2w and 2w+1
+      const v4i sx = expand16_at(wx, sh);
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if ((i >> 1) == wave) accx[i & 1] = mfma(sx, qv[i], accx[i & 1]);
     }
   };
-  // Software pipeline: the MFMAs of stage ks are issued together with the
-  // LDS reads and sign expansion of stage ks+1 (independent instructions,
-  // so the matrix core and the vector ALU work at the same time).  The LDS
-  // ring runs three stages ahead of the multiply.
-  v4i a0[4], b0[4], a1[4], b1[4];
-  auto step = [&](int ks, const v4i (&ac)[4], const v4i (&bc)[4], v4i (&an)[4], v4i (&bn)[4]) {
-    // stages ks+1 and ks+2 are in flight here: leaving only stage ks+2's
-    // loads outstanding means this wave's loads of stage ks+1 have landed
-    DFSSM_WAIT_VMCNT(kLoadsPerStage);
-    DFSSM_BARRIER();  // so have every wave's; stage ks-1 is no longer read
-    issue(ks + 3);
-    read_stage(ks + 1, an, bn);  // past the end: clamped loads, unused
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int t = 0; t < 4; ++t) acc[i][t] = mfma(ac[i], bc[t], acc[i][t]);
-    // interleave: after the LDS reads, one MFMA then three vector ALU ops
-    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // DS reads
-#pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // VALU
-    }
+
+  auto wait_stages = [&](int ahead) {  // at most `ahead` stages of loads in flight
+    static_assert(kStages == 4, "wait counts below");
+    if (ahead > 0)
+      DFSSM_WAIT_VMCNT(kLps);
+    else
+      DFSSM_WAIT_VMCNT(0);
   };
-  issue(0);
-  issue(1);
-  issue(2);
-  DFSSM_WAIT_VMCNT(2 * kLoadsPerStage);  // stage 0 landed, stages 1 and 2 in flight
+
+  // one stage: make stage ks+1 visible, refill the ring slot of stage ks-1
+  // (every wave has finished reading it: it passed this barrier after its
+  // multiplies of stage ks-1), read stage ks+1's sign words, multiply ks
+  auto step = [&](int ks, int slot, const Raw& wc, Raw& wn_) {
+    if (ks + 1 < nks) {
+      // stages issued beyond ks+1 may stay in flight
+      wait_stages(min(nks - 1, ks + kStages - 2) - (ks + 1));
+      DFSSM_BARRIER();
+      if (ks + kStages - 1 < nks) issue(ks + kStages - 1, (slot + kStages - 1) % kStages);
+      wn_ = read_signs((slot + 1) % kStages);
+    }
+    compute(ks, slot, wc);
+  };
+
+#pragma unroll
+  for (int p = 0; p < kStages - 1; ++p)
+    if (p < nks) issue(p, p);
+  // stage 0 has landed once at most the later prologue stages are in flight
+  if (nks >= 3)
+    DFSSM_WAIT_VMCNT(2 * kLps);
+  else if (nks == 2)
+    DFSSM_WAIT_VMCNT(kLps);
+  else
+    DFSSM_WAIT_VMCNT(0);
   DFSSM_BARRIER();
-  read_stage(0, a0, b0);
+  Raw wa = read_signs(0), wb;
   int ks = 0;
-  for (; ks + 1 < nks; ks += 2) {
-    step(ks, a0, b0, a1, b1);
-    step(ks + 1, a1, b1, a0, b0);
+  for (; ks + kStages <= nks; ks += kStages) {
+    step(ks + 0, 0, wa, wb);
+    step(ks + 1, 1, wb, wa);
+    step(ks + 2, 2, wa, wb);
+    step(ks + 3, 3, wb, wa);
   }
-  if (ks < nks) step(ks, a0, b0, a1, b1);
-  // the ring is reused below: drain the loads still in flight and wait for
-  // every wave to finish its last stage
+  if (ks < nks) step(ks, 0, wa, wb);
+  if (ks + 1 < nks) step(ks + 1, 1, wb, wa);
+  if (ks + 2 < nks) step(ks + 2, 2, wa, wb);
+  // the ring is reused below: drain and wait for every wave's last stage
   DFSSM_WAIT_VMCNT(0);
   __syncthreads();
 
-  // ---- epilogue, one n-subtile (16 output rows) at a time: the LoRA term
-  //      from four limb MFMAs (exact int64 acc_b = E_lo + 65536*E_hi) on
-  //      operands staged in LDS, then acc_s = 2*D - sum Q and
-  //      y = s*(alpha*fs + beta*fb); y leaves through a per-wave LDS
-  //      transpose as 16-byte row pieces
-  const bool baligned = (r % 16) == 0;
-  auto swz = [](int rr) { return (rr >> 2) & 3; };
-  // stage 64 LoRA columns [j0, j0+64): limbs of the tile's rows, B of its
-  // columns; 10 x 16 bytes per thread, all loads issued before the stores
-  auto stage_lora = [&](int j0) {
-    uint4 lv[8], bv[2];
+  // ---- epilogue: stage the LoRA operands of the block (rank <= 64)
+  const bool lora_lds = kLoraLds && r > 0;
+  if (lora_lds) {
+    int8_t* limb_lds = lds;               // [4][kBM][64], swizzled chunks
+    int8_t* b_lds = lds + kLimbBytes;     // [rows of the run][64], swizzled chunks
+    const bool baligned = (r % 16) == 0;
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int idx = tid + u * kThreads;  // (limb, row, 16-byte chunk)
       const int limb = idx >> 9, ml = (idx >> 2) & 127, c = idx & 3;
       const int m = min(m0 + ml, M - 1);
-      lv[u] = *reinterpret_cast<const uint4*>(limbs + ((int64_t)limb * M + m) * rp + j0 + 16 * c);
+      *reinterpret_cast<uint4*>(limb_lds + (limb * kBM + ml) * 64 + 16 * (c ^ swz(ml))) =
+          *reinterpret_cast<const uint4*>(a.limbs + ((int64_t)limb * M + m) * rp + 16 * c);
     }
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int idx = tid + u * kThreads;  // (row, 16-byte chunk)
+    for (int idx = tid; idx < 4 * nrows; idx += kThreads) {  // (row, 16-byte chunk)
       const int nl = idx >> 2, c = idx & 3;
       const int n = min(n0 + nl, N - 1);
-      const v4i b = load16_guarded(B + (int64_t)n * r, j0 + 16 * c, r, baligned);
-      bv[u] = make_uint4((uint32_t)b[0], (uint32_t)b[1], (uint32_t)b[2], (uint32_t)b[3]);
+      const v4i b = load16_guarded(a.B + (int64_t)n * r, 16 * c, r, baligned);
+      *reinterpret_cast<v4i*>(b_lds + nl * 64 + 16 * (c ^ swz(nl))) = b;
     }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int idx = tid + u * kThreads;
-      const int limb = idx >> 9, ml = (idx >> 2) & 127, c = idx & 3;
-      const uint32_t mk = m0 + ml < M ? ~0u : 0u;
-      *reinterpret_cast<uint4*>(limb_lds + (limb * kBM + ml) * kBK + 16 * (c ^ swz(ml))) =
-          make_uint4(lv[u].x & mk, lv[u].y & mk, lv[u].z & mk, lv[u].w & mk);
-    }
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int idx = tid + u * kThreads;
-      const int nl = idx >> 2, c = idx & 3;
-      const uint32_t mk = n0 + nl < N ? ~0u : 0u;
-      *reinterpret_cast<uint4*>(b_lds + nl * kBK + 16 * (c ^ swz(nl))) =
-          make_uint4(bv[u].x & mk, bv[u].y & mk, bv[u].z & mk, bv[u].w & mk);
-    }
-  };
-  if (kLoraLds && r > 0) {
-    stage_lora(0);
     __syncthreads();
   }
-  float* ybuf = reinterpret_cast<float*>(lds_raw + 4 * kBM * kBK + kBN * kBK) + wave * 16 * kYPitch;
-  const int sw = 16 * (kg ^ swz(row));
-  const bool nvec = (N & 3) == 0;  // rows of y are 16-byte aligned
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    v4i ehi[4], elo[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) ehi[i] = elo[i] = zero4();
-    const int nl = (wave & 1) * 64 + 16 * t + row;
-    const int n = n0 + nl;
-    if (r > 0) {
-#pragma unroll
-      for (int pass = 0; pass < 4; ++pass) {  // limbs 3, 2, 1, 0
-        const int limb = 3 - pass;
-        if constexpr (kLoraLds) {  // rank <= 64: one chunk, operands in LDS
-          const v4i bl = *reinterpret_cast<const v4i*>(b_lds + nl * kBK + sw);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int ml = (wave >> 1) * 64 + 16 * i + row;
-            const v4i al = *reinterpret_cast<const v4i*>(limb_lds + (limb * kBM + ml) * kBK + sw);
-            if (limb >= 2)
-              ehi[i] = mfma(al, bl, ehi[i]);
-            else
-              elo[i] = mfma(al, bl, elo[i]);
-          }
-        } else {  // higher rank: operands straight from memory
-          for (int j0 = 0; j0 < rp; j0 += 64) {
-            const int jj = j0 + 16 * kg;
-            const v4i bl = n < N ? load16_guarded(B + (int64_t)n * r, jj, r, baligned) : zero4();
-            v4i al[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int m = wm0 + 16 * i + row;
-              al[i] = m < M ? load16(limbs + ((int64_t)limb * M + m) * rp + jj) : zero4();
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              if (limb >= 2)
-                ehi[i] = mfma(al[i], bl, ehi[i]);
-              else
-                elo[i] = mfma(al[i], bl, elo[i]);
-            }
-          }
-        }
-        if (limb == 3 || limb == 1) {  // scale the high digit's sum by 256
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            if (limb == 3)
-              ehi[i] = ehi[i] << 8;
-            else
-              elo[i] = elo[i] << 8;
-          }
-        }
-      }
-    }
-    const float al = al_lds[nl], be = be_lds[nl];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int mlb = (wave >> 1) * 64 + 16 * i + 4 * kg;  // this lane's rows mlb + v
-      const float4 s4 = *reinterpret_cast<const float4*>(&s_lds[mlb]);
-      const int4 q4 = *reinterpret_cast<const int4*>(&sq_lds[mlb]);
-      const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
-      const int32_t qv[4] = {q4.x, q4.y, q4.z, q4.w};
-      float yv[4];
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int32_t as = 2 * acc[i][t][v] - qv[v];
-        const int32_t hi = ehi[i][v], lo = elo[i][v];
-        yv[v] = dfssm_dev::epilogue(sv[v], al, be, as, hi, lo, r > 0);
-        const int m = m0 + mlb + v;
-        if (m < M && n < N) {
-          if (acc_s_out) acc_s_out[(int64_t)m * N + n] = as;
-          if (acc_b_out) acc_b_out[(int64_t)m * N + n] = r > 0 ? (int64_t)lo + ((int64_t)hi << 16) : 0;
-        }
-      }
-      if (y) {
-        // [row 4*kg + v][column row] in, [row lane/4][columns 4*(lane%4)..+3]
-        // out; the buffer is this wave's own and LDS instructions of one
-        // wave complete in order, so no barrier is involved
-#pragma unroll
-        for (int v = 0; v < 4; ++v) ybuf[(4 * kg + v) * kYPitch + row] = yv[v];
-        const int mr = lane >> 2, nc = 4 * (lane & 3);
-        const float4 o = *reinterpret_cast<const float4*>(&ybuf[mr * kYPitch + nc]);
-        const int m = m0 + (wave >> 1) * 64 + 16 * i + mr;
-        const int nn = n0 + (wave & 1) * 64 + 16 * t + nc;
-        if (m < M) {
-          float* dst = y + (int64_t)m * N + nn;
-          if (nvec && nn + 3 < N) {
-            *reinterpret_cast<float4*>(dst) = o;
-          } else {
-            const float ov[4] = {o.x, o.y, o.z, o.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (nn + e < N) dst[e] = ov[e];
-          }
-        }
-      }
-    }
-  }
+  const int l_off = rho * 64 + 16 * (kg ^ swz(rho));
+  const bool fast = lora_lds && !a.acc_s_out && !a.acc_b_out && (N & 3) == 0 && m0 + kBM <= M && n0 + nrows <= N;
+  if (fast)
+    block_epilogue<true, false>(a, L, acc, accx, m0, n0, wave, ntw, extra, rho, kg, l_off);
+  else if (lora_lds)
+    block_epilogue<true, true>(a, L, acc, accx, m0, n0, wave, ntw, extra, rho, kg, l_off);
+  else
+    block_epilogue<false, true>(a, L, acc, accx, m0, n0, wave, ntw, extra, rho, kg, l_off);
+}
+
+template <bool kLoraLds>
+__global__ __launch_bounds__(kThreads, 2) void mfma_scaffold(GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) int8_t lds[kLdsBytes];
+  __shared__ __attribute__((aligned(16))) float al_lds[kMaxRows], be_lds[kMaxRows], s_lds[kBM];
+  __shared__ __attribute__((aligned(16))) int32_t sq_lds[kBM];
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  const int bm = tile / a.bpm, j = tile % a.bpm;
+  // row tiles [rt0, rt1) of the slice: runs of equal length up to one
+  const int rt0 = (int)((int64_t)j * a.nt16 / a.bpm), rt1 = (int)((int64_t)(j + 1) * a.nt16 / a.bpm);
+  const TileLds L{lds, al_lds, be_lds, s_lds, sq_lds};
+  scaffold_block<kLoraLds>(a, L, bm * kBM, rt0, rt1 - rt0);
 }
 
 }  // namespace
 
 namespace dfssm {
+
+int device_cu_count() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  int v = cache[dev].load(std::memory_order_relaxed);
+  if (v <= 0) {
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+    cache[dev].store(v, std::memory_order_relaxed);
+  }
+  return v;
+}
 
 hipError_t launch_mfma_linear(const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N,
                               int64_t r, const uint32_t* w_bits, const float* alpha,
@@ -504,7 +696,7 @@ hipError_t launch_mfma_linear(const int8_t* q, const float* s, int64_t M, int64_
                               const LinearWorkspace& ws, hipStream_t st) {
   if (M == 0 || N == 0) return hipSuccess;
   const int rp = (int)rank_padded(r);
-  mfma_lora_down<<<dim3((unsigned)ceil_div(M, 16), (unsigned)(rp / 16)), dim3(kThreads), 0, st>>>(
+  mfma_lora_down<<<dim3((unsigned)ceil_div(M, 16), (unsigned)(rp / kLdRanks)), dim3(kLdThreads), 0, st>>>(
       q, (int)M, (int)K, (int)r, rp, A, ws.acc_a, ws.limbs, ws.sumq);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -512,15 +704,22 @@ hipError_t launch_mfma_linear(const int8_t* q, const float* s, int64_t M, int64_
     e = hipMemcpyAsync(acc_a_out, ws.acc_a, (size_t)(M * r) * 4, hipMemcpyDeviceToDevice, st);
     if (e != hipSuccess) return e;
   }
-  const int64_t nbm = ceil_div(M, kBM), nbn = ceil_div(N, kBN);
+  // Tiling: each 128-token slice's ceil(N/16) row tiles are dealt to bpm
+  // blocks in runs of at most 17 whose lengths differ by at most one; bpm
+  // is chosen so the blocks fill the chip's block slots (two per CU) in
+  // whole rounds where the shape allows.
+  const int64_t slots = 2 * (int64_t)device_cu_count();
+  const int64_t nbm = ceil_div(M, kBM);
+  const int64_t nt16 = ceil_div(N, 16);
+  int64_t bpm = std::max(ceil_div(slots, nbm), ceil_div(nt16, kRunMax));
+  bpm = std::min(bpm, nt16);
+  const int64_t grid = nbm * bpm;
+  GemmArgs ga{q, s, (int)M, (int)K, (int)N, (int)r, rp, w_bits, alpha, ws.limbs, B, beta, ws.sumq, y,
+              acc_s, acc_b, (int)nt16, (int)bpm};
   if (rp == 64)
-    mfma_scaffold<true><<<dim3((unsigned)(nbm * nbn)), dim3(kThreads), 0, st>>>(
-        q, s, (int)M, (int)K, (int)N, (int)r, rp, w_bits, alpha, ws.limbs, B, beta, ws.sumq, y,
-        acc_s, acc_b, (int)nbm, (int)nbn);
+    mfma_scaffold<true><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
   else
-    mfma_scaffold<false><<<dim3((unsigned)(nbm * nbn)), dim3(kThreads), 0, st>>>(
-        q, s, (int)M, (int)K, (int)N, (int)r, rp, w_bits, alpha, ws.limbs, B, beta, ws.sumq, y,
-        acc_s, acc_b, (int)nbm, (int)nbn);
+    mfma_scaffold<false><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
   return hipGetLastError();
 }
 

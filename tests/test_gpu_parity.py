@@ -90,6 +90,16 @@ def _run_linear(env, M, K, N, r, path, beta_scale=1.0, key=0):
     return ref, host(y), host(acc_s), host(acc_a), host(acc_b)
 
 
+def _run_y_only(env, M, K, N, r, path, key=0):
+    torch, D, o = env
+    ws = S.weights(K, N, r, key=(11, M, K, N, r, key))
+    q, s = o.quantize_act(S.activations(M, K, key=(11, M, K, key)))
+    d = dev_weights(ws)
+    y = D.scaffold_lora_linear(dev(q), dev(s), d["w_bits"], d["alpha"], d["A"], d["B"], d["beta"], path=path)
+    torch.cuda.synchronize()
+    return host(y)
+
+
 @pytest.mark.parametrize("path", ["decode", "mfma"])
 @pytest.mark.parametrize("M,K,N,r", LSHAPES)
 def test_linear(env, path, M, K, N, r):
@@ -102,6 +112,10 @@ def test_linear(env, path, M, K, N, r):
         assert np.array_equal(acc_a, ref["acc_a"]), "acc_a"
     assert np.array_equal(acc_b, ref["acc_b"]), "acc_b"
     assert_y(y, ref, what=f"{path} {M}x{K}x{N} r{r}")
+    # without accumulator outputs the kernels take their unchecked epilogue
+    # on whole tiles: the same y, bit for bit
+    y2 = _run_y_only(env, M, K, N, r, p)
+    assert np.array_equal(y2.view(np.uint32), y.view(np.uint32)), "y without accumulator outputs"
 
 
 @pytest.mark.parametrize("M", [1, 4, 8, 16, 32])
@@ -149,6 +163,39 @@ def test_prefill_full_size_sampled(env):
     assert_y(host(y)[rows], ref, what="prefill sample")
     # every row: acc_s parity with the popcount identity's range bound
     assert np.abs(host(acc_s)).max() <= 127 * K
+    # the benchmark's call (no accumulator outputs: unchecked epilogue on
+    # whole tiles) gives the same y everywhere
+    y2 = D.scaffold_lora_linear(qd, sd, d["w_bits"], d["alpha"], d["A"], d["B"], d["beta"])
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
+
+
+def test_prefill_ragged_sampled(env):
+    """A prefill-sized linear with every tail at once: tokens past a whole
+    128-row tile, output rows past the 256-row tiles and past the 64-row
+    tiles, and K with a 32-column last stage.  Sampled rows (including the
+    partial token tile) against the oracle; the y of the call without
+    accumulator outputs equals the checked one everywhere."""
+    torch, D, o = env
+    M, K, N, r = 2085, 2080, 8532, 64
+    say(f"prefill ragged {M}x{K}x{N} r{r}")
+    ws = S.weights(K, N, r, key=(13,))
+    x = S.activations(M, K, key=(13,))
+    q, s = o.quantize_act(x)
+    d = dev_weights(ws)
+    qd, sd = dev(q), dev(s)
+    y, acc_s, acc_a, acc_b = D.scaffold_lora_linear(qd, sd, d["w_bits"], d["alpha"], d["A"], d["B"], d["beta"],
+                                                    acc=True)
+    y2 = D.scaffold_lora_linear(qd, sd, d["w_bits"], d["alpha"], d["A"], d["B"], d["beta"])
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, 127, 128, 2047, 2048, 2060, M - 1],
+                                     np.random.default_rng(1).choice(M, 17, replace=False)]))
+    ref = o.linear(q[rows], s[rows], **ws)
+    assert np.array_equal(host(acc_s)[rows], ref["acc_s"])
+    assert np.array_equal(host(acc_a)[rows], ref["acc_a"])
+    assert np.array_equal(host(acc_b)[rows], ref["acc_b"])
+    assert_y(host(y)[rows], ref, what="ragged prefill sample")
+    assert torch.equal(y, y2)
 
 
 def test_edge_cases(env):
