@@ -426,18 +426,6 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
   const int nrows = 16 * cnt;
   int8_t* const lds = L.lds;
 
-  // per-row and per-token scalars of the block (read after the K-loop's
-  // final barrier)
-  for (int x = tid; x < nrows; x += kThreads) {
-    const int n = min(n0 + x, N - 1);
-    L.al[x] = a.alpha[n];
-    L.be[x] = r > 0 ? a.beta[n] : 0.0f;
-  }
-  if (tid < kBM) {
-    const int m = min(m0 + tid, M - 1);
-    L.sv[tid] = a.s[m];
-    L.sq[tid] = a.sumq[m];
-  }
 
   // ---- direct-to-LDS load constants: per-lane offsets fixed for the loop
   //      (rows past M or N read the last row; their outputs are never stored)
@@ -605,6 +593,19 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
 #pragma unroll
   for (int p = 0; p < kStages - 1; ++p)
     if (p < nks) issue(p, p);
+  // per-row and per-token scalars of the block (read after the K-loop's
+  // final barrier), loaded while the prologue stages are in flight (the
+  // compiler's wait for these loads also covers the stages)
+  for (int x = tid; x < nrows; x += kThreads) {
+    const int n = min(n0 + x, N - 1);
+    L.al[x] = a.alpha[n];
+    L.be[x] = r > 0 ? a.beta[n] : 0.0f;
+  }
+  if (tid < kBM) {
+    const int m = min(m0 + tid, M - 1);
+    L.sv[tid] = a.s[m];
+    L.sq[tid] = a.sumq[m];
+  }
   // stage 0 has landed once at most the later prologue stages are in flight
   if (nks >= 3)
     DFSSM_WAIT_VMCNT(2 * kLps);

@@ -170,17 +170,19 @@ def test_prefill_full_size_sampled(env):
     assert torch.equal(y, y2)
 
 
-def test_prefill_ragged_sampled(env):
-    """A prefill-sized linear with every tail at once: tokens past a whole
-    128-row tile, output rows past the 256-row tiles and past the 64-row
-    tiles, and K with a 32-column last stage.  Sampled rows (including the
-    partial token tile) against the oracle; the y of the call without
-    accumulator outputs equals the checked one everywhere."""
+@pytest.mark.parametrize("K", [2080, 2048])
+def test_prefill_ragged_sampled(env, K):
+    """A prefill-sized linear with ragged tails: tokens past a whole 128-row
+    tile and output rows past a whole 16-row tile; K = 2080 adds a 32-column
+    last stage (general kernel), K = 2048 takes the wide kernel with its
+    shared 33rd and 34th row tiles.  Sampled rows (including the partial
+    token tile) against the oracle; the y of the call without accumulator
+    outputs equals the checked one everywhere."""
     torch, D, o = env
-    M, K, N, r = 2085, 2080, 8532, 64
+    M, N, r = 2085, 8532, 64
     say(f"prefill ragged {M}x{K}x{N} r{r}")
-    ws = S.weights(K, N, r, key=(13,))
-    x = S.activations(M, K, key=(13,))
+    ws = S.weights(K, N, r, key=(13, K))
+    x = S.activations(M, K, key=(13, K))
     q, s = o.quantize_act(x)
     d = dev_weights(ws)
     qd, sd = dev(q), dev(s)
