@@ -35,12 +35,14 @@
 //    never sits behind a weight load issued shortly before it.
 //  * Per linear: the active group relays its slice; all 16 waves poll their
 //    words of y_{l-1}[0:K_l], reducing their absmax on the way -> Q (the
-//    quantiser's fp32 decisions) -> bit-planes in LDS (ballots, gathered
-//    with v_writelane) and the workgroup's acc_a rows.  Then the active
-//    group runs the popcount GEMV on the workgroup's rows, its first wave
-//    collects the r acc_a words of the XCD and splits them into limbs in
-//    LDS, and the group does the LoRA up-projection and epilogue and stores
-//    its y rows.
+//    quantiser's fp32 decisions), the workgroup's acc_a partials and the
+//    codes as bytes in LDS; after a barrier, wave 0 publishes the
+//    workgroup's acc_a rows at once (the next phase waits on them) while
+//    threads p < K/8 build the bit-planes, each transposing the 8x8 bit
+//    matrix of codes 8p..8p+7.  Then the active group runs the popcount
+//    GEMV on the workgroup's rows, its first wave collects the r acc_a words
+//    of the XCD and splits them into limbs in LDS, and the group does the
+//    LoRA up-projection and epilogue and stores its y rows.
 //  * Row-split constants come precomputed in the layer table, and the loop
 //    index is kept uniform, so per-linear set-up runs on the scalar unit.
 //  * Every wait is bounded: on time-out the workgroup records an error in
@@ -154,41 +156,6 @@ __device__ __forceinline__ uint32_t wave_max_bits_u(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
-// Bit-planes of the codes c of column block I (one code per lane): plane
-// b's ballot gives two 32-column words, written into lanes 16*I + 2*b and
-// 16*I + 2*b + 1 of pw.  v_writelane takes the ballot from a scalar register
-// and ignores EXEC; it does not wait for a scalar register that a VALU
-// instruction (the ballot's compare) has just written, so each block of
-// writes starts with 5 wait states (s_nop 4): without them it can read the
-// previous value.
-#define DFSSM_WL8()                                                                              \
-  "s_nop 4\n\t"                                                                                    \
-  "v_writelane_b32 %0, %1, %9\n\tv_writelane_b32 %0, %2, %10\n\tv_writelane_b32 %0, %3, %11\n\t"      \
-  "v_writelane_b32 %0, %4, %12\n\tv_writelane_b32 %0, %5, %13\n\tv_writelane_b32 %0, %6, %14\n\t"     \
-  "v_writelane_b32 %0, %7, %15\n\tv_writelane_b32 %0, %8, %16"
-template <int I>
-__device__ __forceinline__ void put_planes(int c, int& qs, uint32_t& pw) {
-  qs += c;
-  uint32_t m[16];
-#pragma unroll
-  for (int b = 0; b < 8; ++b) {
-    const uint64_t mk = __ballot((c >> b) & 1);
-    m[2 * b] = (uint32_t)mk;
-    m[2 * b + 1] = (uint32_t)(mk >> 32);
-  }
-  asm(DFSSM_WL8()
-      : "+v"(pw)
-      : "s"(m[0]), "s"(m[1]), "s"(m[2]), "s"(m[3]), "s"(m[4]), "s"(m[5]), "s"(m[6]), "s"(m[7]),
-        "n"(16 * I + 0), "n"(16 * I + 1), "n"(16 * I + 2), "n"(16 * I + 3), "n"(16 * I + 4), "n"(16 * I + 5),
-        "n"(16 * I + 6), "n"(16 * I + 7));
-  asm(DFSSM_WL8()
-      : "+v"(pw)
-      : "s"(m[8]), "s"(m[9]), "s"(m[10]), "s"(m[11]), "s"(m[12]), "s"(m[13]), "s"(m[14]), "s"(m[15]),
-        "n"(16 * I + 8), "n"(16 * I + 9), "n"(16 * I + 10), "n"(16 * I + 11), "n"(16 * I + 12), "n"(16 * I + 13),
-        "n"(16 * I + 14), "n"(16 * I + 15));
-}
-#undef DFSSM_WL8
-
 // One linear's operands of this workgroup's rows, per lane of a group.
 struct Pref {
   uint4 w[kMaxSteps];
@@ -293,9 +260,10 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
   static_assert(dfssm::kChainAccRows * dfssm::kChainWgPerXcd <= 64, "limb table size");
   __shared__ uint4 limb_lds[16];
   __shared__ int32_t dot_part[kAccRows][2 * kGW];
+  __shared__ int32_t qs_part[2 * kGW];
+  __shared__ __attribute__((aligned(8))) int8_t code_lds[dfssm::kChainMaxK];
   __shared__ uint32_t ymax_lds;
   __shared__ int sumq_lds;
-  __shared__ int cnt_dot;
   __shared__ int abort_;
   __shared__ int rho_lds, nx_lds;
   const int wg = blockIdx.x, nwg = gridDim.x;
@@ -312,7 +280,6 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
   const uint32_t xcc = __builtin_amdgcn_s_getreg((20) | (0 << 6) | ((4 - 1) << 11));  // HW_REG_XCC_ID[3:0]
   if (tid == 0) {
     abort_ = 0;
-    cnt_dot = 0;
     ymax_lds = 0;
     sumq_lds = 0;
     ll_store(ex.xmap + wg, tag_place, xcc);
@@ -452,64 +419,73 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
 #pragma unroll
       for (int i = 0; i < kCols; ++i) q[i] = (zero || tid + i * kCT >= K) ? 0 : code(__uint_as_float(yv[i]), inv);
     }
-    if (rho < r) {  // acc_a rows rho + nx*t: per-wave partials in LDS, the last wave publishes
+    // LoRA down partials of rows rho + nx*t and the wave's sum of codes, one
+    // value per wave in LDS; the codes as bytes in LDS for the bit-planes
+    {
+      int qs = 0;
+#pragma unroll
+      for (int i = 0; i < kCols; ++i) qs += q[i];
+      qs = wave_sum_u(qs);
       int acc[kAccRows];
 #pragma unroll
       for (int t = 0; t < kAccRows; ++t) {
         acc[t] = 0;
+        if (rho < r) {
 #pragma unroll
-        for (int i = 0; i < kCols; ++i) acc[t] += __mul24(av[t][i], q[i]);  // |.| < 2^14: full-rate multiply
-        acc[t] = wave_sum_u(acc[t]);
+          for (int i = 0; i < kCols; ++i) acc[t] += __mul24(av[t][i], q[i]);  // |.| < 2^14: full-rate multiply
+          acc[t] = wave_sum_u(acc[t]);
+        }
       }
       if (lane == 0) {
 #pragma unroll
         for (int t = 0; t < kAccRows; ++t) dot_part[t][wave16] = acc[t];
-        // relaxed: one wave's LDS operations complete in issue order, so this
-        // wave's partials are in LDS before its count is; the signal fences
-        // keep the compiler from moving the plain LDS accesses across it (an
-        // acquire-release atomic would also wait for every outstanding
-        // global load and store of the wave)
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        const int old = __hip_atomic_fetch_add(&cnt_dot, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        if (old == 2 * kGW - 1) {
+        qs_part[wave16] = qs;
+      }
 #pragma unroll
-          for (int t = 0; t < kAccRows; ++t) {
-            const int j = rho + nx * t;
-            if (j < r) {
-              int tot = 0;
+      for (int i = 0; i < kCols; ++i)
+        if (tid + i * kCT < K) code_lds[tid + i * kCT] = (int8_t)q[i];
+    }
+    __syncthreads();  // B1
+    // wave 0 publishes the workgroup's LoRA down rows (first thing after B1:
+    // the collect of the next phase waits on these words) and sums the codes
+    if (wave16 == 0) {
+      if (lane < kAccRows) {
+        const int j = rho + nx * lane;
+        if (j < r) {
+          int tot = 0;
 #pragma unroll
-              for (int w = 0; w < 2 * kGW; ++w)
-                tot += __hip_atomic_load(&dot_part[t][w], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-              xcd_store(acc_rel + (int64_t)l * dfssm::kMaxRank + j, ((uint64_t)tag_of(l) << 32) | (uint32_t)tot);
-            }
-          }
-          cnt_dot = 0;
+          for (int w = 0; w < 2 * kGW; ++w) tot += dot_part[lane][w];
+          xcd_store(acc_rel + (int64_t)l * dfssm::kMaxRank + j, ((uint64_t)tag_of(l) << 32) | (uint32_t)tot);
         }
+      } else if (lane == kAccRows) {
+        int tot = 0;
+#pragma unroll
+        for (int w = 0; w < 2 * kGW; ++w) tot += qs_part[w];
+        sumq_lds = tot;
       }
     }
-    // wave16 holds columns kCT*i + 64*wave16 + lane: one ballot per plane
-    // gives two plane words; they are gathered into one register, lane
-    // 16*i + 2*b + h holding half h of plane b of column block i, and stored
-    // with one LDS write per lane
-    {
-      static_assert(kCols * 16 == 64, "one plane word per lane");
-      int qs = 0;
-      uint32_t pw = 0;
-      static_assert(kCols == 4, "column blocks below");
-      if (0 * kCT < K) put_planes<0>(q[0], qs, pw);
-      if (1 * kCT < K) put_planes<1>(q[1], qs, pw);
-      if (2 * kCT < K) put_planes<2>(q[2], qs, pw);
-      if (3 * kCT < K) put_planes<3>(q[3], qs, pw);
-      {
-        const int i = lane >> 4, b = (lane >> 1) & 7;
-        if (i * kCT < K) {
-          const int word = (i * kCT + wave16 * 64) / 32 + (lane & 1);
-          reinterpret_cast<uint32_t*>(pl_lds)[(b * kChunks + (word >> 2)) * 4 + (word & 3)] = pw;
-        }
-      }
-      qs = wave_sum_u(qs);
-      if (lane == 0) __hip_atomic_fetch_add(&sumq_lds, qs, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    // bit-planes: thread p < K/8 transposes the 8x8 bit matrix of codes
+    // 8p .. 8p+7 (byte i = code i) so that byte b holds bit b of the 8 codes,
+    // i.e. byte p of plane b (plane-major, 16-byte chunks of 128 columns)
+    if (tid < (K >> 3)) {
+      const uint2 c = reinterpret_cast<const uint2*>(code_lds)[tid];
+      uint32_t lo = c.x, hi = c.y, t;
+      t = (lo ^ (lo >> 7)) & 0x00AA00AAu;
+      lo ^= t ^ (t << 7);
+      t = (hi ^ (hi >> 7)) & 0x00AA00AAu;
+      hi ^= t ^ (t << 7);
+      t = (lo ^ (lo >> 14)) & 0x0000CCCCu;
+      lo ^= t ^ (t << 14);
+      t = (hi ^ (hi >> 14)) & 0x0000CCCCu;
+      hi ^= t ^ (t << 14);
+      t = (lo ^ __builtin_amdgcn_alignbit(hi, lo, 28)) & 0xF0F0F0F0u;
+      lo ^= t;
+      hi ^= t >> 4;
+      uint8_t* pb = reinterpret_cast<uint8_t*>(pl_lds) + tid;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) pb[b * kChunks * 16] = (uint8_t)(lo >> (8 * b));
+#pragma unroll
+      for (int b = 0; b < 4; ++b) pb[(4 + b) * kChunks * 16] = (uint8_t)(hi >> (8 * b));
     }
     __syncthreads();  // B2
     if (abort_) return;
@@ -568,7 +544,6 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
     }
     __syncthreads();  // B3
     if (abort_) return;
-    if (tid == 0) sumq_lds = 0;  // every read of it came before B3
 
     // ---- 3. LoRA up-projection, epilogue, publish; prefetch linear l+2 ----
     if (active) {
