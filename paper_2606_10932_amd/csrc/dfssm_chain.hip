@@ -217,11 +217,13 @@ __device__ __forceinline__ void load_a_cols(const dfssm::ChainLayerDev& L, int t
   }
 }
 
+// Bounded polls of one {tag, value} word; they also give up once another
+// wave of the workgroup has aborted (abort_ in LDS).
 __device__ __forceinline__ bool poll_ll(const uint64_t* p, uint32_t tag, uint64_t& wd,
-                                        unsigned* status, unsigned code_bit) {
+                                        unsigned* status, unsigned code_bit, const int* abort_flag) {
   long spins = 0;
   while ((uint32_t)((wd = ll_load(p)) >> 32) != tag) {
-    if (++spins > kSpinLimit) {
+    if (++spins > kSpinLimit || *(const volatile int*)abort_flag) {
       atomicOr(status, code_bit);
       return false;
     }
@@ -230,10 +232,10 @@ __device__ __forceinline__ bool poll_ll(const uint64_t* p, uint32_t tag, uint64_
   return true;
 }
 __device__ __forceinline__ bool poll_xcd(__amdgpu_buffer_rsrc_t rs, uint32_t word, uint32_t tag, uint64_t& wd,
-                                         unsigned* status, unsigned code_bit) {
+                                         unsigned* status, unsigned code_bit, const int* abort_flag) {
   long spins = 0;
   while ((uint32_t)((wd = xcd_load(rs, word)) >> 32) != tag) {
-    if (++spins > kSpinLimit) {
+    if (++spins > kSpinLimit || *(const volatile int*)abort_flag) {
       atomicOr(status, code_bit);
       return false;
     }
@@ -262,7 +264,13 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
   __shared__ int32_t dot_part[kAccRows][2 * kGW];
   __shared__ int32_t qs_part[2 * kGW];
   __shared__ __attribute__((aligned(8))) int8_t code_lds[dfssm::kChainMaxK];
-  __shared__ uint32_t ymax_lds;
+  // absmax of the previous output as {linear, bits}: the largest tag wins,
+  // so it needs no reset between linears
+  __shared__ uint64_t ymax_lds;
+  // phase counters (monotonic): waves of the active group whose bit-planes
+  // are in LDS (+kGW per linear) and that have published (+kGW per linear);
+  // the linear whose limbs are in LDS (+1 per linear)
+  __shared__ int pl_cnt, limb_flag, pub_cnt;
   __shared__ int sumq_lds;
   __shared__ int abort_;
   __shared__ int rho_lds, nx_lds;
@@ -281,6 +289,9 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
   if (tid == 0) {
     abort_ = 0;
     ymax_lds = 0;
+    pl_cnt = 0;
+    pub_cnt = 0;
+    limb_flag = 0;
     sumq_lds = 0;
     ll_store(ex.xmap + wg, tag_place, xcc);
   }
@@ -293,7 +304,7 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
       x[t] = 0xffu;
       if (w < nwg) {
         uint64_t wd;
-        if (!poll_ll(ex.xmap + w, tag_place, wd, status, kStPlace)) ok = false;
+        if (!poll_ll(ex.xmap + w, tag_place, wd, status, kStPlace, &abort_)) ok = false;
         x[t] = (uint32_t)wd;
       }
     }
@@ -359,7 +370,7 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
         const int k1 = min(K, (rho + 1) * slice);
         for (int k = rho * slice + gt; k < k1; k += kGT) {
           uint64_t wd;
-          if (!poll_ll(ex.y_ll + prev + k, tag, wd, status, kStY)) {
+          if (!poll_ll(ex.y_ll + prev + k, tag, wd, status, kStY, &abort_)) {
             abort_ = 1;
             break;
           }
@@ -367,6 +378,17 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
         }
       }
       if (rho < r) load_a_cols(Ld, tid, rho, nx, av);
+      // the group active in this linear arrives early (it was idle after the
+      // last B1); it starts polling only once its own workgroup has
+      // published its rows of y_{l-1}: earlier, its polls would only load
+      // the XCD's L2, which the exchange of the previous linear still uses
+      if (active) {
+        long sp = 0;
+        while (__hip_atomic_load(&pub_cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) < kGW * l) {
+          if (++sp > kSpinLimit || abort_) break;
+          __builtin_amdgcn_s_sleep(1);
+        }
+      }
       uint32_t pend = 0;
 #pragma unroll
       for (int i = 0; i < kCols; ++i)
@@ -386,7 +408,7 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
             pend &= ~(1u << i);
           }
         if (pend) {
-          if (++spins > kSpinLimit) {
+          if (++spins > kSpinLimit || abort_) {
             atomicOr(status, kStY);
             abort_ = 1;
             break;
@@ -395,7 +417,8 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
         }
       }
       m = wave_max_bits_u(m);
-      if (lane == 0) __hip_atomic_fetch_max(&ymax_lds, m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      if (lane == 0)
+        __hip_atomic_fetch_max(&ymax_lds, ((uint64_t)l << 32) | m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     } else if (rho < r) {
       load_a_cols(Ld, tid, rho, nx, av);
     }
@@ -413,7 +436,7 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
         q[i] = k < K ? c : 0;
       }
     } else {
-      const float a = __uint_as_float(ymax_lds);
+      const float a = __uint_as_float((uint32_t)ymax_lds);
       const bool zero = a < FLT_MIN;
       const float inv = zero ? 0.0f : 127.0f / a;
 #pragma unroll
@@ -446,65 +469,107 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
         if (tid + i * kCT < K) code_lds[tid + i * kCT] = (int8_t)q[i];
     }
     __syncthreads();  // B1
-    // wave 0 publishes the workgroup's LoRA down rows (first thing after B1:
-    // the collect of the next phase waits on these words) and sums the codes
-    if (wave16 == 0) {
-      if (lane < kAccRows) {
-        const int j = rho + nx * lane;
-        if (j < r) {
-          int tot = 0;
-#pragma unroll
-          for (int w = 0; w < 2 * kGW; ++w) tot += dot_part[lane][w];
-          xcd_store(acc_rel + (int64_t)l * dfssm::kMaxRank + j, ((uint64_t)tag_of(l) << 32) | (uint32_t)tot);
-        }
-      } else if (lane == kAccRows) {
-        int tot = 0;
-#pragma unroll
-        for (int w = 0; w < 2 * kGW; ++w) tot += qs_part[w];
-        sumq_lds = tot;
-      }
-    }
-    // bit-planes: thread p < K/8 transposes the 8x8 bit matrix of codes
-    // 8p .. 8p+7 (byte i = code i) so that byte b holds bit b of the 8 codes,
-    // i.e. byte p of plane b (plane-major, 16-byte chunks of 128 columns)
-    if (tid < (K >> 3)) {
-      const uint2 c = reinterpret_cast<const uint2*>(code_lds)[tid];
-      uint32_t lo = c.x, hi = c.y, t;
-      t = (lo ^ (lo >> 7)) & 0x00AA00AAu;
-      lo ^= t ^ (t << 7);
-      t = (hi ^ (hi >> 7)) & 0x00AA00AAu;
-      hi ^= t ^ (t << 7);
-      t = (lo ^ (lo >> 14)) & 0x0000CCCCu;
-      lo ^= t ^ (t << 14);
-      t = (hi ^ (hi >> 14)) & 0x0000CCCCu;
-      hi ^= t ^ (t << 14);
-      t = (lo ^ __builtin_amdgcn_alignbit(hi, lo, 28)) & 0xF0F0F0F0u;
-      lo ^= t;
-      hi ^= t >> 4;
-      uint8_t* pb = reinterpret_cast<uint8_t*>(pl_lds) + tid;
-#pragma unroll
-      for (int b = 0; b < 4; ++b) pb[b * kChunks * 16] = (uint8_t)(lo >> (8 * b));
-#pragma unroll
-      for (int b = 0; b < 4; ++b) pb[(4 + b) * kChunks * 16] = (uint8_t)(hi >> (8 * b));
-    }
-    __syncthreads();  // B2
     if (abort_) return;
-    if (tid == 0) ymax_lds = 0;  // every read of it came before B2
-    // the group idle in this linear loads the weights of the next one now:
-    // none of its waits before its next GEMV are latency-critical, whereas
-    // loads issued earlier would hold up its polls in this linear (a wave's
-    // loads complete in order)
-    if (!active && l >= 1 && l + 1 < L) prefetch(layers[lu + 1], wg, gt, pf);
 
-    // ---- 2. scaffold GEMV on the prefetched rows; collect acc_a -----------
+    // After B1 the two groups part until the next linear's B0:
+    //  * the idle group's first wave publishes this workgroup's LoRA down
+    //    rows, sums the codes, collects the XCD's acc_a words into limbs in
+    //    LDS and raises limb_flag; the rest of the idle group (and then that
+    //    wave) loads the weights of linear l+1;
+    //  * the active group builds the bit-planes, waits for all 8 of its
+    //    waves to have written them (pl_cnt), runs the GEMV, waits for
+    //    limb_flag, and does the LoRA up-projection and epilogue.
+    // A wave's LDS operations complete in issue order, so a counter or flag
+    // raised after a wave's LDS writes is seen only after those writes; the
+    // signal fences keep the compiler from moving LDS accesses across them.
+    // Every LDS written here is next written after the next linear's B1, so
+    // the next B0 orders its reuse.
     const int RW = 64 >> lgG;
     const int g = lane & (G - 1);
-    int part[kMaxSteps];
-    if (active) {
-      // one bit-plane at a time: weight c_b = 2^b (b < 7), -128 (b = 7);
-      // acc_s = 2 * sum_{bit=1} Q - sum Q
+    if (!active) {
+      if (gt < 64) {
+        if (lane < kAccRows) {
+          const int j = rho + nx * lane;
+          if (j < r) {
+            int tot = 0;
+#pragma unroll
+            for (int w = 0; w < 2 * kGW; ++w) tot += dot_part[lane][w];
+            xcd_store(acc_rel + (int64_t)l * dfssm::kMaxRank + j, ((uint64_t)tag_of(l) << 32) | (uint32_t)tot);
+          }
+        } else if (lane == kAccRows) {
+          int tot = 0;
+#pragma unroll
+          for (int w = 0; w < 2 * kGW; ++w) tot += qs_part[w];
+          sumq_lds = tot;
+        }
+        // lane j collects acc_a[j] (0 past r) and stores its 4 signed
+        // base-256 limbs as bytes of limb_lds[j / 4], dword t = limb t
+        int32_t v = 0;
+        if (gt < r) {
+          const uint32_t tag = tag_of(l);
+          const uint32_t word = (uint32_t)(l * dfssm::kMaxRank + gt);
+          uint64_t wd;
+          if (!poll_xcd(rs_acc, word, tag, wd, status, kStAcc, &abort_)) abort_ = 1;
+          v = (int32_t)(uint32_t)wd;
+        }
+        int8_t d[4];
+        dfssm_dev::split_limbs(v, d);
+        uint8_t* lb = reinterpret_cast<uint8_t*>(limb_lds) + (gt >> 2) * 16 + (gt & 3);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) lb[4 * t] = (uint8_t)d[t];
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        if (lane == 0) __hip_atomic_store(&limb_flag, l + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      }
+      // the group idle in this linear loads the weights of the next one
+      // (it polls nothing more in this linear; its first wave has finished
+      // its collect above)
+      if (l >= 1 && l + 1 < L) prefetch(layers[lu + 1], wg, gt, pf);
+    } else {
+      // bit-planes: thread p < K/8 of the group transposes the 8x8 bit
+      // matrix of codes 8p .. 8p+7 (byte i = code i) so that byte b holds
+      // bit b of the 8 codes, i.e. byte p of plane b (plane-major, 16-byte
+      // chunks of 128 columns)
+      if (gt < (K >> 3)) {
+        const uint2 c = reinterpret_cast<const uint2*>(code_lds)[gt];
+        uint32_t lo = c.x, hi = c.y, t;
+        t = (lo ^ (lo >> 7)) & 0x00AA00AAu;
+        lo ^= t ^ (t << 7);
+        t = (hi ^ (hi >> 7)) & 0x00AA00AAu;
+        hi ^= t ^ (t << 7);
+        t = (lo ^ (lo >> 14)) & 0x0000CCCCu;
+        lo ^= t ^ (t << 14);
+        t = (hi ^ (hi >> 14)) & 0x0000CCCCu;
+        hi ^= t ^ (t << 14);
+        t = (lo ^ __builtin_amdgcn_alignbit(hi, lo, 28)) & 0xF0F0F0F0u;
+        lo ^= t;
+        hi ^= t >> 4;
+        uint8_t* pb = reinterpret_cast<uint8_t*>(pl_lds) + gt;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) pb[b * kChunks * 16] = (uint8_t)(lo >> (8 * b));
+#pragma unroll
+        for (int b = 0; b < 4; ++b) pb[(4 + b) * kChunks * 16] = (uint8_t)(hi >> (8 * b));
+      }
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      if (lane == 0) __hip_atomic_fetch_add(&pl_cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      {
+        long spins = 0;
+        while (__hip_atomic_load(&pl_cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) < kGW * (l + 1)) {
+          if (++spins > kSpinLimit || abort_) {
+            atomicOr(status, kStAcc);
+            abort_ = 1;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+        }
+      }
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+
+      // ---- 2. scaffold GEMV on the prefetched rows: one bit-plane at a
+      //      time, weight c_b = 2^b (b < 7), -128 (b = 7); acc_s =
+      //      2 * sum_{bit=1} Q - sum Q (sum Q subtracted below)
+      int part[kMaxSteps];
       const int C = K >> 7;
-      const int sq = sumq_lds;
       const int n0 = wg * R, n1 = min(N, n0 + R);
 #pragma unroll
       for (int st = 0; st < kMaxSteps; ++st) {
@@ -520,61 +585,55 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
                           __builtin_popcount(w.z & Pb.z) + __builtin_popcount(w.w & Pb.w);
             dsum += b < 7 ? (c << b) : -(c << 7);
           }
-          part[st] = 2 * group_sum(dsum, G) - sq;
+          part[st] = 2 * group_sum(dsum, G);
         }
       }
-      if (gt < 64) {
-        // wave 0 of the group: lane j collects acc_a[j] (0 past r) and
-        // stores its 4 signed base-256 limbs as bytes of limb_lds[j / 4],
-        // dword t = limb t, byte j % 4
-        int32_t v = 0;
-        if (gt < r) {
-          const uint32_t tag = tag_of(l);
-          const uint32_t word = (uint32_t)(l * dfssm::kMaxRank + gt);
-          uint64_t wd;
-          if (!poll_xcd(rs_acc, word, tag, wd, status, kStAcc)) abort_ = 1;
-          v = (int32_t)(uint32_t)wd;
+      {
+        long spins = 0;
+        while (__hip_atomic_load(&limb_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) < l + 1) {
+          if (++spins > kSpinLimit || abort_) {
+            atomicOr(status, kStAcc);
+            abort_ = 1;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
         }
-        int8_t d[4];
-        dfssm_dev::split_limbs(v, d);
-        uint8_t* lb = reinterpret_cast<uint8_t*>(limb_lds) + (gt >> 2) * 16 + (gt & 3);
-#pragma unroll
-        for (int t = 0; t < 4; ++t) lb[4 * t] = (uint8_t)d[t];
       }
-    }
-    __syncthreads();  // B3
-    if (abort_) return;
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
 
-    // ---- 3. LoRA up-projection, epilogue, publish; prefetch linear l+2 ----
-    if (active) {
-      const int r4 = (r + 3) >> 2;
-      const int grp = lane >> lgG;
-      const int n0 = wg * R, n1 = min(N, n0 + R);
-      // limbs of acc_a[4g .. 4g+3], packed per limb (j >= r read as 0)
-      uint32_t lb0 = 0, lb1 = 0, lb2 = 0, lb3 = 0;
-      if (r > 0 && g < r4) {
-        const uint4 t = limb_lds[g];
-        lb0 = t.x;
-        lb1 = t.y;
-        lb2 = t.z;
-        lb3 = t.w;
-      }
+      // ---- 3. LoRA up-projection, epilogue, publish --------------------------
+      if (!abort_) {
+        const int sq = sumq_lds;
+        const int r4 = (r + 3) >> 2;
+        const int grp = lane >> lgG;
+        // limbs of acc_a[4g .. 4g+3], packed per limb (j >= r read as 0)
+        uint32_t lb0 = 0, lb1 = 0, lb2 = 0, lb3 = 0;
+        if (r > 0 && g < r4) {
+          const uint4 t = limb_lds[g];
+          lb0 = t.x;
+          lb1 = t.y;
+          lb2 = t.z;
+          lb3 = t.w;
+        }
 #pragma unroll
-      for (int st = 0; st < kMaxSteps; ++st) {
-        if (n0 + st * kGW * RW + wave * RW >= n1) break;  // uniform per wave
-        int elo = 0, ehi = 0;
-        if (r > 0) {
-          const uint32_t bw = pf.b[st];
-          elo = group_sum(sdot4(bw, lb0, 0) + (sdot4(bw, lb1, 0) << 8), G);
-          ehi = group_sum(sdot4(bw, lb2, 0) + (sdot4(bw, lb3, 0) << 8), G);
-        }
-        const int n = n0 + st * kGW * RW + wave * RW + grp;
-        if (g == 0 && n < n1) {
-          const float y = dfssm_dev::epilogue(s, pf.al[st], pf.be[st], part[st], ehi, elo, r > 0);
-          ll_store(ex.y_ll + Ld.y_off + n, tag_of(l), __float_as_uint(y));
-          y_all[Ld.y_off + n] = y;
+        for (int st = 0; st < kMaxSteps; ++st) {
+          if (n0 + st * kGW * RW + wave * RW >= n1) break;  // uniform per wave
+          int elo = 0, ehi = 0;
+          if (r > 0) {
+            const uint32_t bw = pf.b[st];
+            elo = group_sum(sdot4(bw, lb0, 0) + (sdot4(bw, lb1, 0) << 8), G);
+            ehi = group_sum(sdot4(bw, lb2, 0) + (sdot4(bw, lb3, 0) << 8), G);
+          }
+          const int n = n0 + st * kGW * RW + wave * RW + grp;
+          if (g == 0 && n < n1) {
+            const float y = dfssm_dev::epilogue(s, pf.al[st], pf.be[st], part[st] - sq, ehi, elo, r > 0);
+            ll_store(ex.y_ll + Ld.y_off + n, tag_of(l), __float_as_uint(y));
+            y_all[Ld.y_off + n] = y;
+          }
         }
       }
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      if (lane == 0) __hip_atomic_fetch_add(&pub_cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
     // the next linear's B0 orders every LDS reuse
   }
