@@ -202,18 +202,22 @@ __device__ __forceinline__ void prefetch(const dfssm::ChainLayerDev& L, int wg, 
 }
 
 // This thread's bytes of the LoRA down rows rho + n_x*t (t < kAccRows) of a
-// linear, in the column layout of the codes: a[t][i] is column tid + kCT*i.
+// linear, in the column layout of the codes: byte i of a[t] is column
+// tid + kCT*i (columns past K read column 0; their codes are 0).
 __device__ __forceinline__ void load_a_cols(const dfssm::ChainLayerDev& L, int tid, int rho, int nx,
-                                            int32_t (&a)[kAccRows][kCols]) {
+                                            uint32_t (&a)[kAccRows]) {
+  static_assert(kCols == 4, "four bytes per packed word");
 #pragma unroll
   for (int t = 0; t < kAccRows; ++t) {
     const int j = rho + nx * t;
     const int8_t* arow = L.A + (int64_t)(j < L.r ? j : 0) * L.K;
+    uint32_t w = 0;
 #pragma unroll
     for (int i = 0; i < kCols; ++i) {
       const int k = tid + i * kCT;
-      a[t][i] = gload1s(arow + (k < L.K ? k : 0));
+      w |= (uint32_t)(gload1s(arow + (k < L.K ? k : 0)) & 0xff) << (8 * i);
     }
+    a[t] = w;
   }
 }
 
@@ -261,9 +265,9 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
   // entry g holds acc_a[4g .. 4g+3], dword t = limb t (r <= 64)
   static_assert(dfssm::kChainAccRows * dfssm::kChainWgPerXcd <= 64, "limb table size");
   __shared__ uint4 limb_lds[16];
-  __shared__ int32_t dot_part[kAccRows][2 * kGW];
-  __shared__ int32_t qs_part[2 * kGW];
-  __shared__ __attribute__((aligned(8))) int8_t code_lds[dfssm::kChainMaxK];
+  __shared__ int32_t dot_part[kAccRows][64];  // 16-lane row sums of the 16 waves
+  static_assert(4 * 2 * kGW == 64, "row sums per rank");
+  __shared__ __attribute__((aligned(16))) int8_t code_lds[dfssm::kChainMaxK];
   // absmax of the previous output as {linear, bits}: the largest tag wins,
   // so it needs no reset between linears
   __shared__ uint64_t ymax_lds;
@@ -360,7 +364,7 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
     //         y_{l-1}[0:K] into the XCD's copy; then every thread loads its
     //         A bytes and polls its words of the copy (columns tid + kCT*i)
     //         until all carry tag(l-1); their absmax is reduced into LDS
-    int32_t av[kAccRows][kCols];
+    uint32_t av[kAccRows];  // this thread's A bytes of the two rows, column i in byte i
     uint32_t yv[kCols];
     if (l > 0) {
       const int64_t prev = layers[lu - 1].y_off;
@@ -427,46 +431,44 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
 
     // ---- 1. codes, LoRA down rows, bit-planes: all 16 waves, columns
     //         tid + kCT*i ----------------------------------------------------
+    // column blocks i with tid + kCT*i < K for some thread (uniform)
     int q[kCols];
     if (l == 0) {
 #pragma unroll
       for (int i = 0; i < kCols; ++i) {
-        const int k = tid + i * kCT;
-        const int c = gload1s(q0 + (k < K ? k : 0));
-        q[i] = k < K ? c : 0;
+        q[i] = 0;
+        if (i * kCT < K) {
+          const int k = tid + i * kCT;
+          const int c = gload1s(q0 + (k < K ? k : 0));
+          q[i] = k < K ? c : 0;
+        }
       }
     } else {
       const float a = __uint_as_float((uint32_t)ymax_lds);
       const bool zero = a < FLT_MIN;
       const float inv = zero ? 0.0f : 127.0f / a;
 #pragma unroll
-      for (int i = 0; i < kCols; ++i) q[i] = (zero || tid + i * kCT >= K) ? 0 : code(__uint_as_float(yv[i]), inv);
-    }
-    // LoRA down partials of rows rho + nx*t and the wave's sum of codes, one
-    // value per wave in LDS; the codes as bytes in LDS for the bit-planes
-    {
-      int qs = 0;
-#pragma unroll
-      for (int i = 0; i < kCols; ++i) qs += q[i];
-      qs = wave_sum_u(qs);
-      int acc[kAccRows];
-#pragma unroll
-      for (int t = 0; t < kAccRows; ++t) {
-        acc[t] = 0;
-        if (rho < r) {
-#pragma unroll
-          for (int i = 0; i < kCols; ++i) acc[t] += __mul24(av[t][i], q[i]);  // |.| < 2^14: full-rate multiply
-          acc[t] = wave_sum_u(acc[t]);
-        }
+      for (int i = 0; i < kCols; ++i) {
+        q[i] = 0;
+        if (i * kCT < K) q[i] = (zero || tid + i * kCT >= K) ? 0 : code(__uint_as_float(yv[i]), inv);
       }
-      if (lane == 0) {
+    }
+    // LoRA down partials of rows rho + nx*t: the 4 codes against the 4 A
+    // bytes with one v_dot4, summed over each 16-lane row; the 64 row sums
+    // go to LDS.  The codes go to LDS as bytes (bit-planes, sum of codes).
+    {
+      const uint32_t qp = (uint32_t)(q[0] & 0xff) | ((uint32_t)(q[1] & 0xff) << 8) |
+                          ((uint32_t)(q[2] & 0xff) << 16) | ((uint32_t)q[3] << 24);
+      if (rho < r) {
 #pragma unroll
-        for (int t = 0; t < kAccRows; ++t) dot_part[t][wave16] = acc[t];
-        qs_part[wave16] = qs;
+        for (int t = 0; t < kAccRows; ++t) {
+          const int v = dpp_sum16(sdot4(av[t], qp, 0));
+          if ((lane & 15) == 0) dot_part[t][4 * wave16 + (lane >> 4)] = v;
+        }
       }
 #pragma unroll
       for (int i = 0; i < kCols; ++i)
-        if (tid + i * kCT < K) code_lds[tid + i * kCT] = (int8_t)q[i];
+        if (i * kCT < K && tid + i * kCT < K) code_lds[tid + i * kCT] = (int8_t)q[i];
     }
     __syncthreads();  // B1
     if (abort_) return;
@@ -488,19 +490,29 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
     const int g = lane & (G - 1);
     if (!active) {
       if (gt < 64) {
-        if (lane < kAccRows) {
-          const int j = rho + nx * lane;
-          if (j < r) {
-            int tot = 0;
+        if (rho < r) {
+          static_assert(kAccRows == 2, "two rows per workgroup below");
+          int tot[kAccRows];
 #pragma unroll
-            for (int w = 0; w < 2 * kGW; ++w) tot += dot_part[lane][w];
-            xcd_store(acc_rel + (int64_t)l * dfssm::kMaxRank + j, ((uint64_t)tag_of(l) << 32) | (uint32_t)tot);
+          for (int t = 0; t < kAccRows; ++t) tot[t] = wave_sum_u(dot_part[t][lane]);
+          if (lane < kAccRows) {
+            const int j = rho + nx * lane;
+            if (j < r)
+              xcd_store(acc_rel + (int64_t)l * dfssm::kMaxRank + j,
+                        ((uint64_t)tag_of(l) << 32) | (uint32_t)(lane == 0 ? tot[0] : tot[1]));
           }
-        } else if (lane == kAccRows) {
-          int tot = 0;
-#pragma unroll
-          for (int w = 0; w < 2 * kGW; ++w) tot += qs_part[w];
-          sumq_lds = tot;
+        }
+        {  // sum of the codes, 16 bytes per lane per pass
+          int qs = 0;
+          for (int k = 16 * lane; k < K; k += 16 * 64) {
+            const uint4 c = *reinterpret_cast<const uint4*>(code_lds + k);
+            qs = sdot4(c.x, 0x01010101u, qs);
+            qs = sdot4(c.y, 0x01010101u, qs);
+            qs = sdot4(c.z, 0x01010101u, qs);
+            qs = sdot4(c.w, 0x01010101u, qs);
+          }
+          qs = wave_sum_u(qs);
+          if (lane == 0) sumq_lds = qs;
         }
         // lane j collects acc_a[j] (0 past r) and stores its 4 signed
         // base-256 limbs as bytes of limb_lds[j / 4], dword t = limb t
