@@ -76,9 +76,14 @@ typedef enum { DFSSM_F16 = 0, DFSSM_F32 = 1 } dfssm_dtype;
 
 /* Kernel family selection for dfssm_scaffold_lora_linear_ex. */
 typedef enum {
-  DFSSM_PATH_AUTO = 0,    /* decode kernels for small M, MFMA kernels above */
-  DFSSM_PATH_DECODE = 1,  /* bit-plane popcount GEMV (any M, best for M <= 4) */
-  DFSSM_PATH_MFMA = 2     /* sign bits expanded on chip + int8 MFMA */
+  DFSSM_PATH_AUTO = 0,     /* popcount GEMV for M = 1, few-token MFMA for
+                              M <= 32, prefill MFMA above */
+  DFSSM_PATH_DECODE = 1,   /* bit-plane popcount GEMV (any M, best for M <= 4) */
+  DFSSM_PATH_MFMA = 2,     /* sign bits expanded on chip + int8 MFMA, tiles of
+                              128 tokens (prefill) */
+  DFSSM_PATH_MFMA_FEW = 3  /* the same expansion and MFMA for M <= 32: 16
+                              output rows per workgroup, K split over its
+                              waves; M > 32 gives DFSSM_ERR_UNSUPPORTED */
 } dfssm_path;
 
 /* Per-token absmax int8 quantisation of the activations (the int8 operand

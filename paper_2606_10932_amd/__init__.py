@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(HERE, "libdfssm.so")
 
 OK, ERR_NULL, ERR_SHAPE, ERR_ALIGN, ERR_WORKSPACE, ERR_DEVICE, ERR_UNSUPPORTED = range(7)
 F16, F32 = 0, 1
-PATH_AUTO, PATH_DECODE, PATH_MFMA = 0, 1, 2
+PATH_AUTO, PATH_DECODE, PATH_MFMA, PATH_MFMA_FEW = 0, 1, 2, 3
 
 EXPORTS = ["dfssm_quantize_act", "dfssm_linear_workspace_bytes", "dfssm_scaffold_lora_linear",
            "dfssm_scaffold_lora_linear_ex", "dfssm_chain_workspace_bytes",

@@ -73,6 +73,24 @@ size_t linear_ws_bytes(int64_t M, int64_t K, int64_t r) {
   return dfssm::carve_linear_workspace(nullptr, M, K, r).bytes;
 }
 
+// Kernel family for a linear: the popcount GEMV up to kDecodeM0 tokens, the
+// split-K MFMA kernel up to kSkinnyMaxTokens, the prefill MFMA kernel above.
+hipError_t launch_linear(int path, const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N, int64_t r,
+                         const uint32_t* w_bits, const float* alpha, const int8_t* A, const int8_t* B,
+                         const float* beta, float* y, int32_t* acc_s, int32_t* acc_a, int64_t* acc_b,
+                         const dfssm::LinearWorkspace& ws, hipStream_t hs) {
+  if (path == DFSSM_PATH_AUTO)
+    path = M <= dfssm::kDecodeM0 ? DFSSM_PATH_DECODE
+                                 : (M <= dfssm::kSkinnyMaxTokens ? DFSSM_PATH_MFMA_FEW : DFSSM_PATH_MFMA);
+  if (path == DFSSM_PATH_DECODE)
+    return dfssm::launch_decode_linear(q, s, M, K, N, r, w_bits, alpha, A, B, beta, y, acc_s, acc_a, acc_b, ws,
+                                       hs);
+  if (path == DFSSM_PATH_MFMA_FEW)
+    return dfssm::launch_skinny_linear(q, s, M, K, N, r, w_bits, alpha, A, B, beta, y, acc_s, acc_a, acc_b, ws,
+                                       hs);
+  return dfssm::launch_mfma_linear(q, s, M, K, N, r, w_bits, alpha, A, B, beta, y, acc_s, acc_a, acc_b, ws, hs);
+}
+
 }  // namespace
 
 extern "C" {
@@ -128,8 +146,12 @@ dfssm_status dfssm_scaffold_lora_linear_ex(const int8_t* q, const float* s, int6
   clear_error();
   dfssm_status st = check_linear(M, K, N, r);
   if (st != DFSSM_OK) return st;
-  if (path != DFSSM_PATH_AUTO && path != DFSSM_PATH_DECODE && path != DFSSM_PATH_MFMA)
+  if (path != DFSSM_PATH_AUTO && path != DFSSM_PATH_DECODE && path != DFSSM_PATH_MFMA &&
+      path != DFSSM_PATH_MFMA_FEW)
     return fail(DFSSM_ERR_SHAPE, "path=%d", path);
+  if (path == DFSSM_PATH_MFMA_FEW && M > dfssm::kSkinnyMaxTokens)
+    return fail(DFSSM_ERR_UNSUPPORTED, "path=%d takes M <= %lld, got M=%lld", path,
+                (long long)dfssm::kSkinnyMaxTokens, (long long)M);
   if (M == 0 || N == 0) return DFSSM_OK;
   st = check_ptrs({{q, "q"}, {s, "s"}, {w_bits, "w_bits"}, {alpha, "alpha"}, {workspace, "workspace"}},
                   {{y, "y"}, {acc_s, "acc_s"}, {acc_a, "acc_a"}, {acc_b, "acc_b"}});
@@ -142,13 +164,8 @@ dfssm_status dfssm_scaffold_lora_linear_ex(const int8_t* q, const float* s, int6
   if (workspace_bytes < need)
     return fail(DFSSM_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, need);
   dfssm::LinearWorkspace ws = dfssm::carve_linear_workspace(workspace, M, K, r);
-  if (path == DFSSM_PATH_AUTO) path = M <= dfssm::kDecodeM0 ? DFSSM_PATH_DECODE : DFSSM_PATH_MFMA;
-  hipStream_t hs = (hipStream_t)stream;
-  hipError_t e = path == DFSSM_PATH_DECODE
-                     ? dfssm::launch_decode_linear(q, s, M, K, N, r, w_bits, alpha, A, B, beta, y,
-                                                   acc_s, acc_a, acc_b, ws, hs)
-                     : dfssm::launch_mfma_linear(q, s, M, K, N, r, w_bits, alpha, A, B, beta, y,
-                                                 acc_s, acc_a, acc_b, ws, hs);
+  hipError_t e = launch_linear(path, q, s, M, K, N, r, w_bits, alpha, A, B, beta, y, acc_s, acc_a, acc_b, ws,
+                               (hipStream_t)stream);
   return e == hipSuccess ? DFSSM_OK : device_fail(e, "linear launch");
 }
 
@@ -360,8 +377,8 @@ dfssm_status dfssm_chain_run(const dfssm_layer* layers, int n_layers, int64_t M,
       sl = sbuf;
     }
     dfssm::LinearWorkspace ws = dfssm::carve_linear_workspace(base + c.off_lin, M, L.K, L.r);
-    hipError_t e = dfssm::launch_decode_linear(ql, sl, M, L.K, L.N, L.r, L.w_bits, L.alpha, L.A, L.B,
-                                               L.beta, y_cur, nullptr, nullptr, nullptr, ws, hs);
+    hipError_t e = launch_linear(DFSSM_PATH_AUTO, ql, sl, M, L.K, L.N, L.r, L.w_bits, L.alpha, L.A, L.B,
+                                 L.beta, y_cur, nullptr, nullptr, nullptr, ws, hs);
     if (e != hipSuccess) return device_fail(e, "chain linear launch");
     y_prev = y_cur;
     y_cur += M * L.N;

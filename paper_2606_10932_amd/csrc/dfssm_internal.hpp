@@ -18,8 +18,11 @@ constexpr int64_t kMaxRank = 256;
 // Largest M the bit-plane decode kernels take in one pass; larger M on the
 // decode path is processed in blocks of this many tokens.
 constexpr int kDecodeMaxTokens = 4;
-// Automatic dispatch: M <= kDecodeM0 uses the decode kernels.
-constexpr int64_t kDecodeM0 = 4;
+// Automatic dispatch: M <= kDecodeM0 uses the popcount decode kernels, M up
+// to kSkinnyMaxTokens the few-token MFMA kernel, larger M the prefill MFMA
+// kernel (measured on MI355X: at one token the popcount GEMV is the faster,
+// from two tokens on the few-token MFMA kernel).
+constexpr int64_t kDecodeM0 = 1;
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
@@ -29,7 +32,7 @@ inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 //   limbs  int8  [4][M][rp]       acc_a split into 4 signed base-256 digits,
 //                                 rp = r rounded up to 64 (zero padded)
 //   sumq   int32 [M]              sum_k Q[m,k]
-//   planes uint32 [M][C][8][4]    two's-complement bit-planes of Q, C =
+//   planes uint32 [M][8][C][4]    two's-complement bit-planes of Q, C =
 //                                 ceil(K/128) chunks of 4 words (zero padded)
 struct LinearWorkspace {
   int32_t* acc_a;
@@ -74,6 +77,21 @@ hipError_t launch_quantize(const void* x, int x_dtype, int64_t M, int64_t K, int
 // Decode path: prep (acc_a, bit-planes) then the popcount GEMV with the
 // fused LoRA up-projection and epilogue.
 hipError_t launch_decode_linear(const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N,
+                                int64_t r, const uint32_t* w_bits, const float* alpha,
+                                const int8_t* A, const int8_t* B, const float* beta, float* y,
+                                int32_t* acc_s, int32_t* acc_a_out, int64_t* acc_b,
+                                const LinearWorkspace& ws, hipStream_t st);
+
+// LoRA down-projection for few tokens into the workspace (acc_a, limbs,
+// sum Q) and, with planes, the bit-planes of Q.
+hipError_t launch_small_prep(const int8_t* q, int64_t M, int64_t K, int64_t r, const int8_t* A,
+                             const LinearWorkspace& ws, bool planes, hipStream_t st);
+
+// Few tokens (M <= kSkinnyMaxTokens) on the matrix cores: small_prep, then
+// a split-K expanded-sign int8 MFMA kernel with the LoRA up-projection and
+// epilogue (16 output rows per workgroup).
+constexpr int64_t kSkinnyMaxTokens = 32;
+hipError_t launch_skinny_linear(const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N,
                                 int64_t r, const uint32_t* w_bits, const float* alpha,
                                 const int8_t* A, const int8_t* B, const float* beta, float* y,
                                 int32_t* acc_s, int32_t* acc_a_out, int64_t* acc_b,

@@ -118,6 +118,51 @@ def test_linear(env, path, M, K, N, r):
     assert np.array_equal(y2.view(np.uint32), y.view(np.uint32)), "y without accumulator outputs"
 
 
+# few-token MFMA path (M <= 32): 1 or 2 token tiles, 8- and 16-byte sign
+# loads, K splits of one or more iterations per wave, unaligned sign rows,
+# ragged N, rank 0, rank not a multiple of 16 and ranks above 64
+FSHAPES = [
+    (1, 768, 3352, 16),      # Mamba-2-130M in_proj: 3 waves
+    (1, 2048, 8512, 64),     # Mamba-2-1.3B in_proj
+    (5, 4096, 2048, 64),     # Mamba-2-1.3B out_proj, small batches
+    (16, 4096, 2048, 64),
+    (17, 4096, 2048, 64),
+    (32, 4096, 2048, 64),
+    (3, 160, 77, 5),         # odd sign-row length, N % 4 != 0, r % 16 != 0
+    (1, 32, 1, 0),
+    (9, 96, 33, 1),
+    (2, 256, 31, 256),       # four 64-rank chunks
+    (20, 8192, 130, 64),     # two iterations per wave
+    (32, 4128, 50, 72),      # K % 512 != 0 with 16-byte sign loads, odd row length
+    (12, 12288, 70, 32),
+    (31, 2048, 300, 64),
+]
+
+
+@pytest.mark.parametrize("M,K,N,r", FSHAPES)
+def test_linear_few_tokens(env, M, K, N, r):
+    torch, D, o = env
+    say(f"linear path=few M={M} K={K} N={N} r={r}")
+    ref, y, acc_s, acc_a, acc_b = _run_linear(env, M, K, N, r, D.PATH_MFMA_FEW)
+    assert np.array_equal(acc_s, ref["acc_s"]), "acc_s"
+    if r:
+        assert np.array_equal(acc_a, ref["acc_a"]), "acc_a"
+    assert np.array_equal(acc_b, ref["acc_b"]), "acc_b"
+    assert_y(y, ref, what=f"few {M}x{K}x{N} r{r}")
+    y2 = _run_y_only(env, M, K, N, r, D.PATH_MFMA_FEW)
+    assert np.array_equal(y2.view(np.uint32), y.view(np.uint32)), "y without accumulator outputs"
+
+
+def test_few_tokens_limit(env):
+    """The few-token path refuses M > 32 before launching anything."""
+    torch, D, o = env
+    ws = dev_weights(S.weights(64, 16, 4, key=(14,)))
+    q = torch.zeros((33, 64), dtype=torch.int8, device="cuda")
+    s = torch.zeros((33,), dtype=torch.float32, device="cuda")
+    with pytest.raises(D.DfssmError):
+        D.scaffold_lora_linear(q, s, ws["w_bits"], ws["alpha"], ws["A"], ws["B"], ws["beta"], path=D.PATH_MFMA_FEW)
+
+
 @pytest.mark.parametrize("M", [1, 4, 8, 16, 32])
 def test_out_proj_small_batch_auto(env, M):
     """Mamba-2-1.3B out_proj at the small-batch decode sizes, automatic path."""
@@ -212,7 +257,7 @@ def test_edge_cases(env):
     y = D.scaffold_lora_linear(q0, s0, d["w_bits"], d["alpha"], d["A"], d["B"], d["beta"])
     assert y.shape == (0, N)
     # all-zero activations -> y = 0; A = 0 -> scaffold only
-    for path in (D.PATH_DECODE, D.PATH_MFMA):
+    for path in (D.PATH_DECODE, D.PATH_MFMA, D.PATH_MFMA_FEW):
         x = np.zeros((3, K), np.float32)
         x[1] = S.activations(1, K, key=(12, 1))[0]
         q, s = o.quantize_act(x)
