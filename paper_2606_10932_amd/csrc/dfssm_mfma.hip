@@ -199,33 +199,44 @@ __global__ __launch_bounds__(kLdThreads) void mfma_lora_down(const int8_t* __res
 // feeds 8 MFMAs, and the Q tile in LDS is shared by the 4 waves); a 17th row
 // tile is shared by all 4 waves, wave w taking its token tiles 2w and 2w+1.
 //
-// K-loop: 64 K per stage through a kStages-deep LDS ring filled by
-// direct-to-LDS loads (global_load_lds with a scalar base and a per-lane
-// offset that stays fixed, so the loop does no address arithmetic):
-//   Q stage: 128 rows x 64 bytes, the four 16-byte chunks of row m stored
-//            at chunk slot c ^ ((m >> 1) & 3), so each 8 lanes of a 16-byte
-//            LDS read hit 8 distinct 4-bank groups of the 32 banks;
-//   sign stage: per wave, 64 rows x 2 words ordered [rho][half][t] (a lane
-//            fetches its 4 row tiles' words with one LDS read), then the
-//            17th row tile's 16 rows x 2 words.
-// Each wave issues 5 loads per stage (the 17th tile's words are loaded
-// whether or not the run has one), so "stage ks has landed" is a count of
-// vector-memory operations.
+// K-loop: 64 K per stage; operands reach LDS by direct-to-LDS loads
+// (global_load_lds with a scalar base and a per-lane offset that stays
+// fixed, so the loop does no per-lane address arithmetic):
+//   Q stage: a kStages-deep ring of 128 rows x 64 bytes, the four 16-byte
+//            chunks of row m stored at chunk slot c ^ ((m >> 1) & 3), so each
+//            8 lanes of a 16-byte LDS read hit 8 distinct 4-bank groups of
+//            the 32 banks;
+//   signs:   loaded per "sign group" of kSgStages stages, i.e. 32 bytes of
+//            each row, into two alternating buffers: per wave its 64 rows
+//            (row tiles 4w .. 4w+3), then the 17th row tile's 16 rows, each
+//            row as 8 words.  A load instruction covers 8 whole rows (lane i:
+//            word i % 8 of row i / 8), so it touches 8 cache lines where a
+//            load of one stage's words of 32 rows touched 32.  Word j of a
+//            row (16-row tile position rho) sits at slot j ^ (2*((rho >> 2) & 3)),
+//            which makes the per-stage 4-byte reads of 16 rows x 2 words hit
+//            32 distinct banks.
+// Each wave issues 2 Q loads per stage and 9 sign loads per sign group (the
+// 17th tile's words whether or not the run has one), so "stage ks has
+// landed" is a count of vector-memory operations.
 constexpr int kThreads = 256;
 constexpr int kBM = 128;
 constexpr int kBK = 64;
 constexpr int kStages = 4;
 constexpr int kRunMax = 17;                             // row tiles per block
 constexpr int kQStage = kBM * kBK;                      // 8 KB
-constexpr int kWMain = 4 * 64 * 8;                      // 2 KB: 4 waves x 64 rows x 8 bytes
-constexpr int kStageBytes = kQStage + kWMain + 16 * 8;  // + the 17th tile's words
-constexpr int kLps = 5;                                 // loads per wave per stage
-constexpr int kLdsRing = kStages * kStageBytes;         // 40.5 KB
+constexpr int kQRing = kStages * kQStage;               // 32 KB
+constexpr int kSgStages = 4;                            // stages per sign group (8 words per row)
+constexpr int kSgWave = 64 * 32;                        // 2 KB: a wave's 64 rows x 32 bytes
+constexpr int kSgBuf = 4 * kSgWave + 16 * 32;           // + the 17th tile's rows: 8.5 KB
+constexpr int kLq = 2;                                  // Q loads per wave per stage
+constexpr int kLsg = 9;                                 // sign loads per wave per sign group
+constexpr int kLdsRing = kQRing + 2 * kSgBuf;           // 49 KB
 constexpr int kLimbBytes = 4 * kBM * 64;                // LoRA limbs of the tile, 64 ranks
 constexpr int kLdsLora = kLimbBytes + kRunMax * 16 * 64;  // + B rows of the run
 constexpr int kLdsBytes = kLdsRing > kLdsLora ? kLdsRing : kLdsLora;
 constexpr int kMaxRows = kRunMax * 16;
-static_assert(4 * kLps <= 63, "vector-memory counter range");
+static_assert(kSgStages == kStages, "a sign group is one pass over the Q ring");
+static_assert(2 * kLq + kLsg + kLq <= 63, "vector-memory counter range");
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -248,6 +259,15 @@ __device__ __forceinline__ void lds_dma4(uint32_t voff, const void* sbase, uint3
 // (the compiler's barrier fence would wait for all of them); LDS visibility
 // of the loads is ordered by the DFSSM_WAIT_VMCNT before it
 #define DFSSM_BARRIER() asm volatile("s_barrier" ::: "memory")
+
+// A zero the compiler cannot see through: per-lane arithmetic of rarely
+// taken edge paths that uses it stays inside the K-loop instead of being
+// hoisted into registers that would live across the loop.
+__device__ __forceinline__ int opaque_zero() {
+  int z;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+  return z;
+}
 
 // 16-byte chunk swizzle of 64-byte rows: conflict-free 16-byte reads of one
 // chunk column on gfx950's 32-bank LDS
@@ -440,57 +460,88 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
     voff_q[j] = (uint32_t)((min(m0 + m, M - 1) - m0) * K + 16 * c);
     lds_q[j] = 1024u * (2 * wave + j);
   }
-  // sign words: [3 loads] main rows (two), the 17th tile's rows (lanes < 8)
-  uint32_t voff_w[3], lds_w[3];
-  bool hi_word[3];
+  // sign words, per sign group: 8 loads of the wave's rows (lane i: row
+  // 8j + i / 8 of the wave's 64, word slot i % 8), then the 17th tile's rows
+  // 4w .. 4w+3 (lanes < 32).  Rows 8j + i/8 have (row >> 2) & 3 =
+  // (2j + i / 32) & 3, so the swizzled word a lane fetches depends on j only
+  // through its parity.  Rows past N read row N - 1 (never stored).
+  const bool sg_fast = n0 + 64 * wave + 64 <= N;  // uniform: no row of the wave is clamped
+  uint32_t voff_s[2];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int D = 64 * j + lane;  // word D of the wave's area: t = D % 4, half = (D / 4) % 2, rho = D / 8
-    const int t = D & 3, h = (D >> 2) & 1, rr = D >> 3;
-    const int n = min(n0 + 64 * wave + 16 * t + rr, N - 1);
-    hi_word[j] = h != 0;
-    voff_w[j] = (uint32_t)(((n - n0) * W + h) * 4);
-    lds_w[j] = kQStage + 512u * wave + 256u * j;
+  for (int jp = 0; jp < 2; ++jp) {
+    const int wd = (lane & 7) ^ (2 * ((2 * jp + (lane >> 5)) & 3));
+    voff_s[jp] = (uint32_t)((((lane >> 3) + 64 * wave) * W + wd) * 4);
   }
+  uint32_t voff_x;
   {
-    const int D = 8 * wave + (lane & 7);  // word D of the 17th tile's area: rho = D / 2, half = D % 2
-    const int h = D & 1, rr = D >> 1;
+    const int rr = 4 * wave + (lane >> 3);  // row of the 17th tile (< 16 for lanes < 32)
+    const int wd = (lane & 7) ^ (2 * ((rr >> 2) & 3));
     const int n = min(n0 + 256 + rr, N - 1);
-    hi_word[2] = h != 0;
-    voff_w[2] = (uint32_t)(((n - n0) * W + h) * 4);
-    lds_w[2] = kQStage + kWMain + 32u * wave;
+    voff_x = (uint32_t)(((n - n0) * W + wd) * 4);
   }
   const int8_t* qbase = a.q + (int64_t)m0 * K;
   const uint32_t* wbase = a.w_bits + (int64_t)n0 * W;
   const uint32_t lds0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(uintptr_t)(lds_void*)lds);
 
+  // the sign group of stages 4g .. 4g+3 into buffer g % 2; the last group
+  // may reach past the row (K % 256 != 0): its words are clamped to the
+  // row's last word, and a stage that would use them does not exist (or has
+  // its second word zeroed: K % 64 == 32)
+  auto issue_signs = [&](int g) {
+    const uint32_t sb = lds0 + kQRing + (g & 1) * kSgBuf;
+    const uint32_t* ws = wbase + 8 * g;
+    const bool whole = 8 * g + 8 <= W;  // uniform
+    if (sg_fast && whole) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) lds_dma4(voff_s[j & 1], ws + (int64_t)8 * j * W, sb + kSgWave * wave + 256u * j);
+    } else {
+      const int ln = lane + opaque_zero();
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int rl = 8 * j + (ln >> 3);  // row of the wave's 64
+        const int wd = (ln & 7) ^ (2 * ((rl >> 2) & 3));
+        const int n = min(n0 + 64 * wave + rl, N - 1);
+        const int wc = min(8 * g + wd, W - 1) - 8 * g;
+        lds_dma4((uint32_t)(((n - n0) * W + wc) * 4), ws, sb + kSgWave * wave + 256u * j);
+      }
+    }
+    {
+      uint32_t vx = voff_x;
+      if (!whole) {
+        const int ln = lane + opaque_zero();
+        const int rr = 4 * wave + (ln >> 3);
+        const int wd = (ln & 7) ^ (2 * ((rr >> 2) & 3));
+        const int n = min(n0 + 256 + rr, N - 1);
+        vx = (uint32_t)(((n - n0) * W + min(8 * g + wd, W - 1) - 8 * g) * 4);
+      }
+      if (lane < 32) lds_dma4(vx, ws, sb + 4 * kSgWave + 128u * wave);
+    }
+  };
+  // stage ks's Q into ring slot `slot`, preceded (ks % 4 == 0) by its sign group
   auto issue = [&](int ks, int slot) {
+    if (slot == 0) issue_signs(ks >> 2);
     const int8_t* qs = qbase + ks * kBK;
-    const uint32_t* ws = wbase + 2 * ks;
-    const uint32_t sb = lds0 + slot * kStageBytes;
+    const uint32_t sb = lds0 + slot * kQStage;
     if (ktail && ks == nks - 1) {
-      // past K: Q chunks 2, 3 re-read chunks 0, 1 and the second sign word
-      // re-reads the first (their bits are zeroed when the stage is used)
+      // past K: Q chunks 2, 3 re-read chunks 0, 1 (their sign bits are
+      // zeroed when the stage is used)
 #pragma unroll
       for (int j = 0; j < 2; ++j) lds_dma16(voff_q[j] - (hi_chunk[j] ? 32u : 0u), qs, sb + lds_q[j]);
-#pragma unroll
-      for (int j = 0; j < 2; ++j) lds_dma4(voff_w[j] - (hi_word[j] ? 4u : 0u), ws, sb + lds_w[j]);
-      if (lane < 8) lds_dma4(voff_w[2] - (hi_word[2] ? 4u : 0u), ws, sb + lds_w[2]);
     } else {
 #pragma unroll
       for (int j = 0; j < 2; ++j) lds_dma16(voff_q[j], qs, sb + lds_q[j]);
-#pragma unroll
-      for (int j = 0; j < 2; ++j) lds_dma4(voff_w[j], ws, sb + lds_w[j]);
-      if (lane < 8) lds_dma4(voff_w[2], ws, sb + lds_w[2]);
     }
   };
 
   // LDS read offsets: the Q operand of token tile i is row 16i + rho, chunk
-  // kg; a lane's sign words are [rho][kg / 2][0..4) of its wave's area and
-  // [rho][kg / 2] of the 17th tile's
+  // kg; a lane's sign word of stage s (of its group) is word 2s + kg / 2 of
+  // rows 16t + rho of its wave's area and of the 17th tile's area, at the
+  // swizzled slot
   const int q_off = rho * kBK + 16 * (kg ^ swz(rho));
-  const int w_off = kQStage + 512 * wave + (2 * rho + (kg >> 1)) * 16;
-  const int x_off = kQStage + kWMain + (2 * rho + (kg >> 1)) * 4;
+  // row rho of the wave's area plus the byte of the word slot before the
+  // stage's ^ 8s (bits 3-4 of the row offset are zero, so ^ acts on the slot)
+  const int w_off = kQRing + kSgWave * wave + 32 * rho + 4 * ((kg >> 1) ^ (2 * ((rho >> 2) & 3)));
+  const int x_delta = (4 - wave) * kSgWave;  // uniform: the 17th tile's area
   const uint32_t sh = 16u * (kg & 1);
 
   typedef uint32_t raw_t __attribute__((ext_vector_type(4)));
@@ -498,12 +549,15 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
     raw_t w;
     uint32_t x;
   };
-  // sign words of stage ks: read one stage ahead of their use
-  auto read_signs = [&](int slot) -> Raw {
-    const int8_t* st = lds + slot * kStageBytes;
+  // sign words of stage ks (group ks / 4, stage ks % 4 of it): read one
+  // stage ahead of their use
+  auto read_signs = [&](int ks) -> Raw {
+    const int8_t* st = lds + ((ks >> 2) & 1) * kSgBuf;
+    const int wb = w_off ^ (8 * (ks & 3));
     Raw rw;
-    rw.w = *reinterpret_cast<const raw_t*>(st + w_off);
-    rw.x = *reinterpret_cast<const uint32_t*>(st + x_off);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) rw.w[t] = *reinterpret_cast<const uint32_t*>(st + wb + 512 * t);
+    rw.x = *reinterpret_cast<const uint32_t*>(st + x_delta + wb);
     return rw;
   };
 
@@ -518,7 +572,7 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
   // tile t's 8 MFMAs run while the vector ALU expands tile t+1's signs
   const bool kg_hi = kg >= 2;
   auto compute = [&](int ks, int slot, const Raw& rw) {
-    const int8_t* st = lds + slot * kStageBytes + q_off;
+    const int8_t* st = lds + slot * kQStage + q_off;
     v4i qv[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) qv[i] = *reinterpret_cast<const v4i*>(st + i * 16 * kBK);
@@ -568,24 +622,26 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
     }
   };
 
-  auto wait_stages = [&](int ahead) {  // at most `ahead` stages of loads in flight
-    static_assert(kStages == 4, "wait counts below");
-    if (ahead > 0)
-      DFSSM_WAIT_VMCNT(kLps);
-    else
-      DFSSM_WAIT_VMCNT(0);
-  };
-
   // one stage: make stage ks+1 visible, refill the ring slot of stage ks-1
   // (every wave has finished reading it: it passed this barrier after its
-  // multiplies of stage ks-1), read stage ks+1's sign words, multiply ks
+  // multiplies of stage ks-1) and, at a group start, the sign buffer of the
+  // group before last; read stage ks+1's sign words, multiply ks.  Only the
+  // loads of stage ks+2 (issued one step earlier, with its sign group when
+  // ks+2 starts one) may stay in flight.
   auto step = [&](int ks, int slot, const Raw& wc, Raw& wn_) {
+    static_assert(kStages == 4, "wait counts below");
     if (ks + 1 < nks) {
-      // stages issued beyond ks+1 may stay in flight
-      wait_stages(min(nks - 1, ks + kStages - 2) - (ks + 1));
+      if (ks + 2 < nks) {
+        if ((slot + 2) % kStages == 0)
+          DFSSM_WAIT_VMCNT(kLq + kLsg);
+        else
+          DFSSM_WAIT_VMCNT(kLq);
+      } else {
+        DFSSM_WAIT_VMCNT(0);
+      }
       DFSSM_BARRIER();
       if (ks + kStages - 1 < nks) issue(ks + kStages - 1, (slot + kStages - 1) % kStages);
-      wn_ = read_signs((slot + 1) % kStages);
+      wn_ = read_signs(ks + 1);
     }
     compute(ks, slot, wc);
   };
@@ -606,11 +662,12 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
     L.sv[tid] = a.s[m];
     L.sq[tid] = a.sumq[m];
   }
-  // stage 0 has landed once at most the later prologue stages are in flight
+  // stage 0 (with sign group 0) has landed once at most the later prologue
+  // stages' Q loads are in flight
   if (nks >= 3)
-    DFSSM_WAIT_VMCNT(2 * kLps);
+    DFSSM_WAIT_VMCNT(2 * kLq);
   else if (nks == 2)
-    DFSSM_WAIT_VMCNT(kLps);
+    DFSSM_WAIT_VMCNT(kLq);
   else
     DFSSM_WAIT_VMCNT(0);
   DFSSM_BARRIER();
