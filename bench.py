@@ -44,6 +44,7 @@ def parse():
     p.add_argument("--copies", type=int, default=3, help="distinct weight copies rotated per step")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--no-prefill", action="store_true")
+    p.add_argument("--no-decode", action="store_true", help="skip the single-linear decode-size figures")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="minimum CPU oracle sample time")
     p.add_argument("--copy-calibration-mib", type=int, default=0,
                    help="run one plain device copy of this size first (for HBM counter scaling)")
@@ -192,6 +193,57 @@ def main():
                    "algorithmic_tops": round((ops + lora_ops) / (pms * 1e-3) / 1e12, 1),
                    "frac_i8_peak": round(ops / (pms * 1e-3) / 1e12 / PEAK_I8_TOPS, 4)}
 
+    # ---- single linears at decode sizes ---------------------------------------
+    # Per call: q, s -> y on the automatic path (the one-launch few-token
+    # MFMA kernel up to 32 tokens).  The calls of one graph replay walk
+    # over distinct copies of the weights, about 600 MB in all, so every call
+    # meets its weights outside the 256 MB Infinity Cache; the graph removes
+    # the host's launch cost from the measurement.
+    decode = None
+    if not args.no_decode:
+        decode = []
+        for cfg, name, Ms in ((0, "Mamba-2-130M in_proj K=768 N=3352 r=16", (1,)),
+                              (1, "Mamba-2-1.3B in_proj K=2048 N=8512 r=64", (1,)),
+                              (2, "Mamba-2-1.3B out_proj K=4096 N=2048 r=64", (1, 4, 8, 16, 32))):
+            hw = S.config_weights(cfg)
+            wb = S.weight_bytes(hw)
+            base = {k: dev(v) for k, v in hw.items()}
+            ncall = int(np.ceil(600e6 / wb))
+            cps = [base] + [{k: v.clone() for k, v in base.items()} for _ in range(ncall - 1)]
+            K, N = hw["A"].shape[1], hw["w_bits"].shape[0]
+            r = hw["A"].shape[0]
+            for m in Ms:
+                qd, sd = D.quantize_act(dev(S.config_activations(cfg, m)))
+                yd = torch.empty((m, N), dtype=torch.float32, device="cuda")
+                wsd = torch.empty(D.linear_workspace_bytes(m, K, N, r), dtype=torch.uint8, device="cuda")
+
+                def calls():
+                    for c in cps:
+                        D.scaffold_lora_linear(qd, sd, c["w_bits"], c["alpha"], c["A"], c["B"], c["beta"], y=yd,
+                                               workspace=wsd)
+                side = torch.cuda.Stream()
+                side.wait_stream(torch.cuda.current_stream())
+                with torch.cuda.stream(side):
+                    calls()
+                    g = torch.cuda.CUDAGraph()
+                    with torch.cuda.graph(g, stream=side):
+                        calls()
+                torch.cuda.synchronize()
+                g.replay()
+                torch.cuda.synchronize()
+                reps = 3
+                t0.record(stream)
+                for _ in range(reps):
+                    g.replay()
+                t1.record(stream)
+                torch.cuda.synchronize()
+                us = t0.elapsed_time(t1) * 1e3 / (reps * ncall)
+                decode.append({"workload": f"{name} M={m}", "us_per_call": round(us, 2),
+                               "weight_gbs": round(wb / (us * 1e-6) / 1e9, 1), "weight_bytes": wb,
+                               "path": "few-token MFMA (one launch)"})
+                del g
+            del cps, base
+
     # ---- CPU oracle baseline on a bounded sample ----------------------------
     cpu = None
     if not args.no_cpu:
@@ -236,6 +288,7 @@ def main():
                      "traffic": traffic, "avg_launch_us": round(launch_ms * 1e3, 2),
                      "algorithmic_bytes_per_launch": weight_bytes},
         "prefill": prefill,
+        "decode_linears": decode,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

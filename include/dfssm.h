@@ -76,14 +76,20 @@ typedef enum { DFSSM_F16 = 0, DFSSM_F32 = 1 } dfssm_dtype;
 
 /* Kernel family selection for dfssm_scaffold_lora_linear_ex. */
 typedef enum {
-  DFSSM_PATH_AUTO = 0,     /* popcount GEMV for M = 1, few-token MFMA for
-                              M <= 32, prefill MFMA above */
+  DFSSM_PATH_AUTO = 0,     /* few-token MFMA for M <= 32, prefill MFMA
+                              above */
   DFSSM_PATH_DECODE = 1,   /* bit-plane popcount GEMV (any M, best for M <= 4) */
   DFSSM_PATH_MFMA = 2,     /* sign bits expanded on chip + int8 MFMA, tiles of
                               128 tokens (prefill) */
-  DFSSM_PATH_MFMA_FEW = 3  /* the same expansion and MFMA for M <= 32: 16
-                              output rows per workgroup, K split over its
-                              waves; M > 32 gives DFSSM_ERR_UNSUPPORTED */
+  DFSSM_PATH_MFMA_FEW = 3  /* the same expansion and MFMA for M <= 32 in one
+                              launch: 16 output rows per workgroup, K split
+                              over its waves, the LoRA down-projection in
+                              workgroups of the same grid; M > 32 gives
+                              DFSSM_ERR_UNSUPPORTED.  Test switch: with the
+                              environment variable DFSSM_TEST_LOCAL_LORA=1
+                              no LoRA workgroups run and every output
+                              workgroup computes those values itself (the
+                              path it takes when they never arrive). */
 } dfssm_path;
 
 /* Per-token absmax int8 quantisation of the activations (the int8 operand

@@ -73,8 +73,9 @@ size_t linear_ws_bytes(int64_t M, int64_t K, int64_t r) {
   return dfssm::carve_linear_workspace(nullptr, M, K, r).bytes;
 }
 
-// Kernel family for a linear: the popcount GEMV up to kDecodeM0 tokens, the
-// split-K MFMA kernel up to kSkinnyMaxTokens, the prefill MFMA kernel above.
+// Kernel family for a linear: the popcount GEMV up to kDecodeM0 tokens (none
+// by default), the one-launch few-token MFMA kernel up to kSkinnyMaxTokens,
+// the prefill MFMA kernel above.
 hipError_t launch_linear(int path, const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N, int64_t r,
                          const uint32_t* w_bits, const float* alpha, const int8_t* A, const int8_t* B,
                          const float* beta, float* y, int32_t* acc_s, int32_t* acc_a, int64_t* acc_b,

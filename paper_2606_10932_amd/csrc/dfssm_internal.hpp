@@ -20,9 +20,11 @@ constexpr int64_t kMaxRank = 256;
 constexpr int kDecodeMaxTokens = 4;
 // Automatic dispatch: M <= kDecodeM0 uses the popcount decode kernels, M up
 // to kSkinnyMaxTokens the few-token MFMA kernel, larger M the prefill MFMA
-// kernel (measured on MI355X: at one token the popcount GEMV is the faster,
-// from two tokens on the few-token MFMA kernel).
-constexpr int64_t kDecodeM0 = 1;
+// kernel.  Measured on MI355X, the single-launch few-token kernel is the
+// faster one from one token on (the popcount GEMV needs a second launch for
+// the LoRA down-projection and the bit-planes), so the popcount kernels run
+// on request and inside the persistent chain.
+constexpr int64_t kDecodeM0 = 0;
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
@@ -34,11 +36,14 @@ inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 //   sumq   int32 [M]              sum_k Q[m,k]
 //   planes uint32 [M][8][C][4]    two's-complement bit-planes of Q, C =
 //                                 ceil(K/128) chunks of 4 words (zero padded)
+//   xw     uint64 [M*rp + M]      {tag, value} words of the few-token kernel:
+//                                 acc_a limbs per (token, rank), then sum Q
 struct LinearWorkspace {
   int32_t* acc_a;
   int8_t* limbs;
   int32_t* sumq;
   uint32_t* planes;
+  uint64_t* xw;
   size_t bytes;
 };
 
@@ -57,11 +62,13 @@ inline LinearWorkspace carve_linear_workspace(void* base, int64_t M, int64_t K, 
   size_t o_limb = take((size_t)(4 * M * rank_padded(r)));
   size_t o_sum = take((size_t)M * 4);
   size_t o_pl = take((size_t)(M * plane_chunks(K) * 128));
+  size_t o_xw = take((size_t)(M * rank_padded(r) + M) * 8);
   char* b = static_cast<char*>(base);
   ws.acc_a = reinterpret_cast<int32_t*>(b + o_acc);
   ws.limbs = reinterpret_cast<int8_t*>(b + o_limb);
   ws.sumq = reinterpret_cast<int32_t*>(b + o_sum);
   ws.planes = reinterpret_cast<uint32_t*>(b + o_pl);
+  ws.xw = reinterpret_cast<uint64_t*>(b + o_xw);
   ws.bytes = off;
   return ws;
 }
@@ -87,9 +94,10 @@ hipError_t launch_decode_linear(const int8_t* q, const float* s, int64_t M, int6
 hipError_t launch_small_prep(const int8_t* q, int64_t M, int64_t K, int64_t r, const int8_t* A,
                              const LinearWorkspace& ws, bool planes, hipStream_t st);
 
-// Few tokens (M <= kSkinnyMaxTokens) on the matrix cores: small_prep, then
-// a split-K expanded-sign int8 MFMA kernel with the LoRA up-projection and
-// epilogue (16 output rows per workgroup).
+// Few tokens (M <= kSkinnyMaxTokens) on the matrix cores, one launch: LoRA
+// workgroups publish acc_a and sum Q as tagged words while the others run a
+// split-K expanded-sign int8 MFMA product over 16 output rows each, then the
+// LoRA up-projection and epilogue.
 constexpr int64_t kSkinnyMaxTokens = 32;
 hipError_t launch_skinny_linear(const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N,
                                 int64_t r, const uint32_t* w_bits, const float* alpha,

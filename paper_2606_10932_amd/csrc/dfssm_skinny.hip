@@ -19,9 +19,20 @@
 //  * the waves' partial tiles are summed in LDS; one wave per token tile then
 //    does the LoRA up-projection (four limb MFMAs: E_hi = 256*(B.L3) + B.L2,
 //    E_lo = 256*(B.L1) + B.L0, exact int64 acc_b = E_lo + 65536*E_hi) and the
-//    fp32 epilogue; its operands were loaded at the start.
-// The LoRA down-projection, its limbs and sum_k Q come from small_prep.
+//    fp32 epilogue; its row operands were loaded at the start.
+// One launch: the first nb_lora workgroups compute the LoRA down-projection
+// acc_a = Q A^T (one wave per rank and 4 tokens) and sum_k Q, and publish
+// them as 64-bit words {tag, value} (value: acc_a's 4 signed base-256 limbs
+// as bytes, or sum Q) with agent-scope stores; tag is unique per call, so a
+// word left by an earlier call never validates.  The other workgroups read
+// the words they need after their scaffold product.  The wait is bounded:
+// a lane whose words have not arrived after `spin` polls computes the values
+// itself from A and Q (the integers are the same either way), so no
+// workgroup depends on another being scheduled.
+#include <stdlib.h>
+
 #include <algorithm>
+#include <atomic>
 
 #include "dfssm_internal.hpp"
 
@@ -72,14 +83,186 @@ struct SkinnyArgs {
   int M, K, N, r, rp;
   const uint32_t* w_bits;
   const float* alpha;
-  const int8_t* limbs;  // [4][M][rp]
+  const int8_t* A;
   const int8_t* B;
   const float* beta;
-  const int32_t* sumq;
   float* y;
   int32_t* acc_s_out;
   int64_t* acc_b_out;
+  int32_t* acc_a;  // [M][r], written by the LoRA workgroups (and by fallback lanes)
+  uint64_t* xw;    // [M][rp] limb words, then [M] sum-Q words
+  uint32_t tag;
+  int nb_lora;     // LoRA workgroups at the front of the grid
+  int spin;        // polls of a missing word before computing it locally
 };
+
+__device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
+  return __builtin_amdgcn_sdot4((int)a, (int)b, c, false);
+}
+
+// whole-wave sum, the total in every lane (DPP inside 16-lane rows, then
+// gfx950's permlane swaps across rows and halves)
+__device__ __forceinline__ int wave_sum(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+  v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+  v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);  // row_half_mirror
+  v += __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);  // row_mirror
+  auto p = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v, false, false);
+  v = (int)(p[0] + p[1]);
+  p = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+  return (int)(p[0] + p[1]);
+}
+
+// agent scope: the words cross XCDs (each XCD has its own L2)
+__device__ __forceinline__ void word_store(uint64_t* p, uint32_t tag, uint32_t v) {
+  __hip_atomic_store(p, ((uint64_t)tag << 32) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t word_load(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ uint32_t pack_limbs(int32_t v) {
+  int8_t d[4];
+  dfssm_dev::split_limbs(v, d);
+  return (uint32_t)(uint8_t)d[0] | ((uint32_t)(uint8_t)d[1] << 8) | ((uint32_t)(uint8_t)d[2] << 16) |
+         ((uint32_t)(uint8_t)d[3] << 24);
+}
+
+// sum_k A[j,k] Q[m,k] (j < r) or sum_k Q[m,k] (j < 0), one lane alone
+__device__ int lane_dot(const int8_t* __restrict__ A, const int8_t* __restrict__ q, int K, int j, int m) {
+  const int8_t* qrow = q + (int64_t)m * K;
+  const int8_t* arow = A + (int64_t)(j < 0 ? 0 : j) * K;
+  int acc = 0;
+  for (int k = 0; k < K; k += 16) {
+    const uint4 x = *reinterpret_cast<const uint4*>(qrow + k);
+    const uint4 w = j < 0 ? make_uint4(0x01010101u, 0x01010101u, 0x01010101u, 0x01010101u)
+                          : *reinterpret_cast<const uint4*>(arow + k);
+    acc = sdot4(w.x, x.x, acc);
+    acc = sdot4(w.y, x.y, acc);
+    acc = sdot4(w.z, x.z, acc);
+    acc = sdot4(w.w, x.w, acc);
+  }
+  return acc;
+}
+
+// LoRA workgroup: wave w takes item b*nw + w = (token group of 4, rank j);
+// the wave of rank 0 also sums Q.  Every 16-byte load of a 4 KB column batch
+// is issued before the first v_dot4.
+constexpr int kPrepTokens = 4;
+constexpr int kPrepBatch = 4;
+__device__ void lora_block(const SkinnyArgs& a) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nw = blockDim.x >> 6;
+  const int M = a.M, K = a.K, r = a.r, rp = a.rp;
+  const int item = (int)blockIdx.x * nw + wave;
+  const int j = item % rp, m0 = (item / rp) * kPrepTokens;
+  if (m0 >= M) return;
+  const int mt = min(kPrepTokens, M - m0);
+  const bool jr = j < r, qsum = j == 0;
+  int acc[kPrepTokens], qs[kPrepTokens];
+#pragma unroll
+  for (int m = 0; m < kPrepTokens; ++m) acc[m] = qs[m] = 0;
+  if (jr || qsum) {
+    const int8_t* arow = a.A + (int64_t)(jr ? j : 0) * K;
+    for (int kb = 0; kb < K; kb += 1024 * kPrepBatch) {
+      uint4 av[kPrepBatch], x[kPrepTokens][kPrepBatch];
+#pragma unroll
+      for (int u = 0; u < kPrepBatch; ++u) {
+        const int k = kb + 1024 * u + 16 * lane;
+        const bool ok = k < K;  // K % 32 == 0: a 16-byte chunk is wholly in or out
+        av[u] = (jr && ok) ? *reinterpret_cast<const uint4*>(arow + k) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+        for (int m = 0; m < kPrepTokens; ++m)
+          x[m][u] = (ok && m < mt) ? *reinterpret_cast<const uint4*>(a.q + (int64_t)(m0 + m) * K + k)
+                                   : make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < kPrepBatch; ++u)
+#pragma unroll
+        for (int m = 0; m < kPrepTokens; ++m) {
+          acc[m] = sdot4(av[u].x, x[m][u].x, acc[m]);
+          acc[m] = sdot4(av[u].y, x[m][u].y, acc[m]);
+          acc[m] = sdot4(av[u].z, x[m][u].z, acc[m]);
+          acc[m] = sdot4(av[u].w, x[m][u].w, acc[m]);
+          if (qsum) {
+            qs[m] = sdot4(0x01010101u, x[m][u].x, qs[m]);
+            qs[m] = sdot4(0x01010101u, x[m][u].y, qs[m]);
+            qs[m] = sdot4(0x01010101u, x[m][u].z, qs[m]);
+            qs[m] = sdot4(0x01010101u, x[m][u].w, qs[m]);
+          }
+        }
+    }
+  }
+  int mine = 0, mine_q = 0;
+#pragma unroll
+  for (int m = 0; m < kPrepTokens; ++m) {
+    if (m < mt) {  // uniform
+      const int t = wave_sum(acc[m]);
+      mine = lane == m ? t : mine;
+      if (qsum) {
+        const int tq = wave_sum(qs[m]);
+        mine_q = lane == m ? tq : mine_q;
+      }
+    }
+  }
+  if (lane < mt) {
+    const int m = m0 + lane;
+    if (jr) a.acc_a[(int64_t)m * r + j] = mine;
+    word_store(a.xw + (int64_t)m * rp + j, a.tag, pack_limbs(mine));  // zero limbs for ranks in [r, rp)
+    if (qsum) word_store(a.xw + (int64_t)M * rp + m, a.tag, (uint32_t)mine_q);
+  }
+}
+
+// The limbs of acc_a[m][j0 + 16kg .. +15] as 4 limb operands (byte e of limb
+// t = limb t of rank j0 + 16kg + e) and, with want_sq, sum Q of token m: from
+// the LoRA workgroups' words, or computed here once `spin` polls have passed.
+__device__ void fetch_lora(const SkinnyArgs& a, int m, int j0, int kg, v4i (&lm)[4], int* sq, bool store_acc) {
+  const uint64_t* wp = a.xw + (int64_t)m * a.rp + j0 + 16 * kg;
+  const uint64_t* sp = a.xw + (int64_t)a.M * a.rp + m;
+  uint32_t val[16], vq = 0;
+  bool have = false;
+  for (int it = 0;; ++it) {
+    if (!have) {
+      uint64_t w[16], wq = 0;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) w[e] = word_load(wp + e);
+      if (sq) wq = word_load(sp);
+      bool ok = !sq || (uint32_t)(wq >> 32) == a.tag;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) ok = ok && (uint32_t)(w[e] >> 32) == a.tag;
+      if (ok) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) val[e] = (uint32_t)w[e];
+        vq = (uint32_t)wq;
+        have = true;
+      }
+    }
+    if (__all(have) || it >= a.spin) break;
+    __builtin_amdgcn_s_sleep(2);
+  }
+  if (!have) {
+    // the LoRA workgroups' words did not arrive: compute them here
+#pragma unroll 1
+    for (int e = 0; e < 16; ++e) {
+      const int j = j0 + 16 * kg + e;
+      const int v = j < a.r ? lane_dot(a.A, a.q, a.K, j, m) : 0;
+      val[e] = pack_limbs(v);
+      if (store_acc && j < a.r) a.acc_a[(int64_t)m * a.r + j] = v;
+    }
+    if (sq) vq = (uint32_t)lane_dot(a.A, a.q, a.K, -1, m);
+  }
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      uint32_t o = 0;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) o |= ((val[4 * d + b] >> (8 * t)) & 0xffu) << (8 * b);
+      lm[t][d] = (int)o;
+    }
+  if (sq) *sq = (int)vq;
+}
 
 // MT token tiles of 16 (M <= 16*MT); S MFMA steps per lane per iteration.
 // Block: 16 output rows, nw = blockDim.x / 64 waves (nw >= MT), wave w takes
@@ -87,6 +270,10 @@ struct SkinnyArgs {
 template <int MT, int S>
 __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   __shared__ v4i red[kMaxWaves][MT][64];
+  if ((int)blockIdx.x < a.nb_lora) {
+    lora_block(a);
+    return;
+  }
   constexpr int KW = 64 * S;  // columns per wave iteration
   constexpr int SW = S / 2;   // sign words per lane per iteration
   const int lane = threadIdx.x & 63;
@@ -94,30 +281,24 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   const int nw = blockDim.x >> 6;
   const int rho = lane & 15, kg = lane >> 4;
   const int M = a.M, K = a.K, N = a.N, r = a.r, W = K >> 5;
-  const int n0 = 16 * blockIdx.x;
+  const int n0 = 16 * ((int)blockIdx.x - a.nb_lora);
   const int nrow = min(n0 + rho, N - 1);  // sign / B row of this lane (rows past N are never stored)
   const uint32_t* wrow = a.w_bits + (int64_t)nrow * W;
   const int nit = (K + KW - 1) / KW;
   const bool wvec = (W % SW) == 0;
 
-  // ---- the epilogue operands of the wave that finishes token tile `wave`
-  //      go out first: B bytes and limbs of ranks 0..63, row scales, token
-  //      scales and sums of Q
+  // ---- the row operands of the wave that finishes token tile `wave` go
+  //      out first: B bytes of ranks 0..63, row scales, token scales
   const bool fin = wave < MT;
   const int mtok = 16 * wave + rho;  // token of this lane in the finished tile
   const int mc = min(mtok, M - 1);
   const int nb = n0 + 4 * kg;  // this lane's output rows nb .. nb+3
   const bool ba = (r % 16) == 0;
-  v4i bop = zero4(), lm[4] = {zero4(), zero4(), zero4(), zero4()};
+  v4i bop = zero4();
   float alv[4] = {0.f, 0.f, 0.f, 0.f}, bev[4] = {0.f, 0.f, 0.f, 0.f};
   float sm = 0.f;
-  int sq = 0;
   if (fin) {
-    if (r > 0) {
-      bop = load16_guarded(a.B + (int64_t)nrow * r, 16 * kg, r, ba);
-#pragma unroll
-      for (int t = 0; t < 4; ++t) lm[t] = load16(a.limbs + ((int64_t)t * M + mc) * a.rp + 16 * kg);
-    }
+    if (r > 0) bop = load16_guarded(a.B + (int64_t)nrow * r, 16 * kg, r, ba);
     if ((N & 3) == 0 && nb + 3 < N) {
       const float4 al4 = *reinterpret_cast<const float4*>(a.alpha + nb);
       alv[0] = al4.x; alv[1] = al4.y; alv[2] = al4.z; alv[3] = al4.w;
@@ -134,7 +315,6 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
       }
     }
     sm = a.s[mc];
-    sq = a.sumq[mc];
   }
 
   // ---- scaffold: this wave's share of K
@@ -185,25 +365,30 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   v4i d = red[0][wave][lane];
   for (int w = 1; w < nw; ++w) d += red[w][wave][lane];
 
+  // LoRA limbs of ranks 0..63 and sum Q of this lane's token; the first
+  // block of each tile row also keeps acc_a for the caller if its words had
+  // to be computed here
+  v4i lm[4];
+  int sq = 0;
+  const bool keep = blockIdx.x == a.nb_lora && mtok < M;
+  fetch_lora(a, mc, 0, kg, lm, &sq, keep);
+
   // LoRA up-projection, limbs 3, 2, 1, 0 over the 64-rank chunks
   v4i ehi = zero4(), elo = zero4();
   if (r > 0) {
-#pragma unroll
-    for (int pass = 0; pass < 4; ++pass) {
-      const int limb = 3 - pass;
-      v4i e = limb >= 2 ? ehi : elo;
-      e = mfma(bop, lm[limb], e);
-      for (int j0 = 64; j0 < a.rp; j0 += 64) {
-        const v4i bl = load16_guarded(a.B + (int64_t)nrow * r, j0 + 16 * kg, r, ba);
-        const v4i al = load16(a.limbs + ((int64_t)limb * M + mc) * a.rp + j0 + 16 * kg);
-        e = mfma(bl, al, e);
-      }
-      if (limb == 3 || limb == 1) e = e << 8;
-      if (limb >= 2)
-        ehi = e;
-      else
-        elo = e;
+    v4i e3 = mfma(bop, lm[3], zero4()), e2 = mfma(bop, lm[2], zero4());
+    v4i e1 = mfma(bop, lm[1], zero4()), e0 = mfma(bop, lm[0], zero4());
+    for (int j0 = 64; j0 < a.rp; j0 += 64) {
+      const v4i bl = load16_guarded(a.B + (int64_t)nrow * r, j0 + 16 * kg, r, ba);
+      v4i lj[4];
+      fetch_lora(a, mc, j0, kg, lj, nullptr, keep);
+      e3 = mfma(bl, lj[3], e3);
+      e2 = mfma(bl, lj[2], e2);
+      e1 = mfma(bl, lj[1], e1);
+      e0 = mfma(bl, lj[0], e0);
     }
+    ehi = (e3 << 8) + e2;
+    elo = (e1 << 8) + e0;
   }
 
   // lane (rho, kg) holds D[row nb + v][token mtok]
@@ -232,9 +417,19 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
 
 template <int MT, int S>
 hipError_t launch_t(const SkinnyArgs& a, int nw, hipStream_t st) {
-  const int64_t blocks = dfssm::ceil_div(a.N, 16);
+  const int64_t blocks = a.nb_lora + dfssm::ceil_div(a.N, 16);
   mfma_skinny<MT, S><<<dim3((unsigned)blocks), dim3(64 * nw), 0, st>>>(a);
   return hipGetLastError();
+}
+
+// Per-call tag of the LoRA words (never 0, so zeroed memory never validates).
+uint32_t next_tag() {
+  static std::atomic<uint32_t> seq{0};
+  uint32_t t;
+  do {
+    t = seq.fetch_add(1, std::memory_order_relaxed) + 1;
+  } while (t == 0);
+  return t;
 }
 
 }  // namespace
@@ -248,21 +443,31 @@ hipError_t launch_skinny_linear(const int8_t* q, const float* s, int64_t M, int6
                                 const LinearWorkspace& ws, hipStream_t st) {
   if (M == 0 || N == 0) return hipSuccess;
   if (M > kSkinnyMaxTokens) return hipErrorInvalidValue;
-  hipError_t e = launch_small_prep(q, M, K, r, A, ws, false, st);
-  if (e != hipSuccess) return e;
-  if (acc_a_out && r > 0) {
-    e = hipMemcpyAsync(acc_a_out, ws.acc_a, (size_t)(M * r) * 4, hipMemcpyDeviceToDevice, st);
-    if (e != hipSuccess) return e;
-  }
-  SkinnyArgs a{q, s, (int)M, (int)K, (int)N, (int)r, (int)rank_padded(r), w_bits, alpha, ws.limbs, B, beta,
-               ws.sumq, y, acc_s, acc_b};
-  // 16-byte sign loads (8 MFMA steps) once K gives every wave a full one
-  const int S = K >= 4096 ? 8 : 4;
+  const int rp = (int)rank_padded(r);
+  // 16-byte sign loads (8 MFMA steps) once K gives 4 waves a full one each:
+  // at K = 2048 the 1.3B in_proj's 532 workgroups of 4 waves then fit the
+  // chip's slots in one round (8 waves of 8-byte loads would not)
+  const int S = K >= 2048 ? 8 : 4;
   const int mt = M > 16 ? 2 : 1;
   const int64_t nit = ceil_div(K, 64 * S);
   const int nw = (int)std::max<int64_t>(mt, std::min<int64_t>(kMaxWaves, nit));
-  if (mt == 1) return S == 8 ? launch_t<1, 8>(a, nw, st) : launch_t<1, 4>(a, nw, st);
-  return S == 8 ? launch_t<2, 8>(a, nw, st) : launch_t<2, 4>(a, nw, st);
+  // Test hook: DFSSM_TEST_LOCAL_LORA=1 launches no LoRA workgroups and lets
+  // every lane compute its LoRA values itself at once (the path a lane takes
+  // when the words never arrive).
+  const char* hook = getenv("DFSSM_TEST_LOCAL_LORA");
+  const bool local_only = hook && hook[0] == '1';
+  const int nb_lora = local_only ? 0 : (int)ceil_div(ceil_div(M, kPrepTokens) * rp, nw);
+  SkinnyArgs a{q, s, (int)M, (int)K, (int)N, (int)r, rp, w_bits, alpha, A, B, beta, y, acc_s, acc_b,
+               ws.acc_a, ws.xw, next_tag(), nb_lora, local_only ? 0 : (1 << 14)};
+  hipError_t e;
+  if (mt == 1)
+    e = S == 8 ? launch_t<1, 8>(a, nw, st) : launch_t<1, 4>(a, nw, st);
+  else
+    e = S == 8 ? launch_t<2, 8>(a, nw, st) : launch_t<2, 4>(a, nw, st);
+  if (e != hipSuccess) return e;
+  if (acc_a_out && r > 0)
+    e = hipMemcpyAsync(acc_a_out, ws.acc_a, (size_t)(M * r) * 4, hipMemcpyDeviceToDevice, st);
+  return e;
 }
 
 }  // namespace dfssm

@@ -153,6 +153,22 @@ def test_linear_few_tokens(env, M, K, N, r):
     assert np.array_equal(y2.view(np.uint32), y.view(np.uint32)), "y without accumulator outputs"
 
 
+@pytest.mark.parametrize("M,K,N,r", [(3, 160, 77, 5), (17, 4096, 2048, 64), (2, 256, 31, 256), (1, 32, 1, 0)])
+def test_few_tokens_local_lora(env, M, K, N, r, monkeypatch):
+    """The few-token kernel's fallback: with no LoRA workgroups launched and
+    no polling (a test switch of the library), every lane computes acc_a and
+    sum Q itself; the results are the same integers."""
+    torch, D, o = env
+    say(f"few tokens, local LoRA values M={M} K={K} N={N} r={r}")
+    monkeypatch.setenv("DFSSM_TEST_LOCAL_LORA", "1")
+    ref, y, acc_s, acc_a, acc_b = _run_linear(env, M, K, N, r, D.PATH_MFMA_FEW)
+    assert np.array_equal(acc_s, ref["acc_s"]), "acc_s"
+    if r:
+        assert np.array_equal(acc_a, ref["acc_a"]), "acc_a"
+    assert np.array_equal(acc_b, ref["acc_b"]), "acc_b"
+    assert_y(y, ref, what=f"few local {M}x{K}x{N} r{r}")
+
+
 def test_few_tokens_limit(env):
     """The few-token path refuses M > 32 before launching anything."""
     torch, D, o = env
