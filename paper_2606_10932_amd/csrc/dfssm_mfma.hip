@@ -20,6 +20,8 @@
 // per 16x16 tile, E_hi = 256*(B.L3) + B.L2 and E_lo = 256*(B.L1) + B.L0
 // (each < 2^31 for r <= 256), acc_b = E_lo + 65536*E_hi, so the K-loop holds
 // only the scaffold accumulators.
+#include <stdlib.h>
+
 #include <algorithm>
 #include <atomic>
 
@@ -255,6 +257,8 @@ __device__ __forceinline__ void lds_dma4(uint32_t voff, const void* sbase, uint3
 
 // s_waitcnt with only the vector-memory counter constrained
 #define DFSSM_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(0x0F70 | ((n) & 0xF) | (((n) >> 4) << 14))
+// s_waitcnt with only the LDS/scalar counter constrained, to zero
+#define DFSSM_WAIT_LGKM0() __builtin_amdgcn_s_waitcnt(0xC07F)
 // workgroup barrier that does not drain outstanding direct-to-LDS loads
 // (the compiler's barrier fence would wait for all of them); LDS visibility
 // of the loads is ordered by the DFSSM_WAIT_VMCNT before it
@@ -389,11 +393,12 @@ __device__ __forceinline__ void tile_out(const GemmArgs& a, const TileLds& L, co
 }
 
 // Epilogue of the block, per wave: its (up to) 4 row tiles x 8 token tiles,
-// then its 2 token tiles of the 17th row tile.
+// then its 2 token tiles (xtok, xtok+1) of the shared row tile at row offset
+// xrow of the run.
 template <bool kLdsLora, bool kChecked>
 __device__ __forceinline__ void block_epilogue(const GemmArgs& a, const TileLds& L, const v4i (&acc)[4][8],
                                                const v4i (&accx)[2], int m0, int n0, int wave, int ntw,
-                                               bool extra, int rho, int kg, int l_off) {
+                                               bool extra, int xrow, int xtok, int rho, int kg, int l_off) {
   const int8_t* limb_lds = L.lds;
   const int8_t* b_lds = L.lds + kLimbBytes;
   v4i bop[4];
@@ -417,15 +422,15 @@ __device__ __forceinline__ void block_epilogue(const GemmArgs& a, const TileLds&
     }
   }
   if (extra) {
-    const v4i bx = kLdsLora ? *reinterpret_cast<const v4i*>(b_lds + 256 * 64 + l_off) : zero4();
+    const v4i bx = kLdsLora ? *reinterpret_cast<const v4i*>(b_lds + xrow * 64 + l_off) : zero4();
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const int i = 2 * wave + h;
+      const int i = xtok + h;
       v4i lm[4];
 #pragma unroll
       for (int l = 0; l < 4; ++l)
         lm[l] = kLdsLora ? *reinterpret_cast<const v4i*>(limb_lds + (l * kBM + 16 * i) * 64 + l_off) : zero4();
-      tile_out<kLdsLora, kChecked>(a, L, accx[h], bx, lm, m0, n0, 256, i, rho, kg);
+      tile_out<kLdsLora, kChecked>(a, L, accx[h], bx, lm, m0, n0, xrow, i, rho, kg);
     }
   }
 }
@@ -711,11 +716,11 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
   const int l_off = rho * 64 + 16 * (kg ^ swz(rho));
   const bool fast = lora_lds && !a.acc_s_out && !a.acc_b_out && (N & 3) == 0 && m0 + kBM <= M && n0 + nrows <= N;
   if (fast)
-    block_epilogue<true, false>(a, L, acc, accx, m0, n0, wave, ntw, extra, rho, kg, l_off);
+    block_epilogue<true, false>(a, L, acc, accx, m0, n0, wave, ntw, extra, 256, 2 * wave, rho, kg, l_off);
   else if (lora_lds)
-    block_epilogue<true, true>(a, L, acc, accx, m0, n0, wave, ntw, extra, rho, kg, l_off);
+    block_epilogue<true, true>(a, L, acc, accx, m0, n0, wave, ntw, extra, 256, 2 * wave, rho, kg, l_off);
   else
-    block_epilogue<false, true>(a, L, acc, accx, m0, n0, wave, ntw, extra, rho, kg, l_off);
+    block_epilogue<false, true>(a, L, acc, accx, m0, n0, wave, ntw, extra, 256, 2 * wave, rho, kg, l_off);
 }
 
 template <bool kLoraLds>
@@ -729,6 +734,309 @@ __global__ __launch_bounds__(kThreads, 2) void mfma_scaffold(GemmArgs a) {
   const int rt0 = (int)((int64_t)j * a.nt16 / a.bpm), rt1 = (int)((int64_t)(j + 1) * a.nt16 / a.bpm);
   const TileLds L{lds, al_lds, be_lds, s_lds, sq_lds};
   scaffold_block<kLoraLds>(a, L, bm * kBM, rt0, rt1 - rt0);
+}
+
+
+// ------------------------------------------------------------ ping-pong prefill
+// One block of 8 waves per CU, two per SIMD, in two groups of 4 (waves 0-3
+// and 4-7) that take turns: while one group runs its MFMAs of a stage, the
+// other reads its operands of the next stage from LDS, issues the loads of a
+// later stage and waits for its own loads of the stage after; a block
+// barrier separates the turns, and the second group starts one turn late.
+// So at any time one wave of each SIMD is in its MFMA phase.  (Two 4-wave
+// blocks per CU cannot arrange that: each block's per-stage barrier and
+// loads fell in the same phase on both waves of a SIMD.)
+//
+// Block: 128 tokens x a run of up to 34 row tiles.  Wave w owns row tiles
+// 4w .. 4w+3; the 33rd and 34th are shared, wave w taking token tiles 2i,
+// 2i+1 (i = w % 4) of row tile 32 + w / 4.  Per stage each wave issues one
+// 16-byte direct-to-LDS load of Q (16 token rows) and, at a sign-group start,
+// the 9 loads of its sign rows (its 64 rows, 4 of the 32 shared rows), with
+// the layouts of the 4-wave kernel.
+constexpr int kPPThreads = 512;
+constexpr int kPPRunMax = 34;
+constexpr int kPPSgBuf = 8 * kSgWave + 32 * 32;  // 17 KB
+constexpr int kPPLdsRing = kQRing + 2 * kPPSgBuf;
+constexpr int kPPLdsLora = kLimbBytes + kPPRunMax * 16 * 64;
+constexpr int kPPLdsBytes = kPPLdsRing > kPPLdsLora ? kPPLdsRing : kPPLdsLora;
+constexpr int kPPMaxRows = kPPRunMax * 16;
+
+template <bool kLoraLds>
+__device__ __forceinline__ void scaffold_block_pp(const GemmArgs& a, const TileLds& L, int m0, int rt0, int cnt) {
+  const int M = a.M, K = a.K, N = a.N, r = a.r, rp = a.rp;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS addresses of the loads
+  const int grp = wave >> 2, wi = wave & 3;
+  const int rho = lane & 15, kg = lane >> 4;
+  const int W = K >> 5;
+  const int nks = (K + kBK - 1) / kBK;
+  const bool ktail = (K & (kBK - 1)) != 0;  // the last stage holds 32 columns
+  const int n0 = 16 * rt0;
+  const int ntw = min(max(min(cnt, 32) - 4 * wave, 0), 4);  // this wave's own row tiles
+  const bool extra = cnt > 32 + grp;                         // this wave's shared row tile exists
+  const int nrows = 16 * cnt;
+  int8_t* const lds = L.lds;
+
+  // ---- direct-to-LDS load constants (rows past M or N read the last row;
+  //      their outputs are never stored)
+  uint32_t voff_q;
+  bool hi_chunk;
+  {
+    const int m = 16 * wave + (lane >> 2);  // Q row of this lane's 16-byte slot
+    const int c = (lane & 3) ^ swz(m);
+    hi_chunk = c >= 2;
+    voff_q = (uint32_t)((min(m0 + m, M - 1) - m0) * K + 16 * c);
+  }
+  const bool sg_fast = n0 + 64 * wave + 64 <= N;  // uniform: no own sign row is clamped
+  uint32_t voff_s[2];
+#pragma unroll
+  for (int jp = 0; jp < 2; ++jp) {
+    const int wd = (lane & 7) ^ (2 * ((2 * jp + (lane >> 5)) & 3));
+    voff_s[jp] = (uint32_t)((((lane >> 3) + 64 * wave) * W + wd) * 4);
+  }
+  uint32_t voff_x;
+  {
+    const int rr = 4 * wave + (lane >> 3);  // shared row (< 32 for lanes < 32)
+    const int wd = (lane & 7) ^ (2 * ((rr >> 2) & 3));
+    const int n = min(n0 + 512 + rr, N - 1);
+    voff_x = (uint32_t)(((n - n0) * W + wd) * 4);
+  }
+  const int8_t* qbase = a.q + (int64_t)m0 * K;
+  const uint32_t* wbase = a.w_bits + (int64_t)n0 * W;
+  const uint32_t lds0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(uintptr_t)(lds_void*)lds);
+
+  auto issue_signs = [&](int g) {
+    const uint32_t sb = lds0 + kQRing + (g & 1) * kPPSgBuf;
+    const uint32_t* ws = wbase + 8 * g;
+    const bool whole = 8 * g + 8 <= W;  // uniform
+    if (sg_fast && whole) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) lds_dma4(voff_s[j & 1], ws + (int64_t)8 * j * W, sb + kSgWave * wave + 256u * j);
+    } else {
+      const int ln = lane + opaque_zero();
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int rl = 8 * j + (ln >> 3);
+        const int wd = (ln & 7) ^ (2 * ((rl >> 2) & 3));
+        const int n = min(n0 + 64 * wave + rl, N - 1);
+        const int wc = min(8 * g + wd, W - 1) - 8 * g;
+        lds_dma4((uint32_t)(((n - n0) * W + wc) * 4), ws, sb + kSgWave * wave + 256u * j);
+      }
+    }
+    {
+      uint32_t vx = voff_x;
+      if (!whole) {
+        const int ln = lane + opaque_zero();
+        const int rr = 4 * wave + (ln >> 3);
+        const int wd = (ln & 7) ^ (2 * ((rr >> 2) & 3));
+        const int n = min(n0 + 512 + rr, N - 1);
+        vx = (uint32_t)(((n - n0) * W + min(8 * g + wd, W - 1) - 8 * g) * 4);
+      }
+      if (lane < 32) lds_dma4(vx, ws, sb + 8 * kSgWave + 128u * wave);
+    }
+  };
+  auto issue = [&](int ks, int slot) {
+    if (slot == 0) issue_signs(ks >> 2);
+    const int8_t* qs = qbase + ks * kBK;
+    const uint32_t sb = lds0 + slot * kQStage + 1024u * wave;
+    if (ktail && ks == nks - 1)
+      lds_dma16(voff_q - (hi_chunk ? 32u : 0u), qs, sb);  // chunks past K re-read 0, 1 (zeroed signs)
+    else
+      lds_dma16(voff_q, qs, sb);
+  };
+
+  // LDS read offsets (as in the 4-wave kernel; the shared tile's rows follow
+  // the 8 waves' areas)
+  const int q_off = rho * kBK + 16 * (kg ^ swz(rho));
+  const int w_off = kQRing + kSgWave * wave + 32 * rho + 4 * ((kg >> 1) ^ (2 * ((rho >> 2) & 3)));
+  const int x_delta = 8 * kSgWave + 512 * grp - kSgWave * wave;  // uniform
+  const uint32_t sh = 16u * (kg & 1);
+  const bool kg_hi = kg >= 2;
+
+  typedef uint32_t raw_t __attribute__((ext_vector_type(4)));
+  struct Ops {
+    v4i q[8];
+    v4i qx[2];  // the shared tile's token tiles 2i, 2i+1 (read again: no register indexing)
+    raw_t w;
+    uint32_t x;
+  };
+  auto read_ops = [&](int ks, int slot, Ops& o) {
+    const int8_t* qst = lds + slot * kQStage + q_off;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o.q[i] = *reinterpret_cast<const v4i*>(qst + i * 16 * kBK);
+    if (extra) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) o.qx[h] = *reinterpret_cast<const v4i*>(qst + (2 * wi + h) * 16 * kBK);
+    }
+    const int8_t* st = lds + ((ks >> 2) & 1) * kPPSgBuf;
+    const int wb = w_off ^ (8 * (ks & 3));
+#pragma unroll
+    for (int t = 0; t < 4; ++t) o.w[t] = *reinterpret_cast<const uint32_t*>(st + wb + 512 * t);
+    o.x = *reinterpret_cast<const uint32_t*>(st + x_delta + wb);
+    if (ktail && ks == nks - 1) {  // uniform: sign words past K count as 0
+#pragma unroll
+      for (int t = 0; t < 4; ++t) o.w[t] = kg_hi ? 0u : o.w[t];
+      o.x = kg_hi ? 0u : o.x;
+    }
+  };
+
+  v4i acc[4][8], accx[2];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[t][i] = zero4();
+  accx[0] = accx[1] = zero4();
+
+  auto compute = [&](const Ops& o) {
+    {
+      v4i sg = expand16_at(o.w[0], sh);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const v4i sgn = t + 1 < 4 ? expand16_at(o.w[t + 1], sh) : sg;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[t][i] = mfma(sg, o.q[i], acc[t][i]);
+        sg = sgn;
+      }
+      __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);  // VALU: the first expansion
+#pragma unroll
+      for (int t = 0; t < 3; ++t) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // VALU
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
+        }
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    }
+    if (extra) {  // uniform: the shared row tile, token tiles 2i and 2i+1
+      const v4i sx = expand16_at(o.x, sh);
+      accx[0] = mfma(sx, o.qx[0], accx[0]);
+      accx[1] = mfma(sx, o.qx[1], accx[1]);
+    }
+  };
+
+  // loads a wave issues with stage ks: one Q load, plus the sign group's 9
+  // when ks starts a group (ks % 4 == 0)
+  auto lcount = [](int slot) { return slot == 0 ? 1 + kLsg : 1; };
+
+  // one stage: [memory turn] operands of ks from LDS, the loads of ks+3
+  // (into the slot of ks-1, which both groups have read), own loads of ks+1
+  // complete; barrier; [MFMA turn] multiply ks; barrier
+  auto stage = [&](int ks, int slot) {
+    Ops o;
+    read_ops(ks, slot, o);
+    if (ks + 3 < nks) issue(ks + 3, (slot + 3) % kStages);
+    if (ks + 1 < nks) {
+      const int c2 = lcount((slot + 2) % kStages), c3 = lcount((slot + 3) % kStages);
+      if (ks + 3 < nks) {
+        if (c2 + c3 == 2)
+          DFSSM_WAIT_VMCNT(2);
+        else
+          DFSSM_WAIT_VMCNT(2 + kLsg);
+      } else if (ks + 2 < nks) {
+        if (c2 == 1)
+          DFSSM_WAIT_VMCNT(1);
+        else
+          DFSSM_WAIT_VMCNT(1 + kLsg);
+      } else {
+        DFSSM_WAIT_VMCNT(0);
+      }
+    }
+    // this wave's LDS reads of ks are complete before the barrier: the other
+    // group refills the slot of ks in the turn after next
+    DFSSM_WAIT_LGKM0();
+    DFSSM_BARRIER();
+    __builtin_amdgcn_s_setprio(1);
+    compute(o);
+    __builtin_amdgcn_s_setprio(0);
+    DFSSM_BARRIER();
+  };
+
+#pragma unroll
+  for (int p = 0; p < kStages - 1; ++p)
+    if (p < nks) issue(p, p);
+  for (int x = tid; x < nrows; x += kPPThreads) {
+    const int n = min(n0 + x, N - 1);
+    L.al[x] = a.alpha[n];
+    L.be[x] = r > 0 ? a.beta[n] : 0.0f;
+  }
+  if (tid < kBM) {
+    const int m = min(m0 + tid, M - 1);
+    L.sv[tid] = a.s[m];
+    L.sq[tid] = a.sumq[m];
+  }
+  // stage 0 (with sign group 0) has landed once at most the Q loads of
+  // stages 1 and 2 are in flight
+  if (nks >= 3)
+    DFSSM_WAIT_VMCNT(2);
+  else if (nks == 2)
+    DFSSM_WAIT_VMCNT(1);
+  else
+    DFSSM_WAIT_VMCNT(0);
+  DFSSM_BARRIER();
+  if (grp == 1) DFSSM_BARRIER();  // the second group starts one turn late
+  int ks = 0;
+  for (; ks + kStages <= nks; ks += kStages) {
+    stage(ks + 0, 0);
+    stage(ks + 1, 1);
+    stage(ks + 2, 2);
+    stage(ks + 3, 3);
+  }
+  if (ks < nks) stage(ks, 0);
+  if (ks + 1 < nks) stage(ks + 1, 1);
+  if (ks + 2 < nks) stage(ks + 2, 2);
+  if (grp == 0) DFSSM_BARRIER();  // matches the second group's late start
+  DFSSM_WAIT_VMCNT(0);
+  __syncthreads();
+
+  // ---- epilogue: stage the LoRA operands of the block (rank <= 64)
+  const bool lora_lds = kLoraLds && r > 0;
+  if (lora_lds) {
+    int8_t* limb_lds = lds;            // [4][kBM][64], swizzled chunks
+    int8_t* b_lds = lds + kLimbBytes;  // [rows of the run][64], swizzled chunks
+    const bool baligned = (r % 16) == 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = tid + u * kPPThreads;  // (limb, row, 16-byte chunk)
+      const int limb = idx >> 9, ml = (idx >> 2) & 127, c = idx & 3;
+      const int m = min(m0 + ml, M - 1);
+      *reinterpret_cast<uint4*>(limb_lds + (limb * kBM + ml) * 64 + 16 * (c ^ swz(ml))) =
+          *reinterpret_cast<const uint4*>(a.limbs + ((int64_t)limb * M + m) * rp + 16 * c);
+    }
+    for (int idx = tid; idx < 4 * nrows; idx += kPPThreads) {  // (row, 16-byte chunk)
+      const int nl = idx >> 2, c = idx & 3;
+      const int n = min(n0 + nl, N - 1);
+      const v4i b = load16_guarded(a.B + (int64_t)n * r, 16 * c, r, baligned);
+      *reinterpret_cast<v4i*>(b_lds + nl * 64 + 16 * (c ^ swz(nl))) = b;
+    }
+    __syncthreads();
+  }
+  const int l_off = rho * 64 + 16 * (kg ^ swz(rho));
+  const int xrow = 512 + 16 * grp, xtok = 2 * wi;
+  const bool fast = lora_lds && !a.acc_s_out && !a.acc_b_out && (N & 3) == 0 && m0 + kBM <= M && n0 + nrows <= N;
+  if (fast)
+    block_epilogue<true, false>(a, L, acc, accx, m0, n0, wave, ntw, extra, xrow, xtok, rho, kg, l_off);
+  else if (lora_lds)
+    block_epilogue<true, true>(a, L, acc, accx, m0, n0, wave, ntw, extra, xrow, xtok, rho, kg, l_off);
+  else
+    block_epilogue<false, true>(a, L, acc, accx, m0, n0, wave, ntw, extra, xrow, xtok, rho, kg, l_off);
+}
+
+template <bool kLoraLds>
+__global__ __launch_bounds__(kPPThreads, 1) void mfma_scaffold_pp(GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) int8_t lds[kPPLdsBytes];
+  __shared__ __attribute__((aligned(16))) float al_lds[kPPMaxRows], be_lds[kPPMaxRows], s_lds[kBM];
+  __shared__ __attribute__((aligned(16))) int32_t sq_lds[kBM];
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  const int bm = tile / a.bpm, j = tile % a.bpm;
+  const int rt0 = (int)((int64_t)j * a.nt16 / a.bpm), rt1 = (int)((int64_t)(j + 1) * a.nt16 / a.bpm);
+  const TileLds L{lds, al_lds, be_lds, s_lds, sq_lds};
+  scaffold_block_pp<kLoraLds>(a, L, bm * kBM, rt0, rt1 - rt0);
 }
 
 }  // namespace
@@ -766,18 +1074,32 @@ hipError_t launch_mfma_linear(const int8_t* q, const float* s, int64_t M, int64_
   // blocks in runs of at most 17 whose lengths differ by at most one; bpm
   // is chosen so the blocks fill the chip's block slots (two per CU) in
   // whole rounds where the shape allows.
-  const int64_t slots = 2 * (int64_t)device_cu_count();
+  const int64_t cus = device_cu_count();
   const int64_t nbm = ceil_div(M, kBM);
   const int64_t nt16 = ceil_div(N, 16);
-  int64_t bpm = std::max(ceil_div(slots, nbm), ceil_div(nt16, kRunMax));
-  bpm = std::min(bpm, nt16);
+  // the 8-wave ping-pong kernel (one block per CU) where the runs are long
+  // enough to keep its 8 waves busy (at least 24 row tiles), else the 4-wave
+  // kernel (two blocks per CU).  Test switch: DFSSM_TEST_PREFILL_KERNEL=4 or 8.
+  int64_t bpm8 = std::min(std::max(ceil_div(cus, nbm), ceil_div(nt16, kPPRunMax)), nt16);
+  bool use8 = nt16 >= 24 * bpm8;
+  if (const char* v = getenv("DFSSM_TEST_PREFILL_KERNEL")) {
+    if (v[0] == '4') use8 = false;
+    if (v[0] == '8') use8 = true;
+  }
+  int64_t bpm = use8 ? bpm8 : std::min(std::max(ceil_div(2 * cus, nbm), ceil_div(nt16, kRunMax)), nt16);
   const int64_t grid = nbm * bpm;
   GemmArgs ga{q, s, (int)M, (int)K, (int)N, (int)r, rp, w_bits, alpha, ws.limbs, B, beta, ws.sumq, y,
               acc_s, acc_b, (int)nt16, (int)bpm};
-  if (rp == 64)
+  if (use8) {
+    if (rp == 64)
+      mfma_scaffold_pp<true><<<dim3((unsigned)grid), dim3(kPPThreads), 0, st>>>(ga);
+    else
+      mfma_scaffold_pp<false><<<dim3((unsigned)grid), dim3(kPPThreads), 0, st>>>(ga);
+  } else if (rp == 64) {
     mfma_scaffold<true><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
-  else
+  } else {
     mfma_scaffold<false><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
+  }
   return hipGetLastError();
 }
 

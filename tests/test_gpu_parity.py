@@ -200,13 +200,46 @@ def test_realistic_lora_ratio(env, path):
     assert_y(y, ref, what="realistic ratio")
 
 
-def test_prefill_full_size_sampled(env):
-    """Mamba-2-1.3B in_proj at 2048 tokens (the launch the benchmark times):
+# the two prefill kernels (4-wave blocks, two per CU; 8-wave ping-pong
+# blocks, one per CU) on shapes the automatic choice would not give them
+PSHAPES = [
+    (5, 160, 77, 5),         # K % 128 != 0, r % 4 != 0
+    (33, 128, 130, 64),
+    (130, 2048, 300, 64),
+    (16, 4096, 2048, 64),
+    (2, 256, 31, 256),       # ranks above 64: LoRA operands from memory
+    (300, 2080, 700, 64),    # K % 64 == 32: half last stage
+    (129, 96, 600, 0),       # no LoRA, 2-stage K
+]
+
+
+@pytest.mark.parametrize("kernel", ["4", "8"])
+@pytest.mark.parametrize("M,K,N,r", PSHAPES)
+def test_linear_prefill_kernels(env, kernel, M, K, N, r, monkeypatch):
+    torch, D, o = env
+    say(f"prefill kernel={kernel} M={M} K={K} N={N} r={r}")
+    monkeypatch.setenv("DFSSM_TEST_PREFILL_KERNEL", kernel)
+    ref, y, acc_s, acc_a, acc_b = _run_linear(env, M, K, N, r, D.PATH_MFMA)
+    assert np.array_equal(acc_s, ref["acc_s"]), "acc_s"
+    if r:
+        assert np.array_equal(acc_a, ref["acc_a"]), "acc_a"
+    assert np.array_equal(acc_b, ref["acc_b"]), "acc_b"
+    assert_y(y, ref, what=f"prefill{kernel} {M}x{K}x{N} r{r}")
+    y2 = _run_y_only(env, M, K, N, r, D.PATH_MFMA)
+    assert np.array_equal(y2.view(np.uint32), y.view(np.uint32)), "y without accumulator outputs"
+
+
+@pytest.mark.parametrize("kernel", ["auto", "4"])
+def test_prefill_full_size_sampled(env, kernel, monkeypatch):
+    """Mamba-2-1.3B in_proj at 2048 tokens (the launch the benchmark times,
+    which takes the 8-wave kernel; and the 4-wave kernel on the same shape):
     every acc_s/acc_b/y of a sample of token rows against the oracle run on
     those rows (rows are independent)."""
     torch, D, o = env
     M, K, N, r = 2048, 2048, 8512, 64
-    say(f"prefill {M}x{K}x{N} r{r}")
+    say(f"prefill {M}x{K}x{N} r{r} kernel={kernel}")
+    if kernel != "auto":
+        monkeypatch.setenv("DFSSM_TEST_PREFILL_KERNEL", kernel)
     ws = S.config_weights(4)
     x = S.config_activations(4, M)
     q, s = o.quantize_act(x)
