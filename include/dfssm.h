@@ -80,7 +80,11 @@ typedef enum {
                               above */
   DFSSM_PATH_DECODE = 1,   /* bit-plane popcount GEMV (any M, best for M <= 4) */
   DFSSM_PATH_MFMA = 2,     /* sign bits expanded on chip + int8 MFMA, tiles of
-                              128 tokens (prefill) */
+                              128 tokens (prefill): an 8-wave ping-pong
+                              kernel where each block gets at least 24 row
+                              tiles of 16, a 4-wave kernel otherwise.  Test
+                              switch: DFSSM_TEST_PREFILL_KERNEL=4 or 8 in the
+                              environment forces one of them. */
   DFSSM_PATH_MFMA_FEW = 3  /* the same expansion and MFMA for M <= 32 in one
                               launch: 16 output rows per workgroup, K split
                               over its waves, the LoRA down-projection in

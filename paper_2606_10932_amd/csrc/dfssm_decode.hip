@@ -18,8 +18,6 @@
 //            base-256 int8 limbs and sum_k Q.  Further blocks build the
 //            bit-planes of Q: a thread transposes the 8x8 bit matrix of 8
 //            consecutive codes, so byte b of the result is byte p of plane b.
-//            The split-K MFMA kernel for few tokens uses the same prep
-//            without the planes.
 //  gemv   -- a group of G lanes owns one output row; lane g takes chunks g,
 //            g+G, ... of the row.  A block stages the planes and the limbs in
 //            LDS once; every lane loads its chunks of the row's signs, its B
@@ -69,8 +67,7 @@ constexpr int kPrepBatch = 4;   // 1 KB column blocks loaded before the first v_
 
 // 1-D grid: blocks [0, nb_lora) are LoRA blocks, (rank group, token group)
 // = (b % nrg, b / nrg) with nrg = rp / 4 (wave w: rank 4*(b % nrg) + w);
-// blocks from nb_lora on (kPlanes only) build the bit-planes.
-template <bool kPlanes>
+// blocks from nb_lora on build the bit-planes.
 __global__ __launch_bounds__(kThreads) void small_prep(const int8_t* __restrict__ q, int M, int K, int r,
                                                        int rp, const int8_t* __restrict__ A,
                                                        int32_t* __restrict__ acc_a, int8_t* __restrict__ limbs,
@@ -143,7 +140,6 @@ __global__ __launch_bounds__(kThreads) void small_prep(const int8_t* __restrict_
     }
     return;
   }
-  if (!kPlanes) return;
   // bit-planes, [M][8 planes][C chunks][16 bytes]: thread (m, p) transposes
   // codes 8p .. 8p+7 (zero at and beyond K) so that byte b holds bit b of the
   // 8 codes, which is byte p % 16 of chunk p / 16 of plane b
@@ -453,28 +449,25 @@ hipError_t launch_gemv_mt(const GemvCall& c, int m0, int mt, hipStream_t st) {
   return launch_gemv_cpl<64, MT>(c, m0, mt, st);
 }
 
+// acc_a, its limbs, sum Q and the bit-planes of the M tokens into the
+// workspace
+hipError_t launch_small_prep(const int8_t* q, int64_t M, int64_t K, int64_t r, const int8_t* A,
+                             const dfssm::LinearWorkspace& ws, hipStream_t st) {
+  if (M == 0) return hipSuccess;
+  const int rp = (int)dfssm::rank_padded(r);
+  const int C = (int)dfssm::plane_chunks(K);
+  const int64_t nb_lora = (int64_t)(rp / 4) * dfssm::ceil_div(M, kPrepTokens);
+  const int64_t nb_planes = std::min<int64_t>(dfssm::ceil_div(M * 16 * C, kThreads), 4096);
+  if (nb_lora + nb_planes > 0x7fffffff) return hipErrorInvalidValue;
+  small_prep<<<dim3((unsigned)(nb_lora + nb_planes)), dim3(kThreads), 0, st>>>(
+      q, (int)M, (int)K, (int)r, rp, A, ws.acc_a, ws.limbs, ws.sumq, reinterpret_cast<uint8_t*>(ws.planes), C,
+      (int)nb_lora);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 namespace dfssm {
-
-hipError_t launch_small_prep(const int8_t* q, int64_t M, int64_t K, int64_t r, const int8_t* A,
-                             const LinearWorkspace& ws, bool planes, hipStream_t st) {
-  if (M == 0) return hipSuccess;
-  const int rp = (int)rank_padded(r);
-  const int C = (int)plane_chunks(K);
-  const int64_t nb_lora = (int64_t)(rp / 4) * ceil_div(M, kPrepTokens);
-  int64_t nb_planes = 0;
-  if (planes) nb_planes = std::min<int64_t>(ceil_div(M * 16 * C, kThreads), 4096);
-  if (nb_lora + nb_planes > 0x7fffffff) return hipErrorInvalidValue;
-  if (planes)
-    small_prep<true><<<dim3((unsigned)(nb_lora + nb_planes)), dim3(kThreads), 0, st>>>(
-        q, (int)M, (int)K, (int)r, rp, A, ws.acc_a, ws.limbs, ws.sumq, reinterpret_cast<uint8_t*>(ws.planes), C,
-        (int)nb_lora);
-  else
-    small_prep<false><<<dim3((unsigned)nb_lora), dim3(kThreads), 0, st>>>(
-        q, (int)M, (int)K, (int)r, rp, A, ws.acc_a, ws.limbs, ws.sumq, nullptr, C, (int)nb_lora);
-  return hipGetLastError();
-}
 
 hipError_t launch_decode_linear(const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N,
                                 int64_t r, const uint32_t* w_bits, const float* alpha,
@@ -482,7 +475,7 @@ hipError_t launch_decode_linear(const int8_t* q, const float* s, int64_t M, int6
                                 int32_t* acc_s, int32_t* acc_a_out, int64_t* acc_b,
                                 const LinearWorkspace& ws, hipStream_t st) {
   if (M == 0 || N == 0) return hipSuccess;
-  hipError_t e = launch_small_prep(q, M, K, r, A, ws, true, st);
+  hipError_t e = launch_small_prep(q, M, K, r, A, ws, st);
   if (e != hipSuccess) return e;
   if (acc_a_out && r > 0) {
     e = hipMemcpyAsync(acc_a_out, ws.acc_a, (size_t)(M * r) * 4, hipMemcpyDeviceToDevice, st);

@@ -89,11 +89,6 @@ hipError_t launch_decode_linear(const int8_t* q, const float* s, int64_t M, int6
                                 int32_t* acc_s, int32_t* acc_a_out, int64_t* acc_b,
                                 const LinearWorkspace& ws, hipStream_t st);
 
-// LoRA down-projection for few tokens into the workspace (acc_a, limbs,
-// sum Q) and, with planes, the bit-planes of Q.
-hipError_t launch_small_prep(const int8_t* q, int64_t M, int64_t K, int64_t r, const int8_t* A,
-                             const LinearWorkspace& ws, bool planes, hipStream_t st);
-
 // Few tokens (M <= kSkinnyMaxTokens) on the matrix cores, one launch: LoRA
 // workgroups publish acc_a and sum Q as tagged words while the others run a
 // split-K expanded-sign int8 MFMA product over 16 output rows each, then the
