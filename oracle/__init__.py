@@ -57,6 +57,10 @@ class Oracle:
         lib.dfssm_ref_chain.argtypes = [i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         lib.dfssm_ref_chain.restype = i32
         lib.dfssm_ref_threads.restype = i32
+        lib.dfssm_ref_embed_gather.argtypes = [vp, vp, i64, i64, vp, i64, vp]
+        lib.dfssm_ref_embed_gather.restype = i32
+        lib.dfssm_ref_lm_head.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp]
+        lib.dfssm_ref_lm_head.restype = i32
         self.lib = lib
 
     # -- activation quantisation ------------------------------------------------
@@ -149,6 +153,37 @@ class Oracle:
             yo += M * Ns[l]
             qo += M * Ks[l]
         return ys, qs
+
+    # -- tied int8 embedding / LM head -------------------------------------------
+    def embed_gather(self, E, scale, tok):
+        """x [M,d] float32 = scale[tok] * E[tok, :]."""
+        E = np.ascontiguousarray(E, np.int8)
+        scale = np.ascontiguousarray(scale, np.float32)
+        tok = np.ascontiguousarray(tok, np.int32)
+        V, d = E.shape
+        M = tok.shape[0]
+        x = np.zeros((M, d), np.float32)
+        st = self.lib.dfssm_ref_embed_gather(_p(E), _p(scale), V, d, _p(tok), M, _p(x))
+        if st != OK:
+            raise OracleError(st)
+        return x
+
+    def lm_head(self, q, s, E, scale):
+        """Returns (acc int32 [M,V], logits float32 [M,V])."""
+        q = np.ascontiguousarray(q, np.int8)
+        s = np.ascontiguousarray(s, np.float32)
+        E = np.ascontiguousarray(E, np.int8)
+        scale = np.ascontiguousarray(scale, np.float32)
+        M, d = q.shape
+        V = E.shape[0]
+        if E.shape[1] != d:
+            raise ValueError("E must be [V, d]")
+        acc = np.zeros((M, V), np.int32)
+        logits = np.zeros((M, V), np.float32)
+        st = self.lib.dfssm_ref_lm_head(_p(q), _p(s), M, d, _p(E), _p(scale), V, _p(acc), _p(logits))
+        if st != OK:
+            raise OracleError(st)
+        return acc, logits
 
     def threads(self) -> int:
         return self.lib.dfssm_ref_threads()

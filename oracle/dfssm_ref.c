@@ -212,3 +212,43 @@ int dfssm_ref_chain(int n_layers, int64_t M, const int64_t* K,
   free(sbuf);
   return st;
 }
+
+/* ---- tied int8 embedding / LM head ------------------------------------- */
+
+int dfssm_ref_embed_gather(const int8_t* E, const float* scale, int64_t V, int64_t d,
+                           const int32_t* tok, int64_t M, float* x) {
+  if (d <= 0 || V < 0 || M < 0) return DFSSM_REF_ERR_SHAPE;
+  if (M == 0) return DFSSM_REF_OK;
+  if (!E || !scale || !tok || !x) return DFSSM_REF_ERR_NULL;
+  for (int64_t m = 0; m < M; ++m)
+    if (tok[m] < 0 || (int64_t)tok[m] >= V) return DFSSM_REF_ERR_SHAPE;
+  for (int64_t m = 0; m < M; ++m) {
+    const int64_t v = tok[m];
+    for (int64_t k = 0; k < d; ++k) x[m * d + k] = scale[v] * (float)E[v * d + k];
+  }
+  return DFSSM_REF_OK;
+}
+
+int dfssm_ref_lm_head(const int8_t* q, const float* s, int64_t M, int64_t d,
+                      const int8_t* E, const float* scale, int64_t V,
+                      int32_t* acc, float* logits) {
+  if (d <= 0 || V < 0 || M < 0) return DFSSM_REF_ERR_SHAPE;
+  if (M == 0 || V == 0) return DFSSM_REF_OK;
+  if (!q || !s || !E || !scale) return DFSSM_REF_ERR_NULL;
+#ifdef _OPENMP
+#pragma omp parallel for schedule(static)
+#endif
+  for (int64_t v = 0; v < V; ++v) {
+    for (int64_t m = 0; m < M; ++m) {
+      int64_t sum = 0;
+      for (int64_t k = 0; k < d; ++k) sum += (int64_t)E[v * d + k] * (int64_t)q[m * d + k];
+      if (acc) acc[m * V + v] = (int32_t)sum;
+      if (logits) {
+        float fa = (float)(int32_t)sum;
+        float t = scale[v] * fa;
+        logits[m * V + v] = s[m] * t;
+      }
+    }
+  }
+  return DFSSM_REF_OK;
+}

@@ -39,6 +39,8 @@
  *
  * Parity status: every function here is pinned by the CPU tests (brute
  * force, closed forms, invariants, hand-derived fixtures).
+ *
+ * Also here: the tied int8 embedding gather and LM head (below).
  */
 #ifndef DFSSM_REF_H
 #define DFSSM_REF_H
@@ -94,6 +96,28 @@ int dfssm_ref_chain(int n_layers, int64_t M, const int64_t* K,
                     const int8_t* const* A, const int8_t* const* B,
                     const float* const* beta, const int8_t* q0,
                     const float* s0, float* y_all, int8_t* q_all);
+
+/* The tied int8 embedding / LM head (Sec. 3.3: the embedding matrix is
+ * quantised to int8 per row; Table 1: embedding and LM head are one tied
+ * int8 table of 103 MB).  E [V,d] int8, scale [V] fp32: row v stands for
+ * scale[v] * E[v,:].
+ *
+ * Embedding gather of token ids tok [M] (0 <= tok < V, else
+ * DFSSM_REF_ERR_SHAPE):   x[m,k] = scale[tok[m]] * (float)E[tok[m],k]
+ * (one fp32 multiply, exact inputs).  d > 0. */
+int dfssm_ref_embed_gather(const int8_t* E, const float* scale, int64_t V, int64_t d,
+                           const int32_t* tok, int64_t M, float* x);
+
+/* LM head on per-token int8 hidden states (q, s) = quantise(h), the same
+ * quantiser as the linear's input:
+ *   acc[m,v]    = sum_k E[v,k] * Q[m,k]                 int32, exact
+ *   logits[m,v] = s[m] * (scale[v] * (float)acc[m,v])   fp32, this order,
+ *                                                       one rounding each
+ * (float)acc rounds to nearest-even (|acc| <= 127^2 d may exceed 2^24).
+ * acc or logits may be NULL.  d > 0, M >= 0, V >= 0. */
+int dfssm_ref_lm_head(const int8_t* q, const float* s, int64_t M, int64_t d,
+                      const int8_t* E, const float* scale, int64_t V,
+                      int32_t* acc, float* logits);
 
 /* Number of OpenMP threads the row loops use (1 without OpenMP). */
 int dfssm_ref_threads(void);

@@ -365,6 +365,103 @@ def pin_paper_sizes(o: Oracle):
     # a sign bit per weight: an all-shapes weight set has K*N/8 sign bytes
     ws = S.weights(2048, 8512, 16, key=(95,))
     assert ws["w_bits"].nbytes * 8 == 2048 * 8512
+    # the tied int8 embedding / LM head: one byte per entry of the
+    # 50,280 x 2048 table is "103 MB", 37% of the 278 MB model
+    emb = 50_280 * facts["model_shape"]["d_model"] * np.dtype(np.int8).itemsize
+    assert round(emb / 1e6) == t1["embedding_lm_head_int8_MB"]
+    assert round(100 * emb / 1e6 / t1["total_MB"]) == 37
+
+
+# --------------------------------------------------------------------------
+# tied int8 embedding / LM head
+# --------------------------------------------------------------------------
+def pin_embed_lm_hand(o: Oracle):
+    """Hand-derived: E = [[1, 2], [3, -4], [5, 6]], row scales (0.5, 2, 1)."""
+    E = np.array([[1, 2], [3, -4], [5, 6]], np.int8)
+    sc = np.array([0.5, 2.0, 1.0], F32)
+    x = o.embed_gather(E, sc, np.array([1, 0, 2], np.int32))
+    assert np.array_equal(x, np.array([[6, -8], [0.5, 1], [5, 6]], F32))
+    q = np.array([[1, 1], [2, -1]], np.int8)
+    s = np.array([0.25, 1.0], F32)
+    acc, logits = o.lm_head(q, s, E, sc)
+    assert np.array_equal(acc, np.array([[3, -1, 11], [0, 10, 4]], np.int32))
+    assert np.array_equal(logits, np.array([[0.375, -0.5, 2.75], [0.0, 20.0, 4.0]], F32))
+
+
+def _lm_case(M, V, d, seed):
+    rng = np.random.default_rng(seed)
+    E = rng.integers(-127, 128, (V, d), dtype=np.int8)
+    sc = rng.uniform(1e-3, 2e-2, V).astype(F32)
+    q, s = o_quant(M, d, seed)
+    return E, sc, q, s
+
+
+def o_quant(M, d, seed):
+    """Codes and scales from an independent quantiser written here (the
+    definition: s = a/127, Q = rint(x * (127/a)), fp32 each step)."""
+    x = S.activations(M, d, key=(96, seed)).astype(F32)
+    a = np.abs(x).max(axis=1).astype(F32)
+    s = (a / F32(127)).astype(F32)
+    inv = (F32(127) / a).astype(F32)
+    q = np.clip(np.rint((x * inv[:, None]).astype(F32)), -127, 127).astype(np.int8)
+    return q, s
+
+
+def pin_lm_head_bruteforce(o: Oracle):
+    """acc by an int64 matrix product; logits in the stated fp32 order,
+    element by element with numpy float32 scalars (one rounding each)."""
+    E, sc, q, s = _lm_case(3, 37, 96, 1)
+    acc, logits = o.lm_head(q, s, E, sc)
+    ref = q.astype(np.int64) @ E.astype(np.int64).T
+    assert np.array_equal(acc, ref.astype(np.int32))
+    for m in range(3):
+        for v in range(37):
+            t = F32(sc[v]) * F32(ref[m, v])
+            assert logits[m, v] == F32(s[m]) * t, (m, v)
+    # (float)acc rounds to nearest-even above 2^24: a row of all 127 against
+    # codes of all 127 gives 127^2 * 1056 = 17,032,224 (even, exact) and
+    # with one code 126 gives 17,032,097, which fp32 rounds to 17,032,096
+    E2 = np.full((2, 1056), 127, np.int8)
+    q2 = np.full((1, 1056), 127, np.int8)
+    q2[0, 0] = 126
+    acc2, lg2 = o.lm_head(q2, np.ones(1, F32), E2, np.ones(2, F32))
+    assert acc2[0, 0] == 17_032_097 and lg2[0, 0] == F32(17_032_096)
+
+
+def pin_lm_head_closed_forms(o: Oracle):
+    """All-ones rows with unit scale give the row sum of the codes; identity
+    rows give the codes themselves; the scale of row v scales only logit v."""
+    _, _, q, s = _lm_case(2, 1, 64, 2)
+    acc, _ = o.lm_head(q, s, np.ones((3, 64), np.int8), np.ones(3, F32))
+    assert np.array_equal(acc, np.repeat(q.astype(np.int64).sum(axis=1, keepdims=True), 3, axis=1))
+    acc, logits = o.lm_head(q, s, np.eye(64, dtype=np.int8), np.ones(64, F32))
+    assert np.array_equal(acc, q.astype(np.int32))
+    assert np.array_equal(logits, (s[:, None] * q.astype(F32)).astype(F32))
+    E, sc, q, s = _lm_case(2, 11, 32, 3)
+    _, l1 = o.lm_head(q, s, E, sc)
+    sc2 = sc.copy()
+    sc2[4] *= F32(2)
+    _, l2 = o.lm_head(q, s, E, sc2)
+    assert np.array_equal(np.delete(l1, 4, axis=1), np.delete(l2, 4, axis=1))
+    assert np.array_equal(l2[:, 4], (F32(2) * l1[:, 4]).astype(F32))
+
+
+def pin_embed_gather_bruteforce(o: Oracle):
+    """Each gathered value is one fp32 product scale[t] * E[t, k]; ids out of
+    range are refused."""
+    E, sc, _, _ = _lm_case(1, 29, 64, 4)
+    tok = np.array([28, 0, 5, 5], np.int32)
+    x = o.embed_gather(E, sc, tok)
+    for m, t in enumerate(tok):
+        for k in range(64):
+            assert x[m, k] == F32(sc[t]) * F32(E[t, k])
+    for bad in ([29], [-1]):
+        try:
+            o.embed_gather(E, sc, np.array(bad, np.int32))
+        except OracleError as e:
+            assert e.status == 2
+        else:
+            raise AssertionError("an out-of-range token id was accepted")
 
 
 def pin_validation(o: Oracle):
@@ -381,4 +478,5 @@ def pin_validation(o: Oracle):
 
 ALL_PINS = [pin_f16_decode, pin_quantize_hand_cases, pin_quantize_properties, pin_hand_linear,
             pin_bruteforce, pin_popcount_identity, pin_special_bits, pin_permutation, pin_extremes,
-            pin_rank0, pin_y32_order, pin_chain, pin_paper_sizes, pin_validation]
+            pin_rank0, pin_y32_order, pin_chain, pin_paper_sizes, pin_embed_lm_hand, pin_lm_head_bruteforce,
+            pin_lm_head_closed_forms, pin_embed_gather_bruteforce, pin_validation]

@@ -36,6 +36,14 @@ MUTANTS = [
     ("zero_row_unit_scale", [("if (a < FLT_MIN) {\n      s[m] = 0.0f;", "if (a < FLT_MIN) {\n      s[m] = 1.0f;")]),
     ("chain_keeps_scale", [("for (int64_t m = 0; m < M; ++m) sbuf[m] = 1.0f / 127.0f;", "(void)0;")]),
     ("chain_wrong_prefix_stride", [("N[l - 1], qbuf, sbuf);", "K[l], qbuf, sbuf);")]),
+    ("lm_head_scale_row0", [("float t = scale[v] * fa;", "float t = scale[0] * fa;")]),
+    ("lm_head_missing_s", [("logits[m * V + v] = s[m] * t;", "logits[m * V + v] = t;")]),
+    ("lm_head_scale_order", [("float t = scale[v] * fa;\n        logits[m * V + v] = s[m] * t;",
+                              "float t = s[m] * fa;\n        logits[m * V + v] = scale[v] * t;")]),
+    ("lm_head_E_transposed", [("(int64_t)E[v * d + k] * (int64_t)q[m * d + k]",
+                               "(int64_t)E[(k % V) * d + (v % d)] * (int64_t)q[m * d + k]")]),
+    ("lm_head_acc_int16", [("if (acc) acc[m * V + v] = (int32_t)sum;", "if (acc) acc[m * V + v] = (int16_t)sum;")]),
+    ("embed_row_of_m", [("x[m * d + k] = scale[v] * (float)E[v * d + k];", "x[m * d + k] = scale[v] * (float)E[m * d + k];")]),
 ]
 
 
