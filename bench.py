@@ -45,6 +45,7 @@ def parse():
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--no-prefill", action="store_true")
     p.add_argument("--no-decode", action="store_true", help="skip the single-linear decode-size figures")
+    p.add_argument("--no-lm-head", action="store_true", help="skip the LM head figures")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="minimum CPU oracle sample time")
     p.add_argument("--copy-calibration-mib", type=int, default=0,
                    help="run one plain device copy of this size first (for HBM counter scaling)")
@@ -244,6 +245,48 @@ def main():
                 del g
             del cps, base
 
+    # ---- LM head on the tied int8 embedding ---------------------------------
+    # logits of M tokens over the 1.3B vocabulary (50,280 x 2048 int8 table,
+    # 103 MB).  One graph replay walks over 4 distinct copies of the table
+    # (412 MB), so every call streams its table from HBM.
+    lm = None
+    if not args.no_lm_head:
+        lm = []
+        Eh, sch = S.embedding(S.VOCAB_1P3B, S.D_MODEL_1P3B, key=(40,))
+        tb = Eh.nbytes + sch.nbytes
+        tabs = [(dev(Eh), dev(sch))]
+        tabs += [(tabs[0][0].clone(), tabs[0][1].clone()) for _ in range(3)]
+        del Eh
+        for m in (1, 4):
+            qd, sd = D.quantize_act(dev(S.activations(m, S.D_MODEL_1P3B, key=(45,))))
+            lg = torch.empty((m, S.VOCAB_1P3B), dtype=torch.float32, device="cuda")
+
+            def lcalls():
+                for E_, sc_ in tabs:
+                    D.lm_head(qd, sd, E_, sc_, logits=lg)
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                lcalls()
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=side):
+                    lcalls()
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            reps = 5
+            t0.record(stream)
+            for _ in range(reps):
+                g.replay()
+            t1.record(stream)
+            torch.cuda.synchronize()
+            us = t0.elapsed_time(t1) * 1e3 / (reps * len(tabs))
+            lm.append({"workload": f"LM head 50280 x 2048 int8 table, M={m}", "us_per_call": round(us, 2),
+                       "table_gbs": round(tb / (us * 1e-6) / 1e9, 1),
+                       "frac_hbm_peak": round(tb / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4), "table_bytes": tb})
+            del g
+        del tabs
+
     # ---- CPU oracle baseline on a bounded sample ----------------------------
     cpu = None
     if not args.no_cpu:
@@ -289,6 +332,7 @@ def main():
                      "algorithmic_bytes_per_launch": weight_bytes},
         "prefill": prefill,
         "decode_linears": decode,
+        "lm_head": lm,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

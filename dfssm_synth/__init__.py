@@ -15,6 +15,13 @@ and out_proj 4096 -> 2048; the 130M model has d_model 768 and in_proj
   beta        U(1e-4, 1e-3) fp32 per output row (times beta_scale)
   x           fp16 N(0,1), with a fixed seeded set of round(0.01*K) input
               channels multiplied by 20 (activation outliers)
+  E           int8 embedding table [V, d]: round(N(0,1) * 32) clipped to
+              [-127, 127] (a Gaussian row quantised with absmax near 4 sigma)
+  scale       U(2e-4, 1e-3) fp32 per table row
+  tok         int32 token ids, uniform on [0, V)
+
+The tied embedding of the 1.3B model is 50,280 x 2048 (Table 1: 103 MB in
+int8).
 
 Each tensor set has its own numpy PCG64 stream keyed by
 (config, layer, projection, variant), so sets never share a stream.
@@ -30,6 +37,8 @@ import numpy as np
 IN_PROJ_1P3B = (2048, 8512)
 OUT_PROJ_1P3B = (4096, 2048)
 N_LAYERS_1P3B = 48
+VOCAB_1P3B = 50280
+D_MODEL_1P3B = 2048
 
 
 @dataclass(frozen=True)
@@ -118,3 +127,19 @@ def sweep_input(M: int = 1, K: int = IN_PROJ_1P3B[0], variant: int = 0) -> np.nd
 def weight_bytes(ws: dict) -> int:
     """Bytes of one weight set as stored: signs + A + B + alpha + beta."""
     return int(sum(ws[k].nbytes for k in ("w_bits", "A", "B", "alpha", "beta")))
+
+
+def embedding(V: int, d: int, key=(0,)) -> Tuple[np.ndarray, np.ndarray]:
+    """(E int8 [V, d], scale fp32 [V]) of a tied int8 embedding table."""
+    g = _rng(4, *key)
+    z = g.standard_normal((V, d), dtype=np.float32)
+    z *= np.float32(32.0)
+    np.rint(z, out=z)
+    np.clip(z, -127, 127, out=z)
+    scale = g.uniform(2e-4, 1e-3, size=V).astype(np.float32)
+    return z.astype(np.int8), scale
+
+
+def tokens(M: int, V: int, key=(0,)) -> np.ndarray:
+    """int32 token ids [M], uniform on [0, V)."""
+    return _rng(5, *key).integers(0, V, size=M, dtype=np.int32)

@@ -204,6 +204,38 @@ dfssm_status dfssm_chain_status(const dfssm_layer* layers, int n_layers, int64_t
                                 const void* workspace, size_t workspace_bytes, unsigned* status,
                                 void* stream);
 
+/* The tied int8 embedding table (Sec. 3.3 and Table 1: the token embedding
+ * is stored in int8 with one fp32 scale per row and shared with the LM
+ * head):
+ *   E      [V, d]  int8 table
+ *   scale  [V]     fp32 row scale
+ *
+ * Token gather (the model's input rows):
+ *   tok    [M]     int32 token ids;  x [M, d] fp32 output
+ *   x[m,k] = scale[t] * (float)E[t,k] with t = tok[m] (one fp32 rounding).
+ * The ids are read on the device: an id outside [0, V) is not an error, it
+ * gives a zero row.
+ * Limits: 0 < d <= 65536, d % 16 == 0; 0 < V < 2^30; M >= 0 (0 is a no-op).
+ * Errors: NULL, SHAPE, ALIGN, DEVICE. */
+dfssm_status dfssm_embed_gather(const int8_t* E, const float* scale, int64_t V, int64_t d,
+                                const int32_t* tok, int64_t M, float* x, void* stream);
+
+/* LM head on the tied table: the logits of M tokens over the whole
+ * vocabulary from the int8-quantised final hidden state (q [M, d], s [M],
+ * as dfssm_quantize_act makes them):
+ *   acc[m,v]    = sum_k E[v,k] * Q[m,k]                  (int32, exact)
+ *   logits[m,v] = s[m] * (scale[v] * (float)acc[m,v])    (fp32, rounded
+ *                 after each operation, in this order)
+ *   logits [M, V] fp32 output, or NULL;  acc [M, V] int32 output, or NULL
+ *   (not both NULL).
+ * Made for decoding (a few tokens: each pass of up to 4 tokens, or fewer for
+ * d > 4096, streams the table once); M tokens take ceil(M / 4) passes.
+ * Limits: 0 < d <= 16384, d % 16 == 0; 0 <= V < 2^30; M >= 0 (M or V == 0
+ * is a no-op).
+ * Errors: NULL, SHAPE, ALIGN, DEVICE. */
+dfssm_status dfssm_lm_head(const int8_t* q, const float* s, int64_t M, int64_t d, const int8_t* E,
+                           const float* scale, int64_t V, float* logits, int32_t* acc, void* stream);
+
 /* Static text for a status code. */
 const char* dfssm_status_string(int status);
 /* Thread-local description of the last failure on this thread ("" if none). */

@@ -22,7 +22,8 @@ PATH_AUTO, PATH_DECODE, PATH_MFMA, PATH_MFMA_FEW = 0, 1, 2, 3
 EXPORTS = ["dfssm_quantize_act", "dfssm_linear_workspace_bytes", "dfssm_scaffold_lora_linear",
            "dfssm_scaffold_lora_linear_ex", "dfssm_chain_workspace_bytes",
            "dfssm_scaffold_lora_chain", "dfssm_chain_prepare", "dfssm_chain_run", "dfssm_chain_status",
-           "dfssm_status_string", "dfssm_last_error", "dfssm_version"]
+           "dfssm_embed_gather", "dfssm_lm_head", "dfssm_status_string", "dfssm_last_error",
+           "dfssm_version"]
 
 
 class DfssmError(RuntimeError):
@@ -62,6 +63,10 @@ def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dfssm_chain_run.restype = i32
     lib.dfssm_chain_status.argtypes = [ctypes.POINTER(Layer), i32, i64, vp, sz, ctypes.POINTER(ctypes.c_uint), vp]
     lib.dfssm_chain_status.restype = i32
+    lib.dfssm_embed_gather.argtypes = [vp, vp, i64, i64, vp, i64, vp, vp]
+    lib.dfssm_embed_gather.restype = i32
+    lib.dfssm_lm_head.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp, vp]
+    lib.dfssm_lm_head.restype = i32
     lib.dfssm_status_string.argtypes = [i32]
     lib.dfssm_status_string.restype = ctypes.c_char_p
     lib.dfssm_last_error.restype = ctypes.c_char_p
@@ -233,3 +238,43 @@ def chain_status(layer_arr, M: int, workspace, stream=None) -> int:
     _check(lib.dfssm_chain_status(layer_arr, len(layer_arr), M, workspace.data_ptr(), workspace.numel(),
                                   ctypes.byref(out), _stream(stream)))
     return int(out.value)
+
+
+def embed_gather(E, scale, tok, x=None, stream=None):
+    """x [M, d] fp32 = scale[tok] * E[tok, :] for the int8 table E [V, d],
+    row scales scale [V] and int32 ids tok [M]; ids outside [0, V) give zero
+    rows."""
+    torch = _torch()
+    _need(E, torch.int8, "E", 2)
+    _need(scale, torch.float32, "scale", 1)
+    _need(tok, torch.int32, "tok", 1)
+    V, d = E.shape
+    M = tok.shape[0]
+    x = torch.empty((M, d), dtype=torch.float32, device=E.device) if x is None else x
+    _need(x, torch.float32, "x", 2)
+    if tuple(x.shape) != (M, d) or scale.shape[0] != V:
+        raise ValueError("x must be [M, d] and scale [V]")
+    _check(lib.dfssm_embed_gather(E.data_ptr(), scale.data_ptr(), V, d, tok.data_ptr(), M, x.data_ptr(),
+                                  _stream(stream)))
+    return x
+
+
+def lm_head(q, s, E, scale, logits=None, acc: bool = False, stream=None):
+    """logits [M, V] fp32 = s[m] * (scale[v] * (E Q^T)[m, v]) for int8 codes
+    q [M, d], scales s [M] and the tied int8 table E [V, d] with row scales
+    scale [V].  With acc=True returns (logits, acc int32 [M, V])."""
+    torch = _torch()
+    _need(q, torch.int8, "q", 2)
+    _need(s, torch.float32, "s", 1)
+    _need(E, torch.int8, "E", 2)
+    _need(scale, torch.float32, "scale", 1)
+    M, d = q.shape
+    V = E.shape[0]
+    if E.shape[1] != d or scale.shape[0] != V or s.shape[0] != M:
+        raise ValueError("E must be [V, d], scale [V] and s [M]")
+    logits = torch.empty((M, V), dtype=torch.float32, device=q.device) if logits is None else logits
+    _need(logits, torch.float32, "logits", 2)
+    a = torch.empty((M, V), dtype=torch.int32, device=q.device) if acc else None
+    _check(lib.dfssm_lm_head(q.data_ptr(), s.data_ptr(), M, d, E.data_ptr(), scale.data_ptr(), V,
+                             logits.data_ptr(), _ptr(a), _stream(stream)))
+    return (logits, a) if acc else logits

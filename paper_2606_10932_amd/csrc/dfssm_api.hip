@@ -413,4 +413,35 @@ dfssm_status dfssm_chain_status(const dfssm_layer* layers, int n_layers, int64_t
   return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain status read");
 }
 
+dfssm_status dfssm_embed_gather(const int8_t* E, const float* scale, int64_t V, int64_t d, const int32_t* tok,
+                                int64_t M, float* x, void* stream) {
+  clear_error();
+  if (d <= 0 || d % 16 != 0 || d > dfssm::kMaxK)
+    return fail(DFSSM_ERR_SHAPE, "d=%lld must be a positive multiple of 16 and <= %lld", (long long)d,
+                (long long)dfssm::kMaxK);
+  if (V <= 0 || V > INT32_MAX / 2) return fail(DFSSM_ERR_SHAPE, "V=%lld must be in [1, 2^30)", (long long)V);
+  if (M < 0 || M > INT32_MAX / 2) return fail(DFSSM_ERR_SHAPE, "M=%lld", (long long)M);
+  if (M == 0) return DFSSM_OK;
+  dfssm_status st = check_ptrs({{E, "E"}, {scale, "scale"}, {tok, "tok"}, {x, "x"}}, {});
+  if (st != DFSSM_OK) return st;
+  hipError_t e = dfssm::launch_embed_gather(E, scale, V, d, tok, M, x, (hipStream_t)stream);
+  return e == hipSuccess ? DFSSM_OK : device_fail(e, "embed gather launch");
+}
+
+dfssm_status dfssm_lm_head(const int8_t* q, const float* s, int64_t M, int64_t d, const int8_t* E,
+                           const float* scale, int64_t V, float* logits, int32_t* acc, void* stream) {
+  clear_error();
+  if (d <= 0 || d % 16 != 0 || d > dfssm::kLmHeadMaxD)
+    return fail(DFSSM_ERR_SHAPE, "d=%lld must be a positive multiple of 16 and <= %lld", (long long)d,
+                (long long)dfssm::kLmHeadMaxD);
+  if (V < 0 || V > INT32_MAX / 2) return fail(DFSSM_ERR_SHAPE, "V=%lld must be in [0, 2^30)", (long long)V);
+  if (M < 0 || M > INT32_MAX / 2) return fail(DFSSM_ERR_SHAPE, "M=%lld", (long long)M);
+  if (M == 0 || V == 0) return DFSSM_OK;
+  dfssm_status st = check_ptrs({{q, "q"}, {s, "s"}, {E, "E"}, {scale, "scale"}}, {{logits, "logits"}, {acc, "acc"}});
+  if (st != DFSSM_OK) return st;
+  if (!logits && !acc) return fail(DFSSM_ERR_NULL, "logits and acc are both NULL");
+  hipError_t e = dfssm::launch_lm_head(q, s, M, d, E, scale, V, logits, acc, (hipStream_t)stream);
+  return e == hipSuccess ? DFSSM_OK : device_fail(e, "lm head launch");
+}
+
 }  // extern "C"

@@ -108,6 +108,20 @@ hipError_t launch_mfma_linear(const int8_t* q, const float* s, int64_t M, int64_
                               int32_t* acc_s, int32_t* acc_a_out, int64_t* acc_b,
                               const LinearWorkspace& ws, hipStream_t st);
 
+// ---------------------------------------------------------------- embedding
+// Largest row length of the int8 embedding table the LM head takes (its
+// per-lane slices of the token codes stay in registers).
+constexpr int64_t kLmHeadMaxD = 16384;
+
+// Tied int8 embedding table E [V, d] with row scales: token gather
+// x = scale[t] * E[t, :] (zero rows for ids outside [0, V)), and the LM head
+// logits = s[m] * (scale[v] * (float)(E Q^T)) over all V rows, in passes of
+// up to 4 tokens.  d % 16 == 0.
+hipError_t launch_embed_gather(const int8_t* E, const float* scale, int64_t V, int64_t d, const int32_t* tok,
+                               int64_t M, float* x, hipStream_t st);
+hipError_t launch_lm_head(const int8_t* q, const float* s, int64_t M, int64_t d, const int8_t* E,
+                          const float* scale, int64_t V, float* logits, int32_t* acc, hipStream_t st);
+
 // ---------------------------------------------------------------- chain
 // Largest K the persistent chain kernel takes (its per-thread register
 // staging of the previous output holds K/512 values).

@@ -1,0 +1,216 @@
+// dfssm_lmhead.hip -- the tied int8 embedding table of the model: token
+// gather and LM head, gfx950.
+//
+// The table is int8 per row with a fp32 row scale (Sec. 3.3: the embedding
+// is quantised to int8 per row; Table 1: embedding and LM head tied, 103 MB
+// for the 1.3B model's 50,280 x 2048).  The LM head takes the final hidden
+// state through the same per-token int8 quantiser as the linears:
+//
+//   acc[m,v]    = sum_k E[v,k] Q[m,k]                 exact int32
+//   logits[m,v] = s[m] * (scale[v] * (float)acc)      fp32, this order
+//
+// At a few tokens the LM head streams the whole table once (2 int-ops per
+// byte per token): HBM-bound.  A wave visits R rows at a time (4 KB of the
+// table: R = 2 rows of 2 KB at d = 2048); each lane holds its 16-byte slices
+// of every token's codes for the whole kernel, and every load of the R rows
+// is issued before the first v_dot4.  Waves stride over the row groups, so
+// the waves of the grid read neighbouring 4 KB pieces at any moment; the
+// table is read once, so its loads are non-temporal (no reuse to keep in the
+// caches).  Three workgroups (12 waves) per CU: more waves, bigger visits
+// and each wave owning one contiguous range of rows all measured slower.  Row sums go by DPP inside 16-lane
+// rows and gfx950's permlane swaps across them.
+#include <algorithm>
+
+#include "dfssm_internal.hpp"
+
+namespace {
+
+constexpr int kThreads = 256;
+
+// rows per wave visit: 4 KB of the table, or one row when rows are longer
+template <int NC>
+constexpr int rows_per_visit() { return NC >= 4 ? 1 : 4 / NC; }
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ u32x4 load_stream(const int8_t* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+
+__device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
+  return __builtin_amdgcn_sdot4((int)a, (int)b, c, false);
+}
+
+// whole-wave sum, the total in every lane
+__device__ __forceinline__ int wave_sum(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+  v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+  v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);  // row_half_mirror
+  v += __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);  // row_mirror
+  auto p = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v, false, false);
+  v = (int)(p[0] + p[1]);
+  p = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+  return (int)(p[0] + p[1]);
+}
+
+// MT tokens per pass, NC 1 KB chunks of a row (d <= 1024 * NC).  Lane l
+// owns bytes 16l + 1024c of every row (zero past d).
+template <int MT, int NC>
+__global__ __launch_bounds__(kThreads) void lm_head(const int8_t* __restrict__ q, const float* __restrict__ s,
+                                                    int d, const int8_t* __restrict__ E,
+                                                    const float* __restrict__ scale, int V,
+                                                    float* __restrict__ logits, int32_t* __restrict__ acc_out,
+                                                    int m0, int mt) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = gridDim.x * (kThreads / 64);
+  constexpr int R = rows_per_visit<NC>();
+  const int ngroups = (V + R - 1) / R;
+
+  // this lane's slices of the tokens' codes, and their scales
+  u32x4 qv[MT][NC];
+  float sv[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int k = 16 * lane + 1024 * c;
+      qv[m][c] = (m < mt && k < d) ? *reinterpret_cast<const u32x4*>(q + (int64_t)(m0 + m) * d + k)
+                                   : u32x4{0, 0, 0, 0};
+    }
+    sv[m] = m < mt ? s[m0 + m] : 0.0f;
+  }
+
+  for (int g = blockIdx.x * (kThreads / 64) + wave; g < ngroups; g += nwaves) {
+    const int v0 = g * R;
+    // every load of the R rows first (rows past V are not read)
+    u32x4 ev[R][NC];
+    float sc[R];
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      const int v = v0 + i;
+      const bool ok = v < V;
+      const int8_t* row = E + (int64_t)(ok ? v : 0) * d;
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const int k = 16 * lane + 1024 * c;
+        ev[i][c] = (ok && k < d) ? load_stream(row + k) : u32x4{0, 0, 0, 0};
+      }
+      sc[i] = ok ? scale[v] : 0.0f;
+    }
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      const int v = v0 + i;
+      int tot_m = 0;
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        int a = 0;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+          a = sdot4(ev[i][c].x, qv[m][c].x, a);
+          a = sdot4(ev[i][c].y, qv[m][c].y, a);
+          a = sdot4(ev[i][c].z, qv[m][c].z, a);
+          a = sdot4(ev[i][c].w, qv[m][c].w, a);
+        }
+        const int t = wave_sum(a);
+        tot_m = lane == m ? t : tot_m;  // lane m keeps token m's sum
+      }
+      if (lane < mt && v < V) {
+        const int m = lane;
+        float s_m = sv[0];
+#pragma unroll
+        for (int mm = 1; mm < MT; ++mm) s_m = m == mm ? sv[mm] : s_m;
+        const float fa = (float)tot_m;
+        const float t = sc[i] * fa;
+        if (logits) logits[(int64_t)(m0 + m) * V + v] = s_m * t;
+        if (acc_out) acc_out[(int64_t)(m0 + m) * V + v] = tot_m;
+      }
+    }
+  }
+}
+
+template <int MT, int NC>
+hipError_t launch_t(const int8_t* q, const float* s, int d, const int8_t* E, const float* scale, int V,
+                    float* logits, int32_t* acc, int m0, int mt, hipStream_t st) {
+  const int64_t groups = dfssm::ceil_div(V, rows_per_visit<NC>());
+  int64_t blocks = dfssm::ceil_div(groups, kThreads / 64);
+  blocks = std::max<int64_t>(1, std::min<int64_t>(blocks, 3 * dfssm::device_cu_count()));
+  lm_head<MT, NC><<<dim3((unsigned)blocks), dim3(kThreads), 0, st>>>(q, s, d, E, scale, V, logits, acc, m0, mt);
+  return hipGetLastError();
+}
+
+template <int NC>
+hipError_t launch_nc(const int8_t* q, const float* s, int64_t M, int d, const int8_t* E, const float* scale,
+                     int V, float* logits, int32_t* acc, hipStream_t st) {
+  // tokens per pass: the codes of a pass stay in registers (MT x NC x 16 B)
+  constexpr int MTmax = NC <= 4 ? 4 : (NC <= 8 ? 2 : 1);
+  for (int64_t m0 = 0; m0 < M; m0 += MTmax) {
+    const int mt = (int)std::min<int64_t>(MTmax, M - m0);
+    hipError_t e;
+    if (mt == 1)
+      e = launch_t<1, NC>(q, s, d, E, scale, V, logits, acc, (int)m0, mt, st);
+    else if (mt == 2 && MTmax >= 2)
+      e = launch_t<(MTmax >= 2 ? 2 : 1), NC>(q, s, d, E, scale, V, logits, acc, (int)m0, mt, st);
+    else
+      e = launch_t<MTmax, NC>(q, s, d, E, scale, V, logits, acc, (int)m0, mt, st);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// x[m, k .. k+15] = scale[t] * E[t, k .. k+15] for one 16-byte piece per thread;
+// an id outside [0, V) gives a zero row
+__global__ __launch_bounds__(kThreads) void embed_gather(const int8_t* __restrict__ E, const float* __restrict__ scale,
+                                                         int V, int d, const int32_t* __restrict__ tok, int64_t M,
+                                                         float* __restrict__ x) {
+  const int64_t per_row = d / 16;
+  const int64_t total = M * per_row;
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < total; i += (int64_t)gridDim.x * kThreads) {
+    const int64_t m = i / per_row;
+    const int k = (int)(i % per_row) * 16;
+    const int t = tok[m];
+    float4* dst = reinterpret_cast<float4*>(x + m * d + k);
+    if (t < 0 || t >= V) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) dst[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      continue;
+    }
+    const float sc = scale[t];
+    const uint4 e = *reinterpret_cast<const uint4*>(E + (int64_t)t * d + k);
+    const uint32_t w[4] = {e.x, e.y, e.z, e.w};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float a = sc * (float)(int8_t)(w[u] & 0xff);
+      const float b = sc * (float)(int8_t)((w[u] >> 8) & 0xff);
+      const float c = sc * (float)(int8_t)((w[u] >> 16) & 0xff);
+      const float dd = sc * (float)(int8_t)(w[u] >> 24);
+      dst[u] = make_float4(a, b, c, dd);
+    }
+  }
+}
+
+}  // namespace
+
+namespace dfssm {
+
+hipError_t launch_lm_head(const int8_t* q, const float* s, int64_t M, int64_t d, const int8_t* E,
+                          const float* scale, int64_t V, float* logits, int32_t* acc, hipStream_t st) {
+  if (M == 0 || V == 0) return hipSuccess;
+  const int64_t nc = ceil_div(d, 1024);
+  if (nc <= 1) return launch_nc<1>(q, s, M, (int)d, E, scale, (int)V, logits, acc, st);
+  if (nc <= 2) return launch_nc<2>(q, s, M, (int)d, E, scale, (int)V, logits, acc, st);
+  if (nc <= 4) return launch_nc<4>(q, s, M, (int)d, E, scale, (int)V, logits, acc, st);
+  if (nc <= 8) return launch_nc<8>(q, s, M, (int)d, E, scale, (int)V, logits, acc, st);
+  return launch_nc<16>(q, s, M, (int)d, E, scale, (int)V, logits, acc, st);
+}
+
+hipError_t launch_embed_gather(const int8_t* E, const float* scale, int64_t V, int64_t d, const int32_t* tok,
+                               int64_t M, float* x, hipStream_t st) {
+  if (M == 0) return hipSuccess;
+  const int64_t total = M * (d / 16);
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, kThreads), 4096));
+  embed_gather<<<dim3((unsigned)blocks), dim3(kThreads), 0, st>>>(E, scale, (int)V, (int)d, tok, M, x);
+  return hipGetLastError();
+}
+
+}  // namespace dfssm

@@ -111,6 +111,28 @@ def test_chain_validation(dl):
     assert dl.lib.dfssm_chain_status(arr, 2, 1, 16, 1 << 30, None, None) == dl.ERR_NULL
 
 
+def test_embedding_validation(dl):
+    g = dl.lib.dfssm_embed_gather      # E, scale, V, d, tok, M, x, stream
+    assert g(16, 16, 100, 24, 16, 1, 16, None) == dl.ERR_SHAPE       # d % 16
+    assert g(16, 16, 100, 0, 16, 1, 16, None) == dl.ERR_SHAPE
+    assert g(16, 16, 0, 64, 16, 1, 16, None) == dl.ERR_SHAPE         # empty table
+    assert g(16, 16, 100, 64, 16, -1, 16, None) == dl.ERR_SHAPE
+    assert g(None, 16, 100, 64, 16, 1, 16, None) == dl.ERR_NULL
+    assert g(16, 16, 100, 64, None, 1, 16, None) == dl.ERR_NULL
+    assert g(16, 16, 100, 64, 16, 1, 20, None) == dl.ERR_ALIGN
+    assert g(None, None, 100, 64, None, 0, None, None) == dl.OK      # M = 0
+    h = dl.lib.dfssm_lm_head           # q, s, M, d, E, scale, V, logits, acc, stream
+    assert h(16, 16, 1, 24, 16, 16, 100, 16, None, None) == dl.ERR_SHAPE
+    assert h(16, 16, 1, 16384 + 16, 16, 16, 100, 16, None, None) == dl.ERR_SHAPE
+    assert h(16, 16, 1, 64, 16, 16, -1, 16, None, None) == dl.ERR_SHAPE
+    assert h(16, 16, -1, 64, 16, 16, 100, 16, None, None) == dl.ERR_SHAPE
+    assert h(16, 16, 1, 64, 16, 16, 100, None, None, None) == dl.ERR_NULL   # no output
+    assert h(16, 16, 1, 64, None, 16, 100, 16, None, None) == dl.ERR_NULL
+    assert h(16, 16, 1, 64, 16, 16, 100, 16, 36, None) == dl.ERR_ALIGN
+    assert h(None, None, 0, 64, None, None, 100, None, None, None) == dl.OK
+    assert h(None, None, 1, 64, None, None, 0, None, None, None) == dl.OK   # V = 0
+
+
 def test_workspace_sizes(dl):
     a = dl.linear_workspace_bytes(1, 2048, 8512, 64)
     b = dl.linear_workspace_bytes(2048, 2048, 8512, 64)
