@@ -7,7 +7,8 @@ dfssm_chain_run, i.e. one launch of the persistent chain kernel, on a
 workspace prepared once per weight set (dfssm_chain_prepare, untimed).
 Metric: effective packed-weight GB/s (sign words + LoRA factors + row scales
 read per step / step time) and us per layer; the 2048-token prefill in_proj
-is measured beside it in int8 TOPS.
+is measured beside it in int8 TOPS, the decode-size single linears in us per
+call, and the LM head over the 1.3B tied int8 table (103 MB) in GB/s.
 
 Weights are synthetic and seeded (no trained weights exist here).  The sweep
 reads 210 MB per step, which fits the 256 MB Infinity Cache, so steps rotate
