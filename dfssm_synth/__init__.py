@@ -23,6 +23,16 @@ and out_proj 4096 -> 2048; the 130M model has d_model 768 and in_proj
 The tied embedding of the 1.3B model is 50,280 x 2048 (Table 1: 103 MB in
 int8).
 
+Mamba-2 decode-step parameters and state (d_inner = 2 d_model, heads of 64
+channels, d_state 128 for the 1.3B model, one B/C group, d_conv 4):
+
+  conv_w      U(-0.5, 0.5) fp32 [conv_dim][4];  conv_b U(-0.1, 0.1)
+  dt_bias     U(-6.9, -2.3) (softplus of it spans about 1e-3 .. 0.1)
+  A_log       U(0, 2.77)    (A = -exp(A_log) spans -1 .. -16)
+  D           U(0.5, 1.5);  norm weights U(0.8, 1.2)
+  conv state  N(0, 1) [M][conv_dim][4];  SSM state 0.5 N(0, 1) [M][H][P][N]
+  in_proj out N(0, 1) fp32 [M][2 d_inner + 2 N + H];  residual N(0, 1)
+
 Each tensor set has its own numpy PCG64 stream keyed by
 (config, layer, projection, variant), so sets never share a stream.
 """
@@ -143,3 +153,46 @@ def embedding(V: int, d: int, key=(0,)) -> Tuple[np.ndarray, np.ndarray]:
 def tokens(M: int, V: int, key=(0,)) -> np.ndarray:
     """int32 token ids [M], uniform on [0, V)."""
     return _rng(5, *key).integers(0, V, size=M, dtype=np.int32)
+
+
+def mamba_dims(d_model: int, d_state: int = 128, headdim: int = 64) -> dict:
+    """Sizes of one Mamba-2 mixer (one B/C group, d_conv 4)."""
+    d_inner = 2 * d_model
+    H = d_inner // headdim
+    conv_dim = d_inner + 2 * d_state
+    return dict(d_model=d_model, d_inner=d_inner, d_state=d_state, headdim=headdim, nheads=H,
+                conv_dim=conv_dim, ld=d_inner + conv_dim + H)
+
+
+def mamba_params(d_model: int, d_state: int = 128, headdim: int = 64, key=(0,)) -> dict:
+    """Per-layer parameters of the step around the linears (numpy, host)."""
+    dm = mamba_dims(d_model, d_state, headdim)
+    g = _rng(6, *key)
+    f = np.float32
+    return dict(conv_w=g.uniform(-0.5, 0.5, (dm["conv_dim"], 4)).astype(f),
+                conv_b=g.uniform(-0.1, 0.1, dm["conv_dim"]).astype(f),
+                dt_bias=g.uniform(-6.9, -2.3, dm["nheads"]).astype(f),
+                A_log=g.uniform(0.0, 2.77, dm["nheads"]).astype(f),
+                D=g.uniform(0.5, 1.5, dm["nheads"]).astype(f),
+                norm_w=g.uniform(0.8, 1.2, d_model).astype(f),
+                gate_w=g.uniform(0.8, 1.2, dm["d_inner"]).astype(f))
+
+
+def mamba_state(M: int, d_model: int, d_state: int = 128, headdim: int = 64, key=(0,)) -> dict:
+    """conv_state [M][conv_dim][4] (position 3 newest) and ssm_state [M][H][P][N]."""
+    dm = mamba_dims(d_model, d_state, headdim)
+    g = _rng(7, *key)
+    conv = g.standard_normal((M, dm["conv_dim"], 4), dtype=np.float32)
+    ssm = g.standard_normal((M, dm["nheads"], headdim, d_state), dtype=np.float32)
+    ssm *= np.float32(0.5)
+    return dict(conv_state=conv, ssm_state=ssm)
+
+
+def inproj_out(M: int, d_model: int, d_state: int = 128, headdim: int = 64, key=(0,)) -> np.ndarray:
+    """A stand-in for in_proj's fp32 output rows [z | x | B | C | dt]."""
+    dm = mamba_dims(d_model, d_state, headdim)
+    return _rng(8, *key).standard_normal((M, dm["ld"]), dtype=np.float32)
+
+
+def residual(M: int, d_model: int, key=(0,)) -> np.ndarray:
+    return _rng(9, *key).standard_normal((M, d_model), dtype=np.float32)

@@ -61,6 +61,13 @@ class Oracle:
         lib.dfssm_ref_embed_gather.restype = i32
         lib.dfssm_ref_lm_head.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp]
         lib.dfssm_ref_lm_head.restype = i32
+        f32 = ctypes.c_float
+        lib.dfssm_ref_add_rmsnorm_quant.argtypes = [vp, vp, vp, f32, i64, i64, vp, vp, vp, vp]
+        lib.dfssm_ref_add_rmsnorm_quant.restype = i32
+        lib.dfssm_ref_ssm_step.argtypes = [vp, i64, i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        lib.dfssm_ref_ssm_step.restype = i32
+        lib.dfssm_ref_gate_norm_quant.argtypes = [vp, vp, i64, vp, f32, i64, i64, vp, vp, vp]
+        lib.dfssm_ref_gate_norm_quant.restype = i32
         self.lib = lib
 
     # -- activation quantisation ------------------------------------------------
@@ -184,6 +191,61 @@ class Oracle:
         if st != OK:
             raise OracleError(st)
         return acc, logits
+
+    # ---- Mamba-2 decode step around the linears ----------------------------
+    def add_rmsnorm_quant(self, u, w, eps, delta=None):
+        """Returns (u_out, o, Q, s): u_out = u + delta, o = rmsnorm(u_out) * w
+        (fp32), (Q, s) = quantise(o)."""
+        u = np.ascontiguousarray(u, np.float32)
+        w = np.ascontiguousarray(w, np.float32)
+        M, d = u.shape
+        dl = None if delta is None else np.ascontiguousarray(delta, np.float32)
+        u_out = np.zeros((M, d), np.float32)
+        o = np.zeros((M, d), np.float32)
+        q = np.zeros((M, d), np.int8)
+        s = np.zeros((M,), np.float32)
+        st = self.lib.dfssm_ref_add_rmsnorm_quant(_p(u), _p(dl), _p(w), float(eps), M, d, _p(u_out), _p(o),
+                                                 _p(q), _p(s))
+        if st != OK:
+            raise OracleError(st)
+        return u_out, o, q, s
+
+    def ssm_step(self, zxbcdt, conv_state, ssm_state, conv_w, conv_b, dt_bias, A_log, D, d_inner, d_state,
+                 headdim):
+        """One token per sequence through the conv step and the SSM step.
+        conv_state [M, conv_dim, 4] (position 3 newest) and ssm_state
+        [M, H, P, N] are copied, not modified.  Returns (y [M, d_inner],
+        xbc [M, conv_dim], conv_state', ssm_state')."""
+        zx = np.ascontiguousarray(zxbcdt, np.float32)
+        M, ld = zx.shape
+        conv_dim = d_inner + 2 * d_state
+        cs = np.array(conv_state, np.float32, copy=True, order="C")
+        hs = np.array(ssm_state, np.float32, copy=True, order="C")
+        if cs.shape != (M, conv_dim, 4) or hs.shape != (M, d_inner // headdim, headdim, d_state):
+            raise ValueError("state shapes")
+        arrs = [np.ascontiguousarray(a, np.float32) for a in (conv_w, conv_b, dt_bias, A_log, D)]
+        y = np.zeros((M, d_inner), np.float32)
+        xbc = np.zeros((M, conv_dim), np.float32)
+        st = self.lib.dfssm_ref_ssm_step(_p(zx), ld, M, d_inner, d_state, headdim, _p(cs), *[_p(a) for a in arrs],
+                                         _p(hs), _p(y), _p(xbc))
+        if st != OK:
+            raise OracleError(st)
+        return y, xbc, cs, hs
+
+    def gate_norm_quant(self, y, z, w, eps):
+        """Returns (o, Q, s): o = rmsnorm(y * silu(z)) * w, (Q, s) = quantise(o)."""
+        y = np.ascontiguousarray(y, np.float32)
+        z = np.ascontiguousarray(z, np.float32)
+        w = np.ascontiguousarray(w, np.float32)
+        M, d = y.shape
+        o = np.zeros((M, d), np.float32)
+        q = np.zeros((M, d), np.int8)
+        s = np.zeros((M,), np.float32)
+        st = self.lib.dfssm_ref_gate_norm_quant(_p(y), _p(z), z.shape[1], _p(w), float(eps), M, d, _p(o), _p(q),
+                                               _p(s))
+        if st != OK:
+            raise OracleError(st)
+        return o, q, s
 
     def threads(self) -> int:
         return self.lib.dfssm_ref_threads()

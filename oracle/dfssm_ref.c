@@ -252,3 +252,134 @@ int dfssm_ref_lm_head(const int8_t* q, const float* s, int64_t M, int64_t d,
   }
   return DFSSM_REF_OK;
 }
+
+/* ---- the Mamba-2 decode step around the linears ------------------------ */
+
+static float silu_f(float v) {
+  const double x = (double)v;
+  return (float)(x / (1.0 + exp(-x)));
+}
+
+static float softplus_f(float v) {
+  if (v > 20.0f) return v;
+  return (float)log1p(exp((double)v));
+}
+
+/* r = 1 / sqrt(mean of squares + eps), the sum in fp64 over exact squares. */
+static float rms_scale(const float* v, int64_t d, float eps) {
+  double ss = 0.0;
+  for (int64_t k = 0; k < d; ++k) ss += (double)v[k] * (double)v[k];
+  return (float)(1.0 / sqrt(ss / (double)d + (double)eps));
+}
+
+int dfssm_ref_add_rmsnorm_quant(const float* u, const float* delta, const float* w, float eps,
+                                int64_t M, int64_t d, float* u_out, float* o, int8_t* q,
+                                float* s) {
+  if (M < 0 || d <= 0 || !(eps >= 0.0f)) return DFSSM_REF_ERR_SHAPE;
+  if (M == 0) return DFSSM_REF_OK;
+  if (!u || !w || !q || !s) return DFSSM_REF_ERR_NULL;
+  float* res = (float*)malloc((size_t)d * sizeof(float));
+  float* on = (float*)malloc((size_t)(M * d) * sizeof(float));
+  if (!res || !on) {
+    free(res);
+    free(on);
+    return DFSSM_REF_ERR_NULL;
+  }
+  for (int64_t m = 0; m < M; ++m) {
+    for (int64_t k = 0; k < d; ++k) res[k] = delta ? u[m * d + k] + delta[m * d + k] : u[m * d + k];
+    const float r = rms_scale(res, d, eps);
+    for (int64_t k = 0; k < d; ++k) {
+      const float t = res[k] * r;
+      on[m * d + k] = t * w[k];
+    }
+    if (u_out)
+      for (int64_t k = 0; k < d; ++k) u_out[m * d + k] = res[k];
+  }
+  int st = dfssm_ref_quantize_act(on, DFSSM_REF_F32, M, d, d, q, s);
+  if (o && st == DFSSM_REF_OK) memcpy(o, on, (size_t)(M * d) * sizeof(float));
+  free(res);
+  free(on);
+  return st;
+}
+
+int dfssm_ref_ssm_step(const float* zxbcdt, int64_t ld, int64_t M, int64_t d_inner,
+                       int64_t d_state, int64_t headdim, float* conv_state,
+                       const float* conv_w, const float* conv_b, const float* dt_bias,
+                       const float* A_log, const float* D, float* ssm_state, float* y,
+                       float* xbc) {
+  if (M < 0 || d_inner <= 0 || d_state <= 0 || headdim <= 0 || d_inner % headdim) return DFSSM_REF_ERR_SHAPE;
+  const int64_t N = d_state, P = headdim, H = d_inner / headdim;
+  const int64_t conv_dim = d_inner + 2 * N;
+  if (ld < d_inner + conv_dim + H) return DFSSM_REF_ERR_SHAPE;
+  if (M == 0) return DFSSM_REF_OK;
+  if (!zxbcdt || !conv_state || !conv_w || !conv_b || !dt_bias || !A_log || !D || !ssm_state || !y)
+    return DFSSM_REF_ERR_NULL;
+  float* c_out = (float*)malloc((size_t)conv_dim * sizeof(float));
+  if (!c_out) return DFSSM_REF_ERR_NULL;
+  for (int64_t m = 0; m < M; ++m) {
+    const float* row = zxbcdt + m * ld;
+    /* convolution step: shift the register, append the new input, filter */
+    for (int64_t c = 0; c < conv_dim; ++c) {
+      float* st = conv_state + (m * conv_dim + c) * 4;
+      st[0] = st[1];
+      st[1] = st[2];
+      st[2] = st[3];
+      st[3] = row[d_inner + c];
+      const float* wc = conv_w + c * 4;
+      float v = wc[0] * st[0];
+      v = v + wc[1] * st[1];
+      v = v + wc[2] * st[2];
+      v = v + wc[3] * st[3];
+      v = v + conv_b[c];
+      c_out[c] = silu_f(v);
+    }
+    if (xbc) memcpy(xbc + m * conv_dim, c_out, (size_t)conv_dim * sizeof(float));
+    const float* Bv = c_out + d_inner;
+    const float* Cv = c_out + d_inner + N;
+    /* SSM step, head by head */
+    for (int64_t h = 0; h < H; ++h) {
+      const float dt = softplus_f(row[d_inner + conv_dim + h] + dt_bias[h]);
+      const float A = (float)(-exp((double)A_log[h]));
+      const float dA = (float)exp((double)(dt * A));
+      for (int64_t p = 0; p < P; ++p) {
+        const float x = c_out[h * P + p];
+        const float dtx = dt * x;
+        float* hs = ssm_state + ((m * H + h) * P + p) * N;
+        double acc = 0.0;
+        for (int64_t n = 0; n < N; ++n) {
+          const float t1 = hs[n] * dA;
+          const float t2 = dtx * Bv[n];
+          hs[n] = t1 + t2;
+          acc += (double)hs[n] * (double)Cv[n];
+        }
+        y[m * d_inner + h * P + p] = (float)(acc + (double)D[h] * (double)x);
+      }
+    }
+  }
+  free(c_out);
+  return DFSSM_REF_OK;
+}
+
+int dfssm_ref_gate_norm_quant(const float* y, const float* z, int64_t ldz, const float* w,
+                              float eps, int64_t M, int64_t d, float* o, int8_t* q, float* s) {
+  if (M < 0 || d <= 0 || ldz < d || !(eps >= 0.0f)) return DFSSM_REF_ERR_SHAPE;
+  if (M == 0) return DFSSM_REF_OK;
+  if (!y || !z || !w || !q || !s) return DFSSM_REF_ERR_NULL;
+  float* g = (float*)malloc((size_t)d * sizeof(float));
+  float* on = (float*)malloc((size_t)(M * d) * sizeof(float));
+  if (!g || !on) {
+    free(g);
+    free(on);
+    return DFSSM_REF_ERR_NULL;
+  }
+  for (int64_t m = 0; m < M; ++m) {
+    for (int64_t k = 0; k < d; ++k) g[k] = y[m * d + k] * silu_f(z[m * ldz + k]);
+    const float r = rms_scale(g, d, eps);
+    for (int64_t k = 0; k < d; ++k) on[m * d + k] = (g[k] * r) * w[k];
+  }
+  int st = dfssm_ref_quantize_act(on, DFSSM_REF_F32, M, d, d, q, s);
+  if (o && st == DFSSM_REF_OK) memcpy(o, on, (size_t)(M * d) * sizeof(float));
+  free(g);
+  free(on);
+  return st;
+}

@@ -40,7 +40,8 @@
  * Parity status: every function here is pinned by the CPU tests (brute
  * force, closed forms, invariants, hand-derived fixtures).
  *
- * Also here: the tied int8 embedding gather and LM head (below).
+ * Also here: the tied int8 embedding gather and LM head, and the Mamba-2
+ * decode-step operations around the linears (below).
  */
 #ifndef DFSSM_REF_H
 #define DFSSM_REF_H
@@ -118,6 +119,71 @@ int dfssm_ref_embed_gather(const int8_t* E, const float* scale, int64_t V, int64
 int dfssm_ref_lm_head(const int8_t* q, const float* s, int64_t M, int64_t d,
                       const int8_t* E, const float* scale, int64_t V,
                       int32_t* acc, float* logits);
+
+/* ---- the Mamba-2 decode step around the linears ------------------------
+ *
+ * The paper keeps Mamba-2's layer and lists what runs around the two
+ * projections at batch 1 (Sec. 4.1 and Table 13: RMSNorm, the convolution
+ * step as a stateful shift register, the SSM step as a stateful recurrence,
+ * and gate + norm), with three fixes to the step's semantics (Table 12):
+ * the input enters the state as (x * dt) outer B, d_state is 128 for the
+ * 1.3B model, and the gate is applied before the norm, norm(y * silu(z)).
+ * The remaining sizes follow the public Mamba-2 design: d_inner = 2 d_model,
+ * heads of P = 64 channels (H = d_inner / P), one B/C group, d_conv = 4, and
+ * in_proj's output laid out as [z | x | B | C | dt] (d_inner, d_inner, N, N,
+ * H values).
+ *
+ * Precision (one rounding per operation, in the order written):
+ *   fp32   every elementwise step;
+ *   fp64   exp, log1p, sqrt and divisions inside silu, softplus and the
+ *          norm's scale, each rounded once to fp32 where it is used;
+ *   fp64   the two reductions, sum g^2 of the norms and sum_n h C of the
+ *          SSM output, over exact products of fp32 values, rounded once.
+ *   silu(v)     = (float)(v / (1 + exp(-v)))                  in fp64
+ *   softplus(v) = v > 20 ? v : (float)log1p(exp(v))            in fp64
+ */
+
+/* Residual add + RMSNorm + the linear's quantiser (in_proj's input, and the
+ * final norm before the LM head):
+ *   u'  = u + delta           (fp32; u' = u when delta is NULL)
+ *   r   = (float)(1 / sqrt(sum_k (double)u'^2 / d + eps))
+ *   o   = (u' * r) * w        (fp32)
+ *   (Q, s) = quantise(o)      (dfssm_ref_quantize_act's rule)
+ * u_out and o may be NULL; u_out may equal u.  d > 0. */
+int dfssm_ref_add_rmsnorm_quant(const float* u, const float* delta, const float* w, float eps,
+                                int64_t M, int64_t d, float* u_out, float* o, int8_t* q,
+                                float* s);
+
+/* The convolution step and the SSM step of one token per sequence.
+ *   zxbcdt   [M, ld]  in_proj's output: z at 0, xBC at d_inner (conv_dim =
+ *                     d_inner + 2N values), dt at d_inner + conv_dim (H values)
+ *   conv_state [M][conv_dim][4]   shift register, updated: position 3 is the
+ *                     newest input.  Each step shifts it one place towards
+ *                     position 0 and writes the new xBC at position 3; then
+ *                     c_out = silu((((w0 s0 + w1 s1) + w2 s2) + w3 s3) + b)
+ *   conv_w [conv_dim][4], conv_b [conv_dim]
+ *   dt_bias, A_log, D [H]
+ *   ssm_state [M][H][P][N] fp32, updated
+ *   y [M, d_inner] out; xbc [M, conv_dim] out (the conv outputs) or NULL
+ * Per head h (x = c_out[h P + p], B = c_out[d_inner + n], C = c_out[d_inner +
+ * N + n]):
+ *   dt = softplus(dt_raw + dt_bias)     A = (float)(-exp(A_log))
+ *   dA = (float)exp(dt * A)             (dt * A in fp32)
+ *   h[p][n] = h[p][n] * dA + (dt * x) * B[n]
+ *   y[h P + p] = (float)(sum_n (double)h[p][n] C[n] + (double)D x)
+ * d_inner = H * P; P = headdim. */
+int dfssm_ref_ssm_step(const float* zxbcdt, int64_t ld, int64_t M, int64_t d_inner,
+                       int64_t d_state, int64_t headdim, float* conv_state,
+                       const float* conv_w, const float* conv_b, const float* dt_bias,
+                       const float* A_log, const float* D, float* ssm_state, float* y,
+                       float* xbc);
+
+/* Gate then norm, and the linear's quantiser (out_proj's input):
+ *   g = y * silu(z)   (fp32);  r = (float)(1 / sqrt(sum_k (double)g^2 / d + eps))
+ *   o = (g * r) * w   (fp32);  (Q, s) = quantise(o)
+ * y [M, d]; z rows of stride ldz; o may be NULL.  d > 0. */
+int dfssm_ref_gate_norm_quant(const float* y, const float* z, int64_t ldz, const float* w,
+                              float eps, int64_t M, int64_t d, float* o, int8_t* q, float* s);
 
 /* Number of OpenMP threads the row loops use (1 without OpenMP). */
 int dfssm_ref_threads(void);

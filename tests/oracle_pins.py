@@ -367,6 +367,11 @@ def pin_paper_sizes(o: Oracle):
     assert ws["w_bits"].nbytes * 8 == 2048 * 8512
     # the tied int8 embedding / LM head: one byte per entry of the
     # 50,280 x 2048 table is "103 MB", 37% of the 278 MB model
+    # in_proj's width: [z | x | B | C | dt] of a Mamba-2 mixer with
+    # d_inner = 2 d_model, heads of 64 and Table 12's d_state 128
+    ms = facts["model_shape"]
+    dm = S.mamba_dims(ms["d_model"], ms["d_state"], 64)
+    assert dm["ld"] == 2 * dm["d_inner"] + 2 * ms["d_state"] + dm["nheads"] == S.IN_PROJ_1P3B[1]
     emb = 50_280 * facts["model_shape"]["d_model"] * np.dtype(np.int8).itemsize
     assert round(emb / 1e6) == t1["embedding_lm_head_int8_MB"]
     assert round(100 * emb / 1e6 / t1["total_MB"]) == 37
@@ -464,6 +469,216 @@ def pin_embed_gather_bruteforce(o: Oracle):
             raise AssertionError("an out-of-range token id was accepted")
 
 
+# --------------------------------------------------------------------------
+# Mamba-2 decode step around the linears
+# --------------------------------------------------------------------------
+def _silu64(v):
+    """silu through scipy's logistic function (a library routine)."""
+    from scipy.special import expit
+    v = np.asarray(v, np.float64)
+    return v * expit(v)
+
+
+def pin_rmsnorm(o: Oracle):
+    """Hand case, the normalisation property, scale invariance, the weight
+    acting per channel, the role of eps and the residual add."""
+    # u = [3, 4, 0, 0], eps = 0: mean square 25/4, r = 0.4 (rounded to fp32),
+    # o = [1.2, 1.6, 0, 0]; Q = rint(1.2 / 1.6 * 127) = rint(95.25) = 95
+    u = np.array([[3, 4, 0, 0]], F32)
+    _, on, q, s = o.add_rmsnorm_quant(u, np.ones(4, F32), 0.0)
+    assert np.allclose(on[0], [1.2, 1.6, 0, 0], rtol=1e-7, atol=0)
+    assert q[0].tolist() == [95, 127, 0, 0]
+    assert abs(float(s[0]) - 1.6 / 127) <= 1e-7 * 1.6 / 127
+    # eps = 0, unit weight: mean(o^2) = 1 for any row
+    x = S.residual(3, 512, key=(98,))
+    one = np.ones(512, F32)
+    _, on, q, s = o.add_rmsnorm_quant(x, one, 0.0)
+    assert np.allclose((on.astype(np.float64) ** 2).mean(axis=1), 1.0, rtol=0, atol=1e-6)
+    # eps = 0: scaling the row by a power of two changes nothing
+    _, o2, q2, s2 = o.add_rmsnorm_quant(x * F32(8), one, 0.0)
+    assert np.array_equal(o2, on) and np.array_equal(q2, q) and np.array_equal(s2, s)
+    # the weight scales each channel of the unit-weight output
+    w = np.random.default_rng(99).uniform(0.5, 2.0, 512).astype(F32)
+    _, ow, _, _ = o.add_rmsnorm_quant(x, w, 0.0)
+    assert np.array_equal(ow, (on * w).astype(F32))
+    # eps equal to the mean square halves it into 1/sqrt(2 m): a row of 2s
+    # with eps = 4 gives o = 2 / sqrt(8) = 1/sqrt(2)
+    _, on, _, _ = o.add_rmsnorm_quant(np.full((1, 64), 2.0, F32), np.ones(64, F32), 4.0)
+    assert np.allclose(on, 2 ** -0.5, rtol=2e-7, atol=0)
+    # residual: u + (-u) is a zero row (Q = 0, s = 0); u_out is the sum
+    u_out, on, q, s = o.add_rmsnorm_quant(x, one, 1e-5, delta=-x)
+    assert not u_out.any() and not q.any() and not s.any() and not on.any()
+    d = S.residual(3, 512, key=(100,))
+    u_out, _, _, _ = o.add_rmsnorm_quant(x, one, 1e-5, delta=d)
+    assert np.array_equal(u_out, (x + d).astype(F32))
+
+
+# small mixer for the step pins: d_inner 64, N 8, P 16 -> 4 heads, conv_dim 80
+_DI, _N, _P = 64, 8, 16
+
+
+def _small_params(seed, **over):
+    p = S.mamba_params(_DI // 2, d_state=_N, headdim=_P, key=(101, seed))
+    p.update(over)
+    return p
+
+
+def _zero_state(M):
+    H = _DI // _P
+    return np.zeros((M, _DI + 2 * _N, 4), F32), np.zeros((M, H, _P, _N), F32)
+
+
+def _step(o, zx, cs, hs, p):
+    return o.ssm_step(zx, cs, hs, p["conv_w"], p["conv_b"], p["dt_bias"], p["A_log"], p["D"], _DI, _N, _P)
+
+
+def pin_conv_step(o: Oracle):
+    """An impulse through the shift register: at step t after it, channel c
+    shows silu(w[c][3 - t]); it is gone after 4 steps.  A constant input
+    shows silu(sum_j w[c][j] + b[c]) once the register is full."""
+    p = _small_params(0, conv_b=np.zeros(_DI + 2 * _N, F32))
+    ld = S.mamba_dims(_DI // 2, _N, _P)["ld"]
+    cs, hs = _zero_state(1)
+    chans = [5, _DI + 3, _DI + _N + 7]             # an x, a B and a C channel
+    for t in range(6):
+        zx = np.zeros((1, ld), F32)
+        if t == 0:
+            zx[0, _DI + np.array(chans)] = 1.0
+        _, xbc, cs, hs = _step(o, zx, cs, hs, p)
+        want = np.zeros(_DI + 2 * _N)
+        if t < 4:
+            for c in chans:
+                want[c] = _silu64(p["conv_w"][c, 3 - t])
+        assert np.allclose(xbc[0], want, rtol=1e-6, atol=0), t
+    assert not cs.any()
+    # constant input 1 with a bias: silu(sum_j w[c][j] + b[c]) from step 3 on
+    p = _small_params(1)
+    cs, hs = _zero_state(1)
+    zx = np.zeros((1, ld), F32)
+    zx[0, _DI:_DI + _DI + 2 * _N] = 1.0
+    for _ in range(4):
+        _, xbc, cs, hs = _step(o, zx, cs, hs, p)
+    want = _silu64(p["conv_w"].astype(np.float64).sum(axis=1) + p["conv_b"])
+    assert np.allclose(xbc[0], want, rtol=1e-6, atol=1e-7)
+
+
+def _ident_conv(p):
+    """Taps [0, 0, 0, 1] and no bias: the conv output is silu(newest input)."""
+    w = np.zeros((_DI + 2 * _N, 4), F32)
+    w[:, 3] = 1.0
+    p = dict(p)
+    p["conv_w"], p["conv_b"] = w, np.zeros(_DI + 2 * _N, F32)
+    return p
+
+
+def pin_ssm_step(o: Oracle):
+    """Closed forms of the recurrence h = h dA + (x dt) B, y = C.h + D x:
+    a memoryless head (dA = 0), pure decay over 3 steps, the geometric sum
+    from a zero state, the D skip, and head independence."""
+    H = _DI // _P
+    ld = S.mamba_dims(_DI // 2, _N, _P)["ld"]
+    dt_off = _DI + _DI + 2 * _N
+    rng = np.random.default_rng(102)
+    # (a) dt above the softplus threshold is taken as is; A_log = 30 makes
+    # dt * A far below exp's range, so dA = 0 and the state is (x dt) B
+    p = _ident_conv(_small_params(2, dt_bias=np.full(H, 25.0, F32), A_log=np.full(H, 30.0, F32)))
+    zx = rng.standard_normal((2, ld)).astype(F32)
+    cs = S.mamba_state(2, _DI // 2, _N, _P, key=(103,))
+    y, xbc, _, hs = _step(o, zx, cs["conv_state"], cs["ssm_state"], p)
+    dt = (zx[:, dt_off:dt_off + H] + F32(25.0)).astype(np.float64)              # [M, H]
+    x = xbc[:, :_DI].astype(np.float64).reshape(2, H, _P)
+    B = xbc[:, _DI:_DI + _N].astype(np.float64)
+    C = xbc[:, _DI + _N:].astype(np.float64)
+    h_want = dt[:, :, None, None] * x[:, :, :, None] * B[:, None, None, :]
+    assert np.allclose(hs, h_want, rtol=3e-7, atol=0)
+    y_want = (h_want * C[:, None, None, :]).sum(axis=3) + p["D"][None, :, None] * x
+    bound = 1e-6 * (np.abs(h_want * C[:, None, None, :]).sum(axis=3) + np.abs(p["D"][None, :, None] * x))
+    assert np.all(np.abs(y.reshape(2, H, _P) - y_want) <= bound)
+    # (b) x = 0 (silu(0)): pure decay, h_3 = h_0 exp(3 dt A) with
+    # dt = softplus(v) from numpy's logaddexp
+    p = _ident_conv(_small_params(3))
+    h0 = S.mamba_state(1, _DI // 2, _N, _P, key=(104,))["ssm_state"]
+    zx = np.zeros((1, ld), F32)
+    zx[0, _DI + _DI:_DI + _DI + 2 * _N] = rng.standard_normal(2 * _N)            # B and C inputs
+    zx[0, dt_off:] = rng.standard_normal(H)
+    hs = h0
+    cs = np.zeros((1, _DI + 2 * _N, 4), F32)
+    for _ in range(3):
+        y, xbc, cs, hs = _step(o, zx, cs, hs, p)
+    sp = np.logaddexp(0.0, (zx[0, dt_off:] + p["dt_bias"]).astype(np.float64))
+    A = -np.exp(p["A_log"].astype(np.float64))
+    dec = np.exp(3 * sp * A)
+    h_want = h0[0].astype(np.float64) * dec[:, None, None]
+    assert np.allclose(hs[0], h_want, rtol=2e-6, atol=1e-30)
+    C = xbc[0, _DI + _N:].astype(np.float64)
+    assert np.allclose(y[0].reshape(H, _P), (h_want * C).sum(axis=2), rtol=1e-5, atol=1e-6)
+    # (c) from a zero state with a constant input: h_T = dt x B (1 - dA^T) / (1 - dA)
+    p = _ident_conv(_small_params(4))
+    zx = np.zeros((1, ld), F32)
+    zx[0, _DI:] = rng.standard_normal(ld - _DI)
+    cs, hs = _zero_state(1)
+    T = 5
+    for _ in range(T):
+        y, xbc, cs, hs = _step(o, zx, cs, hs, p)
+    dt = np.logaddexp(0.0, (zx[0, dt_off:] + p["dt_bias"]).astype(np.float64))
+    dA = np.exp(dt * -np.exp(p["A_log"].astype(np.float64)))
+    x = xbc[0, :_DI].astype(np.float64).reshape(H, _P)
+    B = xbc[0, _DI:_DI + _N].astype(np.float64)
+    C = xbc[0, _DI + _N:].astype(np.float64)
+    geo = (1 - dA ** T) / (1 - dA)
+    h_want = (dt * geo)[:, None, None] * x[:, :, None] * B[None, None, :]
+    assert np.allclose(hs[0], h_want, rtol=1e-5, atol=1e-12)
+    y_want = (h_want * C).sum(axis=2) + p["D"][:, None] * x
+    assert np.allclose(y[0].reshape(H, _P), y_want, rtol=1e-5, atol=1e-6)
+    # (d) B = 0 and a zero state: y is the D skip alone, D x rounded once
+    zx[0, _DI + _DI:_DI + _DI + _N] = 0.0
+    cs, hs = _zero_state(1)
+    y, xbc, _, hs = _step(o, zx, cs, hs, p)
+    assert not hs.any()
+    x = xbc[0, :_DI].reshape(H, _P)
+    assert np.array_equal(y[0].reshape(H, _P), (p["D"][:, None] * x).astype(F32))
+    # (e) heads are independent: permuting everything per head permutes y
+    p = _small_params(5)
+    st = S.mamba_state(1, _DI // 2, _N, _P, key=(105,))
+    zx = rng.standard_normal((1, ld)).astype(F32)
+    y, _, _, hs = _step(o, zx, st["conv_state"], st["ssm_state"], p)
+    perm = np.array([2, 0, 3, 1])
+    ch = (perm[:, None] * _P + np.arange(_P)[None, :]).ravel()                    # x channels
+    cperm = np.concatenate([ch, np.arange(_DI, _DI + 2 * _N)])
+    p2 = dict(p)
+    p2["conv_w"], p2["conv_b"] = p["conv_w"][cperm], p["conv_b"][cperm]
+    for k in ("dt_bias", "A_log", "D"):
+        p2[k] = p[k][perm]
+    zx2 = zx.copy()
+    zx2[0, _DI:_DI + _DI + 2 * _N] = zx[0, _DI + cperm]
+    zx2[0, dt_off:] = zx[0, dt_off + perm]
+    zx2[0, :_DI] = zx[0, ch]
+    y2, _, _, hs2 = _step(o, zx2, st["conv_state"][:, cperm], st["ssm_state"][:, perm], p2)
+    assert np.array_equal(y2[0], y[0][ch]) and np.array_equal(hs2[0], hs[0][perm])
+
+
+def pin_gate_norm(o: Oracle):
+    """Gate before norm (Table 12): norm(y silu(z)).  A constant row
+    normalises to 1 whatever the gate, so s = 1/127; an identity gate
+    (silu(30) = 30 in fp32) equals the plain norm of 30 y; silu(0) = 0
+    zeroes a channel; the output has unit mean square."""
+    one = np.ones(64, F32)
+    _, q, s = o.gate_norm_quant(np.full((1, 64), 3.0, F32), np.full((1, 64), 0.7, F32), one, 0.0)
+    assert np.all(q == 127) and abs(float(s[0]) * 127 - 1.0) <= 2e-7
+    y = S.residual(2, 256, key=(106,))
+    w = np.random.default_rng(107).uniform(0.8, 1.2, 256).astype(F32)
+    og, qg, sg = o.gate_norm_quant(y, np.full((2, 256), 30.0, F32), w, 1e-5)
+    _, on, qn, sn = o.add_rmsnorm_quant((y * F32(30.0)).astype(F32), w, 1e-5)
+    assert np.array_equal(og, on) and np.array_equal(qg, qn) and np.array_equal(sg, sn)
+    z = np.random.default_rng(108).standard_normal((2, 256)).astype(F32)
+    z[:, ::7] = 0.0
+    og, qg, _ = o.gate_norm_quant(y, z, np.ones(256, F32), 0.0)
+    assert not og[:, ::7].any() and not qg[:, ::7].any()
+    assert np.allclose((og.astype(np.float64) ** 2).mean(axis=1), 1.0, rtol=0, atol=1e-6)
+    _, q0, s0 = o.gate_norm_quant(np.zeros((1, 64), F32), np.ones((1, 64), F32), one, 1e-5)
+    assert not q0.any() and not s0.any()
+
+
 def pin_validation(o: Oracle):
     """Shapes outside the contract are refused with the shape status."""
     q = np.zeros(64, np.int8)
@@ -479,4 +694,5 @@ def pin_validation(o: Oracle):
 ALL_PINS = [pin_f16_decode, pin_quantize_hand_cases, pin_quantize_properties, pin_hand_linear,
             pin_bruteforce, pin_popcount_identity, pin_special_bits, pin_permutation, pin_extremes,
             pin_rank0, pin_y32_order, pin_chain, pin_paper_sizes, pin_embed_lm_hand, pin_lm_head_bruteforce,
-            pin_lm_head_closed_forms, pin_embed_gather_bruteforce, pin_validation]
+            pin_lm_head_closed_forms, pin_embed_gather_bruteforce, pin_rmsnorm, pin_conv_step, pin_ssm_step,
+            pin_gate_norm, pin_validation]

@@ -44,6 +44,26 @@ MUTANTS = [
                                "(int64_t)E[(k % V) * d + (v % d)] * (int64_t)q[m * d + k]")]),
     ("lm_head_acc_int16", [("if (acc) acc[m * V + v] = (int32_t)sum;", "if (acc) acc[m * V + v] = (int16_t)sum;")]),
     ("embed_row_of_m", [("x[m * d + k] = scale[v] * (float)E[v * d + k];", "x[m * d + k] = scale[v] * (float)E[m * d + k];")]),
+    # the Mamba-2 step around the linears (Table 12's three fixes first)
+    ("ssm_missing_dt", [("const float dtx = dt * x;", "const float dtx = x;")]),
+    ("gate_after_norm", [("g[k] = y[m * d + k] * silu_f(z[m * ldz + k]);", "g[k] = y[m * d + k];"),
+                         ("on[m * d + k] = (g[k] * r) * w[k];",
+                          "on[m * d + k] = ((g[k] * r) * w[k]) * silu_f(z[m * ldz + k]);")]),
+    ("ssm_state_head0", [("float* hs = ssm_state + ((m * H + h) * P + p) * N;",
+                          "float* hs = ssm_state + ((m * H + 0) * P + p) * N;")]),
+    ("conv_taps_reversed", [("float v = wc[0] * st[0];", "float v = wc[3] * st[0];"),
+                            ("v = v + wc[3] * st[3];", "v = v + wc[0] * st[3];")]),
+    ("conv_no_shift", [("      st[0] = st[1];\n      st[1] = st[2];\n      st[2] = st[3];\n", "")]),
+    ("conv_no_bias", [("v = v + conv_b[c];", "(void)0;")]),
+    ("A_positive", [("(float)(-exp((double)A_log[h]))", "(float)(exp((double)A_log[h]))")]),
+    ("no_softplus", [("const float dt = softplus_f(row[d_inner + conv_dim + h] + dt_bias[h]);",
+                      "const float dt = row[d_inner + conv_dim + h] + dt_bias[h];")]),
+    ("missing_D", [(" + (double)D[h] * (double)x)", ")")]),
+    ("B_C_swapped", [("const float* Bv = c_out + d_inner;", "const float* Bv = c_out + d_inner + N;"),
+                     ("const float* Cv = c_out + d_inner + N;", "const float* Cv = c_out + d_inner;")]),
+    ("norm_no_eps", [("sqrt(ss / (double)d + (double)eps)", "sqrt(ss / (double)d)")]),
+    ("norm_sum_not_mean", [("sqrt(ss / (double)d + (double)eps)", "sqrt(ss + (double)eps)")]),
+    ("residual_dropped", [("res[k] = delta ? u[m * d + k] + delta[m * d + k] : u[m * d + k];", "res[k] = u[m * d + k];")]),
 ]
 
 
@@ -56,7 +76,7 @@ def test_mutant_is_caught(tmp_path, name, edits):
     c = tmp_path / "dfssm_ref.c"
     c.write_text(src)
     so = str(tmp_path / f"libref_{name}.so")
-    oracle.build(src=str(c), out=so, extra=["-Wno-unused-variable", "-Wno-unused-but-set-variable"])
+    oracle.build(src=str(c), out=so, extra=["-Wno-unused-variable", "-Wno-unused-but-set-variable", "-Wno-unused-function", "-Wno-unused-parameter"])
     o = Oracle(so)
     failed = []
     for pin in ALL_PINS:
