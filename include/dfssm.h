@@ -236,6 +236,80 @@ dfssm_status dfssm_embed_gather(const int8_t* E, const float* scale, int64_t V, 
 dfssm_status dfssm_lm_head(const int8_t* q, const float* s, int64_t M, int64_t d, const int8_t* E,
                            const float* scale, int64_t V, float* logits, int32_t* acc, void* stream);
 
+/* The Mamba-2 decode step around the two linears (Sec. 4.1: the convolution
+ * step is a stateful shift register and the SSM step a stateful recurrence;
+ * Table 13 lists them with RMSNorm and gate + norm; Table 12 fixes the
+ * step's semantics: the input enters the state as (x * dt) outer B, d_state
+ * is 128 for the 1.3B model, and the gate comes before the norm).  The
+ * other sizes follow the public Mamba-2 design: d_inner = 2 d_model, heads
+ * of 64 channels, one B/C group, a width-4 convolution, and in_proj's output
+ * row laid out as [z | x | B | C | dt] (d_inner, d_inner, N, N, nheads).
+ *
+ * Rounding, the same on every run: fp32 for every elementwise step; exp,
+ * log1p, sqrt and the divisions inside silu(v) = v / (1 + exp(-v)),
+ * softplus(v) = v > 20 ? v : log1p(exp(v)) and the norm's scale in fp64,
+ * rounded once to fp32; the norm's sum of squares and the SSM output's sum
+ * over the state accumulated in fp64.  Results may differ from another
+ * summation order only when an fp64 sum falls within its last bits of an
+ * fp32 rounding boundary. */
+
+/* Residual add, RMSNorm and the linear's per-token quantisation: the input
+ * of in_proj, and the final norm before the LM head.
+ *   u'  = u + delta  (fp32; u' = u when delta is NULL)
+ *   r   = (float)(1 / sqrt(sum_k u'^2 / d + eps))
+ *   o   = (u' * r) * w
+ *   (q, s) = dfssm_quantize_act's rule applied to o
+ *   u, delta, u_out [M, d] fp32; w [d] fp32; q [M, d] int8; s [M] fp32
+ * u_out (may be NULL) receives u'; u_out == u (in place) is allowed.
+ * Limits: 0 < d <= 16384, d % 4 == 0; eps finite, >= 0; M >= 0.
+ * Errors: NULL, SHAPE, ALIGN, DEVICE. */
+dfssm_status dfssm_add_rmsnorm_quant(const float* u, const float* delta, const float* w, float eps,
+                                     int64_t M, int64_t d, float* u_out, int8_t* q, float* s,
+                                     void* stream);
+
+/* Gate then norm, and quantisation: the input of out_proj.
+ *   g = y * silu(z);  r = (float)(1 / sqrt(sum_k g^2 / d + eps));
+ *   o = (g * r) * w;  (q, s) = quantise(o)
+ *   y [M, d] fp32 (the SSM output); z rows of stride ldz fp32 (in_proj's
+ *   output row holds z at its start: pass it with ldz = its row length);
+ *   w [d]; q [M, d] int8; s [M].
+ * Limits: 0 < d <= 16384, d % 4 == 0; ldz >= d, ldz % 4 == 0; eps finite,
+ * >= 0.  Errors: NULL, SHAPE, ALIGN, DEVICE. */
+dfssm_status dfssm_gate_norm_quant(const float* y, const float* z, int64_t ldz, const float* w, float eps,
+                                   int64_t M, int64_t d, int8_t* q, float* s, void* stream);
+
+/* The convolution step and the SSM step for one token of each of M
+ * sequences, updating their state in place.
+ *   zxbcdt  [M, ld] fp32 in_proj's output rows; xBC (conv_dim = d_inner +
+ *           2 d_state values) at column d_inner, dt (nheads) at column
+ *           d_inner + conv_dim
+ *   conv_ring [M][4][conv_dim] fp32 convolution state as a ring: before the
+ *           call with step t, slot (t - k) & 3 holds the xBC input of step
+ *           t - k (k = 1..3; zeros for steps before the first).  The call
+ *           reads those three slots and writes this step's input into slot
+ *           t & 3.  In the model's shift-register form [conv_dim][4] the
+ *           register's position j is ring slot (t - 4 + j) & 3 before step t.
+ *           Advance t by one per call; a new sequence starts from zeros.
+ *   conv_w [conv_dim][4] fp32 (tap 3 meets the newest input), conv_b
+ *           [conv_dim]; dt_bias, A_log, D [nheads] fp32
+ *   ssm_state [M][nheads][headdim][d_state] fp32, updated
+ *   y       [M, d_inner] fp32 out; xbc [M, conv_dim] fp32 out or NULL (the
+ *           convolution outputs)
+ * Per channel c:  v = (((w0 s_{t-3} + w1 s_{t-2}) + w2 s_{t-1}) + w3 s_t)
+ *                 + b;  xbc = silu(v)
+ * Per head h (x = xbc[h*64 + p], B = xbc[d_inner + n], C = xbc[d_inner +
+ * d_state + n]):  dt = softplus(dt_raw + dt_bias); A = -exp(A_log);
+ *   dA = exp(dt * A);  h[p][n] = h[p][n] * dA + (dt * x) * B[n];
+ *   y[h*64 + p] = sum_n h[p][n] C[n] + D x
+ * Limits: headdim == 64 and d_state in {64, 128} (else UNSUPPORTED);
+ * d_inner a positive multiple of 64, <= 65536; ld >= 2 d_inner + 2 d_state
+ * + nheads; step >= 0.  Outputs must not alias the inputs.
+ * Errors: NULL, SHAPE, ALIGN, UNSUPPORTED, DEVICE. */
+dfssm_status dfssm_ssm_step(const float* zxbcdt, int64_t ld, int64_t M, int64_t d_inner, int64_t d_state,
+                            int64_t headdim, int64_t step, float* conv_ring, const float* conv_w,
+                            const float* conv_b, const float* dt_bias, const float* A_log,
+                            const float* D, float* ssm_state, float* y, float* xbc, void* stream);
+
 /* Static text for a status code. */
 const char* dfssm_status_string(int status);
 /* Thread-local description of the last failure on this thread ("" if none). */

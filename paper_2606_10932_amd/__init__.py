@@ -22,8 +22,8 @@ PATH_AUTO, PATH_DECODE, PATH_MFMA, PATH_MFMA_FEW = 0, 1, 2, 3
 EXPORTS = ["dfssm_quantize_act", "dfssm_linear_workspace_bytes", "dfssm_scaffold_lora_linear",
            "dfssm_scaffold_lora_linear_ex", "dfssm_chain_workspace_bytes",
            "dfssm_scaffold_lora_chain", "dfssm_chain_prepare", "dfssm_chain_run", "dfssm_chain_status",
-           "dfssm_embed_gather", "dfssm_lm_head", "dfssm_status_string", "dfssm_last_error",
-           "dfssm_version"]
+           "dfssm_embed_gather", "dfssm_lm_head", "dfssm_add_rmsnorm_quant", "dfssm_gate_norm_quant",
+           "dfssm_ssm_step", "dfssm_status_string", "dfssm_last_error", "dfssm_version"]
 
 
 class DfssmError(RuntimeError):
@@ -67,6 +67,13 @@ def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dfssm_embed_gather.restype = i32
     lib.dfssm_lm_head.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp, vp]
     lib.dfssm_lm_head.restype = i32
+    f32 = ctypes.c_float
+    lib.dfssm_add_rmsnorm_quant.argtypes = [vp, vp, vp, f32, i64, i64, vp, vp, vp, vp]
+    lib.dfssm_add_rmsnorm_quant.restype = i32
+    lib.dfssm_gate_norm_quant.argtypes = [vp, vp, i64, vp, f32, i64, i64, vp, vp, vp]
+    lib.dfssm_gate_norm_quant.restype = i32
+    lib.dfssm_ssm_step.argtypes = [vp, i64, i64, i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.dfssm_ssm_step.restype = i32
     lib.dfssm_status_string.argtypes = [i32]
     lib.dfssm_status_string.restype = ctypes.c_char_p
     lib.dfssm_last_error.restype = ctypes.c_char_p
@@ -278,3 +285,62 @@ def lm_head(q, s, E, scale, logits=None, acc: bool = False, stream=None):
     _check(lib.dfssm_lm_head(q.data_ptr(), s.data_ptr(), M, d, E.data_ptr(), scale.data_ptr(), V,
                              logits.data_ptr(), _ptr(a), _stream(stream)))
     return (logits, a) if acc else logits
+
+
+def add_rmsnorm_quant(u, w, eps: float = 1e-5, delta=None, u_out=None, q=None, s=None, stream=None):
+    """(q int8 [M,d], s fp32 [M]) of rmsnorm(u + delta) * w; u_out (optional,
+    may be u) receives u + delta."""
+    torch = _torch()
+    _need(u, torch.float32, "u", 2)
+    _need(w, torch.float32, "w", 1)
+    _need(delta, torch.float32, "delta", 2)
+    _need(u_out, torch.float32, "u_out", 2)
+    M, d = u.shape
+    q = torch.empty((M, d), dtype=torch.int8, device=u.device) if q is None else q
+    s = torch.empty((M,), dtype=torch.float32, device=u.device) if s is None else s
+    _need(q, torch.int8, "q", 2)
+    _need(s, torch.float32, "s", 1)
+    _check(lib.dfssm_add_rmsnorm_quant(u.data_ptr(), _ptr(delta), w.data_ptr(), float(eps), M, d, _ptr(u_out),
+                                       q.data_ptr(), s.data_ptr(), _stream(stream)))
+    return q, s
+
+
+def gate_norm_quant(y, z, w, eps: float = 1e-5, q=None, s=None, stream=None):
+    """(q, s) of rmsnorm(y * silu(z)) * w; z may be a column slice of a wider
+    row-major tensor (unit column stride)."""
+    torch = _torch()
+    _need(y, torch.float32, "y", 2)
+    _need(w, torch.float32, "w", 1)
+    if z.dim() != 2 or z.stride(1) != 1 or z.dtype != torch.float32 or not z.is_cuda:
+        raise ValueError("z must be a 2-D fp32 device tensor with unit column stride")
+    M, d = y.shape
+    if tuple(z.shape) != (M, d):
+        raise ValueError("z must have y's shape")
+    ldz = z.stride(0) if M > 1 else max(z.stride(0), d)   # a single row's stride may be reported as anything
+    q = torch.empty((M, d), dtype=torch.int8, device=y.device) if q is None else q
+    s = torch.empty((M,), dtype=torch.float32, device=y.device) if s is None else s
+    _check(lib.dfssm_gate_norm_quant(y.data_ptr(), z.data_ptr(), ldz, w.data_ptr(), float(eps), M, d, q.data_ptr(),
+                                     s.data_ptr(), _stream(stream)))
+    return q, s
+
+
+def ssm_step(zxbcdt, step: int, conv_ring, ssm_state, conv_w, conv_b, dt_bias, A_log, D, d_state: int = 128,
+             headdim: int = 64, y=None, xbc=None, stream=None):
+    """Convolution + SSM step of one token per sequence; conv_ring
+    [M, 4, conv_dim] and ssm_state [M, H, P, N] are updated in place.
+    Returns y [M, d_inner]."""
+    torch = _torch()
+    _need(zxbcdt, torch.float32, "zxbcdt", 2)
+    M, ld = zxbcdt.shape
+    H = dt_bias.shape[0]
+    d_inner = H * headdim
+    for t, n in ((conv_ring, "conv_ring"), (ssm_state, "ssm_state"), (conv_w, "conv_w"), (conv_b, "conv_b"),
+                 (dt_bias, "dt_bias"), (A_log, "A_log"), (D, "D")):
+        _need(t, torch.float32, n)
+    y = torch.empty((M, d_inner), dtype=torch.float32, device=zxbcdt.device) if y is None else y
+    _need(y, torch.float32, "y", 2)
+    _need(xbc, torch.float32, "xbc", 2)
+    _check(lib.dfssm_ssm_step(zxbcdt.data_ptr(), ld, M, d_inner, d_state, headdim, int(step), conv_ring.data_ptr(),
+                              conv_w.data_ptr(), conv_b.data_ptr(), dt_bias.data_ptr(), A_log.data_ptr(),
+                              D.data_ptr(), ssm_state.data_ptr(), y.data_ptr(), _ptr(xbc), _stream(stream)))
+    return y

@@ -2,6 +2,7 @@
 // workspace sizing, kernel-family dispatch, the chain driver and error
 // reporting.  Validation is pure host code that runs before any HIP call,
 // so a rejected call enqueues nothing.
+#include <float.h>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -11,6 +12,7 @@
 #include <vector>
 
 #include "dfssm_internal.hpp"
+#include "dfssm_mamba.hpp"
 
 namespace {
 
@@ -442,6 +444,64 @@ dfssm_status dfssm_lm_head(const int8_t* q, const float* s, int64_t M, int64_t d
   if (!logits && !acc) return fail(DFSSM_ERR_NULL, "logits and acc are both NULL");
   hipError_t e = dfssm::launch_lm_head(q, s, M, d, E, scale, V, logits, acc, (hipStream_t)stream);
   return e == hipSuccess ? DFSSM_OK : device_fail(e, "lm head launch");
+}
+
+dfssm_status dfssm_add_rmsnorm_quant(const float* u, const float* delta, const float* w, float eps, int64_t M,
+                                     int64_t d, float* u_out, int8_t* q, float* s, void* stream) {
+  clear_error();
+  if (d <= 0 || d % 4 != 0 || d > dfssm::kNormMaxD)
+    return fail(DFSSM_ERR_SHAPE, "d=%lld must be a positive multiple of 4 and <= %lld", (long long)d,
+                (long long)dfssm::kNormMaxD);
+  if (M < 0 || M > INT32_MAX / 2) return fail(DFSSM_ERR_SHAPE, "M=%lld", (long long)M);
+  if (!(eps >= 0.0f) || eps > FLT_MAX) return fail(DFSSM_ERR_SHAPE, "eps must be finite and >= 0");
+  if (M == 0) return DFSSM_OK;
+  dfssm_status st = check_ptrs({{u, "u"}, {w, "w"}, {q, "q"}, {s, "s"}}, {{delta, "delta"}, {u_out, "u_out"}});
+  if (st != DFSSM_OK) return st;
+  hipError_t e = dfssm::launch_add_rmsnorm_quant(u, delta, w, eps, M, d, u_out, q, s, (hipStream_t)stream);
+  return e == hipSuccess ? DFSSM_OK : device_fail(e, "rmsnorm launch");
+}
+
+dfssm_status dfssm_gate_norm_quant(const float* y, const float* z, int64_t ldz, const float* w, float eps,
+                                   int64_t M, int64_t d, int8_t* q, float* s, void* stream) {
+  clear_error();
+  if (d <= 0 || d % 4 != 0 || d > dfssm::kNormMaxD)
+    return fail(DFSSM_ERR_SHAPE, "d=%lld must be a positive multiple of 4 and <= %lld", (long long)d,
+                (long long)dfssm::kNormMaxD);
+  if (ldz < d || ldz % 4 != 0) return fail(DFSSM_ERR_SHAPE, "ldz=%lld must be >= d and a multiple of 4", (long long)ldz);
+  if (M < 0 || M > INT32_MAX / 2) return fail(DFSSM_ERR_SHAPE, "M=%lld", (long long)M);
+  if (!(eps >= 0.0f) || eps > FLT_MAX) return fail(DFSSM_ERR_SHAPE, "eps must be finite and >= 0");
+  if (M == 0) return DFSSM_OK;
+  dfssm_status st = check_ptrs({{y, "y"}, {z, "z"}, {w, "w"}, {q, "q"}, {s, "s"}}, {});
+  if (st != DFSSM_OK) return st;
+  hipError_t e = dfssm::launch_gate_norm_quant(y, z, ldz, w, eps, M, d, q, s, (hipStream_t)stream);
+  return e == hipSuccess ? DFSSM_OK : device_fail(e, "gate norm launch");
+}
+
+dfssm_status dfssm_ssm_step(const float* zxbcdt, int64_t ld, int64_t M, int64_t d_inner, int64_t d_state,
+                            int64_t headdim, int64_t step, float* conv_ring, const float* conv_w,
+                            const float* conv_b, const float* dt_bias, const float* A_log, const float* D,
+                            float* ssm_state, float* y, float* xbc, void* stream) {
+  clear_error();
+  if (headdim != 64) return fail(DFSSM_ERR_UNSUPPORTED, "headdim=%lld: heads of 64 channels only", (long long)headdim);
+  if (d_state != 64 && d_state != 128)
+    return fail(DFSSM_ERR_UNSUPPORTED, "d_state=%lld: 64 or 128 only", (long long)d_state);
+  if (d_inner <= 0 || d_inner % headdim != 0 || d_inner > 65536)
+    return fail(DFSSM_ERR_SHAPE, "d_inner=%lld must be a positive multiple of headdim and <= 65536",
+                (long long)d_inner);
+  const int64_t H = d_inner / headdim, conv_dim = d_inner + 2 * d_state;
+  if (ld < d_inner + conv_dim + H)
+    return fail(DFSSM_ERR_SHAPE, "ld=%lld < 2 d_inner + 2 d_state + nheads = %lld", (long long)ld,
+                (long long)(d_inner + conv_dim + H));
+  if (M < 0 || M * H * 4 > INT32_MAX) return fail(DFSSM_ERR_SHAPE, "M=%lld", (long long)M);
+  if (step < 0) return fail(DFSSM_ERR_SHAPE, "step=%lld must be >= 0", (long long)step);
+  if (M == 0) return DFSSM_OK;
+  dfssm_status st = check_ptrs({{zxbcdt, "zxbcdt"}, {conv_ring, "conv_ring"}, {conv_w, "conv_w"}, {conv_b, "conv_b"},
+                                {dt_bias, "dt_bias"}, {A_log, "A_log"}, {D, "D"}, {ssm_state, "ssm_state"}, {y, "y"}},
+                               {{xbc, "xbc"}});
+  if (st != DFSSM_OK) return st;
+  hipError_t e = dfssm::launch_ssm_step(zxbcdt, ld, M, d_inner, d_state, step, conv_ring, conv_w, conv_b, dt_bias,
+                                        A_log, D, ssm_state, y, xbc, (hipStream_t)stream);
+  return e == hipSuccess ? DFSSM_OK : device_fail(e, "ssm step launch");
 }
 
 }  // extern "C"

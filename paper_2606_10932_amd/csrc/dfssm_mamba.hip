@@ -1,0 +1,305 @@
+// dfssm_mamba.hip -- the Mamba-2 decode step around the scaffold + LoRA
+// linears, gfx950: residual add + RMSNorm + int8 quantisation (in_proj's
+// input), the convolution step and the SSM step (the two stateful
+// operations, Sec. 4.1 and Table 13), and gate-then-norm + quantisation
+// (out_proj's input, norm(y * silu(z)) as Table 12 fixes it).
+//
+// Rounding follows one pinned order so that the int8 codes fed to the
+// linears come out the same on every run and on the host: fp32 for every
+// elementwise step; exp, log1p, sqrt and the divisions inside silu,
+// softplus and the norm's scale in fp64, rounded once to fp32; the norm's
+// sum of squares and the SSM output's sum over the state in fp64 over exact
+// products.  The library is compiled with contraction off.
+//
+// The convolution state is a ring of 4 slots per sequence, [M][4][conv_dim]:
+// step t reads the inputs of steps t-3, t-2, t-1 from slots (t-3)&3 ..
+// (t-1)&3 and writes its own input into slot t&3, the one no reader of step
+// t touches.  That is the shift register of the model without moving data,
+// and it lets every workgroup read the shared B/C channels while one of them
+// appends to them, with no ordering between workgroups.
+#include <float.h>
+
+#include "dfssm_mamba.hpp"
+
+namespace {
+
+// ---------------------------------------------------------------- helpers
+__device__ __forceinline__ float silu_f(float v) {
+  const double x = (double)v;
+  return (float)(x / (1.0 + exp(-x)));
+}
+
+__device__ __forceinline__ float softplus_f(float v) {
+  if (v > 20.0f) return v;
+  return (float)log1p(exp((double)v));
+}
+
+__device__ __forceinline__ int8_t code(float v, float inv) {
+  float r = rintf(v * inv);  // v_rndne_f32: round to nearest, ties to even
+  r = fminf(fmaxf(r, -127.0f), 127.0f);
+  return (int8_t)(int)r;
+}
+
+template <int W>
+__device__ __forceinline__ double sum_lanes(double v) {
+#pragma unroll
+  for (int off = W / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, W);
+  return v;
+}
+
+__device__ __forceinline__ float max_lanes(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+  return v;
+}
+
+// ---------------------------------------------------------------- norms
+constexpr int kNormThreads = 256;
+
+struct NormArgs {
+  const float* a;     // u (residual) or y (SSM output), rows of d
+  const float* b;     // delta (rows of d, may be null) or z (rows of ldb)
+  int64_t ldb;
+  const float* w;     // [d]
+  float eps;
+  int d;
+  float* u_out;       // residual sum, or null (plain norm only)
+  int8_t* q;          // [M][d]
+  float* s;           // [M]
+};
+
+// One workgroup per token row; VPT float4 per thread held in registers
+// (d <= 1024 * VPT).  GATE: g = y * silu(z); else g = u + delta.
+template <bool GATE, int VPT>
+__global__ __launch_bounds__(kNormThreads) void norm_quant(NormArgs a) {
+  const int64_t m = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int d = a.d;
+  const float* ar = a.a + m * d;
+  const float* br = a.b ? a.b + m * a.ldb : nullptr;
+  __shared__ double red_ss[kNormThreads / 64];
+  __shared__ float red_max[kNormThreads / 64];
+
+  float4 g[VPT];
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) {
+    const int k = 4 * (tid + kNormThreads * i);
+    if (k < d) {
+      float4 x = *reinterpret_cast<const float4*>(ar + k);
+      if (GATE) {
+        const float4 z = *reinterpret_cast<const float4*>(br + k);
+        x.x = x.x * silu_f(z.x);
+        x.y = x.y * silu_f(z.y);
+        x.z = x.z * silu_f(z.z);
+        x.w = x.w * silu_f(z.w);
+      } else if (br) {
+        const float4 dl = *reinterpret_cast<const float4*>(br + k);
+        x.x = x.x + dl.x;
+        x.y = x.y + dl.y;
+        x.z = x.z + dl.z;
+        x.w = x.w + dl.w;
+      }
+      g[i] = x;
+      if (!GATE && a.u_out) *reinterpret_cast<float4*>(a.u_out + m * d + k) = x;
+    } else {
+      g[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  }
+  // sum of squares in fp64 (each fp32 square is exact there)
+  double ss = 0.0;
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) {
+    ss += (double)g[i].x * (double)g[i].x;
+    ss += (double)g[i].y * (double)g[i].y;
+    ss += (double)g[i].z * (double)g[i].z;
+    ss += (double)g[i].w * (double)g[i].w;
+  }
+  ss = sum_lanes<64>(ss);
+  if ((tid & 63) == 0) red_ss[tid >> 6] = ss;
+  __syncthreads();
+  ss = (red_ss[0] + red_ss[1]) + (red_ss[2] + red_ss[3]);
+  const float r = (float)(1.0 / sqrt(ss / (double)d + (double)a.eps));
+
+  float amax = 0.0f;
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) {
+    const int k = 4 * (tid + kNormThreads * i);
+    if (k < d) {
+      const float4 w = *reinterpret_cast<const float4*>(a.w + k);
+      g[i].x = (g[i].x * r) * w.x;
+      g[i].y = (g[i].y * r) * w.y;
+      g[i].z = (g[i].z * r) * w.z;
+      g[i].w = (g[i].w * r) * w.w;
+      amax = fmaxf(amax, fmaxf(fmaxf(fabsf(g[i].x), fabsf(g[i].y)), fmaxf(fabsf(g[i].z), fabsf(g[i].w))));
+    }
+  }
+  amax = max_lanes(amax);
+  if ((tid & 63) == 0) red_max[tid >> 6] = amax;
+  __syncthreads();
+  amax = fmaxf(fmaxf(red_max[0], red_max[1]), fmaxf(red_max[2], red_max[3]));
+
+  int8_t* qr = a.q + m * d;
+  if (amax < FLT_MIN) {  // all-zero (or subnormal-only) row
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int k = 4 * (tid + kNormThreads * i);
+      if (k < d) *reinterpret_cast<uint32_t*>(qr + k) = 0u;
+    }
+    if (tid == 0) a.s[m] = 0.0f;
+    return;
+  }
+  const float inv = 127.0f / amax;
+  if (tid == 0) a.s[m] = amax / 127.0f;
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) {
+    const int k = 4 * (tid + kNormThreads * i);
+    if (k < d) {
+      const uint32_t c = (uint32_t)(uint8_t)code(g[i].x, inv) | (uint32_t)(uint8_t)code(g[i].y, inv) << 8 |
+                         (uint32_t)(uint8_t)code(g[i].z, inv) << 16 | (uint32_t)(uint8_t)code(g[i].w, inv) << 24;
+      *reinterpret_cast<uint32_t*>(qr + k) = c;
+    }
+  }
+}
+
+template <bool GATE>
+hipError_t launch_norm(const NormArgs& a, int64_t M, hipStream_t st) {
+  const int vpt = (int)dfssm::ceil_div(a.d, 4 * kNormThreads);
+  dim3 grid((unsigned)M), block(kNormThreads);
+  if (vpt <= 1)
+    norm_quant<GATE, 1><<<grid, block, 0, st>>>(a);
+  else if (vpt <= 2)
+    norm_quant<GATE, 2><<<grid, block, 0, st>>>(a);
+  else if (vpt <= 4)
+    norm_quant<GATE, 4><<<grid, block, 0, st>>>(a);
+  else if (vpt <= 8)
+    norm_quant<GATE, 8><<<grid, block, 0, st>>>(a);
+  else
+    norm_quant<GATE, 16><<<grid, block, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- SSM step
+constexpr int kHeadDim = 64;      // P
+constexpr int kPBlock = 16;       // channels of a head per workgroup
+constexpr int kSsmThreads = 256;  // 16 channels x 16 lanes over the state
+
+struct SsmArgs {
+  const float* zx;    // [M][ld]: z | xBC | dt
+  int64_t ld;
+  int d_inner, H;
+  int64_t step;
+  float* ring;        // [M][4][conv_dim]
+  const float* conv_w;  // [conv_dim][4]
+  const float* conv_b;
+  const float* dt_bias;
+  const float* A_log;
+  const float* D;
+  float* state;       // [M][H][P][N]
+  float* y;           // [M][d_inner]
+  float* xbc;         // [M][conv_dim] or null
+};
+
+// Workgroup (m, h, pb): channels p = 16 pb .. 16 pb + 15 of head h.  Thread
+// t holds channel p = 16 pb + t/16 and state columns n = (t%16) N/16 ..
+// +N/16 - 1; its row of 16 lanes sums y[p] over the state.
+template <int N>
+__global__ __launch_bounds__(kSsmThreads) void ssm_step(SsmArgs a) {
+  constexpr int NPL = N / 16;  // state columns per lane
+  const int nblk = a.H * (kHeadDim / kPBlock);
+  const int64_t m = blockIdx.x / nblk;
+  const int hb = blockIdx.x % nblk;
+  const int h = hb / (kHeadDim / kPBlock);
+  const int p0 = (hb % (kHeadDim / kPBlock)) * kPBlock;
+  const int tid = threadIdx.x;
+  const int pl = tid >> 4, nc = tid & 15;
+  const int conv_dim = a.d_inner + 2 * N;
+  const float* zr = a.zx + m * a.ld;
+
+  // the state first: it is the bytes that come from HBM
+  float* hs = a.state + (((m * a.H + h) * kHeadDim + p0 + pl) * (int64_t)N + nc * NPL);
+  float4 hv[NPL / 4];
+#pragma unroll
+  for (int j = 0; j < NPL / 4; ++j) hv[j] = reinterpret_cast<const float4*>(hs)[j];
+
+  // convolution step for this workgroup's 16 x channels and all B, C channels
+  __shared__ float xbc_s[kPBlock + 2 * N];
+  const bool owns_bc = (hb == 0);
+  float* ring = a.ring + m * 4 * (int64_t)conv_dim;
+  const int s0 = (int)((a.step + 1) & 3), s1 = (int)((a.step + 2) & 3), s2 = (int)((a.step + 3) & 3);
+  const int sw = (int)(a.step & 3);
+  for (int i = tid; i < kPBlock + 2 * N; i += kSsmThreads) {
+    const int c = i < kPBlock ? h * kHeadDim + p0 + i : a.d_inner + (i - kPBlock);
+    const float in = zr[a.d_inner + c];
+    const float4 w = *reinterpret_cast<const float4*>(a.conv_w + 4 * (int64_t)c);
+    float v = w.x * ring[s0 * (int64_t)conv_dim + c];
+    v = v + w.y * ring[s1 * (int64_t)conv_dim + c];
+    v = v + w.z * ring[s2 * (int64_t)conv_dim + c];
+    v = v + w.w * in;
+    v = v + a.conv_b[c];
+    const float o = silu_f(v);
+    xbc_s[i] = o;
+    if (i < kPBlock || owns_bc) {
+      ring[sw * (int64_t)conv_dim + c] = in;
+      if (a.xbc) a.xbc[m * conv_dim + c] = o;
+    }
+  }
+  const float dt = softplus_f(zr[a.d_inner + conv_dim + h] + a.dt_bias[h]);
+  const float A = (float)(-exp((double)a.A_log[h]));
+  const float dA = (float)exp((double)(dt * A));
+  __syncthreads();
+
+  const float x = xbc_s[pl];
+  const float dtx = dt * x;
+  const float* Bs = xbc_s + kPBlock + nc * NPL;
+  const float* Cs = xbc_s + kPBlock + N + nc * NPL;
+  double acc = 0.0;
+#pragma unroll
+  for (int j = 0; j < NPL / 4; ++j) {
+    float e[4] = {hv[j].x, hv[j].y, hv[j].z, hv[j].w};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float t1 = e[u] * dA;
+      const float t2 = dtx * Bs[4 * j + u];
+      e[u] = t1 + t2;
+      acc += (double)e[u] * (double)Cs[4 * j + u];
+    }
+    reinterpret_cast<float4*>(hs)[j] = make_float4(e[0], e[1], e[2], e[3]);
+  }
+  acc = sum_lanes<16>(acc);
+  if (nc == 0) a.y[m * a.d_inner + h * kHeadDim + p0 + pl] = (float)(acc + (double)a.D[h] * (double)x);
+}
+
+}  // namespace
+
+namespace dfssm {
+
+hipError_t launch_add_rmsnorm_quant(const float* u, const float* delta, const float* w, float eps, int64_t M,
+                                    int64_t d, float* u_out, int8_t* q, float* s, hipStream_t st) {
+  if (M == 0) return hipSuccess;
+  NormArgs a{u, delta, d, w, eps, (int)d, u_out, q, s};
+  return launch_norm<false>(a, M, st);
+}
+
+hipError_t launch_gate_norm_quant(const float* y, const float* z, int64_t ldz, const float* w, float eps,
+                                  int64_t M, int64_t d, int8_t* q, float* s, hipStream_t st) {
+  if (M == 0) return hipSuccess;
+  NormArgs a{y, z, ldz, w, eps, (int)d, nullptr, q, s};
+  return launch_norm<true>(a, M, st);
+}
+
+hipError_t launch_ssm_step(const float* zx, int64_t ld, int64_t M, int64_t d_inner, int64_t d_state, int64_t step,
+                           float* ring, const float* conv_w, const float* conv_b, const float* dt_bias,
+                           const float* A_log, const float* D, float* state, float* y, float* xbc,
+                           hipStream_t st) {
+  if (M == 0) return hipSuccess;
+  const int H = (int)(d_inner / kHeadDim);
+  SsmArgs a{zx, ld, (int)d_inner, H, step, ring, conv_w, conv_b, dt_bias, A_log, D, state, y, xbc};
+  dim3 grid((unsigned)(M * H * (kHeadDim / kPBlock))), block(kSsmThreads);
+  if (d_state == 128)
+    ssm_step<128><<<grid, block, 0, st>>>(a);
+  else
+    ssm_step<64><<<grid, block, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace dfssm

@@ -133,6 +133,34 @@ def test_embedding_validation(dl):
     assert h(None, None, 1, 64, None, None, 0, None, None, None) == dl.OK   # V = 0
 
 
+def test_mamba_step_validation(dl):
+    n = dl.lib.dfssm_add_rmsnorm_quant   # u, delta, w, eps, M, d, u_out, q, s, stream
+    assert n(16, None, 16, 1e-5, 1, 30, None, 16, 16, None) == dl.ERR_SHAPE      # d % 4
+    assert n(16, None, 16, 1e-5, 1, 16384 + 4, None, 16, 16, None) == dl.ERR_SHAPE
+    assert n(16, None, 16, -1.0, 1, 64, None, 16, 16, None) == dl.ERR_SHAPE      # eps < 0
+    assert n(16, None, 16, float("nan"), 1, 64, None, 16, 16, None) == dl.ERR_SHAPE
+    assert n(None, None, 16, 1e-5, 1, 64, None, 16, 16, None) == dl.ERR_NULL
+    assert n(16, 20, 16, 1e-5, 1, 64, None, 16, 16, None) == dl.ERR_ALIGN        # delta
+    assert n(None, None, None, 1e-5, 0, 64, None, None, None, None) == dl.OK     # M = 0
+    g = dl.lib.dfssm_gate_norm_quant     # y, z, ldz, w, eps, M, d, q, s, stream
+    assert g(16, 16, 32, 16, 1e-5, 1, 64, 16, 16, None) == dl.ERR_SHAPE           # ldz < d
+    assert g(16, 16, 66, 16, 1e-5, 1, 64, 16, 16, None) == dl.ERR_SHAPE           # ldz % 4
+    assert g(16, None, 64, 16, 1e-5, 1, 64, 16, 16, None) == dl.ERR_NULL
+    f = dl.lib.dfssm_ssm_step
+
+    def ssm(ld=8512, M=1, di=4096, N=128, P=64, step=0, zx=16, xbc=None):
+        return f(zx, ld, M, di, N, P, step, 16, 16, 16, 16, 16, 16, 16, 16, xbc, None)
+    assert ssm(P=32) == dl.ERR_UNSUPPORTED
+    assert ssm(N=96) == dl.ERR_UNSUPPORTED
+    assert ssm(di=4000) == dl.ERR_SHAPE
+    assert ssm(ld=8511) == dl.ERR_SHAPE
+    assert ssm(step=-1) == dl.ERR_SHAPE
+    assert ssm(M=-1) == dl.ERR_SHAPE
+    assert ssm(zx=None) == dl.ERR_NULL
+    assert ssm(xbc=24) == dl.ERR_ALIGN
+    assert ssm(M=0, zx=None) == dl.OK
+
+
 def test_workspace_sizes(dl):
     a = dl.linear_workspace_bytes(1, 2048, 8512, 64)
     b = dl.linear_workspace_bytes(2048, 2048, 8512, 64)
