@@ -310,6 +310,70 @@ dfssm_status dfssm_ssm_step(const float* zxbcdt, int64_t ld, int64_t M, int64_t 
                             const float* conv_b, const float* dt_bias, const float* A_log,
                             const float* D, float* ssm_state, float* y, float* xbc, void* stream);
 
+/* ---- the whole decode step of the model ------------------------------- */
+
+/* One Mamba-2 layer of the distilled model (host struct of device pointers).
+ * conv_dim = d_inner + 2 d_state, nheads = d_inner / 64, d_inner = 2 d_model. */
+typedef struct {
+  const float* norm_w;   /* [d_model]  RMSNorm before the mixer */
+  dfssm_layer in_proj;   /* K = d_model, N = 2 d_inner + 2 d_state + nheads */
+  const float* conv_w;   /* [conv_dim][4] */
+  const float* conv_b;   /* [conv_dim] */
+  const float* dt_bias;  /* [nheads] */
+  const float* A_log;    /* [nheads] */
+  const float* D;        /* [nheads] */
+  const float* gate_w;   /* [d_inner]  weight of the gated norm */
+  dfssm_layer out_proj;  /* K = d_inner, N = d_model */
+} dfssm_mamba2_layer;
+
+/* The model: tied int8 embedding / LM head table, n_layers layers, final
+ * norm.  `layers` is a HOST array of n_layers entries. */
+typedef struct {
+  int64_t d_model, d_state, n_layers, vocab;
+  float eps;                         /* RMSNorm epsilon (1e-5 in Mamba-2) */
+  const int8_t* E;                   /* [vocab][d_model] int8 */
+  const float* E_scale;              /* [vocab] */
+  const float* norm_f;               /* [d_model] */
+  const dfssm_mamba2_layer* layers;  /* host array */
+} dfssm_mamba2_model;
+
+/* Bytes of the per-sequence state for M sequences (caller-allocated, device):
+ *   conv_ring [n_layers][M][4][conv_dim] fp32 and
+ *   ssm_state [n_layers][M][nheads][64][d_state] fp32,
+ * zero for sequences that start with the next step (their step counter then
+ * counts from there; only step & 3 matters to the ring).  Either output may
+ * be NULL.  Returns DFSSM_OK or SHAPE. */
+dfssm_status dfssm_mamba2_state_bytes(const dfssm_mamba2_model* model, int64_t M, size_t* conv_ring_bytes,
+                                      size_t* ssm_state_bytes);
+
+/* Bytes of device workspace dfssm_mamba2_decode_step needs for M tokens. */
+size_t dfssm_mamba2_workspace_bytes(const dfssm_mamba2_model* model, int64_t M);
+
+/* One decode step of M sequences, all on `stream` (Sec. 4.1: the paper
+ * captures the whole 48-layer forward pass as one CUDA graph, with the SSM
+ * and convolution states preallocated and kept across tokens):
+ *   x = embed_gather(tok); for each layer l:
+ *     u += delta (l > 0);  (q, s) = quantise(rmsnorm(u) * norm_w)
+ *     zx = in_proj(q, s);  y = ssm_step(zx, step, state_l)
+ *     (q, s) = quantise(rmsnorm(y * silu(z)) * gate_w);  delta = out_proj(q, s)
+ *   u += delta;  (q, s) = quantise(rmsnorm(u) * norm_f);  logits = lm_head(q, s)
+ * with the entry points above (in_proj and out_proj on the automatic path).
+ *   tok     [M] int32 device token ids (outside [0, vocab) -> a zero row)
+ *   step    this token's position; only step & 3 is used (the ring slot)
+ *   conv_ring, ssm_state   the state, updated in place
+ *   logits  [M][vocab] fp32 device output
+ * Graph capture: nothing here allocates, copies or synchronises, so the call
+ * can be captured.  A captured step keeps its step & 3 (capture four graphs,
+ * one per value, and replay the one for each token) and the per-call tags of
+ * its few-token linears; it replays correctly because its linears share the
+ * workspace, so every linear finds the exchange words left by another call.
+ * Limits: d_model a multiple of 128 (<= 8192); d_state 64 or 128; every
+ * layer's projections of those shapes; M >= 1; vocab >= 1.
+ * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */
+dfssm_status dfssm_mamba2_decode_step(const dfssm_mamba2_model* model, int64_t M, const int32_t* tok,
+                                      int64_t step, float* conv_ring, float* ssm_state, float* logits,
+                                      void* workspace, size_t workspace_bytes, void* stream);
+
 /* Static text for a status code. */
 const char* dfssm_status_string(int status);
 /* Thread-local description of the last failure on this thread ("" if none). */

@@ -23,7 +23,8 @@ EXPORTS = ["dfssm_quantize_act", "dfssm_linear_workspace_bytes", "dfssm_scaffold
            "dfssm_scaffold_lora_linear_ex", "dfssm_chain_workspace_bytes",
            "dfssm_scaffold_lora_chain", "dfssm_chain_prepare", "dfssm_chain_run", "dfssm_chain_status",
            "dfssm_embed_gather", "dfssm_lm_head", "dfssm_add_rmsnorm_quant", "dfssm_gate_norm_quant",
-           "dfssm_ssm_step", "dfssm_status_string", "dfssm_last_error", "dfssm_version"]
+           "dfssm_ssm_step", "dfssm_mamba2_state_bytes", "dfssm_mamba2_workspace_bytes",
+           "dfssm_mamba2_decode_step", "dfssm_status_string", "dfssm_last_error", "dfssm_version"]
 
 
 class DfssmError(RuntimeError):
@@ -37,6 +38,21 @@ class Layer(ctypes.Structure):
     _fields_ = [("w_bits", ctypes.c_void_p), ("alpha", ctypes.c_void_p), ("A", ctypes.c_void_p),
                 ("B", ctypes.c_void_p), ("beta", ctypes.c_void_p), ("K", ctypes.c_int64),
                 ("N", ctypes.c_int64), ("r", ctypes.c_int64)]
+
+
+class Mamba2Layer(ctypes.Structure):
+    """dfssm_mamba2_layer: one Mamba-2 layer (device pointers)."""
+    _fields_ = [("norm_w", ctypes.c_void_p), ("in_proj", Layer), ("conv_w", ctypes.c_void_p),
+                ("conv_b", ctypes.c_void_p), ("dt_bias", ctypes.c_void_p), ("A_log", ctypes.c_void_p),
+                ("D", ctypes.c_void_p), ("gate_w", ctypes.c_void_p), ("out_proj", Layer)]
+
+
+class Mamba2Model(ctypes.Structure):
+    """dfssm_mamba2_model."""
+    _fields_ = [("d_model", ctypes.c_int64), ("d_state", ctypes.c_int64), ("n_layers", ctypes.c_int64),
+                ("vocab", ctypes.c_int64), ("eps", ctypes.c_float), ("E", ctypes.c_void_p),
+                ("E_scale", ctypes.c_void_p), ("norm_f", ctypes.c_void_p),
+                ("layers", ctypes.POINTER(Mamba2Layer))]
 
 
 def _load(path: str = LIB_PATH) -> ctypes.CDLL:
@@ -74,6 +90,13 @@ def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dfssm_gate_norm_quant.restype = i32
     lib.dfssm_ssm_step.argtypes = [vp, i64, i64, i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.dfssm_ssm_step.restype = i32
+    mp = ctypes.POINTER(Mamba2Model)
+    lib.dfssm_mamba2_state_bytes.argtypes = [mp, i64, ctypes.POINTER(sz), ctypes.POINTER(sz)]
+    lib.dfssm_mamba2_state_bytes.restype = i32
+    lib.dfssm_mamba2_workspace_bytes.argtypes = [mp, i64]
+    lib.dfssm_mamba2_workspace_bytes.restype = sz
+    lib.dfssm_mamba2_decode_step.argtypes = [mp, i64, vp, i64, vp, vp, vp, vp, sz, vp]
+    lib.dfssm_mamba2_decode_step.restype = i32
     lib.dfssm_status_string.argtypes = [i32]
     lib.dfssm_status_string.restype = ctypes.c_char_p
     lib.dfssm_last_error.restype = ctypes.c_char_p
@@ -344,3 +367,60 @@ def ssm_step(zxbcdt, step: int, conv_ring, ssm_state, conv_w, conv_b, dt_bias, A
                               conv_w.data_ptr(), conv_b.data_ptr(), dt_bias.data_ptr(), A_log.data_ptr(),
                               D.data_ptr(), ssm_state.data_ptr(), y.data_ptr(), _ptr(xbc), _stream(stream)))
     return y
+
+
+class Mamba2:
+    """A Mamba-2 model for dfssm_mamba2_decode_step: the host structs over
+    the caller's device tensors (kept referenced here).
+
+    layers: list of dicts with norm_w, conv_w, conv_b, dt_bias, A_log, D,
+    gate_w (fp32 device tensors) and in_proj / out_proj (dicts of w_bits,
+    alpha, A, B, beta as for scaffold_lora_linear)."""
+
+    def __init__(self, E, E_scale, norm_f, layers, d_state: int = 128, eps: float = 1e-5):
+        self._keep = [E, E_scale, norm_f, layers]
+        self.vocab, self.d_model = E.shape
+        self.n_layers = len(layers)
+        self._layers = (Mamba2Layer * self.n_layers)()
+        for i, L in enumerate(layers):
+            self._layers[i] = Mamba2Layer(L["norm_w"].data_ptr(), _proj(L["in_proj"]), L["conv_w"].data_ptr(),
+                                          L["conv_b"].data_ptr(), L["dt_bias"].data_ptr(), L["A_log"].data_ptr(),
+                                          L["D"].data_ptr(), L["gate_w"].data_ptr(), _proj(L["out_proj"]))
+        self.struct = Mamba2Model(self.d_model, d_state, self.n_layers, self.vocab, eps, E.data_ptr(),
+                                  E_scale.data_ptr(), norm_f.data_ptr(), self._layers)
+
+    def state_bytes(self, M: int):
+        c, s = ctypes.c_size_t(0), ctypes.c_size_t(0)
+        _check(lib.dfssm_mamba2_state_bytes(ctypes.byref(self.struct), M, ctypes.byref(c), ctypes.byref(s)))
+        return int(c.value), int(s.value)
+
+    def new_state(self, M: int, device="cuda"):
+        """Zero (conv_ring, ssm_state) for M new sequences."""
+        torch = _torch()
+        c, s = self.state_bytes(M)
+        return (torch.zeros(c // 4, dtype=torch.float32, device=device),
+                torch.zeros(s // 4, dtype=torch.float32, device=device))
+
+    def workspace(self, M: int, device="cuda"):
+        torch = _torch()
+        return torch.empty(int(lib.dfssm_mamba2_workspace_bytes(ctypes.byref(self.struct), M)), dtype=torch.uint8,
+                           device=device)
+
+    def decode_step(self, tok, step: int, conv_ring, ssm_state, workspace, logits=None, stream=None):
+        """One token for each of the M sequences (tok int32 [M]); returns
+        logits [M, vocab]."""
+        torch = _torch()
+        _need(tok, torch.int32, "tok", 1)
+        M = tok.shape[0]
+        logits = torch.empty((M, self.vocab), dtype=torch.float32, device=tok.device) if logits is None else logits
+        _check(lib.dfssm_mamba2_decode_step(ctypes.byref(self.struct), M, tok.data_ptr(), int(step),
+                                            conv_ring.data_ptr(), ssm_state.data_ptr(), logits.data_ptr(),
+                                            workspace.data_ptr(), workspace.numel(), _stream(stream)))
+        return logits
+
+
+def _proj(w) -> Layer:
+    r = 0 if w.get("A") is None else w["A"].shape[0]
+    return Layer(w["w_bits"].data_ptr(), w["alpha"].data_ptr(), _ptr(w.get("A")) if r else None,
+                 _ptr(w.get("B")) if r else None, _ptr(w.get("beta")) if r else None, w["w_bits"].shape[1] * 32,
+                 w["w_bits"].shape[0], r)

@@ -505,3 +505,170 @@ dfssm_status dfssm_ssm_step(const float* zxbcdt, int64_t ld, int64_t M, int64_t 
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------- model step
+namespace {
+
+struct ModelDims {
+  int64_t d_model, d_inner, N, H, conv_dim, ld;
+};
+
+dfssm_status check_model(const dfssm_mamba2_model* md, int64_t M, ModelDims* dims) {
+  if (!md) return fail(DFSSM_ERR_NULL, "model is NULL");
+  // d_model % 128 keeps in_proj's row (4 d_model + 2 d_state + d_model / 32
+  // values) a whole number of 16-byte words for the gated norm's z loads
+  if (md->d_model <= 0 || md->d_model % 128 != 0 || md->d_model > 8192)
+    return fail(DFSSM_ERR_SHAPE, "d_model=%lld must be a positive multiple of 128, <= 8192", (long long)md->d_model);
+  if (md->d_state != 64 && md->d_state != 128)
+    return fail(DFSSM_ERR_UNSUPPORTED, "d_state=%lld: 64 or 128 only", (long long)md->d_state);
+  if (md->n_layers <= 0 || md->n_layers > 4096) return fail(DFSSM_ERR_SHAPE, "n_layers=%lld", (long long)md->n_layers);
+  if (md->vocab <= 0 || md->vocab > INT32_MAX / 2) return fail(DFSSM_ERR_SHAPE, "vocab=%lld", (long long)md->vocab);
+  if (!(md->eps >= 0.0f) || md->eps > FLT_MAX) return fail(DFSSM_ERR_SHAPE, "eps must be finite and >= 0");
+  if (M <= 0 || M > 65536) return fail(DFSSM_ERR_SHAPE, "M=%lld must be in [1, 65536]", (long long)M);
+  ModelDims d;
+  d.d_model = md->d_model;
+  d.d_inner = 2 * md->d_model;
+  d.N = md->d_state;
+  d.H = d.d_inner / 64;
+  d.conv_dim = d.d_inner + 2 * d.N;
+  d.ld = d.d_inner + d.conv_dim + d.H;
+  *dims = d;
+  return DFSSM_OK;
+}
+
+dfssm_status check_model_pointers(const dfssm_mamba2_model* md, const ModelDims& d) {
+  dfssm_status st = check_ptrs({{md->E, "E"}, {md->E_scale, "E_scale"}, {md->norm_f, "norm_f"}}, {});
+  if (st != DFSSM_OK) return st;
+  if (!md->layers) return fail(DFSSM_ERR_NULL, "layers is NULL");
+  for (int64_t l = 0; l < md->n_layers; ++l) {
+    const dfssm_mamba2_layer& L = md->layers[l];
+    char why[256];
+    st = check_ptrs({{L.norm_w, "norm_w"}, {L.conv_w, "conv_w"}, {L.conv_b, "conv_b"}, {L.dt_bias, "dt_bias"},
+                     {L.A_log, "A_log"}, {L.D, "D"}, {L.gate_w, "gate_w"}},
+                    {});
+    const dfssm_layer* pr[2] = {&L.in_proj, &L.out_proj};
+    const int64_t want_k[2] = {d.d_model, d.d_inner}, want_n[2] = {d.ld, d.d_model};
+    for (int i = 0; i < 2 && st == DFSSM_OK; ++i) {
+      const dfssm_layer& P = *pr[i];
+      if (P.K != want_k[i] || P.N != want_n[i])
+        st = fail(DFSSM_ERR_SHAPE, "%s is %lld x %lld, the model needs %lld x %lld", i ? "out_proj" : "in_proj",
+                  (long long)P.K, (long long)P.N, (long long)want_k[i], (long long)want_n[i]);
+      else
+        st = check_linear(1, P.K, P.N, P.r);
+      if (st == DFSSM_OK) st = check_ptrs({{P.w_bits, "w_bits"}, {P.alpha, "alpha"}}, {});
+      if (st == DFSSM_OK && P.r > 0) st = check_ptrs({{P.A, "A"}, {P.B, "B"}, {P.beta, "beta"}}, {});
+    }
+    if (st != DFSSM_OK) {
+      snprintf(why, sizeof(why), "%s", g_last_error);
+      return fail(st, "layer %lld: %s", (long long)l, why);
+    }
+  }
+  return DFSSM_OK;
+}
+
+struct ModelWs {
+  float *u, *delta, *zx, *y, *s;
+  int8_t* q;
+  char* lin;
+  size_t lin_bytes, bytes;
+};
+
+ModelWs carve_model_ws(void* base, const dfssm_mamba2_model* md, const ModelDims& d, int64_t M) {
+  ModelWs w{};
+  size_t off = 0;
+  auto take = [&](size_t n) {
+    size_t o = off;
+    off += (n + 255) & ~(size_t)255;
+    return o;
+  };
+  const size_t o_u = take((size_t)(M * d.d_model) * 4), o_d = take((size_t)(M * d.d_model) * 4);
+  const size_t o_zx = take((size_t)(M * d.ld) * 4), o_y = take((size_t)(M * d.d_inner) * 4);
+  const size_t o_s = take((size_t)M * 4), o_q = take((size_t)(M * d.d_inner));
+  size_t lin = 0;
+  for (int64_t l = 0; md->layers && l < md->n_layers; ++l) {
+    lin = std::max(lin, linear_ws_bytes(M, d.d_model, md->layers[l].in_proj.r));
+    lin = std::max(lin, linear_ws_bytes(M, d.d_inner, md->layers[l].out_proj.r));
+  }
+  const size_t o_lin = take(lin);
+  char* b = static_cast<char*>(base);
+  w.u = reinterpret_cast<float*>(b + o_u);
+  w.delta = reinterpret_cast<float*>(b + o_d);
+  w.zx = reinterpret_cast<float*>(b + o_zx);
+  w.y = reinterpret_cast<float*>(b + o_y);
+  w.s = reinterpret_cast<float*>(b + o_s);
+  w.q = reinterpret_cast<int8_t*>(b + o_q);
+  w.lin = b + o_lin;
+  w.lin_bytes = lin;
+  w.bytes = off;
+  return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+dfssm_status dfssm_mamba2_state_bytes(const dfssm_mamba2_model* model, int64_t M, size_t* conv_ring_bytes,
+                                      size_t* ssm_state_bytes) {
+  clear_error();
+  ModelDims d;
+  dfssm_status st = check_model(model, M, &d);
+  if (st != DFSSM_OK) return st;
+  if (conv_ring_bytes) *conv_ring_bytes = (size_t)(model->n_layers * M * 4 * d.conv_dim) * 4;
+  if (ssm_state_bytes) *ssm_state_bytes = (size_t)(model->n_layers * M * d.H * 64 * d.N) * 4;
+  return DFSSM_OK;
+}
+
+size_t dfssm_mamba2_workspace_bytes(const dfssm_mamba2_model* model, int64_t M) {
+  ModelDims d;
+  if (check_model(model, M, &d) != DFSSM_OK) return 0;
+  return carve_model_ws(nullptr, model, d, M).bytes;
+}
+
+dfssm_status dfssm_mamba2_decode_step(const dfssm_mamba2_model* model, int64_t M, const int32_t* tok,
+                                      int64_t step, float* conv_ring, float* ssm_state, float* logits,
+                                      void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  ModelDims d;
+  dfssm_status st = check_model(model, M, &d);
+  if (st != DFSSM_OK) return st;
+  if (step < 0) return fail(DFSSM_ERR_SHAPE, "step=%lld must be >= 0", (long long)step);
+  st = check_model_pointers(model, d);
+  if (st != DFSSM_OK) return st;
+  st = check_ptrs({{tok, "tok"}, {conv_ring, "conv_ring"}, {ssm_state, "ssm_state"}, {logits, "logits"},
+                   {workspace, "workspace"}},
+                  {});
+  if (st != DFSSM_OK) return st;
+  const ModelWs w = carve_model_ws(workspace, model, d, M);
+  if (workspace_bytes < w.bytes)
+    return fail(DFSSM_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, w.bytes);
+  hipStream_t hs = (hipStream_t)stream;
+  const float eps = model->eps;
+  const int64_t ring_stride = M * 4 * d.conv_dim, state_stride = M * d.H * 64 * d.N;
+  hipError_t e = dfssm::launch_embed_gather(model->E, model->E_scale, model->vocab, d.d_model, tok, M, w.u, hs);
+  for (int64_t l = 0; l < model->n_layers && e == hipSuccess; ++l) {
+    const dfssm_mamba2_layer& L = model->layers[l];
+    e = dfssm::launch_add_rmsnorm_quant(w.u, l > 0 ? w.delta : nullptr, L.norm_w, eps, M, d.d_model, w.u, w.q, w.s, hs);
+    if (e != hipSuccess) break;
+    const dfssm_layer& I = L.in_proj;
+    dfssm::LinearWorkspace lw = dfssm::carve_linear_workspace(w.lin, M, I.K, I.r);
+    e = launch_linear(DFSSM_PATH_AUTO, w.q, w.s, M, I.K, I.N, I.r, I.w_bits, I.alpha, I.A, I.B, I.beta, w.zx,
+                      nullptr, nullptr, nullptr, lw, hs);
+    if (e != hipSuccess) break;
+    e = dfssm::launch_ssm_step(w.zx, d.ld, M, d.d_inner, d.N, step, conv_ring + l * ring_stride, L.conv_w, L.conv_b,
+                               L.dt_bias, L.A_log, L.D, ssm_state + l * state_stride, w.y, nullptr, hs);
+    if (e != hipSuccess) break;
+    e = dfssm::launch_gate_norm_quant(w.y, w.zx, d.ld, L.gate_w, eps, M, d.d_inner, w.q, w.s, hs);
+    if (e != hipSuccess) break;
+    const dfssm_layer& O = L.out_proj;
+    lw = dfssm::carve_linear_workspace(w.lin, M, O.K, O.r);
+    e = launch_linear(DFSSM_PATH_AUTO, w.q, w.s, M, O.K, O.N, O.r, O.w_bits, O.alpha, O.A, O.B, O.beta, w.delta,
+                      nullptr, nullptr, nullptr, lw, hs);
+  }
+  if (e == hipSuccess)
+    e = dfssm::launch_add_rmsnorm_quant(w.u, w.delta, model->norm_f, eps, M, d.d_model, w.u, w.q, w.s, hs);
+  if (e == hipSuccess)
+    e = dfssm::launch_lm_head(w.q, w.s, M, d.d_model, model->E, model->E_scale, model->vocab, logits, nullptr, hs);
+  return e == hipSuccess ? DFSSM_OK : device_fail(e, "decode step launch");
+}
+
+}  // extern "C"

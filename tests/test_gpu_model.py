@@ -1,0 +1,142 @@
+"""GPU parity of the whole decode step (dfssm_mamba2_decode_step): token
+gather, every layer's norm -> in_proj -> conv + SSM step -> gated norm ->
+out_proj with the residual, final norm and LM head, over several tokens.
+
+Against the oracle: the same chain of oracle calls on the same seeded model
+(the 1.3B layer shapes, 2 layers, a 1,000-word table).  Every stage follows
+one rounding order; the SSM output's fp64 sum is taken in another order on
+the device, which can move a value by one ulp and, rarely, a code of
+out_proj's input, so logits must agree within 1e-3 of their largest value
+(and the argmax must agree), and in practice agree bit for bit.
+
+Against itself under graph capture: four captured steps (one per ring
+slot, step & 3) replayed for eight tokens, with new token ids written
+between replays, must give exactly the eager results, replay after replay."""
+import numpy as np
+import pytest
+
+import dfssm_synth as S
+import oracle
+from gpu_util import dev, dev_weights, host, say, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+V, L, EPS = 1000, 2, 1e-5
+
+
+@pytest.fixture(scope="module")
+def env():
+    torch = torch_cuda()
+    import paper_2606_10932_amd as D
+    oracle.build()
+    return torch, D, oracle.get()
+
+
+@pytest.fixture(scope="module")
+def model_host():
+    ws = S.sweep_weights(n_layers=L)
+    layers = []
+    for l in range(L):
+        p = S.mamba_params(2048, key=(140, l))
+        layers.append(dict(p, in_proj=ws[2 * l], out_proj=ws[2 * l + 1]))
+    E, scale = S.embedding(V, 2048, key=(141,))
+    norm_f = np.random.default_rng(142).uniform(0.8, 1.2, 2048).astype(np.float32)
+    return dict(E=E, scale=scale, norm_f=norm_f, layers=layers)
+
+
+def device_model(D, mh):
+    layers = []
+    for ly in mh["layers"]:
+        d = {k: dev(v) for k, v in ly.items() if k not in ("in_proj", "out_proj")}
+        d["in_proj"], d["out_proj"] = dev_weights(ly["in_proj"]), dev_weights(ly["out_proj"])
+        layers.append(d)
+    return D.Mamba2(dev(mh["E"]), dev(mh["scale"]), dev(mh["norm_f"]), layers, d_state=128, eps=EPS)
+
+
+class OracleModel:
+    """The decode step as a sequence of oracle calls (test-side plumbing)."""
+
+    def __init__(self, o, mh, M):
+        self.o, self.mh, self.M = o, mh, M
+        dm = S.mamba_dims(2048)
+        self.conv = [np.zeros((M, dm["conv_dim"], 4), np.float32) for _ in range(L)]
+        self.ssm = [np.zeros((M, 64, 64, 128), np.float32) for _ in range(L)]
+
+    def step(self, tok):
+        o, mh = self.o, self.mh
+        u = o.embed_gather(mh["E"], mh["scale"], tok)
+        delta = None
+        for l, ly in enumerate(mh["layers"]):
+            u, _, q, s = o.add_rmsnorm_quant(u, ly["norm_w"], EPS, delta=delta)
+            zx = o.linear(q, s, **ly["in_proj"])["y32"]
+            y, _, self.conv[l], self.ssm[l] = o.ssm_step(zx, self.conv[l], self.ssm[l], ly["conv_w"], ly["conv_b"],
+                                                         ly["dt_bias"], ly["A_log"], ly["D"], 4096, 128, 64)
+            _, q, s = o.gate_norm_quant(y, zx[:, :4096], ly["gate_w"], EPS)
+            delta = o.linear(q, s, **ly["out_proj"])["y32"]
+        _, _, q, s = o.add_rmsnorm_quant(u, mh["norm_f"], EPS, delta=delta)
+        return o.lm_head(q, s, mh["E"], mh["scale"])[1]
+
+
+@pytest.mark.parametrize("M", [1, 3])
+def test_decode_step_against_oracle(env, model_host, M):
+    torch, D, o = env
+    say(f"decode step M={M} vs oracle")
+    m = device_model(D, model_host)
+    ring, state = m.new_state(M)
+    ws = m.workspace(M)
+    om = OracleModel(o, model_host, M)
+    exact = 0
+    for t in range(5):
+        tok = S.tokens(M, V, key=(143, M, t))
+        ref = om.step(tok)
+        lg = host(m.decode_step(dev(tok), t, ring, state, ws))
+        torch.cuda.synchronize()
+        scale = float(np.abs(ref).max())
+        assert np.abs(lg.astype(np.float64) - ref).max() <= 1e-3 * scale, f"token {t}"
+        assert np.array_equal(lg.argmax(axis=1), ref.argmax(axis=1)), f"token {t}"
+        exact += int(np.array_equal(lg.view(np.uint32), ref.view(np.uint32)))
+    say(f"  {exact} of 5 tokens bit-exact")
+    assert exact >= 3
+
+
+def test_decode_step_graph_replays(env, model_host):
+    torch, D, o = env
+    say("decode step: four captured graphs, eight replays")
+    M = 2
+    m = device_model(D, model_host)
+    # eager reference on its own state
+    ring_e, state_e = m.new_state(M)
+    ws_e = m.workspace(M)
+    toks = [S.tokens(M, V, key=(144, t)) for t in range(8)]
+    eager = [host(m.decode_step(dev(tk), t, ring_e, state_e, ws_e)) for t, tk in enumerate(toks)]
+    torch.cuda.synchronize()
+    # graphs: static token buffer, logits buffer and workspace
+    ring, state = m.new_state(M)
+    ws = m.workspace(M)
+    tok_buf = torch.zeros(M, dtype=torch.int32, device="cuda")
+    lg_buf = torch.empty((M, V), dtype=torch.float32, device="cuda")
+    # capture on scratch state so the real state stays at token 0
+    ring_c, state_c = m.new_state(M)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graphs = []
+    with torch.cuda.stream(side):
+        m.decode_step(tok_buf, 0, ring_c, state_c, ws, logits=lg_buf)     # warm-up outside capture
+        for ph in range(4):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=side):
+                m.decode_step(tok_buf, ph, ring, state, ws, logits=lg_buf)
+            graphs.append(g)
+    torch.cuda.synchronize()
+    # the captures did not run: reset the state the graphs write
+    ring.zero_()
+    state.zero_()
+    torch.cuda.synchronize()
+    for t, tk in enumerate(toks):
+        tok_buf.copy_(dev(tk))
+        torch.cuda.synchronize()
+        graphs[t % 4].replay()
+        torch.cuda.synchronize()
+        got = host(lg_buf)
+        assert np.array_equal(got.view(np.uint32), eager[t].view(np.uint32)), f"replay for token {t}"
+    assert np.array_equal(host(state), host(state_e)) and np.array_equal(host(ring), host(ring_e))

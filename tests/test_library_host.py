@@ -161,6 +161,45 @@ def test_mamba_step_validation(dl):
     assert ssm(M=0, zx=None) == dl.OK
 
 
+def test_model_step_validation(dl):
+    import ctypes
+    good_in = dl.Layer(16, 16, 16, 16, 16, 2048, 8512, 64)
+    good_out = dl.Layer(16, 16, 16, 16, 16, 4096, 2048, 64)
+    lay = (dl.Mamba2Layer * 2)(dl.Mamba2Layer(16, good_in, 16, 16, 16, 16, 16, 16, good_out),
+                               dl.Mamba2Layer(16, good_in, 16, 16, 16, 16, 16, 16, good_out))
+
+    def model(**kw):
+        f = dict(d_model=2048, d_state=128, n_layers=2, vocab=50280, eps=1e-5, E=16, E_scale=16, norm_f=16)
+        f.update(kw)
+        return dl.Mamba2Model(f["d_model"], f["d_state"], f["n_layers"], f["vocab"], f["eps"], f["E"],
+                              f["E_scale"], f["norm_f"], lay)
+
+    step = dl.lib.dfssm_mamba2_decode_step    # model, M, tok, step, ring, state, logits, ws, bytes, stream
+
+    def run(m, M=1, ws_bytes=1 << 40, tok=16, t=0):
+        return step(ctypes.byref(m), M, tok, t, 16, 16, 16, 16, ws_bytes, None)
+    assert run(model(d_model=2000)) == dl.ERR_SHAPE
+    assert run(model(d_model=2080)) == dl.ERR_SHAPE          # not a multiple of 128
+    assert run(model(d_state=96)) == dl.ERR_UNSUPPORTED
+    assert run(model(vocab=0)) == dl.ERR_SHAPE
+    assert run(model(), M=0) == dl.ERR_SHAPE
+    assert run(model(), t=-1) == dl.ERR_SHAPE
+    assert run(model(E=None)) == dl.ERR_NULL
+    assert run(model(), tok=None) == dl.ERR_NULL
+    assert run(model(), ws_bytes=64) == dl.ERR_WORKSPACE
+    lay[1].out_proj.N = 2047
+    assert run(model()) == dl.ERR_SHAPE and "layer 1" in dl.last_error()
+    lay[1].out_proj.N = 2048
+    lay[0].conv_b = None
+    assert run(model()) == dl.ERR_NULL and "layer 0" in dl.last_error()
+    lay[0].conv_b = 16
+    m = model()
+    c, s = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    assert dl.lib.dfssm_mamba2_state_bytes(ctypes.byref(m), 3, ctypes.byref(c), ctypes.byref(s)) == dl.OK
+    assert c.value == 2 * 3 * 4 * 4352 * 4 and s.value == 2 * 3 * 64 * 64 * 128 * 4
+    assert dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1) > 0
+
+
 def test_workspace_sizes(dl):
     a = dl.linear_workspace_bytes(1, 2048, 8512, 64)
     b = dl.linear_workspace_bytes(2048, 2048, 8512, 64)
