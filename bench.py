@@ -8,7 +8,9 @@ workspace prepared once per weight set (dfssm_chain_prepare, untimed).
 Metric: effective packed-weight GB/s (sign words + LoRA factors + row scales
 read per step / step time) and us per layer; the 2048-token prefill in_proj
 is measured beside it in int8 TOPS, the decode-size single linears in us per
-call, and the LM head over the 1.3B tied int8 table (103 MB) in GB/s.
+call, the LM head over the 1.3B tied int8 table (103 MB) in GB/s, and the
+whole 1.3B decode step (48 layers + LM head, as replayed hipGraphs) in
+tokens/s at batch 1, 8, 32, 128 and 512.
 
 Weights are synthetic and seeded (no trained weights exist here).  The sweep
 reads 210 MB per step, which fits the 256 MB Infinity Cache, so steps rotate
@@ -47,6 +49,8 @@ def parse():
     p.add_argument("--no-prefill", action="store_true")
     p.add_argument("--no-decode", action="store_true", help="skip the single-linear decode-size figures")
     p.add_argument("--no-lm-head", action="store_true", help="skip the LM head figures")
+    p.add_argument("--no-model", action="store_true", help="skip the whole-model decode step figures")
+    p.add_argument("--model-batches", default="1,8,32,128,512", help="batch sizes of the decode step figures")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="minimum CPU oracle sample time")
     p.add_argument("--copy-calibration-mib", type=int, default=0,
                    help="run one plain device copy of this size first (for HBM counter scaling)")
@@ -250,7 +254,7 @@ def main():
     # logits of M tokens over the 1.3B vocabulary (50,280 x 2048 int8 table,
     # 103 MB).  One graph replay walks over 4 distinct copies of the table
     # (412 MB), so every call streams its table from HBM.
-    lm = None
+    lm, table0 = None, None
     if not args.no_lm_head:
         lm = []
         Eh, sch = S.embedding(S.VOCAB_1P3B, S.D_MODEL_1P3B, key=(40,))
@@ -286,7 +290,68 @@ def main():
                        "table_gbs": round(tb / (us * 1e-6) / 1e9, 1),
                        "frac_hbm_peak": round(tb / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4), "table_bytes": tb})
             del g
+        table0 = tabs[0]
         del tabs
+
+    # ---- the whole decode step of the 1.3B model ----------------------------
+    # dfssm_mamba2_decode_step (gather, 48 x [norm, in_proj, conv + SSM step,
+    # gated norm, out_proj], final norm, LM head) captured as four graphs,
+    # one per ring slot, replayed token after token on zero-initialised state.
+    # The linears are weight copy 0 of the sweep, the table the LM head's.
+    model_fig = None
+    if not args.no_model:
+        if table0 is None:
+            Eh, sch = S.embedding(S.VOCAB_1P3B, S.D_MODEL_1P3B, key=(40,))
+            table0 = (dev(Eh), dev(sch))
+            del Eh
+        layers = []
+        for l in range(48):
+            lp = {k: dev(v) for k, v in S.mamba_params(2048, key=(150, l)).items()}
+            lp["in_proj"], lp["out_proj"] = copies[0][2 * l], copies[0][2 * l + 1]
+            layers.append(lp)
+        norm_f = dev(np.random.default_rng(151).uniform(0.8, 1.2, 2048).astype(np.float32))
+        mdl = D.Mamba2(table0[0], table0[1], norm_f, layers)
+        param_bytes = 2048 * 4 + sum(v.numel() * 4 for lp in layers for k, v in lp.items()
+                                     if k not in ("in_proj", "out_proj"))
+        table_bytes = table0[0].numel() + table0[1].numel() * 4
+        model_fig = []
+        for Mb in [int(v) for v in args.model_batches.split(",") if v]:
+            ring, state = mdl.new_state(Mb)
+            ws_m = mdl.workspace(Mb)
+            tok = dev(S.tokens(Mb, S.VOCAB_1P3B, key=(152, Mb)))
+            lg = torch.empty((Mb, S.VOCAB_1P3B), dtype=torch.float32, device="cuda")
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            graphs = []
+            with torch.cuda.stream(side):
+                mdl.decode_step(tok, 0, ring, state, ws_m, logits=lg)
+                for ph in range(4):
+                    g = torch.cuda.CUDAGraph()
+                    with torch.cuda.graph(g, stream=side):
+                        mdl.decode_step(tok, ph, ring, state, ws_m, logits=lg)
+                    graphs.append(g)
+            torch.cuda.synchronize()
+            for tt in range(1, 5):
+                graphs[tt % 4].replay()
+            torch.cuda.synchronize()
+            n = 12
+            t0.record(stream)
+            for tt in range(5, 5 + n):
+                graphs[tt % 4].replay()
+            t1.record(stream)
+            torch.cuda.synchronize()
+            ms_tok = t0.elapsed_time(t1) / n
+            # bytes a step must move at least: weights, table, parameters,
+            # the SSM state read and written, the ring (3 slots read, 1 written)
+            step_bytes = weight_bytes + table_bytes + param_bytes + 2 * state.numel() * 4 + ring.numel() * 4
+            model_fig.append({"workload": f"Mamba-2-1.3B decode step, batch {Mb}, 48 layers + LM head",
+                              "ms_per_step": round(ms_tok, 4), "tokens_per_s": round(Mb / (ms_tok * 1e-3), 1),
+                              "us_per_layer": round(ms_tok * 1e3 / 48, 2),
+                              "bytes_per_step": int(step_bytes),
+                              "effective_gbs": round(step_bytes / (ms_tok * 1e-3) / 1e9, 1)})
+            del graphs, g, ring, state, ws_m, lg
+            torch.cuda.synchronize()
+        del mdl, layers
 
     # ---- CPU oracle baseline on a bounded sample ----------------------------
     cpu = None
@@ -334,6 +399,7 @@ def main():
         "prefill": prefill,
         "decode_linears": decode,
         "lm_head": lm,
+        "decode_step": model_fig,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

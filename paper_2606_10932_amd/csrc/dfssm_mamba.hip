@@ -19,6 +19,8 @@
 // appends to them, with no ordering between workgroups.
 #include <float.h>
 
+#include <algorithm>
+
 #include "dfssm_mamba.hpp"
 
 namespace {
@@ -54,7 +56,7 @@ __device__ __forceinline__ float max_lanes(float v) {
 }
 
 // ---------------------------------------------------------------- norms
-constexpr int kNormThreads = 256;
+constexpr int kNormMaxThreads = 1024;
 
 struct NormArgs {
   const float* a;     // u (residual) or y (SSM output), rows of d
@@ -68,42 +70,44 @@ struct NormArgs {
   float* s;           // [M]
 };
 
-// One workgroup per token row; VPT float4 per thread held in registers
-// (d <= 1024 * VPT).  GATE: g = y * silu(z); else g = u + delta.
+// One workgroup per token row, sized to the row (a multiple of 64 threads,
+// at most 1024); VPT float4 per thread held in registers.  The inputs and
+// the weight are loaded together, before the reductions, so the row costs
+// one memory round trip.  GATE: g = y * silu(z); else g = u + delta.
 template <bool GATE, int VPT>
-__global__ __launch_bounds__(kNormThreads) void norm_quant(NormArgs a) {
+__global__ __launch_bounds__(kNormMaxThreads) void norm_quant(NormArgs a) {
   const int64_t m = blockIdx.x;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6;
   const int d = a.d;
   const float* ar = a.a + m * d;
   const float* br = a.b ? a.b + m * a.ldb : nullptr;
-  __shared__ double red_ss[kNormThreads / 64];
-  __shared__ float red_max[kNormThreads / 64];
+  __shared__ double red_ss[kNormMaxThreads / 64];
+  __shared__ float red_max[kNormMaxThreads / 64];
 
-  float4 g[VPT];
+  float4 g[VPT], w[VPT], z[VPT];
 #pragma unroll
   for (int i = 0; i < VPT; ++i) {
-    const int k = 4 * (tid + kNormThreads * i);
-    if (k < d) {
-      float4 x = *reinterpret_cast<const float4*>(ar + k);
-      if (GATE) {
-        const float4 z = *reinterpret_cast<const float4*>(br + k);
-        x.x = x.x * silu_f(z.x);
-        x.y = x.y * silu_f(z.y);
-        x.z = x.z * silu_f(z.z);
-        x.w = x.w * silu_f(z.w);
-      } else if (br) {
-        const float4 dl = *reinterpret_cast<const float4*>(br + k);
-        x.x = x.x + dl.x;
-        x.y = x.y + dl.y;
-        x.z = x.z + dl.z;
-        x.w = x.w + dl.w;
-      }
-      g[i] = x;
-      if (!GATE && a.u_out) *reinterpret_cast<float4*>(a.u_out + m * d + k) = x;
-    } else {
-      g[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    const int k = 4 * (tid + nt * i);
+    const bool in = k < d;
+    g[i] = in ? *reinterpret_cast<const float4*>(ar + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+    z[i] = (in && br) ? *reinterpret_cast<const float4*>(br + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+    w[i] = in ? *reinterpret_cast<const float4*>(a.w + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) {
+    if (GATE) {
+      g[i].x = g[i].x * silu_f(z[i].x);
+      g[i].y = g[i].y * silu_f(z[i].y);
+      g[i].z = g[i].z * silu_f(z[i].z);
+      g[i].w = g[i].w * silu_f(z[i].w);
+    } else if (br) {
+      g[i].x = g[i].x + z[i].x;
+      g[i].y = g[i].y + z[i].y;
+      g[i].z = g[i].z + z[i].z;
+      g[i].w = g[i].w + z[i].w;
     }
+    const int k = 4 * (tid + nt * i);
+    if (!GATE && a.u_out && k < d) *reinterpret_cast<float4*>(a.u_out + m * d + k) = g[i];
   }
   // sum of squares in fp64 (each fp32 square is exact there)
   double ss = 0.0;
@@ -117,32 +121,30 @@ __global__ __launch_bounds__(kNormThreads) void norm_quant(NormArgs a) {
   ss = sum_lanes<64>(ss);
   if ((tid & 63) == 0) red_ss[tid >> 6] = ss;
   __syncthreads();
-  ss = (red_ss[0] + red_ss[1]) + (red_ss[2] + red_ss[3]);
+  ss = 0.0;
+  for (int i = 0; i < nw; ++i) ss += red_ss[i];
   const float r = (float)(1.0 / sqrt(ss / (double)d + (double)a.eps));
 
   float amax = 0.0f;
 #pragma unroll
   for (int i = 0; i < VPT; ++i) {
-    const int k = 4 * (tid + kNormThreads * i);
-    if (k < d) {
-      const float4 w = *reinterpret_cast<const float4*>(a.w + k);
-      g[i].x = (g[i].x * r) * w.x;
-      g[i].y = (g[i].y * r) * w.y;
-      g[i].z = (g[i].z * r) * w.z;
-      g[i].w = (g[i].w * r) * w.w;
-      amax = fmaxf(amax, fmaxf(fmaxf(fabsf(g[i].x), fabsf(g[i].y)), fmaxf(fabsf(g[i].z), fabsf(g[i].w))));
-    }
+    g[i].x = (g[i].x * r) * w[i].x;
+    g[i].y = (g[i].y * r) * w[i].y;
+    g[i].z = (g[i].z * r) * w[i].z;
+    g[i].w = (g[i].w * r) * w[i].w;
+    amax = fmaxf(amax, fmaxf(fmaxf(fabsf(g[i].x), fabsf(g[i].y)), fmaxf(fabsf(g[i].z), fabsf(g[i].w))));
   }
   amax = max_lanes(amax);
   if ((tid & 63) == 0) red_max[tid >> 6] = amax;
   __syncthreads();
-  amax = fmaxf(fmaxf(red_max[0], red_max[1]), fmaxf(red_max[2], red_max[3]));
+  amax = 0.0f;
+  for (int i = 0; i < nw; ++i) amax = fmaxf(amax, red_max[i]);
 
   int8_t* qr = a.q + m * d;
   if (amax < FLT_MIN) {  // all-zero (or subnormal-only) row
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
-      const int k = 4 * (tid + kNormThreads * i);
+      const int k = 4 * (tid + nt * i);
       if (k < d) *reinterpret_cast<uint32_t*>(qr + k) = 0u;
     }
     if (tid == 0) a.s[m] = 0.0f;
@@ -152,7 +154,7 @@ __global__ __launch_bounds__(kNormThreads) void norm_quant(NormArgs a) {
   if (tid == 0) a.s[m] = amax / 127.0f;
 #pragma unroll
   for (int i = 0; i < VPT; ++i) {
-    const int k = 4 * (tid + kNormThreads * i);
+    const int k = 4 * (tid + nt * i);
     if (k < d) {
       const uint32_t c = (uint32_t)(uint8_t)code(g[i].x, inv) | (uint32_t)(uint8_t)code(g[i].y, inv) << 8 |
                          (uint32_t)(uint8_t)code(g[i].z, inv) << 16 | (uint32_t)(uint8_t)code(g[i].w, inv) << 24;
@@ -163,18 +165,16 @@ __global__ __launch_bounds__(kNormThreads) void norm_quant(NormArgs a) {
 
 template <bool GATE>
 hipError_t launch_norm(const NormArgs& a, int64_t M, hipStream_t st) {
-  const int vpt = (int)dfssm::ceil_div(a.d, 4 * kNormThreads);
-  dim3 grid((unsigned)M), block(kNormThreads);
+  const int64_t vec = dfssm::ceil_div(a.d, 4);   // float4 per row
+  const int vpt = (int)dfssm::ceil_div(vec, kNormMaxThreads);
+  const int nt = (int)std::min<int64_t>(kNormMaxThreads, dfssm::round_up(dfssm::ceil_div(vec, vpt), 64));
+  dim3 grid((unsigned)M), block(nt);
   if (vpt <= 1)
     norm_quant<GATE, 1><<<grid, block, 0, st>>>(a);
   else if (vpt <= 2)
     norm_quant<GATE, 2><<<grid, block, 0, st>>>(a);
-  else if (vpt <= 4)
-    norm_quant<GATE, 4><<<grid, block, 0, st>>>(a);
-  else if (vpt <= 8)
-    norm_quant<GATE, 8><<<grid, block, 0, st>>>(a);
   else
-    norm_quant<GATE, 16><<<grid, block, 0, st>>>(a);
+    norm_quant<GATE, 4><<<grid, block, 0, st>>>(a);
   return hipGetLastError();
 }
 
