@@ -196,3 +196,17 @@ def inproj_out(M: int, d_model: int, d_state: int = 128, headdim: int = 64, key=
 
 def residual(M: int, d_model: int, key=(0,)) -> np.ndarray:
     return _rng(9, *key).standard_normal((M, d_model), dtype=np.float32)
+
+
+def weights_i4(K: int, N: int, r: int, key=(0, 0, 0, 0), beta_scale: float = 1.0) -> dict:
+    """A weight set with int4 LoRA factors: the int8 set's signs and scales,
+    A4 [r][K/2] and B4 [N][r/2] as uniform random bytes (every nibble value
+    -8..7 equally likely, two per byte).  r must be even."""
+    if r % 2:
+        raise ValueError("r must be even for packed int4 factors")
+    ws = weights(K, N, 0, key=key)
+    g = _rng(10, *key)
+    A4 = g.integers(0, 256, size=(r, K // 2), dtype=np.uint8)
+    B4 = g.integers(0, 256, size=(N, r // 2), dtype=np.uint8)
+    beta = (g.uniform(1e-4, 1e-3, size=N) * beta_scale).astype(np.float32)
+    return dict(w_bits=ws["w_bits"], alpha=ws["alpha"], A4=A4, B4=B4, beta=beta)

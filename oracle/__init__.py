@@ -62,6 +62,8 @@ class Oracle:
         lib.dfssm_ref_lm_head.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp]
         lib.dfssm_ref_lm_head.restype = i32
         f32 = ctypes.c_float
+        lib.dfssm_ref_unpack_int4.argtypes = [vp, i64, vp]
+        lib.dfssm_ref_unpack_int4.restype = i32
         lib.dfssm_ref_add_rmsnorm_quant.argtypes = [vp, vp, vp, f32, i64, i64, vp, vp, vp, vp]
         lib.dfssm_ref_add_rmsnorm_quant.restype = i32
         lib.dfssm_ref_ssm_step.argtypes = [vp, i64, i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp]
@@ -191,6 +193,30 @@ class Oracle:
         if st != OK:
             raise OracleError(st)
         return acc, logits
+
+    # ---- int4 LoRA factors --------------------------------------------------
+    def unpack_int4(self, packed, n: int):
+        """n int8 values from two's-complement nibbles, low nibble first."""
+        p = np.ascontiguousarray(packed, np.uint8).ravel()
+        if p.size * 2 < n:
+            raise ValueError("too few packed bytes")
+        out = np.zeros(n, np.int8)
+        st = self.lib.dfssm_ref_unpack_int4(_p(p), n, _p(out))
+        if st != OK:
+            raise OracleError(st)
+        return out
+
+    def linear_i4(self, q, s, w_bits, alpha, A4, B4, beta):
+        """The linear with int4 LoRA factors A4 [r][K/2], B4 [N][r/2] bytes:
+        the int8 linear on the unpacked factors."""
+        K = q.shape[1]
+        N = w_bits.shape[0]
+        if A4 is None or A4.size == 0:
+            return self.linear(q, s, w_bits, alpha, None, None, None)
+        r = A4.shape[0]
+        A = self.unpack_int4(A4, r * K).reshape(r, K)
+        B = self.unpack_int4(B4, N * r).reshape(N, r)
+        return self.linear(q, s, w_bits, alpha, A, B, beta)
 
     # ---- Mamba-2 decode step around the linears ----------------------------
     def add_rmsnorm_quant(self, u, w, eps, delta=None):

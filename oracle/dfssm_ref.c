@@ -253,6 +253,20 @@ int dfssm_ref_lm_head(const int8_t* q, const float* s, int64_t M, int64_t d,
   return DFSSM_REF_OK;
 }
 
+/* ---- int4 LoRA factors ------------------------------------------------- */
+
+int dfssm_ref_unpack_int4(const uint8_t* packed, int64_t n, int8_t* out) {
+  if (n < 0) return DFSSM_REF_ERR_SHAPE;
+  if (n == 0) return DFSSM_REF_OK;
+  if (!packed || !out) return DFSSM_REF_ERR_NULL;
+  for (int64_t i = 0; i < n; ++i) {
+    const int byte = packed[i / 2];
+    const int nib = (i % 2 == 0) ? (byte & 0x0f) : (byte >> 4);
+    out[i] = (int8_t)(nib >= 8 ? nib - 16 : nib);
+  }
+  return DFSSM_REF_OK;
+}
+
 /* ---- the Mamba-2 decode step around the linears ------------------------ */
 
 static float silu_f(float v) {

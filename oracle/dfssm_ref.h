@@ -120,6 +120,18 @@ int dfssm_ref_lm_head(const int8_t* q, const float* s, int64_t M, int64_t d,
                       const int8_t* E, const float* scale, int64_t V,
                       int32_t* acc, float* logits);
 
+/* ---- int4 LoRA factors -------------------------------------------------
+ * Table 4 lists the scaffold with an int4 LoRA (perplexity 52.9 against
+ * 49.1 for int8) without giving its format.  Reading: each factor value is
+ * a two's-complement 4-bit integer in [-8, 7], two per byte, value 2i in
+ * the low nibble of byte i and value 2i+1 in the high nibble, rows packed
+ * along their contracted length (A [r][K/2] bytes, B [N][r/2] bytes, r
+ * even); per-channel scales stay folded into beta.  The linear is then the
+ * int8 linear above on the unpacked values, with the same exact integers.
+ *
+ * Unpacks n values from `packed` (ceil(n/2) bytes) into out[n]. */
+int dfssm_ref_unpack_int4(const uint8_t* packed, int64_t n, int8_t* out);
+
 /* ---- the Mamba-2 decode step around the linears ------------------------
  *
  * The paper keeps Mamba-2's layer and lists what runs around the two

@@ -470,6 +470,37 @@ def pin_embed_gather_bruteforce(o: Oracle):
 
 
 # --------------------------------------------------------------------------
+# int4 LoRA factors
+# --------------------------------------------------------------------------
+def _unpack_np(packed: np.ndarray, n: int) -> np.ndarray:
+    """Independent route: numpy shifts and masks, then two's complement."""
+    p = packed.astype(np.uint8).ravel()
+    nib = np.empty(2 * p.size, np.int16)
+    nib[0::2] = p & 0x0F
+    nib[1::2] = p >> 4
+    return np.where(nib >= 8, nib - 16, nib)[:n].astype(np.int8)
+
+
+def pin_int4(o: Oracle):
+    """Hand-derived nibbles, every byte value against numpy's route, and the
+    int4 linear equal to brute force on the unpacked factors."""
+    # 0x2F: low nibble 0xF = -1, high 0x2 = 2; 0x87: 7 then -8; 0x80: 0, -8
+    assert o.unpack_int4(np.array([0x2F, 0x87, 0x80], np.uint8), 6).tolist() == [-1, 2, 7, -8, 0, -8]
+    allb = np.arange(256, dtype=np.uint8)
+    assert np.array_equal(o.unpack_int4(allb, 512), _unpack_np(allb, 512))
+    assert o.unpack_int4(np.array([0x7F], np.uint8), 1).tolist() == [-1]        # odd count
+    ws = S.weights_i4(96, 37, 6, key=(96, 1))
+    x = S.activations(3, 96, key=(96, 2))
+    q, s = o.quantize_act(x)
+    ref = o.linear_i4(q, s, **ws)
+    A = _unpack_np(ws["A4"], 6 * 96).reshape(6, 96)
+    B = _unpack_np(ws["B4"], 37 * 6).reshape(37, 6)
+    acc_s, acc_a, acc_b = bruteforce_int(q, ws["w_bits"], A, B)
+    assert np.array_equal(ref["acc_s"], acc_s) and np.array_equal(ref["acc_a"], acc_a)
+    assert np.array_equal(ref["acc_b"], acc_b)
+
+
+# --------------------------------------------------------------------------
 # Mamba-2 decode step around the linears
 # --------------------------------------------------------------------------
 def _silu64(v):
@@ -695,4 +726,4 @@ ALL_PINS = [pin_f16_decode, pin_quantize_hand_cases, pin_quantize_properties, pi
             pin_bruteforce, pin_popcount_identity, pin_special_bits, pin_permutation, pin_extremes,
             pin_rank0, pin_y32_order, pin_chain, pin_paper_sizes, pin_embed_lm_hand, pin_lm_head_bruteforce,
             pin_lm_head_closed_forms, pin_embed_gather_bruteforce, pin_rmsnorm, pin_conv_step, pin_ssm_step,
-            pin_gate_norm, pin_validation]
+            pin_gate_norm, pin_int4, pin_validation]

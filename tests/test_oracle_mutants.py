@@ -63,6 +63,10 @@ MUTANTS = [
                      ("const float* Cv = c_out + d_inner + N;", "const float* Cv = c_out + d_inner;")]),
     ("norm_no_eps", [("sqrt(ss / (double)d + (double)eps)", "sqrt(ss / (double)d)")]),
     ("norm_sum_not_mean", [("sqrt(ss / (double)d + (double)eps)", "sqrt(ss + (double)eps)")]),
+    ("int4_high_nibble_first", [("const int nib = (i % 2 == 0) ? (byte & 0x0f) : (byte >> 4);",
+                                 "const int nib = (i % 2 == 0) ? (byte >> 4) : (byte & 0x0f);")]),
+    ("int4_unsigned", [("out[i] = (int8_t)(nib >= 8 ? nib - 16 : nib);", "out[i] = (int8_t)nib;")]),
+    ("int4_minus8_as_8", [("out[i] = (int8_t)(nib >= 8 ? nib - 16 : nib);", "out[i] = (int8_t)(nib > 8 ? nib - 16 : nib);")]),
     ("residual_dropped", [("res[k] = delta ? u[m * d + k] + delta[m * d + k] : u[m * d + k];", "res[k] = u[m * d + k];")]),
 ]
 
