@@ -137,6 +137,27 @@ dfssm_status dfssm_scaffold_lora_linear_ex(const int8_t* q, const float* s, int6
                                            int64_t* acc_b, void* workspace,
                                            size_t workspace_bytes, void* stream);
 
+/* The same linear with int4 LoRA factors (Table 4: the scaffold with an
+ * int4 LoRA; the paper gives no format).  Each factor value is a
+ * two's-complement 4-bit integer in [-8, 7], two per byte, value 2i in the
+ * low nibble of byte i:
+ *   A4 [r][K/2] bytes (row j holds A[j, 0..K-1])
+ *   B4 [N][r/2] bytes (row n holds B[n, 0..r-1])
+ * r must be even.  Every other argument, output and result is as in
+ * dfssm_scaffold_lora_linear_ex on the unpacked A and B (the same exact
+ * integers).  The few-token path (M <= 32) reads the packed bytes directly,
+ * half the LoRA bytes of int8; the prefill MFMA and popcount paths first
+ * expand the factors to int8 inside the workspace.  The workspace must hold
+ * dfssm_linear_i4_workspace_bytes(M, K, N, r) bytes.
+ * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */
+size_t dfssm_linear_i4_workspace_bytes(int64_t M, int64_t K, int64_t N, int64_t r);
+dfssm_status dfssm_scaffold_lora_linear_i4(const int8_t* q, const float* s, int64_t M, int64_t K,
+                                           int64_t N, int64_t r, const uint32_t* w_bits,
+                                           const float* alpha, const uint8_t* A4, const uint8_t* B4,
+                                           const float* beta, float* y, int path, int32_t* acc_s,
+                                           int32_t* acc_a, int64_t* acc_b, void* workspace,
+                                           size_t workspace_bytes, void* stream);
+
 /* One projection of a chain (host struct; the pointers in it are device
  * pointers with the layouts above). */
 typedef struct {

@@ -23,7 +23,8 @@ EXPORTS = ["dfssm_quantize_act", "dfssm_linear_workspace_bytes", "dfssm_scaffold
            "dfssm_scaffold_lora_linear_ex", "dfssm_chain_workspace_bytes",
            "dfssm_scaffold_lora_chain", "dfssm_chain_prepare", "dfssm_chain_run", "dfssm_chain_status",
            "dfssm_embed_gather", "dfssm_lm_head", "dfssm_add_rmsnorm_quant", "dfssm_gate_norm_quant",
-           "dfssm_ssm_step", "dfssm_mamba2_state_bytes", "dfssm_mamba2_workspace_bytes",
+           "dfssm_ssm_step", "dfssm_linear_i4_workspace_bytes", "dfssm_scaffold_lora_linear_i4",
+           "dfssm_mamba2_state_bytes", "dfssm_mamba2_workspace_bytes",
            "dfssm_mamba2_decode_step", "dfssm_status_string", "dfssm_last_error", "dfssm_version"]
 
 
@@ -90,6 +91,11 @@ def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dfssm_gate_norm_quant.restype = i32
     lib.dfssm_ssm_step.argtypes = [vp, i64, i64, i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.dfssm_ssm_step.restype = i32
+    lib.dfssm_linear_i4_workspace_bytes.argtypes = [i64, i64, i64, i64]
+    lib.dfssm_linear_i4_workspace_bytes.restype = sz
+    lib.dfssm_scaffold_lora_linear_i4.argtypes = [vp, vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, i32,
+                                                  vp, vp, vp, vp, sz, vp]
+    lib.dfssm_scaffold_lora_linear_i4.restype = i32
     mp = ctypes.POINTER(Mamba2Model)
     lib.dfssm_mamba2_state_bytes.argtypes = [mp, i64, ctypes.POINTER(sz), ctypes.POINTER(sz)]
     lib.dfssm_mamba2_state_bytes.restype = i32
@@ -424,3 +430,40 @@ def _proj(w) -> Layer:
     return Layer(w["w_bits"].data_ptr(), w["alpha"].data_ptr(), _ptr(w.get("A")) if r else None,
                  _ptr(w.get("B")) if r else None, _ptr(w.get("beta")) if r else None, w["w_bits"].shape[1] * 32,
                  w["w_bits"].shape[0], r)
+
+
+def scaffold_lora_linear_i4(q, s, w_bits, alpha, A4=None, B4=None, beta=None, y=None, workspace=None,
+                            path: int = PATH_AUTO, acc: bool = False, stream=None):
+    """The linear with int4 LoRA factors: A4 uint8 [r, K/2], B4 uint8 [N, r/2]
+    (two's-complement nibbles, low nibble first).  Same results as
+    scaffold_lora_linear on the unpacked factors."""
+    torch = _torch()
+    M, K = q.shape
+    N = w_bits.shape[0]
+    r = 0 if A4 is None else A4.shape[0]
+    _need(q, torch.int8, "q", 2)
+    _need(s, torch.float32, "s", 1)
+    _need(alpha, torch.float32, "alpha", 1)
+    if r:
+        _need(A4, torch.uint8, "A4", 2)
+        _need(B4, torch.uint8, "B4", 2)
+        _need(beta, torch.float32, "beta", 1)
+        if tuple(A4.shape) != (r, K // 2) or tuple(B4.shape) != (N, r // 2):
+            raise ValueError("A4 must be [r, K/2] and B4 [N, r/2] bytes")
+    dev = q.device
+    y = torch.empty((M, N), dtype=torch.float32, device=dev) if y is None else y
+    nbytes = int(lib.dfssm_linear_i4_workspace_bytes(M, K, N, r))
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    acc_s = acc_a = acc_b = None
+    if acc:
+        acc_s = torch.empty((M, N), dtype=torch.int32, device=dev)
+        acc_a = torch.empty((M, max(r, 1)), dtype=torch.int32, device=dev)
+        acc_b = torch.empty((M, N), dtype=torch.int64, device=dev)
+    _check(lib.dfssm_scaffold_lora_linear_i4(
+        q.data_ptr(), s.data_ptr(), M, K, N, r, w_bits.data_ptr(), alpha.data_ptr(), _ptr(A4) if r else None,
+        _ptr(B4) if r else None, _ptr(beta) if r else None, y.data_ptr(), path, _ptr(acc_s),
+        _ptr(acc_a) if r else None, _ptr(acc_b), workspace.data_ptr(), workspace.numel(), _stream(stream)))
+    if acc:
+        return y, acc_s, acc_a[:, :r], acc_b
+    return y

@@ -12,6 +12,7 @@
 #include <vector>
 
 #include "dfssm_internal.hpp"
+#include "dfssm_int4.hpp"
 #include "dfssm_mamba.hpp"
 
 namespace {
@@ -170,6 +171,63 @@ dfssm_status dfssm_scaffold_lora_linear_ex(const int8_t* q, const float* s, int6
   hipError_t e = launch_linear(path, q, s, M, K, N, r, w_bits, alpha, A, B, beta, y, acc_s, acc_a, acc_b, ws,
                                (hipStream_t)stream);
   return e == hipSuccess ? DFSSM_OK : device_fail(e, "linear launch");
+}
+
+size_t dfssm_linear_i4_workspace_bytes(int64_t M, int64_t K, int64_t N, int64_t r) {
+  if (M < 0 || K <= 0 || N < 0 || r < 0) return 0;
+  return dfssm::linear_i4_workspace_bytes(M, K, N, r);
+}
+
+dfssm_status dfssm_scaffold_lora_linear_i4(const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N,
+                                           int64_t r, const uint32_t* w_bits, const float* alpha,
+                                           const uint8_t* A4, const uint8_t* B4, const float* beta, float* y,
+                                           int path, int32_t* acc_s, int32_t* acc_a, int64_t* acc_b,
+                                           void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  dfssm_status st = check_linear(M, K, N, r);
+  if (st != DFSSM_OK) return st;
+  if (r % 2 != 0) return fail(DFSSM_ERR_SHAPE, "r=%lld must be even for packed int4 factors", (long long)r);
+  if (path != DFSSM_PATH_AUTO && path != DFSSM_PATH_DECODE && path != DFSSM_PATH_MFMA &&
+      path != DFSSM_PATH_MFMA_FEW)
+    return fail(DFSSM_ERR_SHAPE, "path=%d", path);
+  if (path == DFSSM_PATH_MFMA_FEW && M > dfssm::kSkinnyMaxTokens)
+    return fail(DFSSM_ERR_UNSUPPORTED, "path=%d takes M <= %lld, got M=%lld", path,
+                (long long)dfssm::kSkinnyMaxTokens, (long long)M);
+  if (M == 0 || N == 0) return DFSSM_OK;
+  st = check_ptrs({{q, "q"}, {s, "s"}, {w_bits, "w_bits"}, {alpha, "alpha"}, {workspace, "workspace"}},
+                  {{y, "y"}, {acc_s, "acc_s"}, {acc_a, "acc_a"}, {acc_b, "acc_b"}});
+  if (st != DFSSM_OK) return st;
+  if (r > 0) {
+    st = check_ptrs({{A4, "A4"}, {B4, "B4"}, {beta, "beta"}}, {});
+    if (st != DFSSM_OK) return st;
+  }
+  const size_t need = dfssm::linear_i4_workspace_bytes(M, K, N, r);
+  if (workspace_bytes < need)
+    return fail(DFSSM_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, need);
+  const hipStream_t hs = (hipStream_t)stream;
+  dfssm::LinearWorkspace ws = dfssm::carve_linear_workspace(workspace, M, K, r);
+  if (path == DFSSM_PATH_AUTO)
+    path = M <= dfssm::kDecodeM0 ? DFSSM_PATH_DECODE
+                                 : (M <= dfssm::kSkinnyMaxTokens ? DFSSM_PATH_MFMA_FEW : DFSSM_PATH_MFMA);
+  hipError_t e;
+  if (path == DFSSM_PATH_MFMA_FEW || r == 0) {
+    if (path == DFSSM_PATH_MFMA_FEW)
+      e = dfssm::launch_skinny_linear_i4(q, s, M, K, N, r, w_bits, alpha, A4, B4, beta, y, acc_s, acc_a, acc_b, ws,
+                                         hs);
+    else
+      e = launch_linear(path, q, s, M, K, N, 0, w_bits, alpha, nullptr, nullptr, nullptr, y, acc_s, acc_a, acc_b,
+                        ws, hs);
+  } else {
+    // the int8 kernels on factors expanded into the workspace
+    char* extra = static_cast<char*>(workspace) + dfssm::linear_i4_extra_offset(M, K, r);
+    int8_t* A8 = reinterpret_cast<int8_t*>(extra);
+    int8_t* B8 = reinterpret_cast<int8_t*>(extra + (((size_t)(r * K) + 255) & ~(size_t)255));
+    e = dfssm::launch_unpack_int4(A4, r * K, A8, hs);
+    if (e == hipSuccess) e = dfssm::launch_unpack_int4(B4, N * r, B8, hs);
+    if (e == hipSuccess)
+      e = launch_linear(path, q, s, M, K, N, r, w_bits, alpha, A8, B8, beta, y, acc_s, acc_a, acc_b, ws, hs);
+  }
+  return e == hipSuccess ? DFSSM_OK : device_fail(e, "int4 linear launch");
 }
 
 dfssm_status dfssm_scaffold_lora_linear(const int8_t* q, const float* s, int64_t M, int64_t K,

@@ -34,7 +34,7 @@
 #include <algorithm>
 #include <atomic>
 
-#include "dfssm_internal.hpp"
+#include "dfssm_int4.hpp"
 
 namespace {
 
@@ -73,6 +73,59 @@ __device__ __forceinline__ v4i load16_guarded(const int8_t* row, int start, int 
     o[e >> 2] |= (int)(b << (8 * (e & 3)));
   }
   return o;
+}
+
+// int4 factors: two's-complement nibbles, value 2i in the low nibble of byte
+// i.  sext_nibbles turns 4 bytes holding nibble values 0..15 into the
+// signed values -8..7 (XOR 8, then a subtraction that cannot borrow across
+// bytes); expand_i4 turns 8 packed bytes into the 16 int8 values in order.
+__device__ __forceinline__ uint32_t sext_nibbles(uint32_t t) {
+  t ^= 0x08080808u;
+  return ((t | 0x80808080u) - 0x08080808u) ^ 0x80808080u;
+}
+
+__device__ __forceinline__ uint4 expand_i4(uint2 p) {
+  const uint32_t lo0 = p.x & 0x0F0F0F0Fu, hi0 = (p.x >> 4) & 0x0F0F0F0Fu;
+  const uint32_t lo1 = p.y & 0x0F0F0F0Fu, hi1 = (p.y >> 4) & 0x0F0F0F0Fu;
+  // v_perm_b32 interleaves the low-nibble and high-nibble bytes
+  return make_uint4(sext_nibbles(__builtin_amdgcn_perm(hi0, lo0, 0x05010400u)),
+                    sext_nibbles(__builtin_amdgcn_perm(hi0, lo0, 0x07030602u)),
+                    sext_nibbles(__builtin_amdgcn_perm(hi1, lo1, 0x05010400u)),
+                    sext_nibbles(__builtin_amdgcn_perm(hi1, lo1, 0x07030602u)));
+}
+
+// values start .. start+15 (start % 16 == 0) of a factor row, in bytes
+// (L4: 8 packed bytes at start/2)
+template <bool L4>
+__device__ __forceinline__ uint4 load_row16(const int8_t* row, int start) {
+  if constexpr (L4) return expand_i4(*reinterpret_cast<const uint2*>(row + start / 2));
+  return *reinterpret_cast<const uint4*>(row + start);
+}
+
+// 16 values of a factor row of len values, zero outside [0, len)
+template <bool L4>
+__device__ __forceinline__ v4i load16_row_guarded(const int8_t* row, int start, int len, bool aligned) {
+  if constexpr (!L4) {
+    return load16_guarded(row, start, len, aligned);
+  } else {
+    if (start + 16 <= len && aligned) {
+      const uint4 u = load_row16<true>(row, start);
+      return v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
+    }
+    v4i o = zero4();
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int i = start + e;
+      uint32_t b = 0u;
+      if (i >= 0 && i < len) {
+        const int byte = (uint8_t)row[i >> 1];
+        const int nib = (i & 1) ? (byte >> 4) : (byte & 15);
+        b = (uint32_t)(uint8_t)(int8_t)(nib >= 8 ? nib - 16 : nib);
+      }
+      o[e >> 2] |= (int)(b << (8 * (e & 3)));
+    }
+    return o;
+  }
 }
 
 constexpr int kMaxWaves = 8;
@@ -129,14 +182,15 @@ __device__ __forceinline__ uint32_t pack_limbs(int32_t v) {
 }
 
 // sum_k A[j,k] Q[m,k] (j < r) or sum_k Q[m,k] (j < 0), one lane alone
+template <bool L4>
 __device__ int lane_dot(const int8_t* __restrict__ A, const int8_t* __restrict__ q, int K, int j, int m) {
   const int8_t* qrow = q + (int64_t)m * K;
-  const int8_t* arow = A + (int64_t)(j < 0 ? 0 : j) * K;
+  const int8_t* arow = A + (int64_t)(j < 0 ? 0 : j) * (L4 ? K / 2 : K);
   int acc = 0;
   for (int k = 0; k < K; k += 16) {
     const uint4 x = *reinterpret_cast<const uint4*>(qrow + k);
     const uint4 w = j < 0 ? make_uint4(0x01010101u, 0x01010101u, 0x01010101u, 0x01010101u)
-                          : *reinterpret_cast<const uint4*>(arow + k);
+                          : load_row16<L4>(arow, k);
     acc = sdot4(w.x, x.x, acc);
     acc = sdot4(w.y, x.y, acc);
     acc = sdot4(w.z, x.z, acc);
@@ -150,6 +204,7 @@ __device__ int lane_dot(const int8_t* __restrict__ A, const int8_t* __restrict__
 // is issued before the first v_dot4.
 constexpr int kPrepTokens = 4;
 constexpr int kPrepBatch = 4;
+template <bool L4>
 __device__ void lora_block(const SkinnyArgs& a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -164,14 +219,14 @@ __device__ void lora_block(const SkinnyArgs& a) {
 #pragma unroll
   for (int m = 0; m < kPrepTokens; ++m) acc[m] = qs[m] = 0;
   if (jr || qsum) {
-    const int8_t* arow = a.A + (int64_t)(jr ? j : 0) * K;
+    const int8_t* arow = a.A + (int64_t)(jr ? j : 0) * (L4 ? K / 2 : K);
     for (int kb = 0; kb < K; kb += 1024 * kPrepBatch) {
       uint4 av[kPrepBatch], x[kPrepTokens][kPrepBatch];
 #pragma unroll
       for (int u = 0; u < kPrepBatch; ++u) {
         const int k = kb + 1024 * u + 16 * lane;
         const bool ok = k < K;  // K % 32 == 0: a 16-byte chunk is wholly in or out
-        av[u] = (jr && ok) ? *reinterpret_cast<const uint4*>(arow + k) : make_uint4(0, 0, 0, 0);
+        av[u] = (jr && ok) ? load_row16<L4>(arow, k) : make_uint4(0, 0, 0, 0);
 #pragma unroll
         for (int m = 0; m < kPrepTokens; ++m)
           x[m][u] = (ok && m < mt) ? *reinterpret_cast<const uint4*>(a.q + (int64_t)(m0 + m) * K + k)
@@ -217,6 +272,7 @@ __device__ void lora_block(const SkinnyArgs& a) {
 // The limbs of acc_a[m][j0 + 16kg .. +15] as 4 limb operands (byte e of limb
 // t = limb t of rank j0 + 16kg + e) and, with want_sq, sum Q of token m: from
 // the LoRA workgroups' words, or computed here once `spin` polls have passed.
+template <bool L4>
 __device__ void fetch_lora(const SkinnyArgs& a, int m, int j0, int kg, v4i (&lm)[4], int* sq, bool store_acc) {
   const uint64_t* wp = a.xw + (int64_t)m * a.rp + j0 + 16 * kg;
   const uint64_t* sp = a.xw + (int64_t)a.M * a.rp + m;
@@ -246,11 +302,11 @@ __device__ void fetch_lora(const SkinnyArgs& a, int m, int j0, int kg, v4i (&lm)
 #pragma unroll 1
     for (int e = 0; e < 16; ++e) {
       const int j = j0 + 16 * kg + e;
-      const int v = j < a.r ? lane_dot(a.A, a.q, a.K, j, m) : 0;
+      const int v = j < a.r ? lane_dot<L4>(a.A, a.q, a.K, j, m) : 0;
       val[e] = pack_limbs(v);
       if (store_acc && j < a.r) a.acc_a[(int64_t)m * a.r + j] = v;
     }
-    if (sq) vq = (uint32_t)lane_dot(a.A, a.q, a.K, -1, m);
+    if (sq) vq = (uint32_t)lane_dot<L4>(a.A, a.q, a.K, -1, m);
   }
 #pragma unroll
   for (int t = 0; t < 4; ++t)
@@ -267,11 +323,11 @@ __device__ void fetch_lora(const SkinnyArgs& a, int m, int j0, int kg, v4i (&lm)
 // MT token tiles of 16 (M <= 16*MT); S MFMA steps per lane per iteration.
 // Block: 16 output rows, nw = blockDim.x / 64 waves (nw >= MT), wave w takes
 // iterations w, w + nw, ... of 64*S columns each.
-template <int MT, int S>
+template <int MT, int S, bool L4>
 __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   __shared__ v4i red[kMaxWaves][MT][64];
   if ((int)blockIdx.x < a.nb_lora) {
-    lora_block(a);
+    lora_block<L4>(a);
     return;
   }
   constexpr int KW = 64 * S;  // columns per wave iteration
@@ -294,11 +350,12 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   const int mc = min(mtok, M - 1);
   const int nb = n0 + 4 * kg;  // this lane's output rows nb .. nb+3
   const bool ba = (r % 16) == 0;
+  const int64_t bpitch = L4 ? r / 2 : r;  // bytes per B row
   v4i bop = zero4();
   float alv[4] = {0.f, 0.f, 0.f, 0.f}, bev[4] = {0.f, 0.f, 0.f, 0.f};
   float sm = 0.f;
   if (fin) {
-    if (r > 0) bop = load16_guarded(a.B + (int64_t)nrow * r, 16 * kg, r, ba);
+    if (r > 0) bop = load16_row_guarded<L4>(a.B + (int64_t)nrow * bpitch, 16 * kg, r, ba);
     if ((N & 3) == 0 && nb + 3 < N) {
       const float4 al4 = *reinterpret_cast<const float4*>(a.alpha + nb);
       alv[0] = al4.x; alv[1] = al4.y; alv[2] = al4.z; alv[3] = al4.w;
@@ -371,7 +428,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   v4i lm[4];
   int sq = 0;
   const bool keep = blockIdx.x == a.nb_lora && mtok < M;
-  fetch_lora(a, mc, 0, kg, lm, &sq, keep);
+  fetch_lora<L4>(a, mc, 0, kg, lm, &sq, keep);
 
   // LoRA up-projection, limbs 3, 2, 1, 0 over the 64-rank chunks
   v4i ehi = zero4(), elo = zero4();
@@ -379,9 +436,9 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
     v4i e3 = mfma(bop, lm[3], zero4()), e2 = mfma(bop, lm[2], zero4());
     v4i e1 = mfma(bop, lm[1], zero4()), e0 = mfma(bop, lm[0], zero4());
     for (int j0 = 64; j0 < a.rp; j0 += 64) {
-      const v4i bl = load16_guarded(a.B + (int64_t)nrow * r, j0 + 16 * kg, r, ba);
+      const v4i bl = load16_row_guarded<L4>(a.B + (int64_t)nrow * bpitch, j0 + 16 * kg, r, ba);
       v4i lj[4];
-      fetch_lora(a, mc, j0, kg, lj, nullptr, keep);
+      fetch_lora<L4>(a, mc, j0, kg, lj, nullptr, keep);
       e3 = mfma(bl, lj[3], e3);
       e2 = mfma(bl, lj[2], e2);
       e1 = mfma(bl, lj[1], e1);
@@ -415,10 +472,10 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   }
 }
 
-template <int MT, int S>
+template <int MT, int S, bool L4>
 hipError_t launch_t(const SkinnyArgs& a, int nw, hipStream_t st) {
   const int64_t blocks = a.nb_lora + dfssm::ceil_div(a.N, 16);
-  mfma_skinny<MT, S><<<dim3((unsigned)blocks), dim3(64 * nw), 0, st>>>(a);
+  mfma_skinny<MT, S, L4><<<dim3((unsigned)blocks), dim3(64 * nw), 0, st>>>(a);
   return hipGetLastError();
 }
 
@@ -434,13 +491,16 @@ uint32_t next_tag() {
 
 }  // namespace
 
-namespace dfssm {
+namespace {
 
-hipError_t launch_skinny_linear(const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N,
-                                int64_t r, const uint32_t* w_bits, const float* alpha,
-                                const int8_t* A, const int8_t* B, const float* beta, float* y,
-                                int32_t* acc_s, int32_t* acc_a_out, int64_t* acc_b,
-                                const LinearWorkspace& ws, hipStream_t st) {
+using dfssm::ceil_div;
+
+template <bool L4>
+hipError_t skinny_impl(const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N, int64_t r,
+                       const uint32_t* w_bits, const float* alpha, const int8_t* A, const int8_t* B,
+                       const float* beta, float* y, int32_t* acc_s, int32_t* acc_a_out, int64_t* acc_b,
+                       const dfssm::LinearWorkspace& ws, hipStream_t st) {
+  using namespace dfssm;
   if (M == 0 || N == 0) return hipSuccess;
   if (M > kSkinnyMaxTokens) return hipErrorInvalidValue;
   const int rp = (int)rank_padded(r);
@@ -461,13 +521,34 @@ hipError_t launch_skinny_linear(const int8_t* q, const float* s, int64_t M, int6
                ws.acc_a, ws.xw, next_tag(), nb_lora, local_only ? 0 : (1 << 14)};
   hipError_t e;
   if (mt == 1)
-    e = S == 8 ? launch_t<1, 8>(a, nw, st) : launch_t<1, 4>(a, nw, st);
+    e = S == 8 ? launch_t<1, 8, L4>(a, nw, st) : launch_t<1, 4, L4>(a, nw, st);
   else
-    e = S == 8 ? launch_t<2, 8>(a, nw, st) : launch_t<2, 4>(a, nw, st);
+    e = S == 8 ? launch_t<2, 8, L4>(a, nw, st) : launch_t<2, 4, L4>(a, nw, st);
   if (e != hipSuccess) return e;
   if (acc_a_out && r > 0)
     e = hipMemcpyAsync(acc_a_out, ws.acc_a, (size_t)(M * r) * 4, hipMemcpyDeviceToDevice, st);
   return e;
+}
+
+}  // namespace
+
+namespace dfssm {
+
+hipError_t launch_skinny_linear(const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N,
+                                int64_t r, const uint32_t* w_bits, const float* alpha,
+                                const int8_t* A, const int8_t* B, const float* beta, float* y,
+                                int32_t* acc_s, int32_t* acc_a_out, int64_t* acc_b,
+                                const LinearWorkspace& ws, hipStream_t st) {
+  return skinny_impl<false>(q, s, M, K, N, r, w_bits, alpha, A, B, beta, y, acc_s, acc_a_out, acc_b, ws, st);
+}
+
+hipError_t launch_skinny_linear_i4(const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N,
+                                   int64_t r, const uint32_t* w_bits, const float* alpha,
+                                   const uint8_t* A4, const uint8_t* B4, const float* beta, float* y,
+                                   int32_t* acc_s, int32_t* acc_a_out, int64_t* acc_b,
+                                   const LinearWorkspace& ws, hipStream_t st) {
+  return skinny_impl<true>(q, s, M, K, N, r, w_bits, alpha, reinterpret_cast<const int8_t*>(A4),
+                           reinterpret_cast<const int8_t*>(B4), beta, y, acc_s, acc_a_out, acc_b, ws, st);
 }
 
 }  // namespace dfssm

@@ -200,6 +200,23 @@ def test_model_step_validation(dl):
     assert dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1) > 0
 
 
+def test_int4_linear_validation(dl):
+    f = dl.lib.dfssm_scaffold_lora_linear_i4   # q, s, M, K, N, r, w, alpha, A4, B4, beta, y, path, acc*3, ws, bytes, stream
+
+    def lin(M=1, K=64, N=8, r=4, A4=16, path=0, wsb=1 << 20, y=16):
+        return f(16, 16, M, K, N, r, 16, 16, A4, 16, 16, y, path, None, None, None, 16, wsb, None)
+    assert lin(r=5) == dl.ERR_SHAPE                 # odd rank: half a byte
+    assert lin(K=48) == dl.ERR_SHAPE
+    assert lin(A4=None) == dl.ERR_NULL
+    assert lin(A4=24) == dl.ERR_ALIGN
+    assert lin(path=9) == dl.ERR_SHAPE
+    assert lin(M=33, path=3) == dl.ERR_UNSUPPORTED
+    need = dl.lib.dfssm_linear_i4_workspace_bytes(1, 64, 8, 4)
+    assert need > dl.linear_workspace_bytes(1, 64, 8, 4)
+    assert lin(wsb=need - 1) == dl.ERR_WORKSPACE
+    assert lin(M=0) == dl.OK
+
+
 def test_workspace_sizes(dl):
     a = dl.linear_workspace_bytes(1, 2048, 8512, 64)
     b = dl.linear_workspace_bytes(2048, 2048, 8512, 64)
