@@ -246,7 +246,49 @@ def main():
                 us = t0.elapsed_time(t1) * 1e3 / (reps * ncall)
                 decode.append({"workload": f"{name} M={m}", "us_per_call": round(us, 2),
                                "weight_gbs": round(wb / (us * 1e-6) / 1e9, 1), "weight_bytes": wb,
-                               "path": "few-token MFMA (one launch)"})
+                               "path": "few-token MFMA (one launch)", "lora": "int8"})
+                del g
+            del cps, base
+        # the same projections with int4 LoRA factors (packed bytes read by
+        # the few-token kernel), same method
+        for cfg, name, Ms in ((1, "Mamba-2-1.3B in_proj K=2048 N=8512 r=64", (1,)),
+                              (2, "Mamba-2-1.3B out_proj K=4096 N=2048 r=64", (1, 32))):
+            c = S.CONFIGS[cfg]
+            hw = S.weights_i4(c.K, c.N, c.r, key=(cfg, 0, 0, 4))
+            wb = int(sum(hw[k].nbytes for k in ("w_bits", "alpha", "A4", "B4", "beta")))
+            base = {k: dev(v) for k, v in hw.items()}
+            ncall = int(np.ceil(600e6 / wb))
+            cps = [base] + [{k: v.clone() for k, v in base.items()} for _ in range(ncall - 1)]
+            for m in Ms:
+                qd, sd = D.quantize_act(dev(S.config_activations(cfg, m)))
+                yd = torch.empty((m, c.N), dtype=torch.float32, device="cuda")
+                wsd = torch.empty(int(D.lib.dfssm_linear_i4_workspace_bytes(m, c.K, c.N, c.r)), dtype=torch.uint8,
+                                  device="cuda")
+
+                def calls4():
+                    for cc in cps:
+                        D.scaffold_lora_linear_i4(qd, sd, cc["w_bits"], cc["alpha"], cc["A4"], cc["B4"], cc["beta"],
+                                                  y=yd, workspace=wsd)
+                side = torch.cuda.Stream()
+                side.wait_stream(torch.cuda.current_stream())
+                with torch.cuda.stream(side):
+                    calls4()
+                    g = torch.cuda.CUDAGraph()
+                    with torch.cuda.graph(g, stream=side):
+                        calls4()
+                torch.cuda.synchronize()
+                g.replay()
+                torch.cuda.synchronize()
+                reps = 3
+                t0.record(stream)
+                for _ in range(reps):
+                    g.replay()
+                t1.record(stream)
+                torch.cuda.synchronize()
+                us = t0.elapsed_time(t1) * 1e3 / (reps * ncall)
+                decode.append({"workload": f"{name} M={m}", "us_per_call": round(us, 2),
+                               "weight_gbs": round(wb / (us * 1e-6) / 1e9, 1), "weight_bytes": wb,
+                               "path": "few-token MFMA (one launch)", "lora": "int4"})
                 del g
             del cps, base
 

@@ -221,19 +221,26 @@ __device__ void lora_block(const SkinnyArgs& a) {
   if (jr || qsum) {
     const int8_t* arow = a.A + (int64_t)(jr ? j : 0) * (L4 ? K / 2 : K);
     for (int kb = 0; kb < K; kb += 1024 * kPrepBatch) {
+      // int4: the packed bytes are kept as loaded and expanded at their use,
+      // so no expansion waits on a load before the batch's last load issues
       uint4 av[kPrepBatch], x[kPrepTokens][kPrepBatch];
+      uint2 araw[kPrepBatch];
 #pragma unroll
       for (int u = 0; u < kPrepBatch; ++u) {
         const int k = kb + 1024 * u + 16 * lane;
         const bool ok = k < K;  // K % 32 == 0: a 16-byte chunk is wholly in or out
-        av[u] = (jr && ok) ? load_row16<L4>(arow, k) : make_uint4(0, 0, 0, 0);
+        if constexpr (L4)
+          araw[u] = (jr && ok) ? *reinterpret_cast<const uint2*>(arow + k / 2) : make_uint2(0, 0);
+        else
+          av[u] = (jr && ok) ? load_row16<false>(arow, k) : make_uint4(0, 0, 0, 0);
 #pragma unroll
         for (int m = 0; m < kPrepTokens; ++m)
           x[m][u] = (ok && m < mt) ? *reinterpret_cast<const uint4*>(a.q + (int64_t)(m0 + m) * K + k)
                                    : make_uint4(0, 0, 0, 0);
       }
 #pragma unroll
-      for (int u = 0; u < kPrepBatch; ++u)
+      for (int u = 0; u < kPrepBatch; ++u) {
+        if constexpr (L4) av[u] = expand_i4(araw[u]);
 #pragma unroll
         for (int m = 0; m < kPrepTokens; ++m) {
           acc[m] = sdot4(av[u].x, x[m][u].x, acc[m]);
@@ -247,6 +254,7 @@ __device__ void lora_block(const SkinnyArgs& a) {
             qs[m] = sdot4(0x01010101u, x[m][u].w, qs[m]);
           }
         }
+      }
     }
   }
   int mine = 0, mine_q = 0;
@@ -351,11 +359,22 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   const int nb = n0 + 4 * kg;  // this lane's output rows nb .. nb+3
   const bool ba = (r % 16) == 0;
   const int64_t bpitch = L4 ? r / 2 : r;  // bytes per B row
+  // int4: the packed B bytes are held as loaded and expanded after the
+  // scaffold loop, so the loop's loads do not wait for them
   v4i bop = zero4();
+  uint2 braw = make_uint2(0, 0);
+  bool bpacked = false;
   float alv[4] = {0.f, 0.f, 0.f, 0.f}, bev[4] = {0.f, 0.f, 0.f, 0.f};
   float sm = 0.f;
   if (fin) {
-    if (r > 0) bop = load16_row_guarded<L4>(a.B + (int64_t)nrow * bpitch, 16 * kg, r, ba);
+    if (r > 0) {
+      if (L4 && 16 * kg + 16 <= r && ba) {
+        braw = *reinterpret_cast<const uint2*>(a.B + (int64_t)nrow * bpitch + 8 * kg);
+        bpacked = true;
+      } else {
+        bop = load16_row_guarded<L4>(a.B + (int64_t)nrow * bpitch, 16 * kg, r, ba);
+      }
+    }
     if ((N & 3) == 0 && nb + 3 < N) {
       const float4 al4 = *reinterpret_cast<const float4*>(a.alpha + nb);
       alv[0] = al4.x; alv[1] = al4.y; alv[2] = al4.z; alv[3] = al4.w;
@@ -431,6 +450,16 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   fetch_lora<L4>(a, mc, 0, kg, lm, &sq, keep);
 
   // LoRA up-projection, limbs 3, 2, 1, 0 over the 64-rank chunks
+  if (L4 && bpacked) {
+    // an opaque zero made after the polls: the expansion cannot be moved in
+    // front of them, where it would wait for the B load before the first poll
+    uint32_t z;
+    asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+    braw.x ^= z;
+    braw.y ^= z;
+    const uint4 u = expand_i4(braw);
+    bop = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
+  }
   v4i ehi = zero4(), elo = zero4();
   if (r > 0) {
     v4i e3 = mfma(bop, lm[3], zero4()), e2 = mfma(bop, lm[2], zero4());
