@@ -180,8 +180,8 @@ hipError_t launch_norm(const NormArgs& a, int64_t M, hipStream_t st) {
 
 // ---------------------------------------------------------------- SSM step
 constexpr int kHeadDim = 64;      // P
+constexpr int kSsmThreads = 256;
 constexpr int kPBlock = 16;       // channels of a head per workgroup
-constexpr int kSsmThreads = 256;  // 16 channels x 16 lanes over the state
 
 struct SsmArgs {
   const float* zx;    // [M][ld]: z | xBC | dt
@@ -199,19 +199,21 @@ struct SsmArgs {
   float* xbc;         // [M][conv_dim] or null
 };
 
-// Workgroup (m, h, pb): channels p = 16 pb .. 16 pb + 15 of head h.  Thread
-// t holds channel p = 16 pb + t/16 and state columns n = (t%16) N/16 ..
-// +N/16 - 1; its row of 16 lanes sums y[p] over the state.
-template <int N>
-__global__ __launch_bounds__(kSsmThreads) void ssm_step(SsmArgs a) {
-  constexpr int NPL = N / 16;  // state columns per lane
-  const int nblk = a.H * (kHeadDim / kPBlock);
+// Workgroup (m, h, pb): PB channels p = PB pb .. PB pb + PB - 1 of head h.
+// Thread t holds channel PB pb + t / TPC and NPL consecutive state columns;
+// its TPC lanes sum y[p] over the state.
+template <int N, int PB, int NT = kSsmThreads>
+__global__ __launch_bounds__(NT) void ssm_step(SsmArgs a) {
+  constexpr int TPC = NT / PB;           // threads per channel
+  constexpr int NPL = N / TPC;           // state columns per thread
+  constexpr int NBH = kHeadDim / PB;     // workgroups per head
+  const int nblk = a.H * NBH;
   const int64_t m = blockIdx.x / nblk;
   const int hb = blockIdx.x % nblk;
-  const int h = hb / (kHeadDim / kPBlock);
-  const int p0 = (hb % (kHeadDim / kPBlock)) * kPBlock;
+  const int h = hb / NBH;
+  const int p0 = (hb % NBH) * PB;
   const int tid = threadIdx.x;
-  const int pl = tid >> 4, nc = tid & 15;
+  const int pl = tid / TPC, nc = tid % TPC;
   const int conv_dim = a.d_inner + 2 * N;
   const float* zr = a.zx + m * a.ld;
 
@@ -221,14 +223,15 @@ __global__ __launch_bounds__(kSsmThreads) void ssm_step(SsmArgs a) {
 #pragma unroll
   for (int j = 0; j < NPL / 4; ++j) hv[j] = reinterpret_cast<const float4*>(hs)[j];
 
-  // convolution step for this workgroup's 16 x channels and all B, C channels
-  __shared__ float xbc_s[kPBlock + 2 * N];
+  // convolution step for this workgroup's PB x channels and all B, C channels
+  __shared__ float xbc_s[PB + 2 * N];
+  __shared__ float dt_s[2];
   const bool owns_bc = (hb == 0);
   float* ring = a.ring + m * 4 * (int64_t)conv_dim;
   const int s0 = (int)((a.step + 1) & 3), s1 = (int)((a.step + 2) & 3), s2 = (int)((a.step + 3) & 3);
   const int sw = (int)(a.step & 3);
-  for (int i = tid; i < kPBlock + 2 * N; i += kSsmThreads) {
-    const int c = i < kPBlock ? h * kHeadDim + p0 + i : a.d_inner + (i - kPBlock);
+  for (int i = tid; i < PB + 2 * N; i += NT) {
+    const int c = i < PB ? h * kHeadDim + p0 + i : a.d_inner + (i - PB);
     const float in = zr[a.d_inner + c];
     const float4 w = *reinterpret_cast<const float4*>(a.conv_w + 4 * (int64_t)c);
     float v = w.x * ring[s0 * (int64_t)conv_dim + c];
@@ -238,20 +241,28 @@ __global__ __launch_bounds__(kSsmThreads) void ssm_step(SsmArgs a) {
     v = v + a.conv_b[c];
     const float o = silu_f(v);
     xbc_s[i] = o;
-    if (i < kPBlock || owns_bc) {
+    if (i < PB || owns_bc) {
       ring[sw * (int64_t)conv_dim + c] = in;
       if (a.xbc) a.xbc[m * conv_dim + c] = o;
     }
   }
-  const float dt = softplus_f(zr[a.d_inner + conv_dim + h] + a.dt_bias[h]);
-  const float A = (float)(-exp((double)a.A_log[h]));
-  const float dA = (float)exp((double)(dt * A));
+  // dt and dA once per workgroup, by the last wave (the one with the least
+  // convolution work), through LDS
+  if (tid >= NT - 64) {
+    const float dt = softplus_f(zr[a.d_inner + conv_dim + h] + a.dt_bias[h]);
+    const float A = (float)(-exp((double)a.A_log[h]));
+    if (tid == NT - 64) {
+      dt_s[0] = dt;
+      dt_s[1] = (float)exp((double)(dt * A));
+    }
+  }
   __syncthreads();
+  const float dt = dt_s[0], dA = dt_s[1];
 
   const float x = xbc_s[pl];
   const float dtx = dt * x;
-  const float* Bs = xbc_s + kPBlock + nc * NPL;
-  const float* Cs = xbc_s + kPBlock + N + nc * NPL;
+  const float* Bs = xbc_s + PB + nc * NPL;
+  const float* Cs = xbc_s + PB + N + nc * NPL;
   double acc = 0.0;
 #pragma unroll
   for (int j = 0; j < NPL / 4; ++j) {
@@ -265,8 +276,16 @@ __global__ __launch_bounds__(kSsmThreads) void ssm_step(SsmArgs a) {
     }
     reinterpret_cast<float4*>(hs)[j] = make_float4(e[0], e[1], e[2], e[3]);
   }
-  acc = sum_lanes<16>(acc);
+  acc = sum_lanes<TPC>(acc);
   if (nc == 0) a.y[m * a.d_inner + h * kHeadDim + p0 + pl] = (float)(acc + (double)a.D[h] * (double)x);
+}
+
+template <int N>
+void launch_ssm_n(const SsmArgs& a, int64_t M, hipStream_t st) {
+  // 16 channels per workgroup at every batch: 8 channels, and a whole head
+  // on 256 or 1024 threads (4x fewer repeats of the shared B/C convolution),
+  // all measured the same or slower on the 1.3B decode step
+  ssm_step<N, kPBlock><<<dim3((unsigned)(M * a.H * (kHeadDim / kPBlock))), dim3(kSsmThreads), 0, st>>>(a);
 }
 
 }  // namespace
@@ -294,11 +313,10 @@ hipError_t launch_ssm_step(const float* zx, int64_t ld, int64_t M, int64_t d_inn
   if (M == 0) return hipSuccess;
   const int H = (int)(d_inner / kHeadDim);
   SsmArgs a{zx, ld, (int)d_inner, H, step, ring, conv_w, conv_b, dt_bias, A_log, D, state, y, xbc};
-  dim3 grid((unsigned)(M * H * (kHeadDim / kPBlock))), block(kSsmThreads);
   if (d_state == 128)
-    ssm_step<128><<<grid, block, 0, st>>>(a);
+    launch_ssm_n<128>(a, M, st);
   else
-    ssm_step<64><<<grid, block, 0, st>>>(a);
+    launch_ssm_n<64>(a, M, st);
   return hipGetLastError();
 }
 
