@@ -76,8 +76,10 @@ typedef enum { DFSSM_F16 = 0, DFSSM_F32 = 1 } dfssm_dtype;
 
 /* Kernel family selection for dfssm_scaffold_lora_linear_ex. */
 typedef enum {
-  DFSSM_PATH_AUTO = 0,     /* few-token MFMA for M <= 32, prefill MFMA
-                              above */
+  DFSSM_PATH_AUTO = 0,     /* few-token MFMA for M <= 32, and above in
+                              32-token chunks while
+                              ceil(M/32) * ceil(N/16) * K/2048 <= 2048;
+                              prefill MFMA otherwise */
   DFSSM_PATH_DECODE = 1,   /* bit-plane popcount GEMV (any M, best for M <= 4) */
   DFSSM_PATH_MFMA = 2,     /* sign bits expanded on chip + int8 MFMA, tiles of
                               128 tokens (prefill): an 8-wave ping-pong
@@ -85,11 +87,11 @@ typedef enum {
                               tiles of 16, a 4-wave kernel otherwise.  Test
                               switch: DFSSM_TEST_PREFILL_KERNEL=4 or 8 in the
                               environment forces one of them. */
-  DFSSM_PATH_MFMA_FEW = 3  /* the same expansion and MFMA for M <= 32 in one
-                              launch: 16 output rows per workgroup, K split
-                              over its waves, the LoRA down-projection in
-                              workgroups of the same grid; M > 32 gives
-                              DFSSM_ERR_UNSUPPORTED.  Test switch: with the
+  DFSSM_PATH_MFMA_FEW = 3  /* the same expansion and MFMA for M <= 512 in
+                              one launch: 16 output rows and 32 tokens per
+                              workgroup, K split over its waves, the LoRA
+                              down-projection in workgroups of the same
+                              grid; M > 512 gives DFSSM_ERR_UNSUPPORTED.  Test switch: with the
                               environment variable DFSSM_TEST_LOCAL_LORA=1
                               no LoRA workgroups run and every output
                               workgroup computes those values itself (the

@@ -94,6 +94,9 @@ hipError_t launch_decode_linear(const int8_t* q, const float* s, int64_t M, int6
 // split-K expanded-sign int8 MFMA product over 16 output rows each, then the
 // LoRA up-projection and epilogue.
 constexpr int64_t kSkinnyMaxTokens = 32;
+// Largest M the few-token kernel takes on request: its output blocks then
+// take one 32-token chunk each (a second grid dimension).
+constexpr int64_t kSkinnyChunkedMaxTokens = 512;
 hipError_t launch_skinny_linear(const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N,
                                 int64_t r, const uint32_t* w_bits, const float* alpha,
                                 const int8_t* A, const int8_t* B, const float* beta, float* y,

@@ -335,7 +335,7 @@ template <int MT, int S, bool L4>
 __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   __shared__ v4i red[kMaxWaves][MT][64];
   if ((int)blockIdx.x < a.nb_lora) {
-    lora_block<L4>(a);
+    if (blockIdx.y == 0) lora_block<L4>(a);  // one set of LoRA workgroups for all tokens
     return;
   }
   constexpr int KW = 64 * S;  // columns per wave iteration
@@ -346,6 +346,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   const int rho = lane & 15, kg = lane >> 4;
   const int M = a.M, K = a.K, N = a.N, r = a.r, W = K >> 5;
   const int n0 = 16 * ((int)blockIdx.x - a.nb_lora);
+  const int mb = 32 * (int)blockIdx.y;  // first token of this block's chunk (row y of the grid)
   const int nrow = min(n0 + rho, N - 1);  // sign / B row of this lane (rows past N are never stored)
   const uint32_t* wrow = a.w_bits + (int64_t)nrow * W;
   const int nit = (K + KW - 1) / KW;
@@ -354,7 +355,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   // ---- the row operands of the wave that finishes token tile `wave` go
   //      out first: B bytes of ranks 0..63, row scales, token scales
   const bool fin = wave < MT;
-  const int mtok = 16 * wave + rho;  // token of this lane in the finished tile
+  const int mtok = mb + 16 * wave + rho;  // token of this lane in the finished tile
   const int mc = min(mtok, M - 1);
   const int nb = n0 + 4 * kg;  // this lane's output rows nb .. nb+3
   const bool ba = (r % 16) == 0;
@@ -417,7 +418,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
     v4i x[MT][S];
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
-      const int m = 16 * i + rho;
+      const int m = mb + 16 * i + rho;
       const int8_t* qrow = a.q + (int64_t)min(m, M - 1) * K;
 #pragma unroll
       for (int v = 0; v < S; ++v) {
@@ -446,7 +447,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   // to be computed here
   v4i lm[4];
   int sq = 0;
-  const bool keep = blockIdx.x == a.nb_lora && mtok < M;
+  const bool keep = (int)blockIdx.x == a.nb_lora && mtok < M;
   fetch_lora<L4>(a, mc, 0, kg, lm, &sq, keep);
 
   // LoRA up-projection, limbs 3, 2, 1, 0 over the 64-rank chunks
@@ -503,8 +504,10 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
 
 template <int MT, int S, bool L4>
 hipError_t launch_t(const SkinnyArgs& a, int nw, hipStream_t st) {
+  // x: LoRA workgroups then 16-row output blocks; y: 32-token chunks
   const int64_t blocks = a.nb_lora + dfssm::ceil_div(a.N, 16);
-  mfma_skinny<MT, S, L4><<<dim3((unsigned)blocks), dim3(64 * nw), 0, st>>>(a);
+  const int64_t chunks = dfssm::ceil_div(a.M, 32);
+  mfma_skinny<MT, S, L4><<<dim3((unsigned)blocks, (unsigned)chunks), dim3(64 * nw), 0, st>>>(a);
   return hipGetLastError();
 }
 
@@ -531,7 +534,7 @@ hipError_t skinny_impl(const int8_t* q, const float* s, int64_t M, int64_t K, in
                        const dfssm::LinearWorkspace& ws, hipStream_t st) {
   using namespace dfssm;
   if (M == 0 || N == 0) return hipSuccess;
-  if (M > kSkinnyMaxTokens) return hipErrorInvalidValue;
+  if (M > kSkinnyChunkedMaxTokens) return hipErrorInvalidValue;
   const int rp = (int)rank_padded(r);
   // 16-byte sign loads (8 MFMA steps) once K gives 4 waves a full one each:
   // at K = 2048 the 1.3B in_proj's 532 workgroups of 4 waves then fit the

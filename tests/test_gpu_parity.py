@@ -118,9 +118,10 @@ def test_linear(env, path, M, K, N, r):
     assert np.array_equal(y2.view(np.uint32), y.view(np.uint32)), "y without accumulator outputs"
 
 
-# few-token MFMA path (M <= 32): 1 or 2 token tiles, 8- and 16-byte sign
-# loads, K splits of one or more iterations per wave, unaligned sign rows,
-# ragged N, rank 0, rank not a multiple of 16 and ranks above 64
+# few-token MFMA path (M <= 512, in 32-token chunks above 32): 1 or 2 token
+# tiles, 8- and 16-byte sign loads, K splits of one or more iterations per
+# wave, unaligned sign rows, ragged N, rank 0, rank not a multiple of 16 and
+# ranks above 64, several chunks with a ragged last one
 FSHAPES = [
     (1, 768, 3352, 16),      # Mamba-2-130M in_proj: 3 waves
     (1, 2048, 8512, 64),     # Mamba-2-1.3B in_proj
@@ -136,6 +137,11 @@ FSHAPES = [
     (32, 4128, 50, 72),      # K % 512 != 0 with 16-byte sign loads, odd row length
     (12, 12288, 70, 32),
     (31, 2048, 300, 64),
+    (33, 2048, 8512, 64),    # two chunks, the second of one token
+    (96, 4096, 2048, 64),    # three full chunks
+    (100, 160, 77, 5),       # ragged last chunk, odd shapes
+    (200, 256, 31, 256),
+    (512, 96, 33, 1),        # the largest M the path takes
 ]
 
 
@@ -153,7 +159,8 @@ def test_linear_few_tokens(env, M, K, N, r):
     assert np.array_equal(y2.view(np.uint32), y.view(np.uint32)), "y without accumulator outputs"
 
 
-@pytest.mark.parametrize("M,K,N,r", [(3, 160, 77, 5), (17, 4096, 2048, 64), (2, 256, 31, 256), (1, 32, 1, 0)])
+@pytest.mark.parametrize("M,K,N,r", [(3, 160, 77, 5), (17, 4096, 2048, 64), (2, 256, 31, 256), (1, 32, 1, 0),
+                                     (70, 2048, 300, 64)])
 def test_few_tokens_local_lora(env, M, K, N, r, monkeypatch):
     """The few-token kernel's fallback: with no LoRA workgroups launched and
     no polling (a test switch of the library), every lane computes acc_a and
@@ -170,11 +177,11 @@ def test_few_tokens_local_lora(env, M, K, N, r, monkeypatch):
 
 
 def test_few_tokens_limit(env):
-    """The few-token path refuses M > 32 before launching anything."""
+    """The few-token path refuses M > 512 before launching anything."""
     torch, D, o = env
     ws = dev_weights(S.weights(64, 16, 4, key=(14,)))
-    q = torch.zeros((33, 64), dtype=torch.int8, device="cuda")
-    s = torch.zeros((33,), dtype=torch.float32, device="cuda")
+    q = torch.zeros((513, 64), dtype=torch.int8, device="cuda")
+    s = torch.zeros((513,), dtype=torch.float32, device="cuda")
     with pytest.raises(D.DfssmError):
         D.scaffold_lora_linear(q, s, ws["w_bits"], ws["alpha"], ws["A"], ws["B"], ws["beta"], path=D.PATH_MFMA_FEW)
 

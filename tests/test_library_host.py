@@ -210,7 +210,7 @@ def test_int4_linear_validation(dl):
     assert lin(A4=None) == dl.ERR_NULL
     assert lin(A4=24) == dl.ERR_ALIGN
     assert lin(path=9) == dl.ERR_SHAPE
-    assert lin(M=33, path=3) == dl.ERR_UNSUPPORTED
+    assert lin(M=513, path=3) == dl.ERR_UNSUPPORTED
     need = dl.lib.dfssm_linear_i4_workspace_bytes(1, 64, 8, 4)
     assert need > dl.linear_workspace_bytes(1, 64, 8, 4)
     assert lin(wsb=need - 1) == dl.ERR_WORKSPACE
