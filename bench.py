@@ -304,7 +304,7 @@ def main():
         tabs = [(dev(Eh), dev(sch))]
         tabs += [(tabs[0][0].clone(), tabs[0][1].clone()) for _ in range(3)]
         del Eh
-        for m in (1, 4):
+        for m in (1, 4, 64, 512):
             qd, sd = D.quantize_act(dev(S.activations(m, S.D_MODEL_1P3B, key=(45,))))
             lg = torch.empty((m, S.VOCAB_1P3B), dtype=torch.float32, device="cuda")
 
@@ -330,7 +330,9 @@ def main():
             us = t0.elapsed_time(t1) * 1e3 / (reps * len(tabs))
             lm.append({"workload": f"LM head 50280 x 2048 int8 table, M={m}", "us_per_call": round(us, 2),
                        "table_gbs": round(tb / (us * 1e-6) / 1e9, 1),
-                       "frac_hbm_peak": round(tb / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4), "table_bytes": tb})
+                       "frac_hbm_peak": round(tb / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4), "table_bytes": tb,
+                       "int8_tops": round(2.0 * m * S.VOCAB_1P3B * S.D_MODEL_1P3B / (us * 1e-6) / 1e12, 1),
+                       "kernel": "GEMV passes" if m < 8 else "matrix cores"})
             del g
         table0 = tabs[0]
         del tabs

@@ -251,8 +251,12 @@ dfssm_status dfssm_embed_gather(const int8_t* E, const float* scale, int64_t V, 
  *                 after each operation, in this order)
  *   logits [M, V] fp32 output, or NULL;  acc [M, V] int32 output, or NULL
  *   (not both NULL).
- * Made for decoding (a few tokens: each pass of up to 4 tokens, or fewer for
- * d > 4096, streams the table once); M tokens take ceil(M / 4) passes.
+ * Below 8 tokens, GEMV passes of up to 4 tokens (fewer for d > 4096), each
+ * streaming the table once; from 8 tokens, when d is a multiple of 64 that
+ * splits into 4..8 waves of at most 8 steps of 64 (d = 256 .. 4096), one
+ * pass on the matrix cores that reads the table once for all tokens.  Test
+ * switch: DFSSM_TEST_LM_HEAD_MFMA_TOKENS=<n> in the environment moves the
+ * threshold of 8.
  * Limits: 0 < d <= 16384, d % 16 == 0; 0 <= V < 2^30; M >= 0 (M or V == 0
  * is a no-op).
  * Errors: NULL, SHAPE, ALIGN, DEVICE. */

@@ -20,12 +20,20 @@
 // and each wave owning one contiguous range of rows all measured slower.  Row sums go by DPP inside 16-lane
 // rows and gfx950's permlane swaps across them.
 #include <algorithm>
+#include <stdlib.h>
 
 #include "dfssm_internal.hpp"
 
 namespace {
 
 constexpr int kThreads = 256;
+
+// Tokens from which the LM head runs on the matrix cores.  Test switch:
+// DFSSM_TEST_LM_HEAD_MFMA_TOKENS=<n> in the environment moves the threshold.
+int lm_head_mfma_tokens() {
+  const char* v = getenv("DFSSM_TEST_LM_HEAD_MFMA_TOKENS");
+  return v ? atoi(v) : 8;
+}
 
 // rows per wave visit: 4 KB of the table, or one row when rows are longer
 template <int NC>
@@ -139,6 +147,106 @@ hipError_t launch_t(const int8_t* q, const float* s, int d, const int8_t* E, con
   return hipGetLastError();
 }
 
+// ---- many tokens: the matrix cores ------------------------------------
+// A workgroup owns 64 vocabulary rows (4 row tiles of 16) and every token:
+// its nw waves split d, each holding the E operands of its columns for all
+// 4 row tiles in registers, so the table is read once whatever M is.  Token
+// tiles of 16 stream Q from L2; the waves' partial tiles are summed in LDS
+// and four waves write the logits of one row tile each, in the same fp32
+// order as the GEMV kernel.  v_mfma_i32_16x16x64_i8 contracts 64 columns in
+// an order of its own; E and Q place column c0 + 16 kg + b in byte b of lane
+// (row, kg) alike, so the order is the same on both sides.
+typedef int v4i __attribute__((ext_vector_type(4)));
+constexpr int kMfmaRows = 64;
+constexpr int kMfmaMaxWaves = 8;
+
+__device__ __forceinline__ v4i load16i(const int8_t* p) {
+  const uint4 u = *reinterpret_cast<const uint4*>(p);
+  return v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
+}
+
+template <int KS>
+__global__ __launch_bounds__(64 * kMfmaMaxWaves) void lm_head_mfma(const int8_t* __restrict__ q,
+                                                                  const float* __restrict__ s, int M, int d,
+                                                                  const int8_t* __restrict__ E,
+                                                                  const float* __restrict__ scale, int V,
+                                                                  float* __restrict__ logits,
+                                                                  int32_t* __restrict__ acc_out) {
+  __shared__ v4i red[kMfmaMaxWaves][4][64];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nw = blockDim.x >> 6;
+  const int rho = lane & 15, kg = lane >> 4;
+  const int v0 = blockIdx.x * kMfmaRows;
+  const int c0 = wave * KS * 64 + 16 * kg;  // this lane's first column
+
+  v4i e[4][KS];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int row = v0 + 16 * t + rho;
+    const bool ok = row < V;
+    const int8_t* rp = E + (int64_t)(ok ? row : 0) * d + c0;
+#pragma unroll
+    for (int k = 0; k < KS; ++k) e[t][k] = ok ? load16i(rp + 64 * k) : v4i{0, 0, 0, 0};
+  }
+  const int ntt = (M + 15) / 16;
+  for (int tt = 0; tt < ntt; ++tt) {
+    const int m = 16 * tt + rho;
+    const bool mok = m < M;
+    const int8_t* qp = q + (int64_t)(mok ? m : 0) * d + c0;
+    v4i x[KS];
+#pragma unroll
+    for (int k = 0; k < KS; ++k) x[k] = mok ? load16i(qp + 64 * k) : v4i{0, 0, 0, 0};
+    v4i acc[4] = {v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}};
+#pragma unroll
+    for (int k = 0; k < KS; ++k)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(e[t][k], x[k], acc[t], 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) red[wave][t][lane] = acc[t];
+    __syncthreads();
+    if (wave < 4) {
+      // lane (rho, kg) holds D[row 16 wave + 4 kg + vv][token 16 tt + rho]
+      v4i sum = red[0][wave][lane];
+      for (int w = 1; w < nw; ++w) sum += red[w][wave][lane];
+      if (mok) {
+        const float sm = s[m];
+#pragma unroll
+        for (int vv = 0; vv < 4; ++vv) {
+          const int row = v0 + 16 * wave + 4 * kg + vv;
+          if (row < V) {
+            const float fa = (float)sum[vv];
+            const float tv = scale[row] * fa;
+            if (logits) logits[(int64_t)m * V + row] = sm * tv;
+            if (acc_out) acc_out[(int64_t)m * V + row] = sum[vv];
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// MFMA steps per wave for row length d, or 0 when the MFMA kernel does not
+// take it (d % 64 != 0, or no split of d / 64 steps over 4..8 waves of at
+// most 8 steps)
+int mfma_steps(int64_t d) {
+  if (d % 64 != 0) return 0;
+  const int64_t steps = d / 64;
+  for (int ks = 1; ks <= 8; ++ks)
+    if (steps % ks == 0 && steps / ks <= kMfmaMaxWaves && steps / ks >= 4) return ks;
+  return 0;
+}
+
+template <int KS>
+hipError_t launch_mfma(const int8_t* q, const float* s, int64_t M, int64_t d, const int8_t* E, const float* scale,
+                       int64_t V, float* logits, int32_t* acc, hipStream_t st) {
+  const int nw = (int)(d / 64 / KS);
+  lm_head_mfma<KS><<<dim3((unsigned)dfssm::ceil_div(V, kMfmaRows)), dim3(64 * nw), 0, st>>>(
+      q, s, (int)M, (int)d, E, scale, (int)V, logits, acc);
+  return hipGetLastError();
+}
+
 template <int NC>
 hipError_t launch_nc(const int8_t* q, const float* s, int64_t M, int d, const int8_t* E, const float* scale,
                      int V, float* logits, int32_t* acc, hipStream_t st) {
@@ -196,6 +304,21 @@ namespace dfssm {
 hipError_t launch_lm_head(const int8_t* q, const float* s, int64_t M, int64_t d, const int8_t* E,
                           const float* scale, int64_t V, float* logits, int32_t* acc, hipStream_t st) {
   if (M == 0 || V == 0) return hipSuccess;
+  // from 8 tokens on the matrix cores (the table read once),
+  // below as GEMV passes of up to 4 tokens
+  const int ks = mfma_steps(d);
+  if (M >= lm_head_mfma_tokens() && ks > 0) {
+    switch (ks) {
+      case 1: return launch_mfma<1>(q, s, M, d, E, scale, V, logits, acc, st);
+      case 2: return launch_mfma<2>(q, s, M, d, E, scale, V, logits, acc, st);
+      case 3: return launch_mfma<3>(q, s, M, d, E, scale, V, logits, acc, st);
+      case 4: return launch_mfma<4>(q, s, M, d, E, scale, V, logits, acc, st);
+      case 5: return launch_mfma<5>(q, s, M, d, E, scale, V, logits, acc, st);
+      case 6: return launch_mfma<6>(q, s, M, d, E, scale, V, logits, acc, st);
+      case 7: return launch_mfma<7>(q, s, M, d, E, scale, V, logits, acc, st);
+      default: return launch_mfma<8>(q, s, M, d, E, scale, V, logits, acc, st);
+    }
+  }
   const int64_t nc = ceil_div(d, 1024);
   if (nc <= 1) return launch_nc<1>(q, s, M, (int)d, E, scale, (int)V, logits, acc, st);
   if (nc <= 2) return launch_nc<2>(q, s, M, (int)d, E, scale, (int)V, logits, acc, st);

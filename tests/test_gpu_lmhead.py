@@ -4,6 +4,8 @@ through the C ABI, against the CPU oracle on the same seeded inputs.
 acc is exact int32 and must match bit for bit; the logits follow a fixed
 fp32 order (s * (scale * (float)acc)) and must match the oracle's fp32
 evaluation bit for bit, and the exact product within three roundings.
+Both kernels are covered: the GEMV passes (fewer than 8 tokens) and the
+matrix-core kernel (from 8 tokens), each also forced through a test switch.
 The full-size cases use the 1.3B model's table (50,280 x 2048)."""
 import numpy as np
 import pytest
@@ -62,6 +64,12 @@ LSHAPES = [
     (3, 4112, 130),     # 4 KB chunks + tail: 2 tokens per pass
     (9, 5120, 100),     # 8 KB rows: 2 tokens per pass, 5 passes
     (2, 16384, 65),     # the longest row: 1 token per pass
+    # from 8 tokens the matrix-core kernel (d a multiple of 64 split over 4..8 waves)
+    (8, 2048, 50280),   # the 1.3B table, the smallest batch it takes
+    (64, 2048, 50280),
+    (300, 768, 1001),   # ragged token and row tiles, 6 waves
+    (17, 1024, 77),
+    (40, 4096, 130),    # 8 steps per wave
 ]
 
 
@@ -74,6 +82,19 @@ def test_lm_head(env, table_1p3b, M, d, V):
     x = S.activations(M, d, key=(42, M, d))
     q, s = o.quantize_act(x)
     _check_lm(torch, D, o, q, s, E, scale, f"M={M} d={d} V={V}")
+
+
+@pytest.mark.parametrize("M,d,V,threshold", [(1, 2048, 1001, "1"), (3, 256, 77, "1"), (64, 2048, 1001, "100000"),
+                                              (20, 768, 333, "100000")])
+def test_lm_head_both_kernels(env, M, d, V, threshold, monkeypatch):
+    # the test switch moves the token count from which the matrix-core
+    # kernel runs: few tokens through it, many through the GEMV passes
+    torch, D, o = env
+    say(f"lm_head M={M} d={d} V={V} threshold={threshold}")
+    monkeypatch.setenv("DFSSM_TEST_LM_HEAD_MFMA_TOKENS", threshold)
+    E, scale = S.embedding(V, d, key=(49, d, V))
+    q, s = o.quantize_act(S.activations(M, d, key=(49, M, d)))
+    _check_lm(torch, D, o, q, s, E, scale, f"M={M} d={d} V={V} threshold={threshold}")
 
 
 def test_lm_head_extremes(env):
