@@ -190,18 +190,26 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void lm_head_mfma(const int8_t*
     for (int k = 0; k < KS; ++k) e[t][k] = ok ? load16i(rp + 64 * k) : v4i{0, 0, 0, 0};
   }
   const int ntt = (M + 15) / 16;
-  for (int tt = 0; tt < ntt; ++tt) {
+  auto load_q = [&](int tt, v4i (&x)[KS]) {
     const int m = 16 * tt + rho;
     const bool mok = m < M;
     const int8_t* qp = q + (int64_t)(mok ? m : 0) * d + c0;
-    v4i x[KS];
 #pragma unroll
     for (int k = 0; k < KS; ++k) x[k] = mok ? load16i(qp + 64 * k) : v4i{0, 0, 0, 0};
+  };
+  v4i x[KS];
+  load_q(0, x);
+  const bool vec_store = (V & 3) == 0;  // 4 consecutive rows of a token are 16 aligned bytes
+  for (int tt = 0; tt < ntt; ++tt) {
+    const int m = 16 * tt + rho;
+    const bool mok = m < M;
     v4i acc[4] = {v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}};
 #pragma unroll
     for (int k = 0; k < KS; ++k)
 #pragma unroll
       for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(e[t][k], x[k], acc[t], 0, 0, 0);
+    // the next tile's Q loads go out before this tile's reduction and stores
+    if (tt + 1 < ntt) load_q(tt + 1, x);
 #pragma unroll
     for (int t = 0; t < 4; ++t) red[wave][t][lane] = acc[t];
     __syncthreads();
@@ -211,14 +219,24 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void lm_head_mfma(const int8_t*
       for (int w = 1; w < nw; ++w) sum += red[w][wave][lane];
       if (mok) {
         const float sm = s[m];
+        const int row0 = v0 + 16 * wave + 4 * kg;
+        if (vec_store && row0 + 3 < V) {
+          const float4 sc = *reinterpret_cast<const float4*>(scale + row0);
+          const float f0 = (float)sum[0], f1 = (float)sum[1], f2 = (float)sum[2], f3 = (float)sum[3];
+          const float t0 = sc.x * f0, t1 = sc.y * f1, t2 = sc.z * f2, t3 = sc.w * f3;
+          if (logits)
+            *reinterpret_cast<float4*>(logits + (int64_t)m * V + row0) = make_float4(sm * t0, sm * t1, sm * t2, sm * t3);
+          if (acc_out) *reinterpret_cast<int4*>(acc_out + (int64_t)m * V + row0) = make_int4(sum[0], sum[1], sum[2], sum[3]);
+        } else {
 #pragma unroll
-        for (int vv = 0; vv < 4; ++vv) {
-          const int row = v0 + 16 * wave + 4 * kg + vv;
-          if (row < V) {
-            const float fa = (float)sum[vv];
-            const float tv = scale[row] * fa;
-            if (logits) logits[(int64_t)m * V + row] = sm * tv;
-            if (acc_out) acc_out[(int64_t)m * V + row] = sum[vv];
+          for (int vv = 0; vv < 4; ++vv) {
+            const int row = row0 + vv;
+            if (row < V) {
+              const float fa = (float)sum[vv];
+              const float tv = scale[row] * fa;
+              if (logits) logits[(int64_t)m * V + row] = sm * tv;
+              if (acc_out) acc_out[(int64_t)m * V + row] = sum[vv];
+            }
           }
         }
       }
