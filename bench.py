@@ -417,6 +417,39 @@ def main():
                "sample": f"the full 96-linear sweep (weight copy 0, same input) run {reps} times in {dt:.1f} s",
                "us_per_layer": round(dt / reps / 48 * 1e6, 1)}
 
+        def timed(fn, seconds):
+            n, t0h = 0, time.perf_counter()
+            while True:
+                fn()
+                n += 1
+                el = time.perf_counter() - t0h
+                if el >= seconds:
+                    return el / n, n
+        # the oracle beside the other measured kernels: the LM head at one
+        # token on the 1.3B table, and one decode layer at batch 1
+        Eh, sch = S.embedding(S.VOCAB_1P3B, S.D_MODEL_1P3B, key=(40,))
+        qh, sh = o.quantize_act(S.activations(1, S.D_MODEL_1P3B, key=(45,)))
+        per, n = timed(lambda: o.lm_head(qh, sh, Eh, sch), 2.0)
+        cpu["lm_head_m1_us"] = round(per * 1e6, 1)
+        cpu["lm_head_sample"] = f"LM head, M=1, 50,280 x 2048 table, {n} calls"
+        del Eh
+        lp = S.mamba_params(2048, key=(150, 0))
+        st = S.mamba_state(1, 2048, key=(150,))
+        u0 = S.residual(1, 2048, key=(150,))
+        w_in, w_out = host0[0], host0[1]
+
+        def layer():
+            u, _, q1, s1 = o.add_rmsnorm_quant(u0, lp["norm_w"], 1e-5)
+            zx = o.linear(q1, s1, **w_in)["y32"]
+            y, _, _, _ = o.ssm_step(zx, st["conv_state"], st["ssm_state"], lp["conv_w"], lp["conv_b"],
+                                    lp["dt_bias"], lp["A_log"], lp["D"], 4096, 128, 64)
+            _, q2, s2 = o.gate_norm_quant(y, zx[:, :4096], lp["gate_w"], 1e-5)
+            return o.linear(q2, s2, **w_out)["y32"]
+        per, n = timed(layer, 3.0)
+        cpu["decode_layer_m1_us"] = round(per * 1e6, 1)
+        cpu["decode_layer_sample"] = (f"one 1.3B decode layer at batch 1 (residual norm, in_proj, conv + SSM step, "
+                                      f"gated norm, out_proj), {n} runs")
+
     traffic = measured_traffic()
     out = {
         "metric": "effective packed-weight GB/s (1.3B decode sweep, M=1)",
