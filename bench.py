@@ -201,7 +201,7 @@ def main():
 
     # ---- single linears at decode sizes ---------------------------------------
     # Per call: q, s -> y on the automatic path (the one-launch few-token
-    # MFMA kernel up to 32 tokens).  The calls of one graph replay walk
+    # MFMA kernel at these sizes).  The calls of one graph replay walk
     # over distinct copies of the weights, about 600 MB in all, so every call
     # meets its weights outside the 256 MB Infinity Cache; the graph removes
     # the host's launch cost from the measurement.

@@ -76,10 +76,11 @@ typedef enum { DFSSM_F16 = 0, DFSSM_F32 = 1 } dfssm_dtype;
 
 /* Kernel family selection for dfssm_scaffold_lora_linear_ex. */
 typedef enum {
-  DFSSM_PATH_AUTO = 0,     /* few-token MFMA for M <= 32, and above in
-                              32-token chunks while
-                              ceil(M/32) * ceil(N/16) * K/2048 <= 2048;
-                              prefill MFMA otherwise */
+  DFSSM_PATH_AUTO = 0,     /* few-token MFMA for M <= 32; for 33..512 the
+                              few-token kernel in 64-token blocks or the
+                              prefill kernel, by a cost model of the two
+                              (see the implementation); prefill MFMA
+                              above 512 */
   DFSSM_PATH_DECODE = 1,   /* bit-plane popcount GEMV (any M, best for M <= 4) */
   DFSSM_PATH_MFMA = 2,     /* sign bits expanded on chip + int8 MFMA, tiles of
                               128 tokens (prefill): an 8-wave ping-pong
@@ -88,8 +89,9 @@ typedef enum {
                               switch: DFSSM_TEST_PREFILL_KERNEL=4 or 8 in the
                               environment forces one of them. */
   DFSSM_PATH_MFMA_FEW = 3  /* the same expansion and MFMA for M <= 512 in
-                              one launch: 16 output rows and 32 tokens per
-                              workgroup, K split over its waves, the LoRA
+                              one launch: 16 output rows and up to 32
+                              tokens per workgroup (64 above 32 tokens), K
+                              split over its waves, the LoRA
                               down-projection in workgroups of the same
                               grid; M > 512 gives DFSSM_ERR_UNSUPPORTED.  Test switch: with the
                               environment variable DFSSM_TEST_LOCAL_LORA=1

@@ -78,16 +78,25 @@ size_t linear_ws_bytes(int64_t M, int64_t K, int64_t r) {
 
 // Kernel family of the automatic path: the popcount GEMV up to kDecodeM0
 // tokens (none by default); the one-launch few-token MFMA kernel up to
-// kSkinnyMaxTokens, and above that in 32-token chunks while the chunks'
-// output blocks, weighted by K / 2048, stay within 2048 (about 8 per CU):
-// its cost grows with M, while the prefill kernel's K loop is a serial
-// pipeline of K / 64 stages (~0.7 us each) whatever M is.  Measured on the
-// 1.3B projections: in_proj gains up to M = 96, out_proj up to M = 384.
+// kSkinnyMaxTokens; above, whichever of the few-token kernel in 64-token
+// blocks and the prefill kernel a cost model fitted to the 1.3B projections
+// puts lower (us):
+//   few-token  6 + 0.031 W,  W = ceil(M/64) * ceil(N/16) * K/2048
+//   prefill    31 + 5.2 K/1024 + 0.04 max(0, M - 256) K/2048
+// The prefill kernel's K loop is a serial pipeline of K/64 stages (~0.7 us
+// each) whatever M is; the few-token kernel's cost grows with its blocks.
+// Measured: in_proj (K 2048, N 8512) gains up to M = 96 (the model also
+// takes M = 128, where the prefill kernel is 2.5 us faster), out_proj
+// (K 4096, N 2048) up to M = 512.
 int auto_path(int64_t M, int64_t K, int64_t N) {
   if (M <= dfssm::kDecodeM0) return DFSSM_PATH_DECODE;
   if (M <= dfssm::kSkinnyMaxTokens) return DFSSM_PATH_MFMA_FEW;
-  const double work = (double)dfssm::ceil_div(M, 32) * (double)dfssm::ceil_div(N, 16) * ((double)K / 2048.0);
-  return (M <= dfssm::kSkinnyChunkedMaxTokens && work <= 2048.0) ? DFSSM_PATH_MFMA_FEW : DFSSM_PATH_MFMA;
+  if (M > dfssm::kSkinnyChunkedMaxTokens) return DFSSM_PATH_MFMA;
+  const double k2 = (double)K / 2048.0;
+  const double W = (double)dfssm::ceil_div(M, 64) * (double)dfssm::ceil_div(N, 16) * k2;
+  const double few = 6.0 + 0.031 * W;
+  const double pre = 31.0 + 10.4 * k2 + 0.04 * (double)std::max<int64_t>(0, M - 256) * k2;
+  return few <= pre ? DFSSM_PATH_MFMA_FEW : DFSSM_PATH_MFMA;
 }
 
 // Kernel family for a linear (path already chosen or AUTO).

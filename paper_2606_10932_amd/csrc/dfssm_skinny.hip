@@ -346,7 +346,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   const int rho = lane & 15, kg = lane >> 4;
   const int M = a.M, K = a.K, N = a.N, r = a.r, W = K >> 5;
   const int n0 = 16 * ((int)blockIdx.x - a.nb_lora);
-  const int mb = 32 * (int)blockIdx.y;  // first token of this block's chunk (row y of the grid)
+  const int mb = 16 * MT * (int)blockIdx.y;  // first token of this block's chunk (row y of the grid)
   const int nrow = min(n0 + rho, N - 1);  // sign / B row of this lane (rows past N are never stored)
   const uint32_t* wrow = a.w_bits + (int64_t)nrow * W;
   const int nit = (K + KW - 1) / KW;
@@ -506,7 +506,7 @@ template <int MT, int S, bool L4>
 hipError_t launch_t(const SkinnyArgs& a, int nw, hipStream_t st) {
   // x: LoRA workgroups then 16-row output blocks; y: 32-token chunks
   const int64_t blocks = a.nb_lora + dfssm::ceil_div(a.N, 16);
-  const int64_t chunks = dfssm::ceil_div(a.M, 32);
+  const int64_t chunks = dfssm::ceil_div(a.M, 16 * MT);
   mfma_skinny<MT, S, L4><<<dim3((unsigned)blocks, (unsigned)chunks), dim3(64 * nw), 0, st>>>(a);
   return hipGetLastError();
 }
@@ -539,8 +539,11 @@ hipError_t skinny_impl(const int8_t* q, const float* s, int64_t M, int64_t K, in
   // 16-byte sign loads (8 MFMA steps) once K gives 4 waves a full one each:
   // at K = 2048 the 1.3B in_proj's 532 workgroups of 4 waves then fit the
   // chip's slots in one round (8 waves of 8-byte loads would not)
-  const int S = K >= 2048 ? 8 : 4;
-  const int mt = M > 16 ? 2 : 1;
+  // above 32 tokens, output blocks of 64 tokens (4 token tiles, 8-byte sign
+  // loads): each sign operand expanded once feeds 4 tiles (the 1.3B out_proj
+  // at M = 256: 31.8 us against 41.3 with 32-token blocks)
+  const int S = M > 32 ? 4 : (K >= 2048 ? 8 : 4);
+  const int mt = M > 32 ? 4 : (M > 16 ? 2 : 1);
   const int64_t nit = ceil_div(K, 64 * S);
   const int nw = (int)std::max<int64_t>(mt, std::min<int64_t>(kMaxWaves, nit));
   // Test hook: DFSSM_TEST_LOCAL_LORA=1 launches no LoRA workgroups and lets
@@ -554,8 +557,10 @@ hipError_t skinny_impl(const int8_t* q, const float* s, int64_t M, int64_t K, in
   hipError_t e;
   if (mt == 1)
     e = S == 8 ? launch_t<1, 8, L4>(a, nw, st) : launch_t<1, 4, L4>(a, nw, st);
-  else
+  else if (mt == 2)
     e = S == 8 ? launch_t<2, 8, L4>(a, nw, st) : launch_t<2, 4, L4>(a, nw, st);
+  else
+    e = launch_t<4, 4, L4>(a, nw, st);
   if (e != hipSuccess) return e;
   if (acc_a_out && r > 0)
     e = hipMemcpyAsync(acc_a_out, ws.acc_a, (size_t)(M * r) * 4, hipMemcpyDeviceToDevice, st);

@@ -5,7 +5,8 @@ oracle's fp32 order and within 1e-3 of max|y| against fp64.  Every nibble
 value -8..7 occurs (the factors are uniform random bytes).
 
 Paths: the few-token kernel reading the packed bytes directly (M <= 512,
-in 32-token chunks above 32, with and without its LoRA workgroups), and the prefill MFMA and popcount
+in 64-token blocks above 32, with and without its LoRA workgroups), and the
+prefill MFMA and popcount
 paths on factors expanded in the workspace.  Shapes: the 1.3B projections,
 ragged K and N, r not a multiple of 16 (unaligned packed B rows), r = 2, 0."""
 import numpy as np
@@ -61,7 +62,8 @@ SHAPES = [
     (2, 256, 40, 256),       # four 64-rank chunks
     (1, 768, 3352, 16),      # Mamba-2-130M in_proj
     (3, 64, 9, 0),
-    (70, 2048, 300, 64),     # three 32-token chunks
+    (70, 2048, 300, 64),     # two 64-token blocks, the second ragged
+    (200, 4096, 2048, 64),   # four blocks, out_proj shape
 ]
 
 

@@ -118,8 +118,8 @@ def test_linear(env, path, M, K, N, r):
     assert np.array_equal(y2.view(np.uint32), y.view(np.uint32)), "y without accumulator outputs"
 
 
-# few-token MFMA path (M <= 512, in 32-token chunks above 32): 1 or 2 token
-# tiles, 8- and 16-byte sign loads, K splits of one or more iterations per
+# few-token MFMA path (M <= 512; up to 32 tokens 1 or 2 token tiles per
+# workgroup, above 32 blocks of 64 tokens, 4 tiles): 8- and 16-byte sign loads, K splits of one or more iterations per
 # wave, unaligned sign rows, ragged N, rank 0, rank not a multiple of 16 and
 # ranks above 64, several chunks with a ragged last one
 FSHAPES = [
@@ -137,9 +137,11 @@ FSHAPES = [
     (32, 4128, 50, 72),      # K % 512 != 0 with 16-byte sign loads, odd row length
     (12, 12288, 70, 32),
     (31, 2048, 300, 64),
-    (33, 2048, 8512, 64),    # two chunks, the second of one token
-    (96, 4096, 2048, 64),    # three full chunks
-    (100, 160, 77, 5),       # ragged last chunk, odd shapes
+    (33, 2048, 8512, 64),    # one 64-token block holding 33 tokens
+    (65, 4096, 2048, 64),    # two blocks, the second of one token
+    (96, 4096, 2048, 64),    # two blocks, the second of two full tiles
+    (100, 160, 77, 5),       # ragged last block, odd shapes
+    (130, 4096, 2048, 64),   # three blocks, out_proj shape
     (200, 256, 31, 256),
     (512, 96, 33, 1),        # the largest M the path takes
 ]
