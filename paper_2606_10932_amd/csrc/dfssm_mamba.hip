@@ -181,7 +181,7 @@ hipError_t launch_norm(const NormArgs& a, int64_t M, hipStream_t st) {
 // ---------------------------------------------------------------- SSM step
 constexpr int kHeadDim = 64;      // P
 constexpr int kSsmThreads = 256;
-constexpr int kPBlock = 16;       // channels of a head per workgroup
+constexpr int kPBlock = 32;       // channels of a head per workgroup
 
 struct SsmArgs {
   const float* zx;    // [M][ld]: z | xBC | dt
@@ -199,13 +199,26 @@ struct SsmArgs {
   float* xbc;         // [M][conv_dim] or null
 };
 
-// Workgroup (m, h, pb): PB channels p = PB pb .. PB pb + PB - 1 of head h.
-// Thread t holds channel PB pb + t / TPC and NPL consecutive state columns;
-// its TPC lanes sum y[p] over the state.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// The state is read once and written once per step, 4 MB per sequence:
+// non-temporal accesses keep it from displacing the step's shared inputs
+// in the caches (batch 512: 406 us against 434 with plain accesses).
+__device__ __forceinline__ f32x4 load_state(const f32x4* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ void store_state(f32x4 v, f32x4* p) { __builtin_nontemporal_store(v, p); }
+
+// Workgroup (m, h, pb): PB channels p = PB pb .. PB pb + PB - 1 of head h,
+// whose states are one contiguous PB x N block.  Pass j of thread t holds
+// float4 j NT + t of that block: channel (j NT + t) / L and state columns
+// 4 (t % L) .. + 3, with L = N / 4 lanes per channel, so every load and
+// store of a wave covers 1 KB in one piece; the L lanes of a channel sum
+// y[p] over the state.
 template <int N, int PB, int NT = kSsmThreads>
 __global__ __launch_bounds__(NT) void ssm_step(SsmArgs a) {
-  constexpr int TPC = NT / PB;           // threads per channel
-  constexpr int NPL = N / TPC;           // state columns per thread
+  constexpr int L = N / 4;               // lanes per channel
+  constexpr int J = PB * L / NT;         // passes
+  constexpr int CPJ = NT / L;            // channels per pass
+  static_assert(J * NT == PB * L && CPJ * L == NT, "state block tiling");
   constexpr int NBH = kHeadDim / PB;     // workgroups per head
   const int nblk = a.H * NBH;
   const int64_t m = blockIdx.x / nblk;
@@ -213,15 +226,15 @@ __global__ __launch_bounds__(NT) void ssm_step(SsmArgs a) {
   const int h = hb / NBH;
   const int p0 = (hb % NBH) * PB;
   const int tid = threadIdx.x;
-  const int pl = tid / TPC, nc = tid % TPC;
+  const int pj = tid / L, nc = tid % L;
   const int conv_dim = a.d_inner + 2 * N;
   const float* zr = a.zx + m * a.ld;
 
   // the state first: it is the bytes that come from HBM
-  float* hs = a.state + (((m * a.H + h) * kHeadDim + p0 + pl) * (int64_t)N + nc * NPL);
-  float4 hv[NPL / 4];
+  f32x4* hs = reinterpret_cast<f32x4*>(a.state + ((m * a.H + h) * kHeadDim + p0) * (int64_t)N) + tid;
+  f32x4 hv[J];
 #pragma unroll
-  for (int j = 0; j < NPL / 4; ++j) hv[j] = reinterpret_cast<const float4*>(hs)[j];
+  for (int j = 0; j < J; ++j) hv[j] = load_state(hs + j * NT);
 
   // convolution step for this workgroup's PB x channels and all B, C channels
   __shared__ float xbc_s[PB + 2 * N];
@@ -259,32 +272,40 @@ __global__ __launch_bounds__(NT) void ssm_step(SsmArgs a) {
   __syncthreads();
   const float dt = dt_s[0], dA = dt_s[1];
 
-  const float x = xbc_s[pl];
-  const float dtx = dt * x;
-  const float* Bs = xbc_s + PB + nc * NPL;
-  const float* Cs = xbc_s + PB + N + nc * NPL;
-  double acc = 0.0;
+  const float* Bs = xbc_s + PB + 4 * nc;
+  const float* Cs = xbc_s + PB + N + 4 * nc;
+  const float b[4] = {Bs[0], Bs[1], Bs[2], Bs[3]};
+  const float cc[4] = {Cs[0], Cs[1], Cs[2], Cs[3]};
 #pragma unroll
-  for (int j = 0; j < NPL / 4; ++j) {
+  for (int j = 0; j < J; ++j) {
+    const int p = j * CPJ + pj;
+    const float x = xbc_s[p];
+    const float dtx = dt * x;
     float e[4] = {hv[j].x, hv[j].y, hv[j].z, hv[j].w};
+    double acc = 0.0;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const float t1 = e[u] * dA;
-      const float t2 = dtx * Bs[4 * j + u];
+      const float t2 = dtx * b[u];
       e[u] = t1 + t2;
-      acc += (double)e[u] * (double)Cs[4 * j + u];
+      acc += (double)e[u] * (double)cc[u];
     }
-    reinterpret_cast<float4*>(hs)[j] = make_float4(e[0], e[1], e[2], e[3]);
+    f32x4 o;
+    o.x = e[0];
+    o.y = e[1];
+    o.z = e[2];
+    o.w = e[3];
+    store_state(o, hs + j * NT);
+    acc = sum_lanes<L>(acc);
+    if (nc == 0) a.y[m * a.d_inner + h * kHeadDim + p0 + p] = (float)(acc + (double)a.D[h] * (double)x);
   }
-  acc = sum_lanes<TPC>(acc);
-  if (nc == 0) a.y[m * a.d_inner + h * kHeadDim + p0 + pl] = (float)(acc + (double)a.D[h] * (double)x);
 }
 
 template <int N>
 void launch_ssm_n(const SsmArgs& a, int64_t M, hipStream_t st) {
-  // 16 channels per workgroup at every batch: 8 channels, and a whole head
-  // on 256 or 1024 threads (4x fewer repeats of the shared B/C convolution),
-  // all measured the same or slower on the 1.3B decode step
+  // 32 channels per workgroup: the B/C convolution every workgroup repeats
+  // is then amortised over 16 KB of state (batch 512: 357-364 us against
+  // 404-406 with 16 channels, 363-370 with 64, 489 with 8)
   ssm_step<N, kPBlock><<<dim3((unsigned)(M * a.H * (kHeadDim / kPBlock))), dim3(kSsmThreads), 0, st>>>(a);
 }
 
