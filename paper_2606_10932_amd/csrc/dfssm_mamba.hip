@@ -181,7 +181,6 @@ hipError_t launch_norm(const NormArgs& a, int64_t M, hipStream_t st) {
 // ---------------------------------------------------------------- SSM step
 constexpr int kHeadDim = 64;      // P
 constexpr int kSsmThreads = 256;
-constexpr int kPBlock = 32;       // channels of a head per workgroup
 
 struct SsmArgs {
   const float* zx;    // [M][ld]: z | xBC | dt
@@ -303,10 +302,15 @@ __global__ __launch_bounds__(NT) void ssm_step(SsmArgs a) {
 
 template <int N>
 void launch_ssm_n(const SsmArgs& a, int64_t M, hipStream_t st) {
-  // 32 channels per workgroup: the B/C convolution every workgroup repeats
-  // is then amortised over 16 KB of state (batch 512: 357-364 us against
-  // 404-406 with 16 channels, 363-370 with 64, 489 with 8)
-  ssm_step<N, kPBlock><<<dim3((unsigned)(M * a.H * (kHeadDim / kPBlock))), dim3(kSsmThreads), 0, st>>>(a);
+  // 32 channels per workgroup from 5 sequences: the B/C convolution every
+  // workgroup repeats is then amortised over 16 KB of state (batch 512:
+  // 357-364 us against 404-406 with 16 channels, 363-370 with 64, 489 with
+  // 8).  Up to 4 sequences the step is latency and the 16-channel blocks'
+  // shorter per-thread chain wins (batch 1: 4.05 us against 4.75).
+  if (M <= 4)
+    ssm_step<N, 16><<<dim3((unsigned)(M * a.H * (kHeadDim / 16))), dim3(kSsmThreads), 0, st>>>(a);
+  else
+    ssm_step<N, 32><<<dim3((unsigned)(M * a.H * (kHeadDim / 32))), dim3(kSsmThreads), 0, st>>>(a);
 }
 
 }  // namespace
