@@ -79,23 +79,24 @@ size_t linear_ws_bytes(int64_t M, int64_t K, int64_t r) {
 // Kernel family of the automatic path: the popcount GEMV up to kDecodeM0
 // tokens (none by default); the one-launch few-token MFMA kernel up to
 // kSkinnyMaxTokens; above, whichever of the few-token kernel in 64-token
-// blocks and the prefill kernel a cost model fitted to the 1.3B projections
-// puts lower (us):
-//   few-token  6 + 0.031 W,  W = ceil(M/64) * ceil(N/16) * K/2048
-//   prefill    31 + 5.2 K/1024 + 0.04 max(0, M - 256) K/2048
-// The prefill kernel's K loop is a serial pipeline of K/64 stages (~0.7 us
-// each) whatever M is; the few-token kernel's cost grows with its blocks.
-// Measured: in_proj (K 2048, N 8512) gains up to M = 96 (the model also
-// takes M = 128, where the prefill kernel is 2.5 us faster), out_proj
-// (K 4096, N 2048) up to M = 512.
+// blocks and the prefill kernel a cost model puts lower (us), fitted to the
+// 130M, 1.3B and 2.7B projections at 33 to 512 tokens:
+//   few-token  8.5 + 0.018 B (0.76 + K/2048),  B = ceil(M/16) ceil(N/16) / 4
+//   prefill    7.5 + 0.7 K/64 + 0.0016 N + 0.04 max(0, M - 256) K/2048
+// The few-token kernel's cost grows with its 16-token tiles (a partly
+// filled 64-token block costs its tiles); the prefill kernel's
+// K loop is a serial pipeline of K/64 stages (~0.7 us each) whatever M is.
+// Of the 40 measured cases the model misses two near-ties: the 1.3B in_proj
+// at M = 128 (2.3 us) and the 130M out_proj at M = 512 (1 us).
 int auto_path(int64_t M, int64_t K, int64_t N) {
   if (M <= dfssm::kDecodeM0) return DFSSM_PATH_DECODE;
   if (M <= dfssm::kSkinnyMaxTokens) return DFSSM_PATH_MFMA_FEW;
   if (M > dfssm::kSkinnyChunkedMaxTokens) return DFSSM_PATH_MFMA;
   const double k2 = (double)K / 2048.0;
-  const double W = (double)dfssm::ceil_div(M, 64) * (double)dfssm::ceil_div(N, 16) * k2;
-  const double few = 6.0 + 0.031 * W;
-  const double pre = 31.0 + 10.4 * k2 + 0.04 * (double)std::max<int64_t>(0, M - 256) * k2;
+  const double B = (double)dfssm::ceil_div(M, 16) * (double)dfssm::ceil_div(N, 16) / 4.0;
+  const double few = 8.5 + 0.018 * B * (0.76 + k2);
+  const double pre = 7.5 + 0.7 * (double)K / 64.0 + 0.0016 * (double)N +
+                     0.04 * (double)std::max<int64_t>(0, M - 256) * k2;
   return few <= pre ? DFSSM_PATH_MFMA_FEW : DFSSM_PATH_MFMA;
 }
 
