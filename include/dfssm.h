@@ -353,6 +353,10 @@ typedef struct {
   const float* D;        /* [nheads] */
   const float* gate_w;   /* [d_inner]  weight of the gated norm */
   dfssm_layer out_proj;  /* K = d_inner, N = d_model */
+  int64_t lora_bits;     /* 8 (or 0): A and B of both projections are int8,
+                            as for dfssm_scaffold_lora_linear; 4: they are
+                            packed int4 as for dfssm_scaffold_lora_linear_i4
+                            (A [r][K/2], B [N][r/2] bytes; r even) */
 } dfssm_mamba2_layer;
 
 /* The model: tied int8 embedding / LM head table, n_layers layers, final
@@ -386,7 +390,8 @@ size_t dfssm_mamba2_workspace_bytes(const dfssm_mamba2_model* model, int64_t M);
  *     zx = in_proj(q, s);  y = ssm_step(zx, step, state_l)
  *     (q, s) = quantise(rmsnorm(y * silu(z)) * gate_w);  delta = out_proj(q, s)
  *   u += delta;  (q, s) = quantise(rmsnorm(u) * norm_f);  logits = lm_head(q, s)
- * with the entry points above (in_proj and out_proj on the automatic path).
+ * with the entry points above (in_proj and out_proj on the automatic path,
+ * through the int4 linear for layers with lora_bits = 4).
  *   tok     [M] int32 device token ids (outside [0, vocab) -> a zero row)
  *   step    this token's position; only step & 3 is used (the ring slot)
  *   conv_ring, ssm_state   the state, updated in place

@@ -45,7 +45,8 @@ class Mamba2Layer(ctypes.Structure):
     """dfssm_mamba2_layer: one Mamba-2 layer (device pointers)."""
     _fields_ = [("norm_w", ctypes.c_void_p), ("in_proj", Layer), ("conv_w", ctypes.c_void_p),
                 ("conv_b", ctypes.c_void_p), ("dt_bias", ctypes.c_void_p), ("A_log", ctypes.c_void_p),
-                ("D", ctypes.c_void_p), ("gate_w", ctypes.c_void_p), ("out_proj", Layer)]
+                ("D", ctypes.c_void_p), ("gate_w", ctypes.c_void_p), ("out_proj", Layer),
+                ("lora_bits", ctypes.c_int64)]
 
 
 class Mamba2Model(ctypes.Structure):
@@ -381,7 +382,9 @@ class Mamba2:
 
     layers: list of dicts with norm_w, conv_w, conv_b, dt_bias, A_log, D,
     gate_w (fp32 device tensors) and in_proj / out_proj (dicts of w_bits,
-    alpha, A, B, beta as for scaffold_lora_linear)."""
+    alpha, A, B, beta as for scaffold_lora_linear, or w_bits, alpha, A4,
+    B4, beta as for scaffold_lora_linear_i4; both projections of a layer
+    alike)."""
 
     def __init__(self, E, E_scale, norm_f, layers, d_state: int = 128, eps: float = 1e-5):
         self._keep = [E, E_scale, norm_f, layers]
@@ -389,9 +392,13 @@ class Mamba2:
         self.n_layers = len(layers)
         self._layers = (Mamba2Layer * self.n_layers)()
         for i, L in enumerate(layers):
+            i4 = "A4" in L["in_proj"]
+            if i4 != ("A4" in L["out_proj"]):
+                raise ValueError(f"layer {i}: in_proj and out_proj must both have int4 (A4, B4) or int8 factors")
             self._layers[i] = Mamba2Layer(L["norm_w"].data_ptr(), _proj(L["in_proj"]), L["conv_w"].data_ptr(),
                                           L["conv_b"].data_ptr(), L["dt_bias"].data_ptr(), L["A_log"].data_ptr(),
-                                          L["D"].data_ptr(), L["gate_w"].data_ptr(), _proj(L["out_proj"]))
+                                          L["D"].data_ptr(), L["gate_w"].data_ptr(), _proj(L["out_proj"]),
+                                          4 if i4 else 8)
         self.struct = Mamba2Model(self.d_model, d_state, self.n_layers, self.vocab, eps, E.data_ptr(),
                                   E_scale.data_ptr(), norm_f.data_ptr(), self._layers)
 
@@ -426,10 +433,11 @@ class Mamba2:
 
 
 def _proj(w) -> Layer:
-    r = 0 if w.get("A") is None else w["A"].shape[0]
-    return Layer(w["w_bits"].data_ptr(), w["alpha"].data_ptr(), _ptr(w.get("A")) if r else None,
-                 _ptr(w.get("B")) if r else None, _ptr(w.get("beta")) if r else None, w["w_bits"].shape[1] * 32,
-                 w["w_bits"].shape[0], r)
+    A = w.get("A4", w.get("A"))
+    B = w.get("B4", w.get("B"))
+    r = 0 if A is None else A.shape[0]
+    return Layer(w["w_bits"].data_ptr(), w["alpha"].data_ptr(), _ptr(A) if r else None, _ptr(B) if r else None,
+                 _ptr(w.get("beta")) if r else None, w["w_bits"].shape[1] * 32, w["w_bits"].shape[0], r)
 
 
 def scaffold_lora_linear_i4(q, s, w_bits, alpha, A4=None, B4=None, beta=None, y=None, workspace=None,

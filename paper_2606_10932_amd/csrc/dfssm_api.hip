@@ -115,6 +115,36 @@ hipError_t launch_linear(int path, const int8_t* q, const float* s, int64_t M, i
   return dfssm::launch_mfma_linear(q, s, M, K, N, r, w_bits, alpha, A, B, beta, y, acc_s, acc_a, acc_b, ws, hs);
 }
 
+// The int4 linear after validation: the few-token kernel reads the packed
+// factors itself; the other paths run the int8 kernels on factors expanded
+// into the workspace (linear_i4_workspace_bytes of it).
+hipError_t launch_linear_i4(int path, const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N, int64_t r,
+                            const uint32_t* w_bits, const float* alpha, const uint8_t* A4, const uint8_t* B4,
+                            const float* beta, float* y, int32_t* acc_s, int32_t* acc_a, int64_t* acc_b,
+                            void* workspace, hipStream_t hs) {
+  dfssm::LinearWorkspace ws = dfssm::carve_linear_workspace(workspace, M, K, r);
+  if (path == DFSSM_PATH_AUTO) path = auto_path(M, K, N);
+  hipError_t e;
+  if (path == DFSSM_PATH_MFMA_FEW || r == 0) {
+    if (path == DFSSM_PATH_MFMA_FEW)
+      e = dfssm::launch_skinny_linear_i4(q, s, M, K, N, r, w_bits, alpha, A4, B4, beta, y, acc_s, acc_a, acc_b, ws,
+                                         hs);
+    else
+      e = launch_linear(path, q, s, M, K, N, 0, w_bits, alpha, nullptr, nullptr, nullptr, y, acc_s, acc_a, acc_b,
+                        ws, hs);
+  } else {
+    // the int8 kernels on factors expanded into the workspace
+    char* extra = static_cast<char*>(workspace) + dfssm::linear_i4_extra_offset(M, K, r);
+    int8_t* A8 = reinterpret_cast<int8_t*>(extra);
+    int8_t* B8 = reinterpret_cast<int8_t*>(extra + (((size_t)(r * K) + 255) & ~(size_t)255));
+    e = dfssm::launch_unpack_int4(A4, r * K, A8, hs);
+    if (e == hipSuccess) e = dfssm::launch_unpack_int4(B4, N * r, B8, hs);
+    if (e == hipSuccess)
+      e = launch_linear(path, q, s, M, K, N, r, w_bits, alpha, A8, B8, beta, y, acc_s, acc_a, acc_b, ws, hs);
+  }
+  return e;
+}
+
 }  // namespace
 
 extern "C" {
@@ -224,27 +254,8 @@ dfssm_status dfssm_scaffold_lora_linear_i4(const int8_t* q, const float* s, int6
   const size_t need = dfssm::linear_i4_workspace_bytes(M, K, N, r);
   if (workspace_bytes < need)
     return fail(DFSSM_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, need);
-  const hipStream_t hs = (hipStream_t)stream;
-  dfssm::LinearWorkspace ws = dfssm::carve_linear_workspace(workspace, M, K, r);
-  if (path == DFSSM_PATH_AUTO) path = auto_path(M, K, N);
-  hipError_t e;
-  if (path == DFSSM_PATH_MFMA_FEW || r == 0) {
-    if (path == DFSSM_PATH_MFMA_FEW)
-      e = dfssm::launch_skinny_linear_i4(q, s, M, K, N, r, w_bits, alpha, A4, B4, beta, y, acc_s, acc_a, acc_b, ws,
-                                         hs);
-    else
-      e = launch_linear(path, q, s, M, K, N, 0, w_bits, alpha, nullptr, nullptr, nullptr, y, acc_s, acc_a, acc_b,
-                        ws, hs);
-  } else {
-    // the int8 kernels on factors expanded into the workspace
-    char* extra = static_cast<char*>(workspace) + dfssm::linear_i4_extra_offset(M, K, r);
-    int8_t* A8 = reinterpret_cast<int8_t*>(extra);
-    int8_t* B8 = reinterpret_cast<int8_t*>(extra + (((size_t)(r * K) + 255) & ~(size_t)255));
-    e = dfssm::launch_unpack_int4(A4, r * K, A8, hs);
-    if (e == hipSuccess) e = dfssm::launch_unpack_int4(B4, N * r, B8, hs);
-    if (e == hipSuccess)
-      e = launch_linear(path, q, s, M, K, N, r, w_bits, alpha, A8, B8, beta, y, acc_s, acc_a, acc_b, ws, hs);
-  }
+  const hipError_t e = launch_linear_i4(path, q, s, M, K, N, r, w_bits, alpha, A4, B4, beta, y, acc_s, acc_a,
+                                        acc_b, workspace, (hipStream_t)stream);
   return e == hipSuccess ? DFSSM_OK : device_fail(e, "int4 linear launch");
 }
 
@@ -622,6 +633,8 @@ dfssm_status check_model_pointers(const dfssm_mamba2_model* md, const ModelDims&
     st = check_ptrs({{L.norm_w, "norm_w"}, {L.conv_w, "conv_w"}, {L.conv_b, "conv_b"}, {L.dt_bias, "dt_bias"},
                      {L.A_log, "A_log"}, {L.D, "D"}, {L.gate_w, "gate_w"}},
                     {});
+    if (st == DFSSM_OK && L.lora_bits != 0 && L.lora_bits != 8 && L.lora_bits != 4)
+      st = fail(DFSSM_ERR_SHAPE, "lora_bits=%lld: 8 (or 0) or 4", (long long)L.lora_bits);
     const dfssm_layer* pr[2] = {&L.in_proj, &L.out_proj};
     const int64_t want_k[2] = {d.d_model, d.d_inner}, want_n[2] = {d.ld, d.d_model};
     for (int i = 0; i < 2 && st == DFSSM_OK; ++i) {
@@ -631,6 +644,9 @@ dfssm_status check_model_pointers(const dfssm_mamba2_model* md, const ModelDims&
                   (long long)P.K, (long long)P.N, (long long)want_k[i], (long long)want_n[i]);
       else
         st = check_linear(1, P.K, P.N, P.r);
+      if (st == DFSSM_OK && L.lora_bits == 4 && P.r % 2 != 0)
+        st = fail(DFSSM_ERR_SHAPE, "%s: r=%lld must be even for packed int4 factors", i ? "out_proj" : "in_proj",
+                  (long long)P.r);
       if (st == DFSSM_OK) st = check_ptrs({{P.w_bits, "w_bits"}, {P.alpha, "alpha"}}, {});
       if (st == DFSSM_OK && P.r > 0) st = check_ptrs({{P.A, "A"}, {P.B, "B"}, {P.beta, "beta"}}, {});
     }
@@ -662,8 +678,14 @@ ModelWs carve_model_ws(void* base, const dfssm_mamba2_model* md, const ModelDims
   const size_t o_s = take((size_t)M * 4), o_q = take((size_t)(M * d.d_inner));
   size_t lin = 0;
   for (int64_t l = 0; md->layers && l < md->n_layers; ++l) {
-    lin = std::max(lin, linear_ws_bytes(M, d.d_model, md->layers[l].in_proj.r));
-    lin = std::max(lin, linear_ws_bytes(M, d.d_inner, md->layers[l].out_proj.r));
+    const dfssm_mamba2_layer& L = md->layers[l];
+    if (L.lora_bits == 4) {
+      lin = std::max(lin, dfssm::linear_i4_workspace_bytes(M, d.d_model, d.ld, L.in_proj.r));
+      lin = std::max(lin, dfssm::linear_i4_workspace_bytes(M, d.d_inner, d.d_model, L.out_proj.r));
+    } else {
+      lin = std::max(lin, linear_ws_bytes(M, d.d_model, L.in_proj.r));
+      lin = std::max(lin, linear_ws_bytes(M, d.d_inner, L.out_proj.r));
+    }
   }
   const size_t o_lin = take(lin);
   char* b = static_cast<char*>(base);
@@ -725,10 +747,15 @@ dfssm_status dfssm_mamba2_decode_step(const dfssm_mamba2_model* model, int64_t M
     const dfssm_mamba2_layer& L = model->layers[l];
     e = dfssm::launch_add_rmsnorm_quant(w.u, l > 0 ? w.delta : nullptr, L.norm_w, eps, M, d.d_model, w.u, w.q, w.s, hs);
     if (e != hipSuccess) break;
+    const bool i4 = L.lora_bits == 4;
     const dfssm_layer& I = L.in_proj;
-    dfssm::LinearWorkspace lw = dfssm::carve_linear_workspace(w.lin, M, I.K, I.r);
-    e = launch_linear(DFSSM_PATH_AUTO, w.q, w.s, M, I.K, I.N, I.r, I.w_bits, I.alpha, I.A, I.B, I.beta, w.zx,
-                      nullptr, nullptr, nullptr, lw, hs);
+    if (i4)
+      e = launch_linear_i4(DFSSM_PATH_AUTO, w.q, w.s, M, I.K, I.N, I.r, I.w_bits, I.alpha,
+                           reinterpret_cast<const uint8_t*>(I.A), reinterpret_cast<const uint8_t*>(I.B), I.beta,
+                           w.zx, nullptr, nullptr, nullptr, w.lin, hs);
+    else
+      e = launch_linear(DFSSM_PATH_AUTO, w.q, w.s, M, I.K, I.N, I.r, I.w_bits, I.alpha, I.A, I.B, I.beta, w.zx,
+                        nullptr, nullptr, nullptr, dfssm::carve_linear_workspace(w.lin, M, I.K, I.r), hs);
     if (e != hipSuccess) break;
     e = dfssm::launch_ssm_step(w.zx, d.ld, M, d.d_inner, d.N, step, conv_ring + l * ring_stride, L.conv_w, L.conv_b,
                                L.dt_bias, L.A_log, L.D, ssm_state + l * state_stride, w.y, nullptr, hs);
@@ -736,9 +763,13 @@ dfssm_status dfssm_mamba2_decode_step(const dfssm_mamba2_model* model, int64_t M
     e = dfssm::launch_gate_norm_quant(w.y, w.zx, d.ld, L.gate_w, eps, M, d.d_inner, w.q, w.s, hs);
     if (e != hipSuccess) break;
     const dfssm_layer& O = L.out_proj;
-    lw = dfssm::carve_linear_workspace(w.lin, M, O.K, O.r);
-    e = launch_linear(DFSSM_PATH_AUTO, w.q, w.s, M, O.K, O.N, O.r, O.w_bits, O.alpha, O.A, O.B, O.beta, w.delta,
-                      nullptr, nullptr, nullptr, lw, hs);
+    if (i4)
+      e = launch_linear_i4(DFSSM_PATH_AUTO, w.q, w.s, M, O.K, O.N, O.r, O.w_bits, O.alpha,
+                           reinterpret_cast<const uint8_t*>(O.A), reinterpret_cast<const uint8_t*>(O.B), O.beta,
+                           w.delta, nullptr, nullptr, nullptr, w.lin, hs);
+    else
+      e = launch_linear(DFSSM_PATH_AUTO, w.q, w.s, M, O.K, O.N, O.r, O.w_bits, O.alpha, O.A, O.B, O.beta, w.delta,
+                        nullptr, nullptr, nullptr, dfssm::carve_linear_workspace(w.lin, M, O.K, O.r), hs);
   }
   if (e == hipSuccess)
     e = dfssm::launch_add_rmsnorm_quant(w.u, w.delta, model->norm_f, eps, M, d.d_model, w.u, w.q, w.s, hs);

@@ -3,7 +3,8 @@ gather, every layer's norm -> in_proj -> conv + SSM step -> gated norm ->
 out_proj with the residual, final norm and LM head, over several tokens.
 
 Against the oracle: the same chain of oracle calls on the same seeded model
-(the 1.3B layer shapes, 2 layers, a 1,000-word table).  Every stage follows
+(the 1.3B layer shapes, 2 layers, a 1,000-word table), with int8 LoRA
+factors, and again with int4 ones.  Every stage follows
 one rounding order; the SSM output's fp64 sum is taken in another order on
 the device, which can move a value by one ulp and, rarely, a code of
 out_proj's input, so logits must agree within 1e-3 of their largest value
@@ -44,11 +45,25 @@ def model_host():
     return dict(E=E, scale=scale, norm_f=norm_f, layers=layers)
 
 
+@pytest.fixture(scope="module")
+def model_host_i4():
+    # the same model with int4 LoRA factors (r = 64) in every projection
+    layers = []
+    for l in range(L):
+        p = S.mamba_params(2048, key=(145, l))
+        layers.append(dict(p, in_proj=S.weights_i4(2048, 8512, 64, key=(146, l, 0)),
+                           out_proj=S.weights_i4(4096, 2048, 64, key=(146, l, 1))))
+    E, scale = S.embedding(V, 2048, key=(147,))
+    norm_f = np.random.default_rng(148).uniform(0.8, 1.2, 2048).astype(np.float32)
+    return dict(E=E, scale=scale, norm_f=norm_f, layers=layers)
+
+
 def device_model(D, mh):
     layers = []
     for ly in mh["layers"]:
         d = {k: dev(v) for k, v in ly.items() if k not in ("in_proj", "out_proj")}
-        d["in_proj"], d["out_proj"] = dev_weights(ly["in_proj"]), dev_weights(ly["out_proj"])
+        for pj in ("in_proj", "out_proj"):
+            d[pj] = {k: dev(v) for k, v in ly[pj].items()} if "A4" in ly[pj] else dev_weights(ly[pj])
         layers.append(d)
     return D.Mamba2(dev(mh["E"]), dev(mh["scale"]), dev(mh["norm_f"]), layers, d_state=128, eps=EPS)
 
@@ -62,17 +77,20 @@ class OracleModel:
         self.conv = [np.zeros((M, dm["conv_dim"], 4), np.float32) for _ in range(L)]
         self.ssm = [np.zeros((M, 64, 64, 128), np.float32) for _ in range(L)]
 
+    def _linear(self, q, s, w):
+        return (self.o.linear_i4(q, s, **w) if "A4" in w else self.o.linear(q, s, **w))["y32"]
+
     def step(self, tok):
         o, mh = self.o, self.mh
         u = o.embed_gather(mh["E"], mh["scale"], tok)
         delta = None
         for l, ly in enumerate(mh["layers"]):
             u, _, q, s = o.add_rmsnorm_quant(u, ly["norm_w"], EPS, delta=delta)
-            zx = o.linear(q, s, **ly["in_proj"])["y32"]
+            zx = self._linear(q, s, ly["in_proj"])
             y, _, self.conv[l], self.ssm[l] = o.ssm_step(zx, self.conv[l], self.ssm[l], ly["conv_w"], ly["conv_b"],
                                                          ly["dt_bias"], ly["A_log"], ly["D"], 4096, 128, 64)
             _, q, s = o.gate_norm_quant(y, zx[:, :4096], ly["gate_w"], EPS)
-            delta = o.linear(q, s, **ly["out_proj"])["y32"]
+            delta = self._linear(q, s, ly["out_proj"])
         _, _, q, s = o.add_rmsnorm_quant(u, mh["norm_f"], EPS, delta=delta)
         return o.lm_head(q, s, mh["E"], mh["scale"])[1]
 
@@ -97,6 +115,30 @@ def test_decode_step_against_oracle(env, model_host, M):
         exact += int(np.array_equal(lg.view(np.uint32), ref.view(np.uint32)))
     say(f"  {exact} of 5 tokens bit-exact")
     assert exact >= 3
+
+
+@pytest.mark.parametrize("M,steps", [(2, 4), (130, 1)])
+def test_decode_step_int4_lora(env, model_host_i4, M, steps):
+    # int4 factors in every projection: the few-token kernel reads them
+    # packed (both projections at M = 2, out_proj at M = 130); in_proj at
+    # M = 130 takes the prefill path on factors expanded in the workspace
+    torch, D, o = env
+    say(f"decode step, int4 LoRA, M={M} vs oracle")
+    m = device_model(D, model_host_i4)
+    ring, state = m.new_state(M)
+    ws = m.workspace(M)
+    om = OracleModel(o, model_host_i4, M)
+    exact = 0
+    for t in range(steps):
+        tok = S.tokens(M, V, key=(149, M, t))
+        ref = om.step(tok)
+        lg = host(m.decode_step(dev(tok), t, ring, state, ws))
+        torch.cuda.synchronize()
+        scale = float(np.abs(ref).max())
+        assert np.abs(lg.astype(np.float64) - ref).max() <= 1e-3 * scale, f"token {t}"
+        assert np.array_equal(lg.argmax(axis=1), ref.argmax(axis=1)), f"token {t}"
+        exact += int(np.array_equal(lg.view(np.uint32), ref.view(np.uint32)))
+    say(f"  {exact} of {steps} tokens bit-exact")
 
 
 def test_decode_step_graph_replays(env, model_host):

@@ -198,6 +198,18 @@ def test_model_step_validation(dl):
     assert dl.lib.dfssm_mamba2_state_bytes(ctypes.byref(m), 3, ctypes.byref(c), ctypes.byref(s)) == dl.OK
     assert c.value == 2 * 3 * 4 * 4352 * 4 and s.value == 2 * 3 * 64 * 64 * 128 * 4
     assert dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1) > 0
+    # int4 factors: lora_bits 4 (0 and 8 mean int8), even ranks, and room
+    # for the factors the prefill path expands
+    w8 = dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1024)
+    lay[1].lora_bits = 5
+    assert run(model()) == dl.ERR_SHAPE and "layer 1" in dl.last_error() and "lora_bits" in dl.last_error()
+    lay[0].lora_bits = lay[1].lora_bits = 4
+    lay[0].in_proj.r = 63
+    assert run(model()) == dl.ERR_SHAPE and "even" in dl.last_error()
+    lay[0].in_proj.r = 64
+    w4 = dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1024)
+    assert w4 >= w8 + 64 * 4096 + 2048 * 64     # out_proj: the larger linear workspace
+    assert dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1) > 0
 
 
 def test_int4_linear_validation(dl):
