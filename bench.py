@@ -51,6 +51,8 @@ def parse():
     p.add_argument("--no-lm-head", action="store_true", help="skip the LM head figures")
     p.add_argument("--no-model", action="store_true", help="skip the whole-model decode step figures")
     p.add_argument("--model-batches", default="1,8,32,128,512", help="batch sizes of the decode step figures")
+    p.add_argument("--model-i4-batches", default="1,32",
+                   help="batch sizes of the decode step figures with int4 LoRA factors")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="minimum CPU oracle sample time")
     p.add_argument("--copy-calibration-mib", type=int, default=0,
                    help="run one plain device copy of this size first (for HBM counter scaling)")
@@ -359,7 +361,8 @@ def main():
                                      if k not in ("in_proj", "out_proj"))
         table_bytes = table0[0].numel() + table0[1].numel() * 4
         model_fig = []
-        for Mb in [int(v) for v in args.model_batches.split(",") if v]:
+
+        def time_model(mdl, Mb, wbytes, label):
             ring, state = mdl.new_state(Mb)
             ws_m = mdl.workspace(Mb)
             tok = dev(S.tokens(Mb, S.VOCAB_1P3B, key=(152, Mb)))
@@ -387,14 +390,33 @@ def main():
             ms_tok = t0.elapsed_time(t1) / n
             # bytes a step must move at least: weights, table, parameters,
             # the SSM state read and written, the ring (3 slots read, 1 written)
-            step_bytes = weight_bytes + table_bytes + param_bytes + 2 * state.numel() * 4 + ring.numel() * 4
-            model_fig.append({"workload": f"Mamba-2-1.3B decode step, batch {Mb}, 48 layers + LM head",
+            step_bytes = wbytes + table_bytes + param_bytes + 2 * state.numel() * 4 + ring.numel() * 4
+            model_fig.append({"workload": f"Mamba-2-1.3B decode step, batch {Mb}, 48 layers + LM head{label}",
                               "ms_per_step": round(ms_tok, 4), "tokens_per_s": round(Mb / (ms_tok * 1e-3), 1),
                               "us_per_layer": round(ms_tok * 1e3 / 48, 2),
                               "bytes_per_step": int(step_bytes),
                               "effective_gbs": round(step_bytes / (ms_tok * 1e-3) / 1e9, 1)})
             del graphs, g, ring, state, ws_m, lg
             torch.cuda.synchronize()
+
+        for Mb in [int(v) for v in args.model_batches.split(",") if v]:
+            time_model(mdl, Mb, weight_bytes, "")
+        # the same model with int4 LoRA factors (r = 64) in every projection
+        i4_batches = [int(v) for v in args.model_i4_batches.split(",") if v]
+        if i4_batches:
+            del mdl
+            layers4, wbytes4 = [], 0
+            for l, lp in enumerate(layers):
+                lp4 = {k: v for k, v in lp.items() if k not in ("in_proj", "out_proj")}
+                for j, (pj, K, N) in enumerate((("in_proj", 2048, 8512), ("out_proj", 4096, 2048))):
+                    hw = S.weights_i4(K, N, 64, key=(153, l, j))
+                    wbytes4 += sum(v.nbytes for v in hw.values())
+                    lp4[pj] = {k: dev(v) for k, v in hw.items()}
+                layers4.append(lp4)
+            mdl = D.Mamba2(table0[0], table0[1], norm_f, layers4)
+            for Mb in i4_batches:
+                time_model(mdl, Mb, wbytes4, ", int4 LoRA")
+            del layers4
         del mdl, layers
 
     # ---- CPU oracle baseline on a bounded sample ----------------------------
