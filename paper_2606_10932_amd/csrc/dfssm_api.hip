@@ -757,10 +757,14 @@ dfssm_status dfssm_mamba2_decode_step(const dfssm_mamba2_model* model, int64_t M
       e = launch_linear(DFSSM_PATH_AUTO, w.q, w.s, M, I.K, I.N, I.r, I.w_bits, I.alpha, I.A, I.B, I.beta, w.zx,
                         nullptr, nullptr, nullptr, dfssm::carve_linear_workspace(w.lin, M, I.K, I.r), hs);
     if (e != hipSuccess) break;
+    // the SSM step applies the gate (y * silu(z), one fp32 product per
+    // channel, spread over its workgroups), so the norm after it is a plain
+    // RMSNorm: at batch 1 the gated norm's single workgroup otherwise spends
+    // ~1.2 us on the row's 2 d_model fp64 silus
     e = dfssm::launch_ssm_step(w.zx, d.ld, M, d.d_inner, d.N, step, conv_ring + l * ring_stride, L.conv_w, L.conv_b,
-                               L.dt_bias, L.A_log, L.D, ssm_state + l * state_stride, w.y, nullptr, hs);
+                               L.dt_bias, L.A_log, L.D, ssm_state + l * state_stride, w.y, nullptr, hs, true);
     if (e != hipSuccess) break;
-    e = dfssm::launch_gate_norm_quant(w.y, w.zx, d.ld, L.gate_w, eps, M, d.d_inner, w.q, w.s, hs);
+    e = dfssm::launch_add_rmsnorm_quant(w.y, nullptr, L.gate_w, eps, M, d.d_inner, nullptr, w.q, w.s, hs);
     if (e != hipSuccess) break;
     const dfssm_layer& O = L.out_proj;
     if (i4)

@@ -196,6 +196,7 @@ struct SsmArgs {
   float* state;       // [M][H][P][N]
   float* y;           // [M][d_inner]
   float* xbc;         // [M][conv_dim] or null
+  int gate_y;         // y * silu(z) instead of y
 };
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -237,6 +238,7 @@ __global__ __launch_bounds__(NT) void ssm_step(SsmArgs a) {
 
   // convolution step for this workgroup's PB x channels and all B, C channels
   __shared__ float xbc_s[PB + 2 * N];
+  __shared__ float gz_s[PB];  // silu(z) of the channels, when gating
   __shared__ float dt_s[2];
   const bool owns_bc = (hb == 0);
   float* ring = a.ring + m * 4 * (int64_t)conv_dim;
@@ -253,6 +255,7 @@ __global__ __launch_bounds__(NT) void ssm_step(SsmArgs a) {
     v = v + a.conv_b[c];
     const float o = silu_f(v);
     xbc_s[i] = o;
+    if (i < PB && a.gate_y) gz_s[i] = silu_f(zr[c]);
     if (i < PB || owns_bc) {
       ring[sw * (int64_t)conv_dim + c] = in;
       if (a.xbc) a.xbc[m * conv_dim + c] = o;
@@ -296,7 +299,12 @@ __global__ __launch_bounds__(NT) void ssm_step(SsmArgs a) {
     o.w = e[3];
     store_state(o, hs + j * NT);
     acc = sum_lanes<L>(acc);
-    if (nc == 0) a.y[m * a.d_inner + h * kHeadDim + p0 + p] = (float)(acc + (double)a.D[h] * (double)x);
+    if (nc == 0) {
+      const int c = h * kHeadDim + p0 + p;
+      float yv = (float)(acc + (double)a.D[h] * (double)x);
+      if (a.gate_y) yv = yv * gz_s[p];
+      a.y[m * a.d_inner + c] = yv;
+    }
   }
 }
 
@@ -334,10 +342,10 @@ hipError_t launch_gate_norm_quant(const float* y, const float* z, int64_t ldz, c
 hipError_t launch_ssm_step(const float* zx, int64_t ld, int64_t M, int64_t d_inner, int64_t d_state, int64_t step,
                            float* ring, const float* conv_w, const float* conv_b, const float* dt_bias,
                            const float* A_log, const float* D, float* state, float* y, float* xbc,
-                           hipStream_t st) {
+                           hipStream_t st, bool gate_y) {
   if (M == 0) return hipSuccess;
   const int H = (int)(d_inner / kHeadDim);
-  SsmArgs a{zx, ld, (int)d_inner, H, step, ring, conv_w, conv_b, dt_bias, A_log, D, state, y, xbc};
+  SsmArgs a{zx, ld, (int)d_inner, H, step, ring, conv_w, conv_b, dt_bias, A_log, D, state, y, xbc, gate_y ? 1 : 0};
   if (d_state == 128)
     launch_ssm_n<128>(a, M, st);
   else

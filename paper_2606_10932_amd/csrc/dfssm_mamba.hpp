@@ -21,10 +21,13 @@ hipError_t launch_gate_norm_quant(const float* y, const float* z, int64_t ldz, c
                                   int64_t M, int64_t d, int8_t* q, float* s, hipStream_t st);
 
 // Convolution step (4-slot ring per sequence) and SSM step of one token per
-// sequence; heads of 64 channels, d_state 64 or 128, one B/C group.
+// sequence; heads of 64 channels, d_state 64 or 128, one B/C group.  With
+// gate_y the output is y * silu(z) (z = zx[m][0 .. d_inner)), the gated
+// norm's first product in the same fp32 rounding, so that the norm itself
+// can run as a plain RMSNorm.
 hipError_t launch_ssm_step(const float* zx, int64_t ld, int64_t M, int64_t d_inner, int64_t d_state, int64_t step,
                            float* ring, const float* conv_w, const float* conv_b, const float* dt_bias,
                            const float* A_log, const float* D, float* state, float* y, float* xbc,
-                           hipStream_t st);
+                           hipStream_t st, bool gate_y = false);
 
 }  // namespace dfssm
