@@ -391,7 +391,9 @@ size_t dfssm_mamba2_workspace_bytes(const dfssm_mamba2_model* model, int64_t M);
  *     (q, s) = quantise(rmsnorm(y * silu(z)) * gate_w);  delta = out_proj(q, s)
  *   u += delta;  (q, s) = quantise(rmsnorm(u) * norm_f);  logits = lm_head(q, s)
  * with the entry points above (in_proj and out_proj on the automatic path,
- * through the int4 linear for layers with lora_bits = 4).
+ * through the int4 linear for layers with lora_bits = 4).  The gate's
+ * product y * silu(z) is taken inside the SSM step's kernel, in the same
+ * fp32 rounding, so the results are those of the entry points bit for bit.
  *   tok     [M] int32 device token ids (outside [0, vocab) -> a zero row)
  *   step    this token's position; only step & 3 is used (the ring slot)
  *   conv_ring, ssm_state   the state, updated in place
