@@ -71,7 +71,7 @@ struct NormArgs {
 };
 
 // One workgroup per token row, sized to the row (a multiple of 64 threads,
-// at most 1024); VPT float4 per thread held in registers.  The inputs and
+// at most 512 up to d = 8192, else 1024); VPT float4 per thread held in registers.  The inputs and
 // the weight are loaded together, before the reductions, so the row costs
 // one memory round trip.  GATE: g = y * silu(z); else g = u + delta.
 template <bool GATE, int VPT>
@@ -166,8 +166,12 @@ __global__ __launch_bounds__(kNormMaxThreads) void norm_quant(NormArgs a) {
 template <bool GATE>
 hipError_t launch_norm(const NormArgs& a, int64_t M, hipStream_t st) {
   const int64_t vec = dfssm::ceil_div(a.d, 4);   // float4 per row
-  const int vpt = (int)dfssm::ceil_div(vec, kNormMaxThreads);
-  const int nt = (int)std::min<int64_t>(kNormMaxThreads, dfssm::round_up(dfssm::ceil_div(vec, vpt), 64));
+  // at most 512 threads while 4 float4 per thread cover the row (d <= 8192):
+  // the cross-wave reductions then have 8 partials, not 16 (the 1.3B decode
+  // step at batch 1: 1.138 against 1.158 ms; 256 or 128 threads: 1.167)
+  const int maxt = dfssm::ceil_div(vec, 512) <= 4 ? 512 : kNormMaxThreads;
+  const int vpt = (int)dfssm::ceil_div(vec, maxt);
+  const int nt = (int)std::min<int64_t>(maxt, dfssm::round_up(dfssm::ceil_div(vec, vpt), 64));
   dim3 grid((unsigned)M), block(nt);
   if (vpt <= 1)
     norm_quant<GATE, 1><<<grid, block, 0, st>>>(a);
