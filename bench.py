@@ -122,7 +122,7 @@ def main():
             host0 = hs
         dl = [{k: dev(v) for k, v in ly.items()} for ly in hs]
         arr = D.make_layers(dl)
-        ws = torch.empty(D.chain_workspace_bytes(arr, M), dtype=torch.uint8, device="cuda")
+        ws = torch.zeros(D.chain_workspace_bytes(arr, M), dtype=torch.uint8, device="cuda")
         D.chain_prepare(arr, M, ws)
         copies.append(dl)
         arrays.append(arr)
@@ -178,7 +178,7 @@ def main():
         pw = {k: dev(v) for k, v in S.config_weights(4).items()}
         xq, xs = D.quantize_act(dev(S.config_activations(4, 2048)))
         yp = torch.empty((2048, 8512), dtype=torch.float32, device="cuda")
-        wsp = torch.empty(D.linear_workspace_bytes(2048, 2048, 8512, 64), dtype=torch.uint8, device="cuda")
+        wsp = D.linear_workspace(2048, 2048, 8512, 64)
 
         def pstep():
             D.scaffold_lora_linear(xq, xs, pw["w_bits"], pw["alpha"], pw["A"], pw["B"], pw["beta"], y=yp,
@@ -223,7 +223,7 @@ def main():
             for m in Ms:
                 qd, sd = D.quantize_act(dev(S.config_activations(cfg, m)))
                 yd = torch.empty((m, N), dtype=torch.float32, device="cuda")
-                wsd = torch.empty(D.linear_workspace_bytes(m, K, N, r), dtype=torch.uint8, device="cuda")
+                wsd = D.linear_workspace(m, K, N, r)
 
                 def calls():
                     for c in cps:

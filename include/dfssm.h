@@ -85,19 +85,14 @@ typedef enum {
   DFSSM_PATH_MFMA = 2,     /* sign bits expanded on chip + int8 MFMA, tiles of
                               128 tokens (prefill): an 8-wave ping-pong
                               kernel where each block gets at least 24 row
-                              tiles of 16, a 4-wave kernel otherwise.  Test
-                              switch: DFSSM_TEST_PREFILL_KERNEL=4 or 8 in the
-                              environment forces one of them. */
+                              tiles of 16, a 4-wave kernel otherwise
+                              (dfssm_test_switch can force one of them). */
   DFSSM_PATH_MFMA_FEW = 3  /* the same expansion and MFMA for M <= 512 in
                               one launch: 16 output rows and up to 32
                               tokens per workgroup (64 above 32 tokens), K
                               split over its waves, the LoRA
                               down-projection in workgroups of the same
-                              grid; M > 512 gives DFSSM_ERR_UNSUPPORTED.  Test switch: with the
-                              environment variable DFSSM_TEST_LOCAL_LORA=1
-                              no LoRA workgroups run and every output
-                              workgroup computes those values itself (the
-                              path it takes when they never arrive). */
+                              grid; M > 512 gives DFSSM_ERR_UNSUPPORTED. */
 } dfssm_path;
 
 /* Per-token absmax int8 quantisation of the activations (the int8 operand
@@ -113,13 +108,22 @@ typedef enum {
 dfssm_status dfssm_quantize_act(const void* x, int x_dtype, int64_t M, int64_t K,
                                 int64_t ldx, int8_t* q, float* s, void* stream);
 
-/* Bytes of device workspace dfssm_scaffold_lora_linear needs for (M,K,N,r). */
+/* Bytes of device workspace dfssm_scaffold_lora_linear needs for (M,K,N,r):
+ * about 1 MB of state kept from call to call, plus per-call staging. */
 size_t dfssm_linear_workspace_bytes(int64_t M, int64_t K, int64_t N, int64_t r);
 
 /* The scaffold + LoRA linear (Eq. 3 with a binary scaffold), on already
  * quantised activations (q, s).  Writes y [M,N].  `workspace` is device
  * memory of at least dfssm_linear_workspace_bytes(M,K,N,r) bytes, used for
- * acc_a and per-token staging; its contents on entry do not matter.
+ * acc_a, per-token staging and the exchange words of the few-token path.
+ * The workspace must hold zeros before its first use (hipMemset, or a
+ * zero-filled tensor); after that it belongs to the library: pass it back
+ * unchanged to later calls, of any shape and path, and do not run two
+ * calls on one workspace at the same time.  The exchange words are tagged
+ * per call: from a host counter for a call enqueued directly, and, for a
+ * call captured into a graph, from an epoch that the kernels themselves
+ * advance once per replay; so a captured call replayed any number of
+ * times, with new inputs, computes each replay from that replay's inputs.
  * Errors: NULL, SHAPE, ALIGN, WORKSPACE, DEVICE. */
 dfssm_status dfssm_scaffold_lora_linear(const int8_t* q, const float* s, int64_t M,
                                         int64_t K, int64_t N, int64_t r,
@@ -200,16 +204,21 @@ dfssm_status dfssm_scaffold_lora_chain(const dfssm_layer* layers, int n_layers, 
  * prepared workspace can be run any number of times, as long as nothing
  * but dfssm_chain_run writes to it in between.  Chains the persistent
  * kernel does not take (M > 1, K % 128 != 0, K > 4096, r % 4 != 0, ...)
- * need no preparation and return DFSSM_OK.
+ * run as a sequence of quantise and linear launches; for them preparation
+ * clears the linears' exchange state in the workspace.
  * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */
 dfssm_status dfssm_chain_prepare(const dfssm_layer* layers, int n_layers, int64_t M,
                                  void* workspace, size_t workspace_bytes, void* stream);
 
 /* Runs the chain (same contract as dfssm_scaffold_lora_chain) on a
- * workspace prepared for exactly these layers: at M = 1 one cooperative
- * kernel launch.  If the workspace's fingerprint does not match these
- * layers, the kernel leaves before reading the table, writes nothing and
- * sets status bit 8 (see dfssm_chain_status).
+ * workspace prepared for exactly these layers: at M = 1 one kernel launch
+ * of one workgroup per compute unit, which needs the whole grid resident at
+ * once (nothing else holding the GPU's compute units; otherwise its bounded
+ * waits end it with a status bit, see dfssm_chain_status).  If the
+ * workspace's fingerprint does not match these layers, the kernel leaves
+ * before reading the table, writes nothing and sets status bit 8.  The
+ * kernel advances an epoch in the workspace once per run, so a run captured
+ * in a graph can be replayed with new inputs.
  * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */
 dfssm_status dfssm_chain_run(const dfssm_layer* layers, int n_layers, int64_t M, const int8_t* q0,
                              const float* s0, float* y_all, void* workspace,
@@ -256,9 +265,8 @@ dfssm_status dfssm_embed_gather(const int8_t* E, const float* scale, int64_t V, 
  * Below 8 tokens, GEMV passes of up to 4 tokens (fewer for d > 4096), each
  * streaming the table once; from 8 tokens, when d is a multiple of 64 that
  * splits into 4..8 waves of at most 8 steps of 64 (d = 256 .. 4096), one
- * pass on the matrix cores that reads the table once for all tokens.  Test
- * switch: DFSSM_TEST_LM_HEAD_MFMA_TOKENS=<n> in the environment moves the
- * threshold of 8.
+ * pass on the matrix cores that reads the table once for all tokens
+ * (dfssm_test_switch can move the threshold of 8).
  * Limits: 0 < d <= 16384, d % 16 == 0; 0 <= V < 2^30; M >= 0 (M or V == 0
  * is a no-op).
  * Errors: NULL, SHAPE, ALIGN, DEVICE. */
@@ -398,17 +406,42 @@ size_t dfssm_mamba2_workspace_bytes(const dfssm_mamba2_model* model, int64_t M);
  *   step    this token's position; only step & 3 is used (the ring slot)
  *   conv_ring, ssm_state   the state, updated in place
  *   logits  [M][vocab] fp32 device output
+ * The workspace must hold zeros before its first use and belongs to the
+ * library after that, as dfssm_scaffold_lora_linear's does.
  * Graph capture: nothing here allocates, copies or synchronises, so the call
  * can be captured.  A captured step keeps its step & 3 (capture four graphs,
- * one per value, and replay the one for each token) and the per-call tags of
- * its few-token linears; it replays correctly because its linears share the
- * workspace, so every linear finds the exchange words left by another call.
+ * one per value, and replay the one for each token); its linears advance
+ * their exchange epoch on the device, so every replay computes from its own
+ * token ids and state.
  * Limits: d_model a multiple of 128 (<= 8192); d_state 64 or 128; every
  * layer's projections of those shapes; M >= 1; vocab >= 1.
  * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */
 dfssm_status dfssm_mamba2_decode_step(const dfssm_mamba2_model* model, int64_t M, const int32_t* tok,
                                       int64_t step, float* conv_ring, float* ssm_state, float* logits,
                                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---- test switches ------------------------------------------------------ */
+
+/* For tests only: forces a kernel-family choice that the automatic path
+ * would otherwise make, for the whole process (all switches start at 0,
+ * which leaves every choice automatic; a test sets a switch, runs its
+ * calls, and sets it back to 0).  Results are the same integers and bits
+ * on every choice; only the kernels that compute them change.
+ *   DFSSM_TEST_LOCAL_LORA          1: the few-token kernel launches no LoRA
+ *                                  workgroups; every output workgroup
+ *                                  computes acc_a itself (the path it takes
+ *                                  when the exchange words never arrive)
+ *   DFSSM_TEST_PREFILL_KERNEL      4 or 8: the 4-wave or the 8-wave prefill
+ *                                  kernel on the prefill path
+ *   DFSSM_TEST_LM_HEAD_MFMA_TOKENS n > 0: the LM head runs on the matrix
+ *                                  cores from n tokens instead of 8
+ * Errors: SHAPE for an unknown switch or value. */
+typedef enum {
+  DFSSM_TEST_LOCAL_LORA = 1,
+  DFSSM_TEST_PREFILL_KERNEL = 2,
+  DFSSM_TEST_LM_HEAD_MFMA_TOKENS = 3
+} dfssm_test_switch_id;
+dfssm_status dfssm_test_switch(int which, int value);
 
 /* Static text for a status code. */
 const char* dfssm_status_string(int status);

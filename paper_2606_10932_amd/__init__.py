@@ -25,7 +25,9 @@ EXPORTS = ["dfssm_quantize_act", "dfssm_linear_workspace_bytes", "dfssm_scaffold
            "dfssm_embed_gather", "dfssm_lm_head", "dfssm_add_rmsnorm_quant", "dfssm_gate_norm_quant",
            "dfssm_ssm_step", "dfssm_linear_i4_workspace_bytes", "dfssm_scaffold_lora_linear_i4",
            "dfssm_mamba2_state_bytes", "dfssm_mamba2_workspace_bytes",
-           "dfssm_mamba2_decode_step", "dfssm_status_string", "dfssm_last_error", "dfssm_version"]
+           "dfssm_mamba2_decode_step", "dfssm_test_switch", "dfssm_status_string", "dfssm_last_error",
+           "dfssm_version"]
+TEST_LOCAL_LORA, TEST_PREFILL_KERNEL, TEST_LM_HEAD_MFMA_TOKENS = 1, 2, 3
 
 
 class DfssmError(RuntimeError):
@@ -104,6 +106,8 @@ def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dfssm_mamba2_workspace_bytes.restype = sz
     lib.dfssm_mamba2_decode_step.argtypes = [mp, i64, vp, i64, vp, vp, vp, vp, sz, vp]
     lib.dfssm_mamba2_decode_step.restype = i32
+    lib.dfssm_test_switch.argtypes = [i32, i32]
+    lib.dfssm_test_switch.restype = i32
     lib.dfssm_status_string.argtypes = [i32]
     lib.dfssm_status_string.restype = ctypes.c_char_p
     lib.dfssm_last_error.restype = ctypes.c_char_p
@@ -158,6 +162,18 @@ def linear_workspace_bytes(M: int, K: int, N: int, r: int) -> int:
     return int(lib.dfssm_linear_workspace_bytes(M, K, N, r))
 
 
+def linear_workspace(M: int, K: int, N: int, r: int, device="cuda"):
+    """A zero-filled workspace for the linear (zeros before its first use;
+    pass it back unchanged to later calls)."""
+    return _torch().zeros(max(linear_workspace_bytes(M, K, N, r), 1), dtype=_torch().uint8, device=device)
+
+
+def test_switch(which: int, value: int):
+    """Test-only kernel-family switch (dfssm_test_switch); 0 restores the
+    automatic choice."""
+    _check(lib.dfssm_test_switch(which, value))
+
+
 def quantize_act(x, K: Optional[int] = None, q=None, s=None, stream=None):
     """Per-token absmax int8 quantisation of x ([M, ldx] fp16/fp32 device
     tensor, unit stride along K).  Returns (q int8 [M,K], s fp32 [M])."""
@@ -201,9 +217,8 @@ def scaffold_lora_linear(q, s, w_bits, alpha, A=None, B=None, beta=None, y=None,
     dev = q.device
     y = torch.empty((M, N), dtype=torch.float32, device=dev) if y is None else y
     _need(y, torch.float32, "y", 2)
-    nbytes = linear_workspace_bytes(M, K, N, r)
     if workspace is None:
-        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+        workspace = linear_workspace(M, K, N, r, device=dev)
     acc_s = acc_a = acc_b = None
     if acc:
         acc_s = torch.empty((M, N), dtype=torch.int32, device=dev)
@@ -247,7 +262,7 @@ def scaffold_lora_chain(layers, q0, s0, y_all=None, workspace=None, layer_arr=No
     if y_all is None:
         y_all = torch.empty(total, dtype=torch.float32, device=q0.device)
     if workspace is None:
-        workspace = torch.empty(max(chain_workspace_bytes(arr, M), 1), dtype=torch.uint8, device=q0.device)
+        workspace = torch.zeros(max(chain_workspace_bytes(arr, M), 1), dtype=torch.uint8, device=q0.device)
     _check(lib.dfssm_scaffold_lora_chain(arr, len(arr), M, q0.data_ptr(), s0.data_ptr(), y_all.data_ptr(),
                                          workspace.data_ptr(), workspace.numel(), _stream(stream)))
     outs, off = [], 0
@@ -415,8 +430,9 @@ class Mamba2:
                 torch.zeros(s // 4, dtype=torch.float32, device=device))
 
     def workspace(self, M: int, device="cuda"):
+        """A zero-filled workspace (zeros before its first use)."""
         torch = _torch()
-        return torch.empty(int(lib.dfssm_mamba2_workspace_bytes(ctypes.byref(self.struct), M)), dtype=torch.uint8,
+        return torch.zeros(int(lib.dfssm_mamba2_workspace_bytes(ctypes.byref(self.struct), M)), dtype=torch.uint8,
                            device=device)
 
     def decode_step(self, tok, step: int, conv_ring, ssm_state, workspace, logits=None, stream=None):
@@ -462,7 +478,7 @@ def scaffold_lora_linear_i4(q, s, w_bits, alpha, A4=None, B4=None, beta=None, y=
     y = torch.empty((M, N), dtype=torch.float32, device=dev) if y is None else y
     nbytes = int(lib.dfssm_linear_i4_workspace_bytes(M, K, N, r))
     if workspace is None:
-        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+        workspace = torch.zeros(max(nbytes, 1), dtype=torch.uint8, device=dev)
     acc_s = acc_a = acc_b = None
     if acc:
         acc_s = torch.empty((M, N), dtype=torch.int32, device=dev)

@@ -62,15 +62,7 @@ dfssm_status check_ptrs(std::initializer_list<Ptr> required, std::initializer_li
   return DFSSM_OK;
 }
 
-// Per-launch tag of the persistent chain's exchange words (24 bits, never 0).
-uint32_t next_chain_seq() {
-  static std::atomic<uint32_t> seq{0};
-  uint32_t s;
-  do {
-    s = (seq.fetch_add(1, std::memory_order_relaxed) + 1) & 0xffffffu;
-  } while (s == 0);
-  return s;
-}
+std::atomic<int> g_switch[4];  // dfssm_test_switch values, index = switch id
 
 size_t linear_ws_bytes(int64_t M, int64_t K, int64_t r) {
   return dfssm::carve_linear_workspace(nullptr, M, K, r).bytes;
@@ -147,7 +139,25 @@ hipError_t launch_linear_i4(int path, const int8_t* q, const float* s, int64_t M
 
 }  // namespace
 
+namespace dfssm {
+int test_switch(int which) { return which > 0 && which < 4 ? g_switch[which].load(std::memory_order_relaxed) : 0; }
+}  // namespace dfssm
+
 extern "C" {
+
+dfssm_status dfssm_test_switch(int which, int value) {
+  clear_error();
+  bool ok = false;
+  switch (which) {
+    case DFSSM_TEST_LOCAL_LORA: ok = value == 0 || value == 1; break;
+    case DFSSM_TEST_PREFILL_KERNEL: ok = value == 0 || value == 4 || value == 8; break;
+    case DFSSM_TEST_LM_HEAD_MFMA_TOKENS: ok = value >= 0; break;
+    default: break;
+  }
+  if (!ok) return fail(DFSSM_ERR_SHAPE, "test switch %d: value %d", which, value);
+  g_switch[which].store(value, std::memory_order_relaxed);
+  return DFSSM_OK;
+}
 
 const char* dfssm_version(void) { return "dfssm-gfx950 0.1"; }
 
@@ -279,11 +289,11 @@ dfssm_status dfssm_scaffold_lora_linear(const int8_t* q, const float* s, int64_t
 // chain (M = 1): layer table, its 64-bit fingerprint, then the exchange
 // region: y_ll (one 64-bit word per output of every linear), y_rel (one copy
 // of y_ll per XCD), acc_rel (per XCD, n_layers x kMaxRank words), xmap (one
-// word per workgroup) and the status word.  The larger of the two is
-// required.
+// word per workgroup), the status word and the epoch words.  The larger
+// of the two is required.
 struct ChainLayout {
   size_t off_s, off_lin, seq_bytes;
-  size_t off_table, off_hash, off_yll, off_yrel, off_acc, off_xmap, off_status, pers_bytes;
+  size_t off_table, off_hash, off_yll, off_yrel, off_acc, off_xmap, off_status, off_epoch, pers_bytes;
   int64_t y_words;
 };
 
@@ -316,6 +326,8 @@ static ChainLayout chain_layout(const dfssm_layer* layers, int n_layers, int64_t
   o += (size_t)dfssm::chain_grid() * 8;
   c.off_status = o;
   o += 256;
+  c.off_epoch = o;
+  o += (size_t)dfssm::kEpochGroups * dfssm::kEpochStride * 8;
   c.pers_bytes = o;
   return c;
 }
@@ -407,12 +419,18 @@ dfssm_status dfssm_chain_prepare(const dfssm_layer* layers, int n_layers, int64_
   ChainLayout c;
   st = chain_common(layers, n_layers, M, workspace, workspace_bytes, &c);
   if (st != DFSSM_OK) return st;
-  if (!dfssm::chain_persistent_supported(layers, n_layers, M, dfssm::chain_grid())) return DFSSM_OK;
+  char* base = static_cast<char*>(workspace);
+  if (!dfssm::chain_persistent_supported(layers, n_layers, M, dfssm::chain_grid())) {
+    // the host-sequenced chain: its linears' epoch word and exchange words
+    hipError_t e = dfssm::launch_zero_words(reinterpret_cast<uint64_t*>(base + c.off_lin),
+                                            (int64_t)(dfssm::kLinearStateBytes / 8), (hipStream_t)stream);
+    return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain prepare launch");
+  }
   static thread_local std::vector<dfssm::ChainLayerDev> table;
   const uint64_t h = chain_table(layers, n_layers, table);
-  char* base = static_cast<char*>(workspace);
   auto* exch = reinterpret_cast<uint64_t*>(base + c.off_yll);
-  const int64_t exch_words = (int64_t)(c.off_status + 8 - c.off_yll) / 8;
+  // through the status word and the epoch words after it
+  const int64_t exch_words = (int64_t)(c.pers_bytes - c.off_yll) / 8;
   hipError_t e = dfssm::launch_chain_setup(table.data(), reinterpret_cast<dfssm::ChainLayerDev*>(base + c.off_table),
                                            n_layers, exch, exch_words,
                                            reinterpret_cast<uint64_t*>(base + c.off_hash), h, (hipStream_t)stream);
@@ -444,10 +462,11 @@ dfssm_status dfssm_chain_run(const dfssm_layer* layers, int n_layers, int64_t M,
     ex.acc_rel = reinterpret_cast<uint64_t*>(base + c.off_acc);
     ex.xmap = reinterpret_cast<uint64_t*>(base + c.off_xmap);
     ex.status = reinterpret_cast<unsigned*>(base + c.off_status);
+    ex.epoch = reinterpret_cast<uint64_t*>(base + c.off_epoch);
     ex.r_max = 0;
     for (int l = 0; l < n_layers; ++l) ex.r_max = std::max(ex.r_max, (int32_t)layers[l].r);
     hipError_t e = dfssm::launch_chain_run(reinterpret_cast<const dfssm::ChainLayerDev*>(base + c.off_table),
-                                           n_layers, q0, s0, ex, y_all, next_chain_seq(),
+                                           n_layers, q0, s0, ex, y_all,
                                            reinterpret_cast<const uint64_t*>(base + c.off_hash), h, hs);
     return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain run launch");
   }
@@ -479,7 +498,16 @@ dfssm_status dfssm_chain_run(const dfssm_layer* layers, int n_layers, int64_t M,
 dfssm_status dfssm_scaffold_lora_chain(const dfssm_layer* layers, int n_layers, int64_t M,
                                        const int8_t* q0, const float* s0, float* y_all,
                                        void* workspace, size_t workspace_bytes, void* stream) {
-  dfssm_status st = dfssm_chain_prepare(layers, n_layers, M, workspace, workspace_bytes, stream);
+  // everything the run checks is checked before the prepare enqueues
+  clear_error();
+  dfssm_status st = validate_chain(layers, n_layers, M);
+  if (st != DFSSM_OK || n_layers == 0 || M == 0) return st;
+  st = check_ptrs({{q0, "q0"}, {s0, "s0"}, {y_all, "y_all"}}, {});
+  if (st != DFSSM_OK) return st;
+  ChainLayout c;
+  st = chain_common(layers, n_layers, M, workspace, workspace_bytes, &c);
+  if (st != DFSSM_OK) return st;
+  st = dfssm_chain_prepare(layers, n_layers, M, workspace, workspace_bytes, stream);
   if (st != DFSSM_OK) return st;
   return dfssm_chain_run(layers, n_layers, M, q0, s0, y_all, workspace, workspace_bytes, stream);
 }

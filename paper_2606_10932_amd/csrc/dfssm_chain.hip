@@ -9,8 +9,12 @@
 //
 //  * Data crosses workgroups as 64-bit words {tag:32, value:32}, so a
 //    consumer polls the data itself: a word is valid once its tag equals
-//    the linear's tag.  Tags carry a per-launch sequence number, so words
-//    left from an earlier launch never validate.  No fences are used (on
+//    the linear's tag.  Tags carry the launch's epoch, kept on the device:
+//    every workgroup arrives once, at its start, on the workspace's epoch
+//    words (dfssm_dev::arrive, 64 words so that arrivals meet at 64
+//    addresses), and each word's last arrival moves it on; so words left
+//    from an earlier launch (or an earlier replay of a captured launch)
+//    never validate.  No fences are used (on
 //    MI355X a release/acquire pair costs ~3.5 us: it writes back and
 //    invalidates the whole L2).
 //  * Two levels of exchange.  MI355X has 8 XCDs, each with its own L2; a
@@ -52,6 +56,8 @@
 //    kernel compares that fingerprint with the caller's before it reads the
 //    table, and leaves (status bit 8) if they differ.
 #include <float.h>
+
+#include <algorithm>
 
 #include "dfssm_internal.hpp"
 
@@ -250,7 +256,7 @@ __device__ __forceinline__ bool poll_xcd(__amdgpu_buffer_rsrc_t rs, uint32_t wor
 
 __global__ __launch_bounds__(kCT, 1) void chain_persistent(
     const dfssm::ChainLayerDev* __restrict__ layers, int L, const int8_t* __restrict__ q0,
-    const float* __restrict__ s0, dfssm::ChainExch ex, float* __restrict__ y_all, uint32_t seq,
+    const float* __restrict__ s0, dfssm::ChainExch ex, float* __restrict__ y_all,
     const uint64_t* __restrict__ table_hash, uint64_t expect_hash) {
   unsigned* const status = ex.status;
   // the table was written by a prepare of the same layers, or nothing here
@@ -278,12 +284,22 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
   __shared__ int sumq_lds;
   __shared__ int abort_;
   __shared__ int rho_lds, nx_lds;
+  __shared__ uint32_t seq_lds;
   const int wg = blockIdx.x, nwg = gridDim.x;
   const int tid = threadIdx.x;
   const int group = tid / kGT, gt = tid % kGT, lane = gt & 63, wave = gt >> 6;
   const int wave16 = tid >> 6;  // wave index in the workgroup
 
-  // a word written for linear l carries tag(l); seq differs per launch
+  // the launch's epoch: one arrival per workgroup; the 24-bit sequence
+  // number derived from it is never 0, so zeroed words never validate
+  if (tid == 0) {
+    const uint64_t old = dfssm_dev::arrive(ex.epoch, wg);
+    seq_lds = (uint32_t)((old >> 32) % 0xffffffu) + 1u;
+    dfssm_dev::advance_if_last(ex.epoch, wg, old, nwg);
+  }
+  __syncthreads();
+  const uint32_t seq = seq_lds;
+  // a word written for linear l carries tag(l)
   auto tag_of = [seq](int l) -> uint32_t { return (seq << 8) | (uint32_t)((l + 1) & 0xff); };
   const uint32_t tag_place = seq << 8;
 
@@ -718,14 +734,27 @@ hipError_t launch_chain_setup(const ChainLayerDev* table_host, ChainLayerDev* ta
   return hipSuccess;
 }
 
+// A plain launch: one workgroup per CU fits (launch bounds of 1024 threads,
+// one block per CU), and the kernel's placement step waits, with a bound,
+// for every workgroup to publish its XCD; a grid that is not resident
+// together (other work holding CUs for longer than that bound) ends with
+// the placement status bit instead of waiting.
+hipError_t launch_zero_words(uint64_t* p, int64_t words, hipStream_t st) {
+  if (words <= 0) return hipSuccess;
+  SetupArgs a{};
+  a.zero_base = p;
+  a.zero_words = words;
+  const int64_t blocks = std::min<int64_t>(1024, ceil_div(words, 256));
+  chain_setup<<<dim3((unsigned)blocks), dim3(256), 0, st>>>(a);
+  return hipGetLastError();
+}
+
 hipError_t launch_chain_run(const ChainLayerDev* table_dev, int n_layers, const int8_t* q0, const float* s0,
-                            const ChainExch& ex, float* y_all, uint32_t seq, const uint64_t* hash_dev,
-                            uint64_t hash, hipStream_t st) {
-  int L = n_layers;
-  ChainExch e = ex;
-  void* args[] = {(void*)&table_dev, (void*)&L,   (void*)&q0,       (void*)&s0,   (void*)&e,
-                  (void*)&y_all,     (void*)&seq, (void*)&hash_dev, (void*)&hash};
-  return hipLaunchCooperativeKernel((const void*)chain_persistent, dim3(chain_grid()), dim3(kCT), args, 0, st);
+                            const ChainExch& ex, float* y_all, const uint64_t* hash_dev, uint64_t hash,
+                            hipStream_t st) {
+  chain_persistent<<<dim3(chain_grid()), dim3(kCT), 0, st>>>(table_dev, n_layers, q0, s0, ex, y_all, hash_dev,
+                                                            hash);
+  return hipGetLastError();
 }
 
 }  // namespace dfssm

@@ -27,28 +27,60 @@ constexpr int kDecodeMaxTokens = 4;
 constexpr int64_t kDecodeM0 = 0;
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Test switches (dfssm_test_switch), all 0 unless a test sets them: the
+// kernel-family choices below read them on the host at each launch.
+//   local_lora:           1 = the few-token kernel launches no LoRA
+//                         workgroups (every output workgroup computes those
+//                         values itself)
+//   prefill_kernel:       0 = automatic, 4 or 8 = that prefill kernel
+//   lm_head_mfma_tokens:  0 = 8; else the token count from which the LM
+//                         head runs on the matrix cores
+int test_switch(int which);
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 
 // Per-call workspace (device), every region 256-byte aligned:
+//   epoch  uint64 [64][16]        64 words {epoch:32, arrivals:32} of the
+//                                 few-token kernel, one per 128-byte line
+//   xw     uint64 [kXwWords]      {tag, value} words of the few-token kernel:
+//                                 acc_a limbs per (token, rank), then sum Q;
+//                                 a region of fixed size at a fixed offset,
+//                                 so no other kernel or shape writes over it
 //   acc_a  int32 [M][r]           LoRA down-projection
 //   limbs  int8  [4][M][rp]       acc_a split into 4 signed base-256 digits,
 //                                 rp = r rounded up to 64 (zero padded)
 //   sumq   int32 [M]              sum_k Q[m,k]
 //   planes uint32 [M][8][C][4]    two's-complement bit-planes of Q, C =
 //                                 ceil(K/128) chunks of 4 words (zero padded)
-//   xw     uint64 [M*rp + M]      {tag, value} words of the few-token kernel:
-//                                 acc_a limbs per (token, rank), then sum Q
+// The epoch word and the words carry state from call to call: the
+// workspace must hold zeros before its first use, and after that only the
+// library writes it.
 struct LinearWorkspace {
+  uint64_t* epoch;
+  uint64_t* xw;
   int32_t* acc_a;
   int8_t* limbs;
   int32_t* sumq;
   uint32_t* planes;
-  uint64_t* xw;
   size_t bytes;
 };
 
 inline int64_t rank_padded(int64_t r) { return round_up(r > 0 ? r : 1, 64); }
 inline int64_t plane_chunks(int64_t K) { return ceil_div(K, 128); }
+
+// Few tokens on the matrix cores: the largest M of the one-launch kernel on
+// request, and of its automatic use.
+constexpr int64_t kSkinnyMaxTokens = 32;
+constexpr int64_t kSkinnyChunkedMaxTokens = 512;
+// Exchange words of the few-token kernel: M*rp limb words, then M sum-Q
+// words, for every M <= kSkinnyChunkedMaxTokens and r <= kMaxRank.
+constexpr int64_t kXwWords = kSkinnyChunkedMaxTokens * kMaxRank + kSkinnyChunkedMaxTokens;
+// Epoch words of the few-token kernel (its arrivals spread over them) and
+// their spacing in 64-bit words.
+constexpr int kEpochGroups = 64;
+constexpr int kEpochStride = 16;
+// Bytes before the first per-call region: the epoch words and the words.
+constexpr size_t kLinearStateBytes = (size_t)kEpochGroups * kEpochStride * 8 + (size_t)kXwWords * 8;
 
 inline LinearWorkspace carve_linear_workspace(void* base, int64_t M, int64_t K, int64_t r) {
   LinearWorkspace ws{};
@@ -58,17 +90,19 @@ inline LinearWorkspace carve_linear_workspace(void* base, int64_t M, int64_t K, 
     off += (size_t)round_up((int64_t)n, 256);
     return o;
   };
+  size_t o_ep = take((size_t)kEpochGroups * kEpochStride * 8);
+  size_t o_xw = take((size_t)kXwWords * 8);
   size_t o_acc = take((size_t)(M * r) * 4);
   size_t o_limb = take((size_t)(4 * M * rank_padded(r)));
   size_t o_sum = take((size_t)M * 4);
   size_t o_pl = take((size_t)(M * plane_chunks(K) * 128));
-  size_t o_xw = take((size_t)(M * rank_padded(r) + M) * 8);
   char* b = static_cast<char*>(base);
+  ws.epoch = reinterpret_cast<uint64_t*>(b + o_ep);
+  ws.xw = reinterpret_cast<uint64_t*>(b + o_xw);
   ws.acc_a = reinterpret_cast<int32_t*>(b + o_acc);
   ws.limbs = reinterpret_cast<int8_t*>(b + o_limb);
   ws.sumq = reinterpret_cast<int32_t*>(b + o_sum);
   ws.planes = reinterpret_cast<uint32_t*>(b + o_pl);
-  ws.xw = reinterpret_cast<uint64_t*>(b + o_xw);
   ws.bytes = off;
   return ws;
 }
@@ -92,11 +126,8 @@ hipError_t launch_decode_linear(const int8_t* q, const float* s, int64_t M, int6
 // Few tokens (M <= kSkinnyMaxTokens) on the matrix cores, one launch: LoRA
 // workgroups publish acc_a and sum Q as tagged words while the others run a
 // split-K expanded-sign int8 MFMA product over 16 output rows each, then the
-// LoRA up-projection and epilogue.
-constexpr int64_t kSkinnyMaxTokens = 32;
-// Largest M the few-token kernel takes on request: its output blocks then
-// take one 32-token chunk each (a second grid dimension).
-constexpr int64_t kSkinnyChunkedMaxTokens = 512;
+// LoRA up-projection and epilogue.  Above kSkinnyMaxTokens, on request, its
+// output blocks take one chunk of tokens each (a second grid dimension).
 hipError_t launch_skinny_linear(const int8_t* q, const float* s, int64_t M, int64_t K, int64_t N,
                                 int64_t r, const uint32_t* w_bits, const float* alpha,
                                 const int8_t* A, const int8_t* B, const float* beta, float* y,
@@ -155,6 +186,7 @@ struct ChainExch {
   uint64_t* acc_rel;
   uint64_t* xmap;
   unsigned* status;
+  uint64_t* epoch;  // kEpochGroups words {epoch:32, arrivals:32}, advanced once per launch
   int64_t ysum;
   int32_t r_max;
 };
@@ -186,10 +218,12 @@ bool chain_persistent_supported(const dfssm_layer* layers, int n_layers, int64_t
 hipError_t launch_chain_setup(const ChainLayerDev* table_host, ChainLayerDev* table_dev, int n_layers,
                               uint64_t* exch, int64_t exch_words, uint64_t* hash_dev, uint64_t hash,
                               hipStream_t st);
-// Cooperative launch of the persistent chain kernel on a prepared workspace.
+// Zeroes `words` 64-bit words at p with a fill kernel (capture-safe).
+hipError_t launch_zero_words(uint64_t* p, int64_t words, hipStream_t st);
+// Launch of the persistent chain kernel on a prepared workspace.
 hipError_t launch_chain_run(const ChainLayerDev* table_dev, int n_layers, const int8_t* q0, const float* s0,
-                            const ChainExch& ex, float* y_all, uint32_t seq, const uint64_t* hash_dev,
-                            uint64_t hash, hipStream_t st);
+                            const ChainExch& ex, float* y_all, const uint64_t* hash_dev, uint64_t hash,
+                            hipStream_t st);
 
 }  // namespace dfssm
 
@@ -226,6 +260,40 @@ __device__ __forceinline__ float epilogue(float s, float alpha, float beta, int3
     w = u + v;
   }
   return s * w;
+}
+
+
+// Device-side epoch of a kernel's exchange words, kept in kEpochGroups words
+// {epoch:32, arrivals:32} kEpochStride words apart: each of a launch's
+// `arrivals` members (index i) arrives once with a fetch-add on word
+// i % kEpochGroups, which hands it the epoch; the last member of each word
+// moves it on to {epoch + 1, 0}, and member 0 moves on the words no member
+// uses.  All words start at {0, 0}, so they stay equal between launches.
+// Member i's arrival on its epoch word: returns the word before it.
+__device__ __forceinline__ uint64_t arrive(uint64_t* ep, int i) {
+  return __hip_atomic_fetch_add(ep + (i % dfssm::kEpochGroups) * dfssm::kEpochStride, 1ull, __ATOMIC_RELAXED,
+                                __HIP_MEMORY_SCOPE_AGENT);
+}
+// Tag of the words of the call whose arrival returned `old`: below 2^31
+// and never 0, so zeroed memory never validates.
+__device__ __forceinline__ uint32_t epoch_tag(uint64_t old) {
+  const uint32_t t = ((uint32_t)(old >> 32) + 1u) & 0x7fffffffu;
+  return t ? t : 1u;
+}
+// After member i's arrival returned `old`: the last member of its word
+// moves that word on to {epoch + 1, 0} (every other arrival of the call on
+// it precedes this one, so none reads the new epoch); member 0 does the
+// same for the words no member uses (calls of fewer than 64 members).
+__device__ __forceinline__ void advance_if_last(uint64_t* ep, int i, uint64_t old, int arrivals) {
+  constexpr int G = dfssm::kEpochGroups;
+  const int g = i % G;
+  const int members = arrivals / G + (g < arrivals % G ? 1 : 0);
+  const uint64_t next = (uint64_t)((uint32_t)(old >> 32) + 1u) << 32;
+  if ((uint32_t)old == (uint32_t)(members - 1))
+    __hip_atomic_store(ep + g * dfssm::kEpochStride, next, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (i == 0)
+    for (int e = arrivals; e < G; ++e)
+      __hip_atomic_store(ep + e * dfssm::kEpochStride, next, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 }  // namespace dfssm_dev

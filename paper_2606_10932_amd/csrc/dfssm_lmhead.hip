@@ -28,11 +28,11 @@ namespace {
 
 constexpr int kThreads = 256;
 
-// Tokens from which the LM head runs on the matrix cores.  Test switch:
-// DFSSM_TEST_LM_HEAD_MFMA_TOKENS=<n> in the environment moves the threshold.
+// Tokens from which the LM head runs on the matrix cores (8; the test switch
+// lm_head_mfma_tokens moves it).
 int lm_head_mfma_tokens() {
-  const char* v = getenv("DFSSM_TEST_LM_HEAD_MFMA_TOKENS");
-  return v ? atoi(v) : 8;
+  const int v = dfssm::test_switch(DFSSM_TEST_LM_HEAD_MFMA_TOKENS);
+  return v > 0 ? v : 8;
 }
 
 // rows per wave visit: 4 KB of the table, or one row when rows are longer

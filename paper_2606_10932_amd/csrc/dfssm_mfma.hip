@@ -1079,13 +1079,12 @@ hipError_t launch_mfma_linear(const int8_t* q, const float* s, int64_t M, int64_
   const int64_t nt16 = ceil_div(N, 16);
   // the 8-wave ping-pong kernel (one block per CU) where the runs are long
   // enough to keep its 8 waves busy (at least 24 row tiles), else the 4-wave
-  // kernel (two blocks per CU).  Test switch: DFSSM_TEST_PREFILL_KERNEL=4 or 8.
+  // kernel (two blocks per CU).  Test switch prefill_kernel: 4 or 8.
   int64_t bpm8 = std::min(std::max(ceil_div(cus, nbm), ceil_div(nt16, kPPRunMax)), nt16);
   bool use8 = nt16 >= 24 * bpm8;
-  if (const char* v = getenv("DFSSM_TEST_PREFILL_KERNEL")) {
-    if (v[0] == '4') use8 = false;
-    if (v[0] == '8') use8 = true;
-  }
+  const int forced = test_switch(DFSSM_TEST_PREFILL_KERNEL);
+  if (forced == 4) use8 = false;
+  if (forced == 8) use8 = true;
   int64_t bpm = use8 ? bpm8 : std::min(std::max(ceil_div(2 * cus, nbm), ceil_div(nt16, kRunMax)), nt16);
   const int64_t grid = nbm * bpm;
   GemmArgs ga{q, s, (int)M, (int)K, (int)N, (int)r, rp, w_bits, alpha, ws.limbs, B, beta, ws.sumq, y,

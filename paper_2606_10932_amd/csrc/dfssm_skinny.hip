@@ -23,14 +23,26 @@
 // One launch: the first nb_lora workgroups compute the LoRA down-projection
 // acc_a = Q A^T (one wave per rank and 4 tokens) and sum_k Q, and publish
 // them as 64-bit words {tag, value} (value: acc_a's 4 signed base-256 limbs
-// as bytes, or sum Q) with agent-scope stores; tag is unique per call, so a
-// word left by an earlier call never validates.  The other workgroups read
-// the words they need after their scaffold product.  The wait is bounded:
+// as bytes, or sum Q) with agent-scope stores; a word is valid once its tag
+// is the call's.  A call enqueued directly takes its tag from a host counter
+// (bit 31 set).  A call captured into a graph would replay with a frozen
+// argument, so there the tag is the call's epoch + 1 (below 2^31), kept on
+// the device so that every replay moves it on.  Every reader and writer of the words (each publishing LoRA
+// wave, each output workgroup) is a member of the call with an index i, and
+// arrives once, at its start, with a 64-bit fetch-add on epoch word i % 64
+// of the workspace ({epoch, arrivals}, one per 128-byte line, so that
+// arrivals meet at 64 addresses and not one), which hands it the epoch;
+// the last member to arrive on a word stores {epoch + 1, 0} there, and
+// member 0 stores it into every word no member of this call uses.  All 64
+// words start at {0, 0} and each call moves every one of them on by one,
+// so all of one call agree on its epoch, the next call (stream-ordered
+// after it) starts from the next one, and a word left by an earlier call
+// never validates.
+// The other workgroups read the words they need after their scaffold
+// product.  The wait is bounded:
 // a lane whose words have not arrived after `spin` polls computes the values
 // itself from A and Q (the integers are the same either way), so no
 // workgroup depends on another being scheduled.
-#include <stdlib.h>
-
 #include <algorithm>
 #include <atomic>
 
@@ -144,10 +156,15 @@ struct SkinnyArgs {
   int64_t* acc_b_out;
   int32_t* acc_a;  // [M][r], written by the LoRA workgroups (and by fallback lanes)
   uint64_t* xw;    // [M][rp] limb words, then [M] sum-Q words
-  uint32_t tag;
+  uint64_t* epoch; // kEpochGroups words {epoch:32, arrivals:32}, kEpochStride apart;
+                   // NULL: the call's tag is host_tag
+  uint32_t host_tag;
+  int arrivals;    // members per call: publishing LoRA waves, then output workgroups
+  int lora_members;  // publishing LoRA waves (members 0 .. lora_members - 1)
   int nb_lora;     // LoRA workgroups at the front of the grid
   int spin;        // polls of a missing word before computing it locally
 };
+
 
 __device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
   return __builtin_amdgcn_sdot4((int)a, (int)b, c, false);
@@ -213,6 +230,10 @@ __device__ void lora_block(const SkinnyArgs& a) {
   const int item = (int)blockIdx.x * nw + wave;
   const int j = item % rp, m0 = (item / rp) * kPrepTokens;
   if (m0 >= M) return;
+  // a publishing wave arrives once, at its start (device-epoch calls); the
+  // epoch is needed only when it publishes
+  uint64_t ep_old = 0;
+  if (a.epoch && lane == 0) ep_old = dfssm_dev::arrive(a.epoch, item);
   const int mt = min(kPrepTokens, M - m0);
   const bool jr = j < r, qsum = j == 0;
   int acc[kPrepTokens], qs[kPrepTokens];
@@ -269,19 +290,24 @@ __device__ void lora_block(const SkinnyArgs& a) {
       }
     }
   }
+  const uint64_t old = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(ep_old >> 32)) << 32) |
+                       (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)ep_old);
+  const uint32_t tag = a.epoch ? dfssm_dev::epoch_tag(old) : a.host_tag;
   if (lane < mt) {
     const int m = m0 + lane;
     if (jr) a.acc_a[(int64_t)m * r + j] = mine;
-    word_store(a.xw + (int64_t)m * rp + j, a.tag, pack_limbs(mine));  // zero limbs for ranks in [r, rp)
-    if (qsum) word_store(a.xw + (int64_t)M * rp + m, a.tag, (uint32_t)mine_q);
+    word_store(a.xw + (int64_t)m * rp + j, tag, pack_limbs(mine));  // zero limbs for ranks in [r, rp)
+    if (qsum) word_store(a.xw + (int64_t)M * rp + m, tag, (uint32_t)mine_q);
   }
+  if (a.epoch && lane == 0) dfssm_dev::advance_if_last(a.epoch, item, old, a.arrivals);
 }
 
 // The limbs of acc_a[m][j0 + 16kg .. +15] as 4 limb operands (byte e of limb
 // t = limb t of rank j0 + 16kg + e) and, with want_sq, sum Q of token m: from
 // the LoRA workgroups' words, or computed here once `spin` polls have passed.
 template <bool L4>
-__device__ void fetch_lora(const SkinnyArgs& a, int m, int j0, int kg, v4i (&lm)[4], int* sq, bool store_acc) {
+__device__ void fetch_lora(const SkinnyArgs& a, uint32_t tag, int m, int j0, int kg, v4i (&lm)[4], int* sq,
+                           bool store_acc) {
   const uint64_t* wp = a.xw + (int64_t)m * a.rp + j0 + 16 * kg;
   const uint64_t* sp = a.xw + (int64_t)a.M * a.rp + m;
   uint32_t val[16], vq = 0;
@@ -292,9 +318,9 @@ __device__ void fetch_lora(const SkinnyArgs& a, int m, int j0, int kg, v4i (&lm)
 #pragma unroll
       for (int e = 0; e < 16; ++e) w[e] = word_load(wp + e);
       if (sq) wq = word_load(sp);
-      bool ok = !sq || (uint32_t)(wq >> 32) == a.tag;
+      bool ok = !sq || (uint32_t)(wq >> 32) == tag;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) ok = ok && (uint32_t)(w[e] >> 32) == a.tag;
+      for (int e = 0; e < 16; ++e) ok = ok && (uint32_t)(w[e] >> 32) == tag;
       if (ok) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) val[e] = (uint32_t)w[e];
@@ -334,10 +360,16 @@ __device__ void fetch_lora(const SkinnyArgs& a, int m, int j0, int kg, v4i (&lm)
 template <int MT, int S, bool L4>
 __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   __shared__ v4i red[kMaxWaves][MT][64];
+  __shared__ uint32_t tag_lds;
   if ((int)blockIdx.x < a.nb_lora) {
     if (blockIdx.y == 0) lora_block<L4>(a);  // one set of LoRA workgroups for all tokens
     return;
   }
+  // an output workgroup arrives once, at its start (device-epoch calls); the
+  // epoch is needed only after the scaffold product
+  const int member = a.lora_members + (int)blockIdx.y * (int)(gridDim.x - a.nb_lora) + ((int)blockIdx.x - a.nb_lora);
+  uint64_t ep_old = 0;
+  if (a.epoch && threadIdx.x == 0) ep_old = dfssm_dev::arrive(a.epoch, member);
   constexpr int KW = 64 * S;  // columns per wave iteration
   constexpr int SW = S / 2;   // sign words per lane per iteration
   const int lane = threadIdx.x & 63;
@@ -437,8 +469,17 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   // ---- sum the waves' partial tiles; wave i finishes token tile i
 #pragma unroll
   for (int i = 0; i < MT; ++i) red[wave][i][lane] = acc[i];
+  if (threadIdx.x == 0) {
+    if (a.epoch) {
+      tag_lds = dfssm_dev::epoch_tag(ep_old);
+      dfssm_dev::advance_if_last(a.epoch, member, ep_old, a.arrivals);
+    } else {
+      tag_lds = a.host_tag;
+    }
+  }
   __syncthreads();
   if (!fin) return;
+  const uint32_t tag = tag_lds;
   v4i d = red[0][wave][lane];
   for (int w = 1; w < nw; ++w) d += red[w][wave][lane];
 
@@ -448,7 +489,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   v4i lm[4];
   int sq = 0;
   const bool keep = (int)blockIdx.x == a.nb_lora && mtok < M;
-  fetch_lora<L4>(a, mc, 0, kg, lm, &sq, keep);
+  fetch_lora<L4>(a, tag, mc, 0, kg, lm, &sq, keep);
 
   // LoRA up-projection, limbs 3, 2, 1, 0 over the 64-rank chunks
   if (L4 && bpacked) {
@@ -468,7 +509,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
     for (int j0 = 64; j0 < a.rp; j0 += 64) {
       const v4i bl = load16_row_guarded<L4>(a.B + (int64_t)nrow * bpitch, j0 + 16 * kg, r, ba);
       v4i lj[4];
-      fetch_lora<L4>(a, mc, j0, kg, lj, nullptr, keep);
+      fetch_lora<L4>(a, tag, mc, j0, kg, lj, nullptr, keep);
       e3 = mfma(bl, lj[3], e3);
       e2 = mfma(bl, lj[2], e2);
       e1 = mfma(bl, lj[1], e1);
@@ -511,14 +552,11 @@ hipError_t launch_t(const SkinnyArgs& a, int nw, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Per-call tag of the LoRA words (never 0, so zeroed memory never validates).
-uint32_t next_tag() {
+// Tag of a call enqueued outside graph capture: a process-wide counter with
+// bit 31 set, so it never equals a device-epoch tag (below 2^31) or 0.
+uint32_t host_tag() {
   static std::atomic<uint32_t> seq{0};
-  uint32_t t;
-  do {
-    t = seq.fetch_add(1, std::memory_order_relaxed) + 1;
-  } while (t == 0);
-  return t;
+  return 0x80000000u | (seq.fetch_add(1, std::memory_order_relaxed) & 0x7fffffffu);
 }
 
 }  // namespace
@@ -546,14 +584,27 @@ hipError_t skinny_impl(const int8_t* q, const float* s, int64_t M, int64_t K, in
   const int mt = M > 32 ? 4 : (M > 16 ? 2 : 1);
   const int64_t nit = ceil_div(K, 64 * S);
   const int nw = (int)std::max<int64_t>(mt, std::min<int64_t>(kMaxWaves, nit));
-  // Test hook: DFSSM_TEST_LOCAL_LORA=1 launches no LoRA workgroups and lets
-  // every lane compute its LoRA values itself at once (the path a lane takes
-  // when the words never arrive).
-  const char* hook = getenv("DFSSM_TEST_LOCAL_LORA");
-  const bool local_only = hook && hook[0] == '1';
-  const int nb_lora = local_only ? 0 : (int)ceil_div(ceil_div(M, kPrepTokens) * rp, nw);
+  // Test switch local_lora: no LoRA workgroups, every lane computes its LoRA
+  // values itself at once (the path a lane takes when the words never
+  // arrive).
+  const bool local_only = test_switch(DFSSM_TEST_LOCAL_LORA) == 1;
+  const int64_t lora_waves = ceil_div(M, kPrepTokens) * rp;
+  const int nb_lora = local_only ? 0 : (int)ceil_div(lora_waves, nw);
+  const int64_t out_blocks = ceil_div(N, 16) * ceil_div(M, 16 * mt);
+  const int arrivals = (int)((local_only ? 0 : lora_waves) + out_blocks);
+  // the call's tag: under graph capture from the device epoch (a replay
+  // moves it on), otherwise from a host counter (no arrivals at all)
+  // (if the query fails, the device epoch, which is right either way; the
+  // failed query's error is cleared so that the launch check does not see it)
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(st, &cap) != hipSuccess) {
+    (void)hipGetLastError();
+    cap = hipStreamCaptureStatusActive;
+  }
+  const bool device_epoch = cap != hipStreamCaptureStatusNone;
   SkinnyArgs a{q, s, (int)M, (int)K, (int)N, (int)r, rp, w_bits, alpha, A, B, beta, y, acc_s, acc_b,
-               ws.acc_a, ws.xw, next_tag(), nb_lora, local_only ? 0 : (1 << 14)};
+               ws.acc_a, ws.xw, device_epoch ? ws.epoch : nullptr, device_epoch ? 0u : host_tag(), arrivals,
+               (int)(local_only ? 0 : lora_waves), nb_lora, local_only ? 0 : (1 << 14)};
   hipError_t e;
   if (mt == 1)
     e = S == 8 ? launch_t<1, 8, L4>(a, nw, st) : launch_t<1, 4, L4>(a, nw, st);

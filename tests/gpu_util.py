@@ -1,5 +1,6 @@
 """Helpers shared by the GPU tests: device placement of the seeded inputs and
 the comparison bar against the oracle."""
+import contextlib
 import sys
 
 import numpy as np
@@ -46,3 +47,14 @@ def assert_y(y_gpu: np.ndarray, ref: dict, exact32: bool = True, what: str = "")
     if exact32:
         bad = np.flatnonzero(y_gpu.view(np.uint32) != ref["y32"].view(np.uint32))
         assert bad.size == 0, f"{what}: {bad.size} y differ from the fp32-ordered oracle, first {bad[:5]}"
+
+
+@contextlib.contextmanager
+def forced_switch(D, which: int, value: int):
+    """Sets one of the library's test switches for the body, then restores
+    the automatic choice."""
+    D.test_switch(which, value)
+    try:
+        yield
+    finally:
+        D.test_switch(which, 0)

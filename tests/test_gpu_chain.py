@@ -20,9 +20,26 @@ def env():
     return torch, D, oracle.get()
 
 
-def _check_chain(env, shapes, r, M, key):
+def _with_int8_min(ws: dict, key) -> dict:
+    """The same weight set with -128 (which int8 storage admits, though the
+    seeded draw stops at -127) planted in A and B: a whole row of A, every
+    7th column of A, a whole row of B, every 5th row of B in one rank."""
+    w = {k: v.copy() for k, v in ws.items()}
+    A, B = w["A"], w["B"]
+    if A.shape[0]:
+        g = np.random.default_rng(list(key))
+        A[g.integers(A.shape[0])] = -128
+        A[:, ::7] = -128
+        B[g.integers(B.shape[0])] = -128
+        B[::5, g.integers(B.shape[1])] = -128
+    return w
+
+
+def _check_chain(env, shapes, r, M, key, int8_min=False):
     torch, D, o = env
     layers = [S.weights(K, N, r, key=(20, key, i)) for i, (K, N) in enumerate(shapes)]
+    if int8_min:
+        layers = [_with_int8_min(ly, (20, key, i)) for i, ly in enumerate(layers)]
     x = S.activations(M, shapes[0][0], key=(20, key))
     q0, s0 = o.quantize_act(x)
     ys_ref, _ = o.chain(layers, q0, s0)
@@ -46,6 +63,14 @@ def test_chain_small(env):
 def test_chain_multi_token(env, M):
     say(f"chain M={M}")
     _check_chain(env, [(256, 512), (512, 256), (256, 300)], r=16, M=M, key=M)
+
+
+def test_chain_int8_min(env):
+    """-128 in A and B of every linear of a 1.3B-shaped chain (persistent
+    kernel) and of a multi-token chain (quantise + linear launches)."""
+    say("chain with -128 in the LoRA factors")
+    _check_chain(env, S.sweep_shapes(2), r=64, M=1, key=98, int8_min=True)
+    _check_chain(env, [(256, 512), (512, 256), (256, 300)], r=16, M=3, key=97, int8_min=True)
 
 
 def test_chain_decode_sweep_full(env):

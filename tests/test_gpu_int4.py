@@ -14,7 +14,7 @@ import pytest
 
 import dfssm_synth as S
 import oracle
-from gpu_util import assert_y, dev, host, say, torch_cuda
+from gpu_util import assert_y, dev, forced_switch, host, say, torch_cuda
 
 pytestmark = pytest.mark.gpu
 
@@ -75,13 +75,14 @@ def test_int4_few_tokens(env, M, K, N, r):
 
 
 @pytest.mark.parametrize("M,K,N,r", [(3, 160, 77, 6), (17, 4096, 2048, 64), (2, 256, 40, 256)])
-def test_int4_few_tokens_local_lora(env, M, K, N, r, monkeypatch):
+def test_int4_few_tokens_local_lora(env, M, K, N, r):
     # no LoRA workgroups: every output lane computes the down-projection
     # itself from the packed A rows
     torch, D, o = env
     say(f"int4 linear few, local LoRA M={M} K={K} N={N} r={r}")
-    monkeypatch.setenv("DFSSM_TEST_LOCAL_LORA", "1")
-    _check(*_run(env, M, K, N, r, D.PATH_MFMA_FEW), r, f"int4 few local {M}x{K}x{N} r{r}")
+    with forced_switch(D, D.TEST_LOCAL_LORA, 1):
+        res = _run(env, M, K, N, r, D.PATH_MFMA_FEW)
+    _check(*res, r, f"int4 few local {M}x{K}x{N} r{r}")
 
 
 @pytest.mark.parametrize("M,K,N,r", [(33, 2048, 8512, 64), (130, 4096, 2048, 64), (40, 160, 77, 6),

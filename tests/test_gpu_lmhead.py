@@ -12,7 +12,7 @@ import pytest
 
 import dfssm_synth as S
 import oracle
-from gpu_util import dev, host, say, torch_cuda
+from gpu_util import dev, forced_switch, host, say, torch_cuda
 
 pytestmark = pytest.mark.gpu
 
@@ -84,17 +84,17 @@ def test_lm_head(env, table_1p3b, M, d, V):
     _check_lm(torch, D, o, q, s, E, scale, f"M={M} d={d} V={V}")
 
 
-@pytest.mark.parametrize("M,d,V,threshold", [(1, 2048, 1001, "1"), (3, 256, 77, "1"), (64, 2048, 1001, "100000"),
-                                              (20, 768, 333, "100000")])
-def test_lm_head_both_kernels(env, M, d, V, threshold, monkeypatch):
+@pytest.mark.parametrize("M,d,V,threshold", [(1, 2048, 1001, 1), (3, 256, 77, 1), (64, 2048, 1001, 100000),
+                                              (20, 768, 333, 100000)])
+def test_lm_head_both_kernels(env, M, d, V, threshold):
     # the test switch moves the token count from which the matrix-core
     # kernel runs: few tokens through it, many through the GEMV passes
     torch, D, o = env
     say(f"lm_head M={M} d={d} V={V} threshold={threshold}")
-    monkeypatch.setenv("DFSSM_TEST_LM_HEAD_MFMA_TOKENS", threshold)
     E, scale = S.embedding(V, d, key=(49, d, V))
     q, s = o.quantize_act(S.activations(M, d, key=(49, M, d)))
-    _check_lm(torch, D, o, q, s, E, scale, f"M={M} d={d} V={V} threshold={threshold}")
+    with forced_switch(D, D.TEST_LM_HEAD_MFMA_TOKENS, threshold):
+        _check_lm(torch, D, o, q, s, E, scale, f"M={M} d={d} V={V} threshold={threshold}")
 
 
 def test_lm_head_extremes(env):

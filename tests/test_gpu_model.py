@@ -10,9 +10,15 @@ the device, which can move a value by one ulp and, rarely, a code of
 out_proj's input, so logits must agree within 1e-3 of their largest value
 (and the argmax must agree), and in practice agree bit for bit.
 
-Against itself under graph capture: four captured steps (one per ring
-slot, step & 3) replayed for eight tokens, with new token ids written
-between replays, must give exactly the eager results, replay after replay."""
+Against itself and the oracle under graph capture: four captured steps
+(one per ring slot, step & 3) replayed token after token, with new token
+ids written between replays, must give exactly the eager results, replay
+after replay, and the oracle's within the same bar (at 2 sequences, and at
+130, where in_proj takes the prefill path).
+
+At the full size: the 48-layer 1.3B model with its 50,280-word table at
+batch 1 and 8 over 4 tokens against the oracle, reporting how many tokens'
+logits are bit-exact."""
 import numpy as np
 import pytest
 
@@ -74,8 +80,9 @@ class OracleModel:
     def __init__(self, o, mh, M):
         self.o, self.mh, self.M = o, mh, M
         dm = S.mamba_dims(2048)
-        self.conv = [np.zeros((M, dm["conv_dim"], 4), np.float32) for _ in range(L)]
-        self.ssm = [np.zeros((M, 64, 64, 128), np.float32) for _ in range(L)]
+        n = len(mh["layers"])
+        self.conv = [np.zeros((M, dm["conv_dim"], 4), np.float32) for _ in range(n)]
+        self.ssm = [np.zeros((M, 64, 64, 128), np.float32) for _ in range(n)]
 
     def _linear(self, q, s, w):
         return (self.o.linear_i4(q, s, **w) if "A4" in w else self.o.linear(q, s, **w))["y32"]
@@ -141,15 +148,22 @@ def test_decode_step_int4_lora(env, model_host_i4, M, steps):
     say(f"  {exact} of {steps} tokens bit-exact")
 
 
-def test_decode_step_graph_replays(env, model_host):
+def _logits_check(lg, ref, what):
+    scale = float(np.abs(ref).max())
+    assert np.abs(lg.astype(np.float64) - ref).max() <= 1e-3 * scale, what
+    assert np.array_equal(lg.argmax(axis=1), ref.argmax(axis=1)), what
+    return int(np.array_equal(lg.view(np.uint32), ref.view(np.uint32)))
+
+
+@pytest.mark.parametrize("M,T", [(2, 8), (130, 4)])
+def test_decode_step_graph_replays(env, model_host, M, T, record_property):
     torch, D, o = env
-    say("decode step: four captured graphs, eight replays")
-    M = 2
+    say(f"decode step: four captured graphs, {T} replays at M={M}, against eager and the oracle")
     m = device_model(D, model_host)
     # eager reference on its own state
     ring_e, state_e = m.new_state(M)
     ws_e = m.workspace(M)
-    toks = [S.tokens(M, V, key=(144, t)) for t in range(8)]
+    toks = [S.tokens(M, V, key=(144, M, t)) for t in range(T)]
     eager = [host(m.decode_step(dev(tk), t, ring_e, state_e, ws_e)) for t, tk in enumerate(toks)]
     torch.cuda.synchronize()
     # graphs: static token buffer, logits buffer and workspace
@@ -174,6 +188,8 @@ def test_decode_step_graph_replays(env, model_host):
     ring.zero_()
     state.zero_()
     torch.cuda.synchronize()
+    om = OracleModel(o, model_host, M)
+    exact = 0
     for t, tk in enumerate(toks):
         tok_buf.copy_(dev(tk))
         torch.cuda.synchronize()
@@ -181,4 +197,40 @@ def test_decode_step_graph_replays(env, model_host):
         torch.cuda.synchronize()
         got = host(lg_buf)
         assert np.array_equal(got.view(np.uint32), eager[t].view(np.uint32)), f"replay for token {t}"
+        exact += _logits_check(got, om.step(tk), f"replay for token {t} against the oracle")
     assert np.array_equal(host(state), host(state_e)) and np.array_equal(host(ring), host(ring_e))
+    say(f"  {exact} of {T} replays bit-exact against the oracle")
+    record_property("bit_exact_tokens", f"{exact}/{T}")
+
+
+@pytest.fixture(scope="module")
+def model_host_full():
+    """The 1.3B model: 48 layers of the sweep's seeded projections, seeded
+    layer parameters, the 50,280 x 2048 tied table."""
+    ws = S.sweep_weights(n_layers=48)
+    layers = []
+    for l in range(48):
+        p = S.mamba_params(2048, key=(150, l))
+        layers.append(dict(p, in_proj=ws[2 * l], out_proj=ws[2 * l + 1]))
+    E, scale = S.embedding(50280, 2048, key=(151,))
+    norm_f = np.random.default_rng(152).uniform(0.8, 1.2, 2048).astype(np.float32)
+    return dict(E=E, scale=scale, norm_f=norm_f, layers=layers)
+
+
+@pytest.mark.parametrize("M", [1, 8])
+def test_decode_step_full_model(env, model_host_full, M, record_property):
+    torch, D, o = env
+    T = 4
+    say(f"decode step: 48-layer 1.3B model, batch {M}, {T} tokens vs oracle")
+    m = device_model(D, model_host_full)
+    ring, state = m.new_state(M)
+    ws = m.workspace(M)
+    om = OracleModel(o, model_host_full, M)
+    exact = 0
+    for t in range(T):
+        tok = S.tokens(M, 50280, key=(153, M, t))
+        lg = host(m.decode_step(dev(tok), t, ring, state, ws))
+        torch.cuda.synchronize()
+        exact += _logits_check(lg, om.step(tok), f"token {t}")
+    say(f"  {exact} of {T} tokens bit-exact against the oracle")
+    record_property("bit_exact_tokens", f"{exact}/{T}")
