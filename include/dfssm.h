@@ -132,6 +132,27 @@ dfssm_status dfssm_scaffold_lora_linear(const int8_t* q, const float* s, int64_t
                                         const float* beta, float* y, void* workspace,
                                         size_t workspace_bytes, void* stream);
 
+/* The same linear with no workspace argument, for callers that cannot
+ * allocate device memory (code under graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments, results and errors as
+ * dfssm_scaffold_lora_linear, minus the workspace: the library keeps one
+ * scratch array of dfssm_noalloc_scratch_bytes() bytes (16 MiB) per GPU, in
+ * device memory of the loaded library that stays until the process ends,
+ * and this call allocates nothing.  A call whose workspace would exceed it
+ * (dfssm_linear_workspace_bytes(M, K, N, r) > that size; e.g. M*K above
+ * about 14 M at r = 64) returns DFSSM_ERR_WORKSPACE.  Every call on one GPU
+ * shares its array: calls that overlap on one GPU (two streams, two
+ * threads) race and give unspecified results; calls in one stream are
+ * ordered and fine.
+ * Errors: NULL, SHAPE, ALIGN, WORKSPACE, DEVICE. */
+dfssm_status dfssm_scaffold_lora_linear_noalloc(const int8_t* q, const float* s, int64_t M,
+                                                int64_t K, int64_t N, int64_t r,
+                                                const uint32_t* w_bits, const float* alpha,
+                                                const int8_t* A, const int8_t* B,
+                                                const float* beta, float* y, void* stream);
+/* Size of the scratch array dfssm_scaffold_lora_linear_noalloc uses. */
+size_t dfssm_noalloc_scratch_bytes(void);
+
 /* Same operation with an explicit kernel family and optional integer
  * accumulator outputs (each may be NULL): acc_s int32 [M,N], acc_a int32
  * [M,r], acc_b int64 [M,N].  y may be NULL too.  The accumulators are the

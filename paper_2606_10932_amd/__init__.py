@@ -25,7 +25,8 @@ EXPORTS = ["dfssm_quantize_act", "dfssm_linear_workspace_bytes", "dfssm_scaffold
            "dfssm_embed_gather", "dfssm_lm_head", "dfssm_add_rmsnorm_quant", "dfssm_gate_norm_quant",
            "dfssm_ssm_step", "dfssm_linear_i4_workspace_bytes", "dfssm_scaffold_lora_linear_i4",
            "dfssm_mamba2_state_bytes", "dfssm_mamba2_workspace_bytes",
-           "dfssm_mamba2_decode_step", "dfssm_test_switch", "dfssm_status_string", "dfssm_last_error",
+           "dfssm_mamba2_decode_step", "dfssm_scaffold_lora_linear_noalloc", "dfssm_noalloc_scratch_bytes",
+           "dfssm_test_switch", "dfssm_status_string", "dfssm_last_error",
            "dfssm_version"]
 TEST_LOCAL_LORA, TEST_PREFILL_KERNEL, TEST_LM_HEAD_MFMA_TOKENS = 1, 2, 3
 
@@ -106,6 +107,10 @@ def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dfssm_mamba2_workspace_bytes.restype = sz
     lib.dfssm_mamba2_decode_step.argtypes = [mp, i64, vp, i64, vp, vp, vp, vp, sz, vp]
     lib.dfssm_mamba2_decode_step.restype = i32
+    lib.dfssm_scaffold_lora_linear_noalloc.argtypes = [vp, vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp]
+    lib.dfssm_scaffold_lora_linear_noalloc.restype = i32
+    lib.dfssm_noalloc_scratch_bytes.argtypes = []
+    lib.dfssm_noalloc_scratch_bytes.restype = sz
     lib.dfssm_test_switch.argtypes = [i32, i32]
     lib.dfssm_test_switch.restype = i32
     lib.dfssm_status_string.argtypes = [i32]
@@ -232,6 +237,24 @@ def scaffold_lora_linear(q, s, w_bits, alpha, A=None, B=None, beta=None, y=None,
     _check(st)
     if acc:
         return y, acc_s, acc_a[:, :r], acc_b
+    return y
+
+
+def scaffold_lora_linear_noalloc(q, s, w_bits, alpha, A, B, beta, y, stream=None):
+    """The linear on the library's own scratch array (no workspace; the
+    library allocates nothing).  y [M, N] fp32 must be given."""
+    torch = _torch()
+    M, K = q.shape
+    N = w_bits.shape[0]
+    r = 0 if A is None else A.shape[0]
+    _need(q, torch.int8, "q", 2)
+    _need(s, torch.float32, "s", 1)
+    _need(y, torch.float32, "y", 2)
+    if tuple(y.shape) != (M, N):
+        raise ValueError("y must be [M, N]")
+    _check(lib.dfssm_scaffold_lora_linear_noalloc(
+        q.data_ptr(), s.data_ptr(), M, K, N, r, w_bits.data_ptr(), alpha.data_ptr(), _ptr(A) if r else None,
+        _ptr(B) if r else None, _ptr(beta) if r else None, y.data_ptr(), _stream(stream)))
     return y
 
 

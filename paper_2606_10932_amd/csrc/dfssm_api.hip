@@ -9,6 +9,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <mutex>
 #include <vector>
 
 #include "dfssm_internal.hpp"
@@ -282,6 +283,78 @@ dfssm_status dfssm_scaffold_lora_linear(const int8_t* q, const float* s, int64_t
                                        DFSSM_PATH_AUTO, nullptr, nullptr, nullptr, workspace,
                                        workspace_bytes, stream);
 }
+
+// ---------------------------------------------------------------- no allocation
+// Scratch of dfssm_scaffold_lora_linear_noalloc: the linear's workspace as a
+// device array of this library, zero at load (the state the workspace
+// contract asks for), one copy per GPU, shared by every call on that GPU.
+constexpr size_t kScratchBytes = (size_t)16 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on device `dev`, looked up once per device
+// with that device current.  On the host, `scratch` names a host-side
+// stand-in; kernels get this address instead.
+hipError_t scratch_address(int dev, void** out) {
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    int cur = 0;
+    hipError_t e = hipGetDevice(&cur);
+    if (e == hipSuccess && cur != dev) e = hipSetDevice(dev);
+    void* p = nullptr;
+    if (e == hipSuccess) e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) {
+      const hipError_t e2 = hipSetDevice(cur);
+      if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" dfssm_status dfssm_scaffold_lora_linear_noalloc(const int8_t* q, const float* s, int64_t M, int64_t K,
+                                                           int64_t N, int64_t r, const uint32_t* w_bits,
+                                                           const float* alpha, const int8_t* A, const int8_t* B,
+                                                           const float* beta, float* y, void* stream) {
+  clear_error();
+  dfssm_status st = check_linear(M, K, N, r);
+  if (st != DFSSM_OK) return st;
+  if (M == 0 || N == 0) return DFSSM_OK;
+  st = check_ptrs({{q, "q"}, {s, "s"}, {w_bits, "w_bits"}, {alpha, "alpha"}, {y, "y"}}, {});
+  if (st != DFSSM_OK) return st;
+  if (r > 0) {
+    st = check_ptrs({{A, "A"}, {B, "B"}, {beta, "beta"}}, {});
+    if (st != DFSSM_OK) return st;
+  }
+  const size_t need = linear_ws_bytes(M, K, r);
+  if (need > kScratchBytes)
+    return fail(DFSSM_ERR_WORKSPACE,
+                "M=%lld K=%lld r=%lld needs %zu bytes of scratch; the allocation-free linear holds %zu "
+                "(use dfssm_scaffold_lora_linear with a workspace)",
+                (long long)M, (long long)K, (long long)r, need, kScratchBytes);
+  hipStream_t hs = (hipStream_t)stream;
+  int dev = 0;
+  hipError_t e = hs ? hipStreamGetDevice(hs, &dev) : hipGetDevice(&dev);
+  void* base = nullptr;
+  if (e == hipSuccess) e = scratch_address(dev, &base);
+  if (e != hipSuccess) return device_fail(e, "scratch address");
+  dfssm::LinearWorkspace ws = dfssm::carve_linear_workspace(base, M, K, r);
+  e = launch_linear(DFSSM_PATH_AUTO, q, s, M, K, N, r, w_bits, alpha, A, B, beta, y, nullptr, nullptr, nullptr, ws,
+                    hs);
+  return e == hipSuccess ? DFSSM_OK : device_fail(e, "linear launch");
+}
+
+extern "C" size_t dfssm_noalloc_scratch_bytes(void) { return kScratchBytes; }
 
 // ---------------------------------------------------------------- chain
 // Workspace of the host-sequenced chain: Q [M, Kmax] int8, s [M] fp32, one
