@@ -359,24 +359,18 @@ extern "C" size_t dfssm_noalloc_scratch_bytes(void) { return kScratchBytes; }
 // ---------------------------------------------------------------- chain
 // Workspace of the host-sequenced chain: Q [M, Kmax] int8, s [M] fp32, one
 // linear workspace sized for the largest layer.  Workspace of the persistent
-// chain (M = 1): layer table, its 64-bit fingerprint, then the exchange
-// region: y_ll (one 64-bit word per output of every linear), y_rel (one copy
-// of y_ll per XCD), acc_rel (per XCD, n_layers x kMaxRank words), xmap (one
-// word per workgroup), the status word and the epoch words.  The larger
-// of the two is required.
+// chain (M = 1): its layer table, fingerprint, exchange words, status word
+// and epoch words (dfssm::chain_persistent_bytes).  The larger of the two is
+// required.
 struct ChainLayout {
-  size_t off_s, off_lin, seq_bytes;
-  size_t off_table, off_hash, off_yll, off_yrel, off_acc, off_xmap, off_status, off_epoch, pers_bytes;
-  int64_t y_words;
+  size_t off_s, off_lin, seq_bytes, pers_bytes;
+  bool persistent;
 };
 
 static ChainLayout chain_layout(const dfssm_layer* layers, int n_layers, int64_t M) {
   ChainLayout c{};
-  int64_t kmax = 0, ysum = 0;
-  for (int l = 0; l < n_layers; ++l) {
-    kmax = std::max(kmax, layers[l].K);
-    ysum += layers[l].N;
-  }
+  int64_t kmax = 0;
+  for (int l = 0; l < n_layers; ++l) kmax = std::max(kmax, layers[l].K);
   size_t o = (size_t)dfssm::round_up(M * kmax, 256);
   c.off_s = o;
   o += (size_t)dfssm::round_up(M * 4, 256);
@@ -384,24 +378,8 @@ static ChainLayout chain_layout(const dfssm_layer* layers, int n_layers, int64_t
   size_t lin = 0;
   for (int l = 0; l < n_layers; ++l) lin = std::max(lin, linear_ws_bytes(M, layers[l].K, layers[l].r));
   c.seq_bytes = o + lin;
-  c.off_table = 0;
-  o = (size_t)dfssm::round_up((int64_t)(n_layers * sizeof(dfssm::ChainLayerDev)), 256);
-  c.off_hash = o;
-  o += 256;
-  c.off_yll = o;
-  c.y_words = ysum * M;
-  o += (size_t)dfssm::round_up(c.y_words * 8, 256);
-  c.off_yrel = o;
-  o += (size_t)dfssm::kChainXcds * dfssm::round_up(c.y_words * 8, 256);
-  c.off_acc = o;
-  o += (size_t)dfssm::kChainXcds * n_layers * dfssm::kMaxRank * 8;
-  c.off_xmap = o;
-  o += (size_t)dfssm::chain_grid() * 8;
-  c.off_status = o;
-  o += 256;
-  c.off_epoch = o;
-  o += (size_t)dfssm::kEpochGroups * dfssm::kEpochStride * 8;
-  c.pers_bytes = o;
+  c.persistent = dfssm::chain_persistent_supported(layers, n_layers, M);
+  c.pers_bytes = c.persistent ? dfssm::chain_persistent_bytes(layers, n_layers) : 0;
   return c;
 }
 
@@ -432,41 +410,6 @@ static dfssm_status validate_chain(const dfssm_layer* layers, int n_layers, int6
   return DFSSM_OK;
 }
 
-// The persistent kernel's device table for these layers and its FNV-1a
-// fingerprint (over the table bytes and the layer count).
-static uint64_t chain_table(const dfssm_layer* layers, int n_layers,
-                            std::vector<dfssm::ChainLayerDev>& table) {
-  table.assign(n_layers, dfssm::ChainLayerDev{});
-  int64_t off = 0;
-  for (int l = 0; l < n_layers; ++l) {
-    const dfssm_layer& L = layers[l];
-    // rank 0: the kernel reads through A/B/beta unconditionally (and masks
-    // the values), so give it a valid address
-    const bool lr = L.r > 0;
-    table[l] = dfssm::ChainLayerDev{L.w_bits,
-                                    L.alpha,
-                                    lr ? L.A : reinterpret_cast<const int8_t*>(L.alpha),
-                                    lr ? L.B : reinterpret_cast<const int8_t*>(L.alpha),
-                                    lr ? L.beta : L.alpha,
-                                    (int32_t)L.K,
-                                    (int32_t)L.N,
-                                    (int32_t)L.r,
-                                    __builtin_ctz((unsigned)dfssm::chain_lanes_per_row(L.K)),
-                                    (int32_t)dfssm::ceil_div(L.N, dfssm::chain_grid()),
-                                    0,
-                                    off};
-    off += L.N;
-  }
-  uint64_t h = 1469598103934665603ull;
-  auto mix = [&](const void* p, size_t n) {
-    const unsigned char* b = static_cast<const unsigned char*>(p);
-    for (size_t i = 0; i < n; ++i) h = (h ^ b[i]) * 1099511628211ull;
-  };
-  mix(&n_layers, sizeof(n_layers));
-  mix(table.data(), table.size() * sizeof(table[0]));
-  return h;
-}
-
 size_t dfssm_chain_workspace_bytes(const dfssm_layer* layers, int n_layers, int64_t M) {
   if (!layers || n_layers <= 0 || M <= 0) return 0;
   ChainLayout c = chain_layout(layers, n_layers, M);
@@ -493,20 +436,12 @@ dfssm_status dfssm_chain_prepare(const dfssm_layer* layers, int n_layers, int64_
   st = chain_common(layers, n_layers, M, workspace, workspace_bytes, &c);
   if (st != DFSSM_OK) return st;
   char* base = static_cast<char*>(workspace);
-  if (!dfssm::chain_persistent_supported(layers, n_layers, M, dfssm::chain_grid())) {
-    // the host-sequenced chain: its linears' epoch word and exchange words
-    hipError_t e = dfssm::launch_zero_words(reinterpret_cast<uint64_t*>(base + c.off_lin),
-                                            (int64_t)(dfssm::kLinearStateBytes / 8), (hipStream_t)stream);
-    return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain prepare launch");
-  }
-  static thread_local std::vector<dfssm::ChainLayerDev> table;
-  const uint64_t h = chain_table(layers, n_layers, table);
-  auto* exch = reinterpret_cast<uint64_t*>(base + c.off_yll);
-  // through the status word and the epoch words after it
-  const int64_t exch_words = (int64_t)(c.pers_bytes - c.off_yll) / 8;
-  hipError_t e = dfssm::launch_chain_setup(table.data(), reinterpret_cast<dfssm::ChainLayerDev*>(base + c.off_table),
-                                           n_layers, exch, exch_words,
-                                           reinterpret_cast<uint64_t*>(base + c.off_hash), h, (hipStream_t)stream);
+  hipError_t e;
+  if (c.persistent)
+    e = dfssm::chain_persistent_prepare(layers, n_layers, workspace, (hipStream_t)stream);
+  else  // the host-sequenced chain: its linears' epoch words and exchange words
+    e = dfssm::launch_zero_words(reinterpret_cast<uint64_t*>(base + c.off_lin),
+                                 (int64_t)(dfssm::kLinearStateBytes / 8), (hipStream_t)stream);
   return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain prepare launch");
 }
 
@@ -524,23 +459,8 @@ dfssm_status dfssm_chain_run(const dfssm_layer* layers, int n_layers, int64_t M,
   hipStream_t hs = (hipStream_t)stream;
   char* base = static_cast<char*>(workspace);
 
-  if (dfssm::chain_persistent_supported(layers, n_layers, M, dfssm::chain_grid())) {
-    static thread_local std::vector<dfssm::ChainLayerDev> table;
-    const uint64_t h = chain_table(layers, n_layers, table);
-    dfssm::ChainExch ex{};
-    ex.y_ll = reinterpret_cast<uint64_t*>(base + c.off_yll);
-    // per-XCD copies are spaced by the (256-byte rounded) size of y_ll
-    ex.y_rel = reinterpret_cast<uint64_t*>(base + c.off_yrel);
-    ex.ysum = dfssm::round_up(c.y_words * 8, 256) / 8;
-    ex.acc_rel = reinterpret_cast<uint64_t*>(base + c.off_acc);
-    ex.xmap = reinterpret_cast<uint64_t*>(base + c.off_xmap);
-    ex.status = reinterpret_cast<unsigned*>(base + c.off_status);
-    ex.epoch = reinterpret_cast<uint64_t*>(base + c.off_epoch);
-    ex.r_max = 0;
-    for (int l = 0; l < n_layers; ++l) ex.r_max = std::max(ex.r_max, (int32_t)layers[l].r);
-    hipError_t e = dfssm::launch_chain_run(reinterpret_cast<const dfssm::ChainLayerDev*>(base + c.off_table),
-                                           n_layers, q0, s0, ex, y_all,
-                                           reinterpret_cast<const uint64_t*>(base + c.off_hash), h, hs);
+  if (c.persistent) {
+    hipError_t e = dfssm::chain_persistent_run(layers, n_layers, q0, s0, y_all, workspace, hs);
     return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain run launch");
   }
 
@@ -595,11 +515,11 @@ dfssm_status dfssm_chain_status(const dfssm_layer* layers, int n_layers, int64_t
   ChainLayout c;
   st = chain_common(layers, n_layers, M, const_cast<void*>(workspace), workspace_bytes, &c);
   if (st != DFSSM_OK) return st;
-  if (!dfssm::chain_persistent_supported(layers, n_layers, M, dfssm::chain_grid())) return DFSSM_OK;
+  if (!c.persistent) return DFSSM_OK;
   hipError_t e = hipStreamSynchronize((hipStream_t)stream);
   if (e == hipSuccess)
-    e = hipMemcpy(status, static_cast<const char*>(workspace) + c.off_status, sizeof(unsigned),
-                  hipMemcpyDeviceToHost);
+    e = hipMemcpy(status, static_cast<const char*>(workspace) + dfssm::chain_status_offset(layers, n_layers),
+                  sizeof(unsigned), hipMemcpyDeviceToHost);
   return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain status read");
 }
 

@@ -1,83 +1,117 @@
 // dfssm_chain.hip -- persistent kernel for the re-quantising chain of
 // scaffold + LoRA linears at one token (the decode step's projections run
 // back to back, Sec. 4.1 of the paper, where a CUDA graph removes launch
-// gaps; here one cooperative launch replaces the whole sequence).
+// gaps; here one launch replaces the whole sequence).
 //
 // Every linear depends on all of the previous linear's output (its absmax
 // and its LoRA down-projection are reductions over all of it), so the chain
-// is bound by cross-CU communication latency, not by HBM.  The design:
+// is bound by cross-CU exchange latency, not by HBM.  The design keeps the
+// exchange to two hops per linear, one of them inside an XCD:
 //
-//  * Data crosses workgroups as 64-bit words {tag:32, value:32}, so a
-//    consumer polls the data itself: a word is valid once its tag equals
-//    the linear's tag.  Tags carry the launch's epoch, kept on the device:
-//    every workgroup arrives once, at its start, on the workspace's epoch
-//    words (dfssm_dev::arrive, 64 words so that arrivals meet at 64
-//    addresses), and each word's last arrival moves it on; so words left
-//    from an earlier launch (or an earlier replay of a captured launch)
-//    never validate.  No fences are used (on
-//    MI355X a release/acquire pair costs ~3.5 us: it writes back and
-//    invalidates the whole L2).
-//  * Two levels of exchange.  MI355X has 8 XCDs, each with its own L2; a
-//    cross-XCD word needs an agent-scope store and load (~0.9 us round
-//    trip), a word inside one XCD only a store into that XCD's L2 and a
-//    load that skips the CU's L1 (~0.6 us).  At start every workgroup reads
-//    its XCD id (hardware register XCC_ID) and publishes it, so each knows
-//    its rank rho among the n_x workgroups of its XCD.  Per linear:
-//      - outputs y_{l-1} are stored once at agent scope (y_ll);
-//      - workgroup rho of XCD x copies slice rho of y_{l-1}[0:K] from y_ll
-//        into x's own region (y_rel[x]) as soon as each word is valid;
-//      - every workgroup polls all of y_{l-1}[0:K] in its XCD's region
-//        (L2 hits): 1/n_x of the cross-XCD polling traffic of reading y_ll
-//        directly;
-//      - the LoRA down-projection is computed inside each XCD: workgroup
-//        rho computes acc_a[j] for j = rho + n_x*t (t < kChainAccRows) and
-//        stores it into x's region, so acc_a never crosses an XCD.
-//  * A workgroup is two groups of 8 waves that alternate roles: while one
-//    group computes linear l, the other loads the weights of linear l+1
-//    into its own registers, once the bit-planes of linear l are built.  A
-//    wave's loads complete in order, so a latency-critical wait (a poll)
-//    never sits behind a weight load issued shortly before it.
-//  * Per linear: the active group relays its slice; all 16 waves poll their
-//    words of y_{l-1}[0:K_l], reducing their absmax on the way -> Q (the
-//    quantiser's fp32 decisions), the workgroup's acc_a partials and the
-//    codes as bytes in LDS; after a barrier, wave 0 publishes the
-//    workgroup's acc_a rows at once (the next phase waits on them) while
-//    threads p < K/8 build the bit-planes, each transposing the 8x8 bit
-//    matrix of codes 8p..8p+7.  Then the active group runs the popcount
-//    GEMV on the workgroup's rows, its first wave collects the r acc_a words
-//    of the XCD and splits them into limbs in LDS, and the group does the
-//    LoRA up-projection and epilogue and stores its y rows.
-//  * Row-split constants come precomputed in the layer table, and the loop
-//    index is kept uniform, so per-linear set-up runs on the scalar unit.
-//  * Every wait is bounded: on time-out the workgroup records an error in
-//    the status word and leaves, so the grid always drains.
+//  * 256 workgroups, one per CU.  The dispatcher deals workgroups to the 8
+//    XCDs in turn, starting from some XCD, so workgroup w sits on XCD x =
+//    (w + o) % 8 for an offset o of the launch; the kernel reads x from the
+//    XCC_ID register, and lam = w / 8 is then distinct among the 32
+//    workgroups of each XCD.  lam picks a column slice kap = lam % 8 (K/8
+//    input columns) and a row group h = lam / 8.  (A placement that were not
+//    such a rotation would leave some (x, lam) without a workgroup; the
+//    waits for its words end with a status bit, never with wrong data.)
+//  * Output rows are owned by XCDs: the rows the next linear consumes,
+//    [0, Nc), split evenly (Nc/8 per XCD, Nc/256 per workgroup), the rest
+//    (the tail) spread over all 256 workgroups.  Workgroup (x, lam) is the
+//    "reducer" of its rows; row group h of XCD x is the rows of reducers
+//    8h .. 8h+7.
+//  * Phase A: workgroup (x, kap, h) computes, for every row of its row
+//    group, the partial product over its column slice (bit-plane popcounts
+//    of the sign words against its codes), and publishes it as a word in
+//    XCD-local memory (L2).  Meanwhile its codes wave computes the partial
+//    LoRA down-projection of ranks h*rh .. h*rh + rh - 1 (rh = ceil(r/4))
+//    over the slice, also as XCD-local words: every XCD forms all r rank
+//    totals from its own 32 workgroups (each A byte is read once per XCD),
+//    so acc_a never crosses an XCD.  The codes wave then sums the 8 slice
+//    partials of every rank and leaves acc_a's base-256 limbs in LDS.
+//  * Hop 1 (reducers, one wave, XCD-local): sum the 8 slice partials of
+//    each row, then the LoRA up-projection (exact int64 through the limbs),
+//    the pinned fp32 epilogue, and publish each consumed row's y and the
+//    workgroup's absmax of them at agent scope.
+//  * Hop 2 (phase D of the next linear, agent scope): each workgroup
+//    gathers only its column slice of the previous output (K/8 words) and
+//    the 256 absmax words, quantises its slice (the quantiser's fp32
+//    decisions), builds the 8 bit-planes and the slice's code sum.
+//  * Partial words are laid out slice-major ([slice][row], [slice][rank]),
+//    so one poll instruction of a wave reads 64 consecutive words (4 cache
+//    lines); polls are what limits the hops, not the data.
+//  * Every word crossing workgroups is {tag:32, value:32}; a consumer polls
+//    the data itself, so no fences are used (on MI355X a release/acquire
+//    pair writes back and invalidates the whole L2).  Tags carry the
+//    launch's epoch, kept on the device (one arrival per workgroup on the
+//    workspace's epoch words), so words of an earlier launch or replay never
+//    validate.
+//  * Each workgroup's operands of linear l+2 (its sign words, its rh A
+//    rows' slice, its reducer rows' B rows and scales) are streamed into a
+//    3-slot LDS ring by a dedicated wave with direct-to-LDS loads, so no
+//    latency-critical poll ever waits behind a weight load (a wave's memory
+//    operations complete in issue order).
+//  * Every wait is bounded: on time-out the workgroup records a status bit
+//    and leaves after the next barrier, so the grid always drains.
 //  * The layer table lives in the workspace, written by a setup launch
-//    (dfssm_chain_prepare) together with a fingerprint of the table; the
-//    kernel compares that fingerprint with the caller's before it reads the
-//    table, and leaves (status bit 8) if they differ.
+//    (dfssm_chain_prepare) with its fingerprint; the kernel compares that
+//    fingerprint with the caller's before it reads the table.
 #include <float.h>
 
 #include <algorithm>
+#include <vector>
 
 #include "dfssm_internal.hpp"
 
 namespace {
 
-constexpr int kGT = 512;              // threads per role group
-constexpr int kCT = 2 * kGT;          // threads per workgroup
-constexpr int kGW = kGT / 64;         // waves per group
-static_assert(kGW == dfssm::kChainWaves, "waves per role group");
-constexpr int kMaxSteps = dfssm::kChainMaxSteps;
-constexpr int kCols = dfssm::kChainMaxK / kCT;  // previous-output columns per thread
-constexpr int kChunks = dfssm::kChainMaxK / 128;  // 128-column chunks of the bit-planes
-constexpr int kAccRows = dfssm::kChainAccRows;
-constexpr int kXcds = dfssm::kChainXcds;
-constexpr int kMaxGrid = 256;
+constexpr int kGrid = 256;
+constexpr int kXcds = 8;
+constexpr int kPerXcd = kGrid / kXcds;       // 32 workgroups per XCD
+constexpr int kSlices = 8;                   // column slices per XCD
+constexpr int kGroups = kPerXcd / kSlices;   // 4 row groups per XCD
+constexpr int kMaxR = 64;                    // ranks: 8 per XCD, 2 per row group
+constexpr int kWaves = 8;                    // 0 reducer, 1 codes + LoRA down, 6 loads
+constexpr int kThreads = 64 * kWaves;
+constexpr int kAWaves = kWaves - 1;          // phase A: every wave but 1
+constexpr int kRowLanes = 64 * kAWaves;
+constexpr int kRankGroups = 4;               // ranks split over the row groups h
+constexpr int kMaxRh = kMaxR / kRankGroups;  // ranks per workgroup
+static_assert(kMaxRh * 4 <= 64, "wave 1 sums each rank over 4 lanes");
+constexpr int kPollLanes = 6 * 64;           // waves 1..5 and 7 gather (phase D)
+constexpr int kSlotBytes = 28 * 1024;        // one linear's operands (3 slots: one CU per workgroup)
+constexpr int kRing = 3;
+constexpr int kNB = 28;                      // direct-to-LDS loads per linear, at most
+constexpr int kMaxKs = 512;                  // columns per slice (K <= 4096)
+constexpr int kMaxRed = 64;                  // rows per reducer
+constexpr int kSetupChunk = 32;              // table entries per setup launch
 constexpr long kSpinLimit = 1L << 20;
+static_assert(kGroups * 2 * kXcds == kMaxR, "two ranks per workgroup of a row group");
 
 // status bits
-constexpr unsigned kStY = 1u, kStAcc = 2u, kStPlace = 16u;
+constexpr unsigned kStY = 1u, kStAcc = 2u, kStHash = 8u;
 
+// One linear as the kernel reads it (host-built table in the workspace).
+struct Layer {
+  const uint32_t* w_bits;
+  const float* alpha;
+  const int8_t* A;  // never NULL: alpha when r == 0
+  const int8_t* B;
+  const float* beta;
+  int32_t K, N, r, Nc;     // Nc: rows the next linear consumes (0 for the last)
+  int32_t cpr, tq, trem;   // consumed rows per reducer; tail rows tq (+1 for g < trem)
+  int32_t us, ub;          // direct-to-LDS units (bytes) of the sign rows and B rows
+  int32_t o_a, o_b, o_al, o_be;  // operand offsets inside a ring slot (sign rows at 0)
+  int32_t rh;              // LoRA ranks per row group: ceil(r / 4)
+  int64_t y_off;           // this linear's outputs in y_all
+  int64_t part_off;        // words: [8][N] slice partials of acc_s (XCD-local)
+  int64_t p_off;           // words: [8 XCDs][8 slices][64] partials of acc_a (XCD-local)
+  int64_t yw_off;          // words: [Nc] consumed outputs (agent scope)
+  int64_t mx_off;          // words: [256] per-workgroup absmax of consumed outputs
+};
+
+// ------------------------------------------------------------ exchange words
 // agent scope: crosses XCDs (bypasses the non-coherent per-XCD L2s)
 __device__ __forceinline__ uint64_t ll_load(const uint64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -87,19 +121,14 @@ __device__ __forceinline__ void ll_store(uint64_t* p, uint32_t tag, uint32_t v) 
 }
 // inside one XCD: the store goes through (write-through L1) to the XCD's L2;
 // the load is a buffer load with sc0|nt, which skips the CU's L1 and is
-// served by that L2 (each poll loop also holds the status atomic, which keeps
-// the compiler from hoisting the loads out of it)
-__device__ __forceinline__ void xcd_store(uint64_t* p, uint64_t w) {
-  __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+// served by that L2
+__device__ __forceinline__ void xcd_store(uint64_t* p, uint32_t tag, uint32_t v) {
+  __hip_atomic_store(p, ((uint64_t)tag << 32) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 typedef unsigned v2u __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint64_t xcd_load(__amdgpu_buffer_rsrc_t rs, uint32_t word) {
-  const v2u v = __builtin_amdgcn_raw_buffer_load_b64(rs, word * 8u, 0, 3);
+__device__ __forceinline__ uint64_t xcd_load(__amdgpu_buffer_rsrc_t rs, int64_t word) {
+  const v2u v = __builtin_amdgcn_raw_buffer_load_b64(rs, (int)(word * 8), 0, 3);
   return ((uint64_t)v.y << 32) | v.x;
-}
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t xcd_region(uint64_t* base, int64_t words) {
-  // dword 3 of the resource: 32-bit data format, as the gfx9 family needs
-  return __builtin_amdgcn_make_buffer_rsrc(base, 0, (int)(words * 8), 0x00020000);
 }
 
 __device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
@@ -118,33 +147,24 @@ __device__ __forceinline__ int dpp_sum16(int v) {
   v += __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);  // row_mirror
   return v;
 }
-
-// Sum over aligned groups of G lanes (G = 8..64), result in every lane of
-// the group: DPP butterflies inside a 16-lane row; across rows, gfx950's
-// permlane swaps.  v_permlane16_swap of a value with itself leaves rows
-// (0,0,2,2) in one result and (1,1,3,3) in the other, so their sum is the
-// 32-lane half's total in every lane; v_permlane32_swap does the same for
-// the two halves.
+// Sum over aligned groups of G lanes (G = 1, 2, 4 or 32), in every lane of
+// the group.  For 32: the 16-lane rows by DPP, then v_permlane16_swap of a
+// value with itself leaves rows (0,0,2,2) in one result and (1,1,3,3) in the
+// other, so their sum is the 32-lane half's total.
 __device__ __forceinline__ int group_sum(int v, int G) {
-  v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
-  v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
-  v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);
-  if (G >= 16) v += __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);
+  if (G >= 2) v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
+  if (G >= 4) v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
   if (G >= 32) {
+    v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);
+    v += __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);
     const auto p = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v, false, false);
-    v = (int)(p[0] + p[1]);
-  }
-  if (G >= 64) {
-    const auto p = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
     v = (int)(p[0] + p[1]);
   }
   return v;
 }
-
 // Whole-wave reductions with the result as a uniform value: DPP inside each
-// 16-lane row, then row_bcast:15 (rows 1, 3 take lane 15 of the row below)
-// and row_bcast:31 (rows 2, 3 take lane 31), which leaves the total in lane
-// 63.  No LDS permute on the way.
+// 16-lane row, then row_bcast:15 and row_bcast:31, which leave the total in
+// lane 63.
 __device__ __forceinline__ int wave_sum_u(int v) {
   v = dpp_sum16(v);
   v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);
@@ -162,405 +182,286 @@ __device__ __forceinline__ uint32_t wave_max_bits_u(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
-// One linear's operands of this workgroup's rows, per lane of a group.
-struct Pref {
-  uint4 w[kMaxSteps];
-  uint32_t b[kMaxSteps];
-  float al[kMaxSteps], be[kMaxSteps];
-};
-
-// Loads go through the global address space (the table's pointers are
-// generic, which would otherwise give flat loads) and always read in-range
-// addresses; nothing is masked here, so no instruction waits on a prefetched
-// value before its use.  Values read for lanes outside the data are harmless
-// by construction: lanes past a row's chunks meet all-zero bit-planes, LoRA
-// lanes past r meet zero limbs, A bytes past K meet zero codes, A rows past
-// r are never published, and rows outside the workgroup's range are never
-// stored.
-typedef unsigned v4u __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ uint4 gload16(const void* p) {
-  v4u v = *(const __attribute__((address_space(1))) v4u*)(p);
-  return make_uint4(v.x, v.y, v.z, v.w);
+// ------------------------------------------------------------ row ownership
+// First tail row of global reducer g (= 32 x + lam).
+__device__ __forceinline__ int tail_start(const Layer& L, int g) {
+  return L.Nc + g * L.tq + min(g, L.trem);
 }
-__device__ __forceinline__ uint32_t gload4(const void* p) {
-  return *(const __attribute__((address_space(1))) uint32_t*)(p);
+// Row i of row group (x, h): the group's consumed rows, then its tail rows.
+__device__ __forceinline__ int group_row(const Layer& L, int x, int h, int i) {
+  const int nc = kSlices * L.cpr;
+  return i < nc ? x * (L.Nc / kXcds) + h * nc + i : tail_start(L, kPerXcd * x + kSlices * h) + (i - nc);
 }
-__device__ __forceinline__ int32_t gload1s(const void* p) {
-  return *(const __attribute__((address_space(1))) int8_t*)(p);
+__device__ __forceinline__ int group_rows(const Layer& L, int x, int h) {
+  const int g0 = kPerXcd * x + kSlices * h;
+  return kSlices * L.cpr + tail_start(L, g0 + kSlices) - tail_start(L, g0);
+}
+// Row i of reducer (x, lam).
+__device__ __forceinline__ int reducer_row(const Layer& L, int x, int lam, int i) {
+  return i < L.cpr ? x * (L.Nc / kXcds) + lam * L.cpr + i : tail_start(L, kPerXcd * x + lam) + (i - L.cpr);
+}
+__device__ __forceinline__ int reducer_rows(const Layer& L, int x, int lam) {
+  const int g = kPerXcd * x + lam;
+  return L.cpr + L.tq + (g < L.trem ? 1 : 0);
 }
 
-__device__ __forceinline__ void prefetch(const dfssm::ChainLayerDev& L, int wg, int gt, Pref& p) {
-  const int lane = gt & 63, wave = gt >> 6;
-  const int G = 1 << L.lgG, g = lane & (G - 1), grp = lane >> L.lgG;
-  const int RW = 64 >> L.lgG;
-  const int n0 = wg * L.R, n1 = min(L.N, n0 + L.R);
-  const int C = L.K >> 7, W = L.K >> 5, r4 = L.r >> 2;
-#pragma unroll
-  for (int s = 0; s < kMaxSteps; ++s) {
-    const int n = n0 + s * kGW * RW + wave * RW + grp;
-    const int nc = n < n1 ? n : 0;
-    p.w[s] = gload16(L.w_bits + (int64_t)nc * W + 4 * (g < C ? g : 0));
-    p.al[s] = __uint_as_float(gload4(L.alpha + nc));
-    // the table never holds NULL: with r == 0, A/B/beta point at alpha
-    p.b[s] = gload4(L.B + (int64_t)nc * L.r + 4 * (g < r4 ? g : 0));
-    p.be[s] = __uint_as_float(gload4(L.beta + nc));
-  }
+// ------------------------------------------------------------ direct-to-LDS
+// Lane i's 16 (or 4) bytes from sbase + voff land at m0 + 16*i (4*i).
+// Inline assembly, so the compiler does not make later LDS reads wait for
+// them; the loading wave orders them with an explicit vector-memory wait
+// before the barrier that hands the slot over.
+__device__ __forceinline__ void lds_dma16(uint32_t voff, const void* sbase, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
+}
+__device__ __forceinline__ void lds_dma4(uint32_t voff, const void* sbase, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1" ::"v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
+}
+__device__ __forceinline__ void lds_dma(int unit, uint32_t voff, const void* sbase, uint32_t lds) {
+  if (unit == 16)
+    lds_dma16(voff, sbase, lds);
+  else
+    lds_dma4(voff, sbase, lds);
+}
+// s_waitcnt with only the vector-memory counter constrained
+#define CHAIN_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(0x0F70 | ((n) & 0xF) | (((n) >> 4) << 14))
+// Workgroup barrier for LDS data only: the wave's LDS operations complete
+// first, its vector-memory operations do not have to (the loading wave's
+// direct-to-LDS loads of the next linears stay in flight; no global data
+// crosses a barrier inside a workgroup, every exchange goes through polled
+// tagged words)
+#define CHAIN_BARRIER() asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory")
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
-// This thread's bytes of the LoRA down rows rho + n_x*t (t < kAccRows) of a
-// linear, in the column layout of the codes: byte i of a[t] is column
-// tid + kCT*i (columns past K read column 0; their codes are 0).
-__device__ __forceinline__ void load_a_cols(const dfssm::ChainLayerDev& L, int tid, int rho, int nx,
-                                            uint32_t (&a)[kAccRows]) {
-  static_assert(kCols == 4, "four bytes per packed word");
-#pragma unroll
-  for (int t = 0; t < kAccRows; ++t) {
-    const int j = rho + nx * t;
-    const int8_t* arow = L.A + (int64_t)(j < L.r ? j : 0) * L.K;
-    uint32_t w = 0;
-#pragma unroll
-    for (int i = 0; i < kCols; ++i) {
-      const int k = tid + i * kCT;
-      w |= (uint32_t)(gload1s(arow + (k < L.K ? k : 0)) & 0xff) << (8 * i);
+// floor(u / d) for u < 2^11 and d <= 64 without a division: u * ceil(2^20 / d)
+// >> 20 (the error term u * (ceil(2^20/d) * d - 2^20) / 2^20 < u * 64 / 2^20
+// stays below 1/d, so the floor is exact); m = ceil(2^20 / d) is uniform.
+__device__ __forceinline__ uint32_t recip20(uint32_t d) { return ((1u << 20) + d - 1) / d; }
+__device__ __forceinline__ int udiv(int u, uint32_t m) { return (int)(((uint32_t)u * m) >> 20); }
+
+// The loading wave's batch for one linear: this workgroup's sign rows, its
+// rh A rows' slice, its reducer rows' B rows, alpha and beta, into the slot
+// at LDS address sb.  Every address is in range: lanes past the data read
+// the array's first unit.
+__device__ void issue_batch(const Layer& L, int x, int kap, int h, int lam, uint32_t sb, int lane) {
+  int n_issued = 0;
+  const int K = L.K, Ks = K >> 3, rowbytes = K >> 6;
+  {  // sign rows of the row group, this slice
+    const int us = L.us, upr = rowbytes / us, nA = group_rows(L, x, h);
+    const uint32_t m = recip20((uint32_t)upr);
+    const int nunits = nA * upr, ni = (nunits + 63) >> 6;
+    for (int t = 0; t < ni; ++t) {
+      const int u = 64 * t + lane;
+      uint32_t voff = 0;
+      if (u < nunits) {
+        const int i = udiv(u, m), q = u - i * upr;
+        voff = (uint32_t)((int64_t)group_row(L, x, h, i) * (K >> 3) + kap * rowbytes + q * us);
+      }
+      lds_dma(us, voff, L.w_bits, sb + (uint32_t)(64 * us * t));
     }
-    a[t] = w;
+    n_issued += ni;
   }
+  {  // A rows h*rh .. h*rh + rh - 1, columns of the slice (16-byte units)
+    const int upr = Ks >> 4, nunits = L.rh * upr, ni = (nunits + 63) >> 6;
+    const uint32_t m = recip20((uint32_t)upr);
+    for (int t = 0; t < ni; ++t) {
+      const int u = 64 * t + lane;
+      uint32_t voff = 0;
+      if (u < nunits) {
+        const int jj = udiv(u, m), q = u - jj * upr, j = h * L.rh + jj;
+        if (j < L.r) voff = (uint32_t)((int64_t)j * K + kap * Ks + 16 * q);
+      }
+      lds_dma16(voff, L.A, sb + (uint32_t)(L.o_a + 1024 * t));
+    }
+    n_issued += ni;
+  }
+  const int R = reducer_rows(L, x, lam);
+  if (L.r > 0) {  // B rows of the reducer's rows
+    const int ub = L.ub, upr = L.r / ub, nunits = R * upr, ni = (nunits + 63) >> 6;
+    const uint32_t m = recip20((uint32_t)upr);
+    for (int t = 0; t < ni; ++t) {
+      const int u = 64 * t + lane;
+      uint32_t voff = 0;
+      if (u < nunits) {
+        const int i = udiv(u, m), q = u - i * upr;
+        voff = (uint32_t)((int64_t)reducer_row(L, x, lam, i) * L.r + q * ub);
+      }
+      lds_dma(ub, voff, L.B, sb + (uint32_t)(L.o_b + 64 * ub * t));
+    }
+    n_issued += ni;
+  }
+  {  // alpha and beta of the reducer's rows
+    const uint32_t voff = lane < R ? (uint32_t)reducer_row(L, x, lam, lane) * 4u : 0u;
+    lds_dma4(voff, L.alpha, sb + (uint32_t)L.o_al);
+    lds_dma4(voff, L.beta, sb + (uint32_t)L.o_be);
+    n_issued += 2;
+  }
+  (void)n_issued;
 }
 
-// Bounded polls of one {tag, value} word; they also give up once another
-// wave of the workgroup has aborted (abort_ in LDS).
-__device__ __forceinline__ bool poll_ll(const uint64_t* p, uint32_t tag, uint64_t& wd,
-                                        unsigned* status, unsigned code_bit, const int* abort_flag) {
-  long spins = 0;
-  while ((uint32_t)((wd = ll_load(p)) >> 32) != tag) {
-    if (++spins > kSpinLimit || *(const volatile int*)abort_flag) {
-      atomicOr(status, code_bit);
-      return false;
-    }
-    __builtin_amdgcn_s_sleep(1);
-  }
-  return true;
-}
-__device__ __forceinline__ bool poll_xcd(__amdgpu_buffer_rsrc_t rs, uint32_t word, uint32_t tag, uint64_t& wd,
-                                         unsigned* status, unsigned code_bit, const int* abort_flag) {
-  long spins = 0;
-  while ((uint32_t)((wd = xcd_load(rs, word)) >> 32) != tag) {
-    if (++spins > kSpinLimit || *(const volatile int*)abort_flag) {
-      atomicOr(status, code_bit);
-      return false;
-    }
-    __builtin_amdgcn_s_sleep(1);
-  }
-  return true;
-}
+// Workgroup flags in LDS, read and written as LDS operations: a volatile
+// access through a generic pointer would be a flat access (clang leaves
+// volatile accesses in the generic address space), which also counts as a
+// vector-memory operation and makes every check wait for the wave's
+// outstanding global stores.
+typedef __attribute__((address_space(3))) volatile int lds_flag;
+#define FLAG(v) (*(lds_flag*)(&(v)))
 
-__global__ __launch_bounds__(kCT, 1) void chain_persistent(
-    const dfssm::ChainLayerDev* __restrict__ layers, int L, const int8_t* __restrict__ q0,
-    const float* __restrict__ s0, dfssm::ChainExch ex, float* __restrict__ y_all,
+// Bounded spin helpers: a wait gives up after kSpinLimit rounds or once
+// another wave of the workgroup has aborted (abort_flag in LDS).
+#define CHAIN_SPIN_OR_ABORT(spins, abort_flag, status, bit, on_abort) \
+  do {                                                                 \
+    if (++(spins) > kSpinLimit || FLAG(abort_flag)) {                  \
+      atomicOr((status), (bit));                                       \
+      FLAG(abort_flag) = 1;                                            \
+      on_abort;                                                        \
+    }                                                                  \
+    __builtin_amdgcn_s_sleep(1);                                       \
+  } while (0)
+
+__global__ __launch_bounds__(kThreads, 1) void chain_persistent(
+    const Layer* __restrict__ layers, int L, const int8_t* __restrict__ q0, const float* __restrict__ s0,
+    uint64_t* __restrict__ ex, int64_t ex_words, unsigned* status, uint64_t* epoch, float* __restrict__ y_all,
     const uint64_t* __restrict__ table_hash, uint64_t expect_hash) {
-  unsigned* const status = ex.status;
   // the table was written by a prepare of the same layers, or nothing here
   // is trusted: leave before reading it
   if (*table_hash != expect_hash) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(status, 8u);
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(status, kStHash);
     return;
   }
-  // bit-planes, plane-major: the G lanes of a row read consecutive chunks
-  __shared__ uint4 pl_lds[8 * kChunks];
-  // LoRA down-projection of the current linear as 4 signed base-256 limbs:
-  // entry g holds acc_a[4g .. 4g+3], dword t = limb t (r <= 64)
-  static_assert(dfssm::kChainAccRows * dfssm::kChainWgPerXcd <= 64, "limb table size");
-  __shared__ uint4 limb_lds[16];
-  __shared__ int32_t dot_part[kAccRows][64];  // 16-lane row sums of the 16 waves
-  static_assert(4 * 2 * kGW == 64, "row sums per rank");
-  __shared__ __attribute__((aligned(16))) int8_t code_lds[dfssm::kChainMaxK];
-  // absmax of the previous output as {linear, bits}: the largest tag wins,
-  // so it needs no reset between linears
-  __shared__ uint64_t ymax_lds;
-  // phase counters (monotonic): waves of the active group whose bit-planes
-  // are in LDS (+kGW per linear) and that have published (+kGW per linear);
-  // the linear whose limbs are in LDS (+1 per linear)
-  __shared__ int pl_cnt, limb_flag, pub_cnt;
-  __shared__ int sumq_lds;
-  __shared__ int abort_;
-  __shared__ int rho_lds, nx_lds;
-  __shared__ uint32_t seq_lds;
-  const int wg = blockIdx.x, nwg = gridDim.x;
-  const int tid = threadIdx.x;
-  const int group = tid / kGT, gt = tid % kGT, lane = gt & 63, wave = gt >> 6;
-  const int wave16 = tid >> 6;  // wave index in the workgroup
+  __shared__ __attribute__((aligned(16))) uint8_t ring[kRing][kSlotBytes];
+  __shared__ float ys[kMaxKs];                                        // this slice of y_{l-1}
+  __shared__ __attribute__((aligned(16))) int8_t codes[kMaxKs];       // its codes
+  __shared__ __attribute__((aligned(16))) uint32_t planes[8][kMaxKs / 32];  // their bit-planes
+  __shared__ __attribute__((aligned(16))) uint4 limbs[kMaxR / 4];     // acc_a limbs
+  __shared__ int red[64 * 17];  // wave 1: rank partials by lane, then summed
+  __shared__ uint64_t ymax;  // {linear, absmax bits}: the largest wins, no reset needed
+  __shared__ int sumq[2];    // code sum of the slice, by linear parity
+  __shared__ uint32_t seq_s;
+  // flags (FLAG(): LDS operations): abort; waves done with phase A (+8 per
+  // linear); the linear whose limbs are in LDS; linears whose outputs this
+  // workgroup's reducer has published
+  __shared__ int abort_, rows_done, limbs_ready, pub_done;
 
-  // the launch's epoch: one arrival per workgroup; the 24-bit sequence
-  // number derived from it is never 0, so zeroed words never validate
+  const int wg = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int x = (int)(__builtin_amdgcn_s_getreg((20) | (0 << 6) | ((4 - 1) << 11)) & 7u);  // HW_REG_XCC_ID[3:0]
+  const int lam = wg / kXcds, kap = lam % kSlices, h = lam / kSlices;
+
   if (tid == 0) {
-    const uint64_t old = dfssm_dev::arrive(ex.epoch, wg);
-    seq_lds = (uint32_t)((old >> 32) % 0xffffffu) + 1u;
-    dfssm_dev::advance_if_last(ex.epoch, wg, old, nwg);
+    FLAG(abort_) = 0;
+    FLAG(rows_done) = 0;
+    FLAG(limbs_ready) = 0;
+    FLAG(pub_done) = 0;
+    ymax = 0;
+    // the launch's epoch: one arrival per workgroup; the 24-bit sequence
+    // number derived from it is never 0, so zeroed words never validate
+    const uint64_t old = dfssm_dev::arrive(epoch, wg);
+    seq_s = (uint32_t)((old >> 32) % 0xffffffu) + 1u;
+    dfssm_dev::advance_if_last(epoch, wg, old, kGrid);
   }
-  __syncthreads();
-  const uint32_t seq = seq_lds;
-  // a word written for linear l carries tag(l)
+  const uint32_t sb0 = lds_addr(&ring[0][0]);
+  if (wave == 6) {  // the first two linears' operands
+    issue_batch(layers[0], x, kap, h, lam, sb0, lane);
+    if (L > 1) issue_batch(layers[1], x, kap, h, lam, sb0 + kSlotBytes, lane);
+    CHAIN_WAIT_VMCNT(0);
+  }
+  CHAIN_BARRIER();
+  if (FLAG(abort_)) return;
+  const uint32_t seq = seq_s;
   auto tag_of = [seq](int l) -> uint32_t { return (seq << 8) | (uint32_t)((l + 1) & 0xff); };
-  const uint32_t tag_place = seq << 8;
-
-  // ---- placement: the XCD of every workgroup, this one's rank among the
-  //      workgroups of its XCD, and the smallest XCD's size
-  const uint32_t xcc = __builtin_amdgcn_s_getreg((20) | (0 << 6) | ((4 - 1) << 11));  // HW_REG_XCC_ID[3:0]
-  if (tid == 0) {
-    abort_ = 0;
-    ymax_lds = 0;
-    pl_cnt = 0;
-    pub_cnt = 0;
-    limb_flag = 0;
-    sumq_lds = 0;
-    ll_store(ex.xmap + wg, tag_place, xcc);
-  }
-  if (tid < 64) {
-    uint32_t x[kMaxGrid / 64];
-    bool ok = true;
-#pragma unroll
-    for (int t = 0; t < kMaxGrid / 64; ++t) {
-      const int w = tid + 64 * t;
-      x[t] = 0xffu;
-      if (w < nwg) {
-        uint64_t wd;
-        if (!poll_ll(ex.xmap + w, tag_place, wd, status, kStPlace, &abort_)) ok = false;
-        x[t] = (uint32_t)wd;
-      }
-    }
-    int rho = 0, nx = 0, nmin = nwg;
-    for (int c = 0; c < 16; ++c) {
-      int cnt = 0, below = 0;
-#pragma unroll
-      for (int t = 0; t < kMaxGrid / 64; ++t) {
-        const uint64_t m = __ballot(x[t] == (uint32_t)c);
-        cnt += __popcll(m);
-        // lanes holding workgroups 64t .. 64t+63 that come before wg
-        const int w0 = 64 * t;
-        const uint64_t below_mask = wg <= w0 ? 0ull : (wg >= w0 + 64 ? ~0ull : ((1ull << (wg - w0)) - 1));
-        below += __popcll(m & below_mask);
-      }
-      if (cnt > 0) nmin = min(nmin, cnt);
-      if (c == (int)xcc) {
-        rho = below;
-        nx = cnt;
-      }
-    }
-    const bool bad = __ballot(!ok) != 0 || xcc >= (uint32_t)kXcds || (ex.r_max + nmin - 1) / nmin > kAccRows;
-    if (tid == 0) {
-      rho_lds = rho;
-      nx_lds = nx;
-      if (bad) {
-        atomicOr(status, kStPlace);
-        abort_ = 1;
-      }
-    }
-  }
-  __syncthreads();
-  if (abort_) return;
-  const int rho = __builtin_amdgcn_readfirstlane(rho_lds), nx = __builtin_amdgcn_readfirstlane(nx_lds);
-  uint64_t* const y_rel = ex.y_rel + (int64_t)xcc * ex.ysum;
-  uint64_t* const acc_rel = ex.acc_rel + (int64_t)xcc * L * dfssm::kMaxRank;
-  const __amdgpu_buffer_rsrc_t rs_y = xcd_region(y_rel, ex.ysum);
-  const __amdgpu_buffer_rsrc_t rs_acc = xcd_region(acc_rel, (int64_t)L * dfssm::kMaxRank);
-
-  Pref pf;
-  if (group < L) prefetch(layers[group], wg, gt, pf);
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(ex, 0, (int)(ex_words * 8), 0x00020000);
 
   for (int l = 0; l < L; ++l) {
-    const bool active = group == (l & 1);
-    // the loop index is uniform: keeps the table reads and the row-split
-    // arithmetic on the scalar unit
     const int lu = __builtin_amdgcn_readfirstlane(l);
-    const dfssm::ChainLayerDev Ld = layers[lu];
-    const int K = Ld.K, N = Ld.N, r = Ld.r, lgG = Ld.lgG, G = 1 << lgG, R = Ld.R;
-    const float s = l == 0 ? s0[0] : 1.0f / 127.0f;
+    const Layer Ld = layers[lu];
+    const int K = Ld.K, Ks = K >> 3, Wr = K >> 8, r = Ld.r;
+    const uint8_t* slot = ring[lu % kRing];
+    const uint32_t tg = tag_of(l);
 
-    // ---- 0. the active group relays this workgroup's slice of
-    //         y_{l-1}[0:K] into the XCD's copy; then every thread loads its
-    //         A bytes and polls its words of the copy (columns tid + kCT*i)
-    //         until all carry tag(l-1); their absmax is reduced into LDS
-    uint32_t av[kAccRows];  // this thread's A bytes of the two rows, column i in byte i
-    uint32_t yv[kCols];
-    if (l > 0) {
-      const int64_t prev = layers[lu - 1].y_off;
-      const uint32_t tag = tag_of(l - 1);
-      if (active) {
-        const int slice = (K + nx - 1) / nx;
-        const int k1 = min(K, (rho + 1) * slice);
-        for (int k = rho * slice + gt; k < k1; k += kGT) {
-          uint64_t wd;
-          if (!poll_ll(ex.y_ll + prev + k, tag, wd, status, kStY, &abort_)) {
-            abort_ = 1;
-            break;
-          }
-          xcd_store(y_rel + prev + k, wd);
-        }
-      }
-      if (rho < r) load_a_cols(Ld, tid, rho, nx, av);
-      // the group active in this linear arrives early (it was idle after the
-      // last B1); it starts polling only once its own workgroup has
-      // published its rows of y_{l-1}: earlier, its polls would only load
-      // the XCD's L2, which the exchange of the previous linear still uses
-      if (active) {
-        long sp = 0;
-        while (__hip_atomic_load(&pub_cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) < kGW * l) {
-          if (++sp > kSpinLimit || abort_) break;
-          __builtin_amdgcn_s_sleep(1);
-        }
-      }
-      uint32_t pend = 0;
-#pragma unroll
-      for (int i = 0; i < kCols; ++i)
-        if (tid + i * kCT < K) pend |= 1u << i;
-      long spins = 0;
+    // ---- phase D (waves 1..5, 7): this slice of y_{l-1} and the 256 absmax
+    //      words, polled until all carry tag(l-1).  Polling starts once this
+    //      workgroup's own reducer has published y_{l-1}: the other
+    //      reducers publish at about the same time, and earlier polls would
+    //      only load the fabric the reducers' own exchange uses.
+    if (l > 0 && wave >= 1 && wave != 6) {
+      long sp = 0;
+      while (FLAG(pub_done) < l) CHAIN_SPIN_OR_ABORT(sp, abort_, status, kStY, break);
+      const Layer Lp = layers[lu - 1];
+      const uint32_t tp = tag_of(l - 1);
+      const int ct = (wave == 7 ? 5 : wave - 1) * 64 + lane;
+      const int i0 = ct, i1 = ct + kPollLanes;
+      uint32_t pend = (i0 < Ks ? 1u : 0u) | (i1 < Ks ? 2u : 0u) | (ct < kGrid ? 4u : 0u);
+      if (FLAG(abort_)) pend = 0;
       uint32_t m = 0;
+      const uint64_t* yw = ex + Lp.yw_off + (int64_t)kap * Ks;
       while (pend) {
-        uint64_t wd[kCols];
-#pragma unroll
-        for (int i = 0; i < kCols; ++i)
-          if (pend & (1u << i)) wd[i] = xcd_load(rs_y, (uint32_t)(prev + tid + i * kCT));
-#pragma unroll
-        for (int i = 0; i < kCols; ++i)
-          if ((pend & (1u << i)) && (uint32_t)(wd[i] >> 32) == tag) {
-            yv[i] = (uint32_t)wd[i];
-            m = max(m, yv[i] & 0x7fffffffu);
-            pend &= ~(1u << i);
-          }
-        if (pend) {
-          if (++spins > kSpinLimit || abort_) {
-            atomicOr(status, kStY);
-            abort_ = 1;
-            break;
-          }
-          __builtin_amdgcn_s_sleep(1);
+        uint64_t w0 = 0, w1 = 0, w2 = 0;
+        if (pend & 1u) w0 = ll_load(yw + i0);
+        if (pend & 2u) w1 = ll_load(yw + i1);
+        if (pend & 4u) w2 = ll_load(ex + Lp.mx_off + ct);
+        if ((pend & 1u) && (uint32_t)(w0 >> 32) == tp) {
+          ys[i0] = __uint_as_float((uint32_t)w0);
+          pend &= ~1u;
         }
+        if ((pend & 2u) && (uint32_t)(w1 >> 32) == tp) {
+          ys[i1] = __uint_as_float((uint32_t)w1);
+          pend &= ~2u;
+        }
+        if ((pend & 4u) && (uint32_t)(w2 >> 32) == tp) {
+          m = (uint32_t)w2;
+          pend &= ~4u;
+        }
+        if (pend) CHAIN_SPIN_OR_ABORT(sp, abort_, status, kStY, break);
       }
       m = wave_max_bits_u(m);
       if (lane == 0)
-        __hip_atomic_fetch_max(&ymax_lds, ((uint64_t)l << 32) | m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    } else if (rho < r) {
-      load_a_cols(Ld, tid, rho, nx, av);
+        __hip_atomic_fetch_max(&ymax, ((uint64_t)l << 32) | m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
-    __syncthreads();  // B0
-    if (abort_) return;
+    CHAIN_BARRIER();  // B1
+    if (FLAG(abort_)) return;
 
-    // ---- 1. codes, LoRA down rows, bit-planes: all 16 waves, columns
-    //         tid + kCT*i ----------------------------------------------------
-    // column blocks i with tid + kCT*i < K for some thread (uniform)
-    int q[kCols];
-    if (l == 0) {
+    uint32_t cq0 = 0, cq1 = 0;  // wave 1: codes 8p .. 8p+7 of the slice
+    if (wave == 1) {
+      // ---- codes of the slice: lane p takes columns 8p .. 8p+7, writes
+      //      them as bytes, transposes their 8x8 bit matrix into byte p of
+      //      the 8 planes, and the wave sums them
+      const int p = lane;
+      int qs = 0;
+      if (8 * p < Ks) {
+        int q[8];
+        if (l == 0) {
+          const uint2 c = *reinterpret_cast<const uint2*>(q0 + (int64_t)kap * Ks + 8 * p);
 #pragma unroll
-      for (int i = 0; i < kCols; ++i) {
-        q[i] = 0;
-        if (i * kCT < K) {
-          const int k = tid + i * kCT;
-          const int c = gload1s(q0 + (k < K ? k : 0));
-          q[i] = k < K ? c : 0;
-        }
-      }
-    } else {
-      const float a = __uint_as_float((uint32_t)ymax_lds);
-      const bool zero = a < FLT_MIN;
-      const float inv = zero ? 0.0f : 127.0f / a;
-#pragma unroll
-      for (int i = 0; i < kCols; ++i) {
-        q[i] = 0;
-        if (i * kCT < K) q[i] = (zero || tid + i * kCT >= K) ? 0 : code(__uint_as_float(yv[i]), inv);
-      }
-    }
-    // LoRA down partials of rows rho + nx*t: the 4 codes against the 4 A
-    // bytes with one v_dot4, summed over each 16-lane row; the 64 row sums
-    // go to LDS.  The codes go to LDS as bytes (bit-planes, sum of codes).
-    {
-      const uint32_t qp = (uint32_t)(q[0] & 0xff) | ((uint32_t)(q[1] & 0xff) << 8) |
-                          ((uint32_t)(q[2] & 0xff) << 16) | ((uint32_t)q[3] << 24);
-      if (rho < r) {
-#pragma unroll
-        for (int t = 0; t < kAccRows; ++t) {
-          const int v = dpp_sum16(sdot4(av[t], qp, 0));
-          if ((lane & 15) == 0) dot_part[t][4 * wave16 + (lane >> 4)] = v;
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < kCols; ++i)
-        if (i * kCT < K && tid + i * kCT < K) code_lds[tid + i * kCT] = (int8_t)q[i];
-    }
-    __syncthreads();  // B1
-    if (abort_) return;
-
-    // After B1 the two groups part until the next linear's B0:
-    //  * the idle group's first wave publishes this workgroup's LoRA down
-    //    rows, sums the codes, collects the XCD's acc_a words into limbs in
-    //    LDS and raises limb_flag; the rest of the idle group (and then that
-    //    wave) loads the weights of linear l+1;
-    //  * the active group builds the bit-planes, waits for all 8 of its
-    //    waves to have written them (pl_cnt), runs the GEMV, waits for
-    //    limb_flag, and does the LoRA up-projection and epilogue.
-    // A wave's LDS operations complete in issue order, so a counter or flag
-    // raised after a wave's LDS writes is seen only after those writes; the
-    // signal fences keep the compiler from moving LDS accesses across them.
-    // Every LDS written here is next written after the next linear's B1, so
-    // the next B0 orders its reuse.
-    const int RW = 64 >> lgG;
-    const int g = lane & (G - 1);
-    if (!active) {
-      if (gt < 64) {
-        if (rho < r) {
-          static_assert(kAccRows == 2, "two rows per workgroup below");
-          int tot[kAccRows];
-#pragma unroll
-          for (int t = 0; t < kAccRows; ++t) tot[t] = wave_sum_u(dot_part[t][lane]);
-          if (lane < kAccRows) {
-            const int j = rho + nx * lane;
-            if (j < r)
-              xcd_store(acc_rel + (int64_t)l * dfssm::kMaxRank + j,
-                        ((uint64_t)tag_of(l) << 32) | (uint32_t)(lane == 0 ? tot[0] : tot[1]));
+          for (int e = 0; e < 4; ++e) {
+            q[e] = (int8_t)(c.x >> (8 * e));
+            q[4 + e] = (int8_t)(c.y >> (8 * e));
           }
-        }
-        {  // sum of the codes, 16 bytes per lane per pass
-          int qs = 0;
-          for (int k = 16 * lane; k < K; k += 16 * 64) {
-            const uint4 c = *reinterpret_cast<const uint4*>(code_lds + k);
-            qs = sdot4(c.x, 0x01010101u, qs);
-            qs = sdot4(c.y, 0x01010101u, qs);
-            qs = sdot4(c.z, 0x01010101u, qs);
-            qs = sdot4(c.w, 0x01010101u, qs);
-          }
-          qs = wave_sum_u(qs);
-          if (lane == 0) sumq_lds = qs;
-        }
-        // lane j collects acc_a[j] (0 past r) and stores its 4 signed
-        // base-256 limbs as bytes of limb_lds[j / 4], dword t = limb t
-        int32_t v = 0;
-        if (gt < r) {
-          const uint32_t tag = tag_of(l);
-          const uint32_t word = (uint32_t)(l * dfssm::kMaxRank + gt);
-          uint64_t wd;
-          if (!poll_xcd(rs_acc, word, tag, wd, status, kStAcc, &abort_)) abort_ = 1;
-          v = (int32_t)(uint32_t)wd;
-        }
-        int8_t d[4];
-        dfssm_dev::split_limbs(v, d);
-        uint8_t* lb = reinterpret_cast<uint8_t*>(limb_lds) + (gt >> 2) * 16 + (gt & 3);
+        } else {
+          const float a = __uint_as_float((uint32_t)ymax);
+          const bool zero = a < FLT_MIN;
+          const float inv = zero ? 0.0f : 127.0f / a;
+          const float4 v0 = reinterpret_cast<const float4*>(ys)[2 * p];
+          const float4 v1 = reinterpret_cast<const float4*>(ys)[2 * p + 1];
+          const float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
 #pragma unroll
-        for (int t = 0; t < 4; ++t) lb[4 * t] = (uint8_t)d[t];
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        if (lane == 0) __hip_atomic_store(&limb_flag, l + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-      }
-      // the group idle in this linear loads the weights of the next one
-      // (it polls nothing more in this linear; its first wave has finished
-      // its collect above)
-      if (l >= 1 && l + 1 < L) prefetch(layers[lu + 1], wg, gt, pf);
-    } else {
-      // bit-planes: thread p < K/8 of the group transposes the 8x8 bit
-      // matrix of codes 8p .. 8p+7 (byte i = code i) so that byte b holds
-      // bit b of the 8 codes, i.e. byte p of plane b (plane-major, 16-byte
-      // chunks of 128 columns)
-      if (gt < (K >> 3)) {
-        const uint2 c = reinterpret_cast<const uint2*>(code_lds)[gt];
-        uint32_t lo = c.x, hi = c.y, t;
+          for (int e = 0; e < 8; ++e) q[e] = zero ? 0 : code(v[e], inv);
+        }
+        uint32_t lo = 0, hi = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          lo |= (uint32_t)(q[e] & 0xff) << (8 * e);
+          hi |= (uint32_t)(q[4 + e] & 0xff) << (8 * e);
+          qs += q[e] + q[4 + e];
+        }
+        reinterpret_cast<uint2*>(codes)[p] = make_uint2(lo, hi);
+        cq0 = lo;
+        cq1 = hi;
+        // 8x8 bit transpose: byte b of the result holds bit b of the 8 codes
+        uint32_t t;
         t = (lo ^ (lo >> 7)) & 0x00AA00AAu;
         lo ^= t ^ (t << 7);
         t = (hi ^ (hi >> 7)) & 0x00AA00AAu;
@@ -572,105 +473,194 @@ __global__ __launch_bounds__(kCT, 1) void chain_persistent(
         t = (lo ^ __builtin_amdgcn_alignbit(hi, lo, 28)) & 0xF0F0F0F0u;
         lo ^= t;
         hi ^= t >> 4;
-        uint8_t* pb = reinterpret_cast<uint8_t*>(pl_lds) + gt;
+        uint8_t* pb = reinterpret_cast<uint8_t*>(planes) + p;
 #pragma unroll
-        for (int b = 0; b < 4; ++b) pb[b * kChunks * 16] = (uint8_t)(lo >> (8 * b));
+        for (int b = 0; b < 4; ++b) pb[b * (kMaxKs / 8)] = (uint8_t)(lo >> (8 * b));
 #pragma unroll
-        for (int b = 0; b < 4; ++b) pb[(4 + b) * kChunks * 16] = (uint8_t)(hi >> (8 * b));
+        for (int b = 0; b < 4; ++b) pb[(4 + b) * (kMaxKs / 8)] = (uint8_t)(hi >> (8 * b));
       }
-      __atomic_signal_fence(__ATOMIC_SEQ_CST);
-      if (lane == 0) __hip_atomic_fetch_add(&pl_cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-      {
-        long spins = 0;
-        while (__hip_atomic_load(&pl_cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) < kGW * (l + 1)) {
-          if (++spins > kSpinLimit || abort_) {
-            atomicOr(status, kStAcc);
-            abort_ = 1;
-            break;
-          }
-          __builtin_amdgcn_s_sleep(1);
-        }
-      }
-      __atomic_signal_fence(__ATOMIC_SEQ_CST);
-
-      // ---- 2. scaffold GEMV on the prefetched rows: one bit-plane at a
-      //      time, weight c_b = 2^b (b < 7), -128 (b = 7); acc_s =
-      //      2 * sum_{bit=1} Q - sum Q (sum Q subtracted below)
-      int part[kMaxSteps];
-      const int C = K >> 7;
-      const int n0 = wg * R, n1 = min(N, n0 + R);
-#pragma unroll
-      for (int st = 0; st < kMaxSteps; ++st) {
-        part[st] = 0;
-        // uniform per wave: does this wave own rows in step st?
-        if (n0 + st * kGW * RW + wave * RW < n1) {
-          const uint4 w = pf.w[st];
-          int dsum = 0;
-#pragma unroll
-          for (int b = 0; b < 8; ++b) {
-            const uint4 Pb = g < C ? pl_lds[b * kChunks + g] : make_uint4(0, 0, 0, 0);
-            const int c = __builtin_popcount(w.x & Pb.x) + __builtin_popcount(w.y & Pb.y) +
-                          __builtin_popcount(w.z & Pb.z) + __builtin_popcount(w.w & Pb.w);
-            dsum += b < 7 ? (c << b) : -(c << 7);
-          }
-          part[st] = 2 * group_sum(dsum, G);
-        }
-      }
-      {
-        long spins = 0;
-        while (__hip_atomic_load(&limb_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) < l + 1) {
-          if (++spins > kSpinLimit || abort_) {
-            atomicOr(status, kStAcc);
-            abort_ = 1;
-            break;
-          }
-          __builtin_amdgcn_s_sleep(1);
-        }
-      }
-      __atomic_signal_fence(__ATOMIC_SEQ_CST);
-
-      // ---- 3. LoRA up-projection, epilogue, publish --------------------------
-      if (!abort_) {
-        const int sq = sumq_lds;
-        const int r4 = (r + 3) >> 2;
-        const int grp = lane >> lgG;
-        // limbs of acc_a[4g .. 4g+3], packed per limb (j >= r read as 0)
-        uint32_t lb0 = 0, lb1 = 0, lb2 = 0, lb3 = 0;
-        if (r > 0 && g < r4) {
-          const uint4 t = limb_lds[g];
-          lb0 = t.x;
-          lb1 = t.y;
-          lb2 = t.z;
-          lb3 = t.w;
-        }
-#pragma unroll
-        for (int st = 0; st < kMaxSteps; ++st) {
-          if (n0 + st * kGW * RW + wave * RW >= n1) break;  // uniform per wave
-          int elo = 0, ehi = 0;
-          if (r > 0) {
-            const uint32_t bw = pf.b[st];
-            elo = group_sum(sdot4(bw, lb0, 0) + (sdot4(bw, lb1, 0) << 8), G);
-            ehi = group_sum(sdot4(bw, lb2, 0) + (sdot4(bw, lb3, 0) << 8), G);
-          }
-          const int n = n0 + st * kGW * RW + wave * RW + grp;
-          if (g == 0 && n < n1) {
-            const float y = dfssm_dev::epilogue(s, pf.al[st], pf.be[st], part[st] - sq, ehi, elo, r > 0);
-            ll_store(ex.y_ll + Ld.y_off + n, tag_of(l), __float_as_uint(y));
-            y_all[Ld.y_off + n] = y;
-          }
-        }
-      }
-      __atomic_signal_fence(__ATOMIC_SEQ_CST);
-      if (lane == 0) __hip_atomic_fetch_add(&pub_cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      qs = wave_sum_u(qs);
+      if (lane == 0) sumq[l & 1] = qs;
     }
-    // the next linear's B0 orders every LDS reuse
+    CHAIN_BARRIER();  // B2
+
+    if (wave != 1) {
+      // ---- phase A (every wave but 1): slice partials of the row group's rows.
+      //      G lanes per row, 4 sign words each (words past the row's Wr are
+      //      masked); acc_s partial = 2 * sum_{bit=1} Q - sum Q over the
+      //      slice, sum_{bit=1} Q from the planes (weight 2^b, -128 for
+      //      b = 7), each plane's popcounts summed over the words first.
+      //      All LDS reads of a pass are issued before the first use.
+      const int G = Wr <= 4 ? 1 : (Wr <= 8 ? 2 : 4);
+      const int ta = wave == 0 ? lane : tid - 64;  // 0 .. kRowLanes - 1
+      const int g = ta % G, w0 = 4 * g;
+      uint32_t pw[8][4];
+#pragma unroll
+      for (int b = 0; b < 8; ++b)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) pw[b][k] = planes[b][(w0 + k) & (kMaxKs / 32 - 1)];
+      uint32_t keep[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) keep[k] = w0 + k < Wr ? ~0u : 0u;
+      const int sq = sumq[l & 1];
+      const int nA = group_rows(Ld, x, h);
+      const int per_pass = kRowLanes / G;
+      const int rowbytes = K >> 6;
+      for (int i0 = 0; i0 < nA; i0 += per_pass) {  // uniform trip count
+        const int i = i0 + ta / G;
+        const int ic = i < nA ? i : 0;
+        const uint32_t* srow = reinterpret_cast<const uint32_t*>(slot + (size_t)ic * rowbytes);
+        uint32_t sw[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) sw[k] = srow[(w0 + k) & 15] & keep[k];
+        int d = 0;
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+          uint32_t c = 0;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) c += (uint32_t)__builtin_popcount(sw[k] & pw[b][k]);
+          d += b < 7 ? (int)(c << b) : -(int)(c << 7);
+        }
+        d = group_sum(d, G);
+        if (i < nA && g == 0)
+          xcd_store(ex + Ld.part_off + (int64_t)kap * Ld.N + group_row(Ld, x, h, i), tg,
+                    (uint32_t)(2 * d - sq));
+      }
+      // (the count only tells the reducer when to start polling; what it
+      // accepts is decided by the words' tags)
+      if (lane == 0) __hip_atomic_fetch_add(&rows_done, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+
+    if (wave == 1) {
+      // ---- LoRA down-projection inside the XCD: partials of ranks
+      //      h*rh .. h*rh + rh - 1 over the slice (lane p: columns 8p .. 8p+7,
+      //      two v_dot4 per rank), summed over the lanes through LDS
+      //      (red[p][jj], row stride 17 words: no bank conflicts either way)
+      //      and published as XCD-local words; then lane j sums the 8 slice
+      //      partials of rank j from this XCD's words and stores its 4
+      //      signed base-256 limbs as byte (j % 4) of dword t of limbs[j / 4]
+      //      (0 past r)
+      const int rh = Ld.rh;
+      if (rh > 0) {
+        // all reads first (rows past rh read row 0, lanes past the slice
+        // column 0; their products are dropped)
+        const uint8_t* arow = slot + Ld.o_a + (8 * lane < Ks ? 8 * lane : 0);
+        uint2 aw[kMaxRh];
+#pragma unroll
+        for (int jj = 0; jj < kMaxRh; ++jj) aw[jj] = *reinterpret_cast<const uint2*>(arow + (jj < rh ? jj : 0) * Ks);
+        const bool inb = 8 * lane < Ks;
+#pragma unroll
+        for (int jj = 0; jj < kMaxRh; ++jj)
+          red[lane * 17 + jj] = inb ? sdot4(aw[jj].y, cq1, sdot4(aw[jj].x, cq0, 0)) : 0;
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        const int jj = lane >> 2, part = lane & 3;
+        int rv[16];
+#pragma unroll
+        for (int t = 0; t < 16; ++t) rv[t] = red[(part * 16 + t) * 17 + jj];
+        int v = 0;
+#pragma unroll
+        for (int t = 0; t < 16; ++t) v += rv[t];
+        v = group_sum(v, 4);
+        const int j = h * rh + jj;
+        if (part == 0 && jj < rh && j < r)
+          xcd_store(ex + Ld.p_off + (int64_t)(x * kSlices + kap) * kMaxR + j, tg, (uint32_t)v);
+      }
+      int acc_a = 0;
+      if (r > 0) {
+        long sp = 0;
+        uint32_t pend = lane < r && !FLAG(abort_) ? 0xffu : 0u;
+        while (pend) {
+          uint64_t wa[kSlices];
+#pragma unroll
+          for (int k = 0; k < kSlices; ++k)
+            wa[k] = (pend & (1u << k)) ? xcd_load(rs, Ld.p_off + (int64_t)(x * kSlices + k) * kMaxR + lane) : 0;
+#pragma unroll
+          for (int k = 0; k < kSlices; ++k)
+            if ((pend & (1u << k)) && (uint32_t)(wa[k] >> 32) == tg) {
+              acc_a += (int32_t)(uint32_t)wa[k];
+              pend &= ~(1u << k);
+            }
+          if (pend) CHAIN_SPIN_OR_ABORT(sp, abort_, status, kStAcc, break);
+        }
+      }
+      int8_t dl[4];
+      dfssm_dev::split_limbs(lane < r ? acc_a : 0, dl);
+      uint8_t* lb = reinterpret_cast<uint8_t*>(limbs) + (lane >> 2) * 16 + (lane & 3);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) lb[4 * t] = (uint8_t)dl[t];
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the limbs are in LDS
+      if (lane == 0) FLAG(limbs_ready) = l + 1;
+    } else if (wave == 0) {
+      // ---- reducer: lane i takes row i of this workgroup's rows.  Polling
+      //      starts once this workgroup's own waves have published (the
+      //      partials of the other workgroups of the XCD come at about the
+      //      same time)
+      long sp = 0;
+      while (FLAG(rows_done) < kAWaves * (l + 1)) CHAIN_SPIN_OR_ABORT(sp, abort_, status, kStAcc, break);
+      const int R = reducer_rows(Ld, x, lam);
+      // the row's operands (LDS reads issued together, before the poll)
+      const int rw = r >> 2;
+      const uint32_t* brow = reinterpret_cast<const uint32_t*>(slot + Ld.o_b + (lane < R ? lane : 0) * r);
+      uint32_t bw[kMaxR / 4];
+#pragma unroll
+      for (int w = 0; w < kMaxR / 4; ++w) bw[w] = w < rw ? brow[w] : 0u;
+      const float al = reinterpret_cast<const float*>(slot + Ld.o_al)[lane];
+      const float be = reinterpret_cast<const float*>(slot + Ld.o_be)[lane];
+      const int n = lane < R ? reducer_row(Ld, x, lam, lane) : 0;
+      int acc_s = 0;
+      uint32_t pend = lane < R && !FLAG(abort_) ? 0xffu : 0u;
+      while (pend) {
+        uint64_t wp[kSlices];
+#pragma unroll
+        for (int k = 0; k < kSlices; ++k)
+          wp[k] = (pend & (1u << k)) ? xcd_load(rs, Ld.part_off + (int64_t)k * Ld.N + n) : 0;
+#pragma unroll
+        for (int k = 0; k < kSlices; ++k)
+          if ((pend & (1u << k)) && (uint32_t)(wp[k] >> 32) == tg) {
+            acc_s += (int32_t)(uint32_t)wp[k];
+            pend &= ~(1u << k);
+          }
+        if (pend) CHAIN_SPIN_OR_ABORT(sp, abort_, status, kStAcc, break);
+      }
+      while (FLAG(limbs_ready) < l + 1) CHAIN_SPIN_OR_ABORT(sp, abort_, status, kStAcc, break);
+      if (!FLAG(abort_)) {
+        uint4 lw[kMaxR / 4];
+#pragma unroll
+        for (int w = 0; w < kMaxR / 4; ++w) lw[w] = limbs[w];
+        int e0 = 0, e1 = 0, e2 = 0, e3 = 0;
+#pragma unroll
+        for (int w = 0; w < kMaxR / 4; ++w) {
+          e0 = sdot4(bw[w], lw[w].x, e0);
+          e1 = sdot4(bw[w], lw[w].y, e1);
+          e2 = sdot4(bw[w], lw[w].z, e2);
+          e3 = sdot4(bw[w], lw[w].w, e3);
+        }
+        const int elo = e0 + (e1 << 8), ehi = e2 + (e3 << 8);
+        const float s = l == 0 ? s0[0] : 1.0f / 127.0f;
+        const float y = dfssm_dev::epilogue(s, al, be, acc_s, ehi, elo, r > 0);
+        if (lane < Ld.cpr) ll_store(ex + Ld.yw_off + n, tg, __float_as_uint(y));
+        if (Ld.Nc > 0) {
+          const uint32_t m = wave_max_bits_u(lane < Ld.cpr ? (__float_as_uint(y) & 0x7fffffffu) : 0u);
+          if (lane == 0) ll_store(ex + Ld.mx_off + wg, tg, m);
+        }
+        if (lane < R) y_all[Ld.y_off + n] = y;
+      }
+      if (lane == 0) FLAG(pub_done) = l + 1;
+    } else if (wave == 6) {
+      // ---- loading: linear l+1's operands (issued one linear ago) have
+      //      landed once nothing of this wave is in flight; then linear
+      //      l+2's go into the slot linear l-1 used (every reader of it
+      //      passed B1 of this linear after it was done)
+      CHAIN_WAIT_VMCNT(0);
+      if (l + 2 < L) issue_batch(layers[lu + 2], x, kap, h, lam, sb0 + (uint32_t)(((l + 2) % kRing) * kSlotBytes), lane);
+    }
   }
 }
 
 // Writes a chunk of the layer table and zeroes the exchange region.
 struct SetupArgs {
-  dfssm::ChainLayerDev e[dfssm::kChainSetupChunk];
-  dfssm::ChainLayerDev* table;
+  Layer e[kSetupChunk];
+  Layer* table;
   uint64_t* zero_base;
   int64_t zero_words;
   uint64_t* hash_dst;
@@ -685,60 +675,178 @@ __global__ void chain_setup(SetupArgs a) {
   if (a.hash_dst && i0 == 0) *a.hash_dst = a.hash;
 }
 
+// ------------------------------------------------------------ host side
+struct Plan {
+  std::vector<Layer> table;
+  int64_t ex_words = 0;
+  bool ok = false;
+};
+
+// The kernel's table for these layers, or ok = false if some linear is
+// outside the kernel's limits.
+Plan make_plan(const dfssm_layer* layers, int n) {
+  Plan p;
+  if (n <= 0) return p;
+  p.table.resize(n);
+  int64_t y_off = 0, w = 0;
+  for (int l = 0; l < n; ++l) {
+    const dfssm_layer& D = layers[l];
+    const int64_t K = D.K, N = D.N, r = D.r;
+    const int64_t Nc = l + 1 < n ? layers[l + 1].K : 0;
+    // (N >= 4: at rank 0 the A loads read 16 bytes of alpha)
+    if (K % 256 != 0 || K > 8 * kMaxKs || r < 0 || r > kMaxR || r % 4 != 0 || N < 4 || Nc > N) return p;
+    if (Nc % kGrid != 0) return p;
+    const int64_t cpr = Nc / kGrid, T = N - Nc, tq = T / kGrid, trem = T % kGrid;
+    const int64_t rmax = cpr + tq + (trem > 0 ? 1 : 0);
+    if (rmax > kMaxRed) return p;
+    const int64_t na_max = kSlices * cpr + kSlices * tq + std::min<int64_t>(kSlices, trem);
+    const int64_t rowbytes = K / 64, us = rowbytes % 16 == 0 ? 16 : 4;
+    const int64_t sign_ni = dfssm::ceil_div(na_max * (rowbytes / us), 64);
+    const int64_t a_ni = dfssm::ceil_div(((r + kRankGroups - 1) / kRankGroups) * (K / 8) / 16, 64);
+    const int64_t ub = r % 16 == 0 ? 16 : 4;
+    const int64_t b_ni = r > 0 ? dfssm::ceil_div(rmax * (r / ub), 64) : 0;
+    if (sign_ni + a_ni + b_ni + 2 > kNB) return p;
+    const int64_t o_a = sign_ni * 64 * us, o_b = o_a + a_ni * 1024, o_al = o_b + b_ni * 64 * ub,
+                  o_be = o_al + 256;
+    if (o_be + 256 > kSlotBytes) return p;
+    Layer& e = p.table[l];
+    const bool lr = r > 0;
+    e.w_bits = D.w_bits;
+    e.alpha = D.alpha;
+    // rank 0: the kernel's loads stay on valid addresses, never used
+    e.A = lr ? D.A : reinterpret_cast<const int8_t*>(D.alpha);
+    e.B = lr ? D.B : reinterpret_cast<const int8_t*>(D.alpha);
+    e.beta = lr ? D.beta : D.alpha;
+    e.K = (int32_t)K;
+    e.N = (int32_t)N;
+    e.r = (int32_t)r;
+    e.Nc = (int32_t)Nc;
+    e.cpr = (int32_t)cpr;
+    e.tq = (int32_t)tq;
+    e.trem = (int32_t)trem;
+    e.us = (int32_t)us;
+    e.ub = (int32_t)ub;
+    e.o_a = (int32_t)o_a;
+    e.o_b = (int32_t)o_b;
+    e.o_al = (int32_t)o_al;
+    e.o_be = (int32_t)o_be;
+    e.rh = (int32_t)((r + kRankGroups - 1) / kRankGroups);
+    e.y_off = y_off;
+    y_off += N;
+    e.part_off = w;
+    w += N * kSlices;
+    e.p_off = w;
+    w += (int64_t)kXcds * kSlices * kMaxR;
+    e.yw_off = w;
+    w += Nc;
+    e.mx_off = w;
+    w += kGrid;
+  }
+  p.ex_words = dfssm::round_up(w, 32);
+  p.ok = true;
+  return p;
+}
+
+// Persistent workspace: table, fingerprint, exchange words, status word,
+// epoch words.
+struct PLayout {
+  size_t off_table, off_hash, off_ex, off_status, off_epoch, bytes;
+};
+PLayout playout(const Plan& p, int n) {
+  PLayout o{};
+  size_t at = 0;
+  o.off_table = at;
+  at += (size_t)dfssm::round_up((int64_t)(n * sizeof(Layer)), 256);
+  o.off_hash = at;
+  at += 256;
+  o.off_ex = at;
+  at += (size_t)dfssm::round_up(p.ex_words * 8, 256);
+  o.off_status = at;
+  at += 256;
+  o.off_epoch = at;
+  at += (size_t)dfssm::kEpochGroups * dfssm::kEpochStride * 8;
+  o.bytes = at;
+  return o;
+}
+
+// FNV-1a fingerprint over the table bytes and the layer count.
+uint64_t fingerprint(const Plan& p, int n) {
+  uint64_t h = 1469598103934665603ull;
+  auto mix = [&](const void* q, size_t len) {
+    const unsigned char* b = static_cast<const unsigned char*>(q);
+    for (size_t i = 0; i < len; ++i) h = (h ^ b[i]) * 1099511628211ull;
+  };
+  mix(&n, sizeof(n));
+  mix(p.table.data(), p.table.size() * sizeof(Layer));
+  return h;
+}
+
 }  // namespace
 
 namespace dfssm {
 
-int chain_lanes_per_row(int64_t K) {
-  const int64_t C = K / 128;
-  int G = 8;
-  while (G < C && G < 64) G *= 2;
-  return G;
+int chain_grid() { return kGrid; }
+
+bool chain_persistent_supported(const dfssm_layer* layers, int n_layers, int64_t M) {
+  if (M != 1) return false;
+  return make_plan(layers, n_layers).ok;
 }
 
-int chain_grid() { return kMaxGrid; }  // one workgroup per CU
-
-bool chain_persistent_supported(const dfssm_layer* layers, int n_layers, int64_t M, int nwg) {
-  if (M != 1 || nwg > kMaxGrid) return false;
-  for (int l = 0; l < n_layers; ++l) {
-    const dfssm_layer& L = layers[l];
-    if (L.K % 128 != 0 || L.K > kChainMaxK || L.r % 4 != 0) return false;
-    if (L.r > kChainAccRows * kChainWgPerXcd) return false;
-    const int G = chain_lanes_per_row(L.K);
-    if (L.r / 4 > G) return false;
-    const int64_t R = ceil_div(L.N, nwg);
-    if (ceil_div(R, kChainWaves * (64 / G)) > kChainMaxSteps) return false;
-  }
-  return true;
+size_t chain_persistent_bytes(const dfssm_layer* layers, int n_layers) {
+  const Plan p = make_plan(layers, n_layers);
+  return p.ok ? playout(p, n_layers).bytes : 0;
 }
 
-hipError_t launch_chain_setup(const ChainLayerDev* table_host, ChainLayerDev* table_dev, int n_layers,
-                              uint64_t* exch, int64_t exch_words, uint64_t* hash_dev, uint64_t hash,
-                              hipStream_t st) {
-  for (int first = 0; first < n_layers; first += kChainSetupChunk) {
+size_t chain_status_offset(const dfssm_layer* layers, int n_layers) {
+  const Plan p = make_plan(layers, n_layers);
+  return playout(p, n_layers).off_status;
+}
+
+hipError_t chain_persistent_prepare(const dfssm_layer* layers, int n_layers, void* ws, hipStream_t st) {
+  const Plan p = make_plan(layers, n_layers);
+  if (!p.ok) return hipErrorInvalidValue;
+  const PLayout o = playout(p, n_layers);
+  char* base = static_cast<char*>(ws);
+  const uint64_t h = fingerprint(p, n_layers);
+  Layer* table = reinterpret_cast<Layer*>(base + o.off_table);
+  for (int first = 0; first < n_layers; first += kSetupChunk) {
     SetupArgs a{};
-    a.count = n_layers - first < kChainSetupChunk ? n_layers - first : kChainSetupChunk;
-    for (int i = 0; i < a.count; ++i) a.e[i] = table_host[first + i];
-    a.table = table_dev;
+    a.count = std::min(kSetupChunk, n_layers - first);
+    for (int i = 0; i < a.count; ++i) a.e[i] = p.table[first + i];
+    a.table = table;
     a.first = first;
-    a.zero_base = exch;
-    a.zero_words = first == 0 ? exch_words : 0;
-    // the last chunk publishes the table's fingerprint (stream order puts it
-    // after every chunk)
-    a.hash_dst = first + kChainSetupChunk >= n_layers ? hash_dev : nullptr;
-    a.hash = hash;
-    chain_setup<<<dim3(first == 0 ? 256 : 1), dim3(256), 0, st>>>(a);
-    hipError_t e = hipGetLastError();
+    // the first launch clears the exchange words, the status and the epochs
+    a.zero_base = first == 0 ? reinterpret_cast<uint64_t*>(base + o.off_ex) : nullptr;
+    a.zero_words = first == 0 ? (int64_t)(o.bytes - o.off_ex) / 8 : 0;
+    // the last chunk publishes the fingerprint (stream order puts it after
+    // every chunk)
+    a.hash_dst = first + kSetupChunk >= n_layers ? reinterpret_cast<uint64_t*>(base + o.off_hash) : nullptr;
+    a.hash = h;
+    chain_setup<<<dim3(first == 0 ? 1024 : 1), dim3(256), 0, st>>>(a);
+    const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }
 
-// A plain launch: one workgroup per CU fits (launch bounds of 1024 threads,
-// one block per CU), and the kernel's placement step waits, with a bound,
-// for every workgroup to publish its XCD; a grid that is not resident
-// together (other work holding CUs for longer than that bound) ends with
-// the placement status bit instead of waiting.
+// A plain launch of one workgroup per CU (its LDS use admits one per CU);
+// the kernel needs the whole grid resident at once and ends every wait with
+// a bound, so a grid that is not (other work holding CUs for longer than
+// that bound) ends with a status bit instead of waiting.
+hipError_t chain_persistent_run(const dfssm_layer* layers, int n_layers, const int8_t* q0, const float* s0,
+                                float* y_all, void* ws, hipStream_t st) {
+  const Plan p = make_plan(layers, n_layers);
+  if (!p.ok) return hipErrorInvalidValue;
+  const PLayout o = playout(p, n_layers);
+  char* base = static_cast<char*>(ws);
+  chain_persistent<<<dim3(kGrid), dim3(kThreads), 0, st>>>(
+      reinterpret_cast<const Layer*>(base + o.off_table), n_layers, q0, s0,
+      reinterpret_cast<uint64_t*>(base + o.off_ex), p.ex_words, reinterpret_cast<unsigned*>(base + o.off_status),
+      reinterpret_cast<uint64_t*>(base + o.off_epoch), y_all, reinterpret_cast<const uint64_t*>(base + o.off_hash),
+      fingerprint(p, n_layers));
+  return hipGetLastError();
+}
+
 hipError_t launch_zero_words(uint64_t* p, int64_t words, hipStream_t st) {
   if (words <= 0) return hipSuccess;
   SetupArgs a{};
@@ -746,14 +854,6 @@ hipError_t launch_zero_words(uint64_t* p, int64_t words, hipStream_t st) {
   a.zero_words = words;
   const int64_t blocks = std::min<int64_t>(1024, ceil_div(words, 256));
   chain_setup<<<dim3((unsigned)blocks), dim3(256), 0, st>>>(a);
-  return hipGetLastError();
-}
-
-hipError_t launch_chain_run(const ChainLayerDev* table_dev, int n_layers, const int8_t* q0, const float* s0,
-                            const ChainExch& ex, float* y_all, const uint64_t* hash_dev, uint64_t hash,
-                            hipStream_t st) {
-  chain_persistent<<<dim3(chain_grid()), dim3(kCT), 0, st>>>(table_dev, n_layers, q0, s0, ex, y_all, hash_dev,
-                                                            hash);
   return hipGetLastError();
 }
 

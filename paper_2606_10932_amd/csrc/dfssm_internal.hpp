@@ -156,74 +156,30 @@ hipError_t launch_embed_gather(const int8_t* E, const float* scale, int64_t V, i
 hipError_t launch_lm_head(const int8_t* q, const float* s, int64_t M, int64_t d, const int8_t* E,
                           const float* scale, int64_t V, float* logits, int32_t* acc, hipStream_t st);
 
-// ---------------------------------------------------------------- chain
-// Largest K the persistent chain kernel takes (its per-thread register
-// staging of the previous output holds K/512 values).
-constexpr int kChainMaxK = 4096;
-// Row steps of one workgroup per linear held in registers, and waves per
-// role group of the persistent kernel.
-constexpr int kChainMaxSteps = 2;
-constexpr int kChainWaves = 8;
-// LoRA down-projection rows one workgroup computes per linear; the chain
-// needs r <= kChainAccRows * (workgroups on the smallest XCD).
-constexpr int kChainAccRows = 2;
-// Workgroups per XCD the host assumes when it accepts a chain (256
-// workgroups dealt to 8 XCDs); the kernel checks the real placement.
-constexpr int kChainWgPerXcd = 32;
-// XCDs (L2 domains) the exchange regions provide for.
-constexpr int kChainXcds = 8;
-// Layer-table entries passed by value per setup launch.
-constexpr int kChainSetupChunk = 48;
-
-// Exchange regions of the persistent chain (all inside the workspace):
-//   y_ll    [ysum]                 every linear's outputs as {tag, value} words
-//   y_rel   [kChainXcds][ysum]     each XCD's relayed copy of y_ll
-//   acc_rel [kChainXcds][L][kMaxRank]  each XCD's acc_a words
-//   xmap    [grid]                 workgroup -> XCD id words
-struct ChainExch {
-  uint64_t* y_ll;
-  uint64_t* y_rel;
-  uint64_t* acc_rel;
-  uint64_t* xmap;
-  unsigned* status;
-  uint64_t* epoch;  // kEpochGroups words {epoch:32, arrivals:32}, advanced once per launch
-  int64_t ysum;
-  int32_t r_max;
-};
-
-// One linear of the persistent chain, as the kernel reads it (device table).
-struct ChainLayerDev {
-  const uint32_t* w_bits;
-  const float* alpha;
-  const int8_t* A;
-  const int8_t* B;
-  const float* beta;
-  int32_t K, N, r;
-  int32_t lgG;    // log2 of the lanes per output row (G = 8..64)
-  int32_t R;      // output rows per workgroup, ceil(N / grid)
-  int32_t pad;
-  int64_t y_off;  // offset of this linear's outputs in y_all
-};
-
 // Compute units of the current device (cached per device; 256 if the query
 // fails).
 int device_cu_count();
 
-int chain_lanes_per_row(int64_t K);
+// ---------------------------------------------------------------- chain
+// The persistent chain kernel (M = 1): one launch of one workgroup per CU
+// over a prepared workspace.  Workgroups the grid holds.
 int chain_grid();
-bool chain_persistent_supported(const dfssm_layer* layers, int n_layers, int64_t M, int nwg);
-// Writes the layer table (by value, chunked) to table_dev, zeroes the
-// exchange region [exch, exch + exch_words) and stores the table's
-// fingerprint at hash_dev.
-hipError_t launch_chain_setup(const ChainLayerDev* table_host, ChainLayerDev* table_dev, int n_layers,
-                              uint64_t* exch, int64_t exch_words, uint64_t* hash_dev, uint64_t hash,
-                              hipStream_t st);
+// Whether the persistent kernel takes these linears (M = 1; every K a
+// multiple of 256 and <= 4096; r <= 64, r % 4 == 0; each linear's rows and
+// operands within the kernel's per-workgroup limits).
+bool chain_persistent_supported(const dfssm_layer* layers, int n_layers, int64_t M);
+// Workspace bytes of the persistent chain (layer table, fingerprint,
+// exchange words, status word, epoch words), 0 if not supported; the
+// status word's offset.
+size_t chain_persistent_bytes(const dfssm_layer* layers, int n_layers);
+size_t chain_status_offset(const dfssm_layer* layers, int n_layers);
+// Writes the layer table and its fingerprint and zeroes the rest.
+hipError_t chain_persistent_prepare(const dfssm_layer* layers, int n_layers, void* ws, hipStream_t st);
+// The chain on a prepared workspace: one kernel launch.
+hipError_t chain_persistent_run(const dfssm_layer* layers, int n_layers, const int8_t* q0, const float* s0,
+                                float* y_all, void* ws, hipStream_t st);
 // Zeroes `words` 64-bit words at p with a fill kernel (capture-safe).
 hipError_t launch_zero_words(uint64_t* p, int64_t words, hipStream_t st);
-// Launch of the persistent chain kernel on a prepared workspace.
-hipError_t launch_chain_run(const ChainLayerDev* table_dev, int n_layers, const int8_t* q0, const float* s0,
-                            const ChainExch& ex, float* y_all, const uint64_t* hash_dev, uint64_t hash,
-                            hipStream_t st);
 
 }  // namespace dfssm
 

@@ -80,31 +80,26 @@ def test_chain_decode_sweep_full(env):
 
 
 PERSISTENT_SHAPES = {
-    0: [(128, 256), (256, 4000), (3968, 2048), (2048, 16384), (4096, 130)],
-    8: [(128, 256), (256, 4000), (3968, 2048), (2048, 16384), (4096, 130)],
-    64: [(2048, 4000), (3968, 2048), (2048, 16384), (4096, 130), (128, 64)][:4],
+    # (K, N) of each linear; every K a multiple of 256 (<= 4096), each N at
+    # least the next K.  Ragged N (tails not a multiple of 256), a linear
+    # with 64 rows per reducer (N = 16384), the 130M projections' K = 768,
+    # 1536, and ranks 0, 8, 12, 64.
+    0: [(256, 4000), (3840, 2048), (2048, 16384), (4096, 130)],
+    8: [(256, 4000), (3840, 2048), (2048, 16384), (4096, 130)],
+    12: [(512, 1300), (1280, 777), (768, 3352), (1536, 768)],
+    64: [(2048, 4000), (3840, 2048), (2048, 16000), (4096, 130)],
 }
 
 
-def _lanes_per_row(K):
-    G = 8
-    while G < K // 128 and G < 64:
-        G *= 2
-    return G
-
-
-@pytest.mark.parametrize("r", [0, 8, 64])
+@pytest.mark.parametrize("r", [0, 8, 12, 64])
 def test_chain_persistent_shapes(env, r):
-    """Shapes inside the persistent kernel's limits (K % 128 == 0, K <= 4096,
-    r % 4 == 0, r <= 4 lanes-per-row, at most 2 row steps of 8 waves per
-    workgroup): ragged N, rank 0, and a linear that needs both row steps
-    (N = 16384 at K = 2048)."""
+    """Shapes inside the persistent kernel's limits: ragged N, rank 0 and
+    ranks that are not multiples of 16, the largest reducer share."""
     shapes = PERSISTENT_SHAPES[r]
-    for K, N in shapes:
-        G = _lanes_per_row(K)
-        assert K % 128 == 0 and K <= 4096 and r % 4 == 0 and r // 4 <= G
-        rows_per_wg = -(-N // 256)
-        assert -(-rows_per_wg // (8 * (64 // G))) <= 2
+    for l, (K, N) in enumerate(shapes):
+        Nc = shapes[l + 1][0] if l + 1 < len(shapes) else 0
+        assert K % 256 == 0 and K <= 4096 and r % 4 == 0 and Nc <= N and Nc % 256 == 0
+        assert Nc // 256 + -(-(N - Nc) // 256) <= 64
     say(f"chain persistent r={r}")
     _check_chain(env, shapes, r=r, M=1, key=100 + r)
 
