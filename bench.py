@@ -53,7 +53,10 @@ def parse():
     p.add_argument("--model-batches", default="1,8,32,128,512", help="batch sizes of the decode step figures")
     p.add_argument("--model-i4-batches", default="1,32",
                    help="batch sizes of the decode step figures with int4 LoRA factors")
+    p.add_argument("--no-diag", action="store_true", help="skip the chain's stream and exchange floor diagnostics")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="minimum CPU oracle sample time")
+    p.add_argument("--cpu-single-seconds", type=float, default=4.0,
+                   help="minimum single-thread CPU oracle sample time")
     p.add_argument("--copy-calibration-mib", type=int, default=0,
                    help="run one plain device copy of this size first (for HBM counter scaling)")
     return p.parse_args()
@@ -68,8 +71,9 @@ def chain_source_digest() -> str:
 
 
 def measured_traffic():
-    """HBM bytes per chain launch from the committed counter summary, or None
-    when it is missing or was taken on other kernel sources."""
+    """(L2-miss bytes, DRAM-request bytes) per chain launch from the committed
+    counter summary; (None, None) when it is missing or was taken on other
+    kernel sources."""
     try:
         kv = {}
         with open(TRAFFIC_FILE) as f:
@@ -78,10 +82,21 @@ def measured_traffic():
                     k, v = line.split(":", 1)
                     kv[k.strip()] = v.strip()
         if kv.get("chain_source_sha256") != chain_source_digest():
-            return None
-        return int(float(kv["hbm_bytes_per_launch"]))
+            return None, None
+        return int(float(kv["l2_miss_bytes_per_launch"])), int(float(kv["dram_req_bytes_per_launch"]))
     except (OSError, KeyError, ValueError):
-        return None
+        return None, None
+
+
+def host_cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def main():
@@ -171,6 +186,64 @@ def main():
     t1.record(stream)
     torch.cuda.synchronize()
     ms_warm = t0.elapsed_time(t1) / args.steps
+
+    # ---- diagnostics: the two floors under the chain ---------------------------
+    diag = None
+    if not args.no_diag:
+        # (1) the same layers' operand loads alone, through the chain's own
+        #     loading schedule (no arithmetic, no exchange): the stream floor
+        def sstep(i):
+            c = i % len(copies)
+            D.chain_stream_floor(arrays[c], workspaces[c], stream=stream)
+        for i in range(3):
+            sstep(i)
+        sev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        for i in range(args.steps):
+            sev[i][0].record(stream)
+            sstep(i)
+            sev[i][1].record(stream)
+        torch.cuda.synchronize()
+        stream_ms = float(np.median([a.elapsed_time(b) for a, b in sev]))
+        if max(D.chain_status(arrays[c], M, workspaces[c]) for c in range(len(copies))):
+            print("chain stream diagnostic: status word set", file=sys.stderr)
+            sys.exit(3)
+        stream_gbs = weight_bytes / (stream_ms * 1e-3) / 1e9
+        # (2) the chain on 96 tiny linears (K = N = 256, r = 4, 12 KB of
+        #     weights each): what is left is the per-linear exchange and
+        #     compute latency
+        tiny = [S.weights(256, 256, 4, key=(60, i)) for i in range(96)]
+        tiny_bytes = sum(S.weight_bytes(ly) for ly in tiny)
+        tarr = D.make_layers([{k: dev(v) for k, v in ly.items()} for ly in tiny])
+        tws = torch.zeros(D.chain_workspace_bytes(tarr, 1), dtype=torch.uint8, device="cuda")
+        D.chain_prepare(tarr, 1, tws)
+        tq, ts = D.quantize_act(dev(S.activations(1, 256, key=(61,))))
+        ty = torch.empty(96 * 256, dtype=torch.float32, device="cuda")
+        for i in range(3):
+            D.chain_run(tarr, tq, ts, ty, tws, stream=stream)
+        tev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        for i in range(args.steps):
+            tev[i][0].record(stream)
+            D.chain_run(tarr, tq, ts, ty, tws, stream=stream)
+            tev[i][1].record(stream)
+        torch.cuda.synchronize()
+        tiny_ms = float(np.median([a.elapsed_time(b) for a, b in tev]))
+        if D.chain_status(tarr, 1, tws):
+            print("tiny chain diagnostic: status word set", file=sys.stderr)
+            sys.exit(3)
+        diag = {
+            "stream_floor": {
+                "workload": "the sweep's 96 linears, operand loads only (chain_stream: the persistent chain's "
+                            "direct-to-LDS schedule, no arithmetic, no exchange), 3 weight copies rotated",
+                "us_per_sweep": round(stream_ms * 1e3, 2), "gbs": round(stream_gbs, 1),
+                "frac_hbm_peak": round(stream_gbs / PEAK_HBM_GBS, 4),
+                "chain_over_floor": round(launch_ms / stream_ms, 2)},
+            "exchange_floor": {
+                "workload": "persistent chain of 96 linears K=N=256, r=4, M=1 (%d B of weights in all)" % tiny_bytes,
+                "us_per_sweep": round(tiny_ms * 1e3, 2), "us_per_linear": round(tiny_ms * 1e3 / 96, 3)},
+        }
+        del tarr, tws, ty
 
     # ---- prefill: 2048-token in_proj -----------------------------------------
     prefill = None
@@ -437,7 +510,22 @@ def main():
         cpu = {"value": round(reps * weight_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": o.threads(),
                "kind": "oracle",
                "sample": f"the full 96-linear sweep (weight copy 0, same input) run {reps} times in {dt:.1f} s",
-               "us_per_layer": round(dt / reps / 48 * 1e6, 1)}
+               "us_per_layer": round(dt / reps / 48 * 1e6, 1), "host_cpu": host_cpu_model(),
+               "host_cpus_visible": os.cpu_count()}
+        # the same oracle on one thread
+        threads = o.threads()
+        o.set_threads(1)
+        reps1, t = 0, time.perf_counter()
+        while True:
+            o.chain(host0, q0h, s0h)
+            reps1 += 1
+            dt1 = time.perf_counter() - t
+            if dt1 >= args.cpu_single_seconds:
+                break
+        o.set_threads(threads)
+        cpu["single_thread"] = {"value": round(reps1 * weight_bytes / dt1 / 1e9, 4), "unit": "GB/s", "cores": 1,
+                                "us_per_layer": round(dt1 / reps1 / 48 * 1e6, 1),
+                                "sample": f"the full 96-linear sweep run {reps1} times in {dt1:.1f} s on one thread"}
 
         def timed(fn, seconds):
             n, t0h = 0, time.perf_counter()
@@ -472,7 +560,7 @@ def main():
         cpu["decode_layer_sample"] = (f"one 1.3B decode layer at batch 1 (residual norm, in_proj, conv + SSM step, "
                                       f"gated norm, out_proj), {n} runs")
 
-    traffic = measured_traffic()
+    traffic, dram_bytes = measured_traffic()
     out = {
         "metric": "effective packed-weight GB/s (1.3B decode sweep, M=1)",
         "value": round(gbs, 2),
@@ -494,12 +582,16 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "chain_persistent", "achieved": round(launch_gbs, 2),
                      "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(launch_gbs / PEAK_HBM_GBS, 4),
                      "traffic": traffic, "avg_launch_us": round(launch_ms * 1e3, 2),
+                     "traffic_is": "L2-miss bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-scaled): the "
+                                   "Infinity Cache or HBM serves them",
+                     "dram_req_bytes": dram_bytes,
                      "algorithmic_bytes_per_launch": weight_bytes},
         "prefill": prefill,
         "decode_linears": decode,
         "lm_head": lm,
         "decode_step": model_fig,
         "cpu_baseline": cpu,
+        "diagnostics": diag,
     }
     print(json.dumps(out), flush=True)
 

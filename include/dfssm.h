@@ -223,10 +223,12 @@ dfssm_status dfssm_scaffold_lora_chain(const dfssm_layer* layers, int n_layers, 
  * workspace and clears the exchange region and the status word
  * (stream-ordered, asynchronous).  Needed once per (layers, workspace): a
  * prepared workspace can be run any number of times, as long as nothing
- * but dfssm_chain_run writes to it in between.  Chains the persistent
- * kernel does not take (M > 1, K % 128 != 0, K > 4096, r % 4 != 0, ...)
- * run as a sequence of quantise and linear launches; for them preparation
- * clears the linears' exchange state in the workspace.
+ * but dfssm_chain_run writes to it in between.  The persistent kernel
+ * takes chains at M = 1 with, for every linear, K % 256 == 0, K <= 4096,
+ * r <= 64, r % 4 == 0, N >= 4, the next linear's K a multiple of 256, at
+ * most 64 output rows per workgroup and operands that fit its LDS ring;
+ * other chains run as a sequence of quantise and linear launches, and for
+ * them preparation clears the linears' exchange state in the workspace.
  * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */
 dfssm_status dfssm_chain_prepare(const dfssm_layer* layers, int n_layers, int64_t M,
                                  void* workspace, size_t workspace_bytes, void* stream);
@@ -247,17 +249,31 @@ dfssm_status dfssm_chain_run(const dfssm_layer* layers, int n_layers, int64_t M,
 
 /* Synchronises `stream` and reads the persistent chain's status word into
  * *status (host): 0 = fine; bit 1 = a wait for a previous output timed out;
- * bit 2 = a wait for the LoRA down-projection timed out; bit 8 = the
- * workspace was not prepared for these layers; bit 16 = the workgroups'
- * placement on the XCDs could not be read or leaves an XCD too few
- * workgroups for the rank (r > 2 x workgroups of the smallest XCD).  After a
- * nonzero status the outputs of that run are incomplete.  Bits accumulate
- * over runs until the next dfssm_chain_prepare.
+ * bit 2 = a wait for a row or rank partial timed out (a workgroup of the
+ * grid was not resident, or another one left early); bit 8 = the workspace
+ * was not prepared for these layers.  After a nonzero status the outputs of
+ * that run are incomplete.  Bits accumulate over runs until the next
+ * dfssm_chain_prepare.
  * Always 0 for chains that do not use the persistent kernel.
  * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */
 dfssm_status dfssm_chain_status(const dfssm_layer* layers, int n_layers, int64_t M,
                                 const void* workspace, size_t workspace_bytes, unsigned* status,
                                 void* stream);
+
+/* Diagnostic, not part of the computation: runs only the persistent
+ * chain's operand loads -- each workgroup's direct-to-LDS loads of its sign
+ * words, A slice, B rows and row scales for every linear, with the chain
+ * kernel's placement and LDS ring, back to back (one linear in flight while
+ * the previous lands) -- with no arithmetic, no exchange and no output.
+ * One launch takes the time that streaming the chain's weights alone sets,
+ * the floor under dfssm_chain_run on the same layers.  Needs a workspace
+ * prepared by dfssm_chain_prepare for these layers at M = 1 (it only reads
+ * the layer table; a fingerprint mismatch sets status bit 8 and loads
+ * nothing).
+ * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED (layers the persistent
+ * kernel does not take), DEVICE. */
+dfssm_status dfssm_chain_stream_floor(const dfssm_layer* layers, int n_layers, void* workspace,
+                                      size_t workspace_bytes, void* stream);
 
 /* The tied int8 embedding table (Sec. 3.3 and Table 1: the token embedding
  * is stored in int8 with one fp32 scale per row and shared with the LM

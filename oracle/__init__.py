@@ -57,6 +57,8 @@ class Oracle:
         lib.dfssm_ref_chain.argtypes = [i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         lib.dfssm_ref_chain.restype = i32
         lib.dfssm_ref_threads.restype = i32
+        lib.dfssm_ref_set_threads.argtypes = [i32]
+        lib.dfssm_ref_set_threads.restype = None
         lib.dfssm_ref_embed_gather.argtypes = [vp, vp, i64, i64, vp, i64, vp]
         lib.dfssm_ref_embed_gather.restype = i32
         lib.dfssm_ref_lm_head.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp]
@@ -275,6 +277,10 @@ class Oracle:
 
     def threads(self) -> int:
         return self.lib.dfssm_ref_threads()
+
+    def set_threads(self, n: int) -> None:
+        """Thread count of later oracle calls (timing only; results do not depend on it)."""
+        self.lib.dfssm_ref_set_threads(int(n))
 
 
 class OracleError(RuntimeError):

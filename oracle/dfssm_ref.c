@@ -26,6 +26,14 @@ int dfssm_ref_threads(void) {
 #endif
 }
 
+void dfssm_ref_set_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* IEEE 754 binary16: 1 sign bit, 5 exponent bits (bias 15), 10 fraction
  * bits.  exponent 0 -> subnormal f * 2^-24; exponent 31 -> Inf/NaN;
  * otherwise (1024 + f) * 2^(e - 25).  Every binary16 value is exactly

@@ -199,6 +199,9 @@ int dfssm_ref_gate_norm_quant(const float* y, const float* z, int64_t ldz, const
 
 /* Number of OpenMP threads the row loops use (1 without OpenMP). */
 int dfssm_ref_threads(void);
+/* Sets the number of OpenMP threads later calls use (n > 0; no effect
+ * without OpenMP).  For timing the oracle single-threaded. */
+void dfssm_ref_set_threads(int n);
 
 #ifdef __cplusplus
 }

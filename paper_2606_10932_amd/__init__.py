@@ -22,6 +22,7 @@ PATH_AUTO, PATH_DECODE, PATH_MFMA, PATH_MFMA_FEW = 0, 1, 2, 3
 EXPORTS = ["dfssm_quantize_act", "dfssm_linear_workspace_bytes", "dfssm_scaffold_lora_linear",
            "dfssm_scaffold_lora_linear_ex", "dfssm_chain_workspace_bytes",
            "dfssm_scaffold_lora_chain", "dfssm_chain_prepare", "dfssm_chain_run", "dfssm_chain_status",
+           "dfssm_chain_stream_floor",
            "dfssm_embed_gather", "dfssm_lm_head", "dfssm_add_rmsnorm_quant", "dfssm_gate_norm_quant",
            "dfssm_ssm_step", "dfssm_linear_i4_workspace_bytes", "dfssm_scaffold_lora_linear_i4",
            "dfssm_mamba2_state_bytes", "dfssm_mamba2_workspace_bytes",
@@ -84,6 +85,8 @@ def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dfssm_chain_run.restype = i32
     lib.dfssm_chain_status.argtypes = [ctypes.POINTER(Layer), i32, i64, vp, sz, ctypes.POINTER(ctypes.c_uint), vp]
     lib.dfssm_chain_status.restype = i32
+    lib.dfssm_chain_stream_floor.argtypes = [ctypes.POINTER(Layer), i32, vp, sz, vp]
+    lib.dfssm_chain_stream_floor.restype = i32
     lib.dfssm_embed_gather.argtypes = [vp, vp, i64, i64, vp, i64, vp, vp]
     lib.dfssm_embed_gather.restype = i32
     lib.dfssm_lm_head.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp, vp]
@@ -259,7 +262,8 @@ def scaffold_lora_linear_noalloc(q, s, w_bits, alpha, A, B, beta, y, stream=None
 
 
 def make_layers(layers: Sequence[dict]):
-    """ctypes array of dfssm_layer from dicts of device tensors."""
+    """ctypes array of dfssm_layer from dicts of device tensors.  The array
+    holds references to the tensors, so their memory lives as long as it."""
     arr = (Layer * len(layers))()
     for i, ly in enumerate(layers):
         r = 0 if ly.get("A") is None else ly["A"].shape[0]
@@ -267,6 +271,7 @@ def make_layers(layers: Sequence[dict]):
                        ly["A"].data_ptr() if r else None, ly["B"].data_ptr() if r else None,
                        ly["beta"].data_ptr() if r else None, ly["w_bits"].shape[1] * 32,
                        ly["w_bits"].shape[0], r)
+    arr._tensors = [dict(ly) for ly in layers]
     return arr
 
 
@@ -313,6 +318,13 @@ def chain_status(layer_arr, M: int, workspace, stream=None) -> int:
     _check(lib.dfssm_chain_status(layer_arr, len(layer_arr), M, workspace.data_ptr(), workspace.numel(),
                                   ctypes.byref(out), _stream(stream)))
     return int(out.value)
+
+
+def chain_stream_floor(layer_arr, workspace, stream=None):
+    """Diagnostic: the persistent chain's operand loads alone (no arithmetic,
+    no exchange, no output) on a workspace prepared for these layers at M=1."""
+    _check(lib.dfssm_chain_stream_floor(layer_arr, len(layer_arr), workspace.data_ptr(), workspace.numel(),
+                                        _stream(stream)))
 
 
 def embed_gather(E, scale, tok, x=None, stream=None):

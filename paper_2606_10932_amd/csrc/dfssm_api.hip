@@ -523,6 +523,19 @@ dfssm_status dfssm_chain_status(const dfssm_layer* layers, int n_layers, int64_t
   return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain status read");
 }
 
+dfssm_status dfssm_chain_stream_floor(const dfssm_layer* layers, int n_layers, void* workspace,
+                                      size_t workspace_bytes, void* stream) {
+  clear_error();
+  dfssm_status st = validate_chain(layers, n_layers, 1);
+  if (st != DFSSM_OK || n_layers == 0) return st;
+  ChainLayout c;
+  st = chain_common(layers, n_layers, 1, workspace, workspace_bytes, &c);
+  if (st != DFSSM_OK) return st;
+  if (!c.persistent) return fail(DFSSM_ERR_UNSUPPORTED, "the persistent chain kernel does not take these layers");
+  hipError_t e = dfssm::chain_stream_run(layers, n_layers, workspace, (hipStream_t)stream);
+  return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain stream launch");
+}
+
 dfssm_status dfssm_embed_gather(const int8_t* E, const float* scale, int64_t V, int64_t d, const int32_t* tok,
                                 int64_t M, float* x, void* stream) {
   clear_error();

@@ -247,7 +247,8 @@ __device__ __forceinline__ int udiv(int u, uint32_t m) { return (int)(((uint32_t
 // rh A rows' slice, its reducer rows' B rows, alpha and beta, into the slot
 // at LDS address sb.  Every address is in range: lanes past the data read
 // the array's first unit.
-__device__ void issue_batch(const Layer& L, int x, int kap, int h, int lam, uint32_t sb, int lane) {
+// Returns the number of load instructions issued.
+__device__ int issue_batch(const Layer& L, int x, int kap, int h, int lam, uint32_t sb, int lane) {
   int n_issued = 0;
   const int K = L.K, Ks = K >> 3, rowbytes = K >> 6;
   {  // sign rows of the row group, this slice
@@ -300,7 +301,7 @@ __device__ void issue_batch(const Layer& L, int x, int kap, int h, int lam, uint
     lds_dma4(voff, L.beta, sb + (uint32_t)L.o_be);
     n_issued += 2;
   }
-  (void)n_issued;
+  return n_issued;
 }
 
 // Workgroup flags in LDS, read and written as LDS operations: a volatile
@@ -657,6 +658,63 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
   }
 }
 
+// s_waitcnt vmcnt(n) for a wave-uniform n <= 2 * kNB (the count is an
+// immediate of the instruction).
+__device__ __forceinline__ void wait_vmcnt_le(int n) {
+  switch (n) {
+#define CHAIN_WAIT_CASE(c) \
+  case c:                  \
+    CHAIN_WAIT_VMCNT(c);   \
+    break;
+    CHAIN_WAIT_CASE(1) CHAIN_WAIT_CASE(2) CHAIN_WAIT_CASE(3) CHAIN_WAIT_CASE(4) CHAIN_WAIT_CASE(5)
+    CHAIN_WAIT_CASE(6) CHAIN_WAIT_CASE(7) CHAIN_WAIT_CASE(8) CHAIN_WAIT_CASE(9) CHAIN_WAIT_CASE(10)
+    CHAIN_WAIT_CASE(11) CHAIN_WAIT_CASE(12) CHAIN_WAIT_CASE(13) CHAIN_WAIT_CASE(14) CHAIN_WAIT_CASE(15)
+    CHAIN_WAIT_CASE(16) CHAIN_WAIT_CASE(17) CHAIN_WAIT_CASE(18) CHAIN_WAIT_CASE(19) CHAIN_WAIT_CASE(20)
+    CHAIN_WAIT_CASE(21) CHAIN_WAIT_CASE(22) CHAIN_WAIT_CASE(23) CHAIN_WAIT_CASE(24) CHAIN_WAIT_CASE(25)
+    CHAIN_WAIT_CASE(26) CHAIN_WAIT_CASE(27) CHAIN_WAIT_CASE(28) CHAIN_WAIT_CASE(29) CHAIN_WAIT_CASE(30)
+    CHAIN_WAIT_CASE(31) CHAIN_WAIT_CASE(32) CHAIN_WAIT_CASE(33) CHAIN_WAIT_CASE(34) CHAIN_WAIT_CASE(35)
+    CHAIN_WAIT_CASE(36) CHAIN_WAIT_CASE(37) CHAIN_WAIT_CASE(38) CHAIN_WAIT_CASE(39) CHAIN_WAIT_CASE(40)
+    CHAIN_WAIT_CASE(41) CHAIN_WAIT_CASE(42) CHAIN_WAIT_CASE(43) CHAIN_WAIT_CASE(44) CHAIN_WAIT_CASE(45)
+    CHAIN_WAIT_CASE(46) CHAIN_WAIT_CASE(47) CHAIN_WAIT_CASE(48) CHAIN_WAIT_CASE(49) CHAIN_WAIT_CASE(50)
+    CHAIN_WAIT_CASE(51) CHAIN_WAIT_CASE(52) CHAIN_WAIT_CASE(53) CHAIN_WAIT_CASE(54) CHAIN_WAIT_CASE(55)
+    CHAIN_WAIT_CASE(56)
+#undef CHAIN_WAIT_CASE
+    default:
+      CHAIN_WAIT_VMCNT(0);
+  }
+}
+static_assert(2 * kNB <= 56, "wait_vmcnt_le covers counts up to 56 (the counter holds 63)");
+
+// Diagnostic twin of chain_persistent's loading wave: the same workgroup
+// placement, the same direct-to-LDS batches into the same 3-slot ring, but
+// back to back (batches l+1 and l+2 in flight while batch l lands), with no
+// arithmetic and no exchange.  Its duration is the floor that streaming the
+// chain's operands sets.
+__global__ __launch_bounds__(64, 1) void chain_stream(const Layer* __restrict__ layers, int L, unsigned* status,
+                                                      const uint64_t* __restrict__ table_hash,
+                                                      uint64_t expect_hash) {
+  if (*table_hash != expect_hash) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(status, kStHash);
+    return;
+  }
+  __shared__ __attribute__((aligned(16))) uint8_t ring[kRing][kSlotBytes];
+  const int wg = blockIdx.x, lane = threadIdx.x;
+  const int x = (int)(__builtin_amdgcn_s_getreg((20) | (0 << 6) | ((4 - 1) << 11)) & 7u);  // HW_REG_XCC_ID[3:0]
+  const int lam = wg / kXcds, kap = lam % kSlices, h = lam / kSlices;
+  const uint32_t sb0 = lds_addr(&ring[0][0]);
+  // n1, n2: load instructions of the batches after the one landing
+  issue_batch(layers[0], x, kap, h, lam, sb0, lane);
+  int n1 = L > 1 ? issue_batch(layers[1], x, kap, h, lam, sb0 + kSlotBytes, lane) : 0;
+  for (int l = 0; l < L; ++l) {
+    const int lu = __builtin_amdgcn_readfirstlane(l);
+    int n2 = 0;
+    if (lu + 2 < L)  // into the slot of batch l-1, which has landed
+      n2 = issue_batch(layers[lu + 2], x, kap, h, lam, sb0 + (uint32_t)(((lu + 2) % kRing) * kSlotBytes), lane);
+    wait_vmcnt_le(__builtin_amdgcn_readfirstlane(n1 + n2));  // batch l has landed
+    n1 = n2;
+  }
+}
+
 // Writes a chunk of the layer table and zeroes the exchange region.
 struct SetupArgs {
   Layer e[kSetupChunk];
@@ -844,6 +902,18 @@ hipError_t chain_persistent_run(const dfssm_layer* layers, int n_layers, const i
       reinterpret_cast<uint64_t*>(base + o.off_ex), p.ex_words, reinterpret_cast<unsigned*>(base + o.off_status),
       reinterpret_cast<uint64_t*>(base + o.off_epoch), y_all, reinterpret_cast<const uint64_t*>(base + o.off_hash),
       fingerprint(p, n_layers));
+  return hipGetLastError();
+}
+
+hipError_t chain_stream_run(const dfssm_layer* layers, int n_layers, void* ws, hipStream_t st) {
+  const Plan p = make_plan(layers, n_layers);
+  if (!p.ok) return hipErrorInvalidValue;
+  const PLayout o = playout(p, n_layers);
+  char* base = static_cast<char*>(ws);
+  chain_stream<<<dim3(kGrid), dim3(64), 0, st>>>(reinterpret_cast<const Layer*>(base + o.off_table), n_layers,
+                                                  reinterpret_cast<unsigned*>(base + o.off_status),
+                                                  reinterpret_cast<const uint64_t*>(base + o.off_hash),
+                                                  fingerprint(p, n_layers));
   return hipGetLastError();
 }
 

@@ -178,6 +178,9 @@ hipError_t chain_persistent_prepare(const dfssm_layer* layers, int n_layers, voi
 // The chain on a prepared workspace: one kernel launch.
 hipError_t chain_persistent_run(const dfssm_layer* layers, int n_layers, const int8_t* q0, const float* s0,
                                 float* y_all, void* ws, hipStream_t st);
+// The loading schedule of chain_persistent alone (a diagnostic: no
+// arithmetic, no exchange, nothing written outside LDS).
+hipError_t chain_stream_run(const dfssm_layer* layers, int n_layers, void* ws, hipStream_t st);
 // Zeroes `words` 64-bit words at p with a fill kernel (capture-safe).
 hipError_t launch_zero_words(uint64_t* p, int64_t words, hipStream_t st);
 

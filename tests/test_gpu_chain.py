@@ -137,3 +137,36 @@ def test_chain_prepare_once_run_many(env):
     D.chain_run(arrs[1], dev(q0), dev(s0), y, wss[0])
     assert D.chain_status(arrs[1], 1, wss[0]) & 8
     assert bool((y == -1.0).all())
+
+
+def test_chain_tiny_linears(env):
+    """The exchange-floor workload of the benchmark: 96 linears K = N = 256,
+    r = 4 through the persistent kernel, bit-exact against the oracle."""
+    say("chain: 96 linears K=N=256 r=4")
+    _check_chain(env, [(256, 256)] * 96, r=4, M=1, key=41)
+
+
+def test_chain_stream_floor_diagnostic(env):
+    """The loads-only diagnostic runs on a prepared workspace, leaves the
+    status word clear and the outputs of a later run exact; on a workspace
+    prepared for other layers it sets bit 8."""
+    torch, D, o = env
+    say("chain stream-floor diagnostic")
+    sets = [S.sweep_weights(2, r=64, variant=v) for v in (7, 8)]
+    arrs = [D.make_layers([dev_weights(ly) for ly in hs]) for hs in sets]
+    wss = [torch.zeros(D.chain_workspace_bytes(a, 1), dtype=torch.uint8, device="cuda") for a in arrs]
+    for a, w in zip(arrs, wss):
+        D.chain_prepare(a, 1, w)
+    for _ in range(3):
+        D.chain_stream_floor(arrs[0], wss[0])
+    assert D.chain_status(arrs[0], 1, wss[0]) == 0
+    q0, s0 = o.quantize_act(S.sweep_input(1))
+    ys_ref, _ = o.chain(sets[0], q0, s0)
+    y_all = torch.empty(sum(r.size for r in ys_ref), dtype=torch.float32, device="cuda")
+    D.chain_run(arrs[0], dev(q0), dev(s0), y_all, wss[0])
+    assert D.chain_status(arrs[0], 1, wss[0]) == 0
+    got = host(y_all)
+    ref = np.concatenate([r.reshape(-1) for r in ys_ref])
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+    D.chain_stream_floor(arrs[1], wss[0])
+    assert D.chain_status(arrs[1], 1, wss[0]) & 8

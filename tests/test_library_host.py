@@ -109,6 +109,36 @@ def test_chain_validation(dl):
     st = ctypes.c_uint(7)
     assert dl.lib.dfssm_chain_status(arr, 2, 1, 16, 8, ctypes.byref(st), None) == dl.ERR_WORKSPACE
     assert dl.lib.dfssm_chain_status(arr, 2, 1, 16, 1 << 30, None, None) == dl.ERR_NULL
+    # the loads-only diagnostic: same validation; chains the persistent kernel
+    # does not take (K = 64 here) are refused before any HIP call
+    fs = dl.lib.dfssm_chain_stream_floor
+    assert fs(arr, 2, None, 1 << 30, None) == dl.ERR_NULL
+    assert fs(arr, 2, 16, 8, None) == dl.ERR_WORKSPACE
+    assert fs(arr, 2, 16, 1 << 30, None) == dl.ERR_UNSUPPORTED
+    arr = (L * 2)(L(**good), L(**dict(good, K=128)))
+    assert fs(arr, 2, 16, 1 << 30, None) == dl.ERR_SHAPE
+
+
+def test_make_layers_keeps_tensors(dl):
+    """The layer array holds its tensors: dropping the caller's list must not
+    free memory the array still points at."""
+    import gc
+    import weakref
+    import torch
+    refs = []
+
+    def build():
+        ly = [dict(w_bits=torch.zeros((96, 2), dtype=torch.int32), alpha=torch.zeros(96),
+                   A=torch.zeros((4, 64), dtype=torch.int8), B=torch.zeros((96, 4), dtype=torch.int8),
+                   beta=torch.zeros(96))]
+        refs.append(weakref.ref(ly[0]["w_bits"]))
+        return dl.make_layers(ly)
+    arr = build()
+    gc.collect()
+    assert refs[0]() is not None and refs[0]().data_ptr() == arr[0].w_bits
+    del arr
+    gc.collect()
+    assert refs[0]() is None
 
 
 def test_embedding_validation(dl):
