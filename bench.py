@@ -319,7 +319,30 @@ def main():
                 t1.record(stream)
                 torch.cuda.synchronize()
                 us = t0.elapsed_time(t1) * 1e3 / (reps * ncall)
+                del g
+                # warm: the same number of calls, all on the first copy (its
+                # weights stay in the Infinity Cache and L2)
+
+                def calls_warm():
+                    for _ in cps:
+                        D.scaffold_lora_linear(qd, sd, base["w_bits"], base["alpha"], base["A"], base["B"],
+                                               base["beta"], y=yd, workspace=wsd)
+                with torch.cuda.stream(side):
+                    calls_warm()
+                    g = torch.cuda.CUDAGraph()
+                    with torch.cuda.graph(g, stream=side):
+                        calls_warm()
+                torch.cuda.synchronize()
+                g.replay()
+                torch.cuda.synchronize()
+                t0.record(stream)
+                for _ in range(reps):
+                    g.replay()
+                t1.record(stream)
+                torch.cuda.synchronize()
+                us_warm = t0.elapsed_time(t1) * 1e3 / (reps * ncall)
                 decode.append({"workload": f"{name} M={m}", "us_per_call": round(us, 2),
+                               "us_per_call_warm": round(us_warm, 2),
                                "weight_gbs": round(wb / (us * 1e-6) / 1e9, 1), "weight_bytes": wb,
                                "path": "few-token MFMA (one launch)", "lora": "int8"})
                 del g
@@ -512,6 +535,14 @@ def main():
                "sample": f"the full 96-linear sweep (weight copy 0, same input) run {reps} times in {dt:.1f} s",
                "us_per_layer": round(dt / reps / 48 * 1e6, 1), "host_cpu": host_cpu_model(),
                "host_cpus_visible": os.cpu_count()}
+        def timed(fn, seconds):
+            n, t0h = 0, time.perf_counter()
+            while True:
+                fn()
+                n += 1
+                el = time.perf_counter() - t0h
+                if el >= seconds:
+                    return el / n, n
         # the same oracle on one thread
         threads = o.threads()
         o.set_threads(1)
@@ -527,14 +558,29 @@ def main():
                                 "us_per_layer": round(dt1 / reps1 / 48 * 1e6, 1),
                                 "sample": f"the full 96-linear sweep run {reps1} times in {dt1:.1f} s on one thread"}
 
-        def timed(fn, seconds):
-            n, t0h = 0, time.perf_counter()
-            while True:
-                fn()
-                n += 1
-                el = time.perf_counter() - t0h
-                if el >= seconds:
-                    return el / n, n
+        # the single linears of the other workloads, on one thread and on all;
+        # the 2048-token prefill on a 64-token sample (rows are independent,
+        # so its time scales by 2048/64)
+        def one_cfg(cfg, m, sample_m, seconds):
+            hw = S.config_weights(cfg)
+            qc, sc = o.quantize_act(S.config_activations(cfg, sample_m))
+            out = {}
+            for label, nt in (("us_1_thread", 1), ("us_all_threads", threads)):
+                o.set_threads(nt)
+                per, n = timed(lambda: o.linear(qc, sc, **hw), seconds)
+                out[label] = round(per * 1e6 * m / sample_m, 1)
+            o.set_threads(threads)
+            return out
+        cfgs = []
+        for cfg, m, sm in ((0, 1, 1), (1, 1, 1), (2, 1, 1), (2, 4, 4), (2, 8, 8), (2, 16, 16), (2, 32, 32),
+                           (4, 2048, 64)):
+            e = {"config": f"c{cfg}", "M": m}
+            e.update(one_cfg(cfg, m, sm, 0.6))
+            if sm != m:
+                e["sample"] = f"{sm} of the {m} tokens, time scaled by {m // sm}"
+            cfgs.append(e)
+        cpu["linears"] = cfgs
+
         # the oracle beside the other measured kernels: the LM head at one
         # token on the 1.3B table, and one decode layer at batch 1
         Eh, sch = S.embedding(S.VOCAB_1P3B, S.D_MODEL_1P3B, key=(40,))
