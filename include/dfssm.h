@@ -424,7 +424,9 @@ typedef struct {
 dfssm_status dfssm_mamba2_state_bytes(const dfssm_mamba2_model* model, int64_t M, size_t* conv_ring_bytes,
                                       size_t* ssm_state_bytes);
 
-/* Bytes of device workspace dfssm_mamba2_decode_step needs for M tokens. */
+/* Bytes of device workspace dfssm_mamba2_decode_step needs for M tokens
+ * (at M = 1, for a model of the shape the fused step takes, this includes
+ * the fused step's region: about 39 MB for 48 layers). */
 size_t dfssm_mamba2_workspace_bytes(const dfssm_mamba2_model* model, int64_t M);
 
 /* One decode step of M sequences, all on `stream` (Sec. 4.1: the paper
@@ -452,10 +454,51 @@ size_t dfssm_mamba2_workspace_bytes(const dfssm_mamba2_model* model, int64_t M);
  * token ids and state.
  * Limits: d_model a multiple of 128 (<= 8192); d_state 64 or 128; every
  * layer's projections of those shapes; M >= 1; vocab >= 1.
+ * The fused step: at M = 1, on a workspace that dfssm_mamba2_prepare has
+ * prepared for this model, and for models of the 1.3B layer shape (d_model
+ * 2048, d_state 128, int8 LoRA factors with r <= 64 and r % 4 == 0 in
+ * every projection), the layers run as one persistent launch of one
+ * workgroup per compute unit (between the gather and the final norm and LM
+ * head), with the same arithmetic; every other case runs the per-kernel
+ * sequence above.  The fused launch needs the whole grid resident at once;
+ * its waits are bounded and record a status bit (dfssm_mamba2_status) if
+ * they give up, after which that step's outputs are incomplete.
  * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */
 dfssm_status dfssm_mamba2_decode_step(const dfssm_mamba2_model* model, int64_t M, const int32_t* tok,
                                       int64_t step, float* conv_ring, float* ssm_state, float* logits,
                                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* Prepares `workspace` for the fused step at M = 1 (see
+ * dfssm_mamba2_decode_step): writes the layer table and its fingerprint
+ * into the fused region and clears its exchange words, status and epochs
+ * (stream-ordered, asynchronous), and records on the host that this
+ * workspace holds this model's table.  Needed once per (model, workspace)
+ * before decode steps at M = 1 take the fused path.  Call
+ * dfssm_mamba2_release before freeing a prepared workspace: the record is
+ * kept by address, and a new workspace at the same address would otherwise
+ * be taken for a prepared one.  A no-op (DFSSM_OK) for M > 1 or models of
+ * another shape.
+ * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */
+dfssm_status dfssm_mamba2_prepare(const dfssm_mamba2_model* model, int64_t M, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
+/* Drops the host-side record that dfssm_mamba2_prepare made for
+ * `workspace` (host call, no device work; a no-op if there is none): the
+ * next step on it runs the per-kernel sequence until it is prepared again.
+ * Errors: none. */
+dfssm_status dfssm_mamba2_release(const void* workspace);
+
+/* Synchronises `stream` and reads the fused step's status word into
+ * *status (host): 0 = fine; bit 1 = a wait for a linear's input timed out;
+ * bit 2 = a wait for a row or rank partial timed out; bit 4 = a wait in the
+ * SSM stage (B/C, dt or the partners' progress) timed out; bit 8 = the
+ * fused region does not hold this model's table; bits 16..31 = 1 + the
+ * index of the first linear (2 per layer) at which a workgroup gave up.
+ * Bits accumulate until the next dfssm_mamba2_prepare.  0 when the fused
+ * step is not in use.
+ * Errors: NULL, SHAPE, ALIGN, WORKSPACE, DEVICE. */
+dfssm_status dfssm_mamba2_status(const dfssm_mamba2_model* model, int64_t M, const void* workspace,
+                                 size_t workspace_bytes, unsigned* status, void* stream);
 
 /* ---- test switches ------------------------------------------------------ */
 
@@ -472,11 +515,15 @@ dfssm_status dfssm_mamba2_decode_step(const dfssm_mamba2_model* model, int64_t M
  *                                  kernel on the prefill path
  *   DFSSM_TEST_LM_HEAD_MFMA_TOKENS n > 0: the LM head runs on the matrix
  *                                  cores from n tokens instead of 8
+ *   DFSSM_TEST_STEP_PER_KERNEL     1: the decode step at M = 1 runs the
+ *                                  per-kernel sequence on a prepared
+ *                                  workspace too
  * Errors: SHAPE for an unknown switch or value. */
 typedef enum {
   DFSSM_TEST_LOCAL_LORA = 1,
   DFSSM_TEST_PREFILL_KERNEL = 2,
-  DFSSM_TEST_LM_HEAD_MFMA_TOKENS = 3
+  DFSSM_TEST_LM_HEAD_MFMA_TOKENS = 3,
+  DFSSM_TEST_STEP_PER_KERNEL = 4
 } dfssm_test_switch_id;
 dfssm_status dfssm_test_switch(int which, int value);
 

@@ -9,6 +9,7 @@ package loads the in-tree library and fails loudly if it has not been built
 from __future__ import annotations
 
 import ctypes
+import weakref
 import os
 from typing import List, Optional, Sequence
 
@@ -26,10 +27,10 @@ EXPORTS = ["dfssm_quantize_act", "dfssm_linear_workspace_bytes", "dfssm_scaffold
            "dfssm_embed_gather", "dfssm_lm_head", "dfssm_add_rmsnorm_quant", "dfssm_gate_norm_quant",
            "dfssm_ssm_step", "dfssm_linear_i4_workspace_bytes", "dfssm_scaffold_lora_linear_i4",
            "dfssm_mamba2_state_bytes", "dfssm_mamba2_workspace_bytes",
-           "dfssm_mamba2_decode_step", "dfssm_scaffold_lora_linear_noalloc", "dfssm_noalloc_scratch_bytes",
+           "dfssm_mamba2_decode_step", "dfssm_mamba2_prepare", "dfssm_mamba2_release", "dfssm_mamba2_status", "dfssm_scaffold_lora_linear_noalloc", "dfssm_noalloc_scratch_bytes",
            "dfssm_test_switch", "dfssm_status_string", "dfssm_last_error",
            "dfssm_version"]
-TEST_LOCAL_LORA, TEST_PREFILL_KERNEL, TEST_LM_HEAD_MFMA_TOKENS = 1, 2, 3
+TEST_LOCAL_LORA, TEST_PREFILL_KERNEL, TEST_LM_HEAD_MFMA_TOKENS, TEST_STEP_PER_KERNEL = 1, 2, 3, 4
 
 
 class DfssmError(RuntimeError):
@@ -110,6 +111,12 @@ def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dfssm_mamba2_workspace_bytes.restype = sz
     lib.dfssm_mamba2_decode_step.argtypes = [mp, i64, vp, i64, vp, vp, vp, vp, sz, vp]
     lib.dfssm_mamba2_decode_step.restype = i32
+    lib.dfssm_mamba2_prepare.argtypes = [mp, i64, vp, sz, vp]
+    lib.dfssm_mamba2_prepare.restype = i32
+    lib.dfssm_mamba2_release.argtypes = [vp]
+    lib.dfssm_mamba2_release.restype = i32
+    lib.dfssm_mamba2_status.argtypes = [mp, i64, vp, sz, ctypes.POINTER(ctypes.c_uint), vp]
+    lib.dfssm_mamba2_status.restype = i32
     lib.dfssm_scaffold_lora_linear_noalloc.argtypes = [vp, vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp]
     lib.dfssm_scaffold_lora_linear_noalloc.restype = i32
     lib.dfssm_noalloc_scratch_bytes.argtypes = []
@@ -464,11 +471,31 @@ class Mamba2:
         return (torch.zeros(c // 4, dtype=torch.float32, device=device),
                 torch.zeros(s // 4, dtype=torch.float32, device=device))
 
-    def workspace(self, M: int, device="cuda"):
-        """A zero-filled workspace (zeros before its first use)."""
+    def workspace(self, M: int, device="cuda", prepare: bool = True, stream=None):
+        """A zero-filled workspace (zeros before its first use), prepared for
+        the fused step (dfssm_mamba2_prepare: at M = 1 for models of its
+        shape; a no-op otherwise) unless prepare is False."""
         torch = _torch()
-        return torch.zeros(int(lib.dfssm_mamba2_workspace_bytes(ctypes.byref(self.struct), M)), dtype=torch.uint8,
-                           device=device)
+        ws = torch.zeros(int(lib.dfssm_mamba2_workspace_bytes(ctypes.byref(self.struct), M)), dtype=torch.uint8,
+                         device=device)
+        if prepare:
+            self.prepare(M, ws, stream=stream)
+        return ws
+
+    def prepare(self, M: int, workspace, stream=None):
+        """dfssm_mamba2_prepare; the record is dropped again (dfssm_mamba2_release)
+        when the workspace tensor is freed, so a later tensor at the same
+        address is not taken for a prepared one."""
+        _check(lib.dfssm_mamba2_prepare(ctypes.byref(self.struct), M, workspace.data_ptr(), workspace.numel(),
+                                        _stream(stream)))
+        weakref.finalize(workspace, lib.dfssm_mamba2_release, ctypes.c_void_p(workspace.data_ptr()))
+
+    def status(self, M: int, workspace, stream=None) -> int:
+        """Synchronise and read the fused step's status word (0 = fine)."""
+        out = ctypes.c_uint(0)
+        _check(lib.dfssm_mamba2_status(ctypes.byref(self.struct), M, workspace.data_ptr(), workspace.numel(),
+                                       ctypes.byref(out), _stream(stream)))
+        return int(out.value)
 
     def decode_step(self, tok, step: int, conv_ring, ssm_state, workspace, logits=None, stream=None):
         """One token for each of the M sequences (tok int32 [M]); returns

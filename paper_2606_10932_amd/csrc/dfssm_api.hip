@@ -63,7 +63,7 @@ dfssm_status check_ptrs(std::initializer_list<Ptr> required, std::initializer_li
   return DFSSM_OK;
 }
 
-std::atomic<int> g_switch[4];  // dfssm_test_switch values, index = switch id
+std::atomic<int> g_switch[5];  // dfssm_test_switch values, index = switch id
 
 size_t linear_ws_bytes(int64_t M, int64_t K, int64_t r) {
   return dfssm::carve_linear_workspace(nullptr, M, K, r).bytes;
@@ -141,7 +141,7 @@ hipError_t launch_linear_i4(int path, const int8_t* q, const float* s, int64_t M
 }  // namespace
 
 namespace dfssm {
-int test_switch(int which) { return which > 0 && which < 4 ? g_switch[which].load(std::memory_order_relaxed) : 0; }
+int test_switch(int which) { return which > 0 && which < 5 ? g_switch[which].load(std::memory_order_relaxed) : 0; }
 }  // namespace dfssm
 
 extern "C" {
@@ -153,6 +153,7 @@ dfssm_status dfssm_test_switch(int which, int value) {
     case DFSSM_TEST_LOCAL_LORA: ok = value == 0 || value == 1; break;
     case DFSSM_TEST_PREFILL_KERNEL: ok = value == 0 || value == 4 || value == 8; break;
     case DFSSM_TEST_LM_HEAD_MFMA_TOKENS: ok = value >= 0; break;
+    case DFSSM_TEST_STEP_PER_KERNEL: ok = value == 0 || value == 1; break;
     default: break;
   }
   if (!ok) return fail(DFSSM_ERR_SHAPE, "test switch %d: value %d", which, value);
@@ -696,6 +697,8 @@ struct ModelWs {
   float *u, *delta, *zx, *y, *s;
   int8_t* q;
   char* lin;
+  char* fused;  // the fused step's region (M = 1, models of its shape), or null
+  dfssm::StepFusedInfo fi;
   size_t lin_bytes, bytes;
 };
 
@@ -722,7 +725,10 @@ ModelWs carve_model_ws(void* base, const dfssm_mamba2_model* md, const ModelDims
     }
   }
   const size_t o_lin = take(lin);
+  w.fi = M == 1 ? dfssm::step_fused_info(md) : dfssm::StepFusedInfo{};
+  const size_t o_fused = w.fi.ok ? take(w.fi.bytes) : 0;
   char* b = static_cast<char*>(base);
+  w.fused = w.fi.ok ? b + o_fused : nullptr;
   w.u = reinterpret_cast<float*>(b + o_u);
   w.delta = reinterpret_cast<float*>(b + o_d);
   w.zx = reinterpret_cast<float*>(b + o_zx);
@@ -733,6 +739,35 @@ ModelWs carve_model_ws(void* base, const dfssm_mamba2_model* md, const ModelDims
   w.lin_bytes = lin;
   w.bytes = off;
   return w;
+}
+
+// Workspaces whose fused-step region dfssm_mamba2_prepare wrote, with the
+// fingerprint of the table it wrote there.
+std::mutex g_prep_mu;
+std::vector<std::pair<const void*, uint64_t>> g_prepared;
+
+void note_prepared(const void* ws, uint64_t fp) {
+  std::lock_guard<std::mutex> lk(g_prep_mu);
+  for (auto& e : g_prepared)
+    if (e.first == ws) {
+      e.second = fp;
+      return;
+    }
+  g_prepared.emplace_back(ws, fp);
+}
+void forget_prepared(const void* ws) {
+  std::lock_guard<std::mutex> lk(g_prep_mu);
+  for (size_t i = 0; i < g_prepared.size(); ++i)
+    if (g_prepared[i].first == ws) {
+      g_prepared.erase(g_prepared.begin() + (std::ptrdiff_t)i);
+      return;
+    }
+}
+bool is_prepared(const void* ws, uint64_t fp) {
+  std::lock_guard<std::mutex> lk(g_prep_mu);
+  for (const auto& e : g_prepared)
+    if (e.first == ws) return e.second == fp;
+  return false;
 }
 
 }  // namespace
@@ -775,6 +810,19 @@ dfssm_status dfssm_mamba2_decode_step(const dfssm_mamba2_model* model, int64_t M
     return fail(DFSSM_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, w.bytes);
   hipStream_t hs = (hipStream_t)stream;
   const float eps = model->eps;
+  if (w.fused && dfssm::test_switch(DFSSM_TEST_STEP_PER_KERNEL) == 0 && is_prepared(workspace, w.fi.fingerprint)) {
+    // the fused step: gather, one persistent launch for all layers, final
+    // norm, LM head
+    float* u0 = reinterpret_cast<float*>(w.fused + w.fi.off_u0);
+    float* ufin = reinterpret_cast<float*>(w.fused + w.fi.off_ufin);
+    hipError_t e = dfssm::launch_embed_gather(model->E, model->E_scale, model->vocab, d.d_model, tok, 1, u0, hs);
+    if (e == hipSuccess) e = dfssm::step_fused_run(w.fi, eps, step, conv_ring, ssm_state, w.fused, hs);
+    if (e == hipSuccess)
+      e = dfssm::launch_add_rmsnorm_quant(ufin, nullptr, model->norm_f, eps, 1, d.d_model, nullptr, w.q, w.s, hs);
+    if (e == hipSuccess)
+      e = dfssm::launch_lm_head(w.q, w.s, 1, d.d_model, model->E, model->E_scale, model->vocab, logits, nullptr, hs);
+    return e == hipSuccess ? DFSSM_OK : device_fail(e, "decode step launch");
+  }
   const int64_t ring_stride = M * 4 * d.conv_dim, state_stride = M * d.H * 64 * d.N;
   hipError_t e = dfssm::launch_embed_gather(model->E, model->E_scale, model->vocab, d.d_model, tok, M, w.u, hs);
   for (int64_t l = 0; l < model->n_layers && e == hipSuccess; ++l) {
@@ -814,6 +862,51 @@ dfssm_status dfssm_mamba2_decode_step(const dfssm_mamba2_model* model, int64_t M
   if (e == hipSuccess)
     e = dfssm::launch_lm_head(w.q, w.s, M, d.d_model, model->E, model->E_scale, model->vocab, logits, nullptr, hs);
   return e == hipSuccess ? DFSSM_OK : device_fail(e, "decode step launch");
+}
+
+dfssm_status dfssm_mamba2_prepare(const dfssm_mamba2_model* model, int64_t M, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  clear_error();
+  ModelDims d;
+  dfssm_status st = check_model(model, M, &d);
+  if (st != DFSSM_OK) return st;
+  st = check_model_pointers(model, d);
+  if (st != DFSSM_OK) return st;
+  st = check_ptrs({{workspace, "workspace"}}, {});
+  if (st != DFSSM_OK) return st;
+  const ModelWs w = carve_model_ws(workspace, model, d, M);
+  if (workspace_bytes < w.bytes)
+    return fail(DFSSM_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, w.bytes);
+  if (!w.fused) return DFSSM_OK;
+  const hipError_t e = dfssm::step_fused_prepare(model, w.fused, (hipStream_t)stream);
+  if (e != hipSuccess) return device_fail(e, "decode step prepare launch");
+  note_prepared(workspace, w.fi.fingerprint);
+  return DFSSM_OK;
+}
+
+dfssm_status dfssm_mamba2_release(const void* workspace) {
+  clear_error();
+  if (workspace) forget_prepared(workspace);
+  return DFSSM_OK;
+}
+
+dfssm_status dfssm_mamba2_status(const dfssm_mamba2_model* model, int64_t M, const void* workspace,
+                                 size_t workspace_bytes, unsigned* status, void* stream) {
+  clear_error();
+  if (!status) return fail(DFSSM_ERR_NULL, "status is NULL");
+  *status = 0;
+  ModelDims d;
+  dfssm_status st = check_model(model, M, &d);
+  if (st != DFSSM_OK) return st;
+  st = check_ptrs({{workspace, "workspace"}}, {});
+  if (st != DFSSM_OK) return st;
+  const ModelWs w = carve_model_ws(const_cast<void*>(workspace), model, d, M);
+  if (workspace_bytes < w.bytes)
+    return fail(DFSSM_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, w.bytes);
+  if (!w.fused || !is_prepared(workspace, w.fi.fingerprint)) return DFSSM_OK;
+  hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+  if (e == hipSuccess) e = hipMemcpy(status, w.fused + w.fi.off_status, sizeof(unsigned), hipMemcpyDeviceToHost);
+  return e == hipSuccess ? DFSSM_OK : device_fail(e, "decode step status read");
 }
 
 }  // extern "C"

@@ -63,13 +63,12 @@
 #include <vector>
 
 #include "dfssm_internal.hpp"
+#include "dfssm_persist.hpp"
 
 namespace {
 
-constexpr int kGrid = 256;
-constexpr int kXcds = 8;
-constexpr int kPerXcd = kGrid / kXcds;       // 32 workgroups per XCD
-constexpr int kSlices = 8;                   // column slices per XCD
+using namespace dfssm_px;
+
 constexpr int kGroups = kPerXcd / kSlices;   // 4 row groups per XCD
 constexpr int kMaxR = 64;                    // ranks: 8 per XCD, 2 per row group
 constexpr int kWaves = 8;                    // 0 reducer, 1 codes + LoRA down, 6 loads
@@ -86,7 +85,6 @@ constexpr int kNB = 28;                      // direct-to-LDS loads per linear, 
 constexpr int kMaxKs = 512;                  // columns per slice (K <= 4096)
 constexpr int kMaxRed = 64;                  // rows per reducer
 constexpr int kSetupChunk = 32;              // table entries per setup launch
-constexpr long kSpinLimit = 1L << 20;
 static_assert(kGroups * 2 * kXcds == kMaxR, "two ranks per workgroup of a row group");
 
 // status bits
@@ -111,77 +109,6 @@ struct Layer {
   int64_t mx_off;          // words: [256] per-workgroup absmax of consumed outputs
 };
 
-// ------------------------------------------------------------ exchange words
-// agent scope: crosses XCDs (bypasses the non-coherent per-XCD L2s)
-__device__ __forceinline__ uint64_t ll_load(const uint64_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void ll_store(uint64_t* p, uint32_t tag, uint32_t v) {
-  __hip_atomic_store(p, ((uint64_t)tag << 32) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// inside one XCD: the store goes through (write-through L1) to the XCD's L2;
-// the load is a buffer load with sc0|nt, which skips the CU's L1 and is
-// served by that L2
-__device__ __forceinline__ void xcd_store(uint64_t* p, uint32_t tag, uint32_t v) {
-  __hip_atomic_store(p, ((uint64_t)tag << 32) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
-typedef unsigned v2u __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint64_t xcd_load(__amdgpu_buffer_rsrc_t rs, int64_t word) {
-  const v2u v = __builtin_amdgcn_raw_buffer_load_b64(rs, (int)(word * 8), 0, 3);
-  return ((uint64_t)v.y << 32) | v.x;
-}
-
-__device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
-  return __builtin_amdgcn_sdot4((int)a, (int)b, c, false);
-}
-
-// The quantiser's code of v for inv = 127/a, where |v| <= a: |v * inv| is
-// at most 127 * (1 + 2^-23)^2 < 127.5, so rint() already lands in [-127, 127]
-// and the clamp of the definition never changes the result.
-__device__ __forceinline__ int code(float v, float inv) { return (int)rintf(v * inv); }
-
-__device__ __forceinline__ int dpp_sum16(int v) {
-  v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
-  v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
-  v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);  // row_half_mirror
-  v += __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);  // row_mirror
-  return v;
-}
-// Sum over aligned groups of G lanes (G = 1, 2, 4 or 32), in every lane of
-// the group.  For 32: the 16-lane rows by DPP, then v_permlane16_swap of a
-// value with itself leaves rows (0,0,2,2) in one result and (1,1,3,3) in the
-// other, so their sum is the 32-lane half's total.
-__device__ __forceinline__ int group_sum(int v, int G) {
-  if (G >= 2) v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
-  if (G >= 4) v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
-  if (G >= 32) {
-    v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);
-    v += __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);
-    const auto p = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v, false, false);
-    v = (int)(p[0] + p[1]);
-  }
-  return v;
-}
-// Whole-wave reductions with the result as a uniform value: DPP inside each
-// 16-lane row, then row_bcast:15 and row_bcast:31, which leave the total in
-// lane 63.
-__device__ __forceinline__ int wave_sum_u(int v) {
-  v = dpp_sum16(v);
-  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);
-  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);
-  return __builtin_amdgcn_readlane(v, 63);
-}
-// max of non-negative floats, compared as their bit patterns
-__device__ __forceinline__ uint32_t wave_max_bits_u(uint32_t v) {
-  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));
-  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
-  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));
-  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false));
-  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false));
-  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false));
-  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
-}
-
 // ------------------------------------------------------------ row ownership
 // First tail row of global reducer g (= 32 x + lam).
 __device__ __forceinline__ int tail_start(const Layer& L, int g) {
@@ -204,44 +131,6 @@ __device__ __forceinline__ int reducer_rows(const Layer& L, int x, int lam) {
   const int g = kPerXcd * x + lam;
   return L.cpr + L.tq + (g < L.trem ? 1 : 0);
 }
-
-// ------------------------------------------------------------ direct-to-LDS
-// Lane i's 16 (or 4) bytes from sbase + voff land at m0 + 16*i (4*i).
-// Inline assembly, so the compiler does not make later LDS reads wait for
-// them; the loading wave orders them with an explicit vector-memory wait
-// before the barrier that hands the slot over.
-__device__ __forceinline__ void lds_dma16(uint32_t voff, const void* sbase, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(lds)
-               : "memory", "m0");
-}
-__device__ __forceinline__ void lds_dma4(uint32_t voff, const void* sbase, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1" ::"v"(voff), "s"(sbase), "s"(lds)
-               : "memory", "m0");
-}
-__device__ __forceinline__ void lds_dma(int unit, uint32_t voff, const void* sbase, uint32_t lds) {
-  if (unit == 16)
-    lds_dma16(voff, sbase, lds);
-  else
-    lds_dma4(voff, sbase, lds);
-}
-// s_waitcnt with only the vector-memory counter constrained
-#define CHAIN_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(0x0F70 | ((n) & 0xF) | (((n) >> 4) << 14))
-// Workgroup barrier for LDS data only: the wave's LDS operations complete
-// first, its vector-memory operations do not have to (the loading wave's
-// direct-to-LDS loads of the next linears stay in flight; no global data
-// crosses a barrier inside a workgroup, every exchange goes through polled
-// tagged words)
-#define CHAIN_BARRIER() asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory")
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
-
-// floor(u / d) for u < 2^11 and d <= 64 without a division: u * ceil(2^20 / d)
-// >> 20 (the error term u * (ceil(2^20/d) * d - 2^20) / 2^20 < u * 64 / 2^20
-// stays below 1/d, so the floor is exact); m = ceil(2^20 / d) is uniform.
-__device__ __forceinline__ uint32_t recip20(uint32_t d) { return ((1u << 20) + d - 1) / d; }
-__device__ __forceinline__ int udiv(int u, uint32_t m) { return (int)(((uint32_t)u * m) >> 20); }
 
 // The loading wave's batch for one linear: this workgroup's sign rows, its
 // rh A rows' slice, its reducer rows' B rows, alpha and beta, into the slot
@@ -304,26 +193,6 @@ __device__ int issue_batch(const Layer& L, int x, int kap, int h, int lam, uint3
   return n_issued;
 }
 
-// Workgroup flags in LDS, read and written as LDS operations: a volatile
-// access through a generic pointer would be a flat access (clang leaves
-// volatile accesses in the generic address space), which also counts as a
-// vector-memory operation and makes every check wait for the wave's
-// outstanding global stores.
-typedef __attribute__((address_space(3))) volatile int lds_flag;
-#define FLAG(v) (*(lds_flag*)(&(v)))
-
-// Bounded spin helpers: a wait gives up after kSpinLimit rounds or once
-// another wave of the workgroup has aborted (abort_flag in LDS).
-#define CHAIN_SPIN_OR_ABORT(spins, abort_flag, status, bit, on_abort) \
-  do {                                                                 \
-    if (++(spins) > kSpinLimit || FLAG(abort_flag)) {                  \
-      atomicOr((status), (bit));                                       \
-      FLAG(abort_flag) = 1;                                            \
-      on_abort;                                                        \
-    }                                                                  \
-    __builtin_amdgcn_s_sleep(1);                                       \
-  } while (0)
-
 __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
     const Layer* __restrict__ layers, int L, const int8_t* __restrict__ q0, const float* __restrict__ s0,
     uint64_t* __restrict__ ex, int64_t ex_words, unsigned* status, uint64_t* epoch, float* __restrict__ y_all,
@@ -349,7 +218,7 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
   __shared__ int abort_, rows_done, limbs_ready, pub_done;
 
   const int wg = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int x = (int)(__builtin_amdgcn_s_getreg((20) | (0 << 6) | ((4 - 1) << 11)) & 7u);  // HW_REG_XCC_ID[3:0]
+  const int x = xcc_id();
   const int lam = wg / kXcds, kap = lam % kSlices, h = lam / kSlices;
 
   if (tid == 0) {
@@ -374,7 +243,7 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
   if (FLAG(abort_)) return;
   const uint32_t seq = seq_s;
   auto tag_of = [seq](int l) -> uint32_t { return (seq << 8) | (uint32_t)((l + 1) & 0xff); };
-  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(ex, 0, (int)(ex_words * 8), 0x00020000);
+  (void)ex_words;
 
   for (int l = 0; l < L; ++l) {
     const int lu = __builtin_amdgcn_readfirstlane(l);
@@ -390,7 +259,8 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
     //      only load the fabric the reducers' own exchange uses.
     if (l > 0 && wave >= 1 && wave != 6) {
       long sp = 0;
-      while (FLAG(pub_done) < l) CHAIN_SPIN_OR_ABORT(sp, abort_, status, kStY, break);
+      while (FLAG(pub_done) < l)
+        if (spin_gives_up(sp, &abort_, status, kStY)) break;
       const Layer Lp = layers[lu - 1];
       const uint32_t tp = tag_of(l - 1);
       const int ct = (wave == 7 ? 5 : wave - 1) * 64 + lane;
@@ -416,7 +286,7 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
           m = (uint32_t)w2;
           pend &= ~4u;
         }
-        if (pend) CHAIN_SPIN_OR_ABORT(sp, abort_, status, kStY, break);
+        if (pend && spin_gives_up(sp, &abort_, status, kStY)) break;
       }
       m = wave_max_bits_u(m);
       if (lane == 0)
@@ -524,7 +394,7 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
         }
         d = group_sum(d, G);
         if (i < nA && g == 0)
-          xcd_store(ex + Ld.part_off + (int64_t)kap * Ld.N + group_row(Ld, x, h, i), tg,
+          ll_store(ex + Ld.part_off + (int64_t)kap * Ld.N + group_row(Ld, x, h, i), tg,
                     (uint32_t)(2 * d - sq));
       }
       // (the count only tells the reducer when to start polling; what it
@@ -564,7 +434,7 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
         v = group_sum(v, 4);
         const int j = h * rh + jj;
         if (part == 0 && jj < rh && j < r)
-          xcd_store(ex + Ld.p_off + (int64_t)(x * kSlices + kap) * kMaxR + j, tg, (uint32_t)v);
+          ll_store(ex + Ld.p_off + (int64_t)(x * kSlices + kap) * kMaxR + j, tg, (uint32_t)v);
       }
       int acc_a = 0;
       if (r > 0) {
@@ -574,14 +444,14 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
           uint64_t wa[kSlices];
 #pragma unroll
           for (int k = 0; k < kSlices; ++k)
-            wa[k] = (pend & (1u << k)) ? xcd_load(rs, Ld.p_off + (int64_t)(x * kSlices + k) * kMaxR + lane) : 0;
+            wa[k] = (pend & (1u << k)) ? ll_load(ex + Ld.p_off + (int64_t)(x * kSlices + k) * kMaxR + lane) : 0;
 #pragma unroll
           for (int k = 0; k < kSlices; ++k)
             if ((pend & (1u << k)) && (uint32_t)(wa[k] >> 32) == tg) {
               acc_a += (int32_t)(uint32_t)wa[k];
               pend &= ~(1u << k);
             }
-          if (pend) CHAIN_SPIN_OR_ABORT(sp, abort_, status, kStAcc, break);
+          if (pend && spin_gives_up(sp, &abort_, status, kStAcc)) break;
         }
       }
       int8_t dl[4];
@@ -597,7 +467,8 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
       //      partials of the other workgroups of the XCD come at about the
       //      same time)
       long sp = 0;
-      while (FLAG(rows_done) < kAWaves * (l + 1)) CHAIN_SPIN_OR_ABORT(sp, abort_, status, kStAcc, break);
+      while (FLAG(rows_done) < kAWaves * (l + 1))
+        if (spin_gives_up(sp, &abort_, status, kStAcc)) break;
       const int R = reducer_rows(Ld, x, lam);
       // the row's operands (LDS reads issued together, before the poll)
       const int rw = r >> 2;
@@ -614,16 +485,17 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
         uint64_t wp[kSlices];
 #pragma unroll
         for (int k = 0; k < kSlices; ++k)
-          wp[k] = (pend & (1u << k)) ? xcd_load(rs, Ld.part_off + (int64_t)k * Ld.N + n) : 0;
+          wp[k] = (pend & (1u << k)) ? ll_load(ex + Ld.part_off + (int64_t)k * Ld.N + n) : 0;
 #pragma unroll
         for (int k = 0; k < kSlices; ++k)
           if ((pend & (1u << k)) && (uint32_t)(wp[k] >> 32) == tg) {
             acc_s += (int32_t)(uint32_t)wp[k];
             pend &= ~(1u << k);
           }
-        if (pend) CHAIN_SPIN_OR_ABORT(sp, abort_, status, kStAcc, break);
+        if (pend && spin_gives_up(sp, &abort_, status, kStAcc)) break;
       }
-      while (FLAG(limbs_ready) < l + 1) CHAIN_SPIN_OR_ABORT(sp, abort_, status, kStAcc, break);
+      while (FLAG(limbs_ready) < l + 1)
+        if (spin_gives_up(sp, &abort_, status, kStAcc)) break;
       if (!FLAG(abort_)) {
         uint4 lw[kMaxR / 4];
 #pragma unroll
@@ -699,7 +571,7 @@ __global__ __launch_bounds__(64, 1) void chain_stream(const Layer* __restrict__ 
   }
   __shared__ __attribute__((aligned(16))) uint8_t ring[kRing][kSlotBytes];
   const int wg = blockIdx.x, lane = threadIdx.x;
-  const int x = (int)(__builtin_amdgcn_s_getreg((20) | (0 << 6) | ((4 - 1) << 11)) & 7u);  // HW_REG_XCC_ID[3:0]
+  const int x = xcc_id();
   const int lam = wg / kXcds, kap = lam % kSlices, h = lam / kSlices;
   const uint32_t sb0 = lds_addr(&ring[0][0]);
   // n1, n2: load instructions of the batches after the one landing

@@ -182,6 +182,23 @@ hipError_t chain_persistent_run(const dfssm_layer* layers, int n_layers, const i
 // arithmetic, no exchange, nothing written outside LDS).
 hipError_t chain_stream_run(const dfssm_layer* layers, int n_layers, void* ws, hipStream_t st);
 // Zeroes `words` 64-bit words at p with a fill kernel (capture-safe).
+// The fused decode step at one token (dfssm_step.hip).  Its workspace region
+// (bytes; 0 when the model is not the shape it takes) holds its table, the
+// table's fingerprint, the exchange words, a status word, the epoch words,
+// the gathered embedding row u0 and the final residual row u_fin (offsets
+// relative to the region).
+struct StepFusedInfo {
+  bool ok;
+  size_t bytes, off_hash, off_ex, off_status, off_epoch, off_u0, off_ufin;
+  int64_t ex_words;
+  int n_linears;
+  uint64_t fingerprint;
+};
+StepFusedInfo step_fused_info(const dfssm_mamba2_model* md);
+hipError_t step_fused_prepare(const dfssm_mamba2_model* md, void* ws, hipStream_t st);
+hipError_t step_fused_run(const StepFusedInfo& f, float eps, int64_t step, float* conv_ring, float* ssm_state,
+                          void* ws, hipStream_t st);
+
 hipError_t launch_zero_words(uint64_t* p, int64_t words, hipStream_t st);
 
 }  // namespace dfssm

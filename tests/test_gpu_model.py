@@ -232,5 +232,6 @@ def test_decode_step_full_model(env, model_host_full, M, record_property):
         lg = host(m.decode_step(dev(tok), t, ring, state, ws))
         torch.cuda.synchronize()
         exact += _logits_check(lg, om.step(tok), f"token {t}")
-    say(f"  {exact} of {T} tokens bit-exact against the oracle")
+    assert m.status(M, ws) == 0
+    say(f"  {exact} of {T} tokens bit-exact against the oracle" + (" (the fused step)" if M == 1 else ""))
     record_property("bit_exact_tokens", f"{exact}/{T}")

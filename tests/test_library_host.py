@@ -240,6 +240,25 @@ def test_model_step_validation(dl):
     w4 = dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1024)
     assert w4 >= w8 + 64 * 4096 + 2048 * 64     # out_proj: the larger linear workspace
     assert dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1) > 0
+    # the fused step's region: at M = 1 only, for the 1.3B layer shape with
+    # int8 factors (these layers have int4 ones now: none)
+    lay[0].lora_bits = lay[1].lora_bits = 8
+    w1 = dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1)
+    lay[0].lora_bits = lay[1].lora_bits = 4
+    assert w1 > dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1) + 800 * 1024   # 2 layers: ~0.9 MB
+    lay[0].lora_bits = lay[1].lora_bits = 8
+    # prepare / release / status validate on the host
+    prep, stat = dl.lib.dfssm_mamba2_prepare, dl.lib.dfssm_mamba2_status
+    assert prep(None, 1, 16, 1 << 40, None) == dl.ERR_NULL
+    assert prep(ctypes.byref(model(d_state=96)), 1, 16, 1 << 40, None) == dl.ERR_UNSUPPORTED
+    assert prep(ctypes.byref(m), 1, None, 1 << 40, None) == dl.ERR_NULL
+    assert prep(ctypes.byref(m), 1, 16, 64, None) == dl.ERR_WORKSPACE
+    assert dl.lib.dfssm_mamba2_release(None) == dl.OK and dl.lib.dfssm_mamba2_release(16) == dl.OK
+    st = ctypes.c_uint(7)
+    assert stat(ctypes.byref(m), 1, 16, 1 << 40, None, None) == dl.ERR_NULL
+    assert stat(ctypes.byref(m), 1, 16, 64, ctypes.byref(st), None) == dl.ERR_WORKSPACE
+    # an unprepared workspace: no device read, status 0
+    assert stat(ctypes.byref(m), 1, 16, 1 << 40, ctypes.byref(st), None) == dl.OK and st.value == 0
 
 
 def test_int4_linear_validation(dl):
