@@ -66,12 +66,12 @@ constexpr int kMaxR = 64;
 constexpr int kRankGroups = 4;
 constexpr int kMaxRh = kMaxR / kRankGroups;
 constexpr int kPollLanes = 6 * 64;  // waves 1..5 and 7
+constexpr int kBcLane = 48;         // reducer lanes 48 .. 55: the B/C copies
 constexpr int kSlotBytes = 40 * 1024;
 constexpr int kRing = 3;
 constexpr int kMaxKs = kDi / kSlices;  // 512
 constexpr int kSetupChunk = 16;
 constexpr int kGroups = kPerXcd / kSlices;  // 4 row groups per XCD
-constexpr int kRingFloats = kCpw + 2 * kDs;  // one ring slot's channels in LDS: x then B/C
 
 // status bits
 constexpr unsigned kStIn = 1u, kStAcc = 2u, kStSsm = 4u, kStHash = 8u;
@@ -95,15 +95,16 @@ struct StepLin {
   int32_t rs;      // row slots per reducer
   int32_t us, ub;  // direct-to-LDS units (bytes) of the sign rows and B rows
   int32_t o_a, o_b, o_al, o_be, o_nw;    // slot offsets
-  int32_t o_st, o_rg, o_cw, o_cb, o_hp;  // in_proj: SSM state, ring window, conv_w, conv_b, head parameters
-  int32_t layer, pad;
+  int32_t o_st, o_rg, o_rb, o_cw, o_cb, o_hp;  // in_proj: SSM state, convolution windows (x channels, own
+                                              // B/C channel), conv_w, conv_b, head parameters
+  int32_t layer;
   int64_t part_off;  // XCD-local words [8 slices][N]: row partials
   int64_t p_off;     // XCD-local words [8 XCDs][8 slices][64]: rank partials
   int64_t mx_off;    // XCD-local words [8 XCDs][4 row groups][8 slices]: slice maxima
   int64_t in_off;    // agent words [K]: this linear's input values
-  int64_t ss_off;    // agent words [256][2]: their partial sums of squares (fp64)
-  int64_t bc_off;    // in_proj: agent words [2 d_state]: the B/C rows
-  int64_t dt_off;    // in_proj: agent words [heads]: the dt rows
+  int64_t ss_off;    // agent words [8 XCDs][256][2]: their partial sums of squares (fp64)
+  int64_t bc_off;    // in_proj: agent words [8 XCDs][2 d_state]: the B/C rows after the convolution
+  int64_t dt_off;    // in_proj: agent words [heads][2]: dt and dA of each head
 };
 
 // ---------------------------------------------------------------- helpers
@@ -115,6 +116,7 @@ __device__ __forceinline__ float softplus_f(float v) {
   if (v > 20.0f) return v;
   return (float)log1p(exp((double)v));
 }
+// An fp64 value as two words (high half, low half), each with the tag.
 __device__ __forceinline__ void ll_store64(uint64_t* p, uint32_t tag, double v) {
   const uint64_t b = (uint64_t)__double_as_longlong(v);
   ll_store(p, tag, (uint32_t)(b >> 32));
@@ -211,46 +213,33 @@ __device__ void step_batch(const StepLin& L, int x, int kap, int h, int lam, int
     for (int tt = 0; tt < kCpw * kDs * 4 / 1024; ++tt)
       lds_dma16((uint32_t)(g * kCpw * kDs * 4 + 1024 * tt + 16 * lane), state_l,
                 sb + (uint32_t)(L.o_st + 1024 * tt));
-    // convolution window: for k = 1..3 the ring slot of step t - k, its x
-    // channels (16 floats) then the B/C channels (256 floats)
+    // convolution window: for k = 1..3 the ring slot of step t - k: the 16 x
+    // channels ([3][16] floats), and the own B/C channel (lane k - 1)
     {
-      constexpr int upk = kRingFloats / 4, nunits = 3 * upk, ni = (nunits + 63) / 64;
-      const uint32_t m = recip20((uint32_t)upk);
-      for (int tt = 0; tt < ni; ++tt) {
-        const int u = 64 * tt + lane;
-        uint32_t voff = 0;
-        if (u < nunits) {
-          const int kk = udiv(u, m), q = u - kk * upk;
-          const int slot = (t - 1 - kk) & 3;
-          const int ch = q < kCpw / 4 ? kCpw * g + 4 * q : kDi + 4 * (q - kCpw / 4);
-          voff = (uint32_t)((slot * kConv + ch) * 4);
-        }
-        lds_dma16(voff, ring_l, sb + (uint32_t)(L.o_rg + 1024 * tt));
-      }
+      uint32_t voff = 0;
+      if (lane < 12) voff = (uint32_t)(((((t - 1 - (lane >> 2)) & 3) * kConv) + kCpw * g + 4 * (lane & 3)) * 4);
+      lds_dma16(voff, ring_l, sb + (uint32_t)L.o_rg);
+      const int kk = lane < 3 ? lane : 0;
+      lds_dma4((uint32_t)((((t - 1 - kk) & 3) * kConv + kDi + g) * 4), ring_l, sb + (uint32_t)L.o_rb);
     }
-    {  // convolution weights [channel][4]: x channels, then B/C channels
-      constexpr int nunits = kCpw + 2 * kDs, ni = (nunits + 63) / 64;
-      for (int tt = 0; tt < ni; ++tt) {
-        const int u = 64 * tt + lane;
-        uint32_t voff = 0;
-        if (u < nunits) voff = (uint32_t)((u < kCpw ? kCpw * g + u : kDi + (u - kCpw)) * 16);
-        lds_dma16(voff, L.conv_w, sb + (uint32_t)(L.o_cw + 1024 * tt));
-      }
+    {  // convolution weights [channel][4]: the x channels, then the own B/C channel
+      uint32_t voff = 0;
+      if (lane < kCpw) voff = (uint32_t)((kCpw * g + lane) * 16);
+      if (lane == kCpw) voff = (uint32_t)((kDi + g) * 16);
+      lds_dma16(voff, L.conv_w, sb + (uint32_t)L.o_cw);
     }
-    {  // convolution biases: x channels, then B/C channels
-      constexpr int nunits = (kCpw + 2 * kDs) / 4, ni = (nunits + 63) / 64;
-      for (int tt = 0; tt < ni; ++tt) {
-        const int u = 64 * tt + lane;
-        uint32_t voff = 0;
-        if (u < nunits) voff = (uint32_t)((u < kCpw / 4 ? kCpw * g + 4 * u : kDi + 4 * (u - kCpw / 4)) * 4);
-        lds_dma16(voff, L.conv_b, sb + (uint32_t)(L.o_cb + 1024 * tt));
-      }
+    {  // convolution biases: the x channels, then the own B/C channel
+      uint32_t voff = 0;
+      if (lane < kCpw) voff = (uint32_t)((kCpw * g + lane) * 4);
+      if (lane == kCpw) voff = (uint32_t)((kDi + g) * 4);
+      lds_dma4(voff, L.conv_b, sb + (uint32_t)L.o_cb);
     }
-    {  // the head's dt bias, A_log and D (every lane loads the same word)
-      const uint32_t voff = (uint32_t)((kCpw * g / 64) * 4);
-      lds_dma4(voff, L.dt_bias, sb + (uint32_t)L.o_hp);
-      lds_dma4(voff, L.A_log, sb + (uint32_t)(L.o_hp + 256));
-      lds_dma4(voff, L.Dp, sb + (uint32_t)(L.o_hp + 512));
+    {  // D of this workgroup's head (its channels lie in head 16g / 64); dt
+       // bias and A_log of head g (the dt row this workgroup produces, g < heads)
+      const int hd = g < kNh ? g : kNh - 1;
+      lds_dma4((uint32_t)((kCpw * g / 64) * 4), L.Dp, sb + (uint32_t)L.o_hp);
+      lds_dma4((uint32_t)(hd * 4), L.dt_bias, sb + (uint32_t)(L.o_hp + 256));
+      lds_dma4((uint32_t)(hd * 4), L.A_log, sb + (uint32_t)(L.o_hp + 512));
     }
   }
 }
@@ -349,53 +338,44 @@ __global__ __launch_bounds__(kThreads, 1) void step_persistent(
         const StepLin Lp = lins[ju - 1];
         const uint8_t* ps = ring[(ju - 1) % kRing];
         const uint32_t tp = tag_of(ju - 1);
-        const float* rgw = reinterpret_cast<const float*>(ps + Lp.o_rg);  // [3][x 16 | B/C 256]
-        const float* cw = reinterpret_cast<const float*>(ps + Lp.o_cw);   // [x 16 | B/C 256][4]
-        const float* cb = reinterpret_cast<const float*>(ps + Lp.o_cb);   // [x 16 | B/C 256]
-        int ch = -1;      // window column of this lane's channel
-        float nv = 0.0f;  // its new input
+        const float* rgw = reinterpret_cast<const float*>(ps + Lp.o_rg);  // [3][x 16]: steps t-1, t-2, t-3
+        const float4* cw = reinterpret_cast<const float4*>(ps + Lp.o_cw);  // [x 16 | own B/C]
+        const float* cb = reinterpret_cast<const float*>(ps + Lp.o_cb);    // [x 16 | own B/C]
         if (ct < 2 * kDs) {
+          // B and C after the convolution, from the workgroup that owns the row
           uint64_t w = 0;
           while (!FLAG(abort_)) {
-            w = ll_load(ex + Lp.bc_off + ct);
+            w = ll_load(ex + Lp.bc_off + x * 2 * kDs + ct);
             if ((uint32_t)(w >> 32) == tp) break;
             if (spin_gives_up(sp, &abort_, status, kStSsm)) break;
           }
-          nv = __uint_as_float((uint32_t)w);
-          ch = kCpw + ct;
+          bcc[ct] = __uint_as_float((uint32_t)w);
         } else if (ct < 2 * kDs + kCpw) {
-          nv = zx_s[kCpw + (ct - 2 * kDs)];
-          ch = ct - 2 * kDs;
+          // the convolution of this workgroup's x channel p
+          const int p = ct - 2 * kDs;
+          const float4 wv = cw[p];
+          float v = wv.x * rgw[2 * kCpw + p];
+          v = v + wv.y * rgw[kCpw + p];
+          v = v + wv.z * rgw[p];
+          v = v + wv.w * zx_s[kCpw + p];
+          v = v + cb[p];
+          xc[p] = silu_f(v);
         } else if (ct < 2 * kDs + 2 * kCpw) {
           const int p = ct - 2 * kDs - kCpw;
           szv[p] = silu_f(zx_s[p]);
         } else if (ct == 2 * kDs + 2 * kCpw) {
-          uint64_t w = 0;
+          // dt and dA of the head, from the workgroup that owns its dt row
+          const int hw = kCpw * g / 64;
+          uint64_t w0 = 0, w1 = 0;
           while (!FLAG(abort_)) {
-            w = ll_load(ex + Lp.dt_off + (kCpw * g / 64));
-            if ((uint32_t)(w >> 32) == tp) break;
+            w0 = ll_load(ex + Lp.dt_off + 2 * hw);
+            w1 = ll_load(ex + Lp.dt_off + 2 * hw + 1);
+            if ((uint32_t)(w0 >> 32) == tp && (uint32_t)(w1 >> 32) == tp) break;
             if (spin_gives_up(sp, &abort_, status, kStSsm)) break;
           }
-          const float* hp = reinterpret_cast<const float*>(ps + Lp.o_hp);
-          const float dt = softplus_f(__uint_as_float((uint32_t)w) + hp[0]);
-          const float A = (float)(-exp((double)hp[64]));
-          dts[0] = dt;
-          dts[1] = (float)exp((double)(dt * A));
-          dts[2] = hp[128];
-        }
-        if (ch >= 0) {
-          // window: slot of step t-3, t-2, t-1 at rgw[(k-1) * 272 + ch], k = 3, 2, 1
-          const float4 wv = reinterpret_cast<const float4*>(cw)[ch];
-          float v = wv.x * rgw[2 * kRingFloats + ch];
-          v = v + wv.y * rgw[kRingFloats + ch];
-          v = v + wv.z * rgw[ch];
-          v = v + wv.w * nv;
-          v = v + cb[ch];
-          const float c = silu_f(v);
-          if (ch >= kCpw)
-            bcc[ch - kCpw] = c;
-          else
-            xc[ch] = c;
+          dts[0] = __uint_as_float((uint32_t)w0);
+          dts[1] = __uint_as_float((uint32_t)w1);
+          dts[2] = reinterpret_cast<const float*>(ps + Lp.o_hp)[0];
         }
         // the six waves meet (an LDS counter: waves 0 and 6 are elsewhere)
         __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's LDS writes are done
@@ -420,9 +400,6 @@ __global__ __launch_bounds__(kThreads, 1) void step_persistent(
           // the same sum)
 #pragma unroll
           for (int off = 8; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 16);
-          float4* dst = reinterpret_cast<float4*>(ssm_state + l * state_stride + (int64_t)(kCpw * g + p) * kDs + n0);
-          dst[0] = make_float4(hs[0], hs[1], hs[2], hs[3]);
-          dst[1] = make_float4(hs[4], hs[5], hs[6], hs[7]);
           if (sub == 0) {
             const float y = (float)(acc + (double)dts[2] * (double)xv);
             const float gval = y * szv[p];
@@ -432,13 +409,19 @@ __global__ __launch_bounds__(kThreads, 1) void step_persistent(
           __builtin_amdgcn_s_waitcnt(0xC07F);
           if (lane == 0) __hip_atomic_fetch_add(&g_cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
           if (wave == 1) {
+            // the sum of squares of the 16 gated outputs, one copy per XCD
             STEP_WAIT_FLAG(FLAG(g_cnt) >= 4 * (l + 1), sp, kStSsm);
-            if (lane == 0 && !FLAG(abort_)) {
+            if (lane < kXcds && !FLAG(abort_)) {
               double s2 = 0.0;
               for (int q = 0; q < kCpw; ++q) s2 += (double)gv[q] * (double)gv[q];
-              ll_store64(ex + Ld.ss_off + 2 * g, tg, s2);
+              ll_store64(ex + Ld.ss_off + 2 * (lane * kGrid + g), tg, s2);
             }
           }
+          // the new state last: a wave's stores complete in order, and the
+          // words above are what every other workgroup is waiting for
+          float4* dst = reinterpret_cast<float4*>(ssm_state + l * state_stride + (int64_t)(kCpw * g + p) * kDs + n0);
+          dst[0] = make_float4(hs[0], hs[1], hs[2], hs[3]);
+          dst[1] = make_float4(hs[4], hs[5], hs[6], hs[7]);
         }
       }
       // ---- phase D: this slice of the input and the 256 partial sums of
@@ -456,16 +439,21 @@ __global__ __launch_bounds__(kThreads, 1) void step_persistent(
           ssp[ct] = s2;
         }
       } else {
+        // out_proj: polls start once this workgroup's own gated outputs are
+        // out (the others come at about the same time; earlier polls only
+        // load the fabric)
+        if (!is_in) STEP_WAIT_FLAG(FLAG(g_cnt) >= 4 * (l + 1), sp, kStSsm);
         uint32_t pend = (i0 < Ks ? 1u : 0u) | (i1 < Ks ? 2u : 0u) | (ct < kGrid ? 12u : 0u);
         if (FLAG(abort_)) pend = 0;
         const uint64_t* iw = ex + Ld.in_off + (int64_t)kap * Ks;
+        const uint64_t* ssw = ex + Ld.ss_off + 2 * x * kGrid;  // this XCD's copy
         uint32_t shi = 0, slo = 0;
         while (pend) {
           uint64_t w0 = 0, w1 = 0, w2 = 0, w3 = 0;
           if (pend & 1u) w0 = ll_load(iw + i0);
           if (pend & 2u) w1 = ll_load(iw + i1);
-          if (pend & 4u) w2 = ll_load(ex + Ld.ss_off + 2 * ct);
-          if (pend & 8u) w3 = ll_load(ex + Ld.ss_off + 2 * ct + 1);
+          if (pend & 4u) w2 = ll_load(ssw + 2 * ct);
+          if (pend & 8u) w3 = ll_load(ssw + 2 * ct + 1);
           if ((pend & 1u) && (uint32_t)(w0 >> 32) == tg) {
             ys[i0] = __uint_as_float((uint32_t)w0);
             pend &= ~1u;
@@ -714,13 +702,30 @@ __global__ __launch_bounds__(kThreads, 1) void step_persistent(
           // z and x stay here; the B/C and dt rows go out as words; x and
           // B/C inputs enter the convolution window (ring slot t & 3)
           float* ring_t = conv_ring + l * ring_stride + (t & 3) * kConv;
+          const float ybc = __shfl(y, 2 * kCpw, 64);
           if (lane < 2 * kCpw) zx_s[lane] = y;
           if (lane >= kCpw && lane < 2 * kCpw) ring_t[kCpw * g + (lane - kCpw)] = y;
-          if (lane == 2 * kCpw) {
-            ll_store(ex + Ld.bc_off + g, tg, __float_as_uint(y));
-            ring_t[kDi + g] = y;
+          if (lane == 2 * kCpw) ring_t[kDi + g] = y;
+          if (lane >= kBcLane && lane < kBcLane + kXcds) {
+            // B/C row g after its convolution (window of steps t-3 .. t-1
+            // and y), one copy per XCD: every workgroup reads all 256
+            const float* rb = reinterpret_cast<const float*>(slot + Ld.o_rb);
+            const float4 wv = reinterpret_cast<const float4*>(slot + Ld.o_cw)[kCpw];
+            float v = wv.x * rb[2];
+            v = v + wv.y * rb[1];
+            v = v + wv.z * rb[0];
+            v = v + wv.w * ybc;
+            v = v + reinterpret_cast<const float*>(slot + Ld.o_cb)[kCpw];
+            ll_store(ex + Ld.bc_off + (lane - kBcLane) * 2 * kDs + g, tg, __float_as_uint(silu_f(v)));
           }
-          if (lane == 2 * kCpw + 1 && g < kNh) ll_store(ex + Ld.dt_off + g, tg, __float_as_uint(y));
+          if (lane == 2 * kCpw + 1 && g < kNh) {
+            // the dt row of head g: dt = softplus(dt_raw + dt_bias), dA = exp(dt * A)
+            const float* hp = reinterpret_cast<const float*>(slot + Ld.o_hp);
+            const float dt = softplus_f(y + hp[64]);
+            const float A = (float)(-exp((double)hp[128]));
+            ll_store(ex + Ld.dt_off + 2 * g, tg, __float_as_uint(dt));
+            ll_store(ex + Ld.dt_off + 2 * g + 1, tg, __float_as_uint((float)exp((double)(dt * A))));
+          }
           __builtin_amdgcn_s_waitcnt(0xC07F);  // zx_s is in LDS before the flag
         } else {
           // the residual stream: u += delta, then the next layer's input
@@ -735,7 +740,7 @@ __global__ __launch_bounds__(kThreads, 1) void step_persistent(
               const float v = __shfl(u_reg, k, 64);
               s2 += (double)v * (double)v;
             }
-            if (lane == 0) ll_store64(ex + Ln.ss_off + 2 * g, tn, s2);
+            if (lane < kXcds) ll_store64(ex + Ln.ss_off + 2 * (lane * kGrid + g), tn, s2);
           } else if (lane < kOutRows) {
             u_fin[kOutRows * g + lane] = u_reg;
           }
@@ -842,11 +847,13 @@ StepPlan make_step_plan(const dfssm_mamba2_model* md) {
         e.o_st = (int32_t)o;
         o += kCpw * kDs * 4;
         e.o_rg = (int32_t)o;
-        o += cdiv(3 * kRingFloats / 4, 64) * 1024;
+        o += 1024;
+        e.o_rb = (int32_t)o;
+        o += 256;
         e.o_cw = (int32_t)o;
-        o += cdiv(kCpw + 2 * kDs, 64) * 1024;
+        o += 1024;
         e.o_cb = (int32_t)o;
-        o += cdiv((kCpw + 2 * kDs) / 4, 64) * 1024;
+        o += 256;
         e.o_hp = (int32_t)o;
         o += 3 * 256;
       }
@@ -861,12 +868,12 @@ StepPlan make_step_plan(const dfssm_mamba2_model* md) {
       e.in_off = w;
       w += K;
       e.ss_off = w;
-      w += 2 * kGrid;
+      w += (int64_t)kXcds * 2 * kGrid;
       if (kind == 0) {
         e.bc_off = w;
-        w += 2 * kDs;
+        w += (int64_t)kXcds * 2 * kDs;
         e.dt_off = w;
-        w += kNh;
+        w += 2 * kNh;
       }
     }
   }
