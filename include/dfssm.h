@@ -517,7 +517,10 @@ dfssm_status dfssm_mamba2_status(const dfssm_mamba2_model* model, int64_t M, con
  *                                  cores from n tokens instead of 8
  *   DFSSM_TEST_STEP_PER_KERNEL     1: the decode step at M = 1 runs the
  *                                  per-kernel sequence on a prepared
- *                                  workspace too
+ *                                  workspace too; 2: the fused step takes
+ *                                  every input maximum from the second
+ *                                  exchange (its path for inputs with
+ *                                  many near-equal largest entries)
  * Errors: SHAPE for an unknown switch or value. */
 typedef enum {
   DFSSM_TEST_LOCAL_LORA = 1,

@@ -153,7 +153,7 @@ dfssm_status dfssm_test_switch(int which, int value) {
     case DFSSM_TEST_LOCAL_LORA: ok = value == 0 || value == 1; break;
     case DFSSM_TEST_PREFILL_KERNEL: ok = value == 0 || value == 4 || value == 8; break;
     case DFSSM_TEST_LM_HEAD_MFMA_TOKENS: ok = value >= 0; break;
-    case DFSSM_TEST_STEP_PER_KERNEL: ok = value == 0 || value == 1; break;
+    case DFSSM_TEST_STEP_PER_KERNEL: ok = value >= 0 && value <= 2; break;
     default: break;
   }
   if (!ok) return fail(DFSSM_ERR_SHAPE, "test switch %d: value %d", which, value);
@@ -810,13 +810,15 @@ dfssm_status dfssm_mamba2_decode_step(const dfssm_mamba2_model* model, int64_t M
     return fail(DFSSM_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, w.bytes);
   hipStream_t hs = (hipStream_t)stream;
   const float eps = model->eps;
-  if (w.fused && dfssm::test_switch(DFSSM_TEST_STEP_PER_KERNEL) == 0 && is_prepared(workspace, w.fi.fingerprint)) {
+  const int step_switch = dfssm::test_switch(DFSSM_TEST_STEP_PER_KERNEL);
+  if (w.fused && step_switch != 1 && is_prepared(workspace, w.fi.fingerprint)) {
     // the fused step: gather, one persistent launch for all layers, final
     // norm, LM head
     float* u0 = reinterpret_cast<float*>(w.fused + w.fi.off_u0);
     float* ufin = reinterpret_cast<float*>(w.fused + w.fi.off_ufin);
     hipError_t e = dfssm::launch_embed_gather(model->E, model->E_scale, model->vocab, d.d_model, tok, 1, u0, hs);
-    if (e == hipSuccess) e = dfssm::step_fused_run(w.fi, eps, step, conv_ring, ssm_state, w.fused, hs);
+    if (e == hipSuccess)
+      e = dfssm::step_fused_run(w.fi, eps, step, conv_ring, ssm_state, w.fused, step_switch == 2, hs);
     if (e == hipSuccess)
       e = dfssm::launch_add_rmsnorm_quant(ufin, nullptr, model->norm_f, eps, 1, d.d_model, nullptr, w.q, w.s, hs);
     if (e == hipSuccess)

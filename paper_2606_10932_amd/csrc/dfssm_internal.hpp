@@ -196,8 +196,10 @@ struct StepFusedInfo {
 };
 StepFusedInfo step_fused_info(const dfssm_mamba2_model* md);
 hipError_t step_fused_prepare(const dfssm_mamba2_model* md, void* ws, hipStream_t st);
+// two_hop: the input maxima always take the second exchange (for tests;
+// results are the same bits either way)
 hipError_t step_fused_run(const StepFusedInfo& f, float eps, int64_t step, float* conv_ring, float* ssm_state,
-                          void* ws, hipStream_t st);
+                          void* ws, bool two_hop, hipStream_t st);
 
 hipError_t launch_zero_words(uint64_t* p, int64_t words, hipStream_t st);
 

@@ -102,7 +102,7 @@ struct StepLin {
   int64_t p_off;     // XCD-local words [8 XCDs][8 slices][64]: rank partials
   int64_t mx_off;    // XCD-local words [8 XCDs][4 row groups][8 slices]: slice maxima
   int64_t in_off;    // agent words [K]: this linear's input values
-  int64_t ss_off;    // agent words [8 XCDs][256][2]: their partial sums of squares (fp64)
+  int64_t st_off;    // agent words [8 XCDs][4 row groups][8 slices][8]: each slice's sum of squares and largest entries
   int64_t bc_off;    // in_proj: agent words [8 XCDs][2 d_state]: the B/C rows after the convolution
   int64_t dt_off;    // in_proj: agent words [heads][2]: dt and dA of each head
 };
@@ -116,11 +116,31 @@ __device__ __forceinline__ float softplus_f(float v) {
   if (v > 20.0f) return v;
   return (float)log1p(exp((double)v));
 }
-// An fp64 value as two words (high half, low half), each with the tag.
-__device__ __forceinline__ void ll_store64(uint64_t* p, uint32_t tag, double v) {
+// DPP move of an fp64 value (both halves with the same control); rows the
+// mask leaves out read 0.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ double dpp_f64(double v) {
   const uint64_t b = (uint64_t)__double_as_longlong(v);
-  ll_store(p, tag, (uint32_t)(b >> 32));
-  ll_store(p + 1, tag, (uint32_t)b);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, kCtrl, kRowMask, 0xF, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), kCtrl, kRowMask, 0xF, false);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+__device__ __forceinline__ double readlane_f64(double v, int lane) {
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), lane);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+// Whole-wave fp64 sum, in the same fixed order in every wave: pairs, quads,
+// rows, then the row broadcasts that leave the total in lane 63.
+__device__ __forceinline__ double wave_sum_f64_u(double v) {
+  v = v + dpp_f64<0xB1, 0xF>(v);
+  v = v + dpp_f64<0x4E, 0xF>(v);
+  v = v + dpp_f64<0x141, 0xF>(v);
+  v = v + dpp_f64<0x140, 0xF>(v);
+  v = v + dpp_f64<0x142, 0xA>(v);
+  v = v + dpp_f64<0x143, 0xC>(v);
+  return readlane_f64(v, 63);
 }
 
 // Row k of reducer g (-1: none).  in_proj: z and x of channels 16g..16g+15,
@@ -266,7 +286,8 @@ __device__ __forceinline__ void note_abort_linear(unsigned* status, int j) {
 __global__ __launch_bounds__(kThreads, 1) void step_persistent(
     const StepLin* __restrict__ lins, int L2, int t, const float* __restrict__ u0, float* __restrict__ u_fin,
     float* __restrict__ conv_ring, float* __restrict__ ssm_state, uint64_t* __restrict__ ex, int64_t ex_words,
-    unsigned* status, uint64_t* epoch, const uint64_t* __restrict__ table_hash, uint64_t expect_hash, float eps) {
+    unsigned* status, uint64_t* epoch, const uint64_t* __restrict__ table_hash, uint64_t expect_hash, float eps,
+    int two_hop) {
   if (*table_hash != expect_hash) {
     if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(status, kStHash);
     return;
@@ -277,10 +298,9 @@ __global__ __launch_bounds__(kThreads, 1) void step_persistent(
   __shared__ __attribute__((aligned(16))) uint32_t planes[8][kMaxKs / 32];
   __shared__ __attribute__((aligned(16))) uint4 limbs[kMaxR / 4];
   __shared__ int red[64 * 17];
-  __shared__ double ssp[kGrid];  // the input's 256 partial sums of squares
   __shared__ float zx_s[2 * kCpw];  // in_proj outputs z, x of this workgroup's channels
   __shared__ float bcc[2 * kDs];    // convolved B and C
-  __shared__ float xc[kCpw], szv[kCpw], gv[kCpw];  // convolved x, silu(z), gated SSM outputs
+  __shared__ float xc[kCpw], szv[kCpw];  // convolved x, silu(z)
   __shared__ float dts[3];          // dt, dA, D of the head
   __shared__ float qs_s;            // the token scale of the current linear's input
   __shared__ int sumq[2];
@@ -403,20 +423,10 @@ __global__ __launch_bounds__(kThreads, 1) void step_persistent(
           if (sub == 0) {
             const float y = (float)(acc + (double)dts[2] * (double)xv);
             const float gval = y * szv[p];
-            gv[p] = gval;
             ll_store(ex + Ld.in_off + kCpw * g + p, tg, __float_as_uint(gval));
           }
           __builtin_amdgcn_s_waitcnt(0xC07F);
           if (lane == 0) __hip_atomic_fetch_add(&g_cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-          if (wave == 1) {
-            // the sum of squares of the 16 gated outputs, one copy per XCD
-            STEP_WAIT_FLAG(FLAG(g_cnt) >= 4 * (l + 1), sp, kStSsm);
-            if (lane < kXcds && !FLAG(abort_)) {
-              double s2 = 0.0;
-              for (int q = 0; q < kCpw; ++q) s2 += (double)gv[q] * (double)gv[q];
-              ll_store64(ex + Ld.ss_off + 2 * (lane * kGrid + g), tg, s2);
-            }
-          }
           // the new state last: a wave's stores complete in order, and the
           // words above are what every other workgroup is waiting for
           float4* dst = reinterpret_cast<float4*>(ssm_state + l * state_stride + (int64_t)(kCpw * g + p) * kDs + n0);
@@ -424,36 +434,23 @@ __global__ __launch_bounds__(kThreads, 1) void step_persistent(
           dst[1] = make_float4(hs[4], hs[5], hs[6], hs[7]);
         }
       }
-      // ---- phase D: this slice of the input and the 256 partial sums of
-      //      squares
+      // ---- phase D: this slice of the input
       const int i0 = ct, i1 = ct + kPollLanes;
       if (ju == 0) {
         if (i0 < Ks) ys[i0] = u0[kap * Ks + i0];
         if (i1 < Ks) ys[i1] = u0[kap * Ks + i1];
-        if (ct < kGrid) {
-          double s2 = 0.0;
-          for (int k = 0; k < kOutRows; ++k) {
-            const float v = u0[kOutRows * ct + k];
-            s2 += (double)v * (double)v;
-          }
-          ssp[ct] = s2;
-        }
       } else {
         // out_proj: polls start once this workgroup's own gated outputs are
         // out (the others come at about the same time; earlier polls only
         // load the fabric)
         if (!is_in) STEP_WAIT_FLAG(FLAG(g_cnt) >= 4 * (l + 1), sp, kStSsm);
-        uint32_t pend = (i0 < Ks ? 1u : 0u) | (i1 < Ks ? 2u : 0u) | (ct < kGrid ? 12u : 0u);
+        uint32_t pend = (i0 < Ks ? 1u : 0u) | (i1 < Ks ? 2u : 0u);
         if (FLAG(abort_)) pend = 0;
         const uint64_t* iw = ex + Ld.in_off + (int64_t)kap * Ks;
-        const uint64_t* ssw = ex + Ld.ss_off + 2 * x * kGrid;  // this XCD's copy
-        uint32_t shi = 0, slo = 0;
         while (pend) {
-          uint64_t w0 = 0, w1 = 0, w2 = 0, w3 = 0;
+          uint64_t w0 = 0, w1 = 0;
           if (pend & 1u) w0 = ll_load(iw + i0);
           if (pend & 2u) w1 = ll_load(iw + i1);
-          if (pend & 4u) w2 = ll_load(ssw + 2 * ct);
-          if (pend & 8u) w3 = ll_load(ssw + 2 * ct + 1);
           if ((pend & 1u) && (uint32_t)(w0 >> 32) == tg) {
             ys[i0] = __uint_as_float((uint32_t)w0);
             pend &= ~1u;
@@ -462,17 +459,8 @@ __global__ __launch_bounds__(kThreads, 1) void step_persistent(
             ys[i1] = __uint_as_float((uint32_t)w1);
             pend &= ~2u;
           }
-          if ((pend & 4u) && (uint32_t)(w2 >> 32) == tg) {
-            shi = (uint32_t)w2;
-            pend &= ~4u;
-          }
-          if ((pend & 8u) && (uint32_t)(w3 >> 32) == tg) {
-            slo = (uint32_t)w3;
-            pend &= ~8u;
-          }
           if (pend && spin_gives_up(sp, &abort_, status, kStIn)) break;
         }
-        if (ct < kGrid) ssp[ct] = __longlong_as_double((long long)(((uint64_t)shi << 32) | slo));
       }
     }
     CHAIN_BARRIER();  // B1
@@ -483,39 +471,154 @@ __global__ __launch_bounds__(kThreads, 1) void step_persistent(
 
     uint32_t cq0 = 0, cq1 = 0;  // wave 1: codes 8p .. 8p+7 of the slice
     if (wave == 1) {
-      // ---- the scale r from the 256 partial sums (one fixed order in every
-      //      workgroup), the slice of (v * r) * w, its maximum, the row
-      //      group's maximum over the 8 slices (XCD-local words), the codes
-      double s4 = ((ssp[4 * lane] + ssp[4 * lane + 1]) + ssp[4 * lane + 2]) + ssp[4 * lane + 3];
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) s4 += __shfl_xor(s4, off, 64);
-      const float rr = (float)(1.0 / sqrt(s4 / (double)K + (double)eps));
+      // ---- the scale r and the maximum of |(v * r) * w| over the whole
+      //      input, from one exchange among the row group's 8 workgroups
+      //      (one slice each).  Every workgroup publishes its slice's fp64
+      //      sum of squares (wave 2, below) and the entries whose fp32
+      //      |v * w| lies within 2^-19 of the slice's largest.  The rounding
+      //      of that product and of the two fp32 products of (v * r) * w
+      //      moves a value by less than 2^-21 of it, so no other entry can
+      //      exceed the largest of these: while values stay in the normal
+      //      range (checked below) the maximum over the published entries
+      //      is the input's maximum.  Otherwise (more than two such entries
+      //      in a slice, values near the ends of the range) the slices'
+      //      maxima after r take a second exchange.
       const int p = lane;
       const bool inb = 8 * p < Ks;
       const float* nwv = reinterpret_cast<const float*>(slot + Ld.o_nw);
-      float xv[8];
-      uint32_t m = 0;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int c = inb ? 8 * p + e : 0;
-        const float tv = ys[c] * rr;
-        xv[e] = tv * nwv[c];
-        if (inb) m = max(m, __float_as_uint(xv[e]) & 0x7fffffffu);
+      const uint64_t* stw = ex + Ld.st_off + (int64_t)(x * kGroups + h) * kSlices * 8;
+      // lanes past the slice's end take zeros: they change no maximum and
+      // (with a positive largest product) no candidate
+      float gq[8], wq[8];
+      {
+        const float4* y4 = reinterpret_cast<const float4*>(ys) + (inb ? 2 * p : 0);
+        const float4* w4 = reinterpret_cast<const float4*>(nwv) + (inb ? 2 * p : 0);
+        const float4 ya = y4[0], yb = y4[1], wa = w4[0], wb = w4[1];
+        const float z = 0.0f;
+        gq[0] = inb ? ya.x : z; gq[1] = inb ? ya.y : z; gq[2] = inb ? ya.z : z; gq[3] = inb ? ya.w : z;
+        gq[4] = inb ? yb.x : z; gq[5] = inb ? yb.y : z; gq[6] = inb ? yb.z : z; gq[7] = inb ? yb.w : z;
+        wq[0] = inb ? wa.x : z; wq[1] = inb ? wa.y : z; wq[2] = inb ? wa.z : z; wq[3] = inb ? wa.w : z;
+        wq[4] = inb ? wb.x : z; wq[5] = inb ? wb.y : z; wq[6] = inb ? wb.z : z; wq[7] = inb ? wb.w : z;
       }
-      m = wave_max_bits_u(m);
-      if (lane == 0) ll_store(ex + Ld.mx_off + (x * kGroups + h) * kSlices + kap, tg, m);
-      uint32_t a_bits = 0;
-      if (lane < kSlices) {
+      {
+        float ef[8];
+        uint32_t em = 0, gm = 0, wm = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          ef[e] = fabsf(gq[e] * wq[e]);
+          em = max(em, __float_as_uint(ef[e]));
+          gm = max(gm, __float_as_uint(gq[e]) & 0x7fffffffu);
+          wm = max(wm, __float_as_uint(wq[e]) & 0x7fffffffu);
+        }
+        em = wave_max_bits_u(em);
+        gm = wave_max_bits_u(gm);
+        const float thr = __uint_as_float(em) * (1.0f - 0x1p-19f);
+        int cnt = 0;
+        float a0 = 0.0f, b0 = 0.0f, a1 = 0.0f, b1v = 0.0f;  // (v, w) of this lane's first two
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const bool hit = ef[e] >= thr;
+          a1 = hit && cnt == 1 ? gq[e] : a1;
+          b1v = hit && cnt == 1 ? wq[e] : b1v;
+          a0 = hit && cnt == 0 ? gq[e] : a0;
+          b0 = hit && cnt == 0 ? wq[e] : b0;
+          cnt += hit ? 1 : 0;
+        }
+        // finite values and products, norm weights up to 2^40, at most two
+        // candidates
+        const uint64_t h1 = __ballot(cnt >= 1), h2 = __ballot(cnt >= 2), h3 = __ballot(cnt >= 3);
+        const bool slow_w = gm >= 0x7f800000u || em >= 0x7f800000u || __ballot(wm > 0x53800000u) != 0 ||
+                            h3 != 0 || __popcll(h1) + __popcll(h2) > 2;
+        uint32_t c0g = 0, c0w = 0, c1g = 0, c1w = 0;
+        if (!slow_w) {
+          const int la = __builtin_ctzll(h1);
+          c0g = (uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(a0), la);
+          c0w = (uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(b0), la);
+          c1g = c0g;
+          c1w = c0w;
+          if (h2 != 0) {
+            c1g = (uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(a1), la);
+            c1w = (uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(b1v), la);
+          } else if ((h1 & (h1 - 1)) != 0) {
+            const int lb = __builtin_ctzll(h1 & (h1 - 1));
+            c1g = (uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(a0), lb);
+            c1w = (uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(b0), lb);
+          }
+        }
+        uint32_t v = slow_w ? 1u : 0u;
+        v = lane == 6 ? gm : v;
+        v = lane == 5 ? c1w : v;
+        v = lane == 4 ? c1g : v;
+        v = lane == 3 ? c0w : v;
+        v = lane == 2 ? c0g : v;
+        if (lane >= 2 && lane < 8)
+          ll_store(ex + Ld.st_off + (int64_t)((x * kGroups + h) * kSlices + kap) * 8 + lane, tg, v);
+      }
+      // lane 8k + i: word i of slice k
+      uint32_t sv = 0;
+      {
         long sp = 0;
-        uint64_t w = 0;
         while (!FLAG(abort_)) {
-          w = ll_load(ex + Ld.mx_off + (x * kGroups + h) * kSlices + lane);
-          if ((uint32_t)(w >> 32) == tg) break;
+          const uint64_t w = ll_load(stw + lane);
+          if ((uint32_t)(w >> 32) == tg) {
+            sv = (uint32_t)w;
+            break;
+          }
           if (spin_gives_up(sp, &abort_, status, kStIn)) break;
         }
-        a_bits = (uint32_t)w;
       }
-      a_bits = wave_max_bits_u(a_bits);
+      double S = 0.0;
+#pragma unroll
+      for (int k = 0; k < kSlices; ++k) {
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)sv, 8 * k);
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)sv, 8 * k + 1);
+        S += __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+      }
+      const float rr = (float)(1.0 / sqrt(S / (double)K + (double)eps));
+      float xv[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float tv = gq[e] * rr;
+        xv[e] = tv * wq[e];
+      }
+      const int wd = lane & 7;
+      // lanes 8k + 3 and 8k + 5 take the entry's v from the lane before
+      const uint32_t s_prev = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)sv, 0x111, 0xF, 0xF, false);  // row_shr:1
+      uint32_t cand = 0;
+      bool fail = false;
+      if (wd == 3 || wd == 5) {
+        // a published entry: its (v * r) * w, and r * |v| * |w| not below 2^-60
+        const float gc = __uint_as_float(s_prev), wc = __uint_as_float(sv);
+        const float tv = gc * rr;
+        cand = __float_as_uint(tv * wc) & 0x7fffffffu;
+        fail = fabs((double)gc * (double)wc) * (double)rr < 0x1p-60;
+      } else if (wd == 6) {
+        fail = (double)__uint_as_float(sv) * (double)rr > 0x1p80;  // r * max |v| up to 2^80
+      } else if (wd == 7) {
+        fail = sv != 0;
+      }
+      uint32_t a_bits = 0;
+      if (!two_hop && __ballot(fail) == 0) {
+        a_bits = wave_max_bits_u(cand);
+      } else {
+        uint32_t m = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (inb) m = max(m, __float_as_uint(xv[e]) & 0x7fffffffu);
+        m = wave_max_bits_u(m);
+        if (lane == 0) ll_store(ex + Ld.mx_off + (x * kGroups + h) * kSlices + kap, tg, m);
+        if (lane < kSlices) {
+          long sp = 0;
+          uint64_t w = 0;
+          while (!FLAG(abort_)) {
+            w = ll_load(ex + Ld.mx_off + (x * kGroups + h) * kSlices + lane);
+            if ((uint32_t)(w >> 32) == tg) break;
+            if (spin_gives_up(sp, &abort_, status, kStIn)) break;
+          }
+          a_bits = (uint32_t)w;
+        }
+        a_bits = wave_max_bits_u(a_bits);
+      }
       const float a = __uint_as_float(a_bits);
       const bool zero = a < FLT_MIN;
       const float inv = zero ? 0.0f : 127.0f / a;
@@ -555,6 +658,24 @@ __global__ __launch_bounds__(kThreads, 1) void step_persistent(
       }
       qsum = wave_sum_u(qsum);
       if (lane == 0) sumq[ju & 1] = qsum;
+    } else if (wave == 2) {
+      // ---- the slice's fp64 sum of squares (words 0 and 1 of this
+      //      workgroup's entry; the same order in every workgroup that holds
+      //      the slice)
+      const bool inb = 8 * lane < Ks;
+      const float4* y4 = reinterpret_cast<const float4*>(ys) + (inb ? 2 * lane : 0);
+      const float4 ya = y4[0], yb = y4[1];
+      const float gv[8] = {ya.x, ya.y, ya.z, ya.w, yb.x, yb.y, yb.z, yb.w};
+      double sq = 0.0;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const double d = inb ? (double)gv[e] : 0.0;
+        sq = sq + d * d;
+      }
+      const uint64_t sb = (uint64_t)__double_as_longlong(wave_sum_f64_u(sq));
+      if (lane < 2)
+        ll_store(ex + Ld.st_off + (int64_t)((x * kGroups + h) * kSlices + kap) * 8 + lane, tg,
+                 lane == 0 ? (uint32_t)(sb >> 32) : (uint32_t)sb);
     }
     CHAIN_BARRIER();  // B2
     if (FLAG(abort_)) {
@@ -734,13 +855,6 @@ __global__ __launch_bounds__(kThreads, 1) void step_persistent(
             const StepLin& Ln = lins[ju + 1];
             const uint32_t tn = tag_of(ju + 1);
             if (lane < kOutRows) ll_store(ex + Ln.in_off + kOutRows * g + lane, tn, __float_as_uint(u_reg));
-            double s2 = 0.0;
-#pragma unroll
-            for (int k = 0; k < kOutRows; ++k) {
-              const float v = __shfl(u_reg, k, 64);
-              s2 += (double)v * (double)v;
-            }
-            if (lane < kXcds) ll_store64(ex + Ln.ss_off + 2 * (lane * kGrid + g), tn, s2);
           } else if (lane < kOutRows) {
             u_fin[kOutRows * g + lane] = u_reg;
           }
@@ -867,8 +981,8 @@ StepPlan make_step_plan(const dfssm_mamba2_model* md) {
       w += (int64_t)kXcds * (kPerXcd / kSlices) * kSlices;
       e.in_off = w;
       w += K;
-      e.ss_off = w;
-      w += (int64_t)kXcds * 2 * kGrid;
+      e.st_off = w;
+      w += (int64_t)kXcds * kGroups * kSlices * 8;
       if (kind == 0) {
         e.bc_off = w;
         w += (int64_t)kXcds * 2 * kDs;
@@ -973,7 +1087,7 @@ hipError_t step_fused_prepare(const dfssm_mamba2_model* md, void* ws, hipStream_
 // A plain launch of one workgroup per CU (its LDS use admits one per CU);
 // the whole grid has to be resident at once, and every wait is bounded.
 hipError_t step_fused_run(const StepFusedInfo& f, float eps, int64_t step, float* conv_ring, float* ssm_state,
-                          void* ws, hipStream_t st) {
+                          void* ws, bool two_hop, hipStream_t st) {
   if (!f.ok) return hipErrorInvalidValue;
   char* base = static_cast<char*>(ws);  // the table sits at the region's start
   step_persistent<<<dim3(kGrid), dim3(kThreads), 0, st>>>(
@@ -981,7 +1095,7 @@ hipError_t step_fused_run(const StepFusedInfo& f, float eps, int64_t step, float
       reinterpret_cast<const float*>(base + f.off_u0), reinterpret_cast<float*>(base + f.off_ufin), conv_ring,
       ssm_state, reinterpret_cast<uint64_t*>(base + f.off_ex), f.ex_words,
       reinterpret_cast<unsigned*>(base + f.off_status), reinterpret_cast<uint64_t*>(base + f.off_epoch),
-      reinterpret_cast<const uint64_t*>(base + f.off_hash), f.fingerprint, eps);
+      reinterpret_cast<const uint64_t*>(base + f.off_hash), f.fingerprint, eps, two_hop ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -145,3 +145,51 @@ def test_unprepared_workspace_runs_per_kernel(env, model3):
         torch.cuda.synchronize()
         _logits_check(lg, om.step(tok), f"token {t}")
     assert m.status(1, ws) == 0
+
+
+def _tie_model(model3):
+    """model3 with layer 0's norm weights all 1 and embedding rows whose
+    largest entries tie: row 7 constant (every entry ties), row 8 two
+    largest entries in one lane's eight (3 and 5), row 9 two in different
+    lanes (3 and 17), row 10 all zero."""
+    md = dict(model3)
+    E = model3["E"].copy()
+    E[7] = 40
+    for row, ids in ((8, (3, 5)), (9, (3, 17))):
+        E[row] = np.clip(E[row], -60, 60)
+        E[row, list(ids)] = 100
+    E[10] = 0
+    md["E"] = E
+    md["layers"] = [dict(model3["layers"][0], norm_w=np.ones(2048, np.float32))] + list(model3["layers"][1:])
+    return md
+
+
+@pytest.mark.parametrize("tied", [False, True])
+def test_fused_step_one_and_two_exchanges(env, model3, tied, record_property):
+    """The input maxima from one exchange (the published largest entries)
+    and from the second exchange (forced) give the same bits, both within
+    the bar of the oracle; with tied largest entries (every entry of a
+    constant row ties, which takes the second exchange) and a zero row."""
+    torch, D, o = env
+    md = _tie_model(model3) if tied else model3
+    toks = [np.array([t], np.int32) for t in (7, 8, 9, 10, 7)] if tied else \
+        [S.tokens(1, V, key=(167, t)) for t in range(4)]
+    say(f"fused decode step: one and two exchanges for the input maxima, {'tied' if tied else 'random'} tokens")
+    m = device_model(D, md)
+    ring, state = m.new_state(1)
+    ws = m.workspace(1)
+    ring2, state2 = m.new_state(1)
+    ws2 = m.workspace(1)
+    om = OracleModel(o, md, 1)
+    exact = 0
+    for t, tk in enumerate(toks):
+        lg = host(m.decode_step(dev(tk), t, ring, state, ws))
+        with forced_switch(D, D.TEST_STEP_PER_KERNEL, 2):
+            l2 = host(m.decode_step(dev(tk), t, ring2, state2, ws2))
+        torch.cuda.synchronize()
+        assert m.status(1, ws) == 0 and m.status(1, ws2) == 0
+        assert np.array_equal(lg.view(np.uint32), l2.view(np.uint32)), f"token {t}: one and two exchanges differ"
+        exact += _logits_check(lg, om.step(tk), f"token {t}")
+    assert np.array_equal(host(state), host(state2))
+    say(f"  {exact} of {len(toks)} tokens bit-exact against the oracle")
+    record_property("bit_exact_tokens", f"{exact}/{len(toks)}")
