@@ -458,9 +458,9 @@ def main():
         table_bytes = table0[0].numel() + table0[1].numel() * 4
         model_fig = []
 
-        def time_model(mdl, Mb, wbytes, label):
+        def time_model(mdl, Mb, wbytes, label, prepare=True):
             ring, state = mdl.new_state(Mb)
-            ws_m = mdl.workspace(Mb)
+            ws_m = mdl.workspace(Mb, prepare=prepare)
             tok = dev(S.tokens(Mb, S.VOCAB_1P3B, key=(152, Mb)))
             lg = torch.empty((Mb, S.VOCAB_1P3B), dtype=torch.float32, device="cuda")
             side = torch.cuda.Stream()
@@ -487,8 +487,9 @@ def main():
             # bytes a step must move at least: weights, table, parameters,
             # the SSM state read and written, the ring (3 slots read, 1 written)
             step_bytes = wbytes + table_bytes + param_bytes + 2 * state.numel() * 4 + ring.numel() * 4
+            path = "one persistent launch for the 48 layers" if mdl.fused_path(Mb, ws_m) else "per-kernel sequence"
             model_fig.append({"workload": f"Mamba-2-1.3B decode step, batch {Mb}, 48 layers + LM head{label}",
-                              "ms_per_step": round(ms_tok, 4), "tokens_per_s": round(Mb / (ms_tok * 1e-3), 1),
+                              "path": path, "ms_per_step": round(ms_tok, 4), "tokens_per_s": round(Mb / (ms_tok * 1e-3), 1),
                               "us_per_layer": round(ms_tok * 1e3 / 48, 2),
                               "bytes_per_step": int(step_bytes),
                               "effective_gbs": round(step_bytes / (ms_tok * 1e-3) / 1e9, 1)})
@@ -497,6 +498,10 @@ def main():
 
         for Mb in [int(v) for v in args.model_batches.split(",") if v]:
             time_model(mdl, Mb, weight_bytes, "")
+            if Mb == 1:
+                # the same step on an unprepared workspace: the per-kernel
+                # sequence, for comparison
+                time_model(mdl, Mb, weight_bytes, "", prepare=False)
         # the same model with int4 LoRA factors (r = 64) in every projection
         i4_batches = [int(v) for v in args.model_i4_batches.split(",") if v]
         if i4_batches:

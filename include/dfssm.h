@@ -488,6 +488,13 @@ dfssm_status dfssm_mamba2_prepare(const dfssm_mamba2_model* model, int64_t M, vo
  * Errors: none. */
 dfssm_status dfssm_mamba2_release(const void* workspace);
 
+/* *fused = 1 if dfssm_mamba2_decode_step on this model, M and workspace
+ * takes the fused step (one persistent launch for the layers), else 0
+ * (host call, no device work).
+ * Errors: NULL, SHAPE, ALIGN, WORKSPACE. */
+dfssm_status dfssm_mamba2_fused_path(const dfssm_mamba2_model* model, int64_t M, const void* workspace,
+                                     size_t workspace_bytes, int* fused);
+
 /* Synchronises `stream` and reads the fused step's status word into
  * *status (host): 0 = fine; bit 1 = a wait for a linear's input timed out;
  * bit 2 = a wait for a row or rank partial timed out; bit 4 = a wait in the

@@ -27,7 +27,7 @@ EXPORTS = ["dfssm_quantize_act", "dfssm_linear_workspace_bytes", "dfssm_scaffold
            "dfssm_embed_gather", "dfssm_lm_head", "dfssm_add_rmsnorm_quant", "dfssm_gate_norm_quant",
            "dfssm_ssm_step", "dfssm_linear_i4_workspace_bytes", "dfssm_scaffold_lora_linear_i4",
            "dfssm_mamba2_state_bytes", "dfssm_mamba2_workspace_bytes",
-           "dfssm_mamba2_decode_step", "dfssm_mamba2_prepare", "dfssm_mamba2_release", "dfssm_mamba2_status", "dfssm_scaffold_lora_linear_noalloc", "dfssm_noalloc_scratch_bytes",
+           "dfssm_mamba2_decode_step", "dfssm_mamba2_prepare", "dfssm_mamba2_release", "dfssm_mamba2_status", "dfssm_mamba2_fused_path", "dfssm_scaffold_lora_linear_noalloc", "dfssm_noalloc_scratch_bytes",
            "dfssm_test_switch", "dfssm_status_string", "dfssm_last_error",
            "dfssm_version"]
 TEST_LOCAL_LORA, TEST_PREFILL_KERNEL, TEST_LM_HEAD_MFMA_TOKENS, TEST_STEP_PER_KERNEL = 1, 2, 3, 4
@@ -117,6 +117,8 @@ def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dfssm_mamba2_release.restype = i32
     lib.dfssm_mamba2_status.argtypes = [mp, i64, vp, sz, ctypes.POINTER(ctypes.c_uint), vp]
     lib.dfssm_mamba2_status.restype = i32
+    lib.dfssm_mamba2_fused_path.argtypes = [mp, i64, vp, sz, ctypes.POINTER(ctypes.c_int)]
+    lib.dfssm_mamba2_fused_path.restype = i32
     lib.dfssm_scaffold_lora_linear_noalloc.argtypes = [vp, vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp]
     lib.dfssm_scaffold_lora_linear_noalloc.restype = i32
     lib.dfssm_noalloc_scratch_bytes.argtypes = []
@@ -496,6 +498,13 @@ class Mamba2:
         _check(lib.dfssm_mamba2_status(ctypes.byref(self.struct), M, workspace.data_ptr(), workspace.numel(),
                                        ctypes.byref(out), _stream(stream)))
         return int(out.value)
+
+    def fused_path(self, M: int, workspace) -> bool:
+        """Whether decode_step at M on this workspace takes the fused step."""
+        out = ctypes.c_int(0)
+        _check(lib.dfssm_mamba2_fused_path(ctypes.byref(self.struct), M, workspace.data_ptr(), workspace.numel(),
+                                           ctypes.byref(out)))
+        return bool(out.value)
 
     def decode_step(self, tok, step: int, conv_ring, ssm_state, workspace, logits=None, stream=None):
         """One token for each of the M sequences (tok int32 [M]); returns

@@ -892,6 +892,25 @@ dfssm_status dfssm_mamba2_release(const void* workspace) {
   return DFSSM_OK;
 }
 
+dfssm_status dfssm_mamba2_fused_path(const dfssm_mamba2_model* model, int64_t M, const void* workspace,
+                                     size_t workspace_bytes, int* fused) {
+  clear_error();
+  if (!fused) return fail(DFSSM_ERR_NULL, "fused is NULL");
+  *fused = 0;
+  ModelDims d;
+  dfssm_status st = check_model(model, M, &d);
+  if (st != DFSSM_OK) return st;
+  st = check_ptrs({{workspace, "workspace"}}, {});
+  if (st != DFSSM_OK) return st;
+  const ModelWs w = carve_model_ws(const_cast<void*>(workspace), model, d, M);
+  if (workspace_bytes < w.bytes)
+    return fail(DFSSM_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, w.bytes);
+  *fused = w.fused && dfssm::test_switch(DFSSM_TEST_STEP_PER_KERNEL) != 1 && is_prepared(workspace, w.fi.fingerprint)
+               ? 1
+               : 0;
+  return DFSSM_OK;
+}
+
 dfssm_status dfssm_mamba2_status(const dfssm_mamba2_model* model, int64_t M, const void* workspace,
                                  size_t workspace_bytes, unsigned* status, void* stream) {
   clear_error();

@@ -55,6 +55,9 @@ def test_fused_step_against_oracle_and_per_kernel(env, model3, record_property):
     ws = m.workspace(1)
     ring_k, state_k = m.new_state(1)
     ws_k = m.workspace(1)
+    assert m.fused_path(1, ws) and m.fused_path(1, ws_k)
+    with forced_switch(D, D.TEST_STEP_PER_KERNEL, 1):
+        assert not m.fused_path(1, ws)
     om = OracleModel(o, model3, 1)
     exact = same = 0
     for t in range(T):
@@ -138,6 +141,7 @@ def test_unprepared_workspace_runs_per_kernel(env, model3):
     m = device_model(D, model3)
     ring, state = m.new_state(1)
     ws = m.workspace(1, prepare=False)
+    assert not m.fused_path(1, ws)
     om = OracleModel(o, model3, 1)
     for t in range(2):
         tok = S.tokens(1, V, key=(166, t))

@@ -259,6 +259,11 @@ def test_model_step_validation(dl):
     assert stat(ctypes.byref(m), 1, 16, 64, ctypes.byref(st), None) == dl.ERR_WORKSPACE
     # an unprepared workspace: no device read, status 0
     assert stat(ctypes.byref(m), 1, 16, 1 << 40, ctypes.byref(st), None) == dl.OK and st.value == 0
+    # the path query: the per-kernel sequence on an unprepared workspace
+    fp, fz = dl.lib.dfssm_mamba2_fused_path, ctypes.c_int(7)
+    assert fp(ctypes.byref(m), 1, 16, 1 << 40, None) == dl.ERR_NULL
+    assert fp(ctypes.byref(m), 1, 16, 64, ctypes.byref(fz)) == dl.ERR_WORKSPACE
+    assert fp(ctypes.byref(m), 1, 16, 1 << 40, ctypes.byref(fz)) == dl.OK and fz.value == 0
 
 
 def test_int4_linear_validation(dl):
