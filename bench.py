@@ -36,7 +36,8 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 PEAK_I8_TOPS = 5000.0        # MI355X dense int8 MFMA
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "chain_persistent_1p3b_sweep_traffic.txt")
-CHAIN_SOURCES = ["paper_2606_10932_amd/csrc/dfssm_chain.hip", "paper_2606_10932_amd/csrc/dfssm_internal.hpp"]
+CHAIN_SOURCES = ["paper_2606_10932_amd/csrc/dfssm_chain.hip", "paper_2606_10932_amd/csrc/dfssm_internal.hpp",
+                 "paper_2606_10932_amd/csrc/dfssm_persist.hpp"]
 
 
 def parse():
