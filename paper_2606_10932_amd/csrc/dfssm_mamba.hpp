@@ -7,8 +7,8 @@
 
 namespace dfssm {
 
-// Largest row the two norm kernels hold in registers (16 float4 per thread
-// of a 256-thread workgroup).
+// Largest row the two norm kernels hold in registers: at most 4 float4 per
+// thread, on 512 threads up to d = 8192 and on 1024 threads beyond.
 constexpr int64_t kNormMaxD = 16384;
 
 // u_out = u + delta (delta may be null; u_out may be null or u), then
