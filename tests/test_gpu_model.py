@@ -225,6 +225,7 @@ def test_decode_step_full_model(env, model_host_full, M, record_property):
     m = device_model(D, model_host_full)
     ring, state = m.new_state(M)
     ws = m.workspace(M)
+    assert m.fused_path(M, ws) == (M == 1)   # batch 1: one persistent launch for the 48 layers
     om = OracleModel(o, model_host_full, M)
     exact = 0
     for t in range(T):
