@@ -281,6 +281,40 @@ def main():
     # over distinct copies of the weights, about 600 MB in all, so every call
     # meets its weights outside the 256 MB Infinity Cache; the graph removes
     # the host's launch cost from the measurement.
+    def read_floors(nbytes, ncall):
+        """The floor under a single linear of nbytes of weights: one launch
+        reading nbytes (dfssm_read_floor), over ncall distinct buffers so
+        every read is cold, replayed from a graph as the linears are; and
+        the same graph of empty launches."""
+        nb16 = (nbytes + 15) // 16 * 16
+        bufs = [torch.empty(nb16, dtype=torch.uint8, device="cuda") for _ in range(ncall)]
+        sink = torch.zeros(D.read_floor_sink_words(nb16), dtype=torch.int32, device="cuda")
+        out = {}
+        for label, nb in (("floor_us_read", nb16), ("floor_us_launch", 0)):
+            def calls():
+                for b in bufs:
+                    D.read_floor(b, sink, nbytes=nb)
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                calls()
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=side):
+                    calls()
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            reps = 3
+            t0.record(stream)
+            for _ in range(reps):
+                g.replay()
+            t1.record(stream)
+            torch.cuda.synchronize()
+            out[label] = round(t0.elapsed_time(t1) * 1e3 / (reps * ncall), 2)
+            del g
+        del bufs
+        return out
+
     decode = None
     if not args.no_decode:
         decode = []
@@ -342,10 +376,14 @@ def main():
                 t1.record(stream)
                 torch.cuda.synchronize()
                 us_warm = t0.elapsed_time(t1) * 1e3 / (reps * ncall)
-                decode.append({"workload": f"{name} M={m}", "us_per_call": round(us, 2),
-                               "us_per_call_warm": round(us_warm, 2),
-                               "weight_gbs": round(wb / (us * 1e-6) / 1e9, 1), "weight_bytes": wb,
-                               "path": "few-token MFMA (one launch)", "lora": "int8"})
+                fig = {"workload": f"{name} M={m}", "us_per_call": round(us, 2),
+                       "us_per_call_warm": round(us_warm, 2),
+                       "weight_gbs": round(wb / (us * 1e-6) / 1e9, 1), "weight_bytes": wb,
+                       "path": "few-token MFMA (one launch)", "lora": "int8"}
+                if m == 1 and cfg > 0:
+                    # the floor: a cold one-launch read of the same bytes
+                    fig.update(read_floors(wb, ncall))
+                decode.append(fig)
                 del g
             del cps, base
         # the same projections with int4 LoRA factors (packed bytes read by

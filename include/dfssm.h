@@ -275,6 +275,22 @@ dfssm_status dfssm_chain_status(const dfssm_layer* layers, int n_layers, int64_t
 dfssm_status dfssm_chain_stream_floor(const dfssm_layer* layers, int n_layers, void* workspace,
                                       size_t workspace_bytes, void* stream);
 
+/* Diagnostic, not part of the computation: one launch that reads `bytes`
+ * bytes from the device buffer p (16-byte loads, every thread's loads issued
+ * before their first use, enough workgroups to cover the buffer at once).
+ * Each wave stores the XOR of the 32-bit words it read into its own word of
+ * sink, so the XOR of the first dfssm_read_floor_sink_words(bytes) words
+ * of sink is the XOR of the buffer's words.  Its duration is the floor
+ * under a single-launch linear whose weights take the same bytes (Table 13
+ * prices a decode linear by the bytes it moves).  bytes == 0 makes an empty
+ * launch: the launch floor.
+ *   p      16-byte aligned device buffer (may be NULL when bytes == 0)
+ *   sink   4-byte aligned device uint32 [sink_words]
+ * Errors: NULL, SHAPE (bytes not a multiple of 16), ALIGN, WORKSPACE (sink
+ * too small), DEVICE. */
+size_t dfssm_read_floor_sink_words(size_t bytes);
+dfssm_status dfssm_read_floor(const void* p, size_t bytes, uint32_t* sink, size_t sink_words, void* stream);
+
 /* The tied int8 embedding table (Sec. 3.3 and Table 1: the token embedding
  * is stored in int8 with one fp32 scale per row and shared with the LM
  * head):

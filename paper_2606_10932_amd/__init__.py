@@ -23,7 +23,7 @@ PATH_AUTO, PATH_DECODE, PATH_MFMA, PATH_MFMA_FEW = 0, 1, 2, 3
 EXPORTS = ["dfssm_quantize_act", "dfssm_linear_workspace_bytes", "dfssm_scaffold_lora_linear",
            "dfssm_scaffold_lora_linear_ex", "dfssm_chain_workspace_bytes",
            "dfssm_scaffold_lora_chain", "dfssm_chain_prepare", "dfssm_chain_run", "dfssm_chain_status",
-           "dfssm_chain_stream_floor",
+           "dfssm_chain_stream_floor", "dfssm_read_floor", "dfssm_read_floor_sink_words",
            "dfssm_embed_gather", "dfssm_lm_head", "dfssm_add_rmsnorm_quant", "dfssm_gate_norm_quant",
            "dfssm_ssm_step", "dfssm_linear_i4_workspace_bytes", "dfssm_scaffold_lora_linear_i4",
            "dfssm_mamba2_state_bytes", "dfssm_mamba2_workspace_bytes",
@@ -88,6 +88,10 @@ def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dfssm_chain_status.restype = i32
     lib.dfssm_chain_stream_floor.argtypes = [ctypes.POINTER(Layer), i32, vp, sz, vp]
     lib.dfssm_chain_stream_floor.restype = i32
+    lib.dfssm_read_floor.argtypes = [vp, sz, vp, sz, vp]
+    lib.dfssm_read_floor.restype = i32
+    lib.dfssm_read_floor_sink_words.argtypes = [sz]
+    lib.dfssm_read_floor_sink_words.restype = sz
     lib.dfssm_embed_gather.argtypes = [vp, vp, i64, i64, vp, i64, vp, vp]
     lib.dfssm_embed_gather.restype = i32
     lib.dfssm_lm_head.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp, vp]
@@ -334,6 +338,22 @@ def chain_stream_floor(layer_arr, workspace, stream=None):
     no exchange, no output) on a workspace prepared for these layers at M=1."""
     _check(lib.dfssm_chain_stream_floor(layer_arr, len(layer_arr), workspace.data_ptr(), workspace.numel(),
                                         _stream(stream)))
+
+
+def read_floor_sink_words(nbytes: int) -> int:
+    return int(lib.dfssm_read_floor_sink_words(int(nbytes)))
+
+
+def read_floor(buf, sink, nbytes=None, stream=None):
+    """Diagnostic: one launch reading nbytes (default: all) of the device
+    tensor buf; the XOR of sink's first read_floor_sink_words(nbytes) words
+    (int32, device) is then the XOR of the buffer's 32-bit words.  nbytes = 0
+    is an empty launch."""
+    torch = _torch()
+    _need(sink, torch.int32, "sink", 1)
+    n = buf.numel() * buf.element_size() if nbytes is None else int(nbytes)
+    _check(lib.dfssm_read_floor(buf.data_ptr() if n > 0 else None, n, sink.data_ptr(), sink.numel(),
+                                _stream(stream)))
 
 
 def embed_gather(E, scale, tok, x=None, stream=None):

@@ -537,6 +537,24 @@ dfssm_status dfssm_chain_stream_floor(const dfssm_layer* layers, int n_layers, v
   return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain stream launch");
 }
 
+size_t dfssm_read_floor_sink_words(size_t bytes) { return (size_t)dfssm::read_floor_sink_words((int64_t)bytes); }
+
+dfssm_status dfssm_read_floor(const void* p, size_t bytes, uint32_t* sink, size_t sink_words, void* stream) {
+  clear_error();
+  if (bytes % 16 != 0) return fail(DFSSM_ERR_SHAPE, "bytes=%zu must be a multiple of 16", bytes);
+  if (!sink) return fail(DFSSM_ERR_NULL, "sink is NULL");
+  if (sink_words < (size_t)dfssm::read_floor_sink_words((int64_t)bytes))
+    return fail(DFSSM_ERR_WORKSPACE, "sink holds %zu words < %lld needed", sink_words,
+                (long long)dfssm::read_floor_sink_words((int64_t)bytes));
+  if (reinterpret_cast<uintptr_t>(sink) % 4 != 0) return fail(DFSSM_ERR_ALIGN, "sink is not 4-byte aligned");
+  if (bytes > 0) {
+    const dfssm_status st = check_ptrs({{p, "p"}}, {});
+    if (st != DFSSM_OK) return st;
+  }
+  const hipError_t e = dfssm::launch_read_floor(p, (int64_t)bytes, sink, (hipStream_t)stream);
+  return e == hipSuccess ? DFSSM_OK : device_fail(e, "read floor launch");
+}
+
 dfssm_status dfssm_embed_gather(const int8_t* E, const float* scale, int64_t V, int64_t d, const int32_t* tok,
                                 int64_t M, float* x, void* stream) {
   clear_error();

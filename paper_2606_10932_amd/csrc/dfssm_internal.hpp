@@ -203,6 +203,12 @@ hipError_t step_fused_run(const StepFusedInfo& f, float eps, int64_t step, float
 
 hipError_t launch_zero_words(uint64_t* p, int64_t words, hipStream_t st);
 
+// One launch reading `bytes` (a multiple of 16) from p; the XOR of the
+// read_floor_sink_words(bytes) words it stores to sink is the XOR of every
+// 32-bit word read.  bytes == 0: an empty launch.
+int64_t read_floor_sink_words(int64_t bytes);
+hipError_t launch_read_floor(const void* p, int64_t bytes, uint32_t* sink, hipStream_t st);
+
 }  // namespace dfssm
 
 // ------------------------------------------------------------ device helpers

@@ -170,3 +170,20 @@ def test_chain_stream_floor_diagnostic(env):
     assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
     D.chain_stream_floor(arrs[1], wss[0])
     assert D.chain_status(arrs[1], 1, wss[0]) & 8
+
+
+@pytest.mark.parametrize("nbytes", [2923008, 1458176 + 48, 16, 0])
+def test_read_floor_diagnostic(env, nbytes):
+    """The read-floor diagnostic reads every byte: its sink is the XOR of
+    the buffer's 32-bit words (the 1.3B in_proj's and out_proj's weight
+    bytes, a ragged size, one word, an empty launch)."""
+    torch, D, o = env
+    say(f"read-floor diagnostic, {nbytes} bytes")
+    buf = np.random.default_rng(49).integers(0, 256, size=max(nbytes, 16), dtype=np.uint8)
+    d = dev(buf)
+    nw = D.read_floor_sink_words(nbytes)
+    sink = torch.zeros(nw, dtype=torch.int32, device="cuda")
+    D.read_floor(d, sink, nbytes=nbytes)
+    torch.cuda.synchronize()
+    want = np.bitwise_xor.reduce(buf[:nbytes].view(np.uint32)) if nbytes else np.uint32(0)
+    assert int(np.bitwise_xor.reduce(host(sink).view(np.uint32))) == int(want)

@@ -109,6 +109,16 @@ def test_chain_validation(dl):
     st = ctypes.c_uint(7)
     assert dl.lib.dfssm_chain_status(arr, 2, 1, 16, 8, ctypes.byref(st), None) == dl.ERR_WORKSPACE
     assert dl.lib.dfssm_chain_status(arr, 2, 1, 16, 1 << 30, None, None) == dl.ERR_NULL
+    # the read-floor diagnostic validates before any HIP call
+    rf = dl.lib.dfssm_read_floor
+    assert dl.lib.dfssm_read_floor_sink_words(2923008) == 4 * 357   # one word per wave
+    assert dl.lib.dfssm_read_floor_sink_words(0) == 4
+    assert rf(16, 17, 16, 4, None) == dl.ERR_SHAPE         # not a multiple of 16
+    assert rf(16, 32, None, 4, None) == dl.ERR_NULL        # no sink
+    assert rf(16, 32, 18, 4, None) == dl.ERR_ALIGN         # sink not 4-byte aligned
+    assert rf(16, 16 * 513, 16, 4, None) == dl.ERR_WORKSPACE   # two blocks: 8 words
+    assert rf(None, 32, 16, 4, None) == dl.ERR_NULL
+    assert rf(24, 32, 16, 4, None) == dl.ERR_ALIGN
     # the loads-only diagnostic: same validation; chains the persistent kernel
     # does not take (K = 64 here) are refused before any HIP call
     fs = dl.lib.dfssm_chain_stream_floor
