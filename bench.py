@@ -55,6 +55,7 @@ def parse():
     p.add_argument("--model-i4-batches", default="1,32",
                    help="batch sizes of the decode step figures with int4 LoRA factors")
     p.add_argument("--no-diag", action="store_true", help="skip the chain's stream and exchange floor diagnostics")
+    p.add_argument("--no-i4-sweep", action="store_true", help="skip the decode sweep with int4 LoRA factors")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="minimum CPU oracle sample time")
     p.add_argument("--cpu-single-seconds", type=float, default=4.0,
                    help="minimum single-thread CPU oracle sample time")
@@ -245,6 +246,47 @@ def main():
                 "us_per_sweep": round(tiny_ms * 1e3, 2), "us_per_linear": round(tiny_ms * 1e3 / 96, 3)},
         }
         del tarr, tws, ty
+
+    # ---- the same sweep with int4 LoRA factors (Table 4): 3 rotating copies,
+    #      the same persistent kernel reading the packed factors --------------
+    sweep_i4 = None
+    if not args.no_i4_sweep:
+        arrs4, wss4, keep4, bytes4 = [], [], [], 0
+        for c in range(args.copies):
+            hs4 = [S.weights_i4(K, N, 64, key=(70, i, c)) for i, (K, N) in enumerate(shapes)]
+            if c == 0:
+                bytes4 = sum(int(sum(ly[k].nbytes for k in ("w_bits", "alpha", "A4", "B4", "beta"))) for ly in hs4)
+            dl4 = [{k: dev(v) for k, v in ly.items()} for ly in hs4]
+            a4 = D.make_layers(dl4)
+            w4 = torch.zeros(D.chain_workspace_bytes(a4, M), dtype=torch.uint8, device="cuda")
+            D.chain_prepare(a4, M, w4)
+            arrs4.append(a4)
+            wss4.append(w4)
+            keep4.append(dl4)
+            del hs4
+        for i in range(max(args.warmup, 2)):
+            D.chain_run(arrs4[i % len(arrs4)], q0, s0, y_all, wss4[i % len(arrs4)], stream=stream)
+        ev4 = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for i in range(args.steps):
+            ev4[i][0].record(stream)
+            D.chain_run(arrs4[i % len(arrs4)], q0, s0, y_all, wss4[i % len(arrs4)], stream=stream)
+            ev4[i][1].record(stream)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        ms4 = t0.elapsed_time(t1) / args.steps
+        launch4 = float(np.mean([a.elapsed_time(b) for a, b in ev4]))
+        if max(D.chain_status(arrs4[c], M, wss4[c]) for c in range(len(arrs4))):
+            print("int4 chain status word set: a bounded wait gave up", file=sys.stderr)
+            sys.exit(3)
+        sweep_i4 = {"workload": "Mamba-2-1.3B decode sweep, M=1, 96 linears, int4 LoRA factors r=64, "
+                                f"{len(arrs4)} weight copies rotated",
+                    "ms_per_step": round(ms4, 4), "avg_launch_us": round(launch4 * 1e3, 2),
+                    "weight_bytes": bytes4, "gbs": round(bytes4 / (ms4 * 1e-3) / 1e9, 1),
+                    "frac_hbm_peak": round(bytes4 / (ms4 * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                    "int8_sweep_ms_per_step": round(ms, 4)}
+        del arrs4, wss4, keep4
 
     # ---- prefill: 2048-token in_proj -----------------------------------------
     prefill = None
@@ -682,6 +724,7 @@ def main():
         "decode_step": model_fig,
         "cpu_baseline": cpu,
         "diagnostics": diag,
+        "sweep_int4_lora": sweep_i4,
     }
     print(json.dumps(out), flush=True)
 

@@ -196,6 +196,11 @@ typedef struct {
   const int8_t* B;
   const float* beta;
   int64_t K, N, r;
+  int64_t lora_bits;  /* 0 or 8: A [r][K] and B [N][r] int8; 4: A and B are
+                         packed int4 (Table 4): A [r][K/2], B [N][r/2] bytes
+                         of two's-complement nibbles, value 2i in the low
+                         nibble of byte i (as dfssm_scaffold_lora_linear_i4);
+                         r even */
 } dfssm_layer;
 
 /* Bytes of device workspace dfssm_scaffold_lora_chain needs. */
@@ -210,7 +215,10 @@ size_t dfssm_chain_workspace_bytes(const dfssm_layer* layers, int n_layers, int6
  *   every token, standing in for the normalisation between projections.
  * Requires K_l <= N_{l-1}.  y_all (device) receives every linear's y back
  * to back: sum_l M*N_l floats, linear l at offset sum_{i<l} M*N_i.
- * `layers` is a HOST array of n_layers entries.  M must be 1..4.
+ * `layers` is a HOST array of n_layers entries.  M must be 1..4.  Layers
+ * may mix int8 and packed int4 LoRA factors (lora_bits); at M = 1 the
+ * persistent kernel takes int4 layers with r % 8 == 0, others run the
+ * host-sequenced path.
  * Equivalent to dfssm_chain_prepare followed by dfssm_chain_run.
  * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */
 dfssm_status dfssm_scaffold_lora_chain(const dfssm_layer* layers, int n_layers, int64_t M,

@@ -220,6 +220,21 @@ class Oracle:
         B = self.unpack_int4(B4, N * r).reshape(N, r)
         return self.linear(q, s, w_bits, alpha, A, B, beta)
 
+    def chain_i4(self, layers, q0, s0):
+        """The chain whose layers carry int4 LoRA factors (A4, B4; or int8
+        A, B): the chain on the unpacked factors, as linear_i4 (Table 4
+        keeps the LoRA arithmetic and only narrows the stored factors)."""
+        out = []
+        for ly in layers:
+            if ly.get("A4") is None:
+                out.append(ly)
+                continue
+            K, N, r = ly["w_bits"].shape[1] * 32, ly["w_bits"].shape[0], ly["A4"].shape[0]
+            out.append(dict(w_bits=ly["w_bits"], alpha=ly["alpha"], beta=ly["beta"],
+                            A=self.unpack_int4(ly["A4"], r * K).reshape(r, K),
+                            B=self.unpack_int4(ly["B4"], N * r).reshape(N, r)))
+        return self.chain(out, q0, s0)
+
     # ---- Mamba-2 decode step around the linears ----------------------------
     def add_rmsnorm_quant(self, u, w, eps, delta=None):
         """Returns (u_out, o, Q, s): u_out = u + delta, o = rmsnorm(u_out) * w

@@ -43,7 +43,7 @@ class Layer(ctypes.Structure):
     """dfssm_layer: one projection of a chain (device pointers + sizes)."""
     _fields_ = [("w_bits", ctypes.c_void_p), ("alpha", ctypes.c_void_p), ("A", ctypes.c_void_p),
                 ("B", ctypes.c_void_p), ("beta", ctypes.c_void_p), ("K", ctypes.c_int64),
-                ("N", ctypes.c_int64), ("r", ctypes.c_int64)]
+                ("N", ctypes.c_int64), ("r", ctypes.c_int64), ("lora_bits", ctypes.c_int64)]
 
 
 class Mamba2Layer(ctypes.Structure):
@@ -279,11 +279,7 @@ def make_layers(layers: Sequence[dict]):
     holds references to the tensors, so their memory lives as long as it."""
     arr = (Layer * len(layers))()
     for i, ly in enumerate(layers):
-        r = 0 if ly.get("A") is None else ly["A"].shape[0]
-        arr[i] = Layer(ly["w_bits"].data_ptr(), ly["alpha"].data_ptr(),
-                       ly["A"].data_ptr() if r else None, ly["B"].data_ptr() if r else None,
-                       ly["beta"].data_ptr() if r else None, ly["w_bits"].shape[1] * 32,
-                       ly["w_bits"].shape[0], r)
+        arr[i] = _proj(ly)
     arr._tensors = [dict(ly) for ly in layers]
     return arr
 
@@ -540,11 +536,14 @@ class Mamba2:
 
 
 def _proj(w) -> Layer:
-    A = w.get("A4", w.get("A"))
-    B = w.get("B4", w.get("B"))
+    """dfssm_layer of a projection: int8 factors A, B or packed int4 A4, B4."""
+    i4 = w.get("A4") is not None
+    A = w.get("A4") if i4 else w.get("A")
+    B = w.get("B4") if i4 else w.get("B")
     r = 0 if A is None else A.shape[0]
     return Layer(w["w_bits"].data_ptr(), w["alpha"].data_ptr(), _ptr(A) if r else None, _ptr(B) if r else None,
-                 _ptr(w.get("beta")) if r else None, w["w_bits"].shape[1] * 32, w["w_bits"].shape[0], r)
+                 _ptr(w.get("beta")) if r else None, w["w_bits"].shape[1] * 32, w["w_bits"].shape[0], r,
+                 4 if i4 else 0)
 
 
 def scaffold_lora_linear_i4(q, s, w_bits, alpha, A4=None, B4=None, beta=None, y=None, workspace=None,

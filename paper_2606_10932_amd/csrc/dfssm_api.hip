@@ -398,6 +398,10 @@ static dfssm_status validate_chain(const dfssm_layer* layers, int n_layers, int6
       return fail(st, "layer %d: %s", l, why);
     }
     if (L.N <= 0) return fail(DFSSM_ERR_SHAPE, "layer %d: N must be > 0", l);
+    if (L.lora_bits != 0 && L.lora_bits != 8 && L.lora_bits != 4)
+      return fail(DFSSM_ERR_SHAPE, "layer %d: lora_bits=%lld: 8 (or 0) or 4", l, (long long)L.lora_bits);
+    if (L.lora_bits == 4 && L.r % 2 != 0)
+      return fail(DFSSM_ERR_SHAPE, "layer %d: r=%lld must be even for packed int4 factors", l, (long long)L.r);
     if (l > 0 && L.K > layers[l - 1].N)
       return fail(DFSSM_ERR_SHAPE, "layer %d: K=%lld > previous N=%lld", l, (long long)L.K,
                   (long long)layers[l - 1].N);
@@ -480,8 +484,14 @@ dfssm_status dfssm_chain_run(const dfssm_layer* layers, int n_layers, int64_t M,
       sl = sbuf;
     }
     dfssm::LinearWorkspace ws = dfssm::carve_linear_workspace(base + c.off_lin, M, L.K, L.r);
-    hipError_t e = launch_linear(DFSSM_PATH_AUTO, ql, sl, M, L.K, L.N, L.r, L.w_bits, L.alpha, L.A, L.B,
-                                 L.beta, y_cur, nullptr, nullptr, nullptr, ws, hs);
+    // M <= 4: int4 factors go to the few-token kernel, which reads them packed
+    hipError_t e = L.lora_bits == 4 && L.r > 0
+                       ? dfssm::launch_skinny_linear_i4(ql, sl, M, L.K, L.N, L.r, L.w_bits, L.alpha,
+                                                        reinterpret_cast<const uint8_t*>(L.A),
+                                                        reinterpret_cast<const uint8_t*>(L.B), L.beta, y_cur,
+                                                        nullptr, nullptr, nullptr, ws, hs)
+                       : launch_linear(DFSSM_PATH_AUTO, ql, sl, M, L.K, L.N, L.r, L.w_bits, L.alpha, L.A, L.B,
+                                       L.beta, y_cur, nullptr, nullptr, nullptr, ws, hs);
     if (e != hipSuccess) return device_fail(e, "chain linear launch");
     y_prev = y_cur;
     y_cur += M * L.N;
@@ -700,6 +710,9 @@ dfssm_status check_model_pointers(const dfssm_mamba2_model* md, const ModelDims&
       if (st == DFSSM_OK && L.lora_bits == 4 && P.r % 2 != 0)
         st = fail(DFSSM_ERR_SHAPE, "%s: r=%lld must be even for packed int4 factors", i ? "out_proj" : "in_proj",
                   (long long)P.r);
+      if (st == DFSSM_OK && P.lora_bits != 0 && (P.lora_bits == 4) != (L.lora_bits == 4))
+        st = fail(DFSSM_ERR_SHAPE, "%s: lora_bits=%lld differs from the layer's %lld", i ? "out_proj" : "in_proj",
+                  (long long)P.lora_bits, (long long)L.lora_bits);
       if (st == DFSSM_OK) st = check_ptrs({{P.w_bits, "w_bits"}, {P.alpha, "alpha"}}, {});
       if (st == DFSSM_OK && P.r > 0) st = check_ptrs({{P.A, "A"}, {P.B, "B"}, {P.beta, "beta"}}, {});
     }

@@ -102,6 +102,7 @@ struct Layer {
   int32_t us, ub;          // direct-to-LDS units (bytes) of the sign rows and B rows
   int32_t o_a, o_b, o_al, o_be;  // operand offsets inside a ring slot (sign rows at 0)
   int32_t rh;              // LoRA ranks per row group: ceil(r / 4)
+  int32_t i4;              // 1: A and B are packed int4 (A [r][K/2], B [N][r/2] bytes)
   int64_t y_off;           // this linear's outputs in y_all
   int64_t part_off;        // words: [8][N] slice partials of acc_s (XCD-local)
   int64_t p_off;           // words: [8 XCDs][8 slices][64] partials of acc_a (XCD-local)
@@ -155,30 +156,33 @@ __device__ int issue_batch(const Layer& L, int x, int kap, int h, int lam, uint3
     }
     n_issued += ni;
   }
-  {  // A rows h*rh .. h*rh + rh - 1, columns of the slice (16-byte units)
-    const int upr = Ks >> 4, nunits = L.rh * upr, ni = (nunits + 63) >> 6;
+  {  // A rows h*rh .. h*rh + rh - 1, columns of the slice (16-byte units;
+     // int4: the slice's Ks/2 bytes of each row)
+    const int sb_a = L.i4 ? Ks >> 1 : Ks, rowb = L.i4 ? K >> 1 : K;
+    const int upr = sb_a >> 4, nunits = L.rh * upr, ni = (nunits + 63) >> 6;
     const uint32_t m = recip20((uint32_t)upr);
     for (int t = 0; t < ni; ++t) {
       const int u = 64 * t + lane;
       uint32_t voff = 0;
       if (u < nunits) {
         const int jj = udiv(u, m), q = u - jj * upr, j = h * L.rh + jj;
-        if (j < L.r) voff = (uint32_t)((int64_t)j * K + kap * Ks + 16 * q);
+        if (j < L.r) voff = (uint32_t)((int64_t)j * rowb + kap * sb_a + 16 * q);
       }
       lds_dma16(voff, L.A, sb + (uint32_t)(L.o_a + 1024 * t));
     }
     n_issued += ni;
   }
   const int R = reducer_rows(L, x, lam);
-  if (L.r > 0) {  // B rows of the reducer's rows
-    const int ub = L.ub, upr = L.r / ub, nunits = R * upr, ni = (nunits + 63) >> 6;
+  if (L.r > 0) {  // B rows of the reducer's rows (int4: r/2 bytes each)
+    const int rb = L.i4 ? L.r >> 1 : L.r;
+    const int ub = L.ub, upr = rb / ub, nunits = R * upr, ni = (nunits + 63) >> 6;
     const uint32_t m = recip20((uint32_t)upr);
     for (int t = 0; t < ni; ++t) {
       const int u = 64 * t + lane;
       uint32_t voff = 0;
       if (u < nunits) {
         const int i = udiv(u, m), q = u - i * upr;
-        voff = (uint32_t)((int64_t)reducer_row(L, x, lam, i) * L.r + q * ub);
+        voff = (uint32_t)((int64_t)reducer_row(L, x, lam, i) * rb + q * ub);
       }
       lds_dma(ub, voff, L.B, sb + (uint32_t)(L.o_b + 64 * ub * t));
     }
@@ -415,11 +419,23 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
       if (rh > 0) {
         // all reads first (rows past rh read row 0, lanes past the slice
         // column 0; their products are dropped)
-        const uint8_t* arow = slot + Ld.o_a + (8 * lane < Ks ? 8 * lane : 0);
-        uint2 aw[kMaxRh];
-#pragma unroll
-        for (int jj = 0; jj < kMaxRh; ++jj) aw[jj] = *reinterpret_cast<const uint2*>(arow + (jj < rh ? jj : 0) * Ks);
         const bool inb = 8 * lane < Ks;
+        uint2 aw[kMaxRh];
+        if (Ld.i4) {
+          // 4 bytes (8 nibbles) per rank and lane, expanded to the int8 pair
+          const uint8_t* arow = slot + Ld.o_a + (inb ? 4 * lane : 0);
+          uint32_t a4[kMaxRh];
+#pragma unroll
+          for (int jj = 0; jj < kMaxRh; ++jj)
+            a4[jj] = *reinterpret_cast<const uint32_t*>(arow + (jj < rh ? jj : 0) * (Ks >> 1));
+#pragma unroll
+          for (int jj = 0; jj < kMaxRh; ++jj) unpack_i4x8(a4[jj], aw[jj].x, aw[jj].y);
+        } else {
+          const uint8_t* arow = slot + Ld.o_a + (inb ? 8 * lane : 0);
+#pragma unroll
+          for (int jj = 0; jj < kMaxRh; ++jj)
+            aw[jj] = *reinterpret_cast<const uint2*>(arow + (jj < rh ? jj : 0) * Ks);
+        }
 #pragma unroll
         for (int jj = 0; jj < kMaxRh; ++jj)
           red[lane * 17 + jj] = inb ? sdot4(aw[jj].y, cq1, sdot4(aw[jj].x, cq0, 0)) : 0;
@@ -472,10 +488,20 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
       const int R = reducer_rows(Ld, x, lam);
       // the row's operands (LDS reads issued together, before the poll)
       const int rw = r >> 2;
-      const uint32_t* brow = reinterpret_cast<const uint32_t*>(slot + Ld.o_b + (lane < R ? lane : 0) * r);
       uint32_t bw[kMaxR / 4];
+      if (Ld.i4) {
+        // r/2 bytes per row: each dword is 8 nibbles, two dwords of int8
+        const uint32_t* brow = reinterpret_cast<const uint32_t*>(slot + Ld.o_b + (lane < R ? lane : 0) * (r >> 1));
+        uint32_t b4[kMaxR / 8];
 #pragma unroll
-      for (int w = 0; w < kMaxR / 4; ++w) bw[w] = w < rw ? brow[w] : 0u;
+        for (int w = 0; w < kMaxR / 8; ++w) b4[w] = 2 * w < rw ? brow[w] : 0u;
+#pragma unroll
+        for (int w = 0; w < kMaxR / 8; ++w) unpack_i4x8(b4[w], bw[2 * w], bw[2 * w + 1]);
+      } else {
+        const uint32_t* brow = reinterpret_cast<const uint32_t*>(slot + Ld.o_b + (lane < R ? lane : 0) * r);
+#pragma unroll
+        for (int w = 0; w < kMaxR / 4; ++w) bw[w] = w < rw ? brow[w] : 0u;
+      }
       const float al = reinterpret_cast<const float*>(slot + Ld.o_al)[lane];
       const float be = reinterpret_cast<const float*>(slot + Ld.o_be)[lane];
       const int n = lane < R ? reducer_row(Ld, x, lam, lane) : 0;
@@ -624,7 +650,9 @@ Plan make_plan(const dfssm_layer* layers, int n) {
     const int64_t K = D.K, N = D.N, r = D.r;
     const int64_t Nc = l + 1 < n ? layers[l + 1].K : 0;
     // (N >= 4: at rank 0 the A loads read 16 bytes of alpha)
-    if (K % 256 != 0 || K > 8 * kMaxKs || r < 0 || r > kMaxR || r % 4 != 0 || N < 4 || Nc > N) return p;
+    const bool i4 = D.lora_bits == 4 && r > 0;
+    if (K % 256 != 0 || K > 8 * kMaxKs || r < 0 || r > kMaxR || r % (i4 ? 8 : 4) != 0 || N < 4 || Nc > N)
+      return p;
     if (Nc % kGrid != 0) return p;
     const int64_t cpr = Nc / kGrid, T = N - Nc, tq = T / kGrid, trem = T % kGrid;
     const int64_t rmax = cpr + tq + (trem > 0 ? 1 : 0);
@@ -632,9 +660,11 @@ Plan make_plan(const dfssm_layer* layers, int n) {
     const int64_t na_max = kSlices * cpr + kSlices * tq + std::min<int64_t>(kSlices, trem);
     const int64_t rowbytes = K / 64, us = rowbytes % 16 == 0 ? 16 : 4;
     const int64_t sign_ni = dfssm::ceil_div(na_max * (rowbytes / us), 64);
-    const int64_t a_ni = dfssm::ceil_div(((r + kRankGroups - 1) / kRankGroups) * (K / 8) / 16, 64);
-    const int64_t ub = r % 16 == 0 ? 16 : 4;
-    const int64_t b_ni = r > 0 ? dfssm::ceil_div(rmax * (r / ub), 64) : 0;
+    // int4: half the A slice bytes (Ks/2 per rank) and half the B row bytes
+    const int64_t a_ni = dfssm::ceil_div(((r + kRankGroups - 1) / kRankGroups) * (K / 8) / (i4 ? 32 : 16), 64);
+    const int64_t rb = i4 ? r / 2 : r;
+    const int64_t ub = rb % 16 == 0 ? 16 : 4;
+    const int64_t b_ni = r > 0 ? dfssm::ceil_div(rmax * (rb / ub), 64) : 0;
     if (sign_ni + a_ni + b_ni + 2 > kNB) return p;
     const int64_t o_a = sign_ni * 64 * us, o_b = o_a + a_ni * 1024, o_al = o_b + b_ni * 64 * ub,
                   o_be = o_al + 256;
@@ -661,6 +691,7 @@ Plan make_plan(const dfssm_layer* layers, int n) {
     e.o_al = (int32_t)o_al;
     e.o_be = (int32_t)o_be;
     e.rh = (int32_t)((r + kRankGroups - 1) / kRankGroups);
+    e.i4 = i4 ? 1 : 0;
     e.y_off = y_off;
     y_off += N;
     e.part_off = w;

@@ -42,6 +42,17 @@ __device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
 // at most 127 * (1 + 2^-23)^2 < 127.5, so rint() already lands in [-127, 127]
 // and the clamp of the definition never changes the result.
 __device__ __forceinline__ int code(float v, float inv) { return (int)rintf(v * inv); }
+// Eight two's-complement nibbles (value 2i in the low nibble of byte i) as
+// two dwords of int8, values 0..3 in x and 4..7 in y: v_perm interleaves
+// the low and high nibbles, then bit 3 of each byte is spread over its high
+// half (0x08 * 0x1E = 0xF0, no carry between bytes).
+__device__ __forceinline__ void unpack_i4x8(uint32_t w, uint32_t& x, uint32_t& y) {
+  const uint32_t lo = w & 0x0F0F0F0Fu, hi = (w >> 4) & 0x0F0F0F0Fu;
+  x = __builtin_amdgcn_perm(hi, lo, 0x05010400u);
+  y = __builtin_amdgcn_perm(hi, lo, 0x07030602u);
+  x |= (x & 0x08080808u) * 0x1Eu;
+  y |= (y & 0x08080808u) * 0x1Eu;
+}
 
 __device__ __forceinline__ int dpp_sum16(int v) {
   v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]

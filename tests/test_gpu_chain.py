@@ -187,3 +187,43 @@ def test_read_floor_diagnostic(env, nbytes):
     torch.cuda.synchronize()
     want = np.bitwise_xor.reduce(buf[:nbytes].view(np.uint32)) if nbytes else np.uint32(0)
     assert int(np.bitwise_xor.reduce(host(sink).view(np.uint32))) == int(want)
+
+
+def _check_chain_i4(env, spec, M, key):
+    """A chain whose layers (K, N, r, bits) carry int4 (bits 4) or int8 LoRA
+    factors, against the oracle chain on the unpacked factors."""
+    torch, D, o = env
+    layers = [S.weights_i4(K, N, r, key=(21, key, i)) if bits == 4 else S.weights(K, N, r, key=(21, key, i))
+              for i, (K, N, r, bits) in enumerate(spec)]
+    x = S.activations(M, spec[0][0], key=(21, key))
+    q0, s0 = o.quantize_act(x)
+    ys_ref, _ = o.chain_i4(layers, q0, s0)
+    dl = [{k: dev(v) for k, v in ly.items()} if "A4" in ly else dev_weights(ly) for ly in layers]
+    ys = D.scaffold_lora_chain(dl, dev(q0), dev(s0))
+    torch.cuda.synchronize()
+    for l, (yg, yr) in enumerate(zip(ys, ys_ref)):
+        yg = host(yg)
+        bad = np.flatnonzero(yg.view(np.uint32) != yr.view(np.uint32))
+        assert bad.size == 0, f"linear {l}: {bad.size} values differ"
+
+
+def test_chain_int4_sweep_full(env):
+    """The full 1.3B decode sweep with int4 LoRA factors (Table 4), r = 64,
+    in the persistent kernel: every linear bit-exact."""
+    say("chain full 1.3B sweep, int4 LoRA")
+    _check_chain_i4(env, [(K, N, 64, 4) for K, N in S.sweep_shapes(48)], M=1, key=90)
+
+
+@pytest.mark.parametrize("case", ["ragged", "r12", "mixed1", "mixed2"])
+def test_chain_int4_shapes(env, case):
+    """int4 factors at ranks 8, 16, 24 with ragged N and the largest reducer
+    share (persistent kernel); at r = 12 (host-sequenced: the persistent
+    kernel takes int4 at r % 8 == 0); int4 and int8 layers mixed, with a
+    rank-0 int4 layer, at M = 1 and 2."""
+    spec = {"ragged": [(256, 4000, 8, 4), (3840, 2048, 16, 4), (2048, 16384, 24, 4), (4096, 130, 8, 4)],
+            "r12": [(512, 1300, 12, 4), (1280, 777, 12, 4)],
+            "mixed1": [(2048, 8512, 64, 4), (4096, 2048, 64, 8), (2048, 8512, 32, 4), (4096, 2048, 0, 4)],
+            "mixed2": [(2048, 8512, 64, 4), (4096, 2048, 64, 8), (2048, 8512, 32, 4), (4096, 2048, 0, 4)]}[case]
+    M = 2 if case == "mixed2" else 1
+    say(f"chain with int4 LoRA: {case}, M={M}")
+    _check_chain_i4(env, spec, M=M, key=91 + len(case))
