@@ -480,11 +480,11 @@ size_t dfssm_mamba2_workspace_bytes(const dfssm_mamba2_model* model, int64_t M);
  * layer's projections of those shapes; M >= 1; vocab >= 1.
  * The fused step: at M = 1, on a workspace that dfssm_mamba2_prepare has
  * prepared for this model, and for models of the 1.3B layer shape (d_model
- * 2048, d_state 128, int8 LoRA factors with r <= 64 and r % 4 == 0 in
- * every projection), the layers run as one persistent launch of one
- * workgroup per compute unit (between the gather and the final norm and LM
- * head), with the same arithmetic; every other case runs the per-kernel
- * sequence above.  The fused launch needs the whole grid resident at once;
+ * 2048, d_state 128, LoRA factors with r <= 64 in every projection and
+ * r % 4 == 0 for int8, r % 8 == 0 for int4), the layers run as one
+ * persistent launch of one workgroup per compute unit (between the gather
+ * and the final norm and LM head), with the same arithmetic; every other
+ * case runs the per-kernel sequence above.  The fused launch needs the whole grid resident at once;
  * its waits are bounded and record a status bit (dfssm_mamba2_status) if
  * they give up, after which that step's outputs are incomplete.
  * Errors: NULL, SHAPE, ALIGN, WORKSPACE, UNSUPPORTED, DEVICE. */

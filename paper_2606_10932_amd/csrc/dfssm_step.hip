@@ -98,6 +98,7 @@ struct StepLin {
   int32_t o_st, o_rg, o_rb, o_cw, o_cb, o_hp;  // in_proj: SSM state, convolution windows (x channels, own
                                               // B/C channel), conv_w, conv_b, head parameters
   int32_t layer;
+  int32_t i4;        // 1: A and B are packed int4 (A [r][K/2], B [N][r/2] bytes)
   int64_t part_off;  // XCD-local words [8 slices][N]: row partials
   int64_t p_off;     // XCD-local words [8 XCDs][8 slices][64]: rank partials
   int64_t mx_off;    // XCD-local words [8 XCDs][4 row groups][8 slices]: slice maxima
@@ -188,29 +189,31 @@ __device__ void step_batch(const StepLin& L, int x, int kap, int h, int lam, int
       lds_dma(us, voff, L.w_bits, sb + (uint32_t)(64 * us * tt));
     }
   }
-  if (L.rh > 0) {  // A rows h*rh .. h*rh + rh - 1, the slice's columns
-    const int upr = Ks >> 4, nunits = L.rh * upr, ni = (nunits + 63) >> 6;
+  if (L.rh > 0) {  // A rows h*rh .. h*rh + rh - 1, the slice's columns (int4: Ks/2 bytes)
+    const int sb_a = L.i4 ? Ks >> 1 : Ks, rowb = L.i4 ? K >> 1 : K;
+    const int upr = sb_a >> 4, nunits = L.rh * upr, ni = (nunits + 63) >> 6;
     const uint32_t m = recip20((uint32_t)upr);
     for (int tt = 0; tt < ni; ++tt) {
       const int u = 64 * tt + lane;
       uint32_t voff = 0;
       if (u < nunits) {
         const int jj = udiv(u, m), q = u - jj * upr, j = h * L.rh + jj;
-        if (j < L.r) voff = (uint32_t)((int64_t)j * K + kap * Ks + 16 * q);
+        if (j < L.r) voff = (uint32_t)((int64_t)j * rowb + kap * sb_a + 16 * q);
       }
       lds_dma16(voff, L.A, sb + (uint32_t)(L.o_a + 1024 * tt));
     }
   }
   const int R = reducer_rows(L.kind, g);
-  if (L.r > 0) {  // B rows of the reducer's rows
-    const int ub = L.ub, upr = L.r / ub, nunits = R * upr, ni = (nunits + 63) >> 6;
+  if (L.r > 0) {  // B rows of the reducer's rows (int4: r/2 bytes each)
+    const int rb = L.i4 ? L.r >> 1 : L.r;
+    const int ub = L.ub, upr = rb / ub, nunits = R * upr, ni = (nunits + 63) >> 6;
     const uint32_t m = recip20((uint32_t)upr);
     for (int tt = 0; tt < ni; ++tt) {
       const int u = 64 * tt + lane;
       uint32_t voff = 0;
       if (u < nunits) {
         const int i = udiv(u, m), q = u - i * upr;
-        voff = (uint32_t)((int64_t)reducer_row(L.kind, g, i) * L.r + q * ub);
+        voff = (uint32_t)((int64_t)reducer_row(L.kind, g, i) * rb + q * ub);
       }
       lds_dma(ub, voff, L.B, sb + (uint32_t)(L.o_b + 64 * ub * tt));
     }
@@ -730,11 +733,23 @@ __global__ __launch_bounds__(kThreads, 1) void step_persistent(
       // ---- LoRA down-projection inside the XCD (as the chain)
       const int rh = Ld.rh;
       if (rh > 0) {
-        const uint8_t* arow = slot + Ld.o_a + (8 * lane < Ks ? 8 * lane : 0);
-        uint2 aw[kMaxRh];
-#pragma unroll
-        for (int jj = 0; jj < kMaxRh; ++jj) aw[jj] = *reinterpret_cast<const uint2*>(arow + (jj < rh ? jj : 0) * Ks);
         const bool inb = 8 * lane < Ks;
+        uint2 aw[kMaxRh];
+        if (Ld.i4) {
+          // 4 bytes (8 nibbles) per rank and lane, expanded to the int8 pair
+          const uint8_t* arow = slot + Ld.o_a + (inb ? 4 * lane : 0);
+          uint32_t a4[kMaxRh];
+#pragma unroll
+          for (int jj = 0; jj < kMaxRh; ++jj)
+            a4[jj] = *reinterpret_cast<const uint32_t*>(arow + (jj < rh ? jj : 0) * (Ks >> 1));
+#pragma unroll
+          for (int jj = 0; jj < kMaxRh; ++jj) unpack_i4x8(a4[jj], aw[jj].x, aw[jj].y);
+        } else {
+          const uint8_t* arow = slot + Ld.o_a + (inb ? 8 * lane : 0);
+#pragma unroll
+          for (int jj = 0; jj < kMaxRh; ++jj)
+            aw[jj] = *reinterpret_cast<const uint2*>(arow + (jj < rh ? jj : 0) * Ks);
+        }
 #pragma unroll
         for (int jj = 0; jj < kMaxRh; ++jj)
           red[lane * 17 + jj] = inb ? sdot4(aw[jj].y, cq1, sdot4(aw[jj].x, cq0, 0)) : 0;
@@ -782,10 +797,20 @@ __global__ __launch_bounds__(kThreads, 1) void step_persistent(
       STEP_WAIT_FLAG(FLAG(rows_done) >= kAWaves * (ju + 1), sp, kStAcc);
       const int R = reducer_rows(Ld.kind, g);
       const int rw = r >> 2;
-      const uint32_t* brow = reinterpret_cast<const uint32_t*>(slot + Ld.o_b + (lane < R ? lane : 0) * r);
       uint32_t bw[kMaxR / 4];
+      if (Ld.i4) {
+        // r/2 bytes per row: each dword is 8 nibbles, two dwords of int8
+        const uint32_t* brow = reinterpret_cast<const uint32_t*>(slot + Ld.o_b + (lane < R ? lane : 0) * (r >> 1));
+        uint32_t b4[kMaxR / 8];
 #pragma unroll
-      for (int w = 0; w < kMaxR / 4; ++w) bw[w] = w < rw ? brow[w] : 0u;
+        for (int w = 0; w < kMaxR / 8; ++w) b4[w] = 2 * w < rw ? brow[w] : 0u;
+#pragma unroll
+        for (int w = 0; w < kMaxR / 8; ++w) unpack_i4x8(b4[w], bw[2 * w], bw[2 * w + 1]);
+      } else {
+        const uint32_t* brow = reinterpret_cast<const uint32_t*>(slot + Ld.o_b + (lane < R ? lane : 0) * r);
+#pragma unroll
+        for (int w = 0; w < kMaxR / 4; ++w) bw[w] = w < rw ? brow[w] : 0u;
+      }
       const float al = reinterpret_cast<const float*>(slot + Ld.o_al)[lane];
       const float be = reinterpret_cast<const float*>(slot + Ld.o_be)[lane];
       const int n = lane < R ? reducer_row(Ld.kind, g, lane) : 0;
@@ -913,11 +938,11 @@ StepPlan make_step_plan(const dfssm_mamba2_model* md) {
   int64_t w = 0;
   for (int l = 0; l < n; ++l) {
     const dfssm_mamba2_layer& ML = md->layers[l];
-    if (ML.lora_bits == 4) return p;
     for (int kind = 0; kind < 2; ++kind) {
       const dfssm_layer& P = kind == 0 ? ML.in_proj : ML.out_proj;
       const int64_t K = kind == 0 ? kD : kDi, N = kind == 0 ? kNin : kD, r = P.r;
-      if (P.K != K || P.N != N || r < 0 || r > kMaxR || r % 4 != 0) return p;
+      const bool i4 = ML.lora_bits == 4 && r > 0;
+      if (P.K != K || P.N != N || r < 0 || r > kMaxR || r % (i4 ? 8 : 4) != 0) return p;
       StepLin& e = p.table[2 * l + kind];
       std::memset(&e, 0, sizeof(e));
       const bool lr = r > 0;
@@ -940,11 +965,13 @@ StepPlan make_step_plan(const dfssm_mamba2_model* md) {
       e.rs = kind == 0 ? kInSlots : kOutRows;
       const int64_t rowbytes = K / 64, Ks = K / 8;
       e.us = rowbytes % 16 == 0 ? 16 : 4;
-      e.ub = r % 16 == 0 ? 16 : 4;
+      e.i4 = i4 ? 1 : 0;
+      const int64_t rb = i4 ? r / 2 : r;  // B row bytes
+      e.ub = rb % 16 == 0 ? 16 : 4;
       const int64_t rmax = kind == 0 ? kInSlots : kOutRows;
       const int64_t sign_ni = cdiv(kSlices * e.rs * (rowbytes / e.us), 64);
-      const int64_t a_ni = cdiv(e.rh * Ks / 16, 64);
-      const int64_t b_ni = lr ? cdiv(rmax * (r / e.ub), 64) : 0;
+      const int64_t a_ni = cdiv(e.rh * Ks / (i4 ? 32 : 16), 64);
+      const int64_t b_ni = lr ? cdiv(rmax * (rb / e.ub), 64) : 0;
       const int64_t nw_ni = cdiv(Ks / 4, 64);
       int64_t o = sign_ni * 64 * e.us;
       e.o_a = (int32_t)o;

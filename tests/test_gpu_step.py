@@ -197,3 +197,36 @@ def test_fused_step_one_and_two_exchanges(env, model3, tied, record_property):
     assert np.array_equal(host(state), host(state2))
     say(f"  {exact} of {len(toks)} tokens bit-exact against the oracle")
     record_property("bit_exact_tokens", f"{exact}/{len(toks)}")
+
+
+def test_fused_step_int4_lora(env, model3, record_property):
+    """The fused step with int4 LoRA factors (Table 4) in every projection
+    (r = 64, 8 and 16): against the oracle and the per-kernel step."""
+    torch, D, o = env
+    T = 4
+    md = dict(model3)
+    md["layers"] = [dict({k: v for k, v in ly.items() if k not in ("in_proj", "out_proj")},
+                         in_proj=S.weights_i4(2048, 8512, (64, 8, 16)[l], key=(168, l, 0)),
+                         out_proj=S.weights_i4(4096, 2048, (64, 16, 8)[l], key=(168, l, 1)))
+                    for l, ly in enumerate(model3["layers"])]
+    say(f"fused decode step with int4 LoRA, 3 layers, M=1, {T} tokens")
+    m = device_model(D, md)
+    ring, state = m.new_state(1)
+    ws = m.workspace(1)
+    ring_k, state_k = m.new_state(1)
+    ws_k = m.workspace(1)
+    assert m.fused_path(1, ws)
+    om = OracleModel(o, md, 1)
+    exact = same = 0
+    for t in range(T):
+        tok = S.tokens(1, V, key=(169, t))
+        lg = host(m.decode_step(dev(tok), t, ring, state, ws))
+        with forced_switch(D, D.TEST_STEP_PER_KERNEL, 1):
+            lk = host(m.decode_step(dev(tok), t, ring_k, state_k, ws_k))
+        torch.cuda.synchronize()
+        assert m.status(1, ws) == 0
+        exact += _logits_check(lg, om.step(tok), f"fused int4, token {t}")
+        same += int(np.array_equal(lg.view(np.uint32), lk.view(np.uint32)))
+    say(f"  {exact} of {T} tokens bit-exact against the oracle, {same} against the per-kernel step")
+    record_property("bit_exact_tokens", f"{exact}/{T}")
+    assert exact >= T - 1

@@ -251,12 +251,17 @@ def test_model_step_validation(dl):
     assert w4 >= w8 + 64 * 4096 + 2048 * 64     # out_proj: the larger linear workspace
     assert dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1) > 0
     # the fused step's region: at M = 1 only, for the 1.3B layer shape with
-    # int8 factors (these layers have int4 ones now: none)
-    lay[0].lora_bits = lay[1].lora_bits = 8
-    w1 = dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1)
+    # int8 factors (r % 4 == 0) or int4 ones (r % 8 == 0); not for int4 at r = 12
     lay[0].lora_bits = lay[1].lora_bits = 4
-    assert w1 > dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1) + 800 * 1024   # 2 layers: ~0.9 MB
+    w1_i4 = dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1)
+    lay[0].in_proj.r = lay[0].out_proj.r = lay[1].in_proj.r = lay[1].out_proj.r = 12
+    w1_i4_r12 = dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1)
     lay[0].lora_bits = lay[1].lora_bits = 8
+    w1_r12 = dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1)
+    lay[0].in_proj.r = lay[0].out_proj.r = lay[1].in_proj.r = lay[1].out_proj.r = 64
+    w1 = dl.lib.dfssm_mamba2_workspace_bytes(ctypes.byref(m), 1)
+    assert w1_r12 > w1_i4_r12 + 800 * 1024   # 2 layers: ~0.9 MB of fused region, int8 only at r = 12
+    assert w1_i4 > w1_i4_r12 + 800 * 1024 and w1 > 800 * 1024
     # prepare / release / status validate on the host
     prep, stat = dl.lib.dfssm_mamba2_prepare, dl.lib.dfssm_mamba2_status
     assert prep(None, 1, 16, 1 << 40, None) == dl.ERR_NULL
