@@ -34,7 +34,7 @@
 //    each row, then the LoRA up-projection (exact int64 through the limbs),
 //    the pinned fp32 epilogue, and publish each consumed row's y and the
 //    workgroup's absmax of them at agent scope.
-//  * Hop 2 (phase D of the next linear, agent scope): each workgroup
+//  * Hop 2 (the next linear's codes wave, agent scope): each workgroup
 //    gathers only its column slice of the previous output (K/8 words) and
 //    the 256 absmax words, quantises its slice (the quantiser's fp32
 //    decisions), builds the 8 bit-planes and the slice's code sum.
@@ -78,7 +78,6 @@ constexpr int kRowLanes = 64 * kAWaves;
 constexpr int kRankGroups = 4;               // ranks split over the row groups h
 constexpr int kMaxRh = kMaxR / kRankGroups;  // ranks per workgroup
 static_assert(kMaxRh * 4 <= 64, "wave 1 sums each rank over 4 lanes");
-constexpr int kPollLanes = 6 * 64;           // waves 1..5 and 7 gather (phase D)
 constexpr int kSlotBytes = 28 * 1024;        // one linear's operands (3 slots: one CU per workgroup)
 constexpr int kRing = 3;
 constexpr int kNB = 28;                      // direct-to-LDS loads per linear, at most
@@ -208,12 +207,10 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
     return;
   }
   __shared__ __attribute__((aligned(16))) uint8_t ring[kRing][kSlotBytes];
-  __shared__ float ys[kMaxKs];                                        // this slice of y_{l-1}
   __shared__ __attribute__((aligned(16))) int8_t codes[kMaxKs];       // its codes
   __shared__ __attribute__((aligned(16))) uint32_t planes[8][kMaxKs / 32];  // their bit-planes
   __shared__ __attribute__((aligned(16))) uint4 limbs[kMaxR / 4];     // acc_a limbs
   __shared__ int red[64 * 17];  // wave 1: rank partials by lane, then summed
-  __shared__ uint64_t ymax;  // {linear, absmax bits}: the largest wins, no reset needed
   __shared__ int sumq[2];    // code sum of the slice, by linear parity
   __shared__ uint32_t seq_s;
   // flags (FLAG(): LDS operations): abort; waves done with phase A (+8 per
@@ -230,7 +227,6 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
     FLAG(rows_done) = 0;
     FLAG(limbs_ready) = 0;
     FLAG(pub_done) = 0;
-    ymax = 0;
     // the launch's epoch: one arrival per workgroup; the 24-bit sequence
     // number derived from it is never 0, so zeroed words never validate
     const uint64_t old = dfssm_dev::arrive(epoch, wg);
@@ -256,75 +252,70 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
     const uint8_t* slot = ring[lu % kRing];
     const uint32_t tg = tag_of(l);
 
-    // ---- phase D (waves 1..5, 7): this slice of y_{l-1} and the 256 absmax
-    //      words, polled until all carry tag(l-1).  Polling starts once this
-    //      workgroup's own reducer has published y_{l-1}: the other
-    //      reducers publish at about the same time, and earlier polls would
-    //      only load the fabric the reducers' own exchange uses.
-    if (l > 0 && wave >= 1 && wave != 6) {
-      long sp = 0;
-      while (FLAG(pub_done) < l)
-        if (spin_gives_up(sp, &abort_, status, kStY)) break;
-      const Layer Lp = layers[lu - 1];
-      const uint32_t tp = tag_of(l - 1);
-      const int ct = (wave == 7 ? 5 : wave - 1) * 64 + lane;
-      const int i0 = ct, i1 = ct + kPollLanes;
-      uint32_t pend = (i0 < Ks ? 1u : 0u) | (i1 < Ks ? 2u : 0u) | (ct < kGrid ? 4u : 0u);
-      if (FLAG(abort_)) pend = 0;
-      uint32_t m = 0;
-      const uint64_t* yw = ex + Lp.yw_off + (int64_t)kap * Ks;
-      while (pend) {
-        uint64_t w0 = 0, w1 = 0, w2 = 0;
-        if (pend & 1u) w0 = ll_load(yw + i0);
-        if (pend & 2u) w1 = ll_load(yw + i1);
-        if (pend & 4u) w2 = ll_load(ex + Lp.mx_off + ct);
-        if ((pend & 1u) && (uint32_t)(w0 >> 32) == tp) {
-          ys[i0] = __uint_as_float((uint32_t)w0);
-          pend &= ~1u;
-        }
-        if ((pend & 2u) && (uint32_t)(w1 >> 32) == tp) {
-          ys[i1] = __uint_as_float((uint32_t)w1);
-          pend &= ~2u;
-        }
-        if ((pend & 4u) && (uint32_t)(w2 >> 32) == tp) {
-          m = (uint32_t)w2;
-          pend &= ~4u;
-        }
-        if (pend && spin_gives_up(sp, &abort_, status, kStY)) break;
-      }
-      m = wave_max_bits_u(m);
-      if (lane == 0)
-        __hip_atomic_fetch_max(&ymax, ((uint64_t)l << 32) | m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    }
-    CHAIN_BARRIER();  // B1
-    if (FLAG(abort_)) return;
-
+    // ---- the slice's codes (wave 1).  Lane p takes columns 8p .. 8p+7:
+    //      for l > 0 it polls their 8 words of y_{l-1} and 4 of the 256
+    //      absmax words until all carry tag(l-1), then quantises the 8
+    //      values in registers; for l = 0 it reads the caller's codes.  It
+    //      writes the codes as bytes, transposes their 8x8 bit matrix into
+    //      byte p of the 8 planes, and the wave sums them.  Polling starts
+    //      once this workgroup's own reducer has published y_{l-1} (the
+    //      other reducers publish at about the same time, and earlier polls
+    //      would only load the fabric); by then every wave of the
+    //      workgroup has finished reading the previous planes (the reducer
+    //      waits for the phase-A waves first), so no barrier is needed
+    //      before they are rewritten.
     uint32_t cq0 = 0, cq1 = 0;  // wave 1: codes 8p .. 8p+7 of the slice
     if (wave == 1) {
-      // ---- codes of the slice: lane p takes columns 8p .. 8p+7, writes
-      //      them as bytes, transposes their 8x8 bit matrix into byte p of
-      //      the 8 planes, and the wave sums them
       const int p = lane;
-      int qs = 0;
-      if (8 * p < Ks) {
-        int q[8];
-        if (l == 0) {
+      const bool inb = 8 * p < Ks;
+      int q[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      if (l == 0) {
+        if (inb) {
           const uint2 c = *reinterpret_cast<const uint2*>(q0 + (int64_t)kap * Ks + 8 * p);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             q[e] = (int8_t)(c.x >> (8 * e));
             q[4 + e] = (int8_t)(c.y >> (8 * e));
           }
-        } else {
-          const float a = __uint_as_float((uint32_t)ymax);
-          const bool zero = a < FLT_MIN;
-          const float inv = zero ? 0.0f : 127.0f / a;
-          const float4 v0 = reinterpret_cast<const float4*>(ys)[2 * p];
-          const float4 v1 = reinterpret_cast<const float4*>(ys)[2 * p + 1];
-          const float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-#pragma unroll
-          for (int e = 0; e < 8; ++e) q[e] = zero ? 0 : code(v[e], inv);
         }
+      } else {
+        long sp = 0;
+        while (FLAG(pub_done) < l)
+          if (spin_gives_up(sp, &abort_, status, kStY)) break;
+        const Layer Lp = layers[lu - 1];
+        const uint32_t tp = tag_of(l - 1);
+        const uint64_t* yw = ex + Lp.yw_off + (int64_t)kap * Ks + (inb ? 8 * p : 0);
+        const uint64_t* mw = ex + Lp.mx_off + 4 * p;
+        uint32_t pend = (inb ? 0xFFu : 0u) | 0xF00u;
+        if (FLAG(abort_)) pend = 0;
+        float v[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+        uint32_t mv[4] = {0u, 0u, 0u, 0u};
+        while (pend) {
+          uint64_t w[12];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) w[k] = ((pend >> k) & 1u) ? ll_load(yw + k) : 0;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) w[8 + k] = ((pend >> (8 + k)) & 1u) ? ll_load(mw + k) : 0;
+#pragma unroll
+          for (int k = 0; k < 12; ++k)
+            if (((pend >> k) & 1u) && (uint32_t)(w[k] >> 32) == tp) {
+              if (k < 8)
+                v[k] = __uint_as_float((uint32_t)w[k]);
+              else
+                mv[k - 8] = (uint32_t)w[k];
+              pend &= ~(1u << k);
+            }
+          if (pend && spin_gives_up(sp, &abort_, status, kStY)) break;
+        }
+        const uint32_t m = wave_max_bits_u(max(max(mv[0], mv[1]), max(mv[2], mv[3])));
+        const float a = __uint_as_float(m);
+        const bool zero = a < FLT_MIN;
+        const float inv = zero ? 0.0f : 127.0f / a;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) q[e] = zero || !inb ? 0 : code(v[e], inv);
+      }
+      int qs = 0;
+      if (inb) {
         uint32_t lo = 0, hi = 0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -358,6 +349,7 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
       if (lane == 0) sumq[l & 1] = qs;
     }
     CHAIN_BARRIER();  // B2
+    if (FLAG(abort_)) return;
 
     if (wave != 1) {
       // ---- phase A (every wave but 1): slice partials of the row group's rows.
@@ -549,7 +541,7 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
       // ---- loading: linear l+1's operands (issued one linear ago) have
       //      landed once nothing of this wave is in flight; then linear
       //      l+2's go into the slot linear l-1 used (every reader of it
-      //      passed B1 of this linear after it was done)
+      //      passed B2 of this linear after it was done)
       CHAIN_WAIT_VMCNT(0);
       if (l + 2 < L) issue_batch(layers[lu + 2], x, kap, h, lam, sb0 + (uint32_t)(((l + 2) % kRing) * kSlotBytes), lane);
     }
