@@ -106,7 +106,7 @@ struct Layer {
   int64_t part_off;        // words: [8][N] slice partials of acc_s (XCD-local)
   int64_t p_off;           // words: [8 XCDs][8 slices][64] partials of acc_a (XCD-local)
   int64_t yw_off;          // words: [Nc] consumed outputs (agent scope)
-  int64_t mx_off;          // words: [256] per-workgroup absmax of consumed outputs
+  int64_t mx_off;          // words: [8 XCDs][256] per-workgroup absmax of consumed outputs, one copy per XCD
 };
 
 // ------------------------------------------------------------ row ownership
@@ -285,7 +285,7 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
         const Layer Lp = layers[lu - 1];
         const uint32_t tp = tag_of(l - 1);
         const uint64_t* yw = ex + Lp.yw_off + (int64_t)kap * Ks + (inb ? 8 * p : 0);
-        const uint64_t* mw = ex + Lp.mx_off + 4 * p;
+        const uint64_t* mw = ex + Lp.mx_off + x * kGrid + 4 * p;  // this XCD's copy
         uint32_t pend = (inb ? 0xFFu : 0u) | 0xF00u;
         if (FLAG(abort_)) pend = 0;
         float v[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
@@ -532,7 +532,8 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
         if (lane < Ld.cpr) ll_store(ex + Ld.yw_off + n, tg, __float_as_uint(y));
         if (Ld.Nc > 0) {
           const uint32_t m = wave_max_bits_u(lane < Ld.cpr ? (__float_as_uint(y) & 0x7fffffffu) : 0u);
-          if (lane == 0) ll_store(ex + Ld.mx_off + wg, tg, m);
+          // one copy per XCD: every workgroup reads all 256
+          if (lane < kXcds) ll_store(ex + Ld.mx_off + lane * kGrid + wg, tg, m);
         }
         if (lane < R) y_all[Ld.y_off + n] = y;
       }
@@ -693,7 +694,7 @@ Plan make_plan(const dfssm_layer* layers, int n) {
     e.yw_off = w;
     w += Nc;
     e.mx_off = w;
-    w += kGrid;
+    w += (int64_t)kXcds * kGrid;
   }
   p.ex_words = dfssm::round_up(w, 32);
   p.ok = true;
