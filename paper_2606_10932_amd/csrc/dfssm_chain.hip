@@ -105,7 +105,7 @@ struct Layer {
   int64_t y_off;           // this linear's outputs in y_all
   int64_t part_off;        // words: [8][N] slice partials of acc_s (XCD-local)
   int64_t p_off;           // words: [8 XCDs][8 slices][64] partials of acc_a (XCD-local)
-  int64_t yw_off;          // words: [Nc] consumed outputs (agent scope)
+  int64_t yw_off;          // words: [8 XCDs][Nc] consumed outputs, one copy per XCD
   int64_t mx_off;          // words: [8 XCDs][256] per-workgroup absmax of consumed outputs, one copy per XCD
 };
 
@@ -284,7 +284,7 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
           if (spin_gives_up(sp, &abort_, status, kStY)) break;
         const Layer Lp = layers[lu - 1];
         const uint32_t tp = tag_of(l - 1);
-        const uint64_t* yw = ex + Lp.yw_off + (int64_t)kap * Ks + (inb ? 8 * p : 0);
+        const uint64_t* yw = ex + Lp.yw_off + (int64_t)x * Lp.Nc + (int64_t)kap * Ks + (inb ? 8 * p : 0);
         const uint64_t* mw = ex + Lp.mx_off + x * kGrid + 4 * p;  // this XCD's copy
         uint32_t pend = (inb ? 0xFFu : 0u) | 0xF00u;
         if (FLAG(abort_)) pend = 0;
@@ -529,7 +529,11 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
         const int elo = e0 + (e1 << 8), ehi = e2 + (e3 << 8);
         const float s = l == 0 ? s0[0] : 1.0f / 127.0f;
         const float y = dfssm_dev::epilogue(s, al, be, acc_s, ehi, elo, r > 0);
-        if (lane < Ld.cpr) ll_store(ex + Ld.yw_off + n, tg, __float_as_uint(y));
+        if (lane < Ld.cpr) {
+          // one copy per XCD: the 32 workgroups of a slice read it from 8 XCDs
+#pragma unroll
+          for (int xr = 0; xr < kXcds; ++xr) ll_store(ex + Ld.yw_off + (int64_t)xr * Ld.Nc + n, tg, __float_as_uint(y));
+        }
         if (Ld.Nc > 0) {
           const uint32_t m = wave_max_bits_u(lane < Ld.cpr ? (__float_as_uint(y) & 0x7fffffffu) : 0u);
           // one copy per XCD: every workgroup reads all 256
@@ -692,7 +696,7 @@ Plan make_plan(const dfssm_layer* layers, int n) {
     e.p_off = w;
     w += (int64_t)kXcds * kSlices * kMaxR;
     e.yw_off = w;
-    w += Nc;
+    w += (int64_t)kXcds * Nc;
     e.mx_off = w;
     w += (int64_t)kXcds * kGrid;
   }
