@@ -359,7 +359,11 @@ __global__ __launch_bounds__(kThreads, 1) void chain_persistent(
       //      b = 7), each plane's popcounts summed over the words first.
       //      All LDS reads of a pass are issued before the first use.
       const int G = Wr <= 4 ? 1 : (Wr <= 8 ? 2 : 4);
-      const int ta = wave == 0 ? lane : tid - 64;  // 0 .. kRowLanes - 1
+      // lane blocks of 64 in the order waves 5, 3, 2, 0, 7, 6, 4: the
+      // first four sit on four different SIMDs (waves w and w + 4 share
+      // one), so short linears and the last pass spread over the SIMDs
+      // instead of doubling up on one
+      const int ta = 64 * ((0x45061273 >> (4 * wave)) & 0xF) + lane;  // 0 .. kRowLanes - 1
       const int g = ta % G, w0 = 4 * g;
       uint32_t pw[8][4];
 #pragma unroll
