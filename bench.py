@@ -244,6 +244,12 @@ def main():
             "exchange_floor": {
                 "workload": "persistent chain of 96 linears K=N=256, r=4, M=1 (%d B of weights in all)" % tiny_bytes,
                 "us_per_sweep": round(tiny_ms * 1e3, 2), "us_per_linear": round(tiny_ms * 1e3 / 96, 3)},
+            "hop": {
+                "workload": "one agent-scope word passed between two workgroups on two XCDs "
+                            "(dfssm_exchange_pingpong), median over the pairs",
+                "round_trip_ns_1_pair": round(D.exchange_pingpong(1, 2000), 1),
+                "round_trip_ns_128_pairs": round(D.exchange_pingpong(128, 2000), 1),
+                "round_trip_ns_release_acquire": round(D.exchange_pingpong(1, 200, fence=True), 1)},
         }
         del tarr, tws, ty
 

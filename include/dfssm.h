@@ -297,6 +297,22 @@ dfssm_status dfssm_chain_stream_floor(const dfssm_layer* layers, int n_layers, v
  * Errors: NULL, SHAPE (bytes not a multiple of 16), ALIGN, WORKSPACE (sink
  * too small), DEVICE. */
 size_t dfssm_read_floor_sink_words(size_t bytes);
+
+/* Diagnostic, not part of the computation: the cost of one exchange hop of
+ * the persistent kernels (Sec. 4.1: the decode path is bound by latency,
+ * not by bytes).  npairs pairs of workgroups, the two of a pair on
+ * different XCDs, pass one 64-bit word back and forth iters times with
+ * agent-scope stores and polling loads (fence != 0: a release store and
+ * acquire loads instead); *ns_per_round_trip (host) receives the median over
+ * the pairs of one round trip (two hops).  Synchronises `stream` to read
+ * the result.  Every wait is bounded.
+ *   workspace  device, dfssm_exchange_pingpong_bytes() bytes, 16-byte
+ *              aligned; its contents on entry do not matter
+ * Errors: NULL, SHAPE (npairs outside 1..128, iters outside 1..100000),
+ * ALIGN, WORKSPACE, DEVICE (also when a wait gave up). */
+size_t dfssm_exchange_pingpong_bytes(void);
+dfssm_status dfssm_exchange_pingpong(int npairs, int iters, int fence, void* workspace, size_t workspace_bytes,
+                                     double* ns_per_round_trip, void* stream);
 dfssm_status dfssm_read_floor(const void* p, size_t bytes, uint32_t* sink, size_t sink_words, void* stream);
 
 /* The tied int8 embedding table (Sec. 3.3 and Table 1: the token embedding

@@ -24,6 +24,7 @@ EXPORTS = ["dfssm_quantize_act", "dfssm_linear_workspace_bytes", "dfssm_scaffold
            "dfssm_scaffold_lora_linear_ex", "dfssm_chain_workspace_bytes",
            "dfssm_scaffold_lora_chain", "dfssm_chain_prepare", "dfssm_chain_run", "dfssm_chain_status",
            "dfssm_chain_stream_floor", "dfssm_read_floor", "dfssm_read_floor_sink_words",
+           "dfssm_exchange_pingpong", "dfssm_exchange_pingpong_bytes",
            "dfssm_embed_gather", "dfssm_lm_head", "dfssm_add_rmsnorm_quant", "dfssm_gate_norm_quant",
            "dfssm_ssm_step", "dfssm_linear_i4_workspace_bytes", "dfssm_scaffold_lora_linear_i4",
            "dfssm_mamba2_state_bytes", "dfssm_mamba2_workspace_bytes",
@@ -92,6 +93,10 @@ def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dfssm_read_floor.restype = i32
     lib.dfssm_read_floor_sink_words.argtypes = [sz]
     lib.dfssm_read_floor_sink_words.restype = sz
+    lib.dfssm_exchange_pingpong_bytes.argtypes = []
+    lib.dfssm_exchange_pingpong_bytes.restype = sz
+    lib.dfssm_exchange_pingpong.argtypes = [i32, i32, i32, vp, sz, ctypes.POINTER(ctypes.c_double), vp]
+    lib.dfssm_exchange_pingpong.restype = i32
     lib.dfssm_embed_gather.argtypes = [vp, vp, i64, i64, vp, i64, vp, vp]
     lib.dfssm_embed_gather.restype = i32
     lib.dfssm_lm_head.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp, vp]
@@ -334,6 +339,17 @@ def chain_stream_floor(layer_arr, workspace, stream=None):
     no exchange, no output) on a workspace prepared for these layers at M=1."""
     _check(lib.dfssm_chain_stream_floor(layer_arr, len(layer_arr), workspace.data_ptr(), workspace.numel(),
                                         _stream(stream)))
+
+
+def exchange_pingpong(npairs: int = 1, iters: int = 2000, fence: bool = False, stream=None) -> float:
+    """Diagnostic: ns per round trip (two hops) of one agent-scope word
+    between workgroups on two XCDs, median over npairs concurrent pairs."""
+    torch = _torch()
+    ws = torch.empty(int(lib.dfssm_exchange_pingpong_bytes()), dtype=torch.uint8, device="cuda")
+    out = ctypes.c_double(0.0)
+    _check(lib.dfssm_exchange_pingpong(int(npairs), int(iters), 1 if fence else 0, ws.data_ptr(), ws.numel(),
+                                       ctypes.byref(out), _stream(stream)))
+    return float(out.value)
 
 
 def read_floor_sink_words(nbytes: int) -> int:

@@ -547,6 +547,39 @@ dfssm_status dfssm_chain_stream_floor(const dfssm_layer* layers, int n_layers, v
   return e == hipSuccess ? DFSSM_OK : device_fail(e, "chain stream launch");
 }
 
+size_t dfssm_exchange_pingpong_bytes(void) { return dfssm::kPingBytes; }
+
+dfssm_status dfssm_exchange_pingpong(int npairs, int iters, int fence, void* workspace, size_t workspace_bytes,
+                                     double* ns_per_round_trip, void* stream) {
+  clear_error();
+  if (!ns_per_round_trip) return fail(DFSSM_ERR_NULL, "ns_per_round_trip is NULL");
+  *ns_per_round_trip = 0.0;
+  if (npairs < 1 || npairs > 128 || iters < 1 || iters > 100000)
+    return fail(DFSSM_ERR_SHAPE, "npairs=%d (1..128), iters=%d (1..100000)", npairs, iters);
+  const dfssm_status st = check_ptrs({{workspace, "workspace"}}, {});
+  if (st != DFSSM_OK) return st;
+  if (workspace_bytes < dfssm::kPingBytes)
+    return fail(DFSSM_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, dfssm::kPingBytes);
+  hipStream_t hs = (hipStream_t)stream;
+  hipError_t e = dfssm::launch_exchange_pingpong(npairs, iters, fence != 0, workspace, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  std::vector<int64_t> ticks(256);
+  unsigned failed = 0;
+  const char* b = static_cast<const char*>(workspace);
+  if (e == hipSuccess)
+    e = hipMemcpy(ticks.data(), b + dfssm::kPingWordsBytes, 256 * 8, hipMemcpyDeviceToHost);
+  if (e == hipSuccess)
+    e = hipMemcpy(&failed, b + dfssm::kPingWordsBytes + dfssm::kPingTicksBytes, 4, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return device_fail(e, "exchange ping-pong");
+  if (failed) return fail(DFSSM_ERR_DEVICE, "exchange ping-pong: a bounded wait gave up");
+  // the pinging side's loop, median over the pairs, in ns (100 MHz ticks)
+  std::vector<int64_t> ping;
+  for (int p = 0; p < npairs; ++p) ping.push_back(ticks[2 * p]);
+  std::sort(ping.begin(), ping.end());
+  *ns_per_round_trip = (double)ping[ping.size() / 2] * 10.0 / iters;
+  return DFSSM_OK;
+}
+
 size_t dfssm_read_floor_sink_words(size_t bytes) { return (size_t)dfssm::read_floor_sink_words((int64_t)bytes); }
 
 dfssm_status dfssm_read_floor(const void* p, size_t bytes, uint32_t* sink, size_t sink_words, void* stream) {

@@ -46,3 +46,73 @@ hipError_t launch_read_floor(const void* p, int64_t bytes, uint32_t* sink, hipSt
 }
 
 }  // namespace dfssm
+
+// ------------------------------------------------------------ exchange hop
+// Workgroups 2i and 2i+1 (on two XCDs: the dispatcher deals workgroups to
+// the XCDs in turn) pass one 64-bit word back and forth `iters` times at
+// agent scope, as the persistent kernels' exchange words do; with kFence
+// the store is a release and the load an acquire (the fence pair a
+// release/acquire protocol would need).  Each side records the
+// s_memrealtime ticks (100 MHz) of its whole loop.  Waits are bounded: a
+// side that gives up sets *fail and leaves, and its partner gives up in turn.
+namespace {
+constexpr long kPingSpin = 1L << 22;
+
+template <bool kFence>
+__global__ __launch_bounds__(64) void exchange_pingpong(uint64_t* words, int iters, int npairs, int64_t* ticks,
+                                                        unsigned* fail) {
+  const int wg = blockIdx.x;
+  if (wg >= 2 * npairs || threadIdx.x != 0) return;
+  const int pair = wg >> 1, side = wg & 1;
+  uint64_t* mine = words + (int64_t)(2 * pair + side) * 64;  // 512 bytes apart
+  const uint64_t* theirs = words + (int64_t)(2 * pair + (side ^ 1)) * 64;
+  const int64_t t0 = (int64_t)__builtin_amdgcn_s_memrealtime();
+  for (int i = 1; i <= iters; ++i) {
+    if (side == 0) {
+      if (kFence)
+        __hip_atomic_store(mine, (uint64_t)i, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      else
+        __hip_atomic_store(mine, (uint64_t)i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    long sp = 0;
+    for (;;) {
+      const uint64_t v = kFence ? __hip_atomic_load(theirs, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT)
+                                : __hip_atomic_load(theirs, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (v == (uint64_t)i) break;
+      // every 1024 polls: the bound, and whether the partner gave up
+      if ((++sp & 1023) == 0 &&
+          (sp > kPingSpin || __hip_atomic_load(fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0)) {
+        atomicOr(fail, 1u);
+        return;
+      }
+    }
+    if (side == 1) {
+      if (kFence)
+        __hip_atomic_store(mine, (uint64_t)i, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      else
+        __hip_atomic_store(mine, (uint64_t)i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  ticks[wg] = (int64_t)__builtin_amdgcn_s_memrealtime() - t0;
+}
+}  // namespace
+
+namespace dfssm {
+
+hipError_t launch_exchange_pingpong(int npairs, int iters, bool fence, void* ws, hipStream_t st) {
+  char* b = static_cast<char*>(ws);
+  uint64_t* words = reinterpret_cast<uint64_t*>(b);
+  int64_t* ticks = reinterpret_cast<int64_t*>(b + kPingWordsBytes);
+  unsigned* fail = reinterpret_cast<unsigned*>(b + kPingWordsBytes + kPingTicksBytes);
+  // every word, tick and the flag start at zero (a fill kernel: no memset
+  // node if the caller captures this)
+  hipError_t e = launch_zero_words(words, (int64_t)(kPingBytes / 8), st);
+  if (e != hipSuccess) return e;
+  if (fence)
+    exchange_pingpong<true><<<dim3(256), dim3(64), 0, st>>>(words, iters, npairs, ticks, fail);
+  else
+    exchange_pingpong<false><<<dim3(256), dim3(64), 0, st>>>(words, iters, npairs, ticks, fail);
+  return hipGetLastError();
+}
+
+}  // namespace dfssm

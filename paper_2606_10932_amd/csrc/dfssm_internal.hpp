@@ -209,6 +209,12 @@ hipError_t launch_zero_words(uint64_t* p, int64_t words, hipStream_t st);
 int64_t read_floor_sink_words(int64_t bytes);
 hipError_t launch_read_floor(const void* p, int64_t bytes, uint32_t* sink, hipStream_t st);
 
+// The exchange ping-pong diagnostic's workspace: 256 x 64 words, 256 tick
+// counts, the give-up flag.
+constexpr size_t kPingWordsBytes = 256 * 64 * 8, kPingTicksBytes = 256 * 8;
+constexpr size_t kPingBytes = kPingWordsBytes + kPingTicksBytes + 256;
+hipError_t launch_exchange_pingpong(int npairs, int iters, bool fence, void* ws, hipStream_t st);
+
 }  // namespace dfssm
 
 // ------------------------------------------------------------ device helpers

@@ -690,7 +690,9 @@ __global__ __launch_bounds__(kThreads, 1) void step_persistent(
       // ---- phase A: slice partials of every slot of the row group (as the
       //      chain; slots without a row are skipped)
       const int G = Wr <= 4 ? 1 : (Wr <= 8 ? 2 : 4);
-      const int ta = wave == 0 ? lane : tid - 64;
+      // lane blocks of 64 in the order waves 5, 3, 2, 0, 7, 6, 4: the first
+      // four sit on four different SIMDs (waves w and w + 4 share one)
+      const int ta = 64 * ((0x45061273 >> (4 * wave)) & 0xF) + lane;
       const int gg = ta % G, w0 = 4 * gg;
       uint32_t pw[8][4];
 #pragma unroll

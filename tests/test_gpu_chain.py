@@ -227,3 +227,16 @@ def test_chain_int4_shapes(env, case):
     M = 2 if case == "mixed2" else 1
     say(f"chain with int4 LoRA: {case}, M={M}")
     _check_chain_i4(env, spec, M=M, key=91 + len(case))
+
+
+def test_exchange_pingpong_diagnostic(env):
+    """The exchange-hop diagnostic runs to completion (no bounded wait gives
+    up) and reports a round trip between 100 ns and 100 us; the fenced
+    variant costs at least as much."""
+    torch, D, o = env
+    say("exchange ping-pong diagnostic")
+    one = D.exchange_pingpong(1, 500)
+    many = D.exchange_pingpong(128, 500)
+    fenced = D.exchange_pingpong(1, 50, fence=True)
+    say(f"  round trip {one:.0f} ns (1 pair), {many:.0f} ns (128 pairs), fenced {fenced:.0f} ns")
+    assert 100 < one < 1e5 and 100 < many < 1e5 and fenced >= 0.8 * one

@@ -110,6 +110,15 @@ def test_chain_validation(dl):
     assert dl.lib.dfssm_chain_status(arr, 2, 1, 16, 8, ctypes.byref(st), None) == dl.ERR_WORKSPACE
     assert dl.lib.dfssm_chain_status(arr, 2, 1, 16, 1 << 30, None, None) == dl.ERR_NULL
     # the read-floor diagnostic validates before any HIP call
+    pp, ppb = dl.lib.dfssm_exchange_pingpong, dl.lib.dfssm_exchange_pingpong_bytes()
+    ns = ctypes.c_double(1.0)
+    assert ppb >= 256 * 64 * 8
+    assert pp(0, 10, 0, 16, ppb, ctypes.byref(ns), None) == dl.ERR_SHAPE and ns.value == 0.0
+    assert pp(129, 10, 0, 16, ppb, ctypes.byref(ns), None) == dl.ERR_SHAPE
+    assert pp(1, 0, 0, 16, ppb, ctypes.byref(ns), None) == dl.ERR_SHAPE
+    assert pp(1, 10, 0, None, ppb, ctypes.byref(ns), None) == dl.ERR_NULL
+    assert pp(1, 10, 0, 16, ppb - 1, ctypes.byref(ns), None) == dl.ERR_WORKSPACE
+    assert pp(1, 10, 0, 16, ppb, None, None) == dl.ERR_NULL
     rf = dl.lib.dfssm_read_floor
     assert dl.lib.dfssm_read_floor_sink_words(2923008) == 4 * 357   # one word per wave
     assert dl.lib.dfssm_read_floor_sink_words(0) == 4
