@@ -447,7 +447,8 @@ def main():
             for m in Ms:
                 qd, sd = D.quantize_act(dev(S.config_activations(cfg, m)))
                 yd = torch.empty((m, c.N), dtype=torch.float32, device="cuda")
-                wsd = torch.empty(int(D.lib.dfssm_linear_i4_workspace_bytes(m, c.K, c.N, c.r)), dtype=torch.uint8,
+                # a workspace holds zeros before its first use (its epoch words)
+                wsd = torch.zeros(int(D.lib.dfssm_linear_i4_workspace_bytes(m, c.K, c.N, c.r)), dtype=torch.uint8,
                                   device="cuda")
 
                 def calls4():
