@@ -47,6 +47,7 @@
 #include <atomic>
 
 #include "dfssm_int4.hpp"
+#include "dfssm_persist.hpp"
 
 namespace {
 
@@ -155,7 +156,10 @@ struct SkinnyArgs {
   int32_t* acc_s_out;
   int64_t* acc_b_out;
   int32_t* acc_a;  // [M][r], written by the LoRA workgroups (and by fallback lanes)
-  uint64_t* xw;    // [M][rp] limb words, then [M] sum-Q words
+  uint64_t* xw;    // [xcopies][xstride]: [M][rp] limb words, then [M] sum-Q words
+  int64_t xstride; // M * rp + M
+  int xcopies;     // 8: one copy per XCD (every output workgroup reads the same
+                   // words, so the copies spread its polls) when they fit; else 1
   uint64_t* epoch; // kEpochGroups words {epoch:32, arrivals:32}, kEpochStride apart;
                    // NULL: the call's tag is host_tag
   uint32_t host_tag;
@@ -293,11 +297,15 @@ __device__ void lora_block(const SkinnyArgs& a) {
   const uint64_t old = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(ep_old >> 32)) << 32) |
                        (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)ep_old);
   const uint32_t tag = a.epoch ? dfssm_dev::epoch_tag(old) : a.host_tag;
-  if (lane < mt) {
-    const int m = m0 + lane;
-    if (jr) a.acc_a[(int64_t)m * r + j] = mine;
-    word_store(a.xw + (int64_t)m * rp + j, tag, pack_limbs(mine));  // zero limbs for ranks in [r, rp)
-    if (qsum) word_store(a.xw + (int64_t)M * rp + m, tag, (uint32_t)mine_q);
+  // lane c*mt + i stores token m0 + i's words into copy c (lane i holds them)
+  const int src = lane % mt;
+  const int vm = __shfl(mine, src, 64), vq = __shfl(mine_q, src, 64);
+  if (lane < mt && jr) a.acc_a[(int64_t)(m0 + lane) * r + j] = mine;
+  if (lane < mt * a.xcopies) {
+    const int cpy = lane / mt, m = m0 + (lane - cpy * mt);
+    uint64_t* xc = a.xw + (int64_t)cpy * a.xstride;
+    word_store(xc + (int64_t)m * rp + j, tag, pack_limbs(vm));  // zero limbs for ranks in [r, rp)
+    if (qsum) word_store(xc + (int64_t)M * rp + m, tag, (uint32_t)vq);
   }
   if (a.epoch && lane == 0) dfssm_dev::advance_if_last(a.epoch, item, old, a.arrivals);
 }
@@ -308,8 +316,10 @@ __device__ void lora_block(const SkinnyArgs& a) {
 template <bool L4>
 __device__ void fetch_lora(const SkinnyArgs& a, uint32_t tag, int m, int j0, int kg, v4i (&lm)[4], int* sq,
                            bool store_acc) {
-  const uint64_t* wp = a.xw + (int64_t)m * a.rp + j0 + 16 * kg;
-  const uint64_t* sp = a.xw + (int64_t)a.M * a.rp + m;
+  // this XCD's copy of the words
+  const uint64_t* xc = a.xw + (a.xcopies > 1 ? (int64_t)dfssm_px::xcc_id() * a.xstride : 0);
+  const uint64_t* wp = xc + (int64_t)m * a.rp + j0 + 16 * kg;
+  const uint64_t* sp = xc + (int64_t)a.M * a.rp + m;
   uint32_t val[16], vq = 0;
   bool have = false;
   for (int it = 0;; ++it) {
@@ -602,9 +612,11 @@ hipError_t skinny_impl(const int8_t* q, const float* s, int64_t M, int64_t K, in
     cap = hipStreamCaptureStatusActive;
   }
   const bool device_epoch = cap != hipStreamCaptureStatusNone;
+  const int64_t xstride = M * rp + M;
+  const int xcopies = 8 * xstride <= kXwWords ? 8 : 1;
   SkinnyArgs a{q, s, (int)M, (int)K, (int)N, (int)r, rp, w_bits, alpha, A, B, beta, y, acc_s, acc_b,
-               ws.acc_a, ws.xw, device_epoch ? ws.epoch : nullptr, device_epoch ? 0u : host_tag(), arrivals,
-               (int)(local_only ? 0 : lora_waves), nb_lora, local_only ? 0 : (1 << 14)};
+               ws.acc_a, ws.xw, xstride, xcopies, device_epoch ? ws.epoch : nullptr, device_epoch ? 0u : host_tag(),
+               arrivals, (int)(local_only ? 0 : lora_waves), nb_lora, local_only ? 0 : (1 << 14)};
   hipError_t e;
   if (mt == 1)
     e = S == 8 ? launch_t<1, 8, L4>(a, nw, st) : launch_t<1, 4, L4>(a, nw, st);
