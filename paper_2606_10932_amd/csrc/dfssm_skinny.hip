@@ -311,37 +311,61 @@ __device__ void lora_block(const SkinnyArgs& a) {
 }
 
 // The limbs of acc_a[m][j0 + 16kg .. +15] as 4 limb operands (byte e of limb
-// t = limb t of rank j0 + 16kg + e) and, with want_sq, sum Q of token m: from
-// the LoRA workgroups' words, or computed here once `spin` polls have passed.
+// t = limb t of rank j0 + 16kg + e) and, with want_sq, sum Q of token m, for
+// the lane (rho, kg) of the wave that finishes the token tile starting at t0
+// (m = min(t0 + rho, M - 1)): from the LoRA workgroups' words, or computed
+// here once `spin` polls have passed.  The polls are token-major: lane L
+// reads rank j0 + L of each of the tile's nt distinct tokens (one 512-byte
+// load per token) and lanes below nt read the sum-Q words, so a poll round
+// is nt + 1 coalesced loads; the words then reach their lanes through the
+// wave's LDS tile wx [16][kWxPitch] (sq: wq [16]).
+constexpr int kWxPitch = 68;  // words per token row of wx (16 bytes of skew)
 template <bool L4>
-__device__ void fetch_lora(const SkinnyArgs& a, uint32_t tag, int m, int j0, int kg, v4i (&lm)[4], int* sq,
-                           bool store_acc) {
+__device__ void fetch_lora(const SkinnyArgs& a, uint32_t tag, int t0, int j0, int rho, int kg, uint32_t* wx,
+                           int* wq, v4i (&lm)[4], int* sq, bool store_acc) {
+  const int lane = threadIdx.x & 63;
+  const int M = a.M, rp = a.rp;
+  const int nt = max(1, min(16, M - t0));  // distinct tokens of the tile (tokens past M repeat M - 1)
+  const int m = min(t0 + min(rho, nt - 1), M - 1);
   // this XCD's copy of the words
   const uint64_t* xc = a.xw + (a.xcopies > 1 ? (int64_t)dfssm_px::xcc_id() * a.xstride : 0);
-  const uint64_t* wp = xc + (int64_t)m * a.rp + j0 + 16 * kg;
-  const uint64_t* sp = xc + (int64_t)a.M * a.rp + m;
-  uint32_t val[16], vq = 0;
+  const uint64_t* wp = xc + (int64_t)min(t0, M - 1) * rp + j0 + lane;
+  const uint64_t* sp = xc + (int64_t)M * rp + min(t0 + min(lane, nt - 1), M - 1);
   bool have = false;
   for (int it = 0;; ++it) {
-    if (!have) {
-      uint64_t w[16], wq = 0;
+    uint64_t w[16], wqv = 0;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) w[e] = word_load(wp + e);
-      if (sq) wq = word_load(sp);
-      bool ok = !sq || (uint32_t)(wq >> 32) == tag;
+    for (int i = 0; i < 16; ++i)
+      if (i < nt) w[i] = word_load(wp + (int64_t)i * rp);  // nt is uniform
+    if (sq) wqv = word_load(sp);
+    bool ok = !sq || (uint32_t)(wqv >> 32) == tag;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) ok = ok && (uint32_t)(w[e] >> 32) == tag;
-      if (ok) {
+    for (int i = 0; i < 16; ++i)
+      if (i < nt) ok = ok && (uint32_t)(w[i] >> 32) == tag;
+    if (__all(ok)) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) val[e] = (uint32_t)w[e];
-        vq = (uint32_t)wq;
-        have = true;
-      }
+      for (int i = 0; i < 16; ++i)
+        if (i < nt) wx[i * kWxPitch + lane] = (uint32_t)w[i];
+      if (sq && lane < nt) wq[lane] = (int)(uint32_t)wqv;
+      have = true;
+      break;
     }
-    if (__all(have) || it >= a.spin) break;
+    if (it >= a.spin) break;
     __builtin_amdgcn_s_sleep(2);
   }
-  if (!have) {
+  uint32_t val[16], vq = 0;
+  if (have) {
+    // the LDS writes above and these reads are the same wave's, in order
+    __builtin_amdgcn_wave_barrier();
+    const int rt = min(rho, nt - 1);
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      const uint4 u = *reinterpret_cast<const uint4*>(wx + rt * kWxPitch + 16 * kg + 4 * d);
+      val[4 * d] = u.x; val[4 * d + 1] = u.y; val[4 * d + 2] = u.z; val[4 * d + 3] = u.w;
+    }
+    if (sq) vq = (uint32_t)wq[rt];
+    __builtin_amdgcn_wave_barrier();  // wx is written again by the next chunk's call
+  } else {
     // the LoRA workgroups' words did not arrive: compute them here
 #pragma unroll 1
     for (int e = 0; e < 16; ++e) {
@@ -370,6 +394,8 @@ __device__ void fetch_lora(const SkinnyArgs& a, uint32_t tag, int m, int j0, int
 template <int MT, int S, bool L4>
 __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   __shared__ v4i red[kMaxWaves][MT][64];
+  __shared__ __align__(16) uint32_t wx[MT][16 * kWxPitch];
+  __shared__ int wq[MT][16];
   __shared__ uint32_t tag_lds;
   if ((int)blockIdx.x < a.nb_lora) {
     if (blockIdx.y == 0) lora_block<L4>(a);  // one set of LoRA workgroups for all tokens
@@ -499,7 +525,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   v4i lm[4];
   int sq = 0;
   const bool keep = (int)blockIdx.x == a.nb_lora && mtok < M;
-  fetch_lora<L4>(a, tag, mc, 0, kg, lm, &sq, keep);
+  fetch_lora<L4>(a, tag, mb + 16 * wave, 0, rho, kg, wx[wave], wq[wave], lm, &sq, keep);
 
   // LoRA up-projection, limbs 3, 2, 1, 0 over the 64-rank chunks
   if (L4 && bpacked) {
@@ -519,7 +545,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
     for (int j0 = 64; j0 < a.rp; j0 += 64) {
       const v4i bl = load16_row_guarded<L4>(a.B + (int64_t)nrow * bpitch, j0 + 16 * kg, r, ba);
       v4i lj[4];
-      fetch_lora<L4>(a, tag, mc, j0, kg, lj, nullptr, keep);
+      fetch_lora<L4>(a, tag, mb + 16 * wave, j0, rho, kg, wx[wave], wq[wave], lj, nullptr, keep);
       e3 = mfma(bl, lj[3], e3);
       e2 = mfma(bl, lj[2], e2);
       e1 = mfma(bl, lj[1], e1);
