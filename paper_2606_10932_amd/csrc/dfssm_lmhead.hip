@@ -172,7 +172,10 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void lm_head_mfma(const int8_t*
                                                                   const float* __restrict__ scale, int V,
                                                                   float* __restrict__ logits,
                                                                   int32_t* __restrict__ acc_out) {
-  __shared__ v4i red[kMfmaMaxWaves][4][64];
+  // two buffers of the waves' partial tiles: tile tt + 2 writes the buffer
+  // of tile tt only after the barrier of tile tt + 1, which every reader of
+  // tile tt passes with its LDS reads done, so one barrier per tile suffices
+  __shared__ v4i red[2][kMfmaMaxWaves][4][64];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nw = blockDim.x >> 6;
@@ -189,41 +192,58 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void lm_head_mfma(const int8_t*
 #pragma unroll
     for (int k = 0; k < KS; ++k) e[t][k] = ok ? load16i(rp + 64 * k) : v4i{0, 0, 0, 0};
   }
+  // the row scales of the tile this wave finishes (waves 0..3: row tile
+  // `wave`), loaded once
+  const bool vec_store = (V & 3) == 0;  // 4 consecutive rows of a token are 16 aligned bytes
+  const int row0 = v0 + 16 * (wave & 3) + 4 * kg;
+  float scv[4] = {0.f, 0.f, 0.f, 0.f};
+  if (wave < 4) {
+    if (vec_store && row0 + 3 < V) {
+      const float4 sc = *reinterpret_cast<const float4*>(scale + row0);
+      scv[0] = sc.x; scv[1] = sc.y; scv[2] = sc.z; scv[3] = sc.w;
+    } else {
+#pragma unroll
+      for (int vv = 0; vv < 4; ++vv) scv[vv] = row0 + vv < V ? scale[row0 + vv] : 0.f;
+    }
+  }
   const int ntt = (M + 15) / 16;
-  auto load_q = [&](int tt, v4i (&x)[KS]) {
+  // a tile's token scale goes out just before its Q codes: the wait for the
+  // codes before the tile's MFMAs covers it, so the reduction after them
+  // never waits for the next tile's loads (a wave's loads complete in order)
+  auto load_q = [&](int tt, v4i (&x)[KS], float& sm) {
     const int m = 16 * tt + rho;
     const bool mok = m < M;
+    sm = s[mok ? m : 0];
     const int8_t* qp = q + (int64_t)(mok ? m : 0) * d + c0;
 #pragma unroll
     for (int k = 0; k < KS; ++k) x[k] = mok ? load16i(qp + 64 * k) : v4i{0, 0, 0, 0};
   };
   v4i x[KS];
-  load_q(0, x);
-  const bool vec_store = (V & 3) == 0;  // 4 consecutive rows of a token are 16 aligned bytes
+  float sm_next;
+  load_q(0, x, sm_next);
   for (int tt = 0; tt < ntt; ++tt) {
     const int m = 16 * tt + rho;
     const bool mok = m < M;
+    const float sm = sm_next;
     v4i acc[4] = {v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}};
 #pragma unroll
     for (int k = 0; k < KS; ++k)
 #pragma unroll
       for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(e[t][k], x[k], acc[t], 0, 0, 0);
-    // the next tile's Q loads go out before this tile's reduction and stores
-    if (tt + 1 < ntt) load_q(tt + 1, x);
+    // the next tile's loads go out before this tile's reduction and stores
+    if (tt + 1 < ntt) load_q(tt + 1, x, sm_next);
+    v4i (&rb)[kMfmaMaxWaves][4][64] = red[tt & 1];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) red[wave][t][lane] = acc[t];
+    for (int t = 0; t < 4; ++t) rb[wave][t][lane] = acc[t];
     __syncthreads();
     if (wave < 4) {
       // lane (rho, kg) holds D[row 16 wave + 4 kg + vv][token 16 tt + rho]
-      v4i sum = red[0][wave][lane];
-      for (int w = 1; w < nw; ++w) sum += red[w][wave][lane];
+      v4i sum = rb[0][wave][lane];
+      for (int w = 1; w < nw; ++w) sum += rb[w][wave][lane];
       if (mok) {
-        const float sm = s[m];
-        const int row0 = v0 + 16 * wave + 4 * kg;
         if (vec_store && row0 + 3 < V) {
-          const float4 sc = *reinterpret_cast<const float4*>(scale + row0);
           const float f0 = (float)sum[0], f1 = (float)sum[1], f2 = (float)sum[2], f3 = (float)sum[3];
-          const float t0 = sc.x * f0, t1 = sc.y * f1, t2 = sc.z * f2, t3 = sc.w * f3;
+          const float t0 = scv[0] * f0, t1 = scv[1] * f1, t2 = scv[2] * f2, t3 = scv[3] * f3;
           if (logits)
             *reinterpret_cast<float4*>(logits + (int64_t)m * V + row0) = make_float4(sm * t0, sm * t1, sm * t2, sm * t3);
           if (acc_out) *reinterpret_cast<int4*>(acc_out + (int64_t)m * V + row0) = make_int4(sum[0], sum[1], sum[2], sum[3]);
@@ -233,7 +253,7 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void lm_head_mfma(const int8_t*
             const int row = row0 + vv;
             if (row < V) {
               const float fa = (float)sum[vv];
-              const float tv = scale[row] * fa;
+              const float tv = scv[vv] * fa;
               if (logits) logits[(int64_t)m * V + row] = sm * tv;
               if (acc_out) acc_out[(int64_t)m * V + row] = sum[vv];
             }
@@ -241,7 +261,6 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void lm_head_mfma(const int8_t*
         }
       }
     }
-    __syncthreads();
   }
 }
 
