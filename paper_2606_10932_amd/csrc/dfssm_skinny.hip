@@ -157,9 +157,10 @@ struct SkinnyArgs {
   int64_t* acc_b_out;
   int32_t* acc_a;  // [M][r], written by the LoRA workgroups (and by fallback lanes)
   uint64_t* xw;    // [xcopies][xstride]: [M][rp] limb words, then [M] sum-Q words
-  int64_t xstride; // M * rp + M
+  int64_t xstride; // M * rp + M, rounded up to 32 words
   int xcopies;     // 8: one copy per XCD (every output workgroup reads the same
-                   // words, so the copies spread its polls) when they fit; else 1
+                   // words, so the copies spread its polls) at r > 32 when they
+                   // fit; else 1
   uint64_t* epoch; // kEpochGroups words {epoch:32, arrivals:32}, kEpochStride apart;
                    // NULL: the call's tag is host_tag
   uint32_t host_tag;
@@ -297,15 +298,27 @@ __device__ void lora_block(const SkinnyArgs& a) {
   const uint64_t old = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(ep_old >> 32)) << 32) |
                        (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)ep_old);
   const uint32_t tag = a.epoch ? dfssm_dev::epoch_tag(old) : a.host_tag;
-  // lane c*mt + i stores token m0 + i's words into copy c (lane i holds them)
-  const int src = lane % mt;
-  const int vm = __shfl(mine, src, 64), vq = __shfl(mine_q, src, 64);
-  if (lane < mt && jr) a.acc_a[(int64_t)(m0 + lane) * r + j] = mine;
-  if (lane < mt * a.xcopies) {
-    const int cpy = lane / mt, m = m0 + (lane - cpy * mt);
-    uint64_t* xc = a.xw + (int64_t)cpy * a.xstride;
-    word_store(xc + (int64_t)m * rp + j, tag, pack_limbs(vm));  // zero limbs for ranks in [r, rp)
-    if (qsum) word_store(xc + (int64_t)M * rp + m, tag, (uint32_t)vq);
+  if (a.xcopies == 1) {
+    if (lane < mt) {
+      const int m = m0 + lane;
+      if (jr) a.acc_a[(int64_t)m * r + j] = mine;
+      word_store(a.xw + (int64_t)m * rp + j, tag, pack_limbs(mine));  // zero limbs for ranks in [r, rp)
+      if (qsum) word_store(a.xw + (int64_t)M * rp + m, tag, (uint32_t)mine_q);
+    }
+  } else {
+    // lane c*mt + i stores token m0 + i's words into copy c (lane i holds
+    // them).  Every instruction here delays the words: this branch's
+    // shuffles cost the single copy ~0.3 us a call at r = 16, and a lane
+    // modulo in their place cost more.
+    const int src = lane % mt;
+    const int vm = __shfl(mine, src, 64), vq = __shfl(mine_q, src, 64);
+    if (lane < mt && jr) a.acc_a[(int64_t)(m0 + lane) * r + j] = mine;
+    if (lane < mt * a.xcopies) {
+      const int cpy = lane / mt, m = m0 + (lane - cpy * mt);
+      uint64_t* xc = a.xw + (int64_t)cpy * a.xstride;
+      word_store(xc + (int64_t)m * rp + j, tag, pack_limbs(vm));  // zero limbs for ranks in [r, rp)
+      if (qsum) word_store(xc + (int64_t)M * rp + m, tag, (uint32_t)vq);
+    }
   }
   if (a.epoch && lane == 0) dfssm_dev::advance_if_last(a.epoch, item, old, a.arrivals);
 }
@@ -314,58 +327,89 @@ __device__ void lora_block(const SkinnyArgs& a) {
 // t = limb t of rank j0 + 16kg + e) and, with want_sq, sum Q of token m, for
 // the lane (rho, kg) of the wave that finishes the token tile starting at t0
 // (m = min(t0 + rho, M - 1)): from the LoRA workgroups' words, or computed
-// here once `spin` polls have passed.  The polls are token-major: lane L
-// reads rank j0 + L of each of the tile's nt distinct tokens (one 512-byte
-// load per token) and lanes below nt read the sum-Q words, so a poll round
-// is nt + 1 coalesced loads; the words then reach their lanes through the
-// wave's LDS tile wx [16][kWxPitch] (sq: wq [16]).
+// here once `spin` polls have passed.  CP: the words come in one copy per
+// XCD, and this wave polls its XCD's copy.
+//   - CP and at most NC distinct tokens in the tile (nt): the polls are
+//     token-major.  Lane L reads rank j0 + L of each token (one 512-byte
+//     load per token), lanes below nt read the sum-Q words, and the words
+//     reach their lanes through the wave's LDS tile wx [NC][kWxPitch] (sq:
+//     wq [NC]).  More tokens per round hold more loads in registers: 16
+//     took 31 more VGPRs (a wave per SIMD), and 4 gave the int4 kernel a
+//     stack frame; NC = 4 (int8 factors) or 2 (int4).
+//   - otherwise each lane polls its own 16 words and keeps them once in.
 constexpr int kWxPitch = 68;  // words per token row of wx (16 bytes of skew)
-template <bool L4>
+constexpr int kCoalTokens = 4;
+template <bool L4, bool CP>
 __device__ void fetch_lora(const SkinnyArgs& a, uint32_t tag, int t0, int j0, int rho, int kg, uint32_t* wx,
                            int* wq, v4i (&lm)[4], int* sq, bool store_acc) {
   const int lane = threadIdx.x & 63;
   const int M = a.M, rp = a.rp;
   const int nt = max(1, min(16, M - t0));  // distinct tokens of the tile (tokens past M repeat M - 1)
   const int m = min(t0 + min(rho, nt - 1), M - 1);
-  // this XCD's copy of the words
-  const uint64_t* xc = a.xw + (a.xcopies > 1 ? (int64_t)dfssm_px::xcc_id() * a.xstride : 0);
-  const uint64_t* wp = xc + (int64_t)min(t0, M - 1) * rp + j0 + lane;
-  const uint64_t* sp = xc + (int64_t)M * rp + min(t0 + min(lane, nt - 1), M - 1);
-  bool have = false;
-  for (int it = 0;; ++it) {
-    uint64_t w[16], wqv = 0;
-#pragma unroll
-    for (int i = 0; i < 16; ++i)
-      if (i < nt) w[i] = word_load(wp + (int64_t)i * rp);  // nt is uniform
-    if (sq) wqv = word_load(sp);
-    bool ok = !sq || (uint32_t)(wqv >> 32) == tag;
-#pragma unroll
-    for (int i = 0; i < 16; ++i)
-      if (i < nt) ok = ok && (uint32_t)(w[i] >> 32) == tag;
-    if (__all(ok)) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i)
-        if (i < nt) wx[i * kWxPitch + lane] = (uint32_t)w[i];
-      if (sq && lane < nt) wq[lane] = (int)(uint32_t)wqv;
-      have = true;
-      break;
-    }
-    if (it >= a.spin) break;
-    __builtin_amdgcn_s_sleep(2);
-  }
+  const uint64_t* xc = CP ? a.xw + (int64_t)dfssm_px::xcc_id() * a.xstride : a.xw;
+  constexpr int NC = L4 ? 2 : kCoalTokens;
   uint32_t val[16], vq = 0;
-  if (have) {
-    // the LDS writes above and these reads are the same wave's, in order
-    __builtin_amdgcn_wave_barrier();
-    const int rt = min(rho, nt - 1);
+  bool have = false;
+  if (CP && nt <= NC) {  // uniform
+    const uint64_t* wp = xc + (int64_t)min(t0, M - 1) * rp + j0 + lane;
+    const uint64_t* sp = xc + (int64_t)M * rp + min(t0 + min(lane, nt - 1), M - 1);
+    for (int it = 0;; ++it) {
+      uint64_t w[NC], wqv = 0;
 #pragma unroll
-    for (int d = 0; d < 4; ++d) {
-      const uint4 u = *reinterpret_cast<const uint4*>(wx + rt * kWxPitch + 16 * kg + 4 * d);
-      val[4 * d] = u.x; val[4 * d + 1] = u.y; val[4 * d + 2] = u.z; val[4 * d + 3] = u.w;
+      for (int i = 0; i < NC; ++i)
+        if (i < nt) w[i] = word_load(wp + (int64_t)i * rp);
+      if (sq) wqv = word_load(sp);
+      bool ok = !sq || (uint32_t)(wqv >> 32) == tag;
+#pragma unroll
+      for (int i = 0; i < NC; ++i)
+        if (i < nt) ok = ok && (uint32_t)(w[i] >> 32) == tag;
+      if (__all(ok)) {
+#pragma unroll
+        for (int i = 0; i < NC; ++i)
+          if (i < nt) wx[i * kWxPitch + lane] = (uint32_t)w[i];
+        if (sq && lane < nt) wq[lane] = (int)(uint32_t)wqv;
+        have = true;
+        break;
+      }
+      if (it >= a.spin) break;
+      __builtin_amdgcn_s_sleep(2);
     }
-    if (sq) vq = (uint32_t)wq[rt];
-    __builtin_amdgcn_wave_barrier();  // wx is written again by the next chunk's call
+    if (have) {
+      // the LDS writes above and these reads are the same wave's, in order
+      __builtin_amdgcn_wave_barrier();
+      const int rt = min(rho, nt - 1);
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        const uint4 u = *reinterpret_cast<const uint4*>(wx + rt * kWxPitch + 16 * kg + 4 * d);
+        val[4 * d] = u.x; val[4 * d + 1] = u.y; val[4 * d + 2] = u.z; val[4 * d + 3] = u.w;
+      }
+      if (sq) vq = (uint32_t)wq[rt];
+      __builtin_amdgcn_wave_barrier();  // wx is written again by the next chunk's call
+    }
   } else {
+    const uint64_t* wp = xc + (int64_t)m * rp + j0 + 16 * kg;
+    const uint64_t* sp = xc + (int64_t)M * rp + m;
+    for (int it = 0;; ++it) {
+      if (!have) {
+        uint64_t w[16], wqv = 0;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) w[e] = word_load(wp + e);
+        if (sq) wqv = word_load(sp);
+        bool ok = !sq || (uint32_t)(wqv >> 32) == tag;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) ok = ok && (uint32_t)(w[e] >> 32) == tag;
+        if (ok) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) val[e] = (uint32_t)w[e];
+          vq = (uint32_t)wqv;
+          have = true;
+        }
+      }
+      if (__all(have) || it >= a.spin) break;
+      __builtin_amdgcn_s_sleep(2);
+    }
+  }
+  if (!have) {
     // the LoRA workgroups' words did not arrive: compute them here
 #pragma unroll 1
     for (int e = 0; e < 16; ++e) {
@@ -388,14 +432,15 @@ __device__ void fetch_lora(const SkinnyArgs& a, uint32_t tag, int t0, int j0, in
   if (sq) *sq = (int)vq;
 }
 
-// MT token tiles of 16 (M <= 16*MT); S MFMA steps per lane per iteration.
+// MT token tiles of 16 (M <= 16*MT); S MFMA steps per lane per iteration;
+// CP: the LoRA words come in one copy per XCD (a.xcopies == 8).
 // Block: 16 output rows, nw = blockDim.x / 64 waves (nw >= MT), wave w takes
 // iterations w, w + nw, ... of 64*S columns each.
-template <int MT, int S, bool L4>
+template <int MT, int S, bool L4, bool CP>
 __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   __shared__ v4i red[kMaxWaves][MT][64];
-  __shared__ __align__(16) uint32_t wx[MT][16 * kWxPitch];
-  __shared__ int wq[MT][16];
+  __shared__ __align__(16) uint32_t wx[MT][CP ? kCoalTokens * kWxPitch : 4];
+  __shared__ int wq[MT][CP ? kCoalTokens : 1];
   __shared__ uint32_t tag_lds;
   if ((int)blockIdx.x < a.nb_lora) {
     if (blockIdx.y == 0) lora_block<L4>(a);  // one set of LoRA workgroups for all tokens
@@ -525,7 +570,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   v4i lm[4];
   int sq = 0;
   const bool keep = (int)blockIdx.x == a.nb_lora && mtok < M;
-  fetch_lora<L4>(a, tag, mb + 16 * wave, 0, rho, kg, wx[wave], wq[wave], lm, &sq, keep);
+  fetch_lora<L4, CP>(a, tag, mb + 16 * wave, 0, rho, kg, wx[wave], wq[wave], lm, &sq, keep);
 
   // LoRA up-projection, limbs 3, 2, 1, 0 over the 64-rank chunks
   if (L4 && bpacked) {
@@ -545,7 +590,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
     for (int j0 = 64; j0 < a.rp; j0 += 64) {
       const v4i bl = load16_row_guarded<L4>(a.B + (int64_t)nrow * bpitch, j0 + 16 * kg, r, ba);
       v4i lj[4];
-      fetch_lora<L4>(a, tag, mb + 16 * wave, j0, rho, kg, wx[wave], wq[wave], lj, nullptr, keep);
+      fetch_lora<L4, CP>(a, tag, mb + 16 * wave, j0, rho, kg, wx[wave], wq[wave], lj, nullptr, keep);
       e3 = mfma(bl, lj[3], e3);
       e2 = mfma(bl, lj[2], e2);
       e1 = mfma(bl, lj[1], e1);
@@ -579,13 +624,20 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   }
 }
 
-template <int MT, int S, bool L4>
+template <int MT, int S, bool L4, bool CP>
 hipError_t launch_t(const SkinnyArgs& a, int nw, hipStream_t st) {
   // x: LoRA workgroups then 16-row output blocks; y: 32-token chunks
   const int64_t blocks = a.nb_lora + dfssm::ceil_div(a.N, 16);
   const int64_t chunks = dfssm::ceil_div(a.M, 16 * MT);
-  mfma_skinny<MT, S, L4><<<dim3((unsigned)blocks, (unsigned)chunks), dim3(64 * nw), 0, st>>>(a);
+  mfma_skinny<MT, S, L4, CP><<<dim3((unsigned)blocks, (unsigned)chunks), dim3(64 * nw), 0, st>>>(a);
   return hipGetLastError();
+}
+
+template <bool L4, bool CP>
+hipError_t launch_tiles(const SkinnyArgs& a, int mt, int S, int nw, hipStream_t st) {
+  if (mt == 1) return S == 8 ? launch_t<1, 8, L4, CP>(a, nw, st) : launch_t<1, 4, L4, CP>(a, nw, st);
+  if (mt == 2) return S == 8 ? launch_t<2, 8, L4, CP>(a, nw, st) : launch_t<2, 4, L4, CP>(a, nw, st);
+  return launch_t<4, 4, L4, CP>(a, nw, st);
 }
 
 // Tag of a call enqueued outside graph capture: a process-wide counter with
@@ -638,18 +690,22 @@ hipError_t skinny_impl(const int8_t* q, const float* s, int64_t M, int64_t K, in
     cap = hipStreamCaptureStatusActive;
   }
   const bool device_epoch = cap != hipStreamCaptureStatusNone;
-  const int64_t xstride = M * rp + M;
-  const int xcopies = 8 * xstride <= kXwWords ? 8 : 1;
+  // One copy of the LoRA words per XCD, each on a 256-byte boundary (no
+  // cache line holds words of two copies), when the LoRA down-projection
+  // is the longer path (r > 32) at up to kCoalTokens tokens: every output
+  // workgroup then waits on the words, and the copies took 1.2-2.3 us off
+  // a call at M = 1 to 4 (1.3B projections, r = 64; int4 at M = 3, 4, where
+  // the polls go lane by lane: 0.8 us).  At r <= 32 the words are mostly in
+  // before the first poll, and from 5 tokens the lane-by-lane polls of one
+  // copy were as fast or faster.
+  const int64_t xstride = round_up(M * rp + M, 32);
+  const int xcopies = r > 32 && M <= kCoalTokens && 8 * xstride <= kXwWords ? 8 : 1;
   SkinnyArgs a{q, s, (int)M, (int)K, (int)N, (int)r, rp, w_bits, alpha, A, B, beta, y, acc_s, acc_b,
                ws.acc_a, ws.xw, xstride, xcopies, device_epoch ? ws.epoch : nullptr, device_epoch ? 0u : host_tag(),
                arrivals, (int)(local_only ? 0 : lora_waves), nb_lora, local_only ? 0 : (1 << 14)};
-  hipError_t e;
-  if (mt == 1)
-    e = S == 8 ? launch_t<1, 8, L4>(a, nw, st) : launch_t<1, 4, L4>(a, nw, st);
-  else if (mt == 2)
-    e = S == 8 ? launch_t<2, 8, L4>(a, nw, st) : launch_t<2, 4, L4>(a, nw, st);
-  else
-    e = launch_t<4, 4, L4>(a, nw, st);
+  // the two poll forms are separate instantiations: in one kernel their
+  // union of registers cost a wave per SIMD and spilled
+  hipError_t e = xcopies > 1 ? launch_tiles<L4, true>(a, mt, S, nw, st) : launch_tiles<L4, false>(a, mt, S, nw, st);
   if (e != hipSuccess) return e;
   if (acc_a_out && r > 0)
     e = hipMemcpyAsync(acc_a_out, ws.acc_a, (size_t)(M * r) * 4, hipMemcpyDeviceToDevice, st);

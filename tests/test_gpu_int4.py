@@ -53,6 +53,7 @@ SHAPES = [
     # (M, K, N, r)
     (1, 2048, 8512, 64),     # Mamba-2-1.3B in_proj
     (1, 4096, 2048, 64),     # Mamba-2-1.3B out_proj
+    (2, 4096, 2048, 64),     # the most tokens the copies' token-major polls take (int4)
     (4, 4096, 2048, 64),
     (17, 4096, 2048, 64),    # two token tiles
     (32, 2048, 300, 64),

@@ -167,6 +167,7 @@ def test_linear_int8_min(env, path, M, K, N, r):
 FSHAPES = [
     (1, 768, 3352, 16),      # Mamba-2-130M in_proj: 3 waves
     (1, 2048, 8512, 64),     # Mamba-2-1.3B in_proj
+    (4, 2048, 8512, 64),     # the most tokens the copies' token-major polls take (int8)
     (5, 4096, 2048, 64),     # Mamba-2-1.3B out_proj, small batches
     (16, 4096, 2048, 64),
     (17, 4096, 2048, 64),
