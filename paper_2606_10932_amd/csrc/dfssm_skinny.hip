@@ -339,9 +339,45 @@ __device__ void lora_block(const SkinnyArgs& a) {
 //   - otherwise each lane polls its own 16 words and keeps them once in.
 constexpr int kWxPitch = 68;  // words per token row of wx (16 bytes of skew)
 constexpr int kCoalTokens = 4;
+
+// Token-major polls of n <= NC consecutive tokens from tok0 (tok0 + n <= M)
+// in the copy xc: lane L reads rank j0 + L of each, lanes below n the sum-Q
+// words (want_sq).  On success the words are in wx rows 0 .. n-1 and wq[0 ..
+// n-1]; false once `spin` polls have passed without all of them.
+template <int NC>
+__device__ bool poll_tokens(const SkinnyArgs& a, uint32_t tag, const uint64_t* xc, int tok0, int n, int j0,
+                            bool want_sq, uint32_t* wx, int* wq) {
+  const int lane = threadIdx.x & 63;
+  const int rp = a.rp;
+  const uint64_t* wp = xc + (int64_t)tok0 * rp + j0 + lane;
+  const uint64_t* sp = xc + (int64_t)a.M * rp + tok0 + min(lane, n - 1);
+  for (int it = 0;; ++it) {
+    uint64_t w[NC], wqv = 0;
+#pragma unroll
+    for (int i = 0; i < NC; ++i)
+      if (i < n) w[i] = word_load(wp + (int64_t)i * rp);  // n is uniform
+    if (want_sq) wqv = word_load(sp);
+    bool ok = !want_sq || (uint32_t)(wqv >> 32) == tag;
+#pragma unroll
+    for (int i = 0; i < NC; ++i)
+      if (i < n) ok = ok && (uint32_t)(w[i] >> 32) == tag;
+    if (__all(ok)) {
+#pragma unroll
+      for (int i = 0; i < NC; ++i)
+        if (i < n) wx[i * kWxPitch + lane] = (uint32_t)w[i];
+      if (want_sq && lane < n) wq[lane] = (int)(uint32_t)wqv;
+      return true;
+    }
+    if (it >= a.spin) return false;
+    __builtin_amdgcn_s_sleep(2);
+  }
+}
+
+// pre: 0 poll here; 1 the tile's words are already in wx / wq (the
+// workgroup's waves polled them together); 2 those polls gave up.
 template <bool L4, bool CP>
 __device__ void fetch_lora(const SkinnyArgs& a, uint32_t tag, int t0, int j0, int rho, int kg, uint32_t* wx,
-                           int* wq, v4i (&lm)[4], int* sq, bool store_acc) {
+                           int* wq, v4i (&lm)[4], int* sq, bool store_acc, int pre) {
   const int lane = threadIdx.x & 63;
   const int M = a.M, rp = a.rp;
   const int nt = max(1, min(16, M - t0));  // distinct tokens of the tile (tokens past M repeat M - 1)
@@ -350,30 +386,11 @@ __device__ void fetch_lora(const SkinnyArgs& a, uint32_t tag, int t0, int j0, in
   constexpr int NC = L4 ? 2 : kCoalTokens;
   uint32_t val[16], vq = 0;
   bool have = false;
-  if (CP && nt <= NC) {  // uniform
-    const uint64_t* wp = xc + (int64_t)min(t0, M - 1) * rp + j0 + lane;
-    const uint64_t* sp = xc + (int64_t)M * rp + min(t0 + min(lane, nt - 1), M - 1);
-    for (int it = 0;; ++it) {
-      uint64_t w[NC], wqv = 0;
-#pragma unroll
-      for (int i = 0; i < NC; ++i)
-        if (i < nt) w[i] = word_load(wp + (int64_t)i * rp);
-      if (sq) wqv = word_load(sp);
-      bool ok = !sq || (uint32_t)(wqv >> 32) == tag;
-#pragma unroll
-      for (int i = 0; i < NC; ++i)
-        if (i < nt) ok = ok && (uint32_t)(w[i] >> 32) == tag;
-      if (__all(ok)) {
-#pragma unroll
-        for (int i = 0; i < NC; ++i)
-          if (i < nt) wx[i * kWxPitch + lane] = (uint32_t)w[i];
-        if (sq && lane < nt) wq[lane] = (int)(uint32_t)wqv;
-        have = true;
-        break;
-      }
-      if (it >= a.spin) break;
-      __builtin_amdgcn_s_sleep(2);
-    }
+  if (CP && (pre != 0 || nt <= NC)) {  // uniform
+    if (pre == 0)
+      have = poll_tokens<NC>(a, tag, xc, min(t0, M - 1), nt, j0, sq != nullptr, wx, wq);
+    else
+      have = pre == 1;
     if (have) {
       // the LDS writes above and these reads are the same wave's, in order
       __builtin_amdgcn_wave_barrier();
@@ -433,14 +450,18 @@ __device__ void fetch_lora(const SkinnyArgs& a, uint32_t tag, int t0, int j0, in
 }
 
 // MT token tiles of 16 (M <= 16*MT); S MFMA steps per lane per iteration;
-// CP: the LoRA words come in one copy per XCD (a.xcopies == 8).
+// PM: how the output waves get the LoRA words: 0 from one copy, lane by
+// lane; 1 from their XCD's copy (a.xcopies == 8), the finishing wave alone;
+// 2 (MT == 1) from their XCD's copy, several waves together.
 // Block: 16 output rows, nw = blockDim.x / 64 waves (nw >= MT), wave w takes
 // iterations w, w + nw, ... of 64*S columns each.
-template <int MT, int S, bool L4, bool CP>
+template <int MT, int S, bool L4, int PM>
 __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
+  constexpr bool CP = PM > 0;
   __shared__ v4i red[kMaxWaves][MT][64];
-  __shared__ __align__(16) uint32_t wx[MT][CP ? kCoalTokens * kWxPitch : 4];
-  __shared__ int wq[MT][CP ? kCoalTokens : 1];
+  __shared__ __align__(16) uint32_t wx[MT][PM == 2 ? 16 * kWxPitch : (CP ? kCoalTokens * kWxPitch : 4)];
+  __shared__ int wq[MT][PM == 2 ? 16 : (CP ? kCoalTokens : 1)];
+  __shared__ int gok[PM == 2 ? kMaxWaves : 1];
   __shared__ uint32_t tag_lds;
   if ((int)blockIdx.x < a.nb_lora) {
     if (blockIdx.y == 0) lora_block<L4>(a);  // one set of LoRA workgroups for all tokens
@@ -559,8 +580,30 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
     }
   }
   __syncthreads();
-  if (!fin) return;
   const uint32_t tag = tag_lds;
+  // with more tokens than one wave's polls take (G), the first ceil(n / G)
+  // waves of a one-tile workgroup each poll G tokens into the tile's LDS
+  // rows, and all meet at a barrier (one wave holding 16 tokens' loads
+  // would take 31 more VGPRs)
+  int pre = 0;
+  if constexpr (PM == 2 && MT == 1) {
+    {
+      constexpr int G = L4 ? 2 : kCoalTokens;
+      const int ntk = max(1, min(16, M - mb));
+      const int ng = (ntk + G - 1) / G;  // <= nw (host)
+      if (wave < ng) {
+        const uint64_t* xc = a.xw + (int64_t)dfssm_px::xcc_id() * a.xstride;
+        const int t = G * wave, n = min(G, ntk - t);
+        const bool ok = poll_tokens<G>(a, tag, xc, mb + t, n, 0, true, wx[0] + t * kWxPitch, wq[0] + t);
+        if (lane == 0) gok[wave] = ok ? 1 : 0;
+      }
+      __syncthreads();
+      pre = 1;
+      for (int w = 0; w < ng; ++w)
+        if (gok[w] == 0) pre = 2;
+    }
+  }
+  if (!fin) return;
   v4i d = red[0][wave][lane];
   for (int w = 1; w < nw; ++w) d += red[w][wave][lane];
 
@@ -570,7 +613,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   v4i lm[4];
   int sq = 0;
   const bool keep = (int)blockIdx.x == a.nb_lora && mtok < M;
-  fetch_lora<L4, CP>(a, tag, mb + 16 * wave, 0, rho, kg, wx[wave], wq[wave], lm, &sq, keep);
+  fetch_lora<L4, CP>(a, tag, mb + 16 * wave, 0, rho, kg, wx[wave], wq[wave], lm, &sq, keep, pre);
 
   // LoRA up-projection, limbs 3, 2, 1, 0 over the 64-rank chunks
   if (L4 && bpacked) {
@@ -590,7 +633,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
     for (int j0 = 64; j0 < a.rp; j0 += 64) {
       const v4i bl = load16_row_guarded<L4>(a.B + (int64_t)nrow * bpitch, j0 + 16 * kg, r, ba);
       v4i lj[4];
-      fetch_lora<L4, CP>(a, tag, mb + 16 * wave, j0, rho, kg, wx[wave], wq[wave], lj, nullptr, keep);
+      fetch_lora<L4, CP>(a, tag, mb + 16 * wave, j0, rho, kg, wx[wave], wq[wave], lj, nullptr, keep, 0);
       e3 = mfma(bl, lj[3], e3);
       e2 = mfma(bl, lj[2], e2);
       e1 = mfma(bl, lj[1], e1);
@@ -624,20 +667,24 @@ __global__ __launch_bounds__(64 * kMaxWaves) void mfma_skinny(SkinnyArgs a) {
   }
 }
 
-template <int MT, int S, bool L4, bool CP>
+template <int MT, int S, bool L4, int PM>
 hipError_t launch_t(const SkinnyArgs& a, int nw, hipStream_t st) {
   // x: LoRA workgroups then 16-row output blocks; y: 32-token chunks
   const int64_t blocks = a.nb_lora + dfssm::ceil_div(a.N, 16);
   const int64_t chunks = dfssm::ceil_div(a.M, 16 * MT);
-  mfma_skinny<MT, S, L4, CP><<<dim3((unsigned)blocks, (unsigned)chunks), dim3(64 * nw), 0, st>>>(a);
+  mfma_skinny<MT, S, L4, PM><<<dim3((unsigned)blocks, (unsigned)chunks), dim3(64 * nw), 0, st>>>(a);
   return hipGetLastError();
 }
 
-template <bool L4, bool CP>
+// the copy forms (PM > 0) are taken at M <= 8: one token tile
+template <bool L4, int PM>
 hipError_t launch_tiles(const SkinnyArgs& a, int mt, int S, int nw, hipStream_t st) {
-  if (mt == 1) return S == 8 ? launch_t<1, 8, L4, CP>(a, nw, st) : launch_t<1, 4, L4, CP>(a, nw, st);
-  if (mt == 2) return S == 8 ? launch_t<2, 8, L4, CP>(a, nw, st) : launch_t<2, 4, L4, CP>(a, nw, st);
-  return launch_t<4, 4, L4, CP>(a, nw, st);
+  if (mt == 1) return S == 8 ? launch_t<1, 8, L4, PM>(a, nw, st) : launch_t<1, 4, L4, PM>(a, nw, st);
+  if constexpr (PM == 0) {
+    if (mt == 2) return S == 8 ? launch_t<2, 8, L4, PM>(a, nw, st) : launch_t<2, 4, L4, PM>(a, nw, st);
+    return launch_t<4, 4, L4, PM>(a, nw, st);
+  }
+  return hipErrorInvalidValue;
 }
 
 // Tag of a call enqueued outside graph capture: a process-wide counter with
@@ -698,14 +745,23 @@ hipError_t skinny_impl(const int8_t* q, const float* s, int64_t M, int64_t K, in
   // the polls go lane by lane: 0.8 us).  At r <= 32 the words are mostly in
   // before the first poll, and from 5 tokens the lane-by-lane polls of one
   // copy were as fast or faster.
+  // From G + 1 to 8 tokens (G = 4, or 2 with int4 factors) and one chunk of
+  // 64 ranks, the copies are polled by ceil(M / G) waves together (1.3B,
+  // r = 64, M = 5 / 8: in_proj 8.6 -> 7.4 / 8.4 -> 8.0 us, out_proj M = 8
+  // 8.4 -> 7.7; int4 in_proj M = 4 / 8 8.6 -> 7.6 / ~10 -> 8.4).  At 16
+  // tokens they were no faster than one copy polled lane by lane.
   const int64_t xstride = round_up(M * rp + M, 32);
-  const int xcopies = r > 32 && M <= kCoalTokens && 8 * xstride <= kXwWords ? 8 : 1;
+  const int64_t gsize = L4 ? 2 : kCoalTokens;
+  const bool group = rp == 64 && M > gsize && M <= 8 && ceil_div(M, gsize) <= nw;
+  const int xcopies = r > 32 && (M <= kCoalTokens || group) && 8 * xstride <= kXwWords ? 8 : 1;
   SkinnyArgs a{q, s, (int)M, (int)K, (int)N, (int)r, rp, w_bits, alpha, A, B, beta, y, acc_s, acc_b,
                ws.acc_a, ws.xw, xstride, xcopies, device_epoch ? ws.epoch : nullptr, device_epoch ? 0u : host_tag(),
                arrivals, (int)(local_only ? 0 : lora_waves), nb_lora, local_only ? 0 : (1 << 14)};
   // the two poll forms are separate instantiations: in one kernel their
   // union of registers cost a wave per SIMD and spilled
-  hipError_t e = xcopies > 1 ? launch_tiles<L4, true>(a, mt, S, nw, st) : launch_tiles<L4, false>(a, mt, S, nw, st);
+  hipError_t e = xcopies == 1 ? launch_tiles<L4, 0>(a, mt, S, nw, st)
+                 : group       ? launch_tiles<L4, 2>(a, mt, S, nw, st)
+                               : launch_tiles<L4, 1>(a, mt, S, nw, st);
   if (e != hipSuccess) return e;
   if (acc_a_out && r > 0)
     e = hipMemcpyAsync(acc_a_out, ws.acc_a, (size_t)(M * r) * 4, hipMemcpyDeviceToDevice, st);

@@ -55,6 +55,8 @@ SHAPES = [
     (1, 4096, 2048, 64),     # Mamba-2-1.3B out_proj
     (2, 4096, 2048, 64),     # the most tokens the copies' token-major polls take (int4)
     (4, 4096, 2048, 64),
+    (7, 2048, 8512, 64),     # the copies polled by four waves together (2 tokens each)
+    (16, 2048, 8512, 64),    # more tokens than the waves' group polls take: one copy
     (17, 4096, 2048, 64),    # two token tiles
     (32, 2048, 300, 64),
     (3, 160, 77, 6),         # r % 16 != 0: packed B rows of 3 bytes

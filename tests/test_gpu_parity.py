@@ -169,6 +169,9 @@ FSHAPES = [
     (1, 2048, 8512, 64),     # Mamba-2-1.3B in_proj
     (4, 2048, 8512, 64),     # the most tokens the copies' token-major polls take (int8)
     (5, 4096, 2048, 64),     # Mamba-2-1.3B out_proj, small batches
+    (7, 2048, 8512, 64),     # the copies polled by two waves together, the second with 3 tokens
+    (8, 2048, 8512, 64),
+    (13, 2048, 8512, 64),    # above 8 tokens: one copy again
     (16, 4096, 2048, 64),
     (17, 4096, 2048, 64),
     (32, 4096, 2048, 64),

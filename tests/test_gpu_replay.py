@@ -41,7 +41,7 @@ def _capture(torch, fn):
     return g
 
 
-@pytest.mark.parametrize("M", [1, 17])
+@pytest.mark.parametrize("M", [1, 8, 17])
 @pytest.mark.parametrize("K,N", [(2048, 8512), (4096, 2048)])   # Mamba-2-1.3B in_proj, out_proj
 def test_linear_graph_replays(env, K, N, M):
     torch, D, o = env
