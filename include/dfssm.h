@@ -562,6 +562,9 @@ dfssm_status dfssm_mamba2_status(const dfssm_mamba2_model* model, int64_t M, con
  *                                  kernel on the prefill path
  *   DFSSM_TEST_LM_HEAD_MFMA_TOKENS n > 0: the LM head runs on the matrix
  *                                  cores from n tokens instead of 8
+ *   DFSSM_TEST_LM_HEAD_TILED_TOKENS n > 0: on the matrix cores, the tiled
+ *                                  kernel (both operands staged in LDS)
+ *                                  from n tokens instead of 64
  *   DFSSM_TEST_STEP_PER_KERNEL     1: the decode step at M = 1 runs the
  *                                  per-kernel sequence on a prepared
  *                                  workspace too; 2: the fused step takes
@@ -573,7 +576,8 @@ typedef enum {
   DFSSM_TEST_LOCAL_LORA = 1,
   DFSSM_TEST_PREFILL_KERNEL = 2,
   DFSSM_TEST_LM_HEAD_MFMA_TOKENS = 3,
-  DFSSM_TEST_STEP_PER_KERNEL = 4
+  DFSSM_TEST_STEP_PER_KERNEL = 4,
+  DFSSM_TEST_LM_HEAD_TILED_TOKENS = 5
 } dfssm_test_switch_id;
 dfssm_status dfssm_test_switch(int which, int value);
 

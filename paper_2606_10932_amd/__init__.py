@@ -32,6 +32,7 @@ EXPORTS = ["dfssm_quantize_act", "dfssm_linear_workspace_bytes", "dfssm_scaffold
            "dfssm_test_switch", "dfssm_status_string", "dfssm_last_error",
            "dfssm_version"]
 TEST_LOCAL_LORA, TEST_PREFILL_KERNEL, TEST_LM_HEAD_MFMA_TOKENS, TEST_STEP_PER_KERNEL = 1, 2, 3, 4
+TEST_LM_HEAD_TILED_TOKENS = 5
 
 
 class DfssmError(RuntimeError):

@@ -63,7 +63,7 @@ dfssm_status check_ptrs(std::initializer_list<Ptr> required, std::initializer_li
   return DFSSM_OK;
 }
 
-std::atomic<int> g_switch[5];  // dfssm_test_switch values, index = switch id
+std::atomic<int> g_switch[6];  // dfssm_test_switch values, index = switch id
 
 size_t linear_ws_bytes(int64_t M, int64_t K, int64_t r) {
   return dfssm::carve_linear_workspace(nullptr, M, K, r).bytes;
@@ -141,7 +141,7 @@ hipError_t launch_linear_i4(int path, const int8_t* q, const float* s, int64_t M
 }  // namespace
 
 namespace dfssm {
-int test_switch(int which) { return which > 0 && which < 5 ? g_switch[which].load(std::memory_order_relaxed) : 0; }
+int test_switch(int which) { return which > 0 && which < 6 ? g_switch[which].load(std::memory_order_relaxed) : 0; }
 }  // namespace dfssm
 
 extern "C" {
@@ -154,6 +154,7 @@ dfssm_status dfssm_test_switch(int which, int value) {
     case DFSSM_TEST_PREFILL_KERNEL: ok = value == 0 || value == 4 || value == 8; break;
     case DFSSM_TEST_LM_HEAD_MFMA_TOKENS: ok = value >= 0; break;
     case DFSSM_TEST_STEP_PER_KERNEL: ok = value >= 0 && value <= 2; break;
+    case DFSSM_TEST_LM_HEAD_TILED_TOKENS: ok = value >= 0; break;
     default: break;
   }
   if (!ok) return fail(DFSSM_ERR_SHAPE, "test switch %d: value %d", which, value);

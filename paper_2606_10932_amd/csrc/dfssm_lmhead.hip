@@ -23,6 +23,7 @@
 #include <stdlib.h>
 
 #include "dfssm_internal.hpp"
+#include "dfssm_persist.hpp"
 
 namespace {
 
@@ -33,6 +34,13 @@ constexpr int kThreads = 256;
 int lm_head_mfma_tokens() {
   const int v = dfssm::test_switch(DFSSM_TEST_LM_HEAD_MFMA_TOKENS);
   return v > 0 ? v : 8;
+}
+
+// Tokens from which the matrix-core path runs the tiled kernel (64; the
+// test switch lm_head_tiled_tokens moves it).
+int lm_head_tiled_tokens() {
+  const int v = dfssm::test_switch(DFSSM_TEST_LM_HEAD_TILED_TOKENS);
+  return v > 0 ? v : 64;
 }
 
 // rows per wave visit: 4 KB of the table, or one row when rows are longer
@@ -264,6 +272,157 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void lm_head_mfma(const int8_t*
   }
 }
 
+// ---- many tokens, tiled: a GEMM with both operands staged in LDS --------
+// A workgroup (4 waves) owns kTlRows vocabulary rows x TB tokens; wave
+// (wr, wt) = (w & 1, w >> 1) owns rows 64 wr .. +63 (4 row tiles) and
+// tokens TB/2 wt .. +TB/2-1 (TB/32 token tiles).  Each 64-column stage of
+// the E rows and the Q rows is brought into a ring of kTlRing LDS slots by
+// direct-to-LDS loads, 16-byte chunk c of row r at position c ^ ((r >> 1)
+// & 3) (as the prefill kernel's Q tiles: conflict-free reads); one wait and
+// one barrier per stage.  E and Q place column 64 st + 16 kg + b in byte b of
+// lane (row, kg) alike, so the int32 sums equal the other kernels' and the
+// logits keep their fp32 order.  Workgroup id: the ntb token blocks of a row
+// block are consecutive ids with the same id mod 8, so they run on one XCD
+// back to back and read the row block's 256 KB of the table from HBM once.
+constexpr int kTlRows = 128;
+constexpr int kTlRing = 3;
+constexpr int kTlThreads = 256;
+
+template <int TB>
+__global__ __launch_bounds__(kTlThreads, 2) void lm_head_tiled(const int8_t* __restrict__ q,
+                                                              const float* __restrict__ s, int M, int d,
+                                                              const int8_t* __restrict__ E,
+                                                              const float* __restrict__ scale, int V,
+                                                              float* __restrict__ logits,
+                                                              int32_t* __restrict__ acc_out, int nrb, int ntb) {
+  constexpr int kStageE = kTlRows * 64, kStageQ = TB * 64, kStage = kStageE + kStageQ;
+  constexpr int NJ = TB / 32;                // token tiles per wave
+  constexpr int LE = kTlRows / 64, LQ = TB / 64;  // direct-to-LDS loads per wave per stage (1 KB each)
+  __shared__ __align__(16) int8_t ring[kTlRing * kStage];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int rho = lane & 15, kg = lane >> 4;
+  const int id = (int)blockIdx.x, x = id & 7, k = id >> 3;
+  const int tb = k % ntb, rb = (k / ntb) * 8 + x;
+  if (rb >= nrb) return;
+  const int v0 = rb * kTlRows, m0 = tb * TB;
+  // lane offsets of this wave's loads: 16 rows of 64 bytes per load, lane i
+  // takes row i / 4 and the chunk that belongs at position i % 4 (rows and
+  // tokens past the ends repeat the last one; their results are not stored)
+  uint32_t voe[LE], voq[LQ];
+#pragma unroll
+  for (int u = 0; u < LE; ++u) {
+    const int rl = 16 * (LE * wave + u) + (lane >> 2);
+    const int c = (lane & 3) ^ ((rl >> 1) & 3);
+    voe[u] = (uint32_t)min(v0 + rl, V - 1) * (uint32_t)d + 16u * (uint32_t)c;
+  }
+#pragma unroll
+  for (int u = 0; u < LQ; ++u) {
+    const int tl = 16 * (wave + 4 * u) + (lane >> 2);
+    const int c = (lane & 3) ^ ((tl >> 1) & 3);
+    voq[u] = (uint32_t)min(m0 + tl, M - 1) * (uint32_t)d + 16u * (uint32_t)c;
+  }
+  const uint32_t ring0 = dfssm_px::lds_addr(ring);
+  const int ns = d / 64;
+  auto issue = [&](int st) {
+    const uint32_t slot = ring0 + (uint32_t)((st % kTlRing) * kStage);
+#pragma unroll
+    for (int u = 0; u < LE; ++u) dfssm_px::lds_dma16(voe[u], E + 64 * st, slot + (uint32_t)((LE * wave + u) * 1024));
+#pragma unroll
+    for (int u = 0; u < LQ; ++u)
+      dfssm_px::lds_dma16(voq[u], q + 64 * st, slot + (uint32_t)(kStageE + (wave + 4 * u) * 1024));
+  };
+  const int wr = wave & 1, wt = wave >> 1;
+  v4i acc[4][NJ];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+  for (int st = 0; st < kTlRing - 1 && st < ns; ++st) issue(st);
+  for (int st = 0; st < ns; ++st) {
+    // this wave's loads of stage st are in once at most the loads of the
+    // later stages it has issued remain; the barrier then makes
+    // every wave's loads visible and frees the slot of stage st - 1
+    static_assert(kTlRing >= 2 && kTlRing <= 6, "wait counts below cover rings of 2 to 6 slots");
+    switch (min(ns - 1 - st, kTlRing - 2)) {  // the later stages issued
+      case 4: CHAIN_WAIT_VMCNT(4 * (LE + LQ)); break;
+      case 3: CHAIN_WAIT_VMCNT(3 * (LE + LQ)); break;
+      case 2: CHAIN_WAIT_VMCNT(2 * (LE + LQ)); break;
+      case 1: CHAIN_WAIT_VMCNT(LE + LQ); break;
+      default: CHAIN_WAIT_VMCNT(0); break;
+    }
+    CHAIN_BARRIER();
+    if (st + kTlRing - 1 < ns) issue(st + kTlRing - 1);
+    const int8_t* sl = ring + (st % kTlRing) * kStage;
+    v4i a[4], b[NJ];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 64 * wr + 16 * i + rho;
+      a[i] = *reinterpret_cast<const v4i*>(sl + r * 64 + 16 * (kg ^ ((r >> 1) & 3)));
+    }
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int t = (TB / 2) * wt + 16 * j + rho;
+      b[j] = *reinterpret_cast<const v4i*>(sl + kStageE + t * 64 + 16 * (kg ^ ((t >> 1) & 3)));
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[i], b[j], acc[i][j], 0, 0, 0);
+  }
+  // lane (rho, kg) of tile (i, j) holds D[row 64 wr + 16 i + 4 kg + v][token TB/2 wt + 16 j + rho]
+  const bool vec_store = (V & 3) == 0;
+  float sm[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) sm[j] = s[min(m0 + (TB / 2) * wt + 16 * j + rho, M - 1)];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row0 = v0 + 64 * wr + 16 * i + 4 * kg;
+    const bool whole = vec_store && row0 + 3 < V;
+    float sc[4];
+    if (whole) {
+      const float4 t = *reinterpret_cast<const float4*>(scale + row0);
+      sc[0] = t.x; sc[1] = t.y; sc[2] = t.z; sc[3] = t.w;
+    } else {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) sc[v] = row0 + v < V ? scale[row0 + v] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int m = m0 + (TB / 2) * wt + 16 * j + rho;
+      if (m >= M) continue;
+      const v4i sum = acc[i][j];
+      if (whole) {
+        const float t0 = sc[0] * (float)sum[0], t1 = sc[1] * (float)sum[1];
+        const float t2 = sc[2] * (float)sum[2], t3 = sc[3] * (float)sum[3];
+        if (logits)
+          *reinterpret_cast<float4*>(logits + (int64_t)m * V + row0) =
+              make_float4(sm[j] * t0, sm[j] * t1, sm[j] * t2, sm[j] * t3);
+        if (acc_out) *reinterpret_cast<int4*>(acc_out + (int64_t)m * V + row0) = make_int4(sum[0], sum[1], sum[2], sum[3]);
+      } else {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          if (row0 + v < V) {
+            const float tv = sc[v] * (float)sum[v];
+            if (logits) logits[(int64_t)m * V + row0 + v] = sm[j] * tv;
+            if (acc_out) acc_out[(int64_t)m * V + row0 + v] = sum[v];
+          }
+        }
+      }
+    }
+  }
+}
+
+template <int TB>
+hipError_t launch_tiled(const int8_t* q, const float* s, int64_t M, int64_t d, const int8_t* E, const float* scale,
+                        int64_t V, float* logits, int32_t* acc, hipStream_t st) {
+  const int64_t nrb = dfssm::ceil_div(V, kTlRows), ntb = dfssm::ceil_div(M, TB);
+  const int64_t blocks = dfssm::ceil_div(nrb, 8) * 8 * ntb;
+  lm_head_tiled<TB><<<dim3((unsigned)blocks), dim3(kTlThreads), 0, st>>>(q, s, (int)M, (int)d, E, scale, (int)V, logits,
+                                                                         acc, (int)nrb, (int)ntb);
+  return hipGetLastError();
+}
+
 // MFMA steps per wave for row length d, or 0 when the MFMA kernel does not
 // take it (d % 64 != 0, or no split of d / 64 steps over 4..8 waves of at
 // most 8 steps)
@@ -345,6 +504,10 @@ hipError_t launch_lm_head(const int8_t* q, const float* s, int64_t M, int64_t d,
   // below as GEMV passes of up to 4 tokens
   const int ks = mfma_steps(d);
   if (M >= lm_head_mfma_tokens() && ks > 0) {
+    // from 64 tokens the tiled kernel (its load offsets are 32-bit)
+    if (M >= lm_head_tiled_tokens() && V * d < (int64_t)1 << 31 && M * d < (int64_t)1 << 31)
+      return M >= 128 ? launch_tiled<128>(q, s, M, d, E, scale, V, logits, acc, st)
+                      : launch_tiled<64>(q, s, M, d, E, scale, V, logits, acc, st);
     switch (ks) {
       case 1: return launch_mfma<1>(q, s, M, d, E, scale, V, logits, acc, st);
       case 2: return launch_mfma<2>(q, s, M, d, E, scale, V, logits, acc, st);

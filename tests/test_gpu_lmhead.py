@@ -66,10 +66,15 @@ LSHAPES = [
     (2, 16384, 65),     # the longest row: 1 token per pass
     # from 8 tokens the matrix-core kernel (d a multiple of 64 split over 4..8 waves)
     (8, 2048, 50280),   # the 1.3B table, the smallest batch it takes
-    (64, 2048, 50280),
-    (300, 768, 1001),   # ragged token and row tiles, 6 waves
     (17, 1024, 77),
     (40, 4096, 130),    # 8 steps per wave
+    # from 64 tokens the tiled kernel (64-token blocks below 128 tokens, 128 from there)
+    (64, 2048, 50280),
+    (512, 2048, 50280),  # the 1.3B table at the largest decode batch
+    (64, 256, 200),     # 4 stages of 64 columns
+    (65, 512, 129),     # a second token block of one token; V % 4 != 0
+    (130, 1024, 77),    # one partly filled row block
+    (300, 768, 1001),   # ragged token and row blocks
 ]
 
 
@@ -95,6 +100,20 @@ def test_lm_head_both_kernels(env, M, d, V, threshold):
     q, s = o.quantize_act(S.activations(M, d, key=(49, M, d)))
     with forced_switch(D, D.TEST_LM_HEAD_MFMA_TOKENS, threshold):
         _check_lm(torch, D, o, q, s, E, scale, f"M={M} d={d} V={V} threshold={threshold}")
+
+
+@pytest.mark.parametrize("M,d,V,threshold", [(8, 2048, 1001, 8), (17, 1024, 77, 8), (64, 2048, 1001, 100000),
+                                              (300, 768, 1001, 100000)])
+def test_lm_head_tiled_switch(env, M, d, V, threshold):
+    # the test switch moves the token count from which the matrix-core path
+    # runs the tiled kernel: few tokens through it, many through the kernel
+    # that holds the table slice in registers
+    torch, D, o = env
+    say(f"lm_head tiled switch M={M} d={d} V={V} threshold={threshold}")
+    E, scale = S.embedding(V, d, key=(50, d, V))
+    q, s = o.quantize_act(S.activations(M, d, key=(50, M, d)))
+    with forced_switch(D, D.TEST_LM_HEAD_TILED_TOKENS, threshold):
+        _check_lm(torch, D, o, q, s, E, scale, f"M={M} d={d} V={V} tiled threshold={threshold}")
 
 
 def test_lm_head_extremes(env):
