@@ -342,8 +342,10 @@ dfssm_status dfssm_embed_gather(const int8_t* E, const float* scale, int64_t V, 
  * Below 8 tokens, GEMV passes of up to 4 tokens (fewer for d > 4096), each
  * streaming the table once; from 8 tokens, when d is a multiple of 64 that
  * splits into 4..8 waves of at most 8 steps of 64 (d = 256 .. 4096), one
- * pass on the matrix cores that reads the table once for all tokens
- * (dfssm_test_switch can move the threshold of 8).
+ * pass on the matrix cores that reads the table once for all tokens; from
+ * 64 tokens (and V * d, M * d < 2^31) a tiled matrix-core kernel that
+ * stages both operands in LDS (dfssm_test_switch can move both thresholds).
+ * All choices give the same bits.
  * Limits: 0 < d <= 16384, d % 16 == 0; 0 <= V < 2^30; M >= 0 (M or V == 0
  * is a no-op).
  * Errors: NULL, SHAPE, ALIGN, DEVICE. */
