@@ -324,7 +324,7 @@ __device__ void lora_block(const SkinnyArgs& a) {
 }
 
 // The limbs of acc_a[m][j0 + 16kg .. +15] as 4 limb operands (byte e of limb
-// t = limb t of rank j0 + 16kg + e) and, with want_sq, sum Q of token m, for
+// t = limb t of rank j0 + 16kg + e) and, when sq is given, sum Q of token m, for
 // the lane (rho, kg) of the wave that finishes the token tile starting at t0
 // (m = min(t0 + rho, M - 1)): from the LoRA workgroups' words, or computed
 // here once `spin` polls have passed.  CP: the words come in one copy per
