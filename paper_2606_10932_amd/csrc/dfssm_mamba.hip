@@ -314,15 +314,20 @@ __global__ __launch_bounds__(NT) void ssm_step(SsmArgs a) {
 
 template <int N>
 void launch_ssm_n(const SsmArgs& a, int64_t M, hipStream_t st) {
-  // 32 channels per workgroup from 5 sequences: the B/C convolution every
-  // workgroup repeats is then amortised over 16 KB of state (batch 512:
-  // 357-364 us against 404-406 with 16 channels, 363-370 with 64, 489 with
-  // 8).  Up to 4 sequences the step is latency and the 16-channel blocks'
-  // shorter per-thread chain wins (batch 1: 4.05 us against 4.75).
+  // More channels per workgroup amortise the B/C convolution every
+  // workgroup repeats over more state, and leave fewer workgroups: 64
+  // channels (32 KB of state) from 16 sequences, 32 from 5.  Per step of
+  // 48 layers' states in a graph (us per call), 32 / 64 channels: batch
+  // 8: 8.6 / 9.3; 12: 10.8 / 11.2; 16: 16.6 / 13.1; 32: 28.0 / 28.4; 256:
+  // 187 / 182; 512: 375 / 363.  Up to 4 sequences the step is latency and
+  // the 16-channel blocks' shorter per-thread chain wins (batch 1: 4.05 us
+  // against 4.75).
   if (M <= 4)
     ssm_step<N, 16><<<dim3((unsigned)(M * a.H * (kHeadDim / 16))), dim3(kSsmThreads), 0, st>>>(a);
-  else
+  else if (M < 16)
     ssm_step<N, 32><<<dim3((unsigned)(M * a.H * (kHeadDim / 32))), dim3(kSsmThreads), 0, st>>>(a);
+  else
+    ssm_step<N, 64><<<dim3((unsigned)(M * a.H * (kHeadDim / 64))), dim3(kSsmThreads), 0, st>>>(a);
 }
 
 }  // namespace

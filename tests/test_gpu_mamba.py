@@ -150,6 +150,8 @@ SSHAPES = [
     (2, 1024, 64, 0, 5),       # d_state 64
     (1, 32, 128, 3, 5),        # one head
     (5, 96, 64, 1, 4),         # three heads, ragged M
+    (16, 2048, 128, 1, 3),     # 64 channels per workgroup from 16 sequences
+    (33, 1024, 64, 0, 2),      # the same with d_state 64
 ]
 
 
