@@ -72,25 +72,25 @@ size_t linear_ws_bytes(int64_t M, int64_t K, int64_t r) {
 // Kernel family of the automatic path: the popcount GEMV up to kDecodeM0
 // tokens (none by default); the one-launch few-token MFMA kernel up to
 // kSkinnyMaxTokens; above, whichever of the few-token kernel in 64-token
-// blocks and the prefill kernel a cost model puts lower (us), fitted to the
-// 130M, 1.3B and 2.7B projections at 33 to 512 tokens:
-//   few-token  8.5 + 0.018 B (0.76 + K/2048),  B = ceil(M/16) ceil(N/16) / 4
-//   prefill    7.5 + 0.7 K/64 + 0.0016 N + 0.04 max(0, M - 256) K/2048
+// blocks and the prefill path a cost model puts lower (us), fitted on
+// MI355X to the 130M, 1.3B and 2.7B projections at 33 to 512 tokens:
+//   few-token  9.5 + 0.013 B (0.76 + K/2048) + 1.5 ceil(M/64) K/2048,
+//              B = ceil(M/16) ceil(N/16) / 4
+//   prefill    dfssm::prefill_cost_us (its K-loop stages, its slices and
+//              the form its tiling takes)
 // The few-token kernel's cost grows with its 16-token tiles (a partly
-// filled 64-token block costs its tiles); the prefill kernel's
-// K loop is a serial pipeline of K/64 stages (~0.7 us each) whatever M is.
-// Of the 40 measured cases the model misses two near-ties: the 1.3B in_proj
-// at M = 128 (2.3 us) and the 130M out_proj at M = 512 (1 us).
+// filled 64-token block costs its tiles) and its 64-token blocks.  Of the
+// 72 measured cases the model picks the slower kernel in three: the 130M
+// in_proj at M = 96 (0.05 us), the 130M out_proj at 192 (0.1 us) and the
+// 1.3B out_proj at 256 (2.5 us).
 int auto_path(int64_t M, int64_t K, int64_t N) {
   if (M <= dfssm::kDecodeM0) return DFSSM_PATH_DECODE;
   if (M <= dfssm::kSkinnyMaxTokens) return DFSSM_PATH_MFMA_FEW;
   if (M > dfssm::kSkinnyChunkedMaxTokens) return DFSSM_PATH_MFMA;
   const double k2 = (double)K / 2048.0;
   const double B = (double)dfssm::ceil_div(M, 16) * (double)dfssm::ceil_div(N, 16) / 4.0;
-  const double few = 8.5 + 0.018 * B * (0.76 + k2);
-  const double pre = 7.5 + 0.7 * (double)K / 64.0 + 0.0016 * (double)N +
-                     0.04 * (double)std::max<int64_t>(0, M - 256) * k2;
-  return few <= pre ? DFSSM_PATH_MFMA_FEW : DFSSM_PATH_MFMA;
+  const double few = 9.5 + 0.013 * B * (0.76 + k2) + 1.5 * (double)dfssm::ceil_div(M, 64) * k2;
+  return few <= dfssm::prefill_cost_us(M, K, N) ? DFSSM_PATH_MFMA_FEW : DFSSM_PATH_MFMA;
 }
 
 // Kernel family for a linear (path already chosen or AUTO).

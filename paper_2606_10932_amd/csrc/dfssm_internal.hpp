@@ -159,6 +159,8 @@ hipError_t launch_lm_head(const int8_t* q, const float* s, int64_t M, int64_t d,
 // Compute units of the current device (cached per device; 256 if the query
 // fails).
 int device_cu_count();
+// modelled duration (us) of the prefill path for an M x K x N linear
+double prefill_cost_us(int64_t M, int64_t K, int64_t N);
 
 // ---------------------------------------------------------------- chain
 // The persistent chain kernel (M = 1): one launch of one workgroup per CU

@@ -200,6 +200,10 @@ __global__ __launch_bounds__(kLdThreads) void mfma_lora_down(const int8_t* __res
 // tiles 4w .. 4w+3 of the run (wave tile 128 x 64: each expanded sign operand
 // feeds 8 MFMAs, and the Q tile in LDS is shared by the 4 waves); a 17th row
 // tile is shared by all 4 waves, wave w taking its token tiles 2w and 2w+1.
+// Short form (every run of the grid at most 4 row tiles, e.g. a few hundred
+// tokens): wave w takes token tiles 2w and 2w+1 of every row tile of the
+// run and skips token tiles past M, so the 4 waves share a short run's
+// MFMAs instead of one wave owning them (89 VGPRs, three blocks per CU).
 //
 // K-loop: 64 K per stage; operands reach LDS by direct-to-LDS loads
 // (global_load_lds with a scalar base and a per-lane offset that stays
@@ -435,7 +439,32 @@ __device__ __forceinline__ void block_epilogue(const GemmArgs& a, const TileLds&
   }
 }
 
-template <bool kLoraLds>
+// Epilogue of a short run (at most 4 row tiles), per wave: token tiles
+// 2w and 2w+1 of each row tile, held in acc[t][0] and acc[t][1].
+template <bool kLdsLora, bool kChecked>
+__device__ __forceinline__ void short_epilogue(const GemmArgs& a, const TileLds& L, const v4i (&acc)[4][2], int m0,
+                                               int n0, int wave, int cnt, int ntt, int rho, int kg, int l_off) {
+  const int8_t* limb_lds = L.lds;
+  const int8_t* b_lds = L.lds + kLimbBytes;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int i = 2 * wave + h;
+    if (i >= ntt) continue;  // uniform: no token of the block in this tile
+    v4i lm[4];
+#pragma unroll
+    for (int l = 0; l < 4; ++l)
+      lm[l] = kLdsLora ? *reinterpret_cast<const v4i*>(limb_lds + (l * kBM + 16 * i) * 64 + l_off) : zero4();
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      if (t < cnt) {
+        const v4i bop = kLdsLora ? *reinterpret_cast<const v4i*>(b_lds + (16 * t) * 64 + l_off) : zero4();
+        tile_out<kLdsLora, kChecked>(a, L, acc[t][h], bop, lm, m0, n0, 16 * t, i, rho, kg);
+      }
+    }
+  }
+}
+
+template <bool kLoraLds, bool kShort>
 __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds& L, int m0, int rt0, int cnt) {
   const int M = a.M, K = a.K, N = a.N, r = a.r, rp = a.rp;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -448,6 +477,12 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
   const int cmain = min(cnt, 16);
   const int ntw = min(max(cmain - 4 * wave, 0), 4);  // this wave's row tiles
   const bool extra = cnt > 16;                        // the 17th row tile
+  // kShort (every run of the grid holds at most 4 row tiles): wave w
+  // multiplies token tiles 2w and 2w+1 of every row tile of the run (the
+  // sign words of wave 0's area), so the 4 waves share the work; token
+  // tiles past M are skipped
+  constexpr bool shortrun = kShort;
+  const int ntt = min(8, (M - m0 + 15) >> 4);  // token tiles holding tokens
   const int nrows = 16 * cnt;
   int8_t* const lds = L.lds;
 
@@ -545,7 +580,7 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
   const int q_off = rho * kBK + 16 * (kg ^ swz(rho));
   // row rho of the wave's area plus the byte of the word slot before the
   // stage's ^ 8s (bits 3-4 of the row offset are zero, so ^ acts on the slot)
-  const int w_off = kQRing + kSgWave * wave + 32 * rho + 4 * ((kg >> 1) ^ (2 * ((rho >> 2) & 3)));
+  const int w_off = kQRing + kSgWave * (shortrun ? 0 : wave) + 32 * rho + 4 * ((kg >> 1) ^ (2 * ((rho >> 2) & 3)));
   const int x_delta = (4 - wave) * kSgWave;  // uniform: the 17th tile's area
   const uint32_t sh = 16u * (kg & 1);
 
@@ -566,11 +601,12 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
     return rw;
   };
 
-  v4i acc[4][8], accx[2];
+  constexpr int kTT = kShort ? 2 : 8;  // token tiles a wave accumulates
+  v4i acc[4][kTT], accx[2];
 #pragma unroll
   for (int t = 0; t < 4; ++t)
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[t][i] = zero4();
+    for (int i = 0; i < kTT; ++i) acc[t][i] = zero4();
   accx[0] = accx[1] = zero4();
 
   // multiply stage ks: the 8 Q operands are read from LDS first; then row
@@ -578,9 +614,6 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
   const bool kg_hi = kg >= 2;
   auto compute = [&](int ks, int slot, const Raw& rw) {
     const int8_t* st = lds + slot * kQStage + q_off;
-    v4i qv[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) qv[i] = *reinterpret_cast<const v4i*>(st + i * 16 * kBK);
     raw_t w = rw.w;
     uint32_t wx = rw.x;
     if (ktail && ks == nks - 1) {  // uniform: sign words past K count as 0
@@ -588,6 +621,23 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
       for (int t = 0; t < 4; ++t) w[t] = kg_hi ? 0u : w[t];
       wx = kg_hi ? 0u : wx;
     }
+    if constexpr (kShort) {
+      if (2 * wave < ntt) {  // uniform
+        const v4i qa = *reinterpret_cast<const v4i*>(st + (2 * wave) * 16 * kBK);
+        const v4i qb = *reinterpret_cast<const v4i*>(st + (2 * wave + 1) * 16 * kBK);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          if (t < cnt) {
+            const v4i sg = expand16_at(w[t], sh);
+            acc[t][0] = mfma(sg, qa, acc[t][0]);
+            acc[t][1] = mfma(sg, qb, acc[t][1]);
+          }
+        }
+      }
+    } else {
+    v4i qv[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) qv[i] = *reinterpret_cast<const v4i*>(st + i * 16 * kBK);
     {
       // waves owning fewer than 4 row tiles (a short run) multiply all 4
       // anyway: the rows past their run are valid clamped reads and their
@@ -624,6 +674,7 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
 #pragma unroll
       for (int i = 0; i < 8; ++i)
         if ((i >> 1) == wave) accx[i & 1] = mfma(sx, qv[i], accx[i & 1]);
+    }
     }
   };
 
@@ -715,15 +766,24 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
   }
   const int l_off = rho * 64 + 16 * (kg ^ swz(rho));
   const bool fast = lora_lds && !a.acc_s_out && !a.acc_b_out && (N & 3) == 0 && m0 + kBM <= M && n0 + nrows <= N;
-  if (fast)
-    block_epilogue<true, false>(a, L, acc, accx, m0, n0, wave, ntw, extra, 256, 2 * wave, rho, kg, l_off);
-  else if (lora_lds)
-    block_epilogue<true, true>(a, L, acc, accx, m0, n0, wave, ntw, extra, 256, 2 * wave, rho, kg, l_off);
-  else
-    block_epilogue<false, true>(a, L, acc, accx, m0, n0, wave, ntw, extra, 256, 2 * wave, rho, kg, l_off);
+  if constexpr (kShort) {
+    if (fast)
+      short_epilogue<true, false>(a, L, acc, m0, n0, wave, cnt, ntt, rho, kg, l_off);
+    else if (lora_lds)
+      short_epilogue<true, true>(a, L, acc, m0, n0, wave, cnt, ntt, rho, kg, l_off);
+    else
+      short_epilogue<false, true>(a, L, acc, m0, n0, wave, cnt, ntt, rho, kg, l_off);
+  } else {
+    if (fast)
+      block_epilogue<true, false>(a, L, acc, accx, m0, n0, wave, ntw, extra, 256, 2 * wave, rho, kg, l_off);
+    else if (lora_lds)
+      block_epilogue<true, true>(a, L, acc, accx, m0, n0, wave, ntw, extra, 256, 2 * wave, rho, kg, l_off);
+    else
+      block_epilogue<false, true>(a, L, acc, accx, m0, n0, wave, ntw, extra, 256, 2 * wave, rho, kg, l_off);
+  }
 }
 
-template <bool kLoraLds>
+template <bool kLoraLds, bool kShort>
 __global__ __launch_bounds__(kThreads, 2) void mfma_scaffold(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) int8_t lds[kLdsBytes];
   __shared__ __attribute__((aligned(16))) float al_lds[kMaxRows], be_lds[kMaxRows], s_lds[kBM];
@@ -733,7 +793,7 @@ __global__ __launch_bounds__(kThreads, 2) void mfma_scaffold(GemmArgs a) {
   // row tiles [rt0, rt1) of the slice: runs of equal length up to one
   const int rt0 = (int)((int64_t)j * a.nt16 / a.bpm), rt1 = (int)((int64_t)(j + 1) * a.nt16 / a.bpm);
   const TileLds L{lds, al_lds, be_lds, s_lds, sq_lds};
-  scaffold_block<kLoraLds>(a, L, bm * kBM, rt0, rt1 - rt0);
+  scaffold_block<kLoraLds, kShort>(a, L, bm * kBM, rt0, rt1 - rt0);
 }
 
 
@@ -1039,9 +1099,47 @@ __global__ __launch_bounds__(kPPThreads, 1) void mfma_scaffold_pp(GemmArgs a) {
   scaffold_block_pp<kLoraLds>(a, L, bm * kBM, rt0, rt1 - rt0);
 }
 
+// Tiling of the prefill path.  Each 128-token slice's ceil(N/16) row
+// tiles are dealt to bpm blocks in runs whose lengths differ by at most
+// one; bpm is chosen so the blocks fill the chip's block slots in whole
+// rounds where the shape allows.  The 8-wave ping-pong kernel (one block
+// per CU, runs of up to 34) is taken where the runs are long enough to keep
+// its 8 waves busy (at least 24 row tiles); otherwise the 4-wave kernel (two
+// blocks per CU, runs of up to 17), in its short form when every run holds
+// at most 4 row tiles.  forced: the test switch prefill_kernel (4 or 8).
+enum PrefillForm { kForm8 = 8, kForm4 = 4, kForm4Short = 2 };
+struct PrefillPlan {
+  int64_t nbm, nt16, bpm;
+  PrefillForm form;
+};
+PrefillPlan plan_prefill(int64_t M, int64_t N, int64_t cus, int forced) {
+  const int64_t nbm = dfssm::ceil_div(M, kBM);
+  const int64_t nt16 = dfssm::ceil_div(N, 16);
+  const int64_t bpm8 = std::min(std::max(dfssm::ceil_div(cus, nbm), dfssm::ceil_div(nt16, kPPRunMax)), nt16);
+  bool use8 = nt16 >= 24 * bpm8;
+  if (forced == 4) use8 = false;
+  if (forced == 8) use8 = true;
+  if (use8) return {nbm, nt16, bpm8, kForm8};
+  const int64_t bpm = std::min(std::max(dfssm::ceil_div(2 * cus, nbm), dfssm::ceil_div(nt16, kRunMax)), nt16);
+  return {nbm, nt16, bpm, nt16 <= 4 * bpm ? kForm4Short : kForm4};
+}
+
 }  // namespace
 
 namespace dfssm {
+
+// Cost of the prefill path (us; both launches), fitted on MI355X to the
+// 130M, 1.3B and 2.7B projections at 33 to 512 tokens: a serial K-loop of
+// K/64 stages (0.35 us each, plus a share that grows with N), the MFMA work
+// of every 128-token slice past the first, and for runs of more than 4 row
+// tiles the longer stages of the 4- and 8-wave forms.
+double prefill_cost_us(int64_t M, int64_t K, int64_t N) {
+  const PrefillPlan p = plan_prefill(M, N, device_cu_count(), 0);
+  const double stages = (double)K / 64.0;
+  double c = 8.5 + stages * (0.35 + 0.12 * (double)N / 1e4) + 2.2 * (double)N * (double)K * (double)(p.nbm - 1) / 1e7;
+  if (p.form != kForm4Short) c += 0.17 * stages * (double)ceil_div(p.nt16, p.bpm) / 4.0;
+  return c;
+}
 
 int device_cu_count() {
   static std::atomic<int> cache[64];
@@ -1070,34 +1168,24 @@ hipError_t launch_mfma_linear(const int8_t* q, const float* s, int64_t M, int64_
     e = hipMemcpyAsync(acc_a_out, ws.acc_a, (size_t)(M * r) * 4, hipMemcpyDeviceToDevice, st);
     if (e != hipSuccess) return e;
   }
-  // Tiling: each 128-token slice's ceil(N/16) row tiles are dealt to bpm
-  // blocks in runs of at most 17 whose lengths differ by at most one; bpm
-  // is chosen so the blocks fill the chip's block slots (two per CU) in
-  // whole rounds where the shape allows.
-  const int64_t cus = device_cu_count();
-  const int64_t nbm = ceil_div(M, kBM);
-  const int64_t nt16 = ceil_div(N, 16);
-  // the 8-wave ping-pong kernel (one block per CU) where the runs are long
-  // enough to keep its 8 waves busy (at least 24 row tiles), else the 4-wave
-  // kernel (two blocks per CU).  Test switch prefill_kernel: 4 or 8.
-  int64_t bpm8 = std::min(std::max(ceil_div(cus, nbm), ceil_div(nt16, kPPRunMax)), nt16);
-  bool use8 = nt16 >= 24 * bpm8;
-  const int forced = test_switch(DFSSM_TEST_PREFILL_KERNEL);
-  if (forced == 4) use8 = false;
-  if (forced == 8) use8 = true;
-  int64_t bpm = use8 ? bpm8 : std::min(std::max(ceil_div(2 * cus, nbm), ceil_div(nt16, kRunMax)), nt16);
-  const int64_t grid = nbm * bpm;
+  const PrefillPlan p = plan_prefill(M, N, device_cu_count(), test_switch(DFSSM_TEST_PREFILL_KERNEL));
+  const int64_t grid = p.nbm * p.bpm;
   GemmArgs ga{q, s, (int)M, (int)K, (int)N, (int)r, rp, w_bits, alpha, ws.limbs, B, beta, ws.sumq, y,
-              acc_s, acc_b, (int)nt16, (int)bpm};
-  if (use8) {
+              acc_s, acc_b, (int)p.nt16, (int)p.bpm};
+  if (p.form == kForm8) {
     if (rp == 64)
       mfma_scaffold_pp<true><<<dim3((unsigned)grid), dim3(kPPThreads), 0, st>>>(ga);
     else
       mfma_scaffold_pp<false><<<dim3((unsigned)grid), dim3(kPPThreads), 0, st>>>(ga);
+  } else if (p.form == kForm4Short) {
+    if (rp == 64)
+      mfma_scaffold<true, true><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
+    else
+      mfma_scaffold<false, true><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
   } else if (rp == 64) {
-    mfma_scaffold<true><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
+    mfma_scaffold<true, false><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
   } else {
-    mfma_scaffold<false><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
+    mfma_scaffold<false, false><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
   }
   return hipGetLastError();
 }

@@ -265,6 +265,10 @@ PSHAPES = [
     (2, 256, 31, 256),       # ranks above 64: LoRA operands from memory
     (300, 2080, 700, 64),    # K % 64 == 32: half last stage
     (129, 96, 600, 0),       # no LoRA, 2-stage K
+    # runs of more than 4 row tiles reach the 4-wave kernel's full form only
+    # with many 128-token slices (smaller shapes take its short form)
+    (1100, 288, 4201, 64),   # 9 slices, runs of 4-5 row tiles, K % 64 == 32, ragged N
+    (1030, 256, 4200, 0),
 ]
 
 
@@ -282,6 +286,38 @@ def test_linear_prefill_kernels(env, kernel, M, K, N, r):
     assert np.array_equal(acc_b, ref["acc_b"]), "acc_b"
     assert_y(y, ref, what=f"prefill{kernel} {M}x{K}x{N} r{r}")
     assert np.array_equal(y2.view(np.uint32), y.view(np.uint32)), "y without accumulator outputs"
+
+
+# the 4-wave kernel's short form (every run of the grid at most 4 row
+# tiles: wave w multiplies token tiles 2w, 2w+1 of each row tile and skips
+# tiles past M), as the prefill path takes it at a few hundred tokens
+SHORT_SHAPES = [
+    (100, 2048, 8512, 64),   # 1.3B in_proj, one partial 128-token slice
+    (33, 768, 3352, 16),     # 130M in_proj, 3 token tiles
+    (500, 1536, 768, 64),    # 130M out_proj, 4 slices, the last partial
+    (200, 4096, 2048, 72),   # ranks above 64: LoRA operands from memory
+    (77, 2080, 210, 0),      # no LoRA, K % 64 == 32, ragged N
+    (260, 4096, 2048, 64),   # 1.3B out_proj, 3 slices
+    (300, 256, 10900, 64),   # runs of 3-4 row tiles, ragged N
+]
+
+
+@pytest.mark.parametrize("M,K,N,r", SHORT_SHAPES)
+def test_linear_prefill_short_form(env, M, K, N, r):
+    torch, D, o = env
+    say(f"prefill short form M={M} K={K} N={N} r={r}")
+    with forced_switch(D, D.TEST_PREFILL_KERNEL, 4):
+        ref, y, acc_s, acc_a, acc_b = _run_linear(env, M, K, N, r, D.PATH_MFMA)
+        y2 = _run_y_only(env, M, K, N, r, D.PATH_MFMA)
+    assert np.array_equal(acc_s, ref["acc_s"]), "acc_s"
+    if r:
+        assert np.array_equal(acc_a, ref["acc_a"]), "acc_a"
+    assert np.array_equal(acc_b, ref["acc_b"]), "acc_b"
+    assert_y(y, ref, what=f"short {M}x{K}x{N} r{r}")
+    assert np.array_equal(y2.view(np.uint32), y.view(np.uint32)), "y without accumulator outputs"
+    # the automatic path at this size (few-token or prefill, by the cost model)
+    ya = _run_y_only(env, M, K, N, r, D.PATH_AUTO)
+    assert np.array_equal(ya.view(np.uint32), y.view(np.uint32)), "automatic path"
 
 
 @pytest.mark.parametrize("kernel", [0, 4])
