@@ -200,10 +200,12 @@ __global__ __launch_bounds__(kLdThreads) void mfma_lora_down(const int8_t* __res
 // tiles 4w .. 4w+3 of the run (wave tile 128 x 64: each expanded sign operand
 // feeds 8 MFMAs, and the Q tile in LDS is shared by the 4 waves); a 17th row
 // tile is shared by all 4 waves, wave w taking its token tiles 2w and 2w+1.
-// Short form (every run of the grid at most 4 row tiles, e.g. a few hundred
-// tokens): wave w takes token tiles 2w and 2w+1 of every row tile of the
-// run and skips token tiles past M, so the 4 waves share a short run's
-// MFMAs instead of one wave owning them (89 VGPRs, three blocks per CU).
+// Short forms (every run of the grid at most 4, or at most kShortRun = 8,
+// row tiles, e.g. a few hundred tokens): wave w takes token tiles 2w and
+// 2w+1 of every row tile of the run and skips token tiles past M, so the 4
+// waves share a short run's MFMAs instead of each multiplying its 4 row
+// tiles whatever the run (three blocks per CU).  The 8-tile form holds
+// twice the accumulators; runs of at most 4 keep the smaller one.
 //
 // K-loop: 64 K per stage; operands reach LDS by direct-to-LDS loads
 // (global_load_lds with a scalar base and a per-lane offset that stays
@@ -241,6 +243,7 @@ constexpr int kLimbBytes = 4 * kBM * 64;                // LoRA limbs of the til
 constexpr int kLdsLora = kLimbBytes + kRunMax * 16 * 64;  // + B rows of the run
 constexpr int kLdsBytes = kLdsRing > kLdsLora ? kLdsRing : kLdsLora;
 constexpr int kMaxRows = kRunMax * 16;
+constexpr int kShortRun = 8;  // row tiles per run, at most, of the short form
 static_assert(kSgStages == kStages, "a sign group is one pass over the Q ring");
 static_assert(2 * kLq + kLsg + kLq <= 63, "vector-memory counter range");
 
@@ -439,10 +442,10 @@ __device__ __forceinline__ void block_epilogue(const GemmArgs& a, const TileLds&
   }
 }
 
-// Epilogue of a short run (at most 4 row tiles), per wave: token tiles
-// 2w and 2w+1 of each row tile, held in acc[t][0] and acc[t][1].
-template <bool kLdsLora, bool kChecked>
-__device__ __forceinline__ void short_epilogue(const GemmArgs& a, const TileLds& L, const v4i (&acc)[4][2], int m0,
+// Epilogue of a short run (at most kShortRun row tiles), per wave: token
+// tiles 2w and 2w+1 of each row tile, held in acc[t][0] and acc[t][1].
+template <bool kLdsLora, bool kChecked, int kSR>
+__device__ __forceinline__ void short_epilogue(const GemmArgs& a, const TileLds& L, const v4i (&acc)[kSR][2], int m0,
                                                int n0, int wave, int cnt, int ntt, int rho, int kg, int l_off) {
   const int8_t* limb_lds = L.lds;
   const int8_t* b_lds = L.lds + kLimbBytes;
@@ -455,7 +458,7 @@ __device__ __forceinline__ void short_epilogue(const GemmArgs& a, const TileLds&
     for (int l = 0; l < 4; ++l)
       lm[l] = kLdsLora ? *reinterpret_cast<const v4i*>(limb_lds + (l * kBM + 16 * i) * 64 + l_off) : zero4();
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
+    for (int t = 0; t < kSR; ++t) {
       if (t < cnt) {
         const v4i bop = kLdsLora ? *reinterpret_cast<const v4i*>(b_lds + (16 * t) * 64 + l_off) : zero4();
         tile_out<kLdsLora, kChecked>(a, L, acc[t][h], bop, lm, m0, n0, 16 * t, i, rho, kg);
@@ -464,7 +467,7 @@ __device__ __forceinline__ void short_epilogue(const GemmArgs& a, const TileLds&
   }
 }
 
-template <bool kLoraLds, bool kShort>
+template <bool kLoraLds, int kSR>
 __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds& L, int m0, int rt0, int cnt) {
   const int M = a.M, K = a.K, N = a.N, r = a.r, rp = a.rp;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -477,10 +480,12 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
   const int cmain = min(cnt, 16);
   const int ntw = min(max(cmain - 4 * wave, 0), 4);  // this wave's row tiles
   const bool extra = cnt > 16;                        // the 17th row tile
-  // kShort (every run of the grid holds at most 4 row tiles): wave w
-  // multiplies token tiles 2w and 2w+1 of every row tile of the run (the
-  // sign words of wave 0's area), so the 4 waves share the work; token
-  // tiles past M are skipped
+  // kSR > 0 (every run of the grid holds at most kSR row tiles): wave
+  // w multiplies token tiles 2w and 2w+1 of every row tile of the run (the
+  // sign words of the areas of waves 0 and 1, which hold the run's rows
+  // 0-63 and 64-127), so the 4 waves share the work; token tiles past M are
+  // skipped
+  constexpr bool kShort = kSR > 0;
   constexpr bool shortrun = kShort;
   const int ntt = min(8, (M - m0 + 15) >> 4);  // token tiles holding tokens
   const int nrows = 16 * cnt;
@@ -588,6 +593,7 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
   struct Raw {
     raw_t w;
     uint32_t x;
+    raw_t w2;  // short form: row tiles 4-7 of the run
   };
   // sign words of stage ks (group ks / 4, stage ks % 4 of it): read one
   // stage ahead of their use
@@ -598,13 +604,20 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
 #pragma unroll
     for (int t = 0; t < 4; ++t) rw.w[t] = *reinterpret_cast<const uint32_t*>(st + wb + 512 * t);
     rw.x = *reinterpret_cast<const uint32_t*>(st + x_delta + wb);
+    if constexpr (kSR > 4) {
+      if (cnt > 4) {  // uniform
+#pragma unroll
+        for (int t = 0; t < 4; ++t) rw.w2[t] = *reinterpret_cast<const uint32_t*>(st + wb + kSgWave + 512 * t);
+      }
+    }
     return rw;
   };
 
-  constexpr int kTT = kShort ? 2 : 8;  // token tiles a wave accumulates
-  v4i acc[4][kTT], accx[2];
+  constexpr int kTT = kShort ? 2 : 8;          // token tiles a wave accumulates
+  constexpr int kRT = kShort ? kSR : 4;        // row tiles
+  v4i acc[kRT][kTT], accx[2];
 #pragma unroll
-  for (int t = 0; t < 4; ++t)
+  for (int t = 0; t < kRT; ++t)
 #pragma unroll
     for (int i = 0; i < kTT; ++i) acc[t][i] = zero4();
   accx[0] = accx[1] = zero4();
@@ -622,13 +635,18 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
       wx = kg_hi ? 0u : wx;
     }
     if constexpr (kShort) {
+      raw_t w2 = rw.w2;
+      if (kSR > 4 && ktail && ks == nks - 1) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) w2[t] = kg_hi ? 0u : w2[t];
+      }
       if (2 * wave < ntt) {  // uniform
         const v4i qa = *reinterpret_cast<const v4i*>(st + (2 * wave) * 16 * kBK);
         const v4i qb = *reinterpret_cast<const v4i*>(st + (2 * wave + 1) * 16 * kBK);
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
+        for (int t = 0; t < kSR; ++t) {
           if (t < cnt) {
-            const v4i sg = expand16_at(w[t], sh);
+            const v4i sg = expand16_at(t < 4 ? w[t] : w2[t - 4], sh);
             acc[t][0] = mfma(sg, qa, acc[t][0]);
             acc[t][1] = mfma(sg, qb, acc[t][1]);
           }
@@ -768,11 +786,11 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
   const bool fast = lora_lds && !a.acc_s_out && !a.acc_b_out && (N & 3) == 0 && m0 + kBM <= M && n0 + nrows <= N;
   if constexpr (kShort) {
     if (fast)
-      short_epilogue<true, false>(a, L, acc, m0, n0, wave, cnt, ntt, rho, kg, l_off);
+      short_epilogue<true, false, kSR>(a, L, acc, m0, n0, wave, cnt, ntt, rho, kg, l_off);
     else if (lora_lds)
-      short_epilogue<true, true>(a, L, acc, m0, n0, wave, cnt, ntt, rho, kg, l_off);
+      short_epilogue<true, true, kSR>(a, L, acc, m0, n0, wave, cnt, ntt, rho, kg, l_off);
     else
-      short_epilogue<false, true>(a, L, acc, m0, n0, wave, cnt, ntt, rho, kg, l_off);
+      short_epilogue<false, true, kSR>(a, L, acc, m0, n0, wave, cnt, ntt, rho, kg, l_off);
   } else {
     if (fast)
       block_epilogue<true, false>(a, L, acc, accx, m0, n0, wave, ntw, extra, 256, 2 * wave, rho, kg, l_off);
@@ -783,7 +801,7 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
   }
 }
 
-template <bool kLoraLds, bool kShort>
+template <bool kLoraLds, int kSR>
 __global__ __launch_bounds__(kThreads, 2) void mfma_scaffold(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) int8_t lds[kLdsBytes];
   __shared__ __attribute__((aligned(16))) float al_lds[kMaxRows], be_lds[kMaxRows], s_lds[kBM];
@@ -793,7 +811,7 @@ __global__ __launch_bounds__(kThreads, 2) void mfma_scaffold(GemmArgs a) {
   // row tiles [rt0, rt1) of the slice: runs of equal length up to one
   const int rt0 = (int)((int64_t)j * a.nt16 / a.bpm), rt1 = (int)((int64_t)(j + 1) * a.nt16 / a.bpm);
   const TileLds L{lds, al_lds, be_lds, s_lds, sq_lds};
-  scaffold_block<kLoraLds, kShort>(a, L, bm * kBM, rt0, rt1 - rt0);
+  scaffold_block<kLoraLds, kSR>(a, L, bm * kBM, rt0, rt1 - rt0);
 }
 
 
@@ -1106,8 +1124,9 @@ __global__ __launch_bounds__(kPPThreads, 1) void mfma_scaffold_pp(GemmArgs a) {
 // per CU, runs of up to 34) is taken where the runs are long enough to keep
 // its 8 waves busy (at least 24 row tiles); otherwise the 4-wave kernel (two
 // blocks per CU, runs of up to 17), in its short form when every run holds
-// at most 4 row tiles.  forced: the test switch prefill_kernel (4 or 8).
-enum PrefillForm { kForm8 = 8, kForm4 = 4, kForm4Short = 2 };
+// at most kShortRun row tiles.  forced: the test switch prefill_kernel (4
+// or 8).
+enum PrefillForm { kForm8 = 8, kForm4 = 4, kForm4Short = 2 };  // short: runs of at most kShortRun
 struct PrefillPlan {
   int64_t nbm, nt16, bpm;
   PrefillForm form;
@@ -1121,7 +1140,7 @@ PrefillPlan plan_prefill(int64_t M, int64_t N, int64_t cus, int forced) {
   if (forced == 8) use8 = true;
   if (use8) return {nbm, nt16, bpm8, kForm8};
   const int64_t bpm = std::min(std::max(dfssm::ceil_div(2 * cus, nbm), dfssm::ceil_div(nt16, kRunMax)), nt16);
-  return {nbm, nt16, bpm, nt16 <= 4 * bpm ? kForm4Short : kForm4};
+  return {nbm, nt16, bpm, nt16 <= kShortRun * bpm ? kForm4Short : kForm4};
 }
 
 }  // namespace
@@ -1177,15 +1196,20 @@ hipError_t launch_mfma_linear(const int8_t* q, const float* s, int64_t M, int64_
       mfma_scaffold_pp<true><<<dim3((unsigned)grid), dim3(kPPThreads), 0, st>>>(ga);
     else
       mfma_scaffold_pp<false><<<dim3((unsigned)grid), dim3(kPPThreads), 0, st>>>(ga);
+  } else if (p.form == kForm4Short && p.nt16 <= 4 * p.bpm) {  // runs of at most 4 row tiles
+    if (rp == 64)
+      mfma_scaffold<true, 4><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
+    else
+      mfma_scaffold<false, 4><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
   } else if (p.form == kForm4Short) {
     if (rp == 64)
-      mfma_scaffold<true, true><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
+      mfma_scaffold<true, kShortRun><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
     else
-      mfma_scaffold<false, true><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
+      mfma_scaffold<false, kShortRun><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
   } else if (rp == 64) {
-    mfma_scaffold<true, false><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
+    mfma_scaffold<true, 0><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
   } else {
-    mfma_scaffold<false, false><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
+    mfma_scaffold<false, 0><<<dim3((unsigned)grid), dim3(kThreads), 0, st>>>(ga);
   }
   return hipGetLastError();
 }

@@ -265,10 +265,12 @@ PSHAPES = [
     (2, 256, 31, 256),       # ranks above 64: LoRA operands from memory
     (300, 2080, 700, 64),    # K % 64 == 32: half last stage
     (129, 96, 600, 0),       # no LoRA, 2-stage K
-    # runs of more than 4 row tiles reach the 4-wave kernel's full form only
-    # with many 128-token slices (smaller shapes take its short form)
-    (1100, 288, 4201, 64),   # 9 slices, runs of 4-5 row tiles, K % 64 == 32, ragged N
+    # 9 slices: runs of 4-5 row tiles take the 8-row short form, runs of 8-9
+    # the full form (smaller shapes take the 4-row short form)
+    (1100, 288, 4201, 64),   # short, 8-row form; K % 64 == 32, ragged N
     (1030, 256, 4200, 0),
+    (1100, 288, 7400, 64),   # full form
+    (1030, 256, 7300, 0),
 ]
 
 
@@ -288,9 +290,10 @@ def test_linear_prefill_kernels(env, kernel, M, K, N, r):
     assert np.array_equal(y2.view(np.uint32), y.view(np.uint32)), "y without accumulator outputs"
 
 
-# the 4-wave kernel's short form (every run of the grid at most 4 row
-# tiles: wave w multiplies token tiles 2w, 2w+1 of each row tile and skips
-# tiles past M), as the prefill path takes it at a few hundred tokens
+# the 4-wave kernel's short forms (every run of the grid at most 4, or at
+# most 8, row tiles: wave w multiplies token tiles 2w, 2w+1 of each row
+# tile and skips tiles past M), as the prefill path takes them at a few
+# hundred tokens
 SHORT_SHAPES = [
     (100, 2048, 8512, 64),   # 1.3B in_proj, one partial 128-token slice
     (33, 768, 3352, 16),     # 130M in_proj, 3 token tiles
@@ -299,6 +302,8 @@ SHORT_SHAPES = [
     (77, 2080, 210, 0),      # no LoRA, K % 64 == 32, ragged N
     (260, 4096, 2048, 64),   # 1.3B out_proj, 3 slices
     (300, 256, 10900, 64),   # runs of 3-4 row tiles, ragged N
+    (512, 2048, 8512, 64),   # 1.3B in_proj, runs of 4-5: the 8-row form
+    (1100, 256, 4200, 72),   # the 8-row form, ranks above 64
 ]
 
 
