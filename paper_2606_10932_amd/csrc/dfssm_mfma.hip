@@ -79,15 +79,15 @@ __device__ __forceinline__ v4i load16_guarded(const int8_t* row, int start, int 
 
 // ------------------------------------------------------------ lora_down
 // acc_a = Q A^T on the same MFMA.  A block owns 16 tokens x 32 ranks (two
-// 16-rank tiles; blockIdx.y walks the padded rank range rp); its 8 waves
+// 16-rank tiles; blockIdx.y walks the padded rank range rp); its 16 waves
 // split the K steps, each issuing the loads of up to kLdBatch steps before
 // its first multiply, and reduce their partial sums in LDS.  The block writes
 // acc_a, its 4 signed base-256 int8 limbs (zero for ranks in [r, rp)) and,
 // for blockIdx.y == 0, sum_k Q[m,k].
-constexpr int kLdThreads = 512;
+constexpr int kLdThreads = 1024;
 constexpr int kLdWaves = kLdThreads / 64;
 constexpr int kLdRanks = 32;
-constexpr int kLdBatch = 8;
+constexpr int kLdBatch = 4;
 constexpr int kLdPitch = 17;  // padded rank pitch of the partial sums
 
 __global__ __launch_bounds__(kLdThreads) void mfma_lora_down(const int8_t* __restrict__ q, int M, int K,
@@ -167,7 +167,7 @@ __global__ __launch_bounds__(kLdThreads) void mfma_lora_down(const int8_t* __res
     const int i = threadIdx.x;
     const int ml = i >> 5, jl = i & 31;
     const int mm = m0 + ml, jj = j0 + jl;
-    if (mm < M) {
+    if (ml < 16 && mm < M) {  // threads past 16 tokens x 32 ranks have nothing to reduce
       int32_t val = 0;
 #pragma unroll
       for (int w = 0; w < kLdWaves; ++w) val += part[w][jl * kLdPitch + ml];
