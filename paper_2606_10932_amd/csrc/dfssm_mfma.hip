@@ -487,6 +487,9 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
   // skipped
   constexpr bool kShort = kSR > 0;
   constexpr bool shortrun = kShort;
+  // the short forms read only the sign areas of waves 0 (and 1): the other
+  // waves load no sign words (and count none in their waits)
+  const bool sign_wave = !kShort || wave < (kSR > 4 ? 2 : 1);  // uniform
   const int ntt = min(8, (M - m0 + 15) >> 4);  // token tiles holding tokens
   const int nrows = 16 * cnt;
   int8_t* const lds = L.lds;
@@ -564,7 +567,7 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
   };
   // stage ks's Q into ring slot `slot`, preceded (ks % 4 == 0) by its sign group
   auto issue = [&](int ks, int slot) {
-    if (slot == 0) issue_signs(ks >> 2);
+    if (slot == 0 && sign_wave) issue_signs(ks >> 2);
     const int8_t* qs = qbase + ks * kBK;
     const uint32_t sb = lds0 + slot * kQStage;
     if (ktail && ks == nks - 1) {
@@ -706,7 +709,7 @@ __device__ __forceinline__ void scaffold_block(const GemmArgs& a, const TileLds&
     static_assert(kStages == 4, "wait counts below");
     if (ks + 1 < nks) {
       if (ks + 2 < nks) {
-        if ((slot + 2) % kStages == 0)
+        if ((slot + 2) % kStages == 0 && sign_wave)
           DFSSM_WAIT_VMCNT(kLq + kLsg);
         else
           DFSSM_WAIT_VMCNT(kLq);
