@@ -79,10 +79,9 @@ size_t linear_ws_bytes(int64_t M, int64_t K, int64_t r) {
 //   prefill    dfssm::prefill_cost_us (its K-loop stages, its slices and
 //              the form its tiling takes)
 // The few-token kernel's cost grows with its 16-token tiles (a partly
-// filled 64-token block costs its tiles) and its 64-token blocks.  Of the
-// 72 measured cases the model picks the slower kernel in three: the 130M
-// in_proj at M = 96 (0.05 us), the 130M out_proj at 192 (0.1 us) and the
-// 1.3B out_proj at 256 (2.5 us).
+// filled 64-token block costs its tiles) and its 64-token blocks.  On the
+// 72 measured cases the chosen kernel is within 0.9 us (and 5%) of the
+// faster one.
 int auto_path(int64_t M, int64_t K, int64_t N) {
   if (M <= dfssm::kDecodeM0) return DFSSM_PATH_DECODE;
   if (M <= dfssm::kSkinnyMaxTokens) return DFSSM_PATH_MFMA_FEW;
